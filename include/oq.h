@@ -1,0 +1,282 @@
+/*
+ * oq.h -- C ABI of the MI355X (gfx950) W4A4 rotated-linear library.
+ *
+ * The library implements the inference hot path of the paper's W4A4 linear
+ * layer: the online Hadamard half of the composite rotation R = R_SVD . H
+ * (Section 4.1, eq:composite_rot, block-wise form eq:blockdiag, transform
+ * eq:transform), the per-step DiT activation scale (Section 4.2,
+ * eq:perstep_scale), symmetric per-token int4 activation quantization
+ * (eq:scale, eq:quant), the packed-int4 x int4 product with int32
+ * accumulation and the per-token x per-channel dequantization
+ * (eq:lowbit_linear), plus a DiT denoising-step driver built from them
+ * (Experimental Settings, Implementation Details).
+ *
+ * Conventions for every entry point
+ * ---------------------------------
+ *  - Device pointers point to memory of the current HIP device; host
+ *    pointers are marked "host".  The caller allocates and owns every buffer;
+ *    the stateless calls allocate nothing.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Calls are asynchronous on that stream; outputs are valid after the
+ *    stream is synchronized.
+ *  - Every call validates its arguments before launching anything; a call
+ *    that returns an error has launched nothing and written nothing.
+ *  - Return value: OQ_OK (0) or a negative oq_status.  No exception crosses
+ *    the ABI.  oq_status_string() names a code.
+ *  - Stateless calls are thread-safe.  A DiT handle is used from one host
+ *    thread / one stream at a time.
+ *
+ * Data layout
+ * -----------
+ *  X      fp16 activation, row-major [M][ldx], K used channels per row.  It is
+ *         the linear's input already expressed in the SVD basis: the SVD
+ *         factor of the composite rotation is folded into the producer and
+ *         the weight offline; only the Hadamard half runs online.
+ *  Xq     packed int4 codes, row-major [M][K/2] bytes; byte k/2 of a row
+ *         holds channel k (even) in its low nibble and channel k+1 in its
+ *         high nibble, two's complement.  Codes lie in [-7, 7]; 0x8 never
+ *         occurs (q_max = 2^(4-1) - 1 = 7, eq:quant).
+ *  x_scale fp32 [M]: per-token dequantization step, Delta_i / s_t.
+ *  Wq     packed int4 weight codes, [N][K/2] bytes, same nibble order; row n
+ *         is output channel n (the weight is stored output-major, so
+ *         Y = X' . W'^T).
+ *  w_scale fp32 [N]: per-output-channel step Delta_W'.
+ */
+#ifndef OQ_H
+#define OQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  OQ_OK = 0,
+  OQ_ERR_NULL = -1,      /* a required pointer is NULL                              */
+  OQ_ERR_SHAPE = -2,     /* a size is out of range or inconsistent (see each call)  */
+  OQ_ERR_ALIGN = -3,     /* a pointer or leading dimension is not aligned            */
+  OQ_ERR_DEVICE = -4,    /* the current device is not gfx950                        */
+  OQ_ERR_HIP = -5,       /* a HIP runtime call or kernel launch failed              */
+  OQ_ERR_WORKSPACE = -6, /* DiT workspace missing or too small                      */
+  OQ_ERR_ARG = -7        /* another invalid argument (enum value, step index, ...)  */
+} oq_status;
+
+/* Output element type of the dequantizing epilogue. */
+typedef enum { OQ_OUT_F16 = 0, OQ_OUT_BF16 = 1 } oq_out_dtype;
+
+/* Largest Hadamard block the rotation kernel accepts. */
+#define OQ_MAX_HAD_BLOCK 16384
+
+/* Human-readable name of a status code (static storage, never NULL). */
+const char* oq_status_string(int status);
+
+/* Library version string (static storage). */
+const char* oq_version(void);
+
+/*
+ * oq_check_device -- OQ_OK if the current HIP device is gfx950, else
+ * OQ_ERR_DEVICE (or OQ_ERR_HIP if the runtime cannot be queried).  Every
+ * launching call performs the same check once per device.
+ */
+int oq_check_device(void);
+
+/*
+ * oq_rotate_quantize_act -- online Hadamard rotation, step scale and
+ * per-token int4 quantization of one activation (Section 4.1 eq:transform
+ * with the block-diagonal Hadamard of eq:blockdiag; Section 4.2 eq:scale,
+ * eq:quant; the per-step scale of eq:perstep_scale in its per-(layer, step)
+ * scalar form).
+ *
+ * For each row i:  y = X[i, 0:K] . blockdiag(H_b) / sqrt(b)   (Sylvester
+ * order, H[r][c] = (-1)^popcount(r & c), blocks of b contiguous channels);
+ * z = s_t * y;  Delta_i = max_k |z_k| / 7;  q_k = clamp(round_half_even(
+ * z_k / Delta_i), -7, 7);  x_scale[i] = Delta_i / s_t.  A row of zeros gives
+ * zero codes and x_scale 0.  s_t = s_table[t] when s_table is not NULL, else
+ * 1; it is read on the host when the call is made.
+ *
+ * X        device fp16 [M][ldx]
+ * M        rows (tokens), >= 0 (0 is a no-op)
+ * K        channels, multiple of 8 and of had_block, <= 65536
+ * ldx      row stride of X in elements, >= K, multiple of 8
+ * had_block Hadamard block b: power of two, 1 <= b <= OQ_MAX_HAD_BLOCK, b | K
+ * s_table  host fp32 table or NULL; t indexes it (t >= 0)
+ * Xq       device [M][K/2] bytes;  x_scale device fp32 [M]
+ * Pointers X, Xq must be 16-byte aligned; x_scale 4-byte aligned.
+ * Errors: OQ_ERR_NULL, OQ_ERR_SHAPE, OQ_ERR_ALIGN, OQ_ERR_ARG (t < 0),
+ * OQ_ERR_DEVICE, OQ_ERR_HIP.
+ */
+int oq_rotate_quantize_act(const void* X, int64_t M, int64_t K, int64_t ldx,
+                           int32_t had_block, const float* s_table, int32_t t,
+                           uint8_t* Xq, float* x_scale, void* stream);
+
+/*
+ * oq_rotate_debug_f32 -- same computation as oq_rotate_quantize_act, but
+ * writes the pre-rounding ratio r = z / Delta_i of every element as fp32
+ * [M][K] (row-major, contiguous) together with x_scale, so that a code that
+ * differs from a reference can be classified as a rounding-boundary case.
+ * Arguments and errors as above; ratio must be 16-byte aligned.
+ */
+int oq_rotate_debug_f32(const void* X, int64_t M, int64_t K, int64_t ldx,
+                        int32_t had_block, const float* s_table, int32_t t,
+                        float* ratio, float* x_scale, void* stream);
+
+/*
+ * oq_w4a4_linear -- int4 x int4 product with int32 accumulation and the
+ * fused dequantization epilogue (eq:lowbit_linear; all scales folded into
+ * the dequantization as in the Implementation Details).
+ *
+ * acc[i][n] = sum_k q[i][k] * wq[n][k]           (exact, int32)
+ * Y[i][n]   = round_to_out(float(acc) * x_scale[i] * w_scale[n] + bias[n])
+ *
+ * Xq, x_scale  device, as produced by oq_rotate_quantize_act, [M][K/2], [M]
+ * Wq, w_scale  device, [N][K/2], [N] (oq_quantize_weights* produce them)
+ * bias         device fp16 [N] or NULL
+ * M >= 0, N >= 1, K >= 64 with K % 64 == 0, K <= 65536
+ * Y            device [M][ldy] of out_dtype (oq_out_dtype), ldy >= N, ldy % 8 == 0
+ * Xq, Wq, Y 16-byte aligned.  Errors: OQ_ERR_NULL, OQ_ERR_SHAPE,
+ * OQ_ERR_ALIGN, OQ_ERR_ARG (out_dtype), OQ_ERR_DEVICE, OQ_ERR_HIP.
+ */
+int oq_w4a4_linear(const uint8_t* Xq, const float* x_scale, int64_t M,
+                   const uint8_t* Wq, const float* w_scale, const void* bias,
+                   int64_t N, int64_t K, void* Y, int64_t ldy, int32_t out_dtype,
+                   void* stream);
+
+/*
+ * oq_w4a4_gemm_i32 -- the integer product alone: acc[i][n] (int32) written
+ * to device [M][ldc], ldc >= N, ldc % 4 == 0.  Shapes and errors as
+ * oq_w4a4_linear.  For parity checks of the accumulators.
+ */
+int oq_w4a4_gemm_i32(const uint8_t* Xq, int64_t M, const uint8_t* Wq, int64_t N,
+                     int64_t K, int32_t* acc, int64_t ldc, void* stream);
+
+/*
+ * oq_quantize_weights -- offline weight preparation on the device: fold the
+ * Hadamard half of the rotation into the weight and quantize it per output
+ * channel with round-to-nearest (eq:transform W' = R^T W in the output-major
+ * storage used here: row n of W' is row n of W_u times blockdiag(H_b)/sqrt(b);
+ * eq:scale / eq:quant per output channel; the DiT-side RTN solver of the
+ * Implementation Details).  W_u is the weight already expressed in the SVD
+ * basis (the SVD factor folded offline), device fp16 [N][ldw].  Identical to
+ * oq_rotate_quantize_act with s_t = 1 applied to the weight rows; writes Wq
+ * [N][K/2] and w_scale [N].  Shapes, alignment and errors as
+ * oq_rotate_quantize_act.
+ */
+int oq_quantize_weights(const void* W_u, int64_t N, int64_t K, int64_t ldw,
+                        int32_t had_block, uint8_t* Wq, float* w_scale, void* stream);
+
+/*
+ * oq_quantize_weights_host -- the same weight preparation on the host in
+ * float64 from a float64 weight (for weights that are not fp16-exact).
+ * W_u host [N][K] row-major; Wq host [N][K/2]; w_scale host fp32 [N].
+ * Runs synchronously on the calling thread.  Errors: OQ_ERR_NULL,
+ * OQ_ERR_SHAPE.
+ */
+int oq_quantize_weights_host(const double* W_u, int64_t N, int64_t K, int32_t had_block,
+                             uint8_t* Wq, float* w_scale);
+
+/* ------------------------------------------------------------------------ */
+/* DiT denoising-step driver                                                 */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * One denoising step of a DiT action head whose every block linear is a
+ * rotated W4A4 linear (Experimental Settings: W4A4 on all linears, RTN
+ * weights and the per-step activation scale table on the DiT side, Euler
+ * denoising steps).  Block structure, arch OQ_DIT_PI (Pi-0.5 action expert):
+ *
+ *   r   = x_t . W_in^T + b_in                                (fp32 residual)
+ *   per block l, step t (modulation m = mod[l][t], scales s = s_table[l][t]):
+ *     h   = fp16(rms(r) * g1 * (1 + m.sc1) + m.sh1)
+ *     qkv = fp16(W4A4(h; Wqkv, s[0]))                        q|k|v along N
+ *     o   = fp16(softmax(q k^T / sqrt(hd)) v) per head, keys = [prefix ; k]
+ *     r  += m.gt1 * W4A4(o; Wo, s[1])
+ *     h2  = fp16(rms(r) * g2 * (1 + m.sc2) + m.sh2)
+ *     gu  = fp16(W4A4(h2; Wgu, s[2]))                        gate|up along N
+ *     a   = fp16(gelu_tanh(gate) * up)
+ *     r  += m.gt2 * W4A4(a; Wd, s[3])
+ *   v   = fp16(rms(r) * g_f) . W_out^T + b_out ;  x_{t+1} = x_t + dt * v
+ *
+ * rms(r) = r / sqrt(mean(r^2) + 1e-6), dt = -1/steps, the Hadamard block of a
+ * linear is the largest power of two dividing its input size.
+ * Only OQ_DIT_PI is implemented by this version; OQ_DIT_GR00T is reserved.
+ */
+typedef enum { OQ_DIT_PI = 0, OQ_DIT_GR00T = 1 } oq_dit_arch;
+
+typedef struct {
+  int32_t arch;        /* oq_dit_arch                                        */
+  int32_t n_blocks;    /* >= 1                                               */
+  int32_t hidden;      /* D, multiple of 64; = n_heads * head_dim           */
+  int32_t mlp;         /* F, multiple of 64                                  */
+  int32_t n_heads;
+  int32_t head_dim;    /* <= 128, multiple of 8                              */
+  int32_t tokens;      /* S action tokens per sample                         */
+  int32_t prefix;      /* P prefix tokens per sample (keys before the S own) */
+  int32_t batch;       /* B samples                                          */
+  int32_t steps;       /* T denoising steps                                  */
+  int32_t action_dim;  /* A, multiple of 8                                   */
+} oq_dit_config;
+
+/* A prepared W4A4 weight: device Wq [N][K/2] and w_scale fp32 [N]. */
+typedef struct {
+  const uint8_t* wq;
+  const float* w_scale;
+} oq_qweight;
+
+/* Per-block device pointers (borrowed; the caller keeps them alive until
+ * oq_dit_destroy).  All vectors fp16. */
+typedef struct {
+  const void* g1;          /* [D] norm gain before attention                   */
+  const void* g2;          /* [D] norm gain before the MLP                     */
+  oq_qweight qkv;          /* N = 3D, K = D                                    */
+  oq_qweight o;            /* N = D,  K = D                                    */
+  oq_qweight gate_up;      /* N = 2F, K = D                                    */
+  oq_qweight down;         /* N = D,  K = F                                    */
+  const void* prefix_k;    /* [B][P][D] fp16, step-invariant                   */
+  const void* prefix_v;    /* [B][P][D] fp16                                   */
+} oq_dit_block;
+
+typedef struct {
+  const void* w_in;        /* fp16 [D][A]                                      */
+  const void* b_in;        /* fp16 [D]                                         */
+  const void* w_out;       /* fp16 [A][D]                                      */
+  const void* b_out;       /* fp16 [A]                                         */
+  const void* g_f;         /* fp16 [D] final norm gain                         */
+  const oq_dit_block* blocks; /* host array [n_blocks], copied by oq_dit_create */
+  const void* mod;         /* fp16 device [n_blocks][steps][6][D]:
+                              sc1, sh1, gt1, sc2, sh2, gt2                      */
+  const float* s_table;    /* host fp32 [n_blocks][steps][4], copied           */
+} oq_dit_weights;
+
+typedef struct oq_dit oq_dit;
+
+/* Workspace size in bytes for a config (device memory the caller provides). */
+int oq_dit_workspace_bytes(const oq_dit_config* cfg, size_t* bytes);
+
+/* Validate cfg and weights and create a handle (host memory only).
+ * Errors: OQ_ERR_NULL, OQ_ERR_SHAPE, OQ_ERR_ARG, OQ_ERR_DEVICE. */
+int oq_dit_create(const oq_dit_config* cfg, const oq_dit_weights* w, oq_dit** out);
+
+/* Attach caller-owned device workspace (256-byte aligned, at least
+ * oq_dit_workspace_bytes).  Errors: OQ_ERR_NULL, OQ_ERR_WORKSPACE, OQ_ERR_ALIGN. */
+int oq_dit_set_workspace(oq_dit* h, void* workspace, size_t bytes);
+
+/* One Euler step t (0 <= t < steps) on x (device fp32 [B][S][A], in place). */
+int oq_dit_step(oq_dit* h, float* x, int32_t t, void* stream);
+
+/* n_steps consecutive steps t = 0 .. n_steps-1 on x, in place. */
+int oq_dit_denoise(oq_dit* h, float* x, int32_t n_steps, void* stream);
+
+/* Run block l of step t alone on a residual (device fp32 [B*S][D], in place);
+ * for per-block parity checks with a teacher-forced input. */
+int oq_dit_run_block(oq_dit* h, int32_t l, int32_t t, float* resid, void* stream);
+
+/* Free the handle (not the borrowed weights or the workspace). NULL is a no-op. */
+void oq_dit_destroy(oq_dit* h);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OQ_H */

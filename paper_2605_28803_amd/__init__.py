@@ -1,0 +1,136 @@
+"""MI355X (gfx950) W4A4 rotated linear: Python binding of liboq.so.
+
+Thin marshalling layer over the C ABI in include/oq.h: every computation runs
+in the library's HIP kernels; torch only provides device memory and the
+stream.  Functions have the names of the C entry points without the ``oq_``
+prefix.  Raises OQError on a non-zero status.
+"""
+from __future__ import annotations
+
+import ctypes as C
+
+import numpy as np
+import torch
+
+from . import _lib
+
+OUT_F16, OUT_BF16 = 0, 1
+
+
+class OQError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        lib = _lib.load()
+        super().__init__(f"{where}: {lib.oq_status_string(status).decode()} ({status})")
+        self.status = status
+
+
+def lib():
+    return _lib.load()
+
+
+def _check(status: int, where: str):
+    if status != 0:
+        raise OQError(status, where)
+
+
+def _stream(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return C.c_void_p(s.cuda_stream)
+
+
+def _ptr(t):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _s_table(s_table):
+    if s_table is None:
+        return None, None
+    arr = np.ascontiguousarray(np.asarray(s_table, dtype=np.float32).reshape(-1))
+    return arr, arr.ctypes.data_as(C.POINTER(C.c_float))
+
+
+def version() -> str:
+    return lib().oq_version().decode()
+
+
+def check_device() -> int:
+    return lib().oq_check_device()
+
+
+def status_string(code: int) -> str:
+    return lib().oq_status_string(code).decode()
+
+
+def rotate_quantize_act(X, had_block, s_table=None, t=0, Xq=None, x_scale=None, stream=None):
+    """X: fp16 [M, K] (row stride X.stride(0)).  Returns (Xq uint8 [M, K/2], x_scale f32 [M])."""
+    M, K = X.shape
+    if Xq is None:
+        Xq = torch.empty((M, K // 2), dtype=torch.uint8, device=X.device)
+    if x_scale is None:
+        x_scale = torch.empty((M,), dtype=torch.float32, device=X.device)
+    keep, sp = _s_table(s_table)
+    _check(lib().oq_rotate_quantize_act(_ptr(X), M, K, X.stride(0), had_block, sp, t, _ptr(Xq),
+                                        _ptr(x_scale), _stream(stream)), "oq_rotate_quantize_act")
+    del keep
+    return Xq, x_scale
+
+
+def rotate_debug_f32(X, had_block, s_table=None, t=0, stream=None):
+    """Pre-rounding ratios z/Delta (f32 [M, K]) and x_scale."""
+    M, K = X.shape
+    ratio = torch.empty((M, K), dtype=torch.float32, device=X.device)
+    x_scale = torch.empty((M,), dtype=torch.float32, device=X.device)
+    keep, sp = _s_table(s_table)
+    _check(lib().oq_rotate_debug_f32(_ptr(X), M, K, X.stride(0), had_block, sp, t, _ptr(ratio),
+                                     _ptr(x_scale), _stream(stream)), "oq_rotate_debug_f32")
+    del keep
+    return ratio, x_scale
+
+
+def w4a4_linear(Xq, x_scale, Wq, w_scale, bias=None, out_dtype=OUT_F16, Y=None, stream=None):
+    """Y [M, N] (fp16 or bf16) = dequant(Xq . Wq^T)."""
+    M = Xq.shape[0]
+    N, Kh = Wq.shape
+    K = 2 * Kh
+    if Y is None:
+        dt = torch.float16 if out_dtype == OUT_F16 else torch.bfloat16
+        Y = torch.empty((M, N), dtype=dt, device=Xq.device)
+    _check(lib().oq_w4a4_linear(_ptr(Xq), _ptr(x_scale), M, _ptr(Wq), _ptr(w_scale), _ptr(bias), N, K,
+                                _ptr(Y), Y.stride(0), out_dtype, _stream(stream)), "oq_w4a4_linear")
+    return Y
+
+
+def w4a4_gemm_i32(Xq, Wq, acc=None, stream=None):
+    M = Xq.shape[0]
+    N, Kh = Wq.shape
+    if acc is None:
+        acc = torch.empty((M, N), dtype=torch.int32, device=Xq.device)
+    _check(lib().oq_w4a4_gemm_i32(_ptr(Xq), M, _ptr(Wq), N, 2 * Kh, _ptr(acc), acc.stride(0),
+                                  _stream(stream)), "oq_w4a4_gemm_i32")
+    return acc
+
+
+def quantize_weights(W_u, had_block, Wq=None, w_scale=None, stream=None):
+    """W_u fp16 [N, K] on the device -> (Wq uint8 [N, K/2], w_scale f32 [N])."""
+    N, K = W_u.shape
+    if Wq is None:
+        Wq = torch.empty((N, K // 2), dtype=torch.uint8, device=W_u.device)
+    if w_scale is None:
+        w_scale = torch.empty((N,), dtype=torch.float32, device=W_u.device)
+    _check(lib().oq_quantize_weights(_ptr(W_u), N, K, W_u.stride(0), had_block, _ptr(Wq), _ptr(w_scale),
+                                     _stream(stream)), "oq_quantize_weights")
+    return Wq, w_scale
+
+
+def quantize_weights_host(W_u: np.ndarray, had_block: int):
+    """float64 host weight [N, K] -> (Wq uint8 [N, K/2], w_scale f32 [N]) numpy arrays."""
+    W = np.ascontiguousarray(W_u, dtype=np.float64)
+    N, K = W.shape
+    Wq = np.empty((N, K // 2), dtype=np.uint8)
+    ws = np.empty((N,), dtype=np.float32)
+    _check(lib().oq_quantize_weights_host(W.ctypes.data, N, K, had_block, Wq.ctypes.data, ws.ctypes.data),
+           "oq_quantize_weights_host")
+    return Wq, ws
+
+
+

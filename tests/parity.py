@@ -1,0 +1,89 @@
+"""Helpers of the GPU-vs-oracle parity tests (test code; shares nothing with
+the HIP path).
+
+Tolerances (the three bars of the parity criterion):
+  * int4 codes: bit-exact, except elements whose exact ratio r = z/Delta lies
+    within the fp32 error bound tau of a rounding boundary (a half integer);
+    such a mismatch must be exactly one code, and the count must stay below
+    1e-4 of the elements.
+  * int32 accumulators: bit-exact when the oracle is fed the GPU's codes.
+  * fp16 / bf16 outputs: relative L2 error <= 2e-3 against the oracle fed the
+    same codes and scales.
+
+tau.  The kernel forms the unnormalized transform u in fp32 with a summation
+tree of depth d <= log2(b) + 1, so |u_hat - u| <= gamma_d * l1 with
+gamma_d = d 2^-24 / (1 - d 2^-24) and l1 the largest per-block sum of |x|.
+The row maximum inherits the same error, and three more fp32 roundings form
+the multiplier g ~ 7 / max|u|.  Hence
+    |r_gpu - r_exact| <= 14 gamma_d l1 / max|u| + 21 * 2^-24  =: tau_row.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+U32 = 2.0 ** -24
+CODE_MISMATCH_FRAC = 1e-4
+REL_L2_OUT = 2e-3
+
+
+def unpack_int4(packed: np.ndarray) -> np.ndarray:
+    """uint8 [R, K/2] (low nibble = even channel, two's complement) -> int64 [R, K]."""
+    p = np.asarray(packed, dtype=np.uint8)
+    lo = (p & 0xF).astype(np.int64)
+    hi = (p >> 4).astype(np.int64)
+    lo = np.where(lo >= 8, lo - 16, lo)
+    hi = np.where(hi >= 8, hi - 16, hi)
+    out = np.empty(p.shape[:-1] + (2 * p.shape[-1],), dtype=np.int64)
+    out[..., 0::2] = lo
+    out[..., 1::2] = hi
+    return out
+
+
+def tau_rows(x: np.ndarray, b: int) -> np.ndarray:
+    """Per-row bound on |r_gpu - r_exact| for activation rows x [M, K]."""
+    x = np.asarray(x, dtype=np.float64)
+    M, K = x.shape
+    d = int(np.log2(b)) + 1
+    gamma = d * U32 / (1 - d * U32)
+    l1 = np.abs(x).reshape(M, K // b, b).sum(axis=2).max(axis=1)
+    # max|u| (unnormalized) = sqrt(b) * max|y|; recomputed from the data.
+    from oracle.hadamard import fwht  # the oracle's transform, exact to ~1e-15
+    umax = np.abs(fwht(x, b)).max(axis=1) * np.sqrt(b)
+    safe = np.where(umax > 0, umax, 1.0)
+    return np.where(umax > 0, 14 * gamma * l1 / safe + 21 * U32, 0.0)
+
+
+def dist_to_boundary(r: np.ndarray) -> np.ndarray:
+    """Distance of each ratio to the nearest half integer."""
+    return np.abs(np.abs(r - np.floor(r)) - 0.5)
+
+
+def check_codes(q_gpu, q_ref, r_ref, tau_row):
+    """Returns (n_mismatch, n_boundary_1ulp) and asserts the code criterion."""
+    q_gpu = np.asarray(q_gpu)
+    q_ref = np.asarray(q_ref)
+    mism = q_gpu != q_ref
+    n = int(mism.sum())
+    total = q_ref.size
+    near = dist_to_boundary(r_ref) <= tau_row[:, None]
+    if n:
+        assert np.all(np.abs(q_gpu[mism] - q_ref[mism]) == 1), "a code differs by more than one step"
+        assert np.all(near[mism]), "a code differs away from a rounding boundary"
+    assert n <= CODE_MISMATCH_FRAC * total, f"{n} code mismatches of {total}"
+    assert q_gpu.min() >= -7 and q_gpu.max() <= 7, "code outside [-7, 7]"
+    ulp = np.spacing(np.abs(r_ref).astype(np.float32)).astype(np.float64)
+    n_ulp = int((dist_to_boundary(r_ref) <= ulp).sum())
+    return n, n_ulp
+
+
+def rel_l2(a, b) -> float:
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    den = np.linalg.norm(b)
+    return float(np.linalg.norm(a - b) / (den if den > 0 else 1.0))
+
+
+def pack_int4(codes: np.ndarray) -> np.ndarray:
+    """int [R, K] codes in [-8, 7] -> uint8 [R, K/2], low nibble = even channel."""
+    c = np.asarray(codes, dtype=np.int64) & 0xF
+    return (c[..., 0::2] | (c[..., 1::2] << 4)).astype(np.uint8)

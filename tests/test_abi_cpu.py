@@ -1,0 +1,104 @@
+"""The C ABI without a GPU: the library loads, exports every declared entry
+point, rejects bad arguments before touching the device, and the host-side
+weight preparation matches the oracle."""
+import ctypes as C
+import os
+
+import numpy as np
+import pytest
+
+from paper_2605_28803_amd import _lib
+import paper_2605_28803_amd as oq
+from oracle import quant
+from tests import parity
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "oq.h")
+
+OK, NULL, SHAPE, ALIGN, DEVICE, HIP, WORKSPACE, ARG = 0, -1, -2, -3, -4, -5, -6, -7
+P16 = C.c_void_p(0x10000)     # fake, 16-byte aligned; never dereferenced on error paths
+P4 = C.c_void_p(0x10004)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return _lib.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _lib.header_symbols(HEADER)
+    assert len(names) >= 15
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_status_strings(lib):
+    for code in (OK, NULL, SHAPE, ALIGN, DEVICE, HIP, WORKSPACE, ARG):
+        s = lib.oq_status_string(code).decode()
+        assert s.startswith("OQ_")
+    assert "unknown" in lib.oq_status_string(12345).decode()
+    assert "gfx950" in lib.oq_version().decode()
+
+
+def test_rotate_quantize_rejects_bad_arguments(lib):
+    f = lib.oq_rotate_quantize_act
+    assert f(None, 4, 64, 64, 64, None, 0, P16, P16, None) == NULL
+    assert f(P16, 4, 64, 64, 64, None, 0, None, P16, None) == NULL
+    assert f(P16, -1, 64, 64, 64, None, 0, P16, P16, None) == SHAPE
+    assert f(P16, 4, 60, 64, 4, None, 0, P16, P16, None) == SHAPE        # K % 8
+    assert f(P16, 4, 96, 96, 64, None, 0, P16, P16, None) == SHAPE       # b does not divide K
+    assert f(P16, 4, 64, 64, 48, None, 0, P16, P16, None) == SHAPE       # b not a power of two
+    assert f(P16, 4, 64, 32, 64, None, 0, P16, P16, None) == SHAPE       # ldx < K
+    assert f(P16, 4, 40, 40, 8, None, 0, P16, P16, None) == SHAPE        # K/8 = 5 unsupported
+    assert f(P16, 4, 32768, 32768, 64, None, 0, P16, P16, None) == SHAPE  # K too large
+    assert f(P4, 4, 64, 64, 64, None, 0, P16, P16, None) == ALIGN
+    assert f(P16, 4, 64, 68, 64, None, 0, P16, P16, None) == ALIGN       # ldx % 8
+    assert f(P16, 4, 64, 64, 64, None, -1, P16, P16, None) == ARG
+
+
+def test_gemm_rejects_bad_arguments(lib):
+    g = lib.oq_w4a4_linear
+    assert g(None, P16, 4, P16, P16, None, 64, 64, P16, 64, 0, None) == NULL
+    assert g(P16, None, 4, P16, P16, None, 64, 64, P16, 64, 0, None) == NULL
+    assert g(P16, P16, 4, P16, P16, None, 64, 32, P16, 64, 0, None) == SHAPE   # K < 64
+    assert g(P16, P16, 4, P16, P16, None, 64, 96, P16, 64, 0, None) == SHAPE   # K % 64
+    assert g(P16, P16, 4, P16, P16, None, 0, 64, P16, 64, 0, None) == SHAPE    # N < 1
+    assert g(P16, P16, 4, P16, P16, None, 64, 64, P16, 32, 0, None) == SHAPE   # ldy < N
+    assert g(P4, P16, 4, P16, P16, None, 64, 64, P16, 64, 0, None) == ALIGN
+    assert g(P16, P16, 4, P16, P16, None, 64, 64, P16, 68, 0, None) == ALIGN   # ldy % 8
+    assert g(P16, P16, 4, P16, P16, None, 64, 64, P16, 64, 7, None) == ARG     # out dtype
+    h = lib.oq_w4a4_gemm_i32
+    assert h(P16, 4, None, 64, 64, P16, 64, None) == NULL
+    assert h(P16, 4, P16, 64, 64, P16, 66, None) == ALIGN
+
+
+def test_valid_call_without_gpu_fails_cleanly(lib):
+    try:
+        import torch
+        if torch.cuda.is_available():
+            pytest.skip("a GPU is present")
+    except Exception:
+        pass
+    st = lib.oq_rotate_quantize_act(P16, 4, 64, 64, 64, None, 0, P16, P16, None)
+    assert st in (HIP, DEVICE)
+
+
+@pytest.mark.parametrize("N,K,b", [(8, 64, 64), (33, 1024, 1024), (16, 1536, 512), (5, 256, 8)])
+def test_host_weight_preparation_matches_oracle(N, K, b):
+    rng = np.random.default_rng(N * K + b)
+    W = rng.standard_normal((N, K)) * 0.02
+    Wq, ws = oq.quantize_weights_host(W, b)
+    qo, wso, ro = quant.quantize_weights(W, b)
+    q = parity.unpack_int4(Wq)
+    # Both sides are float64; codes may differ only within 1e-12 of a boundary.
+    diff = q != qo
+    assert np.all(~diff | (parity.dist_to_boundary(ro) < 1e-12))
+    assert np.allclose(ws, wso.astype(np.float32), rtol=1e-7, atol=0)
+    assert not np.any((Wq & 0xF) == 8) and not np.any((Wq >> 4) == 8)
+
+
+def test_host_weight_preparation_rejects_bad_arguments(lib):
+    f = lib.oq_quantize_weights_host
+    assert f(None, 4, 64, 64, P16, P16) == NULL
+    assert f(P16, 4, 64, 48, P16, P16) == SHAPE
+    assert f(P16, 0, 64, 64, P16, P16) == SHAPE

@@ -1,0 +1,99 @@
+"""W4A4 product and dequantizing epilogue against the oracle (GPU).
+
+int32 accumulators must be bit-exact given identical codes; fp16 / bf16
+outputs within 2e-3 relative L2 of the oracle fed identical codes and scales;
+the full rotated linear (independent codes on both sides) within the same."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2605_28803_amd as oq
+from oracle import linear, quant
+from tests import parity
+from workloads import configs, linear_inputs
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+
+
+def _codes(rng, R, K):
+    return rng.integers(-7, 8, size=(R, K))
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 64, 64), (50, 1024, 1024), (64, 128, 128), (200, 320, 1024),
+                                   (257, 192, 1536), (130, 3072, 1024), (33, 256, 4096),
+                                   (300, 512, 6144)])
+def test_i32_accumulators_bit_exact(M, N, K):
+    print(f"gemm i32 M={M} N={N} K={K}", flush=True)
+    rng = np.random.default_rng(M + N + K)
+    q, qw = _codes(rng, M, K), _codes(rng, N, K)
+    acc = oq.w4a4_gemm_i32(torch.from_numpy(parity.pack_int4(q)).to(DEV),
+                           torch.from_numpy(parity.pack_int4(qw)).to(DEV))
+    torch.cuda.synchronize()
+    assert np.array_equal(acc.cpu().numpy().astype(np.int64), linear.int_gemm(q, qw))
+
+
+def test_i32_extreme_magnitudes():
+    """Every code +-7 at K = 16384: |acc| = 49 K, the largest the format allows."""
+    K = 16384
+    q = np.full((3, K), 7)
+    q[1] = -7
+    q[2, ::2] = -7
+    qw = np.full((4, K), 7)
+    qw[1] = -7
+    qw[2, 1::2] = -7
+    acc = oq.w4a4_gemm_i32(torch.from_numpy(parity.pack_int4(q)).to(DEV),
+                           torch.from_numpy(parity.pack_int4(qw)).to(DEV)).cpu().numpy()
+    assert np.array_equal(acc.astype(np.int64), linear.int_gemm(q, qw))
+    assert acc[0, 0] == 49 * K and acc[1, 0] == -49 * K
+
+
+@pytest.mark.parametrize("out_dtype", [oq.OUT_F16, oq.OUT_BF16])
+@pytest.mark.parametrize("M,N,K", [(50, 1024, 1024), (200, 320, 2048), (77, 1000, 4096)])
+def test_dequant_epilogue(M, N, K, out_dtype):
+    rng = np.random.default_rng(M * N + K)
+    q, qw = _codes(rng, M, K), _codes(rng, N, K)
+    xs = rng.uniform(0.01, 2.0, M).astype(np.float32)
+    ws = rng.uniform(1e-4, 1e-2, N).astype(np.float32)
+    bias = (rng.standard_normal(N) * 0.1).astype(np.float16)
+    Y = oq.w4a4_linear(torch.from_numpy(parity.pack_int4(q)).to(DEV), torch.from_numpy(xs).to(DEV),
+                       torch.from_numpy(parity.pack_int4(qw)).to(DEV), torch.from_numpy(ws).to(DEV),
+                       bias=torch.from_numpy(bias).to(DEV), out_dtype=out_dtype)
+    ref = linear.dequant(linear.int_gemm(q, qw), xs, ws, bias.astype(np.float64))
+    err = parity.rel_l2(Y.float().cpu().numpy(), ref)
+    print(f"dequant rel_l2={err:.3e}")
+    assert err <= parity.REL_L2_OUT
+
+
+def test_full_rotated_linear_1024():
+    """The single rotated linear: X [64 x 1024] with 8 outlier channels x50,
+    W [1024 x 1024] ~ N(0, 0.02^2), U random orthogonal folded into W, b = 1024,
+    s_t = 1.  Both sides quantize independently."""
+    case = configs.LINEAR_1024
+    inp = linear_inputs.make_linear_inputs(case)
+    w_u = inp["w"] @ inp["u"]
+    b = case.had_block
+    X = torch.from_numpy(inp["x"].astype(np.float16)).to(DEV)
+    Xq, xs = oq.rotate_quantize_act(X, b)
+    Wq, ws = oq.quantize_weights_host(w_u, b)
+    Y = oq.w4a4_linear(Xq, xs, torch.from_numpy(Wq).to(DEV), torch.from_numpy(ws).to(DEV))
+    torch.cuda.synchronize()
+    ref = linear.w4a4_linear(inp["x"], w_u, b)
+    # Codes of the activation against the oracle's.
+    tau = parity.tau_rows(inp["x"], b)
+    n_mis, _ = parity.check_codes(parity.unpack_int4(Xq.cpu().numpy()), ref["q"], ref["ratio"], tau)
+    # Accumulators exact given the GPU's own codes.
+    acc = oq.w4a4_gemm_i32(Xq, torch.from_numpy(Wq).to(DEV)).cpu().numpy()
+    q_gpu = parity.unpack_int4(Xq.cpu().numpy())
+    assert np.array_equal(acc.astype(np.int64), linear.int_gemm(q_gpu, parity.unpack_int4(Wq)))
+    # Output against the oracle fed the GPU's codes and scales, and against the
+    # fully independent oracle pipeline.
+    y = Y.float().cpu().numpy()
+    same = linear.dequant(acc, xs.cpu().numpy(), ws)
+    assert parity.rel_l2(y, same) <= parity.REL_L2_OUT
+    e_ind = parity.rel_l2(y, ref["y"])
+    print(f"cfg linear_1024: code mismatches={n_mis}, rel_l2 vs independent oracle={e_ind:.3e}")
+    assert e_ind <= parity.REL_L2_OUT
+    # Information: the quantized layer approximates the unrotated fp64 product.
+    exact = (inp["x"] @ inp["u"].T) @ inp["w"].T
+    print(f"  W4A4 vs exact fp64 rel_l2={parity.rel_l2(y, exact):.3e}")
