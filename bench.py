@@ -1,0 +1,293 @@
+#!/usr/bin/env python3
+"""Benchmark: DiT denoising-step latency of the W4A4 Pi-0.5 action expert on one MI355X.
+
+Workload: 18 blocks, hidden 1024, MLP 4096 (gate|up, down), 8 heads x 128,
+50 action tokens attending to 816 prefix tokens, batch 1, 10 denoising steps,
+per-step scales s[l][t] log-uniform in [0.5, 4], every block linear W4A4 with
+Hadamard blocks 1024 / 4096, seeded Gaussian weights (synthetic).  One bench
+step = one denoising step (all of: rotate-quantize, W4A4 GEMM + epilogue,
+norms, attention, Euler) with t cycling over the 10 steps.  Inputs are resident
+in HBM before timing.
+
+Also reported (same JSON line):
+  kernels    the W4A4 linears of one step timed alone through the C ABI with
+             HIP events on the launch stream: rotate-quantize GB/s and GEMM
+             GB/s / TOPS against their rooflines;
+  roofline   the dominant kernel of the step (the W4A4 GEMM) against HBM peak;
+  cpu_baseline  the oracle on this host on a bounded sample (3 of 18 blocks of
+             one step), scaled to denoising steps per second.
+
+--sweep writes the rotate-quantize / GEMM roofline sweep (M x K = N grid) as
+JSON lines to gpurun_out/sweep.jsonl instead.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "W4A4 linear TOPS & %MFMA peak; rotate-quant GB/s; DiT denoise-step latency"
+HBM_PEAK_GBS = 8000.0
+INT8_PEAK_TOPS = 5000.0  # dense int8 MFMA, TOP/s
+
+
+def _events_time(fn, iters, stream):
+    import torch
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(iters):
+        fn()
+    end.record(stream)
+    end.synchronize()
+    return start.elapsed_time(end) / iters  # ms
+
+
+def dit_linears(cfg):
+    """(name, K, N, M) of the four W4A4 linears of one block."""
+    M = cfg.batch * cfg.tokens
+    D, F = cfg.hidden, cfg.mlp
+    return [("qkv", D, 3 * D, M), ("o", D, D, M), ("gate_up", D, 2 * F, M), ("down", F, D, M)]
+
+
+def gemm_bytes(M, N, K, out_bytes):
+    """Algorithmic HBM bytes of one W4A4 GEMM launch: packed codes of both
+    operands, both scale vectors, the output (fp16 store, or fp32 residual
+    read + write)."""
+    return (M * K + N * K) // 2 + 4 * (M + N) + out_bytes * M * N
+
+
+def rq_bytes(M, K):
+    """Algorithmic HBM bytes of one rotate-quantize launch: fp16 in, int4 + fp32 scale out."""
+    return 2 * M * K + M * K // 2 + 4 * M
+
+
+def time_linears(cfg, qweights, stream, iters=200):
+    """Time each W4A4 linear shape of the step (rotate-quantize + GEMM) through the C ABI."""
+    import torch
+    import paper_2605_28803_amd as oq
+    out = {}
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device="cpu").manual_seed(0)
+    tot = {"rq_ms": 0.0, "rq_bytes": 0, "gemm_ms": 0.0, "gemm_bytes": 0, "gemm_ops": 0, "gemm_launches": 0,
+           "rq_launches": 0}
+    names = {"qkv": "wqkv", "o": "wo", "gate_up": "wgu", "down": "wd"}
+    for name, K, N, M in dit_linears(cfg):
+        X = (torch.randn((M, K), generator=g) * 2).half().to(dev)
+        Wq, ws = qweights[0][names[name]]
+        Xq, xs = oq.rotate_quantize_act(X, K & -K, stream=stream)
+        # Every linear is timed with the fp16-store epilogue; inside the step the
+        # o and down projections add into the fp32 residual instead.
+        Y = torch.empty((M, N), dtype=torch.float16, device=dev)
+        gemm = lambda: oq.w4a4_linear(Xq, xs, Wq, ws, Y=Y, stream=stream)
+        rq = lambda: oq.rotate_quantize_act(X, K & -K, Xq=Xq, x_scale=xs, stream=stream)
+        for _ in range(10):
+            rq(); gemm()
+        t_rq = _events_time(rq, iters, stream)
+        t_g = _events_time(gemm, iters, stream)
+        b_g = gemm_bytes(M, N, K, 2)
+        b_r = rq_bytes(M, K)
+        out[name] = {"M": M, "N": N, "K": K, "rq_us": round(t_rq * 1e3, 3), "gemm_us": round(t_g * 1e3, 3),
+                     "rq_GBs": round(b_r / (t_rq * 1e-3) / 1e9, 1), "gemm_GBs": round(b_g / (t_g * 1e-3) / 1e9, 1),
+                     "gemm_TOPs": round(2 * M * N * K / (t_g * 1e-3) / 1e12, 3)}
+        tot["rq_ms"] += t_rq
+        tot["rq_bytes"] += b_r
+        tot["gemm_ms"] += t_g
+        tot["gemm_bytes"] += b_g
+        tot["gemm_ops"] += 2 * M * N * K
+        tot["gemm_launches"] += 1
+        tot["rq_launches"] += 1
+    return out, tot
+
+
+def cpu_baseline(cfg, inp, n_blocks_sample=3):
+    """The oracle, untouched, on a bounded sample: n_blocks_sample blocks of one
+    denoising step (weights quantized beforehand, not timed), scaled to the
+    full step.  Returns the dict for the JSON line."""
+    from oracle import dit as odit
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([int(i.get("num_threads", 1)) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = 1
+    L = n_blocks_sample
+    w = dict(inp["w"])
+    w["blocks"] = inp["w"]["blocks"][:L]
+    qb = odit.quantize_block_weights(cfg, w["blocks"])
+    B, S = inp["batch"], cfg.tokens
+    r = odit.in_projection(w, inp["x0"])
+    t0 = time.perf_counter()
+    for l in range(L):
+        r = odit.block(cfg, w, qb, inp["mod"], inp["s_table"], r, l, 0, B, S, prefix=(inp["kp"], inp["vp"]))
+    dt = time.perf_counter() - t0
+    per_step = dt * cfg.n_blocks / L
+    return {"value": round(1.0 / per_step, 5), "unit": "DiT denoise-steps/s", "cores": cores, "kind": "oracle",
+            "sample": f"{L} of {cfg.n_blocks} blocks of one denoising step ({dt:.2f} s), scaled x{cfg.n_blocks / L:g}; "
+                      f"float64 numpy, BLAS threads={cores}, host cpus={len(os.sched_getaffinity(0))}"}
+
+
+def run_dit(args):
+    import torch
+    import paper_2605_28803_amd as oq
+    from workloads import configs, dit_inputs
+
+    cfg = configs.DIT_PI
+    t0 = time.perf_counter()
+    inp = dit_inputs.make_dit_inputs(cfg)
+    model = oq.DiT(cfg, inp, device="cuda:0")
+    setup_s = time.perf_counter() - t0
+    print(f"[bench] setup {setup_s:.1f} s", file=sys.stderr, flush=True)
+    stream = torch.cuda.current_stream()
+    x = torch.from_numpy(inp["x0"].astype(np.float32)).cuda()
+    x_init = x.clone()
+
+    t = 0
+    for _ in range(args.warmup):
+        model.step(x, t % cfg.steps, stream=stream)
+        t += 1
+    torch.cuda.synchronize()
+    x.copy_(x_init)
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for k in range(args.steps):
+        model.step(x, k % cfg.steps, stream=stream)
+    end.record(stream)
+    end.synchronize()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / args.steps
+    assert torch.isfinite(x).all().item(), "non-finite action state"
+    print(f"[bench] {args.steps} steps, {ms:.3f} ms/step", file=sys.stderr, flush=True)
+
+    kern, tot = time_linears(cfg, model.qweights, stream)
+    gemm_avg_us = tot["gemm_ms"] / tot["gemm_launches"] * 1e3
+    gemm_avg_bytes = tot["gemm_bytes"] / tot["gemm_launches"]
+    achieved = gemm_avg_bytes / (gemm_avg_us * 1e-6) / 1e9
+    rq_gbs = tot["rq_bytes"] / (tot["rq_ms"] * 1e-3) / 1e9
+    traffic = None
+    tpath = os.path.join(ROOT, "profiles", "traffic_dit_gemm.json")
+    if os.path.exists(tpath):
+        try:
+            traffic = json.load(open(tpath)).get("bytes_per_launch")
+        except Exception:
+            traffic = None
+    line = {
+        "metric": METRIC,
+        "value": round(1000.0 / ms, 3),
+        "unit": "DiT denoise-steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int4xint4->i32",
+        "data": "synthetic",
+        "config": {"workload": "dit_pi05_expert: 18 blocks, hidden 1024, mlp 4096 (gate|up, down), 8x128 heads, "
+                               "50 action + 816 prefix tokens, batch 1, 10 denoising steps, W4A4 all block linears, "
+                               "Hadamard 1024/4096, s_t log-uniform [0.5,4]",
+                   "global_batch": 1, "seq_len": cfg.tokens, "timing": "warm (weights + prefix K/V fit the MALL)"},
+        "dit_step_latency_us": round(ms * 1e3, 2),
+        "roofline": {"kernel": "gemm_w4a4_kernel (DiT step shapes, M=50)", "bound": "hbm",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "avg_launch_us": round(gemm_avg_us, 3), "algorithmic_bytes_per_launch": int(gemm_avg_bytes)},
+        "kernels": {"per_linear": kern,
+                    "rotate_quant_GBs": round(rq_gbs, 1),
+                    "gemm_TOPs": round(tot["gemm_ops"] / (tot["gemm_ms"] * 1e-3) / 1e12, 3),
+                    "gemm_frac_int8_peak": round(tot["gemm_ops"] / (tot["gemm_ms"] * 1e-3) / 1e12 / INT8_PEAK_TOPS, 5)},
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline (oracle sample)", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(cfg, inp)
+    model.close()
+    print(json.dumps(line), flush=True)
+
+
+def run_sweep(args):
+    """Rotate-quantize and GEMM roofline sweep over M x (K = N); cold-ish timing
+    (a 512 MB buffer is rewritten between timed launches to evict the MALL)."""
+    import torch
+    import paper_2605_28803_amd as oq
+    from workloads import configs
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    flush = torch.empty((512 << 20,), dtype=torch.uint8, device=dev)
+    os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
+    path = os.path.join(ROOT, "gpurun_out", "sweep.jsonl")
+    Ms = [int(m) for m in args.sweep_m.split(",")] if args.sweep_m else list(configs.SWEEP.Ms)
+    Ks = [int(k) for k in args.sweep_k.split(",")] if args.sweep_k else list(configs.SWEEP.Ks)
+    with open(path, "w") as f:
+        for M in Ms:
+            for K in Ks:
+                N = K
+                g = torch.Generator(device="cpu").manual_seed(1000 + M + K)
+                X = torch.randn((M, K), generator=g).half().to(dev)
+                W = (torch.randn((N, K), generator=g) * 0.02).half().to(dev)
+                Wq, ws = oq.quantize_weights(W, K)
+                del W
+                Xq, xs = oq.rotate_quantize_act(X, K)
+                Y = torch.empty((M, N), dtype=torch.float16, device=dev)
+
+                def timed(fn, reps):
+                    ts = []
+                    for _ in range(reps):
+                        flush.fill_(1)
+                        s = torch.cuda.Event(enable_timing=True)
+                        e = torch.cuda.Event(enable_timing=True)
+                        s.record(stream)
+                        fn()
+                        e.record(stream)
+                        e.synchronize()
+                        ts.append(s.elapsed_time(e))
+                    return float(np.median(ts))
+
+                rq = lambda: oq.rotate_quantize_act(X, K, Xq=Xq, x_scale=xs, stream=stream)
+                gm = lambda: oq.w4a4_linear(Xq, xs, Wq, ws, Y=Y, stream=stream)
+                rq(); gm()
+                reps = 20
+                t_rq = timed(rq, reps)
+                t_g = timed(gm, reps)
+                rec = {"M": M, "K": K, "N": N, "rq_us": round(t_rq * 1e3, 2),
+                       "rq_GBs": round(rq_bytes(M, K) / (t_rq * 1e-3) / 1e9, 1),
+                       "rq_frac_hbm": round(rq_bytes(M, K) / (t_rq * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                       "gemm_us": round(t_g * 1e3, 2),
+                       "gemm_TOPs": round(2 * M * N * K / (t_g * 1e-3) / 1e12, 2),
+                       "gemm_frac_int8": round(2 * M * N * K / (t_g * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4),
+                       "gemm_GBs": round(gemm_bytes(M, N, K, 2) / (t_g * 1e-3) / 1e9, 1)}
+                f.write(json.dumps(rec) + "\n")
+                f.flush()
+                print(json.dumps(rec), flush=True)
+                del Xq, xs, Y, Wq, ws, X
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--sweep", action="store_true")
+    ap.add_argument("--sweep-m", default="")
+    ap.add_argument("--sweep-k", default="")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (--gpus must be 1)", file=sys.stderr)
+        sys.exit(2)
+    if args.sweep:
+        run_sweep(args)
+    else:
+        run_dit(args)
+
+
+if __name__ == "__main__":
+    main()

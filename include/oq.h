@@ -98,7 +98,8 @@ int oq_check_device(void);
  *
  * X        device fp16 [M][ldx]
  * M        rows (tokens), >= 0 (0 is a no-op)
- * K        channels, multiple of 8 and of had_block, <= 65536
+ * K        channels, multiple of 8 and of had_block, <= 16384; K/8 must be a
+ *          power of two times 1 or 3 (every hidden size used here is)
  * ldx      row stride of X in elements, >= K, multiple of 8
  * had_block Hadamard block b: power of two, 1 <= b <= OQ_MAX_HAD_BLOCK, b | K
  * s_table  host fp32 table or NULL; t indexes it (t >= 0)
@@ -133,7 +134,7 @@ int oq_rotate_debug_f32(const void* X, int64_t M, int64_t K, int64_t ldx,
  * Xq, x_scale  device, as produced by oq_rotate_quantize_act, [M][K/2], [M]
  * Wq, w_scale  device, [N][K/2], [N] (oq_quantize_weights* produce them)
  * bias         device fp16 [N] or NULL
- * M >= 0, N >= 1, K >= 64 with K % 64 == 0, K <= 65536
+ * M >= 0, N >= 1, K >= 64 with K % 64 == 0, K <= 16384
  * Y            device [M][ldy] of out_dtype (oq_out_dtype), ldy >= N, ldy % 8 == 0
  * Xq, Wq, Y 16-byte aligned.  Errors: OQ_ERR_NULL, OQ_ERR_SHAPE,
  * OQ_ERR_ALIGN, OQ_ERR_ARG (out_dtype), OQ_ERR_DEVICE, OQ_ERR_HIP.
@@ -271,6 +272,25 @@ int oq_dit_denoise(oq_dit* h, float* x, int32_t n_steps, void* stream);
 /* Run block l of step t alone on a residual (device fp32 [B*S][D], in place);
  * for per-block parity checks with a teacher-forced input. */
 int oq_dit_run_block(oq_dit* h, int32_t l, int32_t t, float* resid, void* stream);
+
+/* Intermediate tensors of the most recent block the handle ran (fp16,
+ * row-major, M = batch * tokens rows), for per-site parity checks: every
+ * quantized linear's fp16 input and every fp16 output of the block can be
+ * compared with the oracle fed the GPU's own upstream values.  Pointers into
+ * the workspace, valid until the next call on the handle. */
+typedef struct {
+  const void* h1;        /* [M][D]  norm output, input of the q|k|v linear      */
+  const void* qkv;       /* [M][3D] q|k|v linear output                          */
+  const void* attn;      /* [M][D]  attention output, input of the o linear      */
+  const void* h2;        /* [M][D]  norm output, input of the gate|up linear     */
+  const void* gate_up;   /* [M][2F] gate|up linear output                        */
+  const void* act;       /* [M][F]  gelu(gate) * up, input of the down linear    */
+  const float* resid;    /* [M][D]  fp32 residual of the last oq_dit_step after
+                            its last block (oq_dit_run_block uses the caller's) */
+} oq_dit_intermediates;
+
+/* Fill *out with the intermediate pointers.  Errors: OQ_ERR_NULL, OQ_ERR_WORKSPACE. */
+int oq_dit_get_intermediates(const oq_dit* h, oq_dit_intermediates* out);
 
 /* Free the handle (not the borrowed weights or the workspace). NULL is a no-op. */
 void oq_dit_destroy(oq_dit* h);

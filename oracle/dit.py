@@ -127,6 +127,54 @@ def cond_kv(cfg, qblocks, cond):
     return out
 
 
+def block(cfg, w, qblocks, mod, s_table, r, l, t, B, S, prefix=None, ckv=None):
+    """Block l at step t on the residual r [B*S, D] (float64); returns the new residual."""
+    D, H, F = cfg.hidden, cfg.n_heads, cfg.mlp
+    blk, qb, m = w["blocks"][l], qblocks[l], mod[l][t]
+    st = s_table[l, t]
+    if cfg.arch == "pi":
+        h = f16(rms_norm(r) * blk["g1"] * (1.0 + m["sc1"]) + m["sh1"])
+        qkv = f16(_lin(h, qb, "wqkv", st[0]))
+        o = np.empty((B * S, D))
+        Kp, Vp = prefix
+        for b in range(B):
+            rows = slice(b * S, (b + 1) * S)
+            kk = np.concatenate([Kp[l, b], qkv[rows, D:2 * D]], axis=0)
+            vv = np.concatenate([Vp[l, b], qkv[rows, 2 * D:]], axis=0)
+            o[rows] = attention(qkv[rows, :D], kk, vv, H)
+        o = f16(o)
+        r = r + m["gt1"] * _lin(o, qb, "wo", st[1])
+        h2 = f16(rms_norm(r) * blk["g2"] * (1.0 + m["sc2"]) + m["sh2"])
+        gu = f16(_lin(h2, qb, "wgu", st[2]))
+        a = f16(gelu_tanh(gu[:, :F]) * gu[:, F:])
+        return r + m["gt2"] * _lin(a, qb, "wd", st[3])
+    if cfg.arch == "gr00t":
+        h = f16(layer_norm(r) * blk["g1"] * (1.0 + m["sc1"]) + m["sh1"])
+        o = np.empty((B * S, D))
+        if l % 2 == 0:
+            q = f16(_lin(h, qb, "wq", st[0]))
+            for b in range(B):
+                rows = slice(b * S, (b + 1) * S)
+                o[rows] = attention(q[rows], ckv[l][b, :, :D], ckv[l][b, :, D:], H)
+        else:
+            qkv = f16(_lin(h, qb, "wqkv", st[0]))
+            for b in range(B):
+                rows = slice(b * S, (b + 1) * S)
+                o[rows] = attention(qkv[rows, :D], qkv[rows, D:2 * D], qkv[rows, 2 * D:], H)
+        o = f16(o)
+        r = r + _lin(o, qb, "wo", st[1])
+        h3 = f16(layer_norm(r) * blk["g3"] + blk["beta3"])
+        f = f16(gelu_tanh(_lin(h3, qb, "wff0", st[2])))
+        return r + _lin(f, qb, "wff2", st[3])
+    raise ValueError(cfg.arch)
+
+
+def in_projection(w, x_t):
+    """r = x_t . W_in^T + b_in for x_t [B, S, A] -> [B*S, D]."""
+    B, S, A = x_t.shape
+    return x_t.reshape(B * S, A) @ np.asarray(w["w_in"], np.float64).T + w["b_in"][None, :]
+
+
 def step(cfg, w, qblocks, mod, s_table, x_t, t, prefix=None, ckv=None, trace=None):
     """One Euler denoising step.  x_t [B, S, A] float64 -> x_{t+1}.
 
@@ -138,48 +186,9 @@ def step(cfg, w, qblocks, mod, s_table, x_t, t, prefix=None, ckv=None, trace=Non
     receives the residual after each block.
     """
     B, S, A = x_t.shape
-    D, H = cfg.hidden, cfg.n_heads
-    F = cfg.mlp
-    r = x_t.reshape(B * S, A) @ np.asarray(w["w_in"], np.float64).T + w["b_in"][None, :]
+    r = in_projection(w, x_t)
     for l in range(len(w["blocks"])):
-        blk, qb, m = w["blocks"][l], qblocks[l], mod[l][t]
-        st = s_table[l, t]
-        if cfg.arch == "pi":
-            h = f16(rms_norm(r) * blk["g1"] * (1.0 + m["sc1"]) + m["sh1"])
-            qkv = f16(_lin(h, qb, "wqkv", st[0]))
-            o = np.empty((B * S, D))
-            Kp, Vp = prefix
-            for b in range(B):
-                rows = slice(b * S, (b + 1) * S)
-                kk = np.concatenate([Kp[l, b], qkv[rows, D:2 * D]], axis=0)
-                vv = np.concatenate([Vp[l, b], qkv[rows, 2 * D:]], axis=0)
-                o[rows] = attention(qkv[rows, :D], kk, vv, H)
-            o = f16(o)
-            r = r + m["gt1"] * _lin(o, qb, "wo", st[1])
-            h2 = f16(rms_norm(r) * blk["g2"] * (1.0 + m["sc2"]) + m["sh2"])
-            gu = f16(_lin(h2, qb, "wgu", st[2]))
-            a = f16(gelu_tanh(gu[:, :F]) * gu[:, F:])
-            r = r + m["gt2"] * _lin(a, qb, "wd", st[3])
-        elif cfg.arch == "gr00t":
-            h = f16(layer_norm(r) * blk["g1"] * (1.0 + m["sc1"]) + m["sh1"])
-            o = np.empty((B * S, D))
-            if l % 2 == 0:
-                q = f16(_lin(h, qb, "wq", st[0]))
-                for b in range(B):
-                    rows = slice(b * S, (b + 1) * S)
-                    o[rows] = attention(q[rows], ckv[l][b, :, :D], ckv[l][b, :, D:], H)
-            else:
-                qkv = f16(_lin(h, qb, "wqkv", st[0]))
-                for b in range(B):
-                    rows = slice(b * S, (b + 1) * S)
-                    o[rows] = attention(qkv[rows, :D], qkv[rows, D:2 * D], qkv[rows, 2 * D:], H)
-            o = f16(o)
-            r = r + _lin(o, qb, "wo", st[1])
-            h3 = f16(layer_norm(r) * blk["g3"] + blk["beta3"])
-            f = f16(gelu_tanh(_lin(h3, qb, "wff0", st[2])))
-            r = r + _lin(f, qb, "wff2", st[3])
-        else:
-            raise ValueError(cfg.arch)
+        r = block(cfg, w, qblocks, mod, s_table, r, l, t, B, S, prefix=prefix, ckv=ckv)
         if trace is not None:
             trace.append(r.copy())
     norm = rms_norm if cfg.arch == "pi" else layer_norm

@@ -134,3 +134,4 @@ def quantize_weights_host(W_u: np.ndarray, had_block: int):
 
 
 
+from .dit import DiT  # noqa: E402,F401

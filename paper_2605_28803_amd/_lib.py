@@ -29,6 +29,10 @@ class oq_dit_weights(C.Structure):
                 ("blocks", C.POINTER(oq_dit_block)), ("mod", vp), ("s_table", fp)]
 
 
+class oq_dit_intermediates(C.Structure):
+    _fields_ = [(n, vp) for n in ("h1", "qkv", "attn", "h2", "gate_up", "act", "resid")]
+
+
 # name -> (restype, argtypes)
 SIGNATURES = {
     "oq_status_string": (C.c_char_p, [i32]),
@@ -46,6 +50,7 @@ SIGNATURES = {
     "oq_dit_step": (i32, [vp, vp, i32, vp]),
     "oq_dit_denoise": (i32, [vp, vp, i32, vp]),
     "oq_dit_run_block": (i32, [vp, i32, i32, vp, vp]),
+    "oq_dit_get_intermediates": (i32, [vp, C.POINTER(oq_dit_intermediates)]),
     "oq_dit_destroy": (None, [vp]),
 }
 

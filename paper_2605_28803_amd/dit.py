@@ -1,0 +1,139 @@
+"""DiT denoising-step driver handle (binding of oq_dit_* in include/oq.h).
+
+Marshalling only: fp16 weights are uploaded, each block linear is quantized on
+the device by oq_quantize_weights (Hadamard fold + per-channel RTN), the
+ctypes structures are filled and the library runs every step in its kernels.
+"""
+from __future__ import annotations
+
+import ctypes as C
+
+import numpy as np
+import torch
+
+from . import _lib
+
+ARCH = {"pi": 0, "gr00t": 1}
+
+
+def _pow2_divisor(n: int) -> int:
+    return n & (-n)
+
+
+class DiT:
+    """Args: cfg (object with arch, hidden, mlp, n_heads, head_dim, tokens,
+    prefix, steps, action_dim), inp (dict with "w", "mod", "s_table", "kp",
+    "vp", "n_blocks", "batch": w_in [D,A], b_in [D], w_out [A,D], b_out [A],
+    g_f [D], blocks[l] with g1, g2, wqkv [3D,D], wo [D,D], wgu [2F,D], wd [D,F];
+    mod[l][t] dict of sc1, sh1, gt1, sc2, sh2, gt2 [D]; s_table [L,T,4];
+    kp / vp [L,B,P,D]).  Values are used as fp16 (weights, gains, modulation,
+    prefix) and fp32 (s_table)."""
+
+    def __init__(self, cfg, inp, device="cuda:0"):
+        from . import _check, quantize_weights  # noqa: F401
+        self.lib = _lib.load()
+        dev = torch.device(device)
+        self.device = dev
+        L, B = inp["n_blocks"], inp["batch"]
+        D, F, A = cfg.hidden, cfg.mlp, cfg.action_dim
+        T = cfg.steps
+        self.M = B * cfg.tokens
+        self.cfg_c = _lib.oq_dit_config(ARCH[cfg.arch], L, D, F, cfg.n_heads, cfg.head_dim, cfg.tokens,
+                                        cfg.prefix, B, T, A)
+        h16 = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float16)).to(dev)
+        w = inp["w"]
+        self._keep = []
+        keep = self._keep.append
+        self.w_in, self.b_in = h16(w["w_in"]), h16(w["b_in"])
+        self.w_out, self.b_out, self.g_f = h16(w["w_out"]), h16(w["b_out"]), h16(w["g_f"])
+        mod = np.empty((L, T, 6, D), dtype=np.float16)
+        names = ("sc1", "sh1", "gt1", "sc2", "sh2", "gt2")
+        for l in range(L):
+            for t in range(T):
+                for k, nm in enumerate(names):
+                    mod[l, t, k] = inp["mod"][l][t][nm]
+        self.mod = torch.from_numpy(mod).to(dev)
+        self.s_table = np.ascontiguousarray(inp["s_table"], dtype=np.float32)
+        blocks = (_lib.oq_dit_block * L)()
+        self.qweights = []
+        for l in range(L):
+            bw = w["blocks"][l]
+            qd = {}
+            for nm in ("wqkv", "wo", "wgu", "wd"):
+                W = h16(bw[nm])
+                qd[nm] = quantize_weights(W, _pow2_divisor(W.shape[1]))
+                del W
+            g1, g2 = h16(bw["g1"]), h16(bw["g2"])
+            kp, vp = h16(inp["kp"][l]), h16(inp["vp"][l])
+            for t_ in (g1, g2, kp, vp):
+                keep(t_)
+            self.qweights.append(qd)
+            qw = lambda nm: _lib.oq_qweight(qd[nm][0].data_ptr(), qd[nm][1].data_ptr())
+            blocks[l] = _lib.oq_dit_block(g1.data_ptr(), g2.data_ptr(), qw("wqkv"), qw("wo"), qw("wgu"),
+                                          qw("wd"), kp.data_ptr(), vp.data_ptr())
+        self._blocks = blocks
+        self.w_c = _lib.oq_dit_weights(self.w_in.data_ptr(), self.b_in.data_ptr(), self.w_out.data_ptr(),
+                                       self.b_out.data_ptr(), self.g_f.data_ptr(), blocks,
+                                       self.mod.data_ptr(),
+                                       self.s_table.ctypes.data_as(C.POINTER(C.c_float)))
+        nbytes = C.c_size_t(0)
+        _check(self.lib.oq_dit_workspace_bytes(C.byref(self.cfg_c), C.byref(nbytes)), "oq_dit_workspace_bytes")
+        self.workspace = torch.empty((nbytes.value,), dtype=torch.uint8, device=dev)
+        handle = C.c_void_p()
+        _check(self.lib.oq_dit_create(C.byref(self.cfg_c), C.byref(self.w_c), C.byref(handle)), "oq_dit_create")
+        self.handle = handle
+        _check(self.lib.oq_dit_set_workspace(self.handle, self.workspace.data_ptr(), nbytes.value),
+               "oq_dit_set_workspace")
+        torch.cuda.synchronize(dev)
+
+    def _stream(self, stream):
+        s = torch.cuda.current_stream(self.device) if stream is None else stream
+        return C.c_void_p(s.cuda_stream)
+
+    def step(self, x, t, stream=None):
+        """x: fp32 [B, S, A] device tensor, updated in place."""
+        from . import _check
+        _check(self.lib.oq_dit_step(self.handle, x.data_ptr(), t, self._stream(stream)), "oq_dit_step")
+        return x
+
+    def denoise(self, x, n_steps, stream=None):
+        from . import _check
+        _check(self.lib.oq_dit_denoise(self.handle, x.data_ptr(), n_steps, self._stream(stream)), "oq_dit_denoise")
+        return x
+
+    def run_block(self, l, t, resid, stream=None):
+        """resid: fp32 [B*S, D] device tensor, updated in place."""
+        from . import _check
+        _check(self.lib.oq_dit_run_block(self.handle, l, t, resid.data_ptr(), self._stream(stream)),
+               "oq_dit_run_block")
+        return resid
+
+    def intermediates(self):
+        """fp16 intermediates of the last block run, as numpy float64 arrays:
+        h1 [M,D], qkv [M,3D], attn [M,D], h2 [M,D], gate_up [M,2F], act [M,F]."""
+        from . import _check
+        it = _lib.oq_dit_intermediates()
+        _check(self.lib.oq_dit_get_intermediates(self.handle, C.byref(it)), "oq_dit_get_intermediates")
+        torch.cuda.synchronize(self.device)
+        D, F, M = self.cfg_c.hidden, self.cfg_c.mlp, self.M
+        base = self.workspace.data_ptr()
+        out = {}
+        for name, cols in (("h1", D), ("qkv", 3 * D), ("attn", D), ("h2", D), ("gate_up", 2 * F), ("act", F)):
+            off = getattr(it, name) - base
+            raw = self.workspace[off: off + M * cols * 2].cpu().numpy()
+            out[name] = raw.view(np.float16).reshape(M, cols).astype(np.float64)
+        off = it.resid - base
+        raw = self.workspace[off: off + M * D * 4].cpu().numpy()
+        out["resid"] = raw.view(np.float32).reshape(M, D).astype(np.float64)
+        return out
+
+    def close(self):
+        if getattr(self, "handle", None):
+            self.lib.oq_dit_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -102,3 +102,21 @@ def test_host_weight_preparation_rejects_bad_arguments(lib):
     assert f(None, 4, 64, 64, P16, P16) == NULL
     assert f(P16, 4, 64, 48, P16, P16) == SHAPE
     assert f(P16, 0, 64, 64, P16, P16) == SHAPE
+
+
+def test_dit_config_validation_without_gpu(lib):
+    size = C.c_size_t(0)
+    good = _lib.oq_dit_config(0, 18, 1024, 4096, 8, 128, 50, 816, 1, 10, 32)
+    assert lib.oq_dit_workspace_bytes(C.byref(good), C.byref(size)) == OK
+    assert size.value > 50 * 1024 * 4
+    bad = _lib.oq_dit_config(0, 18, 1024, 4096, 8, 64, 50, 816, 1, 10, 32)      # heads*hd != D
+    assert lib.oq_dit_workspace_bytes(C.byref(bad), C.byref(size)) == SHAPE
+    bad = _lib.oq_dit_config(0, 18, 1000, 4096, 8, 125, 50, 816, 1, 10, 32)     # D % 64
+    assert lib.oq_dit_workspace_bytes(C.byref(bad), C.byref(size)) == SHAPE
+    bad = _lib.oq_dit_config(0, 18, 1024, 4096, 8, 128, 65, 816, 1, 10, 32)     # tokens > 64
+    assert lib.oq_dit_workspace_bytes(C.byref(bad), C.byref(size)) == SHAPE
+    bad = _lib.oq_dit_config(7, 18, 1024, 4096, 8, 128, 50, 816, 1, 10, 32)     # arch
+    assert lib.oq_dit_workspace_bytes(C.byref(bad), C.byref(size)) == ARG
+    assert lib.oq_dit_workspace_bytes(None, C.byref(size)) == NULL
+    assert lib.oq_dit_step(None, P16, 0, None) == NULL
+    assert lib.oq_dit_create(C.byref(good), None, C.byref(C.c_void_p())) == NULL
