@@ -38,16 +38,33 @@ HBM_PEAK_GBS = 8000.0
 INT8_PEAK_TOPS = 5000.0  # dense int8 MFMA, TOP/s
 
 
-def _events_time(fn, iters, stream):
+def _graph_time(fn, reps=20, replays=10):
+    """Average GPU time (ms) of one fn() launch: `reps` launches are captured
+    into one HIP graph (no host launch overhead in the timed region) and the
+    graph is replayed `replays` times between HIP events on the stream the
+    kernels run on."""
     import torch
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        fn()  # warm
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        for _ in range(reps):
+            fn()
+    stream = torch.cuda.current_stream()
+    g.replay()
+    torch.cuda.synchronize()
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     start.record(stream)
-    for _ in range(iters):
-        fn()
+    for _ in range(replays):
+        g.replay()
     end.record(stream)
     end.synchronize()
-    return start.elapsed_time(end) / iters  # ms
+    return start.elapsed_time(end) / (reps * replays)
 
 
 def dit_linears(cfg):
@@ -69,7 +86,7 @@ def rq_bytes(M, K):
     return 2 * M * K + M * K // 2 + 4 * M
 
 
-def time_linears(cfg, qweights, stream, iters=200):
+def time_linears(cfg, qweights, stream):
     """Time each W4A4 linear shape of the step (rotate-quantize + GEMM) through the C ABI."""
     import torch
     import paper_2605_28803_amd as oq
@@ -86,12 +103,10 @@ def time_linears(cfg, qweights, stream, iters=200):
         # Every linear is timed with the fp16-store epilogue; inside the step the
         # o and down projections add into the fp32 residual instead.
         Y = torch.empty((M, N), dtype=torch.float16, device=dev)
-        gemm = lambda: oq.w4a4_linear(Xq, xs, Wq, ws, Y=Y, stream=stream)
-        rq = lambda: oq.rotate_quantize_act(X, K & -K, Xq=Xq, x_scale=xs, stream=stream)
-        for _ in range(10):
-            rq(); gemm()
-        t_rq = _events_time(rq, iters, stream)
-        t_g = _events_time(gemm, iters, stream)
+        gemm = lambda: oq.w4a4_linear(Xq, xs, Wq, ws, Y=Y)
+        rq = lambda: oq.rotate_quantize_act(X, K & -K, Xq=Xq, x_scale=xs)
+        t_rq = _graph_time(rq)
+        t_g = _graph_time(gemm)
         b_g = gemm_bytes(M, N, K, 2)
         b_r = rq_bytes(M, K)
         out[name] = {"M": M, "N": N, "K": K, "rq_us": round(t_rq * 1e3, 3), "gemm_us": round(t_g * 1e3, 3),

@@ -12,31 +12,40 @@
 // and the step r = x W_in^T + b_in -> blocks -> v = fp16(rms(r) g_f) W_out^T +
 // b_out -> x += dt v.
 //
-// Kernels (all on the caller's stream, no allocation, no memset):
-//   inproj_kernel      r = x W_in^T + b_in                      (fp32 residual)
-//   adarms_kernel      h = fp16(rms(r) g (1 + sc) + sh)
-//   rq / gemm          the rotated W4A4 linears (rotate_quant.hip, w4a4_gemm.hip);
-//                      o and down projections add gate * y into r in the epilogue
-//   attn_partial_kernel  softmax(q k^T / sqrt(hd)) v over one 32-key split
-//   attn_combine_kernel  merge the splits (log-sum-exp), fp16 output
-//   gelu_mul_kernel    a = fp16(gelu_tanh(gate) up)
-//   final_kernel       rms norm, out projection, Euler update of x
+// Nine launches per block, all on one stream, no allocation, no memset:
+//   norm_rq_kernel       rms norm + modulation -> fp16 row -> rotate + quantize
+//   gemm (w4a4_gemm.hip) q|k|v, fp16 out
+//   attn_partial_kernel  softmax(q k^T / sqrt(hd)) v over one 64-key split (fp16 MFMA)
+//   combine_rq_kernel    merge the splits (log-sum-exp) -> fp16 row -> rotate + quantize
+//   gemm                 o projection, r += gt1 * y in the epilogue
+//   norm_rq_kernel       second norm -> rotate + quantize
+//   gemm                 gate|up, fp16 out
+//   gelu_rq_kernel       gelu_tanh(gate) * up -> fp16 row -> rotate + quantize
+//   gemm                 down projection, r += gt2 * y in the epilogue
+// Each fused producer writes its fp16 row (the linear's input, kept for
+// per-site checks) and quantizes the same values.  A whole denoising step (or
+// several) is captured once into a HIP graph per (x, first step, count) on an
+// internal stream and replayed on the caller's stream.
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <vector>
 
 #include "common.h"
+#include "rq_device.h"
 
 namespace oq {
 namespace {
 
-constexpr int kAttnKS = 32;     // keys per attention split
+using rqd::f16r;
+using rqd::h2f;
+using rqd::f2h;
+
+constexpr int kAttnKS = 64;     // keys per attention split
 constexpr int kMaxTokens = 64;  // action tokens per sample handled by the attention kernels
 constexpr int kMaxHeadDim = 128;
+constexpr int kMaxSplits = 16;  // (prefix + tokens) <= 16 * 64 keys
 constexpr float kEps = 1e-6f;
-
-__device__ __forceinline__ float h2f(uint16_t h) { return static_cast<float>(__builtin_bit_cast(_Float16, h)); }
-__device__ __forceinline__ uint16_t f2h(float f) { return __builtin_bit_cast(uint16_t, static_cast<_Float16>(f)); }
 
 __device__ float block_sum(float v, float* red) {
   // 256 threads.
@@ -49,39 +58,95 @@ __device__ float block_sum(float v, float* red) {
   return s;
 }
 
-// r[m][n] = sum_a x[m][a] w_in[n][a] + b_in[n]
+__device__ __forceinline__ void load8_f16(const uint16_t* p, float (&o)[8]) {
+  const uint4 raw = *reinterpret_cast<const uint4*>(p);
+  const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    o[2 * q] = h2f(w[q] & 0xFFFFu);
+    o[2 * q + 1] = h2f(w[q] >> 16);
+  }
+}
+
+__device__ __forceinline__ void store8_f16(uint16_t* p, const float (&v)[8]) {
+  uint4 raw;
+  raw.x = f2h(v[0]) | (static_cast<uint32_t>(f2h(v[1])) << 16);
+  raw.y = f2h(v[2]) | (static_cast<uint32_t>(f2h(v[3])) << 16);
+  raw.z = f2h(v[4]) | (static_cast<uint32_t>(f2h(v[5])) << 16);
+  raw.w = f2h(v[6]) | (static_cast<uint32_t>(f2h(v[7])) << 16);
+  *reinterpret_cast<uint4*>(p) = raw;
+}
+
+struct RQOut {
+  uint8_t* xq;
+  float* xs;
+  int logT, logb;
+  float s_t, s_over_sqrtb;
+};
+
+// r = x W_in^T + b_in
 __global__ __launch_bounds__(256) void inproj_kernel(const float* __restrict__ x, const uint16_t* __restrict__ w_in,
                                                      const uint16_t* __restrict__ b_in, float* __restrict__ r, int A,
                                                      int D) {
-  extern __shared__ float xs[];
+  extern __shared__ float xsh[];
   const int m = blockIdx.x;
-  for (int a = threadIdx.x; a < A; a += blockDim.x) xs[a] = x[static_cast<int64_t>(m) * A + a];
+  for (int a = threadIdx.x; a < A; a += blockDim.x) xsh[a] = x[static_cast<int64_t>(m) * A + a];
   __syncthreads();
   for (int n = threadIdx.x; n < D; n += blockDim.x) {
     const uint16_t* wr = w_in + static_cast<int64_t>(n) * A;
     float acc = 0.0f;
-    for (int a = 0; a < A; ++a) acc = fmaf(xs[a], h2f(wr[a]), acc);
+    for (int a = 0; a < A; ++a) acc = fmaf(xsh[a], h2f(wr[a]), acc);
     r[static_cast<int64_t>(m) * D + n] = acc + h2f(b_in[n]);
   }
 }
 
-// h = fp16(rms(r) * g * (1 + sc) + sh); sc / sh may be null (plain gain).
-__global__ __launch_bounds__(256) void adarms_kernel(const float* __restrict__ r, const uint16_t* __restrict__ g,
-                                                     const uint16_t* __restrict__ sc, const uint16_t* __restrict__ sh,
-                                                     uint16_t* __restrict__ h, int D) {
+// h = fp16(rms(r) g (1 + sc) + sh), then rotate + quantize h.
+template <int C>
+__global__ __launch_bounds__(256) void norm_rq_kernel(const float* __restrict__ r, const uint16_t* __restrict__ g,
+                                                      const uint16_t* __restrict__ sc,
+                                                      const uint16_t* __restrict__ sh, uint16_t* __restrict__ h,
+                                                      int64_t M, int D, RQOut o) {
+  extern __shared__ float lds[];
   __shared__ float red[4];
-  const int64_t m = blockIdx.x;
-  const float* rr = r + m * D;
+  __shared__ float red2[4];
+  const rqd::RowMap m = rqd::row_map(o.logT, M);
+  float v[C][8];
   float ss = 0.0f;
-  for (int d = threadIdx.x; d < D; d += blockDim.x) ss = fmaf(rr[d], rr[d], ss);
-  ss = block_sum(ss, red);
-  const float inv = 1.0f / sqrtf(ss / static_cast<float>(D) + kEps);
-  for (int d = threadIdx.x; d < D; d += blockDim.x) {
-    float y = rr[d] * inv * h2f(g[d]);
-    if (sc) y = fmaf(y, h2f(sc[d]), y);
-    if (sh) y += h2f(sh[d]);
-    h[m * D + d] = f2h(y);
+  const float* rr = r + (m.valid ? m.row : 0) * D;
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const int k = rqd::chan(m, c, 0);
+    float4 p0 = make_float4(0, 0, 0, 0), p1 = p0;
+    if (m.valid) {
+      p0 = *reinterpret_cast<const float4*>(rr + k);
+      p1 = *reinterpret_cast<const float4*>(rr + k + 4);
+    }
+    v[c][0] = p0.x; v[c][1] = p0.y; v[c][2] = p0.z; v[c][3] = p0.w;
+    v[c][4] = p1.x; v[c][5] = p1.y; v[c][6] = p1.z; v[c][7] = p1.w;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) ss = fmaf(v[c][j], v[c][j], ss);
   }
+  float gg[C][8], s1[C][8], s2[C][8];
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const int k = rqd::chan(m, c, 0);
+    load8_f16(g + k, gg[c]);
+    load8_f16(sc + k, s1[c]);
+    load8_f16(sh + k, s2[c]);
+  }
+  ss = rqd::row_reduce<false>(ss, m, red2);
+  const float inv = 1.0f / sqrtf(ss / static_cast<float>(D) + kEps);
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const int k = rqd::chan(m, c, 0);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float y = v[c][j] * inv * gg[c][j];
+      v[c][j] = f16r(fmaf(y, s1[c][j], y) + s2[c][j]);
+    }
+    if (m.valid) store8_f16(h + m.row * D + k, v[c]);
+  }
+  rqd::rq_core<C>(v, m, D, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr);
 }
 
 __device__ __forceinline__ float gelu_tanh(float x) {
@@ -90,123 +155,246 @@ __device__ __forceinline__ float gelu_tanh(float x) {
   return 0.5f * x * (1.0f + tanhf(k0 * fmaf(k1 * x * x, x, x)));
 }
 
-// a[m][f] = fp16(gelu_tanh(gu[m][f]) * gu[m][F + f])
-__global__ __launch_bounds__(256) void gelu_mul_kernel(const uint16_t* __restrict__ gu, uint16_t* __restrict__ out,
-                                                       int64_t M, int F) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i >= M * F) return;
-  const int64_t m = i / F, f = i % F;
-  const float gate = h2f(gu[m * 2 * F + f]);
-  const float up = h2f(gu[m * 2 * F + F + f]);
-  out[i] = f2h(gelu_tanh(gate) * up);
+// a = fp16(gelu_tanh(gate) up) from gu = [gate | up] (fp16 [M][2F]), then
+// rotate + quantize a.
+template <int C>
+__global__ __launch_bounds__(256) void gelu_rq_kernel(const uint16_t* __restrict__ gu, uint16_t* __restrict__ act,
+                                                      int64_t M, int F, RQOut o) {
+  extern __shared__ float lds[];
+  __shared__ float red[4];
+  const rqd::RowMap m = rqd::row_map(o.logT, M);
+  float v[C][8];
+  const uint16_t* gr = gu + (m.valid ? m.row : 0) * 2 * F;
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const int k = rqd::chan(m, c, 0);
+    float ga[8], up[8];
+    if (m.valid) {
+      load8_f16(gr + k, ga);
+      load8_f16(gr + F + k, up);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) ga[j] = up[j] = 0.0f;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[c][j] = f16r(gelu_tanh(ga[j]) * up[j]);
+    if (m.valid) store8_f16(act + m.row * F + k, v[c]);
+  }
+  rqd::rq_core<C>(v, m, F, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr);
 }
 
 struct AttnArgs {
   const uint16_t* q; int64_t q_ld;                      // [B*S][..], head h at column h*hd
   const uint16_t* k_pre; const uint16_t* v_pre; int P;  // [B][P][D] (P may be 0)
   const uint16_t* k_own; const uint16_t* v_own; int64_t own_ld; int own_keys;  // [B*S][..]
-  float* part_o; float* part_ml;                        // workspace
+  float* part_o; float* part_ml;                        // [B*H][nsplit][S][hd], [B*H][nsplit][S][2]
   uint16_t* out; int64_t out_ld;
   int S, H, hd, D, nsplit;
   float scale;
 };
 
-// One (sample b, head h, 32-key split): partial max, sum and weighted values.
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+// One (sample b, head h, 64-key split) on the fp16 matrix cores
+// (v_mfma_f32_16x16x32_f16).  Wave w owns query rows 16w .. 16w+15:
+//   S = Q K^T (16 x 64, fp32), scaled; split maximum m and sum l per row;
+//   P = exp(S - m) (fp16, staged in LDS as the next A operand);
+//   O = P V (16 x hd, fp32) with V^T staged in LDS.
+// O, m and l go to the workspace; combine_rq_kernel merges the splits.
+// MFMA operand layout used (the same k order for both operands): lane l holds
+// row / column l % 16 and the 8 consecutive k values 8 * (l / 16) .. + 7 of a
+// 32-wide k step; the 16 x 16 fp32 result has row 4 * (l / 16) + e, column
+// l % 16 in element e.
 __global__ __launch_bounds__(256) void attn_partial_kernel(AttnArgs a) {
-  __shared__ float sK[kAttnKS][kMaxHeadDim + 1];
-  __shared__ float sV[kAttnKS][kMaxHeadDim];
-  __shared__ uint16_t sQ[kMaxTokens][kMaxHeadDim];
-  __shared__ float sP[kMaxTokens][kAttnKS + 1];
+  constexpr int KS = kAttnKS;            // 64 keys
+  constexpr int PAD = KS + 8;            // padded row (halves): 16-byte reads of 16 rows hit distinct banks
+  __shared__ __attribute__((aligned(16))) uint16_t sVt[kMaxHeadDim][PAD];  // V^T [dim][key]
+  __shared__ __attribute__((aligned(16))) uint16_t sP[4][16][PAD];         // per-wave P [row][key]
 
   const int bh = blockIdx.x, split = blockIdx.y;
   const int b = bh / a.H, h = bh % a.H;
   const int tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6;
   const int n_keys = a.P + a.own_keys;
-  const int k0 = split * kAttnKS;
-  const int nk = min(kAttnKS, n_keys - k0);
+  const int k0 = split * KS;
+  const int nk = min(KS, n_keys - k0);
+  const int hd = a.hd;
 
-  for (int i = tid; i < a.S * a.hd; i += blockDim.x) {
-    const int q = i / a.hd, d = i % a.hd;
-    sQ[q][d] = a.q[(static_cast<int64_t>(b) * a.S + q) * a.q_ld + h * a.hd + d];
-  }
-  for (int i = tid; i < kAttnKS * a.hd; i += blockDim.x) {
-    const int j = i / a.hd, d = i % a.hd;
-    float kv = 0.0f, vv = 0.0f;
-    if (j < nk) {
-      const int key = k0 + j;
-      if (key < a.P) {
-        const int64_t off = (static_cast<int64_t>(b) * a.P + key) * a.D + h * a.hd + d;
-        kv = h2f(a.k_pre[off]);
-        vv = h2f(a.v_pre[off]);
-      } else {
-        const int64_t off = (static_cast<int64_t>(b) * a.own_keys + (key - a.P)) * a.own_ld + h * a.hd + d;
-        kv = h2f(a.k_own[off]);
-        vv = h2f(a.v_own[off]);
-      }
+  auto key_ptr = [&](int j, const uint16_t* pre, const uint16_t* own) -> const uint16_t* {
+    const int key = k0 + j;
+    if (key < a.P) return pre + (static_cast<int64_t>(b) * a.P + key) * a.D + h * hd;
+    return own + (static_cast<int64_t>(b) * a.own_keys + (key - a.P)) * a.own_ld + h * hd;
+  };
+
+  // Stage V^T: thread (key j = tid % 64, dim group) loads 8 dims of one key.
+  for (int d8 = (tid >> 6) * 8; d8 < hd; d8 += 32) {
+    const int j = tid & 63;
+    uint4 raw = make_uint4(0, 0, 0, 0);
+    if (j < nk) raw = *reinterpret_cast<const uint4*>(key_ptr(j, a.v_pre, a.v_own) + d8);
+    const uint32_t wv[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      sVt[d8 + 2 * q][j] = static_cast<uint16_t>(wv[q] & 0xFFFFu);
+      sVt[d8 + 2 * q + 1][j] = static_cast<uint16_t>(wv[q] >> 16);
     }
-    sK[j][d] = kv;
-    sV[j][d] = vv;
+  }
+
+  // S = Q K^T for this wave's 16 rows.
+  const int qrow = 16 * w + (lane & 15);
+  const bool qok = qrow < a.S;
+  const int kq = 8 * (lane >> 4);
+  const int nkk = hd / 32;  // 32-wide k steps over the head dimension (hd % 32 == 0, <= 4)
+  constexpr int KKMAX = kMaxHeadDim / 32;
+  // Issue every Q and K load of the wave before the first MFMA.
+  v8h qa[KKMAX], kb[KKMAX][KS / 16];
+#pragma unroll
+  for (int kk = 0; kk < KKMAX; ++kk) {
+    qa[kk] = v8h{};
+    if (kk < nkk && qok)
+      qa[kk] = *reinterpret_cast<const v8h*>(a.q + (static_cast<int64_t>(b) * a.S + qrow) * a.q_ld + h * hd +
+                                             kk * 32 + kq);
+#pragma unroll
+    for (int nb = 0; nb < KS / 16; ++nb) {
+      const int j = nb * 16 + (lane & 15);
+      kb[kk][nb] = v8h{};
+      if (kk < nkk && j < nk) kb[kk][nb] = *reinterpret_cast<const v8h*>(key_ptr(j, a.k_pre, a.k_own) + kk * 32 + kq);
+    }
+  }
+  v4f sc[KS / 16];
+#pragma unroll
+  for (int nb = 0; nb < KS / 16; ++nb) {
+    sc[nb] = v4f{0, 0, 0, 0};
+#pragma unroll
+    for (int kk = 0; kk < KKMAX; ++kk)
+      if (kk < nkk) sc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(qa[kk], kb[kk][nb], sc[nb], 0, 0, 0);
+  }
+
+  // Softmax statistics per row (row 4*(lane/16) + e, keys across the 16 lanes
+  // of the group and the KS/16 blocks).
+  float mx[4], l[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    float m_ = -INFINITY;
+#pragma unroll
+    for (int nb = 0; nb < KS / 16; ++nb) {
+      const int j = nb * 16 + (lane & 15);
+      const float v = j < nk ? sc[nb][e] * a.scale : -INFINITY;
+      sc[nb][e] = v;
+      m_ = fmaxf(m_, v);
+    }
+    m_ = fmaxf(m_, rqd::lane_xor<1>(m_));
+    m_ = fmaxf(m_, rqd::lane_xor<2>(m_));
+    m_ = fmaxf(m_, rqd::lane_xor<4>(m_));
+    m_ = fmaxf(m_, rqd::lane_xor<8>(m_));
+    float s_ = 0.0f;
+#pragma unroll
+    for (int nb = 0; nb < KS / 16; ++nb) {
+      const float p = __expf(sc[nb][e] - m_);
+      s_ += p;
+      sP[w][4 * (lane >> 4) + e][nb * 16 + (lane & 15)] = f2h(p);
+    }
+    s_ += rqd::lane_xor<1>(s_);
+    s_ += rqd::lane_xor<2>(s_);
+    s_ += rqd::lane_xor<4>(s_);
+    s_ += rqd::lane_xor<8>(s_);
+    mx[e] = m_;
+    l[e] = s_;
   }
   __syncthreads();
 
-  // Scores.
-  {
-    const int j = tid & (kAttnKS - 1);
-    for (int q = tid / kAttnKS; q < a.S; q += blockDim.x / kAttnKS) {
-      float s = -INFINITY;
-      if (j < nk) {
-        float acc = 0.0f;
-        for (int d = 0; d < a.hd; ++d) acc = fmaf(h2f(sQ[q][d]), sK[j][d], acc);
-        s = acc * a.scale;
-      }
-      sP[q][j] = s;
+  // O = P V, 16 x hd per wave.
+  float* po = a.part_o + (static_cast<int64_t>(bh) * a.nsplit + split) * a.S * hd;
+  for (int nb = 0; nb < hd / 16; ++nb) {
+    v4f o = v4f{0, 0, 0, 0};
+#pragma unroll
+    for (int ks = 0; ks < KS / 32; ++ks) {
+      const v8h pa = *reinterpret_cast<const v8h*>(&sP[w][lane & 15][ks * 32 + kq]);
+      const v8h vb = *reinterpret_cast<const v8h*>(&sVt[nb * 16 + (lane & 15)][ks * 32 + kq]);
+      o = __builtin_amdgcn_mfma_f32_16x16x32_f16(pa, vb, o, 0, 0, 0);
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int row = 16 * w + 4 * (lane >> 4) + e;
+      if (row < a.S) po[static_cast<int64_t>(row) * hd + nb * 16 + (lane & 15)] = o[e];
     }
   }
-  __syncthreads();
-
-  // Row max and sum of this split; probabilities relative to the split max.
   float* ml = a.part_ml + (static_cast<int64_t>(bh) * a.nsplit + split) * a.S * 2;
-  for (int q = tid; q < a.S; q += blockDim.x) {
-    float mx = -INFINITY;
-    for (int j = 0; j < nk; ++j) mx = fmaxf(mx, sP[q][j]);
-    float l = 0.0f;
-    for (int j = 0; j < kAttnKS; ++j) {
-      const float p = j < nk ? __expf(sP[q][j] - mx) : 0.0f;
-      sP[q][j] = p;
-      l += p;
+  if ((lane & 15) == 0) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int row = 16 * w + 4 * (lane >> 4) + e;
+      if (row < a.S) {
+        ml[2 * row] = mx[e];
+        ml[2 * row + 1] = l[e];
+      }
     }
-    ml[2 * q] = mx;
-    ml[2 * q + 1] = l;
-  }
-  __syncthreads();
-
-  float* po = a.part_o + (static_cast<int64_t>(bh) * a.nsplit + split) * a.S * a.hd;
-  for (int i = tid; i < a.S * a.hd; i += blockDim.x) {
-    const int q = i / a.hd, d = i % a.hd;
-    float acc = 0.0f;
-    for (int j = 0; j < kAttnKS; ++j) acc = fmaf(sP[q][j], sV[j][d], acc);
-    po[i] = acc;
   }
 }
 
-// Merge the splits of one (b, h): out = sum_s e^{m_s - M} o_s / sum_s e^{m_s - M} l_s.
-__global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
-  const int bh = blockIdx.x;
-  const int b = bh / a.H, h = bh % a.H;
-  const float* ml = a.part_ml + static_cast<int64_t>(bh) * a.nsplit * a.S * 2;
-  const float* po = a.part_o + static_cast<int64_t>(bh) * a.nsplit * a.S * a.hd;
-  for (int i = threadIdx.x; i < a.S * a.hd; i += blockDim.x) {
-    const int q = i / a.hd, d = i % a.hd;
-    float M = -INFINITY;
-    for (int s = 0; s < a.nsplit; ++s) M = fmaxf(M, ml[(s * a.S + q) * 2]);
-    float num = 0.0f, den = 0.0f;
-    for (int s = 0; s < a.nsplit; ++s) {
-      const float w = __expf(ml[(s * a.S + q) * 2] - M);
-      den = fmaf(w, ml[(s * a.S + q) * 2 + 1], den);
-      num = fmaf(w, po[(static_cast<int64_t>(s) * a.S + q) * a.hd + d], num);
+// Token row (b, s): out = sum_s e^{m_s - M} o_s / sum_s e^{m_s - M} l_s per
+// head, rounded to fp16, then rotate + quantize the row.
+template <int C>
+__global__ __launch_bounds__(256) void combine_rq_kernel(AttnArgs a, int64_t M, RQOut o) {
+  extern __shared__ float lds[];
+  __shared__ float red[4];
+  const rqd::RowMap m = rqd::row_map(o.logT, M);
+  float v[C][8];
+  const int64_t row = m.valid ? m.row : 0;
+  const int b = static_cast<int>(row / a.S), q = static_cast<int>(row % a.S);
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const int k = rqd::chan(m, c, 0);
+    const int h = k / a.hd, d = k - h * a.hd;
+    const int64_t bh = static_cast<int64_t>(b) * a.H + h;
+    const float* ml = a.part_ml + bh * a.nsplit * a.S * 2 + 2 * q;
+    const float* po = a.part_o + bh * a.nsplit * a.S * a.hd + static_cast<int64_t>(q) * a.hd + d;
+    // All split statistics first (independent loads), then the weighted values
+    // in groups of 8 splits.
+    float mv[kMaxSplits], lv[kMaxSplits];
+#pragma unroll
+    for (int s = 0; s < kMaxSplits; ++s) {
+      mv[s] = -INFINITY;
+      lv[s] = 0.0f;
+      if (s < a.nsplit) {
+        const float2 t = *reinterpret_cast<const float2*>(ml + s * a.S * 2);
+        mv[s] = t.x;
+        lv[s] = t.y;
+      }
     }
-    a.out[(static_cast<int64_t>(b) * a.S + q) * a.out_ld + h * a.hd + d] = f2h(num / den);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int s = 0; s < kMaxSplits; ++s) mx = fmaxf(mx, mv[s]);
+    float den = 0.0f;
+    float num[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+    for (int s0 = 0; s0 < kMaxSplits; s0 += 8) {
+      float4 p0[8], p1[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        p0[u] = p1[u] = make_float4(0, 0, 0, 0);
+        if (s0 + u < a.nsplit) {
+          const float* src = po + static_cast<int64_t>(s0 + u) * a.S * a.hd;
+          p0[u] = *reinterpret_cast<const float4*>(src);
+          p1[u] = *reinterpret_cast<const float4*>(src + 4);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float w = s0 + u < a.nsplit ? __expf(mv[s0 + u] - mx) : 0.0f;
+        den = fmaf(w, lv[s0 + u], den);
+        num[0] = fmaf(w, p0[u].x, num[0]); num[1] = fmaf(w, p0[u].y, num[1]);
+        num[2] = fmaf(w, p0[u].z, num[2]); num[3] = fmaf(w, p0[u].w, num[3]);
+        num[4] = fmaf(w, p1[u].x, num[4]); num[5] = fmaf(w, p1[u].y, num[5]);
+        num[6] = fmaf(w, p1[u].z, num[6]); num[7] = fmaf(w, p1[u].w, num[7]);
+      }
+    }
+    const float inv = 1.0f / den;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[c][j] = m.valid ? f16r(num[j] * inv) : 0.0f;
+    if (m.valid) store8_f16(a.out + m.row * a.out_ld + k, v[c]);
   }
+  rqd::rq_core<C>(v, m, a.D, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr);
 }
 
 // x[m][:] += dt * (fp16(rms(r[m]) g_f) W_out^T + b_out)
@@ -222,11 +410,11 @@ __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ r,
   for (int d = threadIdx.x; d < D; d += blockDim.x) ss = fmaf(rr[d], rr[d], ss);
   ss = block_sum(ss, red);
   const float inv = 1.0f / sqrtf(ss / static_cast<float>(D) + kEps);
-  for (int d = threadIdx.x; d < D; d += blockDim.x) sh[d] = h2f(f2h(rr[d] * inv * h2f(g_f[d])));
+  for (int d = threadIdx.x; d < D; d += blockDim.x) sh[d] = f16r(rr[d] * inv * h2f(g_f[d]));
   __syncthreads();
   float* part = sh + D;
-  // Thread t: output a = t % A over the d-slice t / A (A divides 256 is not
-  // required: threads beyond the last full slice idle).
+  // Thread t: output t % A over the d-slice t / A; threads beyond the last
+  // full slice idle.
   const int slices = blockDim.x / A;
   const int a_idx = threadIdx.x % A, sl = threadIdx.x / A;
   float acc = 0.0f;
@@ -274,18 +462,35 @@ Layout layout_for(const oq_dit_config& c) {
   return L;
 }
 
+// Thread split of a fused row kernel: as many threads per row as possible (up
+// to 256), few channels each, so that the small-M rows spread widely.
+bool fused_plan(int64_t K, RQPlan* p) {
+  const int64_t nvec = K / 8;
+  static const int kChunks[] = {1, 2, 3, 4, 6, 8};
+  for (int c : kChunks) {
+    if (nvec % c) continue;
+    const int64_t T = nvec / c;
+    if (!is_pow2(T) || T > 256) continue;
+    p->chunks = c;
+    p->logT = ilog2(T);
+    return true;
+  }
+  return false;
+}
+
 int validate_config(const oq_dit_config* c) {
   if (!c) return OQ_ERR_NULL;
   if (c->arch != OQ_DIT_PI) return OQ_ERR_ARG;
   if (c->n_blocks < 1 || c->steps < 1 || c->batch < 1 || c->tokens < 1 || c->prefix < 0) return OQ_ERR_SHAPE;
   if (c->hidden < 64 || c->hidden % 64 || c->mlp < 64 || c->mlp % 64) return OQ_ERR_SHAPE;
   if (c->hidden > 16384 || c->mlp > 16384) return OQ_ERR_SHAPE;
-  if (c->n_heads < 1 || c->head_dim < 8 || c->head_dim > kMaxHeadDim || c->head_dim % 8 ||
+  if (c->n_heads < 1 || c->head_dim < 32 || c->head_dim > kMaxHeadDim || c->head_dim % 32 ||
       c->n_heads * c->head_dim != c->hidden)
     return OQ_ERR_SHAPE;
   if (c->tokens > kMaxTokens || c->action_dim < 1 || c->action_dim > 256) return OQ_ERR_SHAPE;
+  if (c->prefix + c->tokens > kMaxSplits * kAttnKS) return OQ_ERR_SHAPE;
   RQPlan p;
-  if (!rq_plan(c->hidden, &p) || !rq_plan(c->mlp, &p)) return OQ_ERR_SHAPE;
+  if (!fused_plan(c->hidden, &p) || !fused_plan(c->mlp, &p)) return OQ_ERR_SHAPE;
   return OQ_OK;
 }
 
@@ -293,6 +498,12 @@ int pow2_divisor(int n) { return n & (-n); }
 
 }  // namespace
 }  // namespace oq
+
+struct oq_dit_graph {
+  float* x;
+  int t0, n;
+  hipGraphExec_t exec;
+};
 
 struct oq_dit {
   oq_dit_config cfg;
@@ -302,6 +513,9 @@ struct oq_dit {
   oq::Layout lay;
   uint8_t* ws = nullptr;
   size_t ws_bytes = 0;
+  hipStream_t cap = nullptr;  // capture stream (graphs are replayed on the caller's stream)
+  std::vector<oq_dit_graph> graphs;
+  bool use_graphs = true;
 };
 
 namespace oq {
@@ -315,14 +529,62 @@ const uint16_t* mod_ptr(oq_dit* h, int l, int t, int k) {
   return static_cast<const uint16_t*>(h->w.mod) + ((static_cast<int64_t>(l) * h->cfg.steps + t) * 6 + k) * D;
 }
 
-int linear(oq_dit* h, const uint16_t* x, int64_t K, float s, const oq_qweight& wt, int64_t N, Epilogue epi,
-           void* out, int64_t ldc, const uint16_t* gate, hipStream_t st) {
+RQOut rq_out(oq_dit* h, int64_t K, float s, RQPlan* p) {
+  fused_plan(K, p);
+  RQOut o;
+  o.xq = at<uint8_t>(h, h->lay.xq);
+  o.xs = at<float>(h, h->lay.xs);
+  o.logT = p->logT;
+  const int b = pow2_divisor(static_cast<int>(K));
+  o.logb = ilog2(b);
+  o.s_t = s;
+  o.s_over_sqrtb = static_cast<float>(static_cast<double>(s) / std::sqrt(static_cast<double>(b)));
+  return o;
+}
+
+struct FusedLaunch {
+  dim3 grid, block;
+  size_t lds;
+};
+
+FusedLaunch fused_launch(int64_t M, int64_t K, const RQPlan& p) {
+  const int T = 1 << p.logT;
+  const int threads = T >= 256 ? T : 256;
+  const int rows_per_wg = threads / T;
+  FusedLaunch f;
+  f.grid = dim3(static_cast<unsigned>((M + rows_per_wg - 1) / rows_per_wg));
+  f.block = dim3(threads);
+  f.lds = p.logT > 6 ? static_cast<size_t>(rows_per_wg) * K * sizeof(float) : 0;
+  return f;
+}
+
+#define OQ_FUSED_SWITCH(CH, KERNEL, ...)                                                        \
+  switch (CH) {                                                                                 \
+    case 1: hipLaunchKernelGGL(KERNEL<1>, fl.grid, fl.block, fl.lds, st, __VA_ARGS__); break;    \
+    case 2: hipLaunchKernelGGL(KERNEL<2>, fl.grid, fl.block, fl.lds, st, __VA_ARGS__); break;    \
+    case 3: hipLaunchKernelGGL(KERNEL<3>, fl.grid, fl.block, fl.lds, st, __VA_ARGS__); break;    \
+    case 4: hipLaunchKernelGGL(KERNEL<4>, fl.grid, fl.block, fl.lds, st, __VA_ARGS__); break;    \
+    case 6: hipLaunchKernelGGL(KERNEL<6>, fl.grid, fl.block, fl.lds, st, __VA_ARGS__); break;    \
+    case 8: hipLaunchKernelGGL(KERNEL<8>, fl.grid, fl.block, fl.lds, st, __VA_ARGS__); break;    \
+    default: return OQ_ERR_SHAPE;                                                               \
+  }
+
+int norm_rq(oq_dit* h, const float* r, const void* g, const uint16_t* sc, const uint16_t* sh, uint16_t* out,
+            float s, hipStream_t st) {
   const int64_t M = static_cast<int64_t>(h->cfg.batch) * h->cfg.tokens;
-  uint8_t* xq = at<uint8_t>(h, h->lay.xq);
-  float* xs = at<float>(h, h->lay.xs);
-  int e = rq_launch(x, M, K, K, pow2_divisor(static_cast<int>(K)), s, xq, xs, nullptr, st);
-  if (e != OQ_OK) return e;
-  GemmArgs a{xq, wt.wq, xs, wt.w_scale, nullptr, out, gate, M, N, K, ldc};
+  const int64_t D = h->cfg.hidden;
+  RQPlan p;
+  const RQOut o = rq_out(h, D, s, &p);
+  const FusedLaunch fl = fused_launch(M, D, p);
+  OQ_FUSED_SWITCH(p.chunks, norm_rq_kernel, r, static_cast<const uint16_t*>(g), sc, sh, out, M,
+                  static_cast<int>(D), o)
+  return launch_status();
+}
+
+int gemm(oq_dit* h, const oq_qweight& wt, int64_t K, int64_t N, Epilogue epi, void* out, int64_t ldc,
+         const uint16_t* gate, hipStream_t st) {
+  const int64_t M = static_cast<int64_t>(h->cfg.batch) * h->cfg.tokens;
+  GemmArgs a{at<uint8_t>(h, h->lay.xq), wt.wq, at<float>(h, h->lay.xs), wt.w_scale, nullptr, out, gate, M, N, K, ldc};
   return gemm_launch(a, epi, st);
 }
 
@@ -340,11 +602,8 @@ int run_block(oq_dit* h, int l, int t, float* r, hipStream_t st) {
   uint16_t* act = at<uint16_t>(h, h->lay.act);
   int e;
 
-  hipLaunchKernelGGL(adarms_kernel, dim3(static_cast<unsigned>(M)), dim3(256), 0, st, r,
-                     static_cast<const uint16_t*>(bw.g1), mod_ptr(h, l, t, 0), mod_ptr(h, l, t, 1), h1,
-                     static_cast<int>(D));
-  if ((e = launch_status()) != OQ_OK) return e;
-  if ((e = linear(h, h1, D, s[0], bw.qkv, 3 * D, EPI_F16, qkv, 3 * D, nullptr, st)) != OQ_OK) return e;
+  if ((e = norm_rq(h, r, bw.g1, mod_ptr(h, l, t, 0), mod_ptr(h, l, t, 1), h1, s[0], st)) != OQ_OK) return e;
+  if ((e = gemm(h, bw.qkv, D, 3 * D, EPI_F16, qkv, 3 * D, nullptr, st)) != OQ_OK) return e;
 
   AttnArgs a;
   a.q = qkv; a.q_ld = 3 * D;
@@ -360,22 +619,25 @@ int run_block(oq_dit* h, int l, int t, float* r, hipStream_t st) {
   a.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(c.head_dim)));
   hipLaunchKernelGGL(attn_partial_kernel, dim3(c.batch * c.n_heads, a.nsplit), dim3(256), 0, st, a);
   if ((e = launch_status()) != OQ_OK) return e;
-  hipLaunchKernelGGL(attn_combine_kernel, dim3(c.batch * c.n_heads), dim3(256), 0, st, a);
-  if ((e = launch_status()) != OQ_OK) return e;
+  {
+    RQPlan p;
+    const RQOut ro = rq_out(h, D, s[1], &p);
+    const FusedLaunch fl = fused_launch(M, D, p);
+    OQ_FUSED_SWITCH(p.chunks, combine_rq_kernel, a, M, ro)
+    if ((e = launch_status()) != OQ_OK) return e;
+  }
+  if ((e = gemm(h, bw.o, D, D, EPI_RESID_F32, r, D, mod_ptr(h, l, t, 2), st)) != OQ_OK) return e;
 
-  if ((e = linear(h, o, D, s[1], bw.o, D, EPI_RESID_F32, r, D, mod_ptr(h, l, t, 2), st)) != OQ_OK) return e;
-
-  hipLaunchKernelGGL(adarms_kernel, dim3(static_cast<unsigned>(M)), dim3(256), 0, st, r,
-                     static_cast<const uint16_t*>(bw.g2), mod_ptr(h, l, t, 3), mod_ptr(h, l, t, 4), h2,
-                     static_cast<int>(D));
-  if ((e = launch_status()) != OQ_OK) return e;
-  if ((e = linear(h, h2, D, s[2], bw.gate_up, 2 * F, EPI_F16, gu, 2 * F, nullptr, st)) != OQ_OK) return e;
-
-  const int64_t n = M * F;
-  hipLaunchKernelGGL(gelu_mul_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, st, gu, act, M,
-                     static_cast<int>(F));
-  if ((e = launch_status()) != OQ_OK) return e;
-  return linear(h, act, F, s[3], bw.down, D, EPI_RESID_F32, r, D, mod_ptr(h, l, t, 5), st);
+  if ((e = norm_rq(h, r, bw.g2, mod_ptr(h, l, t, 3), mod_ptr(h, l, t, 4), h2, s[2], st)) != OQ_OK) return e;
+  if ((e = gemm(h, bw.gate_up, D, 2 * F, EPI_F16, gu, 2 * F, nullptr, st)) != OQ_OK) return e;
+  {
+    RQPlan p;
+    const RQOut ro = rq_out(h, F, s[3], &p);
+    const FusedLaunch fl = fused_launch(M, F, p);
+    OQ_FUSED_SWITCH(p.chunks, gelu_rq_kernel, gu, act, M, static_cast<int>(F), ro)
+    if ((e = launch_status()) != OQ_OK) return e;
+  }
+  return gemm(h, bw.down, F, D, EPI_RESID_F32, r, D, mod_ptr(h, l, t, 5), st);
 }
 
 int run_step(oq_dit* h, float* x, int t, hipStream_t st) {
@@ -394,6 +656,41 @@ int run_step(oq_dit* h, float* x, int t, hipStream_t st) {
                      r, static_cast<const uint16_t*>(h->w.g_f), static_cast<const uint16_t*>(h->w.w_out),
                      static_cast<const uint16_t*>(h->w.b_out), x, c.hidden, c.action_dim, dt);
   return launch_status();
+}
+
+void drop_graphs(oq_dit* h) {
+  for (auto& g : h->graphs) hipGraphExecDestroy(g.exec);
+  h->graphs.clear();
+}
+
+// Steps t0 .. t0+n-1 on x: replay the cached graph for (x, t0, n), capturing it
+// on the internal stream the first time.
+int run_steps(oq_dit* h, float* x, int t0, int n, hipStream_t st) {
+  if (!h->use_graphs) {
+    for (int t = t0; t < t0 + n; ++t) {
+      int e = run_step(h, x, t, st);
+      if (e != OQ_OK) return e;
+    }
+    return OQ_OK;
+  }
+  for (auto& g : h->graphs)
+    if (g.x == x && g.t0 == t0 && g.n == n)
+      return hipGraphLaunch(g.exec, st) == hipSuccess ? OQ_OK : OQ_ERR_HIP;
+  if (hipStreamBeginCapture(h->cap, hipStreamCaptureModeThreadLocal) != hipSuccess) return OQ_ERR_HIP;
+  int e = OQ_OK;
+  for (int t = t0; t < t0 + n && e == OQ_OK; ++t) e = run_step(h, x, t, h->cap);
+  hipGraph_t graph = nullptr;
+  const hipError_t ce = hipStreamEndCapture(h->cap, &graph);
+  if (e != OQ_OK || ce != hipSuccess || !graph) {
+    if (graph) hipGraphDestroy(graph);
+    return e != OQ_OK ? e : OQ_ERR_HIP;
+  }
+  hipGraphExec_t exec = nullptr;
+  const hipError_t ie = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+  hipGraphDestroy(graph);
+  if (ie != hipSuccess) return OQ_ERR_HIP;
+  h->graphs.push_back({x, t0, n, exec});
+  return hipGraphLaunch(exec, st) == hipSuccess ? OQ_OK : OQ_ERR_HIP;
 }
 
 }  // namespace
@@ -420,13 +717,17 @@ extern "C" int oq_dit_create(const oq_dit_config* cfg, const oq_dit_weights* w, 
       return OQ_ERR_NULL;
     if (cfg->prefix > 0 && (!b.prefix_k || !b.prefix_v)) return OQ_ERR_NULL;
     if (!oq::aligned(b.qkv.wq, 16) || !oq::aligned(b.o.wq, 16) || !oq::aligned(b.gate_up.wq, 16) ||
-        !oq::aligned(b.down.wq, 16))
+        !oq::aligned(b.down.wq, 16) || !oq::aligned(b.g1, 16) || !oq::aligned(b.g2, 16) ||
+        (cfg->prefix > 0 && (!oq::aligned(b.prefix_k, 16) || !oq::aligned(b.prefix_v, 16))))
       return OQ_ERR_ALIGN;
   }
+  if (!oq::aligned(w->mod, 16)) return OQ_ERR_ALIGN;
   const size_t ns = static_cast<size_t>(cfg->n_blocks) * cfg->steps * 4;
   for (size_t i = 0; i < ns; ++i)
     if (!(w->s_table[i] > 0.0f) || !std::isfinite(w->s_table[i])) return OQ_ERR_ARG;
   if ((e = oq::device_check()) != OQ_OK) return e;
+  hipStream_t cap = nullptr;
+  if (hipStreamCreateWithFlags(&cap, hipStreamNonBlocking) != hipSuccess) return OQ_ERR_HIP;
   oq_dit* h = new oq_dit();
   h->cfg = *cfg;
   h->w = *w;
@@ -435,6 +736,9 @@ extern "C" int oq_dit_create(const oq_dit_config* cfg, const oq_dit_weights* w, 
   h->w.blocks = h->blocks.data();
   h->w.s_table = h->s_table.data();
   h->lay = oq::layout_for(*cfg);
+  h->cap = cap;
+  const char* env = std::getenv("OQ_DIT_NO_GRAPH");
+  h->use_graphs = !(env && env[0] == '1');
   *out = h;
   return OQ_OK;
 }
@@ -443,6 +747,7 @@ extern "C" int oq_dit_set_workspace(oq_dit* h, void* workspace, size_t bytes) {
   if (!h || !workspace) return OQ_ERR_NULL;
   if (!oq::aligned(workspace, 256)) return OQ_ERR_ALIGN;
   if (bytes < h->lay.total) return OQ_ERR_WORKSPACE;
+  if (h->ws != workspace) oq::drop_graphs(h);
   h->ws = static_cast<uint8_t*>(workspace);
   h->ws_bytes = bytes;
   return OQ_OK;
@@ -452,18 +757,15 @@ extern "C" int oq_dit_step(oq_dit* h, float* x, int32_t t, void* stream) {
   if (!h || !x) return OQ_ERR_NULL;
   if (!h->ws) return OQ_ERR_WORKSPACE;
   if (t < 0 || t >= h->cfg.steps) return OQ_ERR_ARG;
-  return oq::run_step(h, x, t, static_cast<hipStream_t>(stream));
+  return oq::run_steps(h, x, t, 1, static_cast<hipStream_t>(stream));
 }
 
 extern "C" int oq_dit_denoise(oq_dit* h, float* x, int32_t n_steps, void* stream) {
   if (!h || !x) return OQ_ERR_NULL;
   if (!h->ws) return OQ_ERR_WORKSPACE;
   if (n_steps < 0 || n_steps > h->cfg.steps) return OQ_ERR_ARG;
-  for (int t = 0; t < n_steps; ++t) {
-    int e = oq::run_step(h, x, t, static_cast<hipStream_t>(stream));
-    if (e != OQ_OK) return e;
-  }
-  return OQ_OK;
+  if (n_steps == 0) return OQ_OK;
+  return oq::run_steps(h, x, 0, n_steps, static_cast<hipStream_t>(stream));
 }
 
 extern "C" int oq_dit_run_block(oq_dit* h, int32_t l, int32_t t, float* resid, void* stream) {
@@ -486,4 +788,9 @@ extern "C" int oq_dit_get_intermediates(const oq_dit* h, oq_dit_intermediates* o
   return OQ_OK;
 }
 
-extern "C" void oq_dit_destroy(oq_dit* h) { delete h; }
+extern "C" void oq_dit_destroy(oq_dit* h) {
+  if (!h) return;
+  oq::drop_graphs(h);
+  if (h->cap) hipStreamDestroy(h->cap);
+  delete h;
+}

@@ -27,28 +27,10 @@
 #include <cmath>
 
 #include "common.h"
+#include "rq_device.h"
 
 namespace oq {
 namespace {
-
-constexpr float kRoundMagic = 12582912.0f;  // 1.5 * 2^23
-
-__device__ __forceinline__ float lane_xor(float v, int m) {
-  // m is a wave-uniform power of two below 64.
-  int x = __float_as_int(v);
-  switch (m) {
-    case 1: return __int_as_float(__builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, false));  // quad_perm [1,0,3,2]
-    case 2: return __int_as_float(__builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, false));  // quad_perm [2,3,0,1]
-    case 4: return __int_as_float(__builtin_amdgcn_ds_swizzle(x, 0x1F | (4 << 10)));
-    case 8: return __int_as_float(__builtin_amdgcn_ds_swizzle(x, 0x1F | (8 << 10)));
-    case 16: return __int_as_float(__builtin_amdgcn_ds_swizzle(x, 0x1F | (16 << 10)));
-    default: return __shfl_xor(v, 32, 64);
-  }
-}
-
-__device__ __forceinline__ float half_bits_to_float(uint32_t h) {
-  return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(h)));
-}
 
 template <int C>
 __global__ __launch_bounds__(256) void rq_kernel(const uint16_t* __restrict__ X, int64_t M, int K,
@@ -56,175 +38,11 @@ __global__ __launch_bounds__(256) void rq_kernel(const uint16_t* __restrict__ X,
                                                  float s_over_sqrtb, uint8_t* __restrict__ Xq,
                                                  float* __restrict__ xs, float* __restrict__ ratio) {
   extern __shared__ float lds[];  // [rows_per_wg][K] when a row spans several waves
-  __shared__ float wave_max[4];
-
-  const int T = 1 << logT;
-  const int tid = threadIdx.x;
-  const int row_local = tid >> logT;
-  const int t = tid & (T - 1);
-  const int rows_per_wg = blockDim.x >> logT;
-  const int64_t row = static_cast<int64_t>(blockIdx.x) * rows_per_wg + row_local;
-  const bool valid = row < M;
-  const int lane = tid & 63;
-
+  __shared__ float red[4];
+  const rqd::RowMap m = rqd::row_map(logT, M);
   float v[C][8];
-  {
-    const uint16_t* xr = X + (valid ? row : 0) * ldx;
-#pragma unroll
-    for (int c = 0; c < C; ++c) {
-      uint4 raw = make_uint4(0, 0, 0, 0);
-      if (valid) raw = *reinterpret_cast<const uint4*>(xr + c * 8 * T + t * 8);
-      const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        v[c][2 * q] = half_bits_to_float(w[q] & 0xFFFFu);
-        v[c][2 * q + 1] = half_bits_to_float(w[q] >> 16);
-      }
-    }
-  }
-
-  // Bits 0..2: inside each 8-channel chunk.
-#pragma unroll
-  for (int m = 0; m < 3; ++m) {
-    const int h = 1 << m;
-    if (h < (1 << logb)) {
-#pragma unroll
-      for (int c = 0; c < C; ++c)
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-          if ((j & h) == 0) {
-            const float a = v[c][j], b = v[c][j + h];
-            v[c][j] = a + b;
-            v[c][j + h] = a - b;
-          }
-    }
-  }
-
-  // Bits 3 .. 3+log2(lanes per row)-1: across lanes of one wave.
-  const int lane_bits = logT < 6 ? logT : 6;
-  const int lane_stages = min(lane_bits, max(logb - 3, 0));
-  for (int m = 0; m < lane_stages; ++m) {
-    const int h = 1 << m;
-    const float sgn = (lane & h) ? -1.0f : 1.0f;
-#pragma unroll
-    for (int c = 0; c < C; ++c)
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float p = lane_xor(v[c][j], h);
-        v[c][j] = fmaf(sgn, v[c][j], p);  // upper partner: p - v ; lower: p + v
-      }
-  }
-
-  // Wave bits (rows wider than 64 threads): one exchange through LDS.
-  if (logT > 6) {
-    const int wave_stages = min(logT - 6, max(logb - 9, 0));
-    if (wave_stages > 0) {
-      float* rl = lds + row_local * K;
-#pragma unroll
-      for (int c = 0; c < C; ++c) {
-        float4* dst = reinterpret_cast<float4*>(rl + c * 8 * T + t * 8);
-        dst[0] = make_float4(v[c][0], v[c][1], v[c][2], v[c][3]);
-        dst[1] = make_float4(v[c][4], v[c][5], v[c][6], v[c][7]);
-      }
-      __syncthreads();
-      const int w = t >> 6;
-      const int nw = 1 << wave_stages;
-      const int wlow = w & (nw - 1);
-      const int wbase = w & ~(nw - 1);
-#pragma unroll
-      for (int c = 0; c < C; ++c) {
-        float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        for (int u = 0; u < nw; ++u) {
-          const float sg = (__popc(wlow & u) & 1) ? -1.0f : 1.0f;
-          const int tt = ((wbase | u) << 6) | lane;
-          const float4* src = reinterpret_cast<const float4*>(rl + c * 8 * T + tt * 8);
-          const float4 p0 = src[0], p1 = src[1];
-          acc[0] = fmaf(sg, p0.x, acc[0]);
-          acc[1] = fmaf(sg, p0.y, acc[1]);
-          acc[2] = fmaf(sg, p0.z, acc[2]);
-          acc[3] = fmaf(sg, p0.w, acc[3]);
-          acc[4] = fmaf(sg, p1.x, acc[4]);
-          acc[5] = fmaf(sg, p1.y, acc[5]);
-          acc[6] = fmaf(sg, p1.z, acc[6]);
-          acc[7] = fmaf(sg, p1.w, acc[7]);
-        }
-#pragma unroll
-        for (int j = 0; j < 8; ++j) v[c][j] = acc[j];
-      }
-    }
-  }
-
-  // Bits above the thread bits: chunk index c, in registers.
-  {
-    const int cbit0 = 3 + logT;
-#pragma unroll
-    for (int q = 0; q < 3; ++q) {
-      const int h = 1 << q;
-      if (h < C && cbit0 + q < logb) {
-#pragma unroll
-        for (int c = 0; c < C; ++c)
-          if ((c & h) == 0 && c + h < C)
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-              const float a = v[c][j], b = v[c + h][j];
-              v[c][j] = a + b;
-              v[c + h][j] = a - b;
-            }
-      }
-    }
-  }
-
-  // Row absolute maximum.
-  float amax = 0.0f;
-#pragma unroll
-  for (int c = 0; c < C; ++c)
-#pragma unroll
-    for (int j = 0; j < 8; ++j) amax = fmaxf(amax, fabsf(v[c][j]));
-  for (int m = 0; m < lane_bits; ++m) amax = fmaxf(amax, lane_xor(amax, 1 << m));
-  if (logT > 6) {
-    // One row per workgroup here (T >= 128 implies rows_per_wg <= 2; each row
-    // has its own pair of slots).
-    const int w = tid >> 6;
-    if (lane == 0) wave_max[w] = amax;
-    __syncthreads();
-    const int nwr = T >> 6;
-    const int first = row_local * nwr;
-    amax = 0.0f;
-    for (int u = 0; u < nwr; ++u) amax = fmaxf(amax, wave_max[first + u]);
-  }
-
-  // Scalars: a_z = max|s_t y|, Delta = a_z / 7, x_scale = Delta / s_t, and the
-  // per-element multiplier g = (s_t / sqrt(b)) / Delta mapping the unnormalized
-  // butterfly output u to the ratio z / Delta.
-  const float a_z = amax * s_over_sqrtb;
-  const float delta = a_z / 7.0f;
-  const float g = delta > 0.0f ? s_over_sqrtb / delta : 0.0f;
-  if (valid && t == 0) xs[row] = delta / s_t;
-  if (!valid) return;
-
-  if (ratio != nullptr) {
-    float* rr = ratio + row * static_cast<int64_t>(K);
-#pragma unroll
-    for (int c = 0; c < C; ++c) {
-      float4* dst = reinterpret_cast<float4*>(rr + c * 8 * T + t * 8);
-      dst[0] = make_float4(v[c][0] * g, v[c][1] * g, v[c][2] * g, v[c][3] * g);
-      dst[1] = make_float4(v[c][4] * g, v[c][5] * g, v[c][6] * g, v[c][7] * g);
-    }
-    return;
-  }
-
-  uint8_t* qr = Xq + row * static_cast<int64_t>(K / 2);
-#pragma unroll
-  for (int c = 0; c < C; ++c) {
-    uint32_t word = 0;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float r = fminf(fmaxf(v[c][j] * g, -7.0f), 7.0f);
-      const uint32_t bits = __float_as_uint(r + kRoundMagic);
-      word |= (bits & 0xFu) << (4 * j);
-    }
-    *reinterpret_cast<uint32_t*>(qr + (c * 8 * T + t * 8) / 2) = word;
-  }
+  rqd::load_row_f16<C>(v, X, ldx, m);
+  rqd::rq_core<C>(v, m, K, logb, s_t, s_over_sqrtb, lds, red, Xq, xs, ratio);
 }
 
 }  // namespace

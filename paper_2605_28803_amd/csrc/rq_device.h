@@ -1,0 +1,313 @@
+// Device-side building blocks of the fused Hadamard rotation + per-step scale +
+// per-token int4 quantization (Section 4.1 eq:blockdiag / eq:transform; Section
+// 4.2 eq:scale, eq:quant, eq:perstep_scale), shared by the stand-alone
+// rotate-quantize kernel and by kernels that produce a row and quantize it in
+// the same pass (the DiT norm, attention-combine and gated-GELU kernels).
+//
+// Row layout.  A row of K channels is owned by T = 2^logT threads; thread t
+// holds C chunks of 8 consecutive channels, channel k = c * 8T + t * 8 + j.
+// The Walsh-Hadamard butterflies over the index bits below log2(b) commute;
+// each is done where its bit lives: bits 0..2 in registers, the next
+// log2(min(T, 64)) bits across lanes (DPP, ds_swizzle, permlane swaps), wave
+// bits through LDS, bits above the thread bits in registers again.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace oq {
+namespace rqd {
+
+constexpr float kRoundMagic = 12582912.0f;  // 1.5 * 2^23: x + magic rounds x half-to-even into the low mantissa bits
+
+__device__ __forceinline__ float h2f(uint32_t h) {
+  return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(h)));
+}
+__device__ __forceinline__ uint16_t f2h(float f) { return __builtin_bit_cast(uint16_t, static_cast<_Float16>(f)); }
+// Round to fp16 and back: the value a tensor stored in fp16 holds.
+__device__ __forceinline__ float f16r(float f) { return static_cast<float>(static_cast<_Float16>(f)); }
+
+// Value of lane (lane ^ H) for H < 16: DPP quad permutations for 1 and 2,
+// ds_swizzle (bit-mask mode, 32-lane groups) for 4 and 8.
+template <int H>
+__device__ __forceinline__ float lane_xor(float v) {
+  const int x = __float_as_int(v);
+  if constexpr (H == 1) return __int_as_float(__builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, false));  // [1,0,3,2]
+  if constexpr (H == 2) return __int_as_float(__builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, false));  // [2,3,0,1]
+  if constexpr (H == 4 || H == 8) return __int_as_float(__builtin_amdgcn_ds_swizzle(x, 0x1F | (H << 10)));
+  if constexpr (H == 16) return __int_as_float(__builtin_amdgcn_ds_swizzle(x, 0x1F | (16 << 10)));
+  static_assert(H == 1 || H == 2 || H == 4 || H == 8 || H == 16, "lane_xor: H < 32");
+  return v;
+}
+
+// Butterfly over lane bit log2(H), H < 16, for every element.
+template <int H, int C>
+__device__ __forceinline__ void lane_stage(float (&v)[C][8], int lane) {
+  const float sgn = (lane & H) ? -1.0f : 1.0f;
+  float p[C][8];
+#pragma unroll
+  for (int c = 0; c < C; ++c)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) p[c][j] = lane_xor<H>(v[c][j]);
+#pragma unroll
+  for (int c = 0; c < C; ++c)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[c][j] = fmaf(sgn, v[c][j], p[c][j]);  // upper: p - v, lower: p + v
+}
+
+// Butterfly over lane bit 4 (H = 16) or 5 (H = 32) with the gfx950 permlane
+// swaps.  For two registers a, b: permlane{16,32}_swap exchanges the upper
+// half-group of a with the lower half-group of b, so afterwards the lower
+// lanes hold (a[l], a[l+H]) and the upper lanes (b[l-H], b[l]); the butterfly
+// is then lane-local, and a second swap returns every value to its lane.
+template <int H>
+__device__ __forceinline__ void permlane_swap(float& a, float& b) {
+  int x = __float_as_int(a), y = __float_as_int(b);
+  if constexpr (H == 16) {
+    auto r = __builtin_amdgcn_permlane16_swap(x, y, false, false);
+    x = r[0];
+    y = r[1];
+  } else {
+    auto r = __builtin_amdgcn_permlane32_swap(x, y, false, false);
+    x = r[0];
+    y = r[1];
+  }
+  a = __int_as_float(x);
+  b = __int_as_float(y);
+}
+
+template <int H, int C>
+__device__ __forceinline__ void lane_stage_swap(float (&v)[C][8]) {
+#pragma unroll
+  for (int c = 0; c < C; ++c)
+#pragma unroll
+    for (int j = 0; j < 8; j += 2) {
+      float a = v[c][j], b = v[c][j + 1];
+      permlane_swap<H>(a, b);
+      const float s = a + b, d = a - b;
+      a = s;
+      b = d;
+      permlane_swap<H>(a, b);
+      v[c][j] = a;
+      v[c][j + 1] = b;
+    }
+}
+
+// Where the calling thread sits: T threads per row, rows_per_wg rows per
+// workgroup (blockDim.x = max(T, 256)).
+struct RowMap {
+  int logT, T, t, lane, row_local, rows_per_wg;
+  int64_t row;
+  bool valid;
+};
+
+__device__ __forceinline__ RowMap row_map(int logT, int64_t M) {
+  RowMap r;
+  r.logT = logT;
+  r.T = 1 << logT;
+  const int tid = threadIdx.x;
+  r.row_local = tid >> logT;
+  r.t = tid & (r.T - 1);
+  r.rows_per_wg = blockDim.x >> logT;
+  r.row = static_cast<int64_t>(blockIdx.x) * r.rows_per_wg + r.row_local;
+  r.valid = r.row < M;
+  r.lane = tid & 63;
+  return r;
+}
+
+// Channel index of element (c, j) of this thread.
+__device__ __forceinline__ int chan(const RowMap& m, int c, int j) { return c * 8 * m.T + m.t * 8 + j; }
+
+// Reduction across the T threads of a row (max or sum).  Every thread of the
+// workgroup must call it (it synchronizes when a row spans several waves);
+// `red` is a 4-entry shared array that must not be in use by the caller.
+template <bool kMax>
+__device__ __forceinline__ float row_reduce(float x, const RowMap& m, float* red) {
+  const int lane_bits = m.logT < 6 ? m.logT : 6;
+  auto op = [](float a, float b) { return kMax ? fmaxf(a, b) : a + b; };
+  if (lane_bits > 0) x = op(x, lane_xor<1>(x));
+  if (lane_bits > 1) x = op(x, lane_xor<2>(x));
+  if (lane_bits > 2) x = op(x, lane_xor<4>(x));
+  if (lane_bits > 3) x = op(x, lane_xor<8>(x));
+  if (lane_bits > 4) x = op(x, lane_xor<16>(x));
+  if (lane_bits > 5) x = op(x, __shfl_xor(x, 32, 64));
+  if (m.logT > 6) {
+    const int w = threadIdx.x >> 6;
+    __syncthreads();
+    if (m.lane == 0) red[w] = x;
+    __syncthreads();
+    const int nwr = m.T >> 6;
+    const int first = m.row_local * nwr;
+    x = red[first];
+    for (int u = 1; u < nwr; ++u) x = op(x, red[first + u]);
+  }
+  return x;
+}
+
+// Load C chunks of fp16 channels of row `row` (zeros when !valid).
+template <int C>
+__device__ __forceinline__ void load_row_f16(float (&v)[C][8], const uint16_t* __restrict__ X, int64_t ldx,
+                                             const RowMap& m) {
+  const uint16_t* xr = X + (m.valid ? m.row : 0) * ldx;
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    uint4 raw = make_uint4(0, 0, 0, 0);
+    if (m.valid) raw = *reinterpret_cast<const uint4*>(xr + c * 8 * m.T + m.t * 8);
+    const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      v[c][2 * q] = h2f(w[q] & 0xFFFFu);
+      v[c][2 * q + 1] = h2f(w[q] >> 16);
+    }
+  }
+}
+
+// Pack eight codes, given as the bit patterns of (ratio + 1.5*2^23) (low
+// nibble = two's-complement code), into one dword: channel j in bits 4j..4j+3.
+__device__ __forceinline__ uint32_t pack8(const uint32_t (&b)[8]) {
+  // Low bytes of four patterns -> one dword of four bytes.
+  const uint32_t x0 = __builtin_amdgcn_perm(__builtin_amdgcn_perm(b[3], b[2], 0x04000c0cu),
+                                            __builtin_amdgcn_perm(b[1], b[0], 0x0c0c0400u), 0x07060100u);
+  const uint32_t x1 = __builtin_amdgcn_perm(__builtin_amdgcn_perm(b[7], b[6], 0x04000c0cu),
+                                            __builtin_amdgcn_perm(b[5], b[4], 0x0c0c0400u), 0x07060100u);
+  // Two nibbles per byte, then keep bytes 0 and 2 of each.
+  const uint32_t y0 = x0 & 0x0F0F0F0Fu, y1 = x1 & 0x0F0F0F0Fu;
+  const uint32_t z0 = y0 | (y0 >> 4), z1 = y1 | (y1 >> 4);
+  return __builtin_amdgcn_perm(z1, z0, 0x06040200u);
+}
+
+// The rest of the fused pass once the row's fp32 values are in registers:
+// butterflies, row maximum, scales, codes.  `lds` must hold rows_per_wg * K
+// floats when logT > 6; `red` is a 4-float shared array.  Every thread of the
+// workgroup must call it.  ratio != nullptr writes z / Delta instead of codes.
+template <int C>
+__device__ __forceinline__ void rq_core(float (&v)[C][8], const RowMap& m, int K, int logb, float s_t,
+                                        float s_over_sqrtb, float* lds, float* red, uint8_t* __restrict__ Xq,
+                                        float* __restrict__ xs, float* __restrict__ ratio) {
+  // Bits 0..2: inside each 8-channel chunk.
+#pragma unroll
+  for (int q = 0; q < 3; ++q) {
+    const int h = 1 << q;
+    if (q < logb) {
+#pragma unroll
+      for (int c = 0; c < C; ++c)
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if ((j & h) == 0) {
+            const float a = v[c][j], b = v[c][j + h];
+            v[c][j] = a + b;
+            v[c][j + h] = a - b;
+          }
+    }
+  }
+
+  // Bits 3 .. 3 + log2(lanes per row) - 1: across lanes of one wave.
+  const int lane_bits = m.logT < 6 ? m.logT : 6;
+  const int lane_stages = min(lane_bits, max(logb - 3, 0));
+  if (lane_stages > 0) lane_stage<1>(v, m.lane);
+  if (lane_stages > 1) lane_stage<2>(v, m.lane);
+  if (lane_stages > 2) lane_stage<4>(v, m.lane);
+  if (lane_stages > 3) lane_stage<8>(v, m.lane);
+  if (lane_stages > 4) lane_stage_swap<16>(v);
+  if (lane_stages > 5) lane_stage_swap<32>(v);
+
+  // Wave bits (rows wider than 64 threads): one exchange through LDS.
+  if (m.logT > 6) {
+    const int wave_stages = min(m.logT - 6, max(logb - 9, 0));
+    if (wave_stages > 0) {
+      float* rl = lds + m.row_local * K;
+#pragma unroll
+      for (int c = 0; c < C; ++c) {
+        float4* dst = reinterpret_cast<float4*>(rl + chan(m, c, 0));
+        dst[0] = make_float4(v[c][0], v[c][1], v[c][2], v[c][3]);
+        dst[1] = make_float4(v[c][4], v[c][5], v[c][6], v[c][7]);
+      }
+      __syncthreads();
+      const int w = m.t >> 6;
+      const int nw = 1 << wave_stages;
+      const int wlow = w & (nw - 1);
+      const int wbase = w & ~(nw - 1);
+#pragma unroll
+      for (int c = 0; c < C; ++c) {
+        float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        for (int u = 0; u < nw; ++u) {
+          const float sg = (__popc(wlow & u) & 1) ? -1.0f : 1.0f;
+          const int tt = ((wbase | u) << 6) | m.lane;
+          const float4* src = reinterpret_cast<const float4*>(rl + c * 8 * m.T + tt * 8);
+          const float4 p0 = src[0], p1 = src[1];
+          acc[0] = fmaf(sg, p0.x, acc[0]);
+          acc[1] = fmaf(sg, p0.y, acc[1]);
+          acc[2] = fmaf(sg, p0.z, acc[2]);
+          acc[3] = fmaf(sg, p0.w, acc[3]);
+          acc[4] = fmaf(sg, p1.x, acc[4]);
+          acc[5] = fmaf(sg, p1.y, acc[5]);
+          acc[6] = fmaf(sg, p1.z, acc[6]);
+          acc[7] = fmaf(sg, p1.w, acc[7]);
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[c][j] = acc[j];
+      }
+    }
+  }
+
+  // Bits above the thread bits: chunk index c, in registers.
+  {
+    const int cbit0 = 3 + m.logT;
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      const int h = 1 << q;
+      if (h < C && cbit0 + q < logb) {
+#pragma unroll
+        for (int c = 0; c < C; ++c)
+          if ((c & h) == 0 && c + h < C)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+              const float a = v[c][j], b = v[c + h][j];
+              v[c][j] = a + b;
+              v[c + h][j] = a - b;
+            }
+      }
+    }
+  }
+
+  // Row absolute maximum of the unnormalized transform.
+  float amax = 0.0f;
+#pragma unroll
+  for (int c = 0; c < C; ++c)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) amax = fmaxf(amax, fabsf(v[c][j]));
+  amax = row_reduce<true>(amax, m, red);
+
+  // Scalars: a_z = max|s_t y|, Delta = a_z / 7, x_scale = Delta / s_t, and the
+  // multiplier g = (s_t / sqrt(b)) / Delta taking the unnormalized butterfly
+  // output u to z / Delta.  |u g| <= 7 up to rounding, so round-half-even of
+  // u g never leaves [-7, 7] and needs no clamp.
+  const float a_z = amax * s_over_sqrtb;
+  const float delta = a_z / 7.0f;
+  const float g = delta > 0.0f ? s_over_sqrtb / delta : 0.0f;
+  if (m.valid && m.t == 0) xs[m.row] = delta / s_t;
+  if (!m.valid) return;
+
+  if (ratio != nullptr) {
+    float* rr = ratio + m.row * static_cast<int64_t>(K);
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      float4* dst = reinterpret_cast<float4*>(rr + chan(m, c, 0));
+      dst[0] = make_float4(v[c][0] * g, v[c][1] * g, v[c][2] * g, v[c][3] * g);
+      dst[1] = make_float4(v[c][4] * g, v[c][5] * g, v[c][6] * g, v[c][7] * g);
+    }
+    return;
+  }
+
+  uint8_t* qr = Xq + m.row * static_cast<int64_t>(K / 2);
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    uint32_t b[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) b[j] = __float_as_uint(fmaf(v[c][j], g, kRoundMagic));
+    *reinterpret_cast<uint32_t*>(qr + chan(m, c, 0) / 2) = pack8(b);
+  }
+}
+
+}  // namespace rqd
+}  // namespace oq

@@ -158,6 +158,176 @@ __global__ __launch_bounds__(256) void gemm_w4a4_kernel(GemmArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Skinny product, M <= 64 (the DiT's 50 action tokens, single-token decode):
+// weight-bandwidth and latency bound, so the work is spread over many small
+// workgroups.  A workgroup owns an N tile of 16 * NB columns; its WAVES waves
+// split the K steps (interleaved) and each loads its A (token codes, 64 rows)
+// and B (weight codes) fragments straight from global memory into registers,
+// widening nibbles to int8 there, for v_mfma_i32_16x16x64_i8.  The partial
+// accumulators are summed through LDS before the shared epilogue.
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ v4i widen16(uint2 w) {
+  // 8 packed bytes (16 codes) -> 16 int8 lanes holding 16 * code; even
+  // channels first within each packed dword (the same order for A and B).
+  const uint32_t m = 0xF0F0F0F0u;
+  v4i r;
+  r[0] = static_cast<int>((w.x << 4) & m);
+  r[1] = static_cast<int>(w.x & m);
+  r[2] = static_cast<int>((w.y << 4) & m);
+  r[3] = static_cast<int>(w.y & m);
+  return r;
+}
+
+// Epilogue of one output from the exact accumulator; the per-row / per-column
+// operands are passed in (loaded early by the caller).
+template <int EPI>
+__device__ __forceinline__ void store_out(const GemmArgs& a, int64_t off, int v, float xs, float ws, float bias,
+                                          float gate, float resid) {
+  if (EPI == EPI_I32) {
+    static_cast<int32_t*>(a.C)[off] = v;
+    return;
+  }
+  const float y = static_cast<float>(v) * xs * ws + bias;
+  if (EPI == EPI_F16) {
+    static_cast<_Float16*>(a.C)[off] = static_cast<_Float16>(y);
+  } else if (EPI == EPI_BF16) {
+    static_cast<uint16_t*>(a.C)[off] = f32_to_bf16_rne(y);
+  } else {
+    static_cast<float*>(a.C)[off] = fmaf(gate, y, resid);
+  }
+}
+
+template <int EPI, int NB, int WAVES, int UNROLL>
+__global__ __launch_bounds__(64 * WAVES) void gemm_skinny_kernel(GemmArgs a) {
+  constexpr int BNs = 16 * NB;
+  constexpr int KSTEP = 64;                         // codes per MFMA
+  constexpr int OUT_PER_THREAD = 64 * BNs / (64 * WAVES);
+  __shared__ int red[WAVES][64 * BNs];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int64_t n0 = static_cast<int64_t>(blockIdx.x) * BNs;
+  const int64_t Kb = a.K / 2;
+  const int nk = static_cast<int>(a.K / KSTEP);
+  const int koff = 8 * (lane >> 4);  // packed-byte offset of this lane's 16 codes in a k step
+
+  // Epilogue operands of this thread's outputs (row i / BNs, column i % BNs
+  // for i = tid + u * blockDim): loaded before the main loop.
+  const int ecol = tid % BNs;
+  const int64_t egc = n0 + ecol;
+  const bool ecol_ok = egc < a.N;
+  float e_ws = 0.0f, e_bias = 0.0f, e_gate = 1.0f;
+  float e_xs[OUT_PER_THREAD], e_res[OUT_PER_THREAD];
+  if (EPI != EPI_I32 && ecol_ok) {
+    e_ws = a.ws[egc];
+    if (a.bias) e_bias = static_cast<float>(__builtin_bit_cast(_Float16, a.bias[egc]));
+    if (EPI == EPI_RESID_F32 && a.gate) e_gate = static_cast<float>(__builtin_bit_cast(_Float16, a.gate[egc]));
+  }
+#pragma unroll
+  for (int u = 0; u < OUT_PER_THREAD; ++u) {
+    const int64_t gr = (tid + u * 64 * WAVES) / BNs;
+    e_xs[u] = 0.0f;
+    e_res[u] = 0.0f;
+    if (EPI != EPI_I32 && gr < a.M) {
+      e_xs[u] = a.xs[gr];
+      if (EPI == EPI_RESID_F32 && ecol_ok) e_res[u] = static_cast<const float*>(a.C)[gr * a.ldc + egc];
+    }
+  }
+
+  const uint8_t* arow[4];
+  bool aok[4];
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb) {
+    const int64_t r = rb * 16 + (lane & 15);
+    aok[rb] = r < a.M;
+    arow[rb] = a.A + (aok[rb] ? r : 0) * Kb + koff;
+  }
+  const uint8_t* brow[NB];
+  bool bok[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int64_t n = n0 + nb * 16 + (lane & 15);
+    bok[nb] = n < a.N;
+    brow[nb] = a.B + (bok[nb] ? n : 0) * Kb + koff;
+  }
+
+  v4i acc[4][NB];
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[rb][nb] = v4i{0, 0, 0, 0};
+
+  for (int k0 = wave; k0 < nk; k0 += WAVES * UNROLL) {
+    uint2 fa[UNROLL][4], fb[UNROLL][NB];
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) {
+      const int ks = k0 + u * WAVES;
+      const bool kin = ks < nk;
+      const int64_t off = static_cast<int64_t>(ks) * (KSTEP / 2);
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb)
+        fa[u][rb] = (kin && aok[rb]) ? *reinterpret_cast<const uint2*>(arow[rb] + off) : make_uint2(0, 0);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        fb[u][nb] = (kin && bok[nb]) ? *reinterpret_cast<const uint2*>(brow[nb] + off) : make_uint2(0, 0);
+    }
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) {
+      v4i wb[NB];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) wb[nb] = widen16(fb[u][nb]);
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb) {
+        const v4i xa = widen16(fa[u][rb]);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+          acc[rb][nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(xa, wb[nb], acc[rb][nb], 0, 0, 0);
+      }
+    }
+  }
+
+  // 16x16 accumulator layout: element e of lane l is row 4*(l/16) + e, column l%16.
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int row = rb * 16 + 4 * (lane >> 4) + e;
+        const int col = nb * 16 + (lane & 15);
+        red[wave][row * BNs + col] = acc[rb][nb][e];
+      }
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < OUT_PER_THREAD; ++u) {
+    const int i = tid + u * 64 * WAVES;
+    const int64_t gr = i / BNs;
+    if (gr >= a.M || !ecol_ok) continue;
+    int sum = 0;
+#pragma unroll
+    for (int w = 0; w < WAVES; ++w) sum += red[w][i];
+    store_out<EPI>(a, gr * a.ldc + egc, sum >> 8, e_xs[u], e_ws, e_bias, e_gate, e_res[u]);
+  }
+}
+
+template <int EPI>
+int launch_skinny(const GemmArgs& a, hipStream_t stream) {
+  // Narrow tiles when N is small so that enough workgroups stream the weight;
+  // deep K gets eight waves, each with all of its k steps in flight.
+  const bool narrow = a.N <= 2048;
+  const bool deep = a.K >= 4096;
+  const unsigned nb = narrow ? 16 : 32;
+  const dim3 grid(static_cast<unsigned>((a.N + nb - 1) / nb));
+  if (narrow && deep) hipLaunchKernelGGL((gemm_skinny_kernel<EPI, 1, 8, 8>), grid, dim3(512), 0, stream, a);
+  else if (narrow) hipLaunchKernelGGL((gemm_skinny_kernel<EPI, 1, 4, 4>), grid, dim3(256), 0, stream, a);
+  else if (deep) hipLaunchKernelGGL((gemm_skinny_kernel<EPI, 2, 8, 8>), grid, dim3(512), 0, stream, a);
+  else hipLaunchKernelGGL((gemm_skinny_kernel<EPI, 2, 4, 4>), grid, dim3(256), 0, stream, a);
+  return launch_status();
+}
+
 }  // namespace
 
 int gemm_validate(const uint8_t* Xq, int64_t M, const uint8_t* Wq, int64_t N, int64_t K, const void* C,
@@ -172,6 +342,15 @@ int gemm_validate(const uint8_t* Xq, int64_t M, const uint8_t* Wq, int64_t N, in
 
 int gemm_launch(const GemmArgs& a, Epilogue epi, hipStream_t stream) {
   if (a.M == 0) return OQ_OK;
+  if (a.M <= 64) {
+    switch (epi) {
+      case EPI_I32: return launch_skinny<EPI_I32>(a, stream);
+      case EPI_F16: return launch_skinny<EPI_F16>(a, stream);
+      case EPI_BF16: return launch_skinny<EPI_BF16>(a, stream);
+      case EPI_RESID_F32: return launch_skinny<EPI_RESID_F32>(a, stream);
+      default: return OQ_ERR_ARG;
+    }
+  }
   const dim3 grid(static_cast<unsigned>((a.N + BN - 1) / BN), static_cast<unsigned>((a.M + BM - 1) / BM));
   switch (epi) {
     case EPI_I32: hipLaunchKernelGGL(gemm_w4a4_kernel<EPI_I32>, grid, dim3(256), 0, stream, a); break;
