@@ -159,6 +159,197 @@ __global__ __launch_bounds__(256) void gemm_w4a4_kernel(GemmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Large product (prefill / batched shapes): 256 x 256 output tile per
+// 512-thread workgroup of 8 waves (2 x 4), each wave a 128 x 64 tile (4 x 2
+// blocks of v_mfma_i32_32x32x32_i8, 128 accumulator registers), so two waves
+// share each SIMD and the hardware overlaps one wave's nibble widening and
+// LDS traffic with the other's MFMAs.  Codes stay packed in LDS (half the LDS
+// traffic of int8 tiles) and are widened to int8 after each 8-byte fragment
+// read.  K step 64 codes (32 packed bytes per row); LDS rows padded to 40
+// bytes (10 dwords: the 8-byte reads of 16 consecutive rows hit 16 distinct
+// bank pairs); two LDS buffers.  Global loads run three K steps ahead through
+// a ring of three register stages; rows past M (N) and steps past the last
+// read clamped addresses, so the loads are branch-free and the compiler
+// counts them exactly.  Tiles are visited XCD-major: consecutive workgroup
+// ids go to different XCDs, so ids are remapped so that each XCD works on a
+// compact group of tiles (shared A rows / B columns stay in that XCD's L2).
+// ---------------------------------------------------------------------------
+
+constexpr int BIG = 256;
+constexpr int BIG_STRIDE = 40;  // packed bytes per LDS row (32 data + 8 pad)
+
+__device__ __forceinline__ v4i widen16_u2(uint2 p) {
+  const uint32_t m = 0xF0F0F0F0u;
+  v4i r;
+  r[0] = static_cast<int>((p.x << 4) & m);
+  r[1] = static_cast<int>(p.x & m);
+  r[2] = static_cast<int>((p.y << 4) & m);
+  r[3] = static_cast<int>(p.y & m);
+  return r;
+}
+
+// Map a linear workgroup id to an output tile (tm, tn): the grid is cut into
+// 8 contiguous chunks, one per XCD (hardware dispatches id i to XCD i % 8),
+// and each chunk is walked in groups of GM tile rows.
+__device__ __forceinline__ void big_tile(int id, int tiles_m, int tiles_n, int* tm, int* tn) {
+  const int total = tiles_m * tiles_n;
+  int lin = id;
+  if (total % 8 == 0) {
+    const int per = total / 8;
+    lin = (id % 8) * per + id / 8;
+  }
+  constexpr int GM = 4;
+  const int group = lin / (GM * tiles_n);
+  const int first_m = group * GM;
+  const int gsize = min(GM, tiles_m - first_m);
+  const int in = lin - group * GM * tiles_n;
+  *tm = first_m + in % gsize;
+  *tn = in / gsize;
+}
+
+template <int EPI>
+__global__ __launch_bounds__(512, 1) void gemm_big_kernel(GemmArgs a) {
+  __shared__ __attribute__((aligned(16))) uint8_t sA[2][BIG * BIG_STRIDE];
+  __shared__ __attribute__((aligned(16))) uint8_t sB[2][BIG * BIG_STRIDE];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave >> 2, wn = wave & 3;  // 2 x 4 waves: rows wm*128, columns wn*64
+  const int tiles_m = static_cast<int>((a.M + BIG - 1) / BIG);
+  const int tiles_n = static_cast<int>((a.N + BIG - 1) / BIG);
+  int tm, tn;
+  big_tile(blockIdx.x, tiles_m, tiles_n, &tm, &tn);
+  const int64_t m0 = static_cast<int64_t>(tm) * BIG;
+  const int64_t n0 = static_cast<int64_t>(tn) * BIG;
+  const int64_t Kb = a.K / 2;
+  const int nk = static_cast<int>(a.K / 64);
+
+  // Global -> LDS: a K step is 256 rows x 32 packed bytes per operand; thread
+  // loads 16 packed bytes of row tid/2 of A and of B.
+  const int lr = tid >> 1, lh = tid & 1;
+  const uint8_t* gA = a.A + min<int64_t>(m0 + lr, a.M - 1) * Kb + lh * 16;
+  const uint8_t* gB = a.B + min<int64_t>(n0 + lr, a.N - 1) * Kb + lh * 16;
+  // Three register stages (plain variables: they must stay in VGPRs).
+  uint4 r0a, r0b, r1a, r1b, r2a, r2b;
+#define OQ_GLOAD(KS, RA, RB)                                                      \
+  {                                                                               \
+    const int64_t off_ = static_cast<int64_t>(min((KS), nk - 1)) * 32;            \
+    RA = *reinterpret_cast<const uint4*>(gA + off_);                              \
+    RB = *reinterpret_cast<const uint4*>(gB + off_);                              \
+  }
+#define OQ_ST16(P, V)                                                \
+  {                                                                  \
+    uint2* q_ = reinterpret_cast<uint2*>(P);                         \
+    q_[0] = make_uint2((V).x, (V).y);                                \
+    q_[1] = make_uint2((V).z, (V).w);                                \
+  }
+#define OQ_LSTORE(BUF, RA, RB)                                       \
+  {                                                                  \
+    OQ_ST16(&sA[(BUF)][lr * BIG_STRIDE + lh * 16], RA)               \
+    OQ_ST16(&sB[(BUF)][lr * BIG_STRIDE + lh * 16], RB)               \
+  }
+
+  v16i acc[4][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0;
+
+  const int frow = lane & 31;
+  const int fofs = 8 * (lane >> 5);  // 8 packed bytes = 16 codes of a 32-code sub-step
+  const uint8_t* pA = &sA[0][(wm * 128 + frow) * BIG_STRIDE + fofs];
+  const uint8_t* pB = &sB[0][(wn * 64 + frow) * BIG_STRIDE + fofs];
+#define OQ_COMPUTE(BUF)                                                                                     \
+  {                                                                                                         \
+    const int bo_ = (BUF) * BIG * BIG_STRIDE;                                                               \
+    _Pragma("unroll") for (int sub = 0; sub < 2; ++sub) {                                                   \
+      v4i fa[4], fb[2];                                                                                     \
+      _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                         \
+        fa[i] = widen16_u2(*reinterpret_cast<const uint2*>(pA + bo_ + i * 32 * BIG_STRIDE + sub * 16));    \
+      _Pragma("unroll") for (int j = 0; j < 2; ++j)                                                         \
+        fb[j] = widen16_u2(*reinterpret_cast<const uint2*>(pB + bo_ + j * 32 * BIG_STRIDE + sub * 16));    \
+      _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                         \
+      _Pragma("unroll") for (int j = 0; j < 2; ++j)                                                         \
+        acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);                 \
+    }                                                                                                       \
+  }
+
+  OQ_GLOAD(0, r0a, r0b)
+  OQ_GLOAD(1, r1a, r1b)
+  OQ_GLOAD(2, r2a, r2b)
+  OQ_LSTORE(0, r0a, r0b)
+  __syncthreads();
+  // Step kt: store step kt+1 (loaded two steps ago) into the other buffer,
+  // start the load of step kt+3, run the MFMAs of step kt, barrier.  At the
+  // top of each iteration stage 1 holds step kt+1 and stage 2 step kt+2.
+  int kt = 0;
+  for (; kt + 3 <= nk; kt += 3) {
+    OQ_LSTORE((kt + 1) & 1, r1a, r1b)
+    OQ_GLOAD(kt + 3, r0a, r0b)
+    OQ_COMPUTE(kt & 1)
+    __syncthreads();
+    OQ_LSTORE((kt + 2) & 1, r2a, r2b)
+    OQ_GLOAD(kt + 4, r1a, r1b)
+    OQ_COMPUTE((kt + 1) & 1)
+    __syncthreads();
+    OQ_LSTORE((kt + 3) & 1, r0a, r0b)
+    OQ_GLOAD(kt + 5, r2a, r2b)
+    OQ_COMPUTE((kt + 2) & 1)
+    __syncthreads();
+  }
+  if (kt < nk) {  // one or two steps left; step kt is already in buffer kt & 1
+    if (kt + 1 < nk) OQ_LSTORE((kt + 1) & 1, r1a, r1b)
+    OQ_COMPUTE(kt & 1)
+    __syncthreads();
+    if (kt + 1 < nk) OQ_COMPUTE((kt + 1) & 1)
+  }
+#undef OQ_GLOAD
+#undef OQ_ST16
+#undef OQ_LSTORE
+#undef OQ_COMPUTE
+
+  // Epilogue (32 x 32 layout: element e of lane l is row 8*(e/4) + 4*(l/32) + e%4, column l%32).
+  const int col_in = lane & 31;
+  const int row_grp = 4 * (lane >> 5);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int64_t gc = n0 + wn * 64 + j * 32 + col_in;
+    if (gc >= a.N) continue;
+    float wsc = 0.0f, bias = 0.0f, gate = 1.0f;
+    if (EPI != EPI_I32) {
+      wsc = a.ws[gc];
+      if (a.bias) bias = static_cast<float>(__builtin_bit_cast(_Float16, a.bias[gc]));
+      if (EPI == EPI_RESID_F32 && a.gate) gate = static_cast<float>(__builtin_bit_cast(_Float16, a.gate[gc]));
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int64_t gr = m0 + wm * 128 + i * 32 + 8 * (e >> 2) + row_grp + (e & 3);
+        if (gr >= a.M) continue;
+        const int v = acc[i][j][e] >> 8;
+        const int64_t off = gr * a.ldc + gc;
+        if (EPI == EPI_I32) {
+          static_cast<int32_t*>(a.C)[off] = v;
+        } else {
+          const float y = static_cast<float>(v) * a.xs[gr] * wsc + bias;
+          if (EPI == EPI_F16) {
+            static_cast<_Float16*>(a.C)[off] = static_cast<_Float16>(y);
+          } else if (EPI == EPI_BF16) {
+            static_cast<uint16_t*>(a.C)[off] = f32_to_bf16_rne(y);
+          } else {
+            float* rp = static_cast<float*>(a.C) + off;
+            *rp = fmaf(gate, y, *rp);
+          }
+        }
+      }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Skinny product, M <= 64 (the DiT's 50 action tokens, single-token decode):
 // weight-bandwidth and latency bound, so the work is spread over many small
 // workgroups.  A workgroup owns an N tile of 16 * NB columns; its WAVES waves
@@ -350,6 +541,19 @@ int gemm_launch(const GemmArgs& a, Epilogue epi, hipStream_t stream) {
       case EPI_RESID_F32: return launch_skinny<EPI_RESID_F32>(a, stream);
       default: return OQ_ERR_ARG;
     }
+  }
+  // Large problems: 256 x 256 tiles when they still fill every CU.
+  const int64_t big_tiles = ((a.M + BIG - 1) / BIG) * ((a.N + BIG - 1) / BIG);
+  if (big_tiles >= 256) {
+    const dim3 g(static_cast<unsigned>(big_tiles));
+    switch (epi) {
+      case EPI_I32: hipLaunchKernelGGL(gemm_big_kernel<EPI_I32>, g, dim3(512), 0, stream, a); break;
+      case EPI_F16: hipLaunchKernelGGL(gemm_big_kernel<EPI_F16>, g, dim3(512), 0, stream, a); break;
+      case EPI_BF16: hipLaunchKernelGGL(gemm_big_kernel<EPI_BF16>, g, dim3(512), 0, stream, a); break;
+      case EPI_RESID_F32: hipLaunchKernelGGL(gemm_big_kernel<EPI_RESID_F32>, g, dim3(512), 0, stream, a); break;
+      default: return OQ_ERR_ARG;
+    }
+    return launch_status();
   }
   const dim3 grid(static_cast<unsigned>((a.N + BN - 1) / BN), static_cast<unsigned>((a.M + BM - 1) / BM));
   switch (epi) {

@@ -33,6 +33,18 @@ def test_i32_accumulators_bit_exact(M, N, K):
     assert np.array_equal(acc.cpu().numpy().astype(np.int64), linear.int_gemm(q, qw))
 
 
+@pytest.mark.parametrize("M,N,K", [(4096, 4096, 256), (4100, 4160, 192), (8192, 2048, 128), (2048, 8320, 64)])
+def test_i32_bit_exact_large_tiles(M, N, K):
+    """Shapes that take the 256 x 256 tile path (>= 256 tiles), with ragged edges."""
+    print(f"gemm i32 large M={M} N={N} K={K}", flush=True)
+    rng = np.random.default_rng(M + 3 * N + 7 * K)
+    q, qw = _codes(rng, M, K), _codes(rng, N, K)
+    acc = oq.w4a4_gemm_i32(torch.from_numpy(parity.pack_int4(q)).to(DEV),
+                           torch.from_numpy(parity.pack_int4(qw)).to(DEV))
+    torch.cuda.synchronize()
+    assert np.array_equal(acc.cpu().numpy().astype(np.int64), linear.int_gemm(q, qw))
+
+
 def test_i32_extreme_magnitudes():
     """Every code +-7 at K = 16384: |acc| = 49 K, the largest the format allows."""
     K = 16384
