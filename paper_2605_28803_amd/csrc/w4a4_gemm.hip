@@ -176,7 +176,9 @@ __global__ __launch_bounds__(256) void gemm_w4a4_kernel(GemmArgs a) {
 // ---------------------------------------------------------------------------
 
 constexpr int BIG = 256;
-constexpr int BIG_STRIDE = 40;  // packed bytes per LDS row (32 data + 8 pad)
+constexpr int BIG_KSTAGE = 128;  // codes per LDS stage (64 packed bytes per row)
+constexpr int BIG_STRIDE = 72;   // packed bytes per LDS row (64 data + 8 pad): 18 dwords, so the
+                                 // 8-byte reads of 16 consecutive rows use 16 distinct bank pairs
 
 __device__ __forceinline__ v4i widen16_u2(uint2 p) {
   const uint32_t m = 0xF0F0F0F0u;
@@ -223,20 +225,25 @@ __global__ __launch_bounds__(512, 1) void gemm_big_kernel(GemmArgs a) {
   const int64_t m0 = static_cast<int64_t>(tm) * BIG;
   const int64_t n0 = static_cast<int64_t>(tn) * BIG;
   const int64_t Kb = a.K / 2;
-  const int nk = static_cast<int>(a.K / 64);
+  const int nk = static_cast<int>((a.K + BIG_KSTAGE - 1) / BIG_KSTAGE);  // stages (the last may be half)
+  const int nk64 = static_cast<int>(a.K / 64);                            // 64-code halves in total
 
-  // Global -> LDS: a K step is 256 rows x 32 packed bytes per operand; thread
-  // loads 16 packed bytes of row tid/2 of A and of B.
+  // Global -> LDS: a stage is 256 rows x 64 packed bytes per operand; thread
+  // loads 32 packed bytes (two 16-byte pieces) of row tid/2 of A and of B.
+  // A half stage past K reads a clamped address; its MFMAs are skipped.
   const int lr = tid >> 1, lh = tid & 1;
-  const uint8_t* gA = a.A + min<int64_t>(m0 + lr, a.M - 1) * Kb + lh * 16;
-  const uint8_t* gB = a.B + min<int64_t>(n0 + lr, a.N - 1) * Kb + lh * 16;
+  const uint8_t* gA = a.A + min<int64_t>(m0 + lr, a.M - 1) * Kb + lh * 32;
+  const uint8_t* gB = a.B + min<int64_t>(n0 + lr, a.N - 1) * Kb + lh * 32;
   // Three register stages (plain variables: they must stay in VGPRs).
-  uint4 r0a, r0b, r1a, r1b, r2a, r2b;
-#define OQ_GLOAD(KS, RA, RB)                                                      \
+  uint4 r0a, r0b, r0c, r0d, r1a, r1b, r1c, r1d, r2a, r2b, r2c, r2d;
+#define OQ_GLOAD(KS, RA, RA2, RB, RB2)                                            \
   {                                                                               \
-    const int64_t off_ = static_cast<int64_t>(min((KS), nk - 1)) * 32;            \
+    const int h_ = min(2 * (KS) + lh, nk64 - 1);                                  \
+    const int64_t off_ = static_cast<int64_t>(h_) * 32 - lh * 32;                 \
     RA = *reinterpret_cast<const uint4*>(gA + off_);                              \
+    RA2 = *reinterpret_cast<const uint4*>(gA + off_ + 16);                        \
     RB = *reinterpret_cast<const uint4*>(gB + off_);                              \
+    RB2 = *reinterpret_cast<const uint4*>(gB + off_ + 16);                        \
   }
 #define OQ_ST16(P, V)                                                \
   {                                                                  \
@@ -244,10 +251,12 @@ __global__ __launch_bounds__(512, 1) void gemm_big_kernel(GemmArgs a) {
     q_[0] = make_uint2((V).x, (V).y);                                \
     q_[1] = make_uint2((V).z, (V).w);                                \
   }
-#define OQ_LSTORE(BUF, RA, RB)                                       \
+#define OQ_LSTORE(BUF, RA, RA2, RB, RB2)                             \
   {                                                                  \
-    OQ_ST16(&sA[(BUF)][lr * BIG_STRIDE + lh * 16], RA)               \
-    OQ_ST16(&sB[(BUF)][lr * BIG_STRIDE + lh * 16], RB)               \
+    OQ_ST16(&sA[(BUF)][lr * BIG_STRIDE + lh * 32], RA)               \
+    OQ_ST16(&sA[(BUF)][lr * BIG_STRIDE + lh * 32 + 16], RA2)         \
+    OQ_ST16(&sB[(BUF)][lr * BIG_STRIDE + lh * 32], RB)               \
+    OQ_ST16(&sB[(BUF)][lr * BIG_STRIDE + lh * 32 + 16], RB2)         \
   }
 
   v16i acc[4][2];
@@ -262,91 +271,120 @@ __global__ __launch_bounds__(512, 1) void gemm_big_kernel(GemmArgs a) {
   const int fofs = 8 * (lane >> 5);  // 8 packed bytes = 16 codes of a 32-code sub-step
   const uint8_t* pA = &sA[0][(wm * 128 + frow) * BIG_STRIDE + fofs];
   const uint8_t* pB = &sB[0][(wn * 64 + frow) * BIG_STRIDE + fofs];
-#define OQ_COMPUTE(BUF)                                                                                     \
+#define OQ_COMPUTE(BUF, NSUB)                                                                               \
   {                                                                                                         \
     const int bo_ = (BUF) * BIG * BIG_STRIDE;                                                               \
-    _Pragma("unroll") for (int sub = 0; sub < 2; ++sub) {                                                   \
-      v4i fa[4], fb[2];                                                                                     \
-      _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                         \
-        fa[i] = widen16_u2(*reinterpret_cast<const uint2*>(pA + bo_ + i * 32 * BIG_STRIDE + sub * 16));    \
-      _Pragma("unroll") for (int j = 0; j < 2; ++j)                                                         \
-        fb[j] = widen16_u2(*reinterpret_cast<const uint2*>(pB + bo_ + j * 32 * BIG_STRIDE + sub * 16));    \
-      _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                         \
-      _Pragma("unroll") for (int j = 0; j < 2; ++j)                                                         \
-        acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);                 \
+    _Pragma("unroll") for (int sub = 0; sub < 4; ++sub) {                                                   \
+      if (sub < (NSUB)) {                                                                                   \
+        v4i fa[4], fb[2];                                                                                   \
+        _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                       \
+          fa[i] = widen16_u2(*reinterpret_cast<const uint2*>(pA + bo_ + i * 32 * BIG_STRIDE + sub * 16));  \
+        _Pragma("unroll") for (int j = 0; j < 2; ++j)                                                       \
+          fb[j] = widen16_u2(*reinterpret_cast<const uint2*>(pB + bo_ + j * 32 * BIG_STRIDE + sub * 16));  \
+        _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                       \
+        _Pragma("unroll") for (int j = 0; j < 2; ++j)                                                       \
+          acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);               \
+      }                                                                                                     \
     }                                                                                                       \
   }
+  // Sub-steps of 32 codes in stage ks: 4, or 2 for a final half stage.
+#define OQ_NSUB(KS) ((2 * (KS) + 2 <= nk64) ? 4 : 2)
 
-  OQ_GLOAD(0, r0a, r0b)
-  OQ_GLOAD(1, r1a, r1b)
-  OQ_GLOAD(2, r2a, r2b)
-  OQ_LSTORE(0, r0a, r0b)
+  OQ_GLOAD(0, r0a, r0b, r0c, r0d)
+  OQ_GLOAD(1, r1a, r1b, r1c, r1d)
+  OQ_GLOAD(2, r2a, r2b, r2c, r2d)
+  OQ_LSTORE(0, r0a, r0b, r0c, r0d)
   __syncthreads();
-  // Step kt: store step kt+1 (loaded two steps ago) into the other buffer,
-  // start the load of step kt+3, run the MFMAs of step kt, barrier.  At the
-  // top of each iteration stage 1 holds step kt+1 and stage 2 step kt+2.
+  // Stage kt: store stage kt+1 (loaded two stages ago) into the other
+  // buffer, start the load of stage kt+3, run the MFMAs of stage kt, barrier.
+  // At the top of each iteration ring slot 1 holds stage kt+1, slot 2 kt+2.
   int kt = 0;
   for (; kt + 3 <= nk; kt += 3) {
-    OQ_LSTORE((kt + 1) & 1, r1a, r1b)
-    OQ_GLOAD(kt + 3, r0a, r0b)
-    OQ_COMPUTE(kt & 1)
+    OQ_LSTORE((kt + 1) & 1, r1a, r1b, r1c, r1d)
+    OQ_GLOAD(kt + 3, r0a, r0b, r0c, r0d)
+    OQ_COMPUTE(kt & 1, 4)
     __syncthreads();
-    OQ_LSTORE((kt + 2) & 1, r2a, r2b)
-    OQ_GLOAD(kt + 4, r1a, r1b)
-    OQ_COMPUTE((kt + 1) & 1)
+    OQ_LSTORE((kt + 2) & 1, r2a, r2b, r2c, r2d)
+    OQ_GLOAD(kt + 4, r1a, r1b, r1c, r1d)
+    OQ_COMPUTE((kt + 1) & 1, 4)
     __syncthreads();
-    OQ_LSTORE((kt + 3) & 1, r0a, r0b)
-    OQ_GLOAD(kt + 5, r2a, r2b)
-    OQ_COMPUTE((kt + 2) & 1)
+    OQ_LSTORE((kt + 3) & 1, r0a, r0b, r0c, r0d)
+    OQ_GLOAD(kt + 5, r2a, r2b, r2c, r2d)
+    OQ_COMPUTE((kt + 2) & 1, OQ_NSUB(kt + 2))
     __syncthreads();
   }
-  if (kt < nk) {  // one or two steps left; step kt is already in buffer kt & 1
-    if (kt + 1 < nk) OQ_LSTORE((kt + 1) & 1, r1a, r1b)
-    OQ_COMPUTE(kt & 1)
+  if (kt < nk) {  // one or two stages left; stage kt is already in buffer kt & 1
+    if (kt + 1 < nk) OQ_LSTORE((kt + 1) & 1, r1a, r1b, r1c, r1d)
+    OQ_COMPUTE(kt & 1, OQ_NSUB(kt))
     __syncthreads();
-    if (kt + 1 < nk) OQ_COMPUTE((kt + 1) & 1)
+    if (kt + 1 < nk) OQ_COMPUTE((kt + 1) & 1, OQ_NSUB(kt + 1))
   }
+#undef OQ_NSUB
 #undef OQ_GLOAD
 #undef OQ_ST16
 #undef OQ_LSTORE
 #undef OQ_COMPUTE
 
   // Epilogue (32 x 32 layout: element e of lane l is row 8*(e/4) + 4*(l/32) + e%4, column l%32).
+  // Each lane's rows come in runs of four consecutive rows: their token scales
+  // are read as one float4 per run (rows past M read as 0).
   const int col_in = lane & 31;
   const int row_grp = 4 * (lane >> 5);
+  float wsc[2], bias[2], gate[2];
+  int64_t gcs[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
-    const int64_t gc = n0 + wn * 64 + j * 32 + col_in;
-    if (gc >= a.N) continue;
-    float wsc = 0.0f, bias = 0.0f, gate = 1.0f;
-    if (EPI != EPI_I32) {
-      wsc = a.ws[gc];
-      if (a.bias) bias = static_cast<float>(__builtin_bit_cast(_Float16, a.bias[gc]));
-      if (EPI == EPI_RESID_F32 && a.gate) gate = static_cast<float>(__builtin_bit_cast(_Float16, a.gate[gc]));
+    gcs[j] = n0 + wn * 64 + j * 32 + col_in;
+    wsc[j] = 0.0f;
+    bias[j] = 0.0f;
+    gate[j] = 1.0f;
+    if (EPI != EPI_I32 && gcs[j] < a.N) {
+      wsc[j] = a.ws[gcs[j]];
+      if (a.bias) bias[j] = static_cast<float>(__builtin_bit_cast(_Float16, a.bias[gcs[j]]));
+      if (EPI == EPI_RESID_F32 && a.gate) gate[j] = static_cast<float>(__builtin_bit_cast(_Float16, a.gate[gcs[j]]));
     }
+  }
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int64_t gr = m0 + wm * 128 + i * 32 + 8 * (e >> 2) + row_grp + (e & 3);
-        if (gr >= a.M) continue;
-        const int v = acc[i][j][e] >> 8;
-        const int64_t off = gr * a.ldc + gc;
-        if (EPI == EPI_I32) {
-          static_cast<int32_t*>(a.C)[off] = v;
+    for (int q = 0; q < 4; ++q) {
+      const int64_t r0 = m0 + wm * 128 + i * 32 + 8 * q + row_grp;
+      float xr[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      if (EPI != EPI_I32) {
+        if (r0 + 3 < a.M && (reinterpret_cast<uintptr_t>(a.xs + r0) & 15) == 0) {
+          const float4 t = *reinterpret_cast<const float4*>(a.xs + r0);
+          xr[0] = t.x; xr[1] = t.y; xr[2] = t.z; xr[3] = t.w;
         } else {
-          const float y = static_cast<float>(v) * a.xs[gr] * wsc + bias;
-          if (EPI == EPI_F16) {
-            static_cast<_Float16*>(a.C)[off] = static_cast<_Float16>(y);
-          } else if (EPI == EPI_BF16) {
-            static_cast<uint16_t*>(a.C)[off] = f32_to_bf16_rne(y);
+#pragma unroll
+          for (int u = 0; u < 4; ++u) xr[u] = r0 + u < a.M ? a.xs[r0 + u] : 0.0f;
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int64_t gc = gcs[j];
+        if (gc >= a.N) continue;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int64_t gr = r0 + u;
+          if (gr >= a.M) continue;
+          const int v = acc[i][j][4 * q + u] >> 8;
+          const int64_t off = gr * a.ldc + gc;
+          if (EPI == EPI_I32) {
+            static_cast<int32_t*>(a.C)[off] = v;
           } else {
-            float* rp = static_cast<float*>(a.C) + off;
-            *rp = fmaf(gate, y, *rp);
+            const float y = static_cast<float>(v) * xr[u] * wsc[j] + bias[j];
+            if (EPI == EPI_F16) {
+              static_cast<_Float16*>(a.C)[off] = static_cast<_Float16>(y);
+            } else if (EPI == EPI_BF16) {
+              static_cast<uint16_t*>(a.C)[off] = f32_to_bf16_rne(y);
+            } else {
+              float* rp = static_cast<float*>(a.C) + off;
+              *rp = fmaf(gate[j], y, *rp);
+            }
           }
         }
       }
-  }
+    }
 }
 
 // ---------------------------------------------------------------------------

@@ -33,7 +33,8 @@ def test_i32_accumulators_bit_exact(M, N, K):
     assert np.array_equal(acc.cpu().numpy().astype(np.int64), linear.int_gemm(q, qw))
 
 
-@pytest.mark.parametrize("M,N,K", [(4096, 4096, 256), (4100, 4160, 192), (8192, 2048, 128), (2048, 8320, 64)])
+@pytest.mark.parametrize("M,N,K", [(4096, 4096, 256), (4100, 4160, 192), (8192, 2048, 128), (2048, 8320, 64),
+                                   (4096, 4096, 320)])
 def test_i32_bit_exact_large_tiles(M, N, K):
     """Shapes that take the 256 x 256 tile path (>= 256 tiles), with ragged edges."""
     print(f"gemm i32 large M={M} N={N} K={K}", flush=True)
