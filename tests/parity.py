@@ -11,8 +11,11 @@ Tolerances (the three bars of the parity criterion):
     same codes and scales.
 
 tau.  The kernel forms the unnormalized transform u in fp32 with a summation
-tree of depth d <= log2(b) + 1, so |u_hat - u| <= gamma_d * l1 with
-gamma_d = d 2^-24 / (1 - d 2^-24) and l1 the largest per-block sum of |x|.
+tree of depth d, so |u_hat - u| <= gamma_d * l1 with gamma_d = d 2^-24 /
+(1 - d 2^-24) and l1 the largest per-block sum of |x|.  The first five
+butterfly stages may run on the matrix cores as one 32-term fp32 sum whose
+internal order is not specified; bounding it as a sequential sum (31 adds)
+gives d <= log2(b) - 5 + 31 + 1 < log2(b) + 32.
 The row maximum inherits the same error, and three more fp32 roundings form
 the multiplier g ~ 7 / max|u|.  Hence
     |r_gpu - r_exact| <= 14 gamma_d l1 / max|u| + 21 * 2^-24  =: tau_row.
@@ -43,7 +46,7 @@ def tau_rows(x: np.ndarray, b: int) -> np.ndarray:
     """Per-row bound on |r_gpu - r_exact| for activation rows x [M, K]."""
     x = np.asarray(x, dtype=np.float64)
     M, K = x.shape
-    d = int(np.log2(b)) + 1
+    d = int(np.log2(b)) + 32
     gamma = d * U32 / (1 - d * U32)
     l1 = np.abs(x).reshape(M, K // b, b).sum(axis=2).max(axis=1)
     # max|u| (unnormalized) = sqrt(b) * max|y|; recomputed from the data.
