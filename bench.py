@@ -13,12 +13,19 @@ Also reported (same JSON line):
   kernels    the W4A4 linears of one step timed alone through the C ABI with
              HIP events on the launch stream: rotate-quantize GB/s and GEMM
              GB/s / TOPS against their rooflines;
-  roofline   the dominant kernel of the step (the W4A4 GEMM) against HBM peak;
+  roofline   the dominant kernel of the step, the W4A4 GEMM, at the block's
+             largest linear (gate|up, M=50, N=8192, K=1024), against HBM peak
+             (traffic from the committed FETCH/WRITE counter summary);
+  prefill    the GEMM at M=K=N=16384 against the int8 MFMA peak and the
+             rotate-quantize at M=K=16384 against HBM peak, cold;
   cpu_baseline  the oracle on this host on a bounded sample (3 of 18 blocks of
              one step), scaled to denoising steps per second.
 
 --sweep writes the rotate-quantize / GEMM roofline sweep (M x K = N grid) as
-JSON lines to gpurun_out/sweep.jsonl instead.
+JSON lines to gpurun_out/sweep.jsonl instead; --roofline-only runs just the
+roofline kernel measurement (the command the committed rocprofv3 summaries of
+that kernel were taken with); --copy-calibration runs a plain copy of known
+size (the counter calibration reference).
 """
 from __future__ import annotations
 
@@ -122,10 +129,107 @@ def time_linears(cfg, qweights, stream):
     return out, tot
 
 
-def cpu_baseline(cfg, inp, n_blocks_sample=3):
-    """The oracle, untouched, on a bounded sample: n_blocks_sample blocks of one
-    denoising step (weights quantized beforehand, not timed), scaled to the
-    full step.  Returns the dict for the JSON line."""
+ROOFLINE_SHAPE = {"name": "gate_up", "M": 50, "N": 8192, "K": 1024}
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_skinny_gate_up_M50_traffic.txt")
+
+
+def roofline_gemm(stream=None):
+    """The roofline kernel: the W4A4 GEMM of the DiT block's gate|up projection
+    (M = 50 tokens, N = 2 x 4096, K = 1024, fp16 out) on seeded weights of
+    block 0, timed alone with HIP events around graph replays (no host launch
+    overhead), and its rotate-quantize producer likewise.  Returns a dict."""
+    import torch
+    import paper_2605_28803_amd as oq
+    from workloads import configs, generators as G
+    cfg = configs.DIT_PI
+    M, N, K = ROOFLINE_SHAPE["M"], ROOFLINE_SHAPE["N"], ROOFLINE_SHAPE["K"]
+    dev = torch.device("cuda:0")
+    W = torch.from_numpy(G.gaussian(cfg.seed, "blk0/wgu", (N, K), cfg.w_std).astype(np.float16)).to(dev)
+    Wq, ws = oq.quantize_weights(W, K & -K)
+    X = torch.from_numpy(G.gaussian(cfg.seed, "roofline/x", (M, K)).astype(np.float16)).to(dev)
+    Xq, xs = oq.rotate_quantize_act(X, K & -K)
+    Y = torch.empty((M, N), dtype=torch.float16, device=dev)
+    torch.cuda.synchronize()
+    t_g = _graph_time(lambda: oq.w4a4_linear(Xq, xs, Wq, ws, Y=Y), reps=50, replays=20)
+    t_r = _graph_time(lambda: oq.rotate_quantize_act(X, K & -K, Xq=Xq, x_scale=xs), reps=50, replays=20)
+    b = gemm_bytes(M, N, K, 2)
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        for line in open(TRAFFIC_FILE):
+            if line.startswith("traffic_bytes_per_launch"):
+                traffic = int(float(line.split("=")[1]))
+    return {"kernel": "gemm_skinny_kernel<fp16 out, 32 columns, 4 waves> (W4A4 gate|up of a DiT block: "
+                      f"M={M}, N={N}, K={K})",
+            "bound": "hbm", "achieved": round(b / (t_g * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(b / (t_g * 1e-3) / 1e9 / HBM_PEAK_GBS, 4), "traffic": traffic,
+            "avg_launch_us": round(t_g * 1e3, 3), "algorithmic_bytes_per_launch": int(b),
+            "rotate_quant_us": round(t_r * 1e3, 3)}
+
+
+def prefill_kernels():
+    """One large shape of each kernel, cold (MALL flushed before each launch):
+    W4A4 GEMM at M = K = N = 16384 (int8-MFMA roofline) and rotate-quantize at
+    M = K = 16384 (HBM roofline)."""
+    import torch
+    import paper_2605_28803_amd as oq
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    flush = torch.empty((512 << 20,), dtype=torch.uint8, device=dev)
+    M = K = N = 16384
+    g = torch.Generator(device=dev).manual_seed(7)
+    X = torch.randn((M, K), generator=g, device=dev).half()
+    W = (torch.randn((N, K), generator=g, device=dev) * 0.02).half()
+    Wq, ws = oq.quantize_weights(W, K)
+    del W
+    Xq, xs = oq.rotate_quantize_act(X, K)
+    Y = torch.empty((M, N), dtype=torch.float16, device=dev)
+
+    def cold(fn, reps):
+        ts = []
+        for _ in range(reps):
+            flush.fill_(1)
+            s = torch.cuda.Event(enable_timing=True)
+            e = torch.cuda.Event(enable_timing=True)
+            s.record(stream)
+            fn()
+            e.record(stream)
+            e.synchronize()
+            ts.append(s.elapsed_time(e))
+        return float(np.median(ts))
+    t_r = cold(lambda: oq.rotate_quantize_act(X, K, Xq=Xq, x_scale=xs), 10)
+    t_g = cold(lambda: oq.w4a4_linear(Xq, xs, Wq, ws, Y=Y), 5)
+    out = {"gemm_M16384_K16384_N16384": {"us": round(t_g * 1e3, 1),
+                                         "TOPs": round(2 * M * N * K / (t_g * 1e-3) / 1e12, 1),
+                                         "frac_int8_peak": round(2 * M * N * K / (t_g * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4)},
+           "rotate_quant_M16384_K16384": {"us": round(t_r * 1e3, 1),
+                                          "GBs": round(rq_bytes(M, K) / (t_r * 1e-3) / 1e9, 1),
+                                          "frac_hbm_peak": round(rq_bytes(M, K) / (t_r * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}}
+    del X, Xq, Y, Wq, flush
+    torch.cuda.empty_cache()
+    return out
+
+
+def copy_calibration():
+    """A plain device copy of a known size (256 MiB read + 256 MiB written), the
+    reference for scaling the FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+    dev = torch.device("cuda:0")
+    a = torch.ones((128 << 20,), dtype=torch.float16, device=dev)
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": a.numel() * 2}), flush=True)
+
+
+def cpu_baseline(cfg, inp, n_blocks_sample=3, min_seconds=10.0):
+    """The oracle, untouched, on a bounded sample of the same workload: the
+    first n_blocks_sample transformer blocks (identical in shape to the rest),
+    run as a chain with t cycling over the denoising steps until at least
+    min_seconds of CPU work are done, scaled to the full depth (the in- and
+    out-projections, 50 x 32 x 1024 each, are left out).  The sampled blocks'
+    weights are quantized beforehand (untimed).  Returns the dict for the JSON
+    line."""
     from oracle import dit as odit
     try:
         from threadpoolctl import threadpool_info
@@ -137,15 +241,23 @@ def cpu_baseline(cfg, inp, n_blocks_sample=3):
     w["blocks"] = inp["w"]["blocks"][:L]
     qb = odit.quantize_block_weights(cfg, w["blocks"])
     B, S = inp["batch"], cfg.tokens
-    r = odit.in_projection(w, inp["x0"])
+    r0 = odit.in_projection(w, inp["x0"])
+    n = 0
     t0 = time.perf_counter()
-    for l in range(L):
-        r = odit.block(cfg, w, qb, inp["mod"], inp["s_table"], r, l, 0, B, S, prefix=(inp["kp"], inp["vp"]))
-    dt = time.perf_counter() - t0
-    per_step = dt * cfg.n_blocks / L
-    return {"value": round(1.0 / per_step, 5), "unit": "DiT denoise-steps/s", "cores": cores, "kind": "oracle",
-            "sample": f"{L} of {cfg.n_blocks} blocks of one denoising step ({dt:.2f} s), scaled x{cfg.n_blocks / L:g}; "
-                      f"float64 numpy, BLAS threads={cores}, host cpus={len(os.sched_getaffinity(0))}"}
+    while True:
+        r = r0
+        for l in range(L):
+            r = odit.block(cfg, w, qb, inp["mod"], inp["s_table"], r, l, (n // L) % cfg.steps, B, S,
+                           prefix=(inp["kp"], inp["vp"]))
+            n += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            break
+    steps_per_s = n / dt / cfg.n_blocks
+    return {"value": round(steps_per_s, 5), "unit": "DiT denoise-steps/s", "cores": cores, "kind": "oracle",
+            "sample": f"{n} block evaluations (blocks 0-{L - 1}, t cycling) in {dt:.1f} s, scaled to "
+                      f"{cfg.n_blocks} blocks per step; float64 numpy, BLAS threads={cores}, "
+                      f"host cpus={len(os.sched_getaffinity(0))}"}
 
 
 def run_dit(args):
@@ -183,17 +295,9 @@ def run_dit(args):
     print(f"[bench] {args.steps} steps, {ms:.3f} ms/step", file=sys.stderr, flush=True)
 
     kern, tot = time_linears(cfg, model.qweights, stream)
-    gemm_avg_us = tot["gemm_ms"] / tot["gemm_launches"] * 1e3
-    gemm_avg_bytes = tot["gemm_bytes"] / tot["gemm_launches"]
-    achieved = gemm_avg_bytes / (gemm_avg_us * 1e-6) / 1e9
     rq_gbs = tot["rq_bytes"] / (tot["rq_ms"] * 1e-3) / 1e9
-    traffic = None
-    tpath = os.path.join(ROOT, "profiles", "traffic_dit_gemm.json")
-    if os.path.exists(tpath):
-        try:
-            traffic = json.load(open(tpath)).get("bytes_per_launch")
-        except Exception:
-            traffic = None
+    roof = roofline_gemm()
+    prefill = None if args.no_prefill else prefill_kernels()
     line = {
         "metric": METRIC,
         "value": round(1000.0 / ms, 3),
@@ -212,11 +316,8 @@ def run_dit(args):
                                "Hadamard 1024/4096, s_t log-uniform [0.5,4]",
                    "global_batch": 1, "seq_len": cfg.tokens, "timing": "warm (weights + prefix K/V fit the MALL)"},
         "dit_step_latency_us": round(ms * 1e3, 2),
-        "roofline": {"kernel": "gemm_w4a4_kernel (DiT step shapes, M=50)", "bound": "hbm",
-                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                     "avg_launch_us": round(gemm_avg_us, 3), "algorithmic_bytes_per_launch": int(gemm_avg_bytes)},
-        "kernels": {"per_linear": kern,
+        "roofline": roof,
+        "kernels": {"per_linear": kern, "prefill": prefill,
                     "rotate_quant_GBs": round(rq_gbs, 1),
                     "gemm_TOPs": round(tot["gemm_ops"] / (tot["gemm_ms"] * 1e-3) / 1e12, 3),
                     "gemm_frac_int8_peak": round(tot["gemm_ops"] / (tot["gemm_ms"] * 1e-3) / 1e12 / INT8_PEAK_TOPS, 5)},
@@ -294,12 +395,19 @@ def main():
     ap.add_argument("--sweep-m", default="")
     ap.add_argument("--sweep-k", default="")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-prefill", action="store_true")
+    ap.add_argument("--roofline-only", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (--gpus must be 1)", file=sys.stderr)
         sys.exit(2)
     if args.sweep:
         run_sweep(args)
+    elif args.roofline_only:
+        print(json.dumps({"roofline": roofline_gemm()}), flush=True)
+    elif args.copy_calibration:
+        copy_calibration()
     else:
         run_dit(args)
 
