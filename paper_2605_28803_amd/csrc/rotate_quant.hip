@@ -25,7 +25,6 @@
 // applied to the per-row scalars only (scale the max, not every element), which
 // is the same map in exact arithmetic.
 #include <cmath>
-#include <cstdlib>
 
 #include "common.h"
 #include "rq_device.h"
@@ -56,10 +55,12 @@ __global__ __launch_bounds__(256) void rq_kernel(const uint16_t* __restrict__ X,
 // receives channels 8q .. 8q+7 (q = l / 16) of chunk l % 16 -- eight
 // consecutive channels, i.e. one packed dword of codes.  Chunk index bits 0-3
 // are lane bits 0-3 (four cross-lane butterflies), the next bits are the
-// group index g in registers, and for rows wider than 4096 channels (W waves
-// per row) the top bits are exchanged through LDS.  Waves are persistent: each
-// loops over rows and loads the next row's fp16 fragments while it transforms
-// the current one.
+// register group index g.  A row wider than 4096 channels spans W waves; its
+// top log2(W) channel bits are the wave index, and the butterflies over them
+// run after a transpose through LDS that gives each wave all W wave-values of
+// NG / W of the groups.  One wave (W = 1) or one workgroup (W > 1) per row
+// pass, no prefetch: the register budget stays small enough for several
+// workgroups per CU, and their loads overlap each other's arithmetic.
 // ---------------------------------------------------------------------------
 
 typedef _Float16 rv8h __attribute__((ext_vector_type(8)));
@@ -78,159 +79,157 @@ __device__ __forceinline__ void hadamard_frags(int lane, rv8h& a1, rv8h& a2) {
   }
 }
 
-template <int NG, int W>
+template <int NG, int W, bool FULL>
 __global__ __launch_bounds__(256) void rq_mfma_kernel(const uint16_t* __restrict__ X, int64_t M, int64_t ldx, int logb,
                                                       float s_t, float s_over_sqrtb, uint8_t* __restrict__ Xq,
                                                       float* __restrict__ xs, float* __restrict__ ratio) {
-  extern __shared__ float lds[];  // W > 1: [4 waves][NG][64 lanes][8] fp32
+  // W > 1: [4 waves][NG groups][2 halves][64 lanes] float4 (consecutive lanes
+  // hit consecutive 16-byte words: no bank conflicts on either side).
+  extern __shared__ float4 xch[];
   __shared__ float red[4];
   constexpr int K = NG * W * 512;
-  constexpr int RPB = 4 / W;  // rows per workgroup pass
+  constexpr int RPB = 4 / W;  // rows per workgroup
+  constexpr int LOGNG = NG >= 8 ? 3 : NG >= 4 ? 2 : NG >= 2 ? 1 : 0;
+  constexpr int LOGW = W >= 4 ? 2 : W >= 2 ? 1 : 0;
+  constexpr int GW = NG / W;  // groups per wave after the transpose
+  static_assert(W == 1 || (NG % W == 0 && (NG & (NG - 1)) == 0), "NG must be a power of two >= W when W > 1");
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int rsub = wv / W, wr = wv % W;
   const int cl = lane & 15, q = lane >> 4;
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * RPB + rsub;
+  const bool valid = row < M;
+  // Butterfly over channel bit `bit` is needed when bit < log2(b); FULL means
+  // b = K (every stage, no branches).
+  auto need = [&](int bit) { return FULL || bit < logb; };
+
+  // Element (g, e) of this lane is channel ((wr * NG + g) * 16 + cl) * 32 + 8q + e.
+  rv8h cur[NG];
+  {
+    const uint16_t* xr = X + (valid ? row : 0) * ldx + (wr * NG * 16 + cl) * 32 + 8 * q;
+#pragma unroll
+    for (int g = 0; g < NG; ++g) cur[g] = valid ? *reinterpret_cast<const rv8h*>(xr + g * 512) : rv8h{};
+  }
   rv8h a1, a2;
   hadamard_frags(lane, a1, a2);
 
-  // Element (g, e) of this lane is channel ((wr * NG + g) * 16 + cl) * 32 + 8q + e.
-  auto load = [&](int64_t row, rv8h (&f)[NG]) {
-    const uint16_t* xr = X + row * ldx + (wr * NG * 16 + cl) * 32 + 8 * q;
+  // H_32 on the matrix cores.
+  float v[NG][8];
 #pragma unroll
-    for (int g = 0; g < NG; ++g) f[g] = *reinterpret_cast<const rv8h*>(xr + g * 512);
-  };
-  const int64_t step = static_cast<int64_t>(gridDim.x) * RPB;
-  // The transform of one row from its fp16 fragments (everything after the loads).
-  auto process = [&](const int64_t row, const bool valid, rv8h (&cur)[NG]) {
-    // H_32 on the matrix cores.
-    float v[NG][8];
+  for (int g = 0; g < NG; ++g) {
+    const rv4f d1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, cur[g], rv4f{0, 0, 0, 0}, 0, 0, 0);
+    const rv4f d2 = __builtin_amdgcn_mfma_f32_16x16x32_f16(a2, cur[g], rv4f{0, 0, 0, 0}, 0, 0, 0);
 #pragma unroll
-    for (int g = 0; g < NG; ++g) {
-      const rv4f d1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, cur[g], rv4f{0, 0, 0, 0}, 0, 0, 0);
-      const rv4f d2 = __builtin_amdgcn_mfma_f32_16x16x32_f16(a2, cur[g], rv4f{0, 0, 0, 0}, 0, 0, 0);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        v[g][r] = d1[r];
-        v[g][4 + r] = d2[r];
-      }
+    for (int r = 0; r < 4; ++r) {
+      v[g][r] = d1[r];
+      v[g][4 + r] = d2[r];
     }
-    // Channel bits 5..8: chunk bits 0..3 = lane bits 0..3.
-    if (logb > 5) rqd::lane_stage<1>(v, lane);
-    if (logb > 6) rqd::lane_stage<2>(v, lane);
-    if (logb > 7) rqd::lane_stage<4>(v, lane);
-    if (logb > 8) rqd::lane_stage<8>(v, lane);
-    // Channel bits 9..: group index g in registers.
+  }
+  // Channel bits 5..8: chunk bits 0..3 = lane bits 0..3.
+  if (need(5)) rqd::lane_stage<1>(v, lane);
+  if (need(6)) rqd::lane_stage<2>(v, lane);
+  if (need(7)) rqd::lane_stage<4>(v, lane);
+  if (need(8)) rqd::lane_stage<8>(v, lane);
+  // Channel bits 9 .. 9 + log2(NG) - 1: group index g in registers.
 #pragma unroll
-    for (int t = 0; t < 5; ++t) {
-      constexpr int dummy = 0;
-      (void)dummy;
-      const int h = 1 << t;
-      if (h < NG && 9 + t < logb) {
+  for (int t = 0; t < LOGNG + 1; ++t) {
+    const int h = 1 << t;
+    if (h < NG && need(9 + t)) {
 #pragma unroll
-        for (int g = 0; g < NG; ++g)
-          if ((g & h) == 0 && g + h < NG)
+      for (int g = 0; g < NG; ++g)
+        if ((g & h) == 0 && g + h < NG)
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              const float x0 = v[g][e], x1 = v[g + h][e];
-              v[g][e] = x0 + x1;
-              v[g + h][e] = x0 - x1;
-            }
-      }
-    }
-    // Wave bits (rows wider than one wave): exchange through LDS.
-    if constexpr (W > 1) {
-      constexpr int LOGNG = NG >= 8 ? 3 : NG >= 4 ? 2 : NG >= 2 ? 1 : 0;
-      const int wbit0 = 9 + LOGNG;
-      const int ws = min(max(logb - wbit0, 0), W == 4 ? 2 : 1);
-      __syncthreads();  // the previous row's LDS reads are done
-      if (ws > 0) {
-        float* mine = lds + (static_cast<int64_t>(wv) * NG * 64 + lane) * 8;
-#pragma unroll
-        for (int g = 0; g < NG; ++g) {
-          float4* d = reinterpret_cast<float4*>(mine + g * 64 * 8);
-          d[0] = make_float4(v[g][0], v[g][1], v[g][2], v[g][3]);
-          d[1] = make_float4(v[g][4], v[g][5], v[g][6], v[g][7]);
-        }
-      }
-      __syncthreads();
-      if (ws > 0) {
-        const int nw = 1 << ws;
-        const int wlow = wr & (nw - 1), wbase = wr & ~(nw - 1);
-#pragma unroll
-        for (int g = 0; g < NG; ++g) {
-          float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-          for (int u = 0; u < nw; ++u) {
-            const float sg = (__popc(wlow & u) & 1) ? -1.0f : 1.0f;
-            const float* src = lds + ((static_cast<int64_t>(rsub * W + (wbase | u)) * NG + g) * 64 + lane) * 8;
-            const float4 p0 = reinterpret_cast<const float4*>(src)[0];
-            const float4 p1 = reinterpret_cast<const float4*>(src)[1];
-            acc[0] = fmaf(sg, p0.x, acc[0]); acc[1] = fmaf(sg, p0.y, acc[1]);
-            acc[2] = fmaf(sg, p0.z, acc[2]); acc[3] = fmaf(sg, p0.w, acc[3]);
-            acc[4] = fmaf(sg, p1.x, acc[4]); acc[5] = fmaf(sg, p1.y, acc[5]);
-            acc[6] = fmaf(sg, p1.z, acc[6]); acc[7] = fmaf(sg, p1.w, acc[7]);
+          for (int e = 0; e < 8; ++e) {
+            const float x0 = v[g][e], x1 = v[g + h][e];
+            v[g][e] = x0 + x1;
+            v[g + h][e] = x0 - x1;
           }
-#pragma unroll
-          for (int e = 0; e < 8; ++e) v[g][e] = acc[e];
-        }
-      }
     }
-
-    // Row maximum: lanes, then the W waves of the row.
-    float amax = 0.0f;
-#pragma unroll
-    for (int g = 0; g < NG; ++g)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf(v[g][e]));
-    amax = fmaxf(amax, rqd::lane_xor<1>(amax));
-    amax = fmaxf(amax, rqd::lane_xor<2>(amax));
-    amax = fmaxf(amax, rqd::lane_xor<4>(amax));
-    amax = fmaxf(amax, rqd::lane_xor<8>(amax));
-    amax = fmaxf(amax, rqd::lane_xor<16>(amax));
-    amax = fmaxf(amax, __shfl_xor(amax, 32, 64));
-    if constexpr (W > 1) {
-      if (lane == 0) red[wv] = amax;
-      __syncthreads();
-      amax = red[rsub * W];
-#pragma unroll
-      for (int u = 1; u < W; ++u) amax = fmaxf(amax, red[rsub * W + u]);
-    }
-
-    const float a_z = amax * s_over_sqrtb;
-    const float delta = a_z / 7.0f;
-    const float gm = delta > 0.0f ? s_over_sqrtb / delta : 0.0f;
-    if (valid && wr == 0 && lane == 0) xs[row] = delta / s_t;
-    if (!valid) return;
-    if (ratio != nullptr) {
+  }
+  // Register slot s holds channel group G(s) (units of 512 channels):
+  // G = wr * NG + s without the wave transpose, and with it (s = gi * W + u)
+  // G = u * NG + wr * GW + gi.
+  const int wbit0 = 9 + LOGNG;
+  const bool xpose = W > 1 && need(wbit0);
+  if constexpr (W > 1) {
+    if (xpose) {
+      float4* mine = xch + static_cast<int64_t>(wv) * NG * 128 + lane;
 #pragma unroll
       for (int g = 0; g < NG; ++g) {
-        float* rr = ratio + row * K + ((wr * NG + g) * 16 + cl) * 32 + 8 * q;
-        reinterpret_cast<float4*>(rr)[0] = make_float4(v[g][0] * gm, v[g][1] * gm, v[g][2] * gm, v[g][3] * gm);
-        reinterpret_cast<float4*>(rr)[1] = make_float4(v[g][4] * gm, v[g][5] * gm, v[g][6] * gm, v[g][7] * gm);
+        mine[g * 128] = make_float4(v[g][0], v[g][1], v[g][2], v[g][3]);
+        mine[g * 128 + 64] = make_float4(v[g][4], v[g][5], v[g][6], v[g][7]);
       }
-      return;
-    }
-    uint8_t* qr = Xq + row * (K / 2);
+      __syncthreads();
 #pragma unroll
-    for (int g = 0; g < NG; ++g) {
-      uint32_t b[8];
+      for (int gi = 0; gi < GW; ++gi)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) b[e] = __float_as_uint(fmaf(v[g][e], gm, rqd::kRoundMagic));
-      *reinterpret_cast<uint32_t*>(qr + ((wr * NG + g) * 16 + cl) * 16 + 4 * q) = rqd::pack8(b);
-    }
-  };
-  {
-    // One row in flight ahead of the one being transformed.
-    rv8h nxt[NG];
-    const int64_t r0 = static_cast<int64_t>(blockIdx.x) * RPB + rsub;
-    if (r0 < M) load(r0, nxt);
-    for (int64_t base = static_cast<int64_t>(blockIdx.x) * RPB; base < M; base += step) {
-      const int64_t row = base + rsub;
-      const bool valid = row < M;
-      rv8h cur[NG];
+        for (int u = 0; u < W; ++u) {
+          const float4* src = xch + static_cast<int64_t>((rsub * W + u) * NG + wr * GW + gi) * 128 + lane;
+          const float4 p0 = src[0], p1 = src[64];
+          float* d = v[gi * W + u];
+          d[0] = p0.x; d[1] = p0.y; d[2] = p0.z; d[3] = p0.w;
+          d[4] = p1.x; d[5] = p1.y; d[6] = p1.z; d[7] = p1.w;
+        }
+      // Wave bits in registers: slot bits 0 .. log2(W) - 1 are u.
 #pragma unroll
-      for (int g = 0; g < NG; ++g) cur[g] = valid ? nxt[g] : rv8h{};
-      if (row + step < M) load(row + step, nxt);
-      process(row, valid, cur);
+      for (int t = 0; t < LOGW; ++t) {
+        const int h = 1 << t;
+        if (need(wbit0 + t)) {
+#pragma unroll
+          for (int s = 0; s < NG; ++s)
+            if ((s & h) == 0)
+#pragma unroll
+              for (int e = 0; e < 8; ++e) {
+                const float x0 = v[s][e], x1 = v[s + h][e];
+                v[s][e] = x0 + x1;
+                v[s + h][e] = x0 - x1;
+              }
+        }
+      }
     }
+  }
+
+  // Row maximum: registers, lanes, then the W waves of the row.
+  float amax = 0.0f;
+#pragma unroll
+  for (int g = 0; g < NG; ++g)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf(v[g][e]));
+  amax = fmaxf(amax, rqd::lane_xor<1>(amax));
+  amax = fmaxf(amax, rqd::lane_xor<2>(amax));
+  amax = fmaxf(amax, rqd::lane_xor<4>(amax));
+  amax = fmaxf(amax, rqd::lane_xor<8>(amax));
+  amax = fmaxf(amax, rqd::lane_xor<16>(amax));
+  amax = fmaxf(amax, __shfl_xor(amax, 32, 64));
+  if constexpr (W > 1) {
+    if (lane == 0) red[wv] = amax;
+    __syncthreads();
+    amax = red[rsub * W];
+#pragma unroll
+    for (int u = 1; u < W; ++u) amax = fmaxf(amax, red[rsub * W + u]);
+  }
+
+  const float a_z = amax * s_over_sqrtb;
+  const float delta = a_z / 7.0f;
+  const float gm = delta > 0.0f ? s_over_sqrtb / delta : 0.0f;
+  if (!valid) return;
+  if (wr == 0 && lane == 0) xs[row] = delta / s_t;
+  auto group_of = [&](int s) { return xpose ? (s % W) * NG + wr * GW + s / W : wr * NG + s; };
+  if (ratio != nullptr) {
+#pragma unroll
+    for (int s = 0; s < NG; ++s) {
+      float* rr = ratio + row * K + (group_of(s) * 16 + cl) * 32 + 8 * q;
+      reinterpret_cast<float4*>(rr)[0] = make_float4(v[s][0] * gm, v[s][1] * gm, v[s][2] * gm, v[s][3] * gm);
+      reinterpret_cast<float4*>(rr)[1] = make_float4(v[s][4] * gm, v[s][5] * gm, v[s][6] * gm, v[s][7] * gm);
+    }
+    return;
+  }
+  uint8_t* qr = Xq + row * (K / 2);
+#pragma unroll
+  for (int s = 0; s < NG; ++s) {
+    uint32_t b[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) b[e] = __float_as_uint(fmaf(v[s][e], gm, rqd::kRoundMagic));
+    *reinterpret_cast<uint32_t*>(qr + (group_of(s) * 16 + cl) * 16 + 4 * q) = rqd::pack8(b);
   }
 }
 
@@ -256,17 +255,19 @@ int rq_mfma_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_blo
   const int logb = ilog2(had_block);
   const float s_over_sqrtb = static_cast<float>(static_cast<double>(s_t) / std::sqrt(static_cast<double>(had_block)));
   const int rpb = 4 / w;
-  const size_t lds = w > 1 ? static_cast<size_t>(4) * ng * 64 * 8 * sizeof(float) : 0;
-  // Persistent workgroups: enough to fill every CU several times over.
-  const int64_t want = (M + rpb - 1) / rpb;
-  const int64_t cap = w > 1 ? 512 : 1024;
-  const unsigned grid = static_cast<unsigned>(want < cap ? want : cap);
+  const size_t lds = w > 1 ? static_cast<size_t>(4) * ng * 128 * sizeof(float4) : 0;
+  // One row per wave (W = 1) or per workgroup (W > 1).
+  const unsigned grid = static_cast<unsigned>((M + rpb - 1) / rpb);
   const uint16_t* x = static_cast<const uint16_t*>(X);
-#define OQ_RQM(NG, W)                                                                                     \
-  if (ng == NG && w == W) {                                                                               \
-    hipLaunchKernelGGL((rq_mfma_kernel<NG, W>), dim3(grid), dim3(256), lds, stream, x, M, ldx, logb, s_t, \
-                       s_over_sqrtb, Xq, x_scale, ratio);                                                 \
-    return launch_status();                                                                               \
+#define OQ_RQM(NG, W)                                                                                         \
+  if (ng == NG && w == W) {                                                                                   \
+    if (had_block == K)                                                                                       \
+      hipLaunchKernelGGL((rq_mfma_kernel<NG, W, true>), dim3(grid), dim3(256), lds, stream, x, M, ldx, logb,  \
+                         s_t, s_over_sqrtb, Xq, x_scale, ratio);                                              \
+    else                                                                                                      \
+      hipLaunchKernelGGL((rq_mfma_kernel<NG, W, false>), dim3(grid), dim3(256), lds, stream, x, M, ldx, logb, \
+                         s_t, s_over_sqrtb, Xq, x_scale, ratio);                                              \
+    return launch_status();                                                                                   \
   }
   OQ_RQM(1, 1)
   OQ_RQM(2, 1)
@@ -314,7 +315,7 @@ int rq_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block, f
               float* x_scale, float* ratio, hipStream_t stream) {
   if (M == 0) return OQ_OK;
   int ng = 0, w = 0;
-  if (had_block >= 32 && rq_mfma_shape(K, &ng, &w) && !std::getenv("OQ_RQ_VALU"))
+  if (had_block >= 32 && rq_mfma_shape(K, &ng, &w))
     return rq_mfma_launch(X, M, K, ldx, had_block, s_t, Xq, x_scale, ratio, stream);
   RQPlan p;
   rq_plan(K, &p);

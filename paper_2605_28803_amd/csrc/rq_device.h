@@ -162,18 +162,17 @@ __device__ __forceinline__ void load_row_f16(float (&v)[C][8], const uint16_t* _
   }
 }
 
-// Pack eight codes, given as the bit patterns of (ratio + 1.5*2^23) (low
-// nibble = two's-complement code), into one dword: channel j in bits 4j..4j+3.
+// Pack eight codes, given as the bit patterns of (ratio + 1.5*2^23), into one
+// dword: channel j in bits 4j..4j+3.  The low byte of each pattern is the code
+// as a two's-complement byte (the constant's low byte is zero, |code| <= 7).
 __device__ __forceinline__ uint32_t pack8(const uint32_t (&b)[8]) {
-  // Low bytes of four patterns -> one dword of four bytes.
-  const uint32_t x0 = __builtin_amdgcn_perm(__builtin_amdgcn_perm(b[3], b[2], 0x04000c0cu),
-                                            __builtin_amdgcn_perm(b[1], b[0], 0x0c0c0400u), 0x07060100u);
-  const uint32_t x1 = __builtin_amdgcn_perm(__builtin_amdgcn_perm(b[7], b[6], 0x04000c0cu),
-                                            __builtin_amdgcn_perm(b[5], b[4], 0x0c0c0400u), 0x07060100u);
-  // Two nibbles per byte, then keep bytes 0 and 2 of each.
-  const uint32_t y0 = x0 & 0x0F0F0F0Fu, y1 = x1 & 0x0F0F0F0Fu;
-  const uint32_t z0 = y0 | (y0 >> 4), z1 = y1 | (y1 >> 4);
-  return __builtin_amdgcn_perm(z1, z0, 0x06040200u);
+  // Low bytes of the even channels -> e = [b0 b2 b4 b6], odd -> o = [b1 b3 b5 b7].
+  const uint32_t e = __builtin_amdgcn_perm(__builtin_amdgcn_perm(b[6], b[4], 0x04000c0cu),
+                                           __builtin_amdgcn_perm(b[2], b[0], 0x0c0c0400u), 0x07060100u);
+  const uint32_t o = __builtin_amdgcn_perm(__builtin_amdgcn_perm(b[7], b[5], 0x04000c0cu),
+                                           __builtin_amdgcn_perm(b[3], b[1], 0x0c0c0400u), 0x07060100u);
+  // Byte i = code(2i) in the low nibble, code(2i+1) in the high nibble.
+  return (e & 0x0F0F0F0Fu) | ((o << 4) & 0xF0F0F0F0u);
 }
 
 // The rest of the fused pass once the row's fp32 values are in registers:
