@@ -25,6 +25,12 @@ CASES = [
     (19, 2048, 2048, 1.0), (50, 4096, 4096, 0.6), (11, 6144, 2048, 3.9), (13, 8192, 8192, 1.0),
     (9, 16384, 16384, 1.3), (4, 16384, 64, 1.0), (5, 4096, 64, 1.0), (6, 12288, 4096, 1.0),
     (129, 2048, 256, 1.0),
+    # rows spanning 2 or 4 waves with a partial block: transpose with one
+    # wave stage, no transpose, and odd M (a half-valid workgroup)
+    (7, 16384, 8192, 1.0), (5, 8192, 4096, 1.0), (3, 16384, 1024, 1.5), (257, 8192, 8192, 0.7),
+    (301, 16384, 16384, 2.0), (1000, 4096, 4096, 1.0), (999, 1024, 256, 1.0),
+    # more rows than one round of resident workgroups
+    (6000, 4096, 4096, 1.0), (6001, 4096, 1024, 1.3), (1100, 8192, 8192, 1.0), (1030, 16384, 16384, 0.9),
 ]
 
 
@@ -122,3 +128,27 @@ def test_device_weight_quantization_matches_oracle():
     tau = parity.tau_rows(W.astype(np.float64), 1024)
     parity.check_codes(parity.unpack_int4(Wq.cpu().numpy()), q_o, r_o, tau)
     assert np.allclose(ws.cpu().numpy(), ws_o, rtol=1e-5)
+
+
+@pytest.mark.parametrize("M,K", [(16384, 16384), (16384, 4096), (65536, 1024)])
+def test_rotate_quantize_full_size_sampled(M, K):
+    """Full-size launch (the prefill / sweep shapes, b = K); sampled rows
+    against the oracle on the same fp16 input."""
+    print(f"rq full-size M={M} K={K}", flush=True)
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev).manual_seed(M + K)
+    X = torch.randn((M, K), generator=g, device=dev, dtype=torch.float32)
+    ch = torch.randperm(K, generator=g, device=dev)[: max(1, K // 100)]
+    X[:, ch] *= 50.0
+    X = X.half()
+    Xq, xs = oq.rotate_quantize_act(X, K)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([np.random.default_rng(K).choice(M, 48, replace=False), [0, M - 1]]))
+    x16 = X[torch.from_numpy(rows).to(dev)].cpu().numpy()
+    q_o, xs_o, r_o = quant.rotate_quantize_act(x16.astype(np.float64), K, 1.0)
+    tau = parity.tau_rows(x16.astype(np.float64), K)
+    q = parity.unpack_int4(Xq[torch.from_numpy(rows).to(dev)].cpu().numpy())
+    n_mis, _ = parity.check_codes(q, q_o, r_o, tau)
+    xs_g = xs[torch.from_numpy(rows).to(dev)].cpu().numpy().astype(np.float64)
+    assert np.all(np.abs(xs_g - xs_o) <= (tau / 7 + 4 * parity.U32) * xs_o)
+    print(f"  sampled {len(rows)} rows: mismatches={n_mis}")

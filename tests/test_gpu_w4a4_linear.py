@@ -110,3 +110,80 @@ def test_full_rotated_linear_1024():
     # Information: the quantized layer approximates the unrotated fp64 product.
     exact = (inp["x"] @ inp["u"].T) @ inp["w"].T
     print(f"  W4A4 vs exact fp64 rel_l2={parity.rel_l2(y, exact):.3e}")
+
+
+def _random_packed(R, K, gen):
+    """Packed int4 codes uniform in [-7, 7], generated on the device."""
+    u = torch.randint(0, 15, (R, K), generator=gen, device=DEV, dtype=torch.int16) - 7
+    n = (u & 0xF).to(torch.uint8)
+    return (n[:, 0::2] | (n[:, 1::2] << 4)).contiguous()
+
+
+@pytest.mark.parametrize("M,N,K", [(16384, 16384, 16384), (4096, 8192, 8192), (816, 32768, 2048)])
+def test_gemm_full_size_sampled(M, N, K):
+    """Full-size launches (the prefill / sweep shapes and the launch bench.py
+    times): sampled rows x sampled columns of the i32 accumulators bit-exact,
+    and of the fp16 epilogue within 2e-3, against the oracle on the same codes."""
+    print(f"gemm full-size M={M} N={N} K={K}", flush=True)
+    gen = torch.Generator(device=DEV).manual_seed(M ^ N ^ K)
+    Xq, Wq = _random_packed(M, K, gen), _random_packed(N, K, gen)
+    xs = torch.rand(M, generator=gen, device=DEV) * 0.1 + 0.01
+    ws = torch.rand(N, generator=gen, device=DEV) * 1e-3 + 1e-4
+    rng = np.random.default_rng(K)
+    rows = np.unique(np.concatenate([rng.choice(M, 24, replace=False), [0, M - 1]]))
+    cols = np.unique(np.concatenate([rng.choice(N, 256, replace=False), [0, N - 1]]))
+    q = parity.unpack_int4(Xq[torch.from_numpy(rows).to(DEV)].cpu().numpy())
+    qw = parity.unpack_int4(Wq[torch.from_numpy(cols).to(DEV)].cpu().numpy())
+    ref = linear.int_gemm(q, qw)
+    acc = oq.w4a4_gemm_i32(Xq, Wq)
+    torch.cuda.synchronize()
+    a = acc[torch.from_numpy(rows).to(DEV)][:, torch.from_numpy(cols).to(DEV)].cpu().numpy()
+    del acc
+    assert np.array_equal(a.astype(np.int64), ref)
+    Y = oq.w4a4_linear(Xq, xs, Wq, ws)
+    torch.cuda.synchronize()
+    y = Y[torch.from_numpy(rows).to(DEV)][:, torch.from_numpy(cols).to(DEV)].float().cpu().numpy()
+    yref = linear.dequant(ref, xs.cpu().numpy()[rows].astype(np.float64), ws.cpu().numpy()[cols].astype(np.float64))
+    err = parity.rel_l2(y, yref)
+    print(f"  sampled {len(rows)}x{len(cols)}: i32 exact, fp16 rel_l2={err:.2e}")
+    assert err <= parity.REL_L2_OUT
+
+
+@pytest.mark.parametrize("name,K,N", configs.PREFILL_GEMMA.linears())
+def test_prefill_layer_linears(name, K, N):
+    """Backbone prefill, Gemma-2B shaped (816 tokens; q|k|v 2048 -> 2560,
+    o 2048 -> 2048, gate|up 2048 -> 32768, down 16384 -> 2048; activations with
+    0.5% outlier channels x30; W ~ N(0, 0.02^2); b = K): device weight codes
+    against the oracle's (boundary rule), activation codes of sampled rows, and
+    the sampled rows' outputs against the oracle fed the GPU's codes."""
+    from workloads import generators as G
+    cfg = configs.PREFILL_GEMMA
+    M = cfg.tokens
+    print(f"prefill {name}: M={M} K={K} N={N}", flush=True)
+    x = G.gaussian(cfg.seed, f"prefill/{name}/x", (M, K))
+    x[:, G.outlier_channels(cfg.seed, f"prefill/{name}/x", K, int(round(cfg.outlier_frac * K)))] *= cfg.outlier_factor
+    x16 = x.astype(np.float16)
+    w16 = G.gaussian(cfg.seed, f"prefill/{name}/w", (N, K), cfg.w_std).astype(np.float16)
+    Wq, ws = oq.quantize_weights(torch.from_numpy(w16).to(DEV), K)
+    Xq, xs = oq.rotate_quantize_act(torch.from_numpy(x16).to(DEV), K)
+    Y = oq.w4a4_linear(Xq, xs, Wq, ws)
+    torch.cuda.synchronize()
+    # Weight codes (every row).
+    qw_o, ws_o, rw_o = quant.quantize_weights(w16.astype(np.float64), K)
+    qw_g = parity.unpack_int4(Wq.cpu().numpy())
+    parity.check_codes(qw_g, qw_o, rw_o, parity.tau_rows(w16.astype(np.float64), K))
+    assert np.allclose(ws.cpu().numpy(), ws_o, rtol=1e-5)
+    # Activation codes and outputs of sampled rows.
+    rows = np.unique(np.concatenate([np.random.default_rng(N).choice(M, 32, replace=False), [M - 1]]))
+    xr = x16[rows].astype(np.float64)
+    q_o, xs_o, r_o = quant.rotate_quantize_act(xr, K, 1.0)
+    q_g = parity.unpack_int4(Xq.cpu().numpy()[rows])
+    parity.check_codes(q_g, q_o, r_o, parity.tau_rows(xr, K))
+    xs_g = xs.cpu().numpy()[rows].astype(np.float64)
+    yref = linear.dequant(linear.int_gemm(q_g, qw_g), xs_g, ws.cpu().numpy().astype(np.float64))
+    err = parity.rel_l2(Y.float().cpu().numpy()[rows], yref)
+    # The independent pipeline (oracle codes and scales throughout), reported.
+    y_ind = linear.dequant(linear.int_gemm(q_o, qw_o), xs_o, ws_o)
+    print(f"  rel_l2 vs oracle on GPU codes {err:.2e}; vs independent oracle "
+          f"{parity.rel_l2(Y.float().cpu().numpy()[rows], y_ind):.2e}")
+    assert err <= parity.REL_L2_OUT
