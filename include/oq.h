@@ -199,9 +199,26 @@ int oq_quantize_weights_host(const double* W_u, int64_t N, int64_t K, int32_t ha
  *     r  += m.gt2 * W4A4(a; Wd, s[3])
  *   v   = fp16(rms(r) * g_f) . W_out^T + b_out ;  x_{t+1} = x_t + dt * v
  *
- * rms(r) = r / sqrt(mean(r^2) + 1e-6), dt = -1/steps, the Hadamard block of a
- * linear is the largest power of two dividing its input size.
- * Only OQ_DIT_PI is implemented by this version; OQ_DIT_GR00T is reserved.
+ * Arch OQ_DIT_GR00T (GR00T-N1.5 DiT; the Appendix on per-step scaling names
+ * AdaLayerNorm -> attention q/k/v -> ... -> LayerNorm -> ff.net[0] -> GELU ->
+ * ff.net[2]):
+ *
+ *   per block l, step t (m = mod[l][t], s = s_table[l][t]):
+ *     h   = fp16(ln(r) * g1 * (1 + m.sc1) + m.sh1)           AdaLayerNorm
+ *     even l (cross-attention):  q = fp16(W4A4(h; Wq, s[0])),
+ *            k|v = fp16(W4A4(cond; Wkv, 1)) per sample, from
+ *            oq_dit_set_condition (step-invariant, computed once)
+ *     odd l (self-attention):    q|k|v = fp16(W4A4(h; Wqkv, s[0]))
+ *     o   = fp16(softmax(q k^T / sqrt(hd)) v) per head and sample
+ *     r  += W4A4(o; Wo, s[1])
+ *     h2  = fp16(ln(r) * g2 + b2)                            LayerNorm
+ *     f   = fp16(gelu_tanh(W4A4(h2; Wff0, s[2])))
+ *     r  += W4A4(f; Wff2, s[3])
+ *   v   = fp16(ln(r) * g_f) . W_out^T + b_out ;  x_{t+1} = x_t + dt * v
+ *
+ * rms(r) = r / sqrt(mean(r^2) + 1e-6), ln(r) = (r - mean) / sqrt(var + 1e-6),
+ * dt = -1/steps (pi, tau 1 -> 0) or +1/steps (gr00t, tau 0 -> 1), the Hadamard
+ * block of a linear is the largest power of two dividing its input size.
  */
 typedef enum { OQ_DIT_PI = 0, OQ_DIT_GR00T = 1 } oq_dit_arch;
 
@@ -211,9 +228,10 @@ typedef struct {
   int32_t hidden;      /* D, multiple of 64; = n_heads * head_dim           */
   int32_t mlp;         /* F, multiple of 64                                  */
   int32_t n_heads;
-  int32_t head_dim;    /* <= 128, multiple of 8                              */
-  int32_t tokens;      /* S action tokens per sample                         */
-  int32_t prefix;      /* P prefix tokens per sample (keys before the S own) */
+  int32_t head_dim;    /* <= 128, multiple of 16                             */
+  int32_t tokens;      /* S action tokens per sample, <= 64                  */
+  int32_t prefix;      /* pi: P prefix tokens per sample (keys before the S
+                          own); gr00t: P conditioning tokens per sample      */
   int32_t batch;       /* B samples                                          */
   int32_t steps;       /* T denoising steps                                  */
   int32_t action_dim;  /* A, multiple of 8                                   */
@@ -230,12 +248,16 @@ typedef struct {
 typedef struct {
   const void* g1;          /* [D] norm gain before attention                   */
   const void* g2;          /* [D] norm gain before the MLP                     */
-  oq_qweight qkv;          /* N = 3D, K = D                                    */
+  oq_qweight qkv;          /* pi and odd gr00t blocks: q|k|v, N = 3D, K = D;
+                              even gr00t blocks: q only, N = D, K = D          */
   oq_qweight o;            /* N = D,  K = D                                    */
-  oq_qweight gate_up;      /* N = 2F, K = D                                    */
+  oq_qweight gate_up;      /* pi: gate|up, N = 2F; gr00t: ff0, N = F; K = D    */
   oq_qweight down;         /* N = D,  K = F                                    */
-  const void* prefix_k;    /* [B][P][D] fp16, step-invariant                   */
-  const void* prefix_v;    /* [B][P][D] fp16                                   */
+  const void* prefix_k;    /* pi: [B][P][D] fp16, step-invariant; gr00t: NULL  */
+  const void* prefix_v;    /* pi: [B][P][D] fp16; gr00t: NULL                  */
+  const void* b2;          /* gr00t: [D] LayerNorm bias before the MLP; pi: NULL */
+  oq_qweight cross_kv;     /* even gr00t blocks: k|v of the conditioning
+                              tokens, N = 2D, K = D; otherwise NULL            */
 } oq_dit_block;
 
 typedef struct {
@@ -245,8 +267,9 @@ typedef struct {
   const void* b_out;       /* fp16 [A]                                         */
   const void* g_f;         /* fp16 [D] final norm gain                         */
   const oq_dit_block* blocks; /* host array [n_blocks], copied by oq_dit_create */
-  const void* mod;         /* fp16 device [n_blocks][steps][6][D]:
-                              sc1, sh1, gt1, sc2, sh2, gt2                      */
+  const void* mod;         /* fp16 device [n_blocks][steps][NM][D] per-step
+                              modulation; pi: NM = 6 (sc1, sh1, gt1, sc2, sh2,
+                              gt2), gr00t: NM = 2 (sc1, sh1)                   */
   const float* s_table;    /* host fp32 [n_blocks][steps][4], copied           */
 } oq_dit_weights;
 
@@ -263,7 +286,18 @@ int oq_dit_create(const oq_dit_config* cfg, const oq_dit_weights* w, oq_dit** ou
  * oq_dit_workspace_bytes).  Errors: OQ_ERR_NULL, OQ_ERR_WORKSPACE, OQ_ERR_ALIGN. */
 int oq_dit_set_workspace(oq_dit* h, void* workspace, size_t bytes);
 
-/* One Euler step t (0 <= t < steps) on x (device fp32 [B][S][A], in place). */
+/* gr00t: compute every cross-attention block's conditioning k|v from cond
+ * (device fp16 [B][P][D], read during the call only) into the workspace:
+ * rotate-quantize with s = 1 and the W4A4 k|v linear, once per conditioning
+ * input (it does not depend on the step).  Required before the first step
+ * of a gr00t handle and again whenever the conditioning or the workspace
+ * changes.  Errors: OQ_ERR_NULL, OQ_ERR_WORKSPACE, OQ_ERR_ARG (pi handle),
+ * OQ_ERR_HIP. */
+int oq_dit_set_condition(oq_dit* h, const void* cond, void* stream);
+
+/* One Euler step t (0 <= t < steps) on x (device fp32 [B][S][A], in place).
+ * Errors: OQ_ERR_NULL, OQ_ERR_WORKSPACE, OQ_ERR_ARG (bad t, or a gr00t handle
+ * without a condition), OQ_ERR_HIP. */
 int oq_dit_step(oq_dit* h, float* x, int32_t t, void* stream);
 
 /* n_steps consecutive steps t = 0 .. n_steps-1 on x, in place. */
@@ -279,14 +313,16 @@ int oq_dit_run_block(oq_dit* h, int32_t l, int32_t t, float* resid, void* stream
  * compared with the oracle fed the GPU's own upstream values.  Pointers into
  * the workspace, valid until the next call on the handle. */
 typedef struct {
-  const void* h1;        /* [M][D]  norm output, input of the q|k|v linear      */
-  const void* qkv;       /* [M][3D] q|k|v linear output                          */
+  const void* h1;        /* [M][D]  norm output, input of the q|k|v (q) linear  */
+  const void* qkv;       /* [M][3D] q|k|v linear output (gr00t even: q, [M][D]) */
   const void* attn;      /* [M][D]  attention output, input of the o linear      */
-  const void* h2;        /* [M][D]  norm output, input of the gate|up linear     */
-  const void* gate_up;   /* [M][2F] gate|up linear output                        */
-  const void* act;       /* [M][F]  gelu(gate) * up, input of the down linear    */
+  const void* h2;        /* [M][D]  norm output, input of the gate|up / ff0 linear */
+  const void* gate_up;   /* [M][2F] gate|up output (gr00t: ff0 output, [M][F])   */
+  const void* act;       /* [M][F]  input of the down / ff2 linear               */
   const float* resid;    /* [M][D]  fp32 residual of the last oq_dit_step after
                             its last block (oq_dit_run_block uses the caller's) */
+  const void* cond_kv;   /* gr00t: [n_blocks/2 rounded up][B*P][2D] k|v of the
+                            conditioning tokens per even block; pi: NULL       */
 } oq_dit_intermediates;
 
 /* Fill *out with the intermediate pointers.  Errors: OQ_ERR_NULL, OQ_ERR_WORKSPACE. */

@@ -21,7 +21,8 @@ class oq_qweight(C.Structure):
 
 class oq_dit_block(C.Structure):
     _fields_ = [("g1", vp), ("g2", vp), ("qkv", oq_qweight), ("o", oq_qweight),
-                ("gate_up", oq_qweight), ("down", oq_qweight), ("prefix_k", vp), ("prefix_v", vp)]
+                ("gate_up", oq_qweight), ("down", oq_qweight), ("prefix_k", vp), ("prefix_v", vp),
+                ("b2", vp), ("cross_kv", oq_qweight)]
 
 
 class oq_dit_weights(C.Structure):
@@ -30,7 +31,7 @@ class oq_dit_weights(C.Structure):
 
 
 class oq_dit_intermediates(C.Structure):
-    _fields_ = [(n, vp) for n in ("h1", "qkv", "attn", "h2", "gate_up", "act", "resid")]
+    _fields_ = [(n, vp) for n in ("h1", "qkv", "attn", "h2", "gate_up", "act", "resid", "cond_kv")]
 
 
 # name -> (restype, argtypes)
@@ -47,6 +48,7 @@ SIGNATURES = {
     "oq_dit_workspace_bytes": (i32, [C.POINTER(oq_dit_config), C.POINTER(C.c_size_t)]),
     "oq_dit_create": (i32, [C.POINTER(oq_dit_config), C.POINTER(oq_dit_weights), C.POINTER(vp)]),
     "oq_dit_set_workspace": (i32, [vp, vp, C.c_size_t]),
+    "oq_dit_set_condition": (i32, [vp, vp, vp]),
     "oq_dit_step": (i32, [vp, vp, i32, vp]),
     "oq_dit_denoise": (i32, [vp, vp, i32, vp]),
     "oq_dit_run_block": (i32, [vp, i32, i32, vp, vp]),

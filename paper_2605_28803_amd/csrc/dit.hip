@@ -26,9 +26,11 @@
 // per-site checks) and quantizes the same values.  A whole denoising step (or
 // several) is captured once into a HIP graph per (x, first step, count) on an
 // internal stream and replayed on the caller's stream.
+#include <algorithm>
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <type_traits>
 #include <vector>
 
 #include "common.h"
@@ -100,8 +102,10 @@ __global__ __launch_bounds__(256) void inproj_kernel(const float* __restrict__ x
   }
 }
 
-// h = fp16(rms(r) g (1 + sc) + sh), then rotate + quantize h.
-template <int C>
+// h = fp16(norm(r) g (1 + sc) + sh), then rotate + quantize h.  norm is the
+// RMS norm (LN = false) or the layer norm (LN = true); sc and sh may be null
+// (zero).
+template <int C, bool LN>
 __global__ __launch_bounds__(256) void norm_rq_kernel(const float* __restrict__ r, const uint16_t* __restrict__ g,
                                                       const uint16_t* __restrict__ sc,
                                                       const uint16_t* __restrict__ sh, uint16_t* __restrict__ h,
@@ -109,9 +113,10 @@ __global__ __launch_bounds__(256) void norm_rq_kernel(const float* __restrict__ 
   extern __shared__ float lds[];
   __shared__ float red[4];
   __shared__ float red2[4];
+  __shared__ float red3[4];
   const rqd::RowMap m = rqd::row_map(o.logT, M);
   float v[C][8];
-  float ss = 0.0f;
+  float sum = 0.0f;
   const float* rr = r + (m.valid ? m.row : 0) * D;
 #pragma unroll
   for (int c = 0; c < C; ++c) {
@@ -124,16 +129,28 @@ __global__ __launch_bounds__(256) void norm_rq_kernel(const float* __restrict__ 
     v[c][0] = p0.x; v[c][1] = p0.y; v[c][2] = p0.z; v[c][3] = p0.w;
     v[c][4] = p1.x; v[c][5] = p1.y; v[c][6] = p1.z; v[c][7] = p1.w;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) ss = fmaf(v[c][j], v[c][j], ss);
+    for (int j = 0; j < 8; ++j) sum += v[c][j];
   }
   float gg[C][8], s1[C][8], s2[C][8];
 #pragma unroll
   for (int c = 0; c < C; ++c) {
     const int k = rqd::chan(m, c, 0);
     load8_f16(g + k, gg[c]);
-    load8_f16(sc + k, s1[c]);
-    load8_f16(sh + k, s2[c]);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) s1[c][j] = s2[c][j] = 0.0f;
+    if (sc) load8_f16(sc + k, s1[c]);
+    if (sh) load8_f16(sh + k, s2[c]);
   }
+  float mu = 0.0f;
+  if constexpr (LN) mu = rqd::row_reduce<false>(sum, m, red3) / static_cast<float>(D);
+  float ss = 0.0f;
+#pragma unroll
+  for (int c = 0; c < C; ++c)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float d = v[c][j] - mu;
+      ss = fmaf(d, d, ss);
+    }
   ss = rqd::row_reduce<false>(ss, m, red2);
   const float inv = 1.0f / sqrtf(ss / static_cast<float>(D) + kEps);
 #pragma unroll
@@ -141,7 +158,7 @@ __global__ __launch_bounds__(256) void norm_rq_kernel(const float* __restrict__ 
     const int k = rqd::chan(m, c, 0);
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const float y = v[c][j] * inv * gg[c][j];
+      const float y = (v[c][j] - mu) * inv * gg[c][j];
       v[c][j] = f16r(fmaf(y, s1[c][j], y) + s2[c][j]);
     }
     if (m.valid) store8_f16(h + m.row * D + k, v[c]);
@@ -155,29 +172,30 @@ __device__ __forceinline__ float gelu_tanh(float x) {
   return 0.5f * x * (1.0f + tanhf(k0 * fmaf(k1 * x * x, x, x)));
 }
 
-// a = fp16(gelu_tanh(gate) up) from gu = [gate | up] (fp16 [M][2F]), then
-// rotate + quantize a.
-template <int C>
+// GATED: a = fp16(gelu_tanh(gate) up) from gu = [gate | up] (fp16 [M][2F]);
+// otherwise a = fp16(gelu_tanh(u)) from u (fp16 [M][F]).  Then rotate +
+// quantize a.
+template <int C, bool GATED>
 __global__ __launch_bounds__(256) void gelu_rq_kernel(const uint16_t* __restrict__ gu, uint16_t* __restrict__ act,
                                                       int64_t M, int F, RQOut o) {
   extern __shared__ float lds[];
   __shared__ float red[4];
   const rqd::RowMap m = rqd::row_map(o.logT, M);
   float v[C][8];
-  const uint16_t* gr = gu + (m.valid ? m.row : 0) * 2 * F;
+  const int64_t ld = GATED ? 2 * static_cast<int64_t>(F) : F;
+  const uint16_t* gr = gu + (m.valid ? m.row : 0) * ld;
 #pragma unroll
   for (int c = 0; c < C; ++c) {
     const int k = rqd::chan(m, c, 0);
     float ga[8], up[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) ga[j] = 0.0f, up[j] = 1.0f;
     if (m.valid) {
       load8_f16(gr + k, ga);
-      load8_f16(gr + F + k, up);
-    } else {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) ga[j] = up[j] = 0.0f;
+      if (GATED) load8_f16(gr + F + k, up);
     }
 #pragma unroll
-    for (int j = 0; j < 8; ++j) v[c][j] = f16r(gelu_tanh(ga[j]) * up[j]);
+    for (int j = 0; j < 8; ++j) v[c][j] = GATED ? f16r(gelu_tanh(ga[j]) * up[j]) : f16r(gelu_tanh(ga[j]));
     if (m.valid) store8_f16(act + m.row * F + k, v[c]);
   }
   rqd::rq_core<C>(v, m, F, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr);
@@ -185,7 +203,8 @@ __global__ __launch_bounds__(256) void gelu_rq_kernel(const uint16_t* __restrict
 
 struct AttnArgs {
   const uint16_t* q; int64_t q_ld;                      // [B*S][..], head h at column h*hd
-  const uint16_t* k_pre; const uint16_t* v_pre; int P;  // [B][P][D] (P may be 0)
+  const uint16_t* k_pre; const uint16_t* v_pre; int P;  // [B][P][pre_ld] (P may be 0)
+  int64_t pre_ld;
   const uint16_t* k_own; const uint16_t* v_own; int64_t own_ld; int own_keys;  // [B*S][..]
   float* part_o; float* part_ml;                        // [B*H][nsplit][S][hd], [B*H][nsplit][S][2]
   uint16_t* out; int64_t out_ld;
@@ -197,7 +216,9 @@ typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 
 // One (sample b, head h, 64-key split) on the fp16 matrix cores
-// (v_mfma_f32_16x16x32_f16).  Wave w owns query rows 16w .. 16w+15:
+// (v_mfma_f32_16x16x32_f16), ceil(S / 16) waves.  Wave w owns query rows
+// 16w .. 16w+15 (head_dim a multiple of 16; the q.k contraction is padded with
+// zeros to a multiple of 32):
 //   S = Q K^T (16 x 64, fp32), scaled; split maximum m and sum l per row;
 //   P = exp(S - m) (fp16, staged in LDS as the next A operand);
 //   O = P V (16 x hd, fp32) with V^T staged in LDS.
@@ -223,12 +244,13 @@ __global__ __launch_bounds__(256) void attn_partial_kernel(AttnArgs a) {
 
   auto key_ptr = [&](int j, const uint16_t* pre, const uint16_t* own) -> const uint16_t* {
     const int key = k0 + j;
-    if (key < a.P) return pre + (static_cast<int64_t>(b) * a.P + key) * a.D + h * hd;
+    if (key < a.P) return pre + (static_cast<int64_t>(b) * a.P + key) * a.pre_ld + h * hd;
     return own + (static_cast<int64_t>(b) * a.own_keys + (key - a.P)) * a.own_ld + h * hd;
   };
 
   // Stage V^T: thread (key j = tid % 64, dim group) loads 8 dims of one key.
-  for (int d8 = (tid >> 6) * 8; d8 < hd; d8 += 32) {
+  const int nwaves = static_cast<int>(blockDim.x >> 6);
+  for (int d8 = (tid >> 6) * 8; d8 < hd; d8 += 8 * nwaves) {
     const int j = tid & 63;
     uint4 raw = make_uint4(0, 0, 0, 0);
     if (j < nk) raw = *reinterpret_cast<const uint4*>(key_ptr(j, a.v_pre, a.v_own) + d8);
@@ -244,21 +266,23 @@ __global__ __launch_bounds__(256) void attn_partial_kernel(AttnArgs a) {
   const int qrow = 16 * w + (lane & 15);
   const bool qok = qrow < a.S;
   const int kq = 8 * (lane >> 4);
-  const int nkk = hd / 32;  // 32-wide k steps over the head dimension (hd % 32 == 0, <= 4)
+  const int nkk = (hd + 31) / 32;  // 32-wide k steps over the head dimension (zero-padded)
   constexpr int KKMAX = kMaxHeadDim / 32;
   // Issue every Q and K load of the wave before the first MFMA.
   v8h qa[KKMAX], kb[KKMAX][KS / 16];
 #pragma unroll
   for (int kk = 0; kk < KKMAX; ++kk) {
     qa[kk] = v8h{};
-    if (kk < nkk && qok)
+    const bool dok = kk * 32 + kq < hd;  // hd % 8 == 0: a chunk of 8 dims is wholly in or out
+    if (kk < nkk && qok && dok)
       qa[kk] = *reinterpret_cast<const v8h*>(a.q + (static_cast<int64_t>(b) * a.S + qrow) * a.q_ld + h * hd +
                                              kk * 32 + kq);
 #pragma unroll
     for (int nb = 0; nb < KS / 16; ++nb) {
       const int j = nb * 16 + (lane & 15);
       kb[kk][nb] = v8h{};
-      if (kk < nkk && j < nk) kb[kk][nb] = *reinterpret_cast<const v8h*>(key_ptr(j, a.k_pre, a.k_own) + kk * 32 + kq);
+      if (kk < nkk && j < nk && dok)
+        kb[kk][nb] = *reinterpret_cast<const v8h*>(key_ptr(j, a.k_pre, a.k_own) + kk * 32 + kq);
     }
   }
   v4f sc[KS / 16];
@@ -397,7 +421,9 @@ __global__ __launch_bounds__(256) void combine_rq_kernel(AttnArgs a, int64_t M, 
   rqd::rq_core<C>(v, m, a.D, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr);
 }
 
-// x[m][:] += dt * (fp16(rms(r[m]) g_f) W_out^T + b_out)
+// x[m][:] += dt * (fp16(norm(r[m]) g_f) W_out^T + b_out), norm = RMS norm or
+// (LN) layer norm.
+template <bool LN>
 __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ r, const uint16_t* __restrict__ g_f,
                                                     const uint16_t* __restrict__ w_out,
                                                     const uint16_t* __restrict__ b_out, float* __restrict__ x, int D,
@@ -406,11 +432,20 @@ __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ r,
   __shared__ float red[4];
   const int64_t m = blockIdx.x;
   const float* rr = r + m * D;
+  float mu = 0.0f;
+  if constexpr (LN) {
+    float s1 = 0.0f;
+    for (int d = threadIdx.x; d < D; d += blockDim.x) s1 += rr[d];
+    mu = block_sum(s1, red) / static_cast<float>(D);
+  }
   float ss = 0.0f;
-  for (int d = threadIdx.x; d < D; d += blockDim.x) ss = fmaf(rr[d], rr[d], ss);
+  for (int d = threadIdx.x; d < D; d += blockDim.x) {
+    const float e = rr[d] - mu;
+    ss = fmaf(e, e, ss);
+  }
   ss = block_sum(ss, red);
   const float inv = 1.0f / sqrtf(ss / static_cast<float>(D) + kEps);
-  for (int d = threadIdx.x; d < D; d += blockDim.x) sh[d] = f16r(rr[d] * inv * h2f(g_f[d]));
+  for (int d = threadIdx.x; d < D; d += blockDim.x) sh[d] = f16r((rr[d] - mu) * inv * h2f(g_f[d]));
   __syncthreads();
   float* part = sh + D;
   // Thread t: output t % A over the d-slice t / A; threads beyond the last
@@ -435,16 +470,23 @@ __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ r,
 
 size_t align256(size_t n) { return (n + 255) & ~static_cast<size_t>(255); }
 
+bool is_gr00t(const oq_dit_config& c) { return c.arch == OQ_DIT_GR00T; }
+int n_cross(const oq_dit_config& c) { return is_gr00t(c) ? (c.n_blocks + 1) / 2 : 0; }
+
 struct Layout {
-  size_t r, h1, qkv, o, h2, gu, act, xq, xs, part_o, part_ml, total;
+  size_t r, h1, qkv, o, h2, gu, act, xq, xs, part_o, part_ml, ckv, total;
 };
 
 Layout layout_for(const oq_dit_config& c) {
   const int64_t M = static_cast<int64_t>(c.batch) * c.tokens;
   const int64_t D = c.hidden, F = c.mlp;
   const int64_t Kmax = std::max(D, F);
-  const int nsplit = (c.prefix + c.tokens + kAttnKS - 1) / kAttnKS;
+  // Keys per sample: pi attends to [prefix ; own], gr00t to the conditioning
+  // tokens (even blocks) or to its own tokens (odd blocks).
+  const int keys = is_gr00t(c) ? std::max(c.prefix, c.tokens) : c.prefix + c.tokens;
+  const int nsplit = (keys + kAttnKS - 1) / kAttnKS;
   const int64_t BH = static_cast<int64_t>(c.batch) * c.n_heads;
+  const int64_t MC = is_gr00t(c) ? static_cast<int64_t>(c.batch) * c.prefix : 0;  // conditioning rows
   Layout L;
   size_t off = 0;
   L.r = off; off += align256(M * D * 4);
@@ -454,10 +496,11 @@ Layout layout_for(const oq_dit_config& c) {
   L.h2 = off; off += align256(M * D * 2);
   L.gu = off; off += align256(M * 2 * F * 2);
   L.act = off; off += align256(M * F * 2);
-  L.xq = off; off += align256(M * Kmax / 2);
-  L.xs = off; off += align256(M * 4);
+  L.xq = off; off += align256(std::max(M * Kmax, MC * D) / 2);
+  L.xs = off; off += align256(std::max(M, MC) * 4);
   L.part_o = off; off += align256(BH * nsplit * c.tokens * c.head_dim * 4);
   L.part_ml = off; off += align256(BH * nsplit * c.tokens * 2 * 4);
+  L.ckv = off; off += align256(static_cast<size_t>(n_cross(c)) * MC * 2 * D * 2);
   L.total = off;
   return L;
 }
@@ -480,15 +523,17 @@ bool fused_plan(int64_t K, RQPlan* p) {
 
 int validate_config(const oq_dit_config* c) {
   if (!c) return OQ_ERR_NULL;
-  if (c->arch != OQ_DIT_PI) return OQ_ERR_ARG;
+  if (c->arch != OQ_DIT_PI && c->arch != OQ_DIT_GR00T) return OQ_ERR_ARG;
   if (c->n_blocks < 1 || c->steps < 1 || c->batch < 1 || c->tokens < 1 || c->prefix < 0) return OQ_ERR_SHAPE;
   if (c->hidden < 64 || c->hidden % 64 || c->mlp < 64 || c->mlp % 64) return OQ_ERR_SHAPE;
   if (c->hidden > 16384 || c->mlp > 16384) return OQ_ERR_SHAPE;
-  if (c->n_heads < 1 || c->head_dim < 32 || c->head_dim > kMaxHeadDim || c->head_dim % 32 ||
+  if (c->n_heads < 1 || c->head_dim < 16 || c->head_dim > kMaxHeadDim || c->head_dim % 16 ||
       c->n_heads * c->head_dim != c->hidden)
     return OQ_ERR_SHAPE;
   if (c->tokens > kMaxTokens || c->action_dim < 1 || c->action_dim > 256) return OQ_ERR_SHAPE;
-  if (c->prefix + c->tokens > kMaxSplits * kAttnKS) return OQ_ERR_SHAPE;
+  const int keys = c->arch == OQ_DIT_GR00T ? std::max(c->prefix, c->tokens) : c->prefix + c->tokens;
+  if (keys > kMaxSplits * kAttnKS) return OQ_ERR_SHAPE;
+  if (c->arch == OQ_DIT_GR00T && c->prefix < 1) return OQ_ERR_SHAPE;
   RQPlan p;
   if (!fused_plan(c->hidden, &p) || !fused_plan(c->mlp, &p)) return OQ_ERR_SHAPE;
   return OQ_OK;
@@ -513,6 +558,7 @@ struct oq_dit {
   oq::Layout lay;
   uint8_t* ws = nullptr;
   size_t ws_bytes = 0;
+  bool cond_ready = false;    // gr00t: conditioning k|v computed into this workspace
   hipStream_t cap = nullptr;  // capture stream (graphs are replayed on the caller's stream)
   std::vector<oq_dit_graph> graphs;
   bool use_graphs = true;
@@ -524,9 +570,12 @@ namespace {
 template <typename T>
 T* at(oq_dit* h, size_t off) { return reinterpret_cast<T*>(h->ws + off); }
 
+int n_mod(const oq_dit_config& c) { return is_gr00t(c) ? 2 : 6; }
+
 const uint16_t* mod_ptr(oq_dit* h, int l, int t, int k) {
   const int64_t D = h->cfg.hidden;
-  return static_cast<const uint16_t*>(h->w.mod) + ((static_cast<int64_t>(l) * h->cfg.steps + t) * 6 + k) * D;
+  const int nm = n_mod(h->cfg);
+  return static_cast<const uint16_t*>(h->w.mod) + ((static_cast<int64_t>(l) * h->cfg.steps + t) * nm + k) * D;
 }
 
 RQOut rq_out(oq_dit* h, int64_t K, float s, RQPlan* p) {
@@ -558,17 +607,22 @@ FusedLaunch fused_launch(int64_t M, int64_t K, const RQPlan& p) {
   return f;
 }
 
-#define OQ_FUSED_SWITCH(CH, KERNEL, ...)                                                        \
-  switch (CH) {                                                                                 \
-    case 1: hipLaunchKernelGGL(KERNEL<1>, fl.grid, fl.block, fl.lds, st, __VA_ARGS__); break;    \
-    case 2: hipLaunchKernelGGL(KERNEL<2>, fl.grid, fl.block, fl.lds, st, __VA_ARGS__); break;    \
-    case 3: hipLaunchKernelGGL(KERNEL<3>, fl.grid, fl.block, fl.lds, st, __VA_ARGS__); break;    \
-    case 4: hipLaunchKernelGGL(KERNEL<4>, fl.grid, fl.block, fl.lds, st, __VA_ARGS__); break;    \
-    case 6: hipLaunchKernelGGL(KERNEL<6>, fl.grid, fl.block, fl.lds, st, __VA_ARGS__); break;    \
-    case 8: hipLaunchKernelGGL(KERNEL<8>, fl.grid, fl.block, fl.lds, st, __VA_ARGS__); break;    \
-    default: return OQ_ERR_SHAPE;                                                               \
+// Calls f(std::integral_constant<int, C>) for the chunk count C of a fused
+// row plan; false for an unsupported count.
+template <typename F>
+bool with_chunks(int chunks, F&& f) {
+  switch (chunks) {
+    case 1: f(std::integral_constant<int, 1>{}); return true;
+    case 2: f(std::integral_constant<int, 2>{}); return true;
+    case 3: f(std::integral_constant<int, 3>{}); return true;
+    case 4: f(std::integral_constant<int, 4>{}); return true;
+    case 6: f(std::integral_constant<int, 6>{}); return true;
+    case 8: f(std::integral_constant<int, 8>{}); return true;
+    default: return false;
   }
+}
 
+// h = fp16(norm(r) g (1 + sc) + sh) and its codes (sc, sh may be null).
 int norm_rq(oq_dit* h, const float* r, const void* g, const uint16_t* sc, const uint16_t* sh, uint16_t* out,
             float s, hipStream_t st) {
   const int64_t M = static_cast<int64_t>(h->cfg.batch) * h->cfg.tokens;
@@ -576,9 +630,36 @@ int norm_rq(oq_dit* h, const float* r, const void* g, const uint16_t* sc, const 
   RQPlan p;
   const RQOut o = rq_out(h, D, s, &p);
   const FusedLaunch fl = fused_launch(M, D, p);
-  OQ_FUSED_SWITCH(p.chunks, norm_rq_kernel, r, static_cast<const uint16_t*>(g), sc, sh, out, M,
-                  static_cast<int>(D), o)
-  return launch_status();
+  const uint16_t* gg = static_cast<const uint16_t*>(g);
+  const bool ln = is_gr00t(h->cfg);
+  const bool ok = with_chunks(p.chunks, [&](auto C) {
+    if (ln)
+      hipLaunchKernelGGL((norm_rq_kernel<decltype(C)::value, true>), fl.grid, fl.block, fl.lds, st, r, gg, sc, sh,
+                         out, M, static_cast<int>(D), o);
+    else
+      hipLaunchKernelGGL((norm_rq_kernel<decltype(C)::value, false>), fl.grid, fl.block, fl.lds, st, r, gg, sc, sh,
+                         out, M, static_cast<int>(D), o);
+  });
+  return ok ? launch_status() : OQ_ERR_SHAPE;
+}
+
+// a = fp16(gelu(...)) of the MLP's first linear output and its codes.
+int gelu_rq(oq_dit* h, const uint16_t* in, uint16_t* act, float s, hipStream_t st) {
+  const int64_t M = static_cast<int64_t>(h->cfg.batch) * h->cfg.tokens;
+  const int64_t F = h->cfg.mlp;
+  RQPlan p;
+  const RQOut o = rq_out(h, F, s, &p);
+  const FusedLaunch fl = fused_launch(M, F, p);
+  const bool gated = !is_gr00t(h->cfg);
+  const bool ok = with_chunks(p.chunks, [&](auto C) {
+    if (gated)
+      hipLaunchKernelGGL((gelu_rq_kernel<decltype(C)::value, true>), fl.grid, fl.block, fl.lds, st, in, act, M,
+                         static_cast<int>(F), o);
+    else
+      hipLaunchKernelGGL((gelu_rq_kernel<decltype(C)::value, false>), fl.grid, fl.block, fl.lds, st, in, act, M,
+                         static_cast<int>(F), o);
+  });
+  return ok ? launch_status() : OQ_ERR_SHAPE;
 }
 
 int gemm(oq_dit* h, const oq_qweight& wt, int64_t K, int64_t N, Epilogue epi, void* out, int64_t ldc,
@@ -588,56 +669,96 @@ int gemm(oq_dit* h, const oq_qweight& wt, int64_t K, int64_t N, Epilogue epi, vo
   return gemm_launch(a, epi, st);
 }
 
-int run_block(oq_dit* h, int l, int t, float* r, hipStream_t st) {
+// Attention (partials over 64-key splits, then the merge fused with the o
+// linear's rotate-quantize).  Keys: `P` rows of k_pre / v_pre (row stride
+// pre_ld) followed by `own` rows of the q|k|v buffer.
+int attention_rq(oq_dit* h, const uint16_t* q, int64_t q_ld, const uint16_t* k_pre, const uint16_t* v_pre,
+                 int P, int64_t pre_ld, const uint16_t* k_own, const uint16_t* v_own, int64_t own_ld, int own,
+                 float s, hipStream_t st) {
+  const oq_dit_config& c = h->cfg;
+  const int64_t M = static_cast<int64_t>(c.batch) * c.tokens;
+  const int64_t D = c.hidden;
+  AttnArgs a;
+  a.q = q; a.q_ld = q_ld;
+  a.k_pre = k_pre; a.v_pre = v_pre; a.P = P; a.pre_ld = pre_ld;
+  a.k_own = k_own; a.v_own = v_own; a.own_ld = own_ld; a.own_keys = own;
+  a.part_o = at<float>(h, h->lay.part_o);
+  a.part_ml = at<float>(h, h->lay.part_ml);
+  a.out = at<uint16_t>(h, h->lay.o); a.out_ld = D;
+  a.S = c.tokens; a.H = c.n_heads; a.hd = c.head_dim; a.D = static_cast<int>(D);
+  a.nsplit = (P + own + kAttnKS - 1) / kAttnKS;
+  a.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(c.head_dim)));
+  const unsigned waves = static_cast<unsigned>((c.tokens + 15) / 16);
+  hipLaunchKernelGGL(attn_partial_kernel, dim3(c.batch * c.n_heads, a.nsplit), dim3(64 * waves), 0, st, a);
+  int e = launch_status();
+  if (e != OQ_OK) return e;
+  RQPlan p;
+  const RQOut ro = rq_out(h, D, s, &p);
+  const FusedLaunch fl = fused_launch(M, D, p);
+  const bool ok = with_chunks(p.chunks, [&](auto C) {
+    hipLaunchKernelGGL((combine_rq_kernel<decltype(C)::value>), fl.grid, fl.block, fl.lds, st, a, M, ro);
+  });
+  return ok ? launch_status() : OQ_ERR_SHAPE;
+}
+
+int run_block_pi(oq_dit* h, int l, int t, float* r, hipStream_t st) {
   const oq_dit_config& c = h->cfg;
   const oq_dit_block& bw = h->blocks[l];
-  const int64_t M = static_cast<int64_t>(c.batch) * c.tokens;
   const int64_t D = c.hidden, F = c.mlp;
   const float* s = &h->s_table[(static_cast<size_t>(l) * c.steps + t) * 4];
   uint16_t* h1 = at<uint16_t>(h, h->lay.h1);
   uint16_t* qkv = at<uint16_t>(h, h->lay.qkv);
-  uint16_t* o = at<uint16_t>(h, h->lay.o);
   uint16_t* h2 = at<uint16_t>(h, h->lay.h2);
   uint16_t* gu = at<uint16_t>(h, h->lay.gu);
   uint16_t* act = at<uint16_t>(h, h->lay.act);
   int e;
-
   if ((e = norm_rq(h, r, bw.g1, mod_ptr(h, l, t, 0), mod_ptr(h, l, t, 1), h1, s[0], st)) != OQ_OK) return e;
   if ((e = gemm(h, bw.qkv, D, 3 * D, EPI_F16, qkv, 3 * D, nullptr, st)) != OQ_OK) return e;
-
-  AttnArgs a;
-  a.q = qkv; a.q_ld = 3 * D;
-  a.k_pre = static_cast<const uint16_t*>(bw.prefix_k);
-  a.v_pre = static_cast<const uint16_t*>(bw.prefix_v);
-  a.P = c.prefix;
-  a.k_own = qkv + D; a.v_own = qkv + 2 * D; a.own_ld = 3 * D; a.own_keys = c.tokens;
-  a.part_o = at<float>(h, h->lay.part_o);
-  a.part_ml = at<float>(h, h->lay.part_ml);
-  a.out = o; a.out_ld = D;
-  a.S = c.tokens; a.H = c.n_heads; a.hd = c.head_dim; a.D = static_cast<int>(D);
-  a.nsplit = (c.prefix + c.tokens + kAttnKS - 1) / kAttnKS;
-  a.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(c.head_dim)));
-  hipLaunchKernelGGL(attn_partial_kernel, dim3(c.batch * c.n_heads, a.nsplit), dim3(256), 0, st, a);
-  if ((e = launch_status()) != OQ_OK) return e;
-  {
-    RQPlan p;
-    const RQOut ro = rq_out(h, D, s[1], &p);
-    const FusedLaunch fl = fused_launch(M, D, p);
-    OQ_FUSED_SWITCH(p.chunks, combine_rq_kernel, a, M, ro)
-    if ((e = launch_status()) != OQ_OK) return e;
-  }
+  if ((e = attention_rq(h, qkv, 3 * D, static_cast<const uint16_t*>(bw.prefix_k),
+                        static_cast<const uint16_t*>(bw.prefix_v), c.prefix, D, qkv + D, qkv + 2 * D, 3 * D,
+                        c.tokens, s[1], st)) != OQ_OK)
+    return e;
   if ((e = gemm(h, bw.o, D, D, EPI_RESID_F32, r, D, mod_ptr(h, l, t, 2), st)) != OQ_OK) return e;
-
   if ((e = norm_rq(h, r, bw.g2, mod_ptr(h, l, t, 3), mod_ptr(h, l, t, 4), h2, s[2], st)) != OQ_OK) return e;
   if ((e = gemm(h, bw.gate_up, D, 2 * F, EPI_F16, gu, 2 * F, nullptr, st)) != OQ_OK) return e;
-  {
-    RQPlan p;
-    const RQOut ro = rq_out(h, F, s[3], &p);
-    const FusedLaunch fl = fused_launch(M, F, p);
-    OQ_FUSED_SWITCH(p.chunks, gelu_rq_kernel, gu, act, M, static_cast<int>(F), ro)
-    if ((e = launch_status()) != OQ_OK) return e;
-  }
+  if ((e = gelu_rq(h, gu, act, s[3], st)) != OQ_OK) return e;
   return gemm(h, bw.down, F, D, EPI_RESID_F32, r, D, mod_ptr(h, l, t, 5), st);
+}
+
+int run_block_gr00t(oq_dit* h, int l, int t, float* r, hipStream_t st) {
+  const oq_dit_config& c = h->cfg;
+  const oq_dit_block& bw = h->blocks[l];
+  const int64_t D = c.hidden, F = c.mlp;
+  const float* s = &h->s_table[(static_cast<size_t>(l) * c.steps + t) * 4];
+  uint16_t* h1 = at<uint16_t>(h, h->lay.h1);
+  uint16_t* qkv = at<uint16_t>(h, h->lay.qkv);
+  uint16_t* h2 = at<uint16_t>(h, h->lay.h2);
+  uint16_t* ff = at<uint16_t>(h, h->lay.gu);
+  uint16_t* act = at<uint16_t>(h, h->lay.act);
+  int e;
+  if ((e = norm_rq(h, r, bw.g1, mod_ptr(h, l, t, 0), mod_ptr(h, l, t, 1), h1, s[0], st)) != OQ_OK) return e;
+  if (l % 2 == 0) {
+    // Cross-attention to the conditioning k|v of this block ([B][P][2D]).
+    if ((e = gemm(h, bw.qkv, D, D, EPI_F16, qkv, D, nullptr, st)) != OQ_OK) return e;
+    const int64_t MC = static_cast<int64_t>(c.batch) * c.prefix;
+    const uint16_t* kv = at<uint16_t>(h, h->lay.ckv) + static_cast<int64_t>(l / 2) * MC * 2 * D;
+    if ((e = attention_rq(h, qkv, D, kv, kv + D, c.prefix, 2 * D, nullptr, nullptr, 0, 0, s[1], st)) != OQ_OK)
+      return e;
+  } else {
+    if ((e = gemm(h, bw.qkv, D, 3 * D, EPI_F16, qkv, 3 * D, nullptr, st)) != OQ_OK) return e;
+    if ((e = attention_rq(h, qkv, 3 * D, nullptr, nullptr, 0, 0, qkv + D, qkv + 2 * D, 3 * D, c.tokens, s[1],
+                          st)) != OQ_OK)
+      return e;
+  }
+  if ((e = gemm(h, bw.o, D, D, EPI_RESID_F32, r, D, nullptr, st)) != OQ_OK) return e;
+  if ((e = norm_rq(h, r, bw.g2, nullptr, static_cast<const uint16_t*>(bw.b2), h2, s[2], st)) != OQ_OK) return e;
+  if ((e = gemm(h, bw.gate_up, D, F, EPI_F16, ff, F, nullptr, st)) != OQ_OK) return e;
+  if ((e = gelu_rq(h, ff, act, s[3], st)) != OQ_OK) return e;
+  return gemm(h, bw.down, F, D, EPI_RESID_F32, r, D, nullptr, st);
+}
+
+int run_block(oq_dit* h, int l, int t, float* r, hipStream_t st) {
+  return is_gr00t(h->cfg) ? run_block_gr00t(h, l, t, r, st) : run_block_pi(h, l, t, r, st);
 }
 
 int run_step(oq_dit* h, float* x, int t, hipStream_t st) {
@@ -651,11 +772,35 @@ int run_step(oq_dit* h, float* x, int t, hipStream_t st) {
   if (e != OQ_OK) return e;
   for (int l = 0; l < c.n_blocks; ++l)
     if ((e = run_block(h, l, t, r, st)) != OQ_OK) return e;
-  const float dt = -1.0f / static_cast<float>(c.steps);
-  hipLaunchKernelGGL(final_kernel, dim3(static_cast<unsigned>(M)), dim3(256), (c.hidden + 256) * sizeof(float), st,
-                     r, static_cast<const uint16_t*>(h->w.g_f), static_cast<const uint16_t*>(h->w.w_out),
-                     static_cast<const uint16_t*>(h->w.b_out), x, c.hidden, c.action_dim, dt);
+  const float dt = (is_gr00t(c) ? 1.0f : -1.0f) / static_cast<float>(c.steps);
+  const size_t lds = (c.hidden + 256) * sizeof(float);
+  if (is_gr00t(c))
+    hipLaunchKernelGGL(final_kernel<true>, dim3(static_cast<unsigned>(M)), dim3(256), lds, st, r,
+                       static_cast<const uint16_t*>(h->w.g_f), static_cast<const uint16_t*>(h->w.w_out),
+                       static_cast<const uint16_t*>(h->w.b_out), x, c.hidden, c.action_dim, dt);
+  else
+    hipLaunchKernelGGL(final_kernel<false>, dim3(static_cast<unsigned>(M)), dim3(256), lds, st, r,
+                       static_cast<const uint16_t*>(h->w.g_f), static_cast<const uint16_t*>(h->w.w_out),
+                       static_cast<const uint16_t*>(h->w.b_out), x, c.hidden, c.action_dim, dt);
   return launch_status();
+}
+
+// gr00t: k|v of the conditioning tokens of every cross-attention block.
+int set_condition(oq_dit* h, const uint16_t* cond, hipStream_t st) {
+  const oq_dit_config& c = h->cfg;
+  const int64_t MC = static_cast<int64_t>(c.batch) * c.prefix;
+  const int64_t D = c.hidden;
+  uint8_t* xq = at<uint8_t>(h, h->lay.xq);
+  float* xs = at<float>(h, h->lay.xs);
+  int e = rq_launch(cond, MC, D, D, pow2_divisor(static_cast<int>(D)), 1.0f, xq, xs, nullptr, st);
+  if (e != OQ_OK) return e;
+  for (int l = 0; l < c.n_blocks; l += 2) {
+    uint16_t* kv = at<uint16_t>(h, h->lay.ckv) + static_cast<int64_t>(l / 2) * MC * 2 * D;
+    const oq_qweight& wt = h->blocks[l].cross_kv;
+    GemmArgs a{xq, wt.wq, xs, wt.w_scale, nullptr, kv, nullptr, MC, 2 * D, D, 2 * D};
+    if ((e = gemm_launch(a, EPI_F16, st)) != OQ_OK) return e;
+  }
+  return OQ_OK;
 }
 
 void drop_graphs(oq_dit* h) {
@@ -693,6 +838,38 @@ int run_steps(oq_dit* h, float* x, int t0, int n, hipStream_t st) {
   return hipGraphLaunch(exec, st) == hipSuccess ? OQ_OK : OQ_ERR_HIP;
 }
 
+bool qw_ok(const oq_qweight& q) { return q.wq && q.w_scale; }
+bool qw_aligned(const oq_qweight& q) { return aligned(q.wq, 16) && aligned(q.w_scale, 4); }
+
+int validate_weights(const oq_dit_config* cfg, const oq_dit_weights* w) {
+  if (!w->blocks || !w->mod || !w->s_table || !w->w_in || !w->b_in || !w->w_out || !w->b_out || !w->g_f)
+    return OQ_ERR_NULL;
+  const bool gr = cfg->arch == OQ_DIT_GR00T;
+  for (int l = 0; l < cfg->n_blocks; ++l) {
+    const oq_dit_block& b = w->blocks[l];
+    if (!b.g1 || !b.g2 || !qw_ok(b.qkv) || !qw_ok(b.o) || !qw_ok(b.gate_up) || !qw_ok(b.down)) return OQ_ERR_NULL;
+    if (!qw_aligned(b.qkv) || !qw_aligned(b.o) || !qw_aligned(b.gate_up) || !qw_aligned(b.down) ||
+        !aligned(b.g1, 16) || !aligned(b.g2, 16))
+      return OQ_ERR_ALIGN;
+    if (gr) {
+      if (!b.b2) return OQ_ERR_NULL;
+      if (!aligned(b.b2, 16)) return OQ_ERR_ALIGN;
+      if (l % 2 == 0) {
+        if (!qw_ok(b.cross_kv)) return OQ_ERR_NULL;
+        if (!qw_aligned(b.cross_kv)) return OQ_ERR_ALIGN;
+      }
+    } else if (cfg->prefix > 0) {
+      if (!b.prefix_k || !b.prefix_v) return OQ_ERR_NULL;
+      if (!aligned(b.prefix_k, 16) || !aligned(b.prefix_v, 16)) return OQ_ERR_ALIGN;
+    }
+  }
+  if (!aligned(w->mod, 16)) return OQ_ERR_ALIGN;
+  const size_t ns = static_cast<size_t>(cfg->n_blocks) * cfg->steps * 4;
+  for (size_t i = 0; i < ns; ++i)
+    if (!(w->s_table[i] > 0.0f) || !std::isfinite(w->s_table[i])) return OQ_ERR_ARG;
+  return OQ_OK;
+}
+
 }  // namespace
 }  // namespace oq
 
@@ -707,24 +884,8 @@ extern "C" int oq_dit_workspace_bytes(const oq_dit_config* cfg, size_t* bytes) {
 extern "C" int oq_dit_create(const oq_dit_config* cfg, const oq_dit_weights* w, oq_dit** out) {
   int e = oq::validate_config(cfg);
   if (e != OQ_OK) return e;
-  if (!w || !out || !w->blocks || !w->mod || !w->s_table || !w->w_in || !w->b_in || !w->w_out || !w->b_out ||
-      !w->g_f)
-    return OQ_ERR_NULL;
-  for (int l = 0; l < cfg->n_blocks; ++l) {
-    const oq_dit_block& b = w->blocks[l];
-    if (!b.g1 || !b.g2 || !b.qkv.wq || !b.qkv.w_scale || !b.o.wq || !b.o.w_scale || !b.gate_up.wq ||
-        !b.gate_up.w_scale || !b.down.wq || !b.down.w_scale)
-      return OQ_ERR_NULL;
-    if (cfg->prefix > 0 && (!b.prefix_k || !b.prefix_v)) return OQ_ERR_NULL;
-    if (!oq::aligned(b.qkv.wq, 16) || !oq::aligned(b.o.wq, 16) || !oq::aligned(b.gate_up.wq, 16) ||
-        !oq::aligned(b.down.wq, 16) || !oq::aligned(b.g1, 16) || !oq::aligned(b.g2, 16) ||
-        (cfg->prefix > 0 && (!oq::aligned(b.prefix_k, 16) || !oq::aligned(b.prefix_v, 16))))
-      return OQ_ERR_ALIGN;
-  }
-  if (!oq::aligned(w->mod, 16)) return OQ_ERR_ALIGN;
-  const size_t ns = static_cast<size_t>(cfg->n_blocks) * cfg->steps * 4;
-  for (size_t i = 0; i < ns; ++i)
-    if (!(w->s_table[i] > 0.0f) || !std::isfinite(w->s_table[i])) return OQ_ERR_ARG;
+  if (!w || !out) return OQ_ERR_NULL;
+  if ((e = oq::validate_weights(cfg, w)) != OQ_OK) return e;
   if ((e = oq::device_check()) != OQ_OK) return e;
   hipStream_t cap = nullptr;
   if (hipStreamCreateWithFlags(&cap, hipStreamNonBlocking) != hipSuccess) return OQ_ERR_HIP;
@@ -732,7 +893,7 @@ extern "C" int oq_dit_create(const oq_dit_config* cfg, const oq_dit_weights* w, 
   h->cfg = *cfg;
   h->w = *w;
   h->blocks.assign(w->blocks, w->blocks + cfg->n_blocks);
-  h->s_table.assign(w->s_table, w->s_table + ns);
+  h->s_table.assign(w->s_table, w->s_table + static_cast<size_t>(cfg->n_blocks) * cfg->steps * 4);
   h->w.blocks = h->blocks.data();
   h->w.s_table = h->s_table.data();
   h->lay = oq::layout_for(*cfg);
@@ -747,22 +908,45 @@ extern "C" int oq_dit_set_workspace(oq_dit* h, void* workspace, size_t bytes) {
   if (!h || !workspace) return OQ_ERR_NULL;
   if (!oq::aligned(workspace, 256)) return OQ_ERR_ALIGN;
   if (bytes < h->lay.total) return OQ_ERR_WORKSPACE;
-  if (h->ws != workspace) oq::drop_graphs(h);
+  if (h->ws != workspace) {
+    oq::drop_graphs(h);
+    h->cond_ready = false;
+  }
   h->ws = static_cast<uint8_t*>(workspace);
   h->ws_bytes = bytes;
   return OQ_OK;
 }
 
+extern "C" int oq_dit_set_condition(oq_dit* h, const void* cond, void* stream) {
+  if (!h || !cond) return OQ_ERR_NULL;
+  if (!h->ws) return OQ_ERR_WORKSPACE;
+  if (!oq::is_gr00t(h->cfg)) return OQ_ERR_ARG;
+  if (!oq::aligned(cond, 16)) return OQ_ERR_ALIGN;
+  const int e = oq::set_condition(h, static_cast<const uint16_t*>(cond), static_cast<hipStream_t>(stream));
+  h->cond_ready = e == OQ_OK;
+  return e;
+}
+
+namespace {
+int step_ready(const oq_dit* h) {
+  if (!h->ws) return OQ_ERR_WORKSPACE;
+  if (oq::is_gr00t(h->cfg) && !h->cond_ready) return OQ_ERR_ARG;
+  return OQ_OK;
+}
+}  // namespace
+
 extern "C" int oq_dit_step(oq_dit* h, float* x, int32_t t, void* stream) {
   if (!h || !x) return OQ_ERR_NULL;
-  if (!h->ws) return OQ_ERR_WORKSPACE;
+  int e = step_ready(h);
+  if (e != OQ_OK) return e;
   if (t < 0 || t >= h->cfg.steps) return OQ_ERR_ARG;
   return oq::run_steps(h, x, t, 1, static_cast<hipStream_t>(stream));
 }
 
 extern "C" int oq_dit_denoise(oq_dit* h, float* x, int32_t n_steps, void* stream) {
   if (!h || !x) return OQ_ERR_NULL;
-  if (!h->ws) return OQ_ERR_WORKSPACE;
+  int e = step_ready(h);
+  if (e != OQ_OK) return e;
   if (n_steps < 0 || n_steps > h->cfg.steps) return OQ_ERR_ARG;
   if (n_steps == 0) return OQ_OK;
   return oq::run_steps(h, x, 0, n_steps, static_cast<hipStream_t>(stream));
@@ -770,7 +954,8 @@ extern "C" int oq_dit_denoise(oq_dit* h, float* x, int32_t n_steps, void* stream
 
 extern "C" int oq_dit_run_block(oq_dit* h, int32_t l, int32_t t, float* resid, void* stream) {
   if (!h || !resid) return OQ_ERR_NULL;
-  if (!h->ws) return OQ_ERR_WORKSPACE;
+  int e = step_ready(h);
+  if (e != OQ_OK) return e;
   if (l < 0 || l >= h->cfg.n_blocks || t < 0 || t >= h->cfg.steps) return OQ_ERR_ARG;
   return oq::run_block(h, l, t, resid, static_cast<hipStream_t>(stream));
 }
@@ -785,6 +970,7 @@ extern "C" int oq_dit_get_intermediates(const oq_dit* h, oq_dit_intermediates* o
   out->gate_up = h->ws + h->lay.gu;
   out->act = h->ws + h->lay.act;
   out->resid = reinterpret_cast<const float*>(h->ws + h->lay.r);
+  out->cond_kv = oq::is_gr00t(h->cfg) ? h->ws + h->lay.ckv : nullptr;
   return OQ_OK;
 }
 

@@ -22,22 +22,30 @@ def _pow2_divisor(n: int) -> int:
 
 class DiT:
     """Args: cfg (object with arch, hidden, mlp, n_heads, head_dim, tokens,
-    prefix, steps, action_dim), inp (dict with "w", "mod", "s_table", "kp",
-    "vp", "n_blocks", "batch": w_in [D,A], b_in [D], w_out [A,D], b_out [A],
-    g_f [D], blocks[l] with g1, g2, wqkv [3D,D], wo [D,D], wgu [2F,D], wd [D,F];
-    mod[l][t] dict of sc1, sh1, gt1, sc2, sh2, gt2 [D]; s_table [L,T,4];
-    kp / vp [L,B,P,D]).  Values are used as fp16 (weights, gains, modulation,
-    prefix) and fp32 (s_table)."""
+    prefix, steps, action_dim), inp (dict with "w", "mod", "s_table",
+    "n_blocks", "batch" and, for arch "pi", "kp" / "vp" [L,B,P,D], for arch
+    "gr00t", "cond" [B,P,D]).  w: w_in [D,A], b_in [D], w_out [A,D], b_out [A],
+    g_f [D] and blocks[l]:
+      pi:    g1, g2, wqkv [3D,D], wo [D,D], wgu [2F,D], wd [D,F];
+      gr00t: g1, g3, beta3, wo, wff0 [F,D], wff2 [D,F] and, even l, wq [D,D] and
+             wkv [2D,D] (conditioning k|v), odd l, wqkv [3D,D].
+    mod[l][t]: dict of sc1, sh1, gt1, sc2, sh2, gt2 (pi) or sc1, sh1 (gr00t)
+    [D].  Values are used as fp16 (weights, gains, modulation, prefix,
+    conditioning) and fp32 (s_table).  A gr00t handle computes the
+    conditioning k|v at construction (oq_dit_set_condition)."""
 
     def __init__(self, cfg, inp, device="cuda:0"):
         from . import _check, quantize_weights  # noqa: F401
         self.lib = _lib.load()
         dev = torch.device(device)
         self.device = dev
+        self.arch = cfg.arch
+        gr = cfg.arch == "gr00t"
         L, B = inp["n_blocks"], inp["batch"]
         D, F, A = cfg.hidden, cfg.mlp, cfg.action_dim
         T = cfg.steps
         self.M = B * cfg.tokens
+        self.MC = B * cfg.prefix if gr else 0
         self.cfg_c = _lib.oq_dit_config(ARCH[cfg.arch], L, D, F, cfg.n_heads, cfg.head_dim, cfg.tokens,
                                         cfg.prefix, B, T, A)
         h16 = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float16)).to(dev)
@@ -46,8 +54,8 @@ class DiT:
         keep = self._keep.append
         self.w_in, self.b_in = h16(w["w_in"]), h16(w["b_in"])
         self.w_out, self.b_out, self.g_f = h16(w["w_out"]), h16(w["b_out"]), h16(w["g_f"])
-        mod = np.empty((L, T, 6, D), dtype=np.float16)
-        names = ("sc1", "sh1", "gt1", "sc2", "sh2", "gt2")
+        names = ("sc1", "sh1") if gr else ("sc1", "sh1", "gt1", "sc2", "sh2", "gt2")
+        mod = np.empty((L, T, len(names), D), dtype=np.float16)
         for l in range(L):
             for t in range(T):
                 for k, nm in enumerate(names):
@@ -56,21 +64,33 @@ class DiT:
         self.s_table = np.ascontiguousarray(inp["s_table"], dtype=np.float32)
         blocks = (_lib.oq_dit_block * L)()
         self.qweights = []
+        null = _lib.oq_qweight(None, None)
         for l in range(L):
             bw = w["blocks"][l]
             qd = {}
-            for nm in ("wqkv", "wo", "wgu", "wd"):
+            for nm in [n for n in bw if n.startswith("w")]:
                 W = h16(bw[nm])
                 qd[nm] = quantize_weights(W, _pow2_divisor(W.shape[1]))
                 del W
-            g1, g2 = h16(bw["g1"]), h16(bw["g2"])
-            kp, vp = h16(inp["kp"][l]), h16(inp["vp"][l])
-            for t_ in (g1, g2, kp, vp):
-                keep(t_)
             self.qweights.append(qd)
             qw = lambda nm: _lib.oq_qweight(qd[nm][0].data_ptr(), qd[nm][1].data_ptr())
-            blocks[l] = _lib.oq_dit_block(g1.data_ptr(), g2.data_ptr(), qw("wqkv"), qw("wo"), qw("wgu"),
-                                          qw("wd"), kp.data_ptr(), vp.data_ptr())
+            g1 = h16(bw["g1"])
+            keep(g1)
+            if gr:
+                g2, b2 = h16(bw["g3"]), h16(bw["beta3"])
+                keep(g2)
+                keep(b2)
+                even = l % 2 == 0
+                blocks[l] = _lib.oq_dit_block(g1.data_ptr(), g2.data_ptr(), qw("wq" if even else "wqkv"), qw("wo"),
+                                              qw("wff0"), qw("wff2"), None, None, b2.data_ptr(),
+                                              qw("wkv") if even else null)
+            else:
+                g2 = h16(bw["g2"])
+                kp, vp = h16(inp["kp"][l]), h16(inp["vp"][l])
+                for t_ in (g2, kp, vp):
+                    keep(t_)
+                blocks[l] = _lib.oq_dit_block(g1.data_ptr(), g2.data_ptr(), qw("wqkv"), qw("wo"), qw("wgu"),
+                                              qw("wd"), kp.data_ptr(), vp.data_ptr(), None, null)
         self._blocks = blocks
         self.w_c = _lib.oq_dit_weights(self.w_in.data_ptr(), self.b_in.data_ptr(), self.w_out.data_ptr(),
                                        self.b_out.data_ptr(), self.g_f.data_ptr(), blocks,
@@ -84,7 +104,15 @@ class DiT:
         self.handle = handle
         _check(self.lib.oq_dit_set_workspace(self.handle, self.workspace.data_ptr(), nbytes.value),
                "oq_dit_set_workspace")
+        if gr:
+            self.set_condition(h16(inp["cond"]))
         torch.cuda.synchronize(dev)
+
+    def set_condition(self, cond, stream=None):
+        """cond: fp16 [B, P, D] device tensor (gr00t)."""
+        from . import _check
+        _check(self.lib.oq_dit_set_condition(self.handle, cond.data_ptr(), self._stream(stream)),
+               "oq_dit_set_condition")
 
     def _stream(self, stream):
         s = torch.cuda.current_stream(self.device) if stream is None else stream
@@ -110,21 +138,33 @@ class DiT:
 
     def intermediates(self):
         """fp16 intermediates of the last block run, as numpy float64 arrays:
-        h1 [M,D], qkv [M,3D], attn [M,D], h2 [M,D], gate_up [M,2F], act [M,F]."""
+        h1 [M,D], qkv [M,3D], attn [M,D], h2 [M,D], gate_up [M,2F] (gr00t:
+        ff0 output [M,F]), act [M,F], resid [M,D] (fp32) and, for gr00t,
+        q [M,D] (the q output of a cross-attention block, stored with row
+        stride D where the q|k|v output of a self-attention block starts)
+        and cond_kv [n_cross, B*P, 2D]."""
         from . import _check
         it = _lib.oq_dit_intermediates()
         _check(self.lib.oq_dit_get_intermediates(self.handle, C.byref(it)), "oq_dit_get_intermediates")
         torch.cuda.synchronize(self.device)
         D, F, M = self.cfg_c.hidden, self.cfg_c.mlp, self.M
+        gr = self.arch == "gr00t"
         base = self.workspace.data_ptr()
+
+        def view(ptr, n, dtype, shape):
+            off = ptr - base
+            raw = self.workspace[off: off + n * np.dtype(dtype).itemsize].cpu().numpy()
+            return raw.view(dtype).reshape(shape).astype(np.float64)
+
         out = {}
-        for name, cols in (("h1", D), ("qkv", 3 * D), ("attn", D), ("h2", D), ("gate_up", 2 * F), ("act", F)):
-            off = getattr(it, name) - base
-            raw = self.workspace[off: off + M * cols * 2].cpu().numpy()
-            out[name] = raw.view(np.float16).reshape(M, cols).astype(np.float64)
-        off = it.resid - base
-        raw = self.workspace[off: off + M * D * 4].cpu().numpy()
-        out["resid"] = raw.view(np.float32).reshape(M, D).astype(np.float64)
+        for name, cols in (("h1", D), ("qkv", 3 * D), ("attn", D), ("h2", D), ("gate_up", F if gr else 2 * F),
+                           ("act", F)):
+            out[name] = view(getattr(it, name), M * cols, np.float16, (M, cols))
+        out["resid"] = view(it.resid, M * D, np.float32, (M, D))
+        if gr:
+            out["q"] = view(it.qkv, M * D, np.float16, (M, D))
+            nc = (self.cfg_c.n_blocks + 1) // 2
+            out["cond_kv"] = view(it.cond_kv, nc * self.MC * 2 * D, np.float16, (nc, self.MC, 2 * D))
         return out
 
     def close(self):

@@ -118,5 +118,15 @@ def test_dit_config_validation_without_gpu(lib):
     bad = _lib.oq_dit_config(7, 18, 1024, 4096, 8, 128, 50, 816, 1, 10, 32)     # arch
     assert lib.oq_dit_workspace_bytes(C.byref(bad), C.byref(size)) == ARG
     assert lib.oq_dit_workspace_bytes(None, C.byref(size)) == NULL
+    # GR00T-shaped head: 32 x 48 heads, 300 conditioning tokens, batch 64.
+    gr = _lib.oq_dit_config(1, 16, 1536, 6144, 32, 48, 16, 300, 64, 4, 32)
+    assert lib.oq_dit_workspace_bytes(C.byref(gr), C.byref(size)) == OK
+    # The conditioning k|v of the 8 cross-attention blocks: 8 x 64 x 300 x 3072 fp16.
+    assert size.value >= 8 * 64 * 300 * 2 * 1536 * 2
+    bad = _lib.oq_dit_config(1, 16, 1536, 6144, 48, 32, 16, 0, 64, 4, 32)     # no conditioning tokens
+    assert lib.oq_dit_workspace_bytes(C.byref(bad), C.byref(size)) == SHAPE
+    bad = _lib.oq_dit_config(1, 16, 1280, 5120, 32, 40, 16, 300, 64, 4, 32)   # head_dim % 16
+    assert lib.oq_dit_workspace_bytes(C.byref(bad), C.byref(size)) == SHAPE
+    assert lib.oq_dit_set_condition(None, P16, None) == NULL
     assert lib.oq_dit_step(None, P16, 0, None) == NULL
     assert lib.oq_dit_create(C.byref(good), None, C.byref(C.c_void_p())) == NULL

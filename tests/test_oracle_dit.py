@@ -120,6 +120,32 @@ def test_block_residual_uses_every_linear():
         assert not np.allclose(run([blk]), base), name
 
 
+def test_gr00t_blocks_use_every_linear():
+    """Both GR00T block kinds (cross-attention with the conditioning k|v linear,
+    self-attention): zeroing any one quantized weight changes the residual.
+    The blocks are quantized once; a zeroed weight is zero codes and a zero
+    scale (what the quantizer gives for an all-zero row)."""
+    cfg = configs.DIT_GR00T
+    inp = dit_inputs.make_dit_inputs(cfg, n_blocks=2, batch=2)
+    w = inp["w"]
+    qb0 = dit.quantize_block_weights(cfg, w["blocks"])
+    assert np.all(quant.quantize_sym(np.zeros((3, 64)))[0] == 0)
+
+    def run(qb):
+        ckv = dit.cond_kv(cfg, qb, inp["cond"])
+        tr = []
+        dit.step(cfg, w, qb, inp["mod"], inp["s_table"], inp["x0"], 0, ckv=ckv, trace=tr)
+        return tr
+
+    base = run(qb0)
+    for l, names in ((0, ("wq", "wkv", "wo", "wff0", "wff2")), (1, ("wqkv", "wo", "wff0", "wff2"))):
+        for name in names:
+            qb = [dict(b) for b in qb0]
+            qw, ws = qb[l][name]
+            qb[l][name] = (np.zeros_like(qw), np.zeros_like(ws))
+            assert not np.allclose(run(qb)[l], base[l]), (l, name)
+
+
 def test_step_scale_changes_only_boundary_codes():
     """eq:perstep_scale reading: s_t multiplies before the per-token quantizer and
     is divided back out, so the block output does not depend on s_t beyond
