@@ -271,19 +271,33 @@ __global__ __launch_bounds__(512, 1) void gemm_big_kernel(GemmArgs a) {
   const int fofs = 8 * (lane >> 5);  // 8 packed bytes = 16 codes of a 32-code sub-step
   const uint8_t* pA = &sA[0][(wm * 128 + frow) * BIG_STRIDE + fofs];
   const uint8_t* pB = &sB[0][(wn * 64 + frow) * BIG_STRIDE + fofs];
+// The packed fragments of sub-step sub + 1 are read from LDS while sub-step
+// sub is widened and multiplied (two register sets of raw fragments).
 #define OQ_COMPUTE(BUF, NSUB)                                                                               \
   {                                                                                                         \
     const int bo_ = (BUF) * BIG * BIG_STRIDE;                                                               \
+    uint2 ra_[2][4], rb_[2][2];                                                                             \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                           \
+      ra_[0][i] = *reinterpret_cast<const uint2*>(pA + bo_ + i * 32 * BIG_STRIDE);                          \
+    _Pragma("unroll") for (int j = 0; j < 2; ++j)                                                           \
+      rb_[0][j] = *reinterpret_cast<const uint2*>(pB + bo_ + j * 32 * BIG_STRIDE);                          \
     _Pragma("unroll") for (int sub = 0; sub < 4; ++sub) {                                                   \
       if (sub < (NSUB)) {                                                                                   \
+        const int cur_ = sub & 1;                                                                           \
+        if (sub + 1 < (NSUB)) {                                                                             \
+          _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                     \
+            ra_[cur_ ^ 1][i] = *reinterpret_cast<const uint2*>(pA + bo_ + i * 32 * BIG_STRIDE + (sub + 1) * 16); \
+          _Pragma("unroll") for (int j = 0; j < 2; ++j)                                                     \
+            rb_[cur_ ^ 1][j] = *reinterpret_cast<const uint2*>(pB + bo_ + j * 32 * BIG_STRIDE + (sub + 1) * 16); \
+        }                                                                                                   \
+        __builtin_amdgcn_sched_barrier(0);                                                                  \
         v4i fa[4], fb[2];                                                                                   \
-        _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                       \
-          fa[i] = widen16_u2(*reinterpret_cast<const uint2*>(pA + bo_ + i * 32 * BIG_STRIDE + sub * 16));  \
-        _Pragma("unroll") for (int j = 0; j < 2; ++j)                                                       \
-          fb[j] = widen16_u2(*reinterpret_cast<const uint2*>(pB + bo_ + j * 32 * BIG_STRIDE + sub * 16));  \
+        _Pragma("unroll") for (int i = 0; i < 4; ++i) fa[i] = widen16_u2(ra_[cur_][i]);                     \
+        _Pragma("unroll") for (int j = 0; j < 2; ++j) fb[j] = widen16_u2(rb_[cur_][j]);                     \
         _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                       \
         _Pragma("unroll") for (int j = 0; j < 2; ++j)                                                       \
           acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);               \
+        __builtin_amdgcn_sched_barrier(0);                                                                  \
       }                                                                                                     \
     }                                                                                                       \
   }
