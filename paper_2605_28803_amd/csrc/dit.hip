@@ -226,8 +226,11 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 // MFMA operand layout used (the same k order for both operands): lane l holds
 // row / column l % 16 and the 8 consecutive k values 8 * (l / 16) .. + 7 of a
 // 32-wide k step; the 16 x 16 fp32 result has row 4 * (l / 16) + e, column
-// l % 16 in element e.
-__global__ __launch_bounds__(256) void attn_partial_kernel(AttnArgs a) {
+// l % 16 in element e.  WAVES = ceil(S / 16) waves; HD = head_dim when it is
+// one of the compiled sizes (the loops then unroll completely), 0 otherwise
+// (a.hd at run time).
+template <int WAVES, int HD>
+__global__ __launch_bounds__(64 * WAVES) void attn_partial_kernel(AttnArgs a) {
   constexpr int KS = kAttnKS;            // 64 keys
   constexpr int PAD = KS + 8;            // padded row (halves): 16-byte reads of 16 rows hit distinct banks
   __shared__ __attribute__((aligned(16))) uint16_t sVt[kMaxHeadDim][PAD];  // V^T [dim][key]
@@ -240,7 +243,7 @@ __global__ __launch_bounds__(256) void attn_partial_kernel(AttnArgs a) {
   const int n_keys = a.P + a.own_keys;
   const int k0 = split * KS;
   const int nk = min(KS, n_keys - k0);
-  const int hd = a.hd;
+  const int hd = HD > 0 ? HD : a.hd;
 
   auto key_ptr = [&](int j, const uint16_t* pre, const uint16_t* own) -> const uint16_t* {
     const int key = k0 + j;
@@ -248,17 +251,24 @@ __global__ __launch_bounds__(256) void attn_partial_kernel(AttnArgs a) {
     return own + (static_cast<int64_t>(b) * a.own_keys + (key - a.P)) * a.own_ld + h * hd;
   };
 
+  // Loads are branch-free so that they issue together: an out-of-range key,
+  // query row or head dimension reads a clamped valid address and the value
+  // is replaced by zeros.
   // Stage V^T: thread (key j = tid % 64, dim group) loads 8 dims of one key.
-  const int nwaves = static_cast<int>(blockDim.x >> 6);
-  for (int d8 = (tid >> 6) * 8; d8 < hd; d8 += 8 * nwaves) {
+  {
     const int j = tid & 63;
-    uint4 raw = make_uint4(0, 0, 0, 0);
-    if (j < nk) raw = *reinterpret_cast<const uint4*>(key_ptr(j, a.v_pre, a.v_own) + d8);
-    const uint32_t wv[4] = {raw.x, raw.y, raw.z, raw.w};
+    const bool jok = j < nk;
+    const uint16_t* vp = key_ptr(jok ? j : 0, a.v_pre, a.v_own);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      sVt[d8 + 2 * q][j] = static_cast<uint16_t>(wv[q] & 0xFFFFu);
-      sVt[d8 + 2 * q + 1][j] = static_cast<uint16_t>(wv[q] >> 16);
+    for (int d8 = (tid >> 6) * 8; d8 < hd; d8 += 8 * WAVES) {
+      uint4 raw = *reinterpret_cast<const uint4*>(vp + d8);
+      if (!jok) raw = make_uint4(0, 0, 0, 0);
+      const uint32_t wv[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        sVt[d8 + 2 * q][j] = static_cast<uint16_t>(wv[q] & 0xFFFFu);
+        sVt[d8 + 2 * q + 1][j] = static_cast<uint16_t>(wv[q] >> 16);
+      }
     }
   }
 
@@ -267,22 +277,29 @@ __global__ __launch_bounds__(256) void attn_partial_kernel(AttnArgs a) {
   const bool qok = qrow < a.S;
   const int kq = 8 * (lane >> 4);
   const int nkk = (hd + 31) / 32;  // 32-wide k steps over the head dimension (zero-padded)
-  constexpr int KKMAX = kMaxHeadDim / 32;
+  constexpr int KKMAX = HD > 0 ? (HD + 31) / 32 : kMaxHeadDim / 32;
+  const uint16_t* qp = a.q + (static_cast<int64_t>(b) * a.S + (qok ? qrow : 0)) * a.q_ld + h * hd;
+  const uint16_t* kp[KS / 16];
+  bool kok[KS / 16];
+#pragma unroll
+  for (int nb = 0; nb < KS / 16; ++nb) {
+    const int j = nb * 16 + (lane & 15);
+    kok[nb] = j < nk;
+    kp[nb] = key_ptr(kok[nb] ? j : 0, a.k_pre, a.k_own);
+  }
   // Issue every Q and K load of the wave before the first MFMA.
   v8h qa[KKMAX], kb[KKMAX][KS / 16];
 #pragma unroll
   for (int kk = 0; kk < KKMAX; ++kk) {
-    qa[kk] = v8h{};
-    const bool dok = kk * 32 + kq < hd;  // hd % 8 == 0: a chunk of 8 dims is wholly in or out
-    if (kk < nkk && qok && dok)
-      qa[kk] = *reinterpret_cast<const v8h*>(a.q + (static_cast<int64_t>(b) * a.S + qrow) * a.q_ld + h * hd +
-                                             kk * 32 + kq);
+    // hd % 8 == 0: a chunk of 8 dims is wholly inside or outside the head.
+    const bool dok = kk < nkk && kk * 32 + kq < hd;
+    const int d = dok ? kk * 32 + kq : 0;
+    qa[kk] = *reinterpret_cast<const v8h*>(qp + d);
+    if (!(dok && qok)) qa[kk] = v8h{};
 #pragma unroll
     for (int nb = 0; nb < KS / 16; ++nb) {
-      const int j = nb * 16 + (lane & 15);
-      kb[kk][nb] = v8h{};
-      if (kk < nkk && j < nk && dok)
-        kb[kk][nb] = *reinterpret_cast<const v8h*>(key_ptr(j, a.k_pre, a.k_own) + kk * 32 + kq);
+      kb[kk][nb] = *reinterpret_cast<const v8h*>(kp[nb] + d);
+      if (!(dok && kok[nb])) kb[kk][nb] = v8h{};
     }
   }
   v4f sc[KS / 16];
@@ -689,7 +706,22 @@ int attention_rq(oq_dit* h, const uint16_t* q, int64_t q_ld, const uint16_t* k_p
   a.nsplit = (P + own + kAttnKS - 1) / kAttnKS;
   a.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(c.head_dim)));
   const unsigned waves = static_cast<unsigned>((c.tokens + 15) / 16);
-  hipLaunchKernelGGL(attn_partial_kernel, dim3(c.batch * c.n_heads, a.nsplit), dim3(64 * waves), 0, st, a);
+  const dim3 grid(c.batch * c.n_heads, a.nsplit);
+  auto launch = [&](auto W) {
+    constexpr int WV = decltype(W)::value;
+    switch (c.head_dim) {
+      case 48: hipLaunchKernelGGL((attn_partial_kernel<WV, 48>), grid, dim3(64 * WV), 0, st, a); break;
+      case 64: hipLaunchKernelGGL((attn_partial_kernel<WV, 64>), grid, dim3(64 * WV), 0, st, a); break;
+      case 128: hipLaunchKernelGGL((attn_partial_kernel<WV, 128>), grid, dim3(64 * WV), 0, st, a); break;
+      default: hipLaunchKernelGGL((attn_partial_kernel<WV, 0>), grid, dim3(64 * WV), 0, st, a); break;
+    }
+  };
+  switch (waves) {
+    case 1: launch(std::integral_constant<int, 1>{}); break;
+    case 2: launch(std::integral_constant<int, 2>{}); break;
+    case 3: launch(std::integral_constant<int, 3>{}); break;
+    default: launch(std::integral_constant<int, 4>{}); break;
+  }
   int e = launch_status();
   if (e != OQ_OK) return e;
   RQPlan p;

@@ -1,0 +1,208 @@
+// Matrix-core rotate-quantize of one row held as fp16 fragments (Section 4.1
+// eq:blockdiag / eq:transform, Section 4.2 eq:scale, eq:quant,
+// eq:perstep_scale), shared by the stand-alone kernel and by the DiT kernels
+// that produce an fp16 row and quantize it in the same pass.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "rq_device.h"
+
+namespace oq {
+namespace rqm {
+
+// ---------------------------------------------------------------------------
+// Layout for Hadamard blocks b >= 32 and K = 512 * NG * W.
+//
+// The first five butterfly stages (H_32 over each chunk of 32 channels) are a
+// product with a constant +-1 matrix, done on v_mfma_f32_16x16x32_f16 straight
+// from the fp16 input (exact products, fp32 sums): B operand = 16 chunks x 32
+// channels of the row, A operand = H_32 with its rows permuted so that lane l
+// receives channels 8q .. 8q+7 (q = l / 16) of chunk l % 16 -- eight
+// consecutive channels, i.e. one packed dword of codes.  Chunk index bits 0-3
+// are lane bits 0-3 (four cross-lane butterflies), the next bits are the
+// register group index g.  A row wider than 4096 channels spans W waves; its
+// top log2(W) channel bits are the wave index, and the butterflies over them
+// run after a transpose through LDS that gives each wave all W wave-values of
+// NG / W of the groups.  One wave (W = 1) or one workgroup (W > 1) per row
+// pass, no prefetch: the register budget stays small enough for several
+// workgroups per CU, and their loads overlap each other's arithmetic.
+// ---------------------------------------------------------------------------
+
+typedef _Float16 rv8h __attribute__((ext_vector_type(8)));
+typedef float rv4f __attribute__((ext_vector_type(4)));
+
+// Lane l's A fragments: A[m = l % 16][k = 8 (l / 16) + i] = H_32[rho(m)][k],
+// rho(4q + r) = 8q + r (first product) and 8q + 4 + r (second product).
+__device__ __forceinline__ void hadamard_frags(int lane, rv8h& a1, rv8h& a2) {
+  const int m = lane & 15;
+  const int row1 = 8 * (m >> 2) + (m & 3), row2 = row1 + 4;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int k = 8 * (lane >> 4) + i;
+    a1[i] = (__popc(row1 & k) & 1) ? static_cast<_Float16>(-1.0f) : static_cast<_Float16>(1.0f);
+    a2[i] = (__popc(row2 & k) & 1) ? static_cast<_Float16>(-1.0f) : static_cast<_Float16>(1.0f);
+  }
+}
+
+// Constants of the (NG, W) layout.
+template <int NG, int W>
+struct Shape {
+  static constexpr int K = NG * W * 512;
+  static constexpr int RPB = 4 / W;  // rows per 256-thread workgroup
+  static constexpr int LOGNG = NG >= 16 ? 4 : NG >= 8 ? 3 : NG >= 4 ? 2 : NG >= 2 ? 1 : 0;
+  static constexpr int LOGW = W >= 4 ? 2 : W >= 2 ? 1 : 0;
+  static constexpr int GW = NG / W;  // groups per wave after the transpose
+  static_assert(W == 1 || (NG % W == 0 && (NG & (NG - 1)) == 0), "NG must be a power of two >= W when W > 1");
+  static_assert(NG <= 16, "at most 16 register groups");
+};
+
+// First of the 8 consecutive channels of group g held by `lane` of wave wr:
+// ((wr * NG + g) * 16 + lane % 16) * 32 + 8 * (lane / 16).
+template <int NG>
+__device__ __forceinline__ int chan0(int wr, int g, int lane) {
+  return ((wr * NG + g) * 16 + (lane & 15)) * 32 + 8 * (lane >> 4);
+}
+
+// Everything after the row is in fragments: H_32 on the matrix cores, the
+// remaining butterflies, the row maximum, the scale and the codes (or, with
+// ratio != nullptr, the fp32 ratios z / Delta).  cur[g] holds channels
+// chan0(wr, g, lane) .. + 7.  Every wave of the workgroup calls it: it
+// synchronizes when W > 1 (xch: [4][NG][2][64] float4 of LDS), and `red` is
+// a 4-float shared array.
+template <int NG, int W, bool FULL>
+__device__ __forceinline__ void rq_row(const rv8h (&cur)[NG], const rv8h& a1, const rv8h& a2, int64_t row, bool valid,
+                                       int lane, int wv, int logb, float s_t, float s_over_sqrtb,
+                                       uint8_t* __restrict__ Xq, float* __restrict__ xs, float* __restrict__ ratio,
+                                       float4* xch, float* red) {
+  using S = Shape<NG, W>;
+  constexpr int K = S::K, LOGNG = S::LOGNG, LOGW = S::LOGW, GW = S::GW;
+  const int rsub = wv / W, wr = wv % W;
+  const int cl = lane & 15, q = lane >> 4;
+  // Butterfly over channel bit `bit` is needed when bit < log2(b); FULL means
+  // b = K (every stage, no branches).
+  auto need = [&](int bit) { return FULL || bit < logb; };
+  // H_32 on the matrix cores.
+  float v[NG][8];
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    const rv4f d1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, cur[g], rv4f{0, 0, 0, 0}, 0, 0, 0);
+    const rv4f d2 = __builtin_amdgcn_mfma_f32_16x16x32_f16(a2, cur[g], rv4f{0, 0, 0, 0}, 0, 0, 0);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      v[g][r] = d1[r];
+      v[g][4 + r] = d2[r];
+    }
+  }
+  // Channel bits 5..8: chunk bits 0..3 = lane bits 0..3.
+  if (need(5)) rqd::lane_stage<1>(v, lane);
+  if (need(6)) rqd::lane_stage<2>(v, lane);
+  if (need(7)) rqd::lane_stage<4>(v, lane);
+  if (need(8)) rqd::lane_stage<8>(v, lane);
+  // Channel bits 9 .. 9 + log2(NG) - 1: group index g in registers.
+#pragma unroll
+  for (int t = 0; t < LOGNG + 1; ++t) {
+    const int h = 1 << t;
+    if (h < NG && need(9 + t)) {
+#pragma unroll
+      for (int g = 0; g < NG; ++g)
+        if ((g & h) == 0 && g + h < NG)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float x0 = v[g][e], x1 = v[g + h][e];
+            v[g][e] = x0 + x1;
+            v[g + h][e] = x0 - x1;
+          }
+    }
+  }
+  // Register slot s holds channel group G(s) (units of 512 channels):
+  // G = wr * NG + s without the wave transpose, and with it (s = gi * W + u)
+  // G = u * NG + wr * GW + gi.
+  const int wbit0 = 9 + LOGNG;
+  const bool xpose = W > 1 && need(wbit0);
+  if constexpr (W > 1) {
+    if (xpose) {
+      float4* mine = xch + static_cast<int64_t>(wv) * NG * 128 + lane;
+#pragma unroll
+      for (int g = 0; g < NG; ++g) {
+        mine[g * 128] = make_float4(v[g][0], v[g][1], v[g][2], v[g][3]);
+        mine[g * 128 + 64] = make_float4(v[g][4], v[g][5], v[g][6], v[g][7]);
+      }
+      __syncthreads();
+#pragma unroll
+      for (int gi = 0; gi < GW; ++gi)
+#pragma unroll
+        for (int u = 0; u < W; ++u) {
+          const float4* src = xch + static_cast<int64_t>((rsub * W + u) * NG + wr * GW + gi) * 128 + lane;
+          const float4 p0 = src[0], p1 = src[64];
+          float* d = v[gi * W + u];
+          d[0] = p0.x; d[1] = p0.y; d[2] = p0.z; d[3] = p0.w;
+          d[4] = p1.x; d[5] = p1.y; d[6] = p1.z; d[7] = p1.w;
+        }
+      // Wave bits in registers: slot bits 0 .. log2(W) - 1 are u.
+#pragma unroll
+      for (int t = 0; t < LOGW; ++t) {
+        const int h = 1 << t;
+        if (need(wbit0 + t)) {
+#pragma unroll
+          for (int s = 0; s < NG; ++s)
+            if ((s & h) == 0)
+#pragma unroll
+              for (int e = 0; e < 8; ++e) {
+                const float x0 = v[s][e], x1 = v[s + h][e];
+                v[s][e] = x0 + x1;
+                v[s + h][e] = x0 - x1;
+              }
+        }
+      }
+    }
+  }
+
+  // Row maximum: registers, lanes, then the W waves of the row.
+  float amax = 0.0f;
+#pragma unroll
+  for (int g = 0; g < NG; ++g)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf(v[g][e]));
+  amax = fmaxf(amax, rqd::lane_xor<1>(amax));
+  amax = fmaxf(amax, rqd::lane_xor<2>(amax));
+  amax = fmaxf(amax, rqd::lane_xor<4>(amax));
+  amax = fmaxf(amax, rqd::lane_xor<8>(amax));
+  amax = fmaxf(amax, rqd::lane_xor<16>(amax));
+  amax = fmaxf(amax, __shfl_xor(amax, 32, 64));
+  if constexpr (W > 1) {
+    if (lane == 0) red[wv] = amax;
+    __syncthreads();
+    amax = red[rsub * W];
+#pragma unroll
+    for (int u = 1; u < W; ++u) amax = fmaxf(amax, red[rsub * W + u]);
+  }
+
+  const float a_z = amax * s_over_sqrtb;
+  const float delta = a_z / 7.0f;
+  const float gm = delta > 0.0f ? s_over_sqrtb / delta : 0.0f;
+  if (!valid) return;
+  if (wr == 0 && lane == 0) xs[row] = delta / s_t;
+  auto group_of = [&](int s) { return xpose ? (s % W) * NG + wr * GW + s / W : wr * NG + s; };
+  if (ratio != nullptr) {
+#pragma unroll
+    for (int s = 0; s < NG; ++s) {
+      float* rr = ratio + row * K + (group_of(s) * 16 + cl) * 32 + 8 * q;
+      reinterpret_cast<float4*>(rr)[0] = make_float4(v[s][0] * gm, v[s][1] * gm, v[s][2] * gm, v[s][3] * gm);
+      reinterpret_cast<float4*>(rr)[1] = make_float4(v[s][4] * gm, v[s][5] * gm, v[s][6] * gm, v[s][7] * gm);
+    }
+    return;
+  }
+  uint8_t* qr = Xq + row * (K / 2);
+#pragma unroll
+  for (int s = 0; s < NG; ++s) {
+    uint32_t b[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) b[e] = __float_as_uint(fmaf(v[s][e], gm, rqd::kRoundMagic));
+    *reinterpret_cast<uint32_t*>(qr + (group_of(s) * 16 + cl) * 16 + 4 * q) = rqd::pack8(b);
+  }
+}
+
+}  // namespace rqm
+}  // namespace oq
