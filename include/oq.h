@@ -225,7 +225,7 @@ typedef enum { OQ_DIT_PI = 0, OQ_DIT_GR00T = 1 } oq_dit_arch;
 typedef struct {
   int32_t arch;        /* oq_dit_arch                                        */
   int32_t n_blocks;    /* >= 1                                               */
-  int32_t hidden;      /* D, multiple of 64; = n_heads * head_dim           */
+  int32_t hidden;      /* D, multiple of 64, <= 8192; = n_heads * head_dim  */
   int32_t mlp;         /* F, multiple of 64                                  */
   int32_t n_heads;
   int32_t head_dim;    /* <= 128, multiple of 16                             */

@@ -49,17 +49,6 @@ constexpr int kMaxHeadDim = 128;
 constexpr int kMaxSplits = 16;  // (prefix + tokens) <= 16 * 64 keys
 constexpr float kEps = 1e-6f;
 
-__device__ float block_sum(float v, float* red) {
-  // 256 threads.
-  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
-  const int w = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 0) red[w] = v;
-  __syncthreads();
-  float s = red[0] + red[1] + red[2] + red[3];
-  __syncthreads();
-  return s;
-}
-
 __device__ __forceinline__ void load8_f16(const uint16_t* p, float (&o)[8]) {
   const uint4 raw = *reinterpret_cast<const uint4*>(p);
   const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
@@ -438,50 +427,113 @@ __global__ __launch_bounds__(256) void combine_rq_kernel(AttnArgs a, int64_t M, 
   rqd::rq_core<C>(v, m, a.D, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr);
 }
 
+__device__ __forceinline__ float wave_sum(float v) {
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+  return v;
+}
+
 // x[m][:] += dt * (fp16(norm(r[m]) g_f) W_out^T + b_out), norm = RMS norm or
-// (LN) layer norm.
+// (LN) layer norm.  Four rows per 256-thread workgroup: wave w normalizes row
+// m0 + w into LDS (reductions inside the wave), then thread t computes the
+// partial dot products of output a = t / 8 over the d-slice t % 8 for all
+// four rows (16-byte W_out loads shared by the rows), reduced over the 8
+// slices with lane shuffles (outputs in groups of 32).  D % 64 == 0.
 template <bool LN>
 __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ r, const uint16_t* __restrict__ g_f,
                                                     const uint16_t* __restrict__ w_out,
-                                                    const uint16_t* __restrict__ b_out, float* __restrict__ x, int D,
-                                                    int A, float dt) {
-  extern __shared__ float sh[];  // [D] normalized row, then [256] partial sums
-  __shared__ float red[4];
-  const int64_t m = blockIdx.x;
-  const float* rr = r + m * D;
-  float mu = 0.0f;
-  if constexpr (LN) {
-    float s1 = 0.0f;
-    for (int d = threadIdx.x; d < D; d += blockDim.x) s1 += rr[d];
-    mu = block_sum(s1, red) / static_cast<float>(D);
+                                                    const uint16_t* __restrict__ b_out, float* __restrict__ x,
+                                                    int64_t M, int D, int A, float dt) {
+  extern __shared__ float sh[];  // [4][D] normalized rows
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t m0 = static_cast<int64_t>(blockIdx.x) * 4;
+  {
+    const int64_t m = m0 + w;
+    const bool ok = m < M;
+    const float* rr = r + (ok ? m : 0) * D;
+    float* row = sh + w * D;
+    // Rows of up to 2048 channels stay in registers (one batch of loads,
+    // compile-time indices); wider rows are read again for each pass.
+    constexpr int CR = 8;
+    float s1 = 0.0f, ss = 0.0f, mu = 0.0f, inv = 0.0f;
+    if (D <= 256 * CR) {
+      float4 rv[CR];
+#pragma unroll
+      for (int c = 0; c < CR; ++c) {
+        const int d = lane * 4 + 256 * c;
+        rv[c] = d < D ? *reinterpret_cast<const float4*>(rr + d) : make_float4(0, 0, 0, 0);
+        s1 += (rv[c].x + rv[c].y) + (rv[c].z + rv[c].w);
+      }
+      mu = LN ? wave_sum(s1) / static_cast<float>(D) : 0.0f;
+#pragma unroll
+      for (int c = 0; c < CR; ++c) {
+        const int d = lane * 4 + 256 * c;
+        if (d < D) {
+          const float e0 = rv[c].x - mu, e1 = rv[c].y - mu, e2 = rv[c].z - mu, e3 = rv[c].w - mu;
+          ss = fmaf(e0, e0, fmaf(e1, e1, fmaf(e2, e2, fmaf(e3, e3, ss))));
+        }
+      }
+      inv = 1.0f / sqrtf(wave_sum(ss) / static_cast<float>(D) + kEps);
+#pragma unroll
+      for (int c = 0; c < CR; ++c) {
+        const int d = lane * 4 + 256 * c;
+        if (d < D) {
+          const uint2 gq = *reinterpret_cast<const uint2*>(g_f + d);
+          row[d] = f16r((rv[c].x - mu) * inv * h2f(gq.x & 0xFFFFu));
+          row[d + 1] = f16r((rv[c].y - mu) * inv * h2f(gq.x >> 16));
+          row[d + 2] = f16r((rv[c].z - mu) * inv * h2f(gq.y & 0xFFFFu));
+          row[d + 3] = f16r((rv[c].w - mu) * inv * h2f(gq.y >> 16));
+        }
+      }
+    } else {
+      for (int d = lane * 4; d < D; d += 256) {
+        const float4 v = *reinterpret_cast<const float4*>(rr + d);
+        s1 += (v.x + v.y) + (v.z + v.w);
+      }
+      mu = LN ? wave_sum(s1) / static_cast<float>(D) : 0.0f;
+      for (int d = lane * 4; d < D; d += 256) {
+        const float4 v = *reinterpret_cast<const float4*>(rr + d);
+        const float e0 = v.x - mu, e1 = v.y - mu, e2 = v.z - mu, e3 = v.w - mu;
+        ss = fmaf(e0, e0, fmaf(e1, e1, fmaf(e2, e2, fmaf(e3, e3, ss))));
+      }
+      inv = 1.0f / sqrtf(wave_sum(ss) / static_cast<float>(D) + kEps);
+      for (int d = lane * 4; d < D; d += 256) {
+        const float4 v = *reinterpret_cast<const float4*>(rr + d);
+        const uint2 gq = *reinterpret_cast<const uint2*>(g_f + d);
+        row[d] = f16r((v.x - mu) * inv * h2f(gq.x & 0xFFFFu));
+        row[d + 1] = f16r((v.y - mu) * inv * h2f(gq.x >> 16));
+        row[d + 2] = f16r((v.z - mu) * inv * h2f(gq.y & 0xFFFFu));
+        row[d + 3] = f16r((v.w - mu) * inv * h2f(gq.y >> 16));
+      }
+    }
   }
-  float ss = 0.0f;
-  for (int d = threadIdx.x; d < D; d += blockDim.x) {
-    const float e = rr[d] - mu;
-    ss = fmaf(e, e, ss);
-  }
-  ss = block_sum(ss, red);
-  const float inv = 1.0f / sqrtf(ss / static_cast<float>(D) + kEps);
-  for (int d = threadIdx.x; d < D; d += blockDim.x) sh[d] = f16r((rr[d] - mu) * inv * h2f(g_f[d]));
   __syncthreads();
-  float* part = sh + D;
-  // Thread t: output t % A over the d-slice t / A; threads beyond the last
-  // full slice idle.
-  const int slices = blockDim.x / A;
-  const int a_idx = threadIdx.x % A, sl = threadIdx.x / A;
-  float acc = 0.0f;
-  if (sl < slices) {
-    const int per = (D + slices - 1) / slices;
-    const int d0 = sl * per, d1 = min(D, d0 + per);
-    const uint16_t* wr = w_out + static_cast<int64_t>(a_idx) * D;
-    for (int d = d0; d < d1; ++d) acc = fmaf(sh[d], h2f(wr[d]), acc);
-  }
-  part[threadIdx.x] = acc;
-  __syncthreads();
-  if (threadIdx.x < A) {
-    float v = h2f(b_out[threadIdx.x]);
-    for (int s = 0; s < slices; ++s) v += part[s * A + threadIdx.x];
-    x[m * A + threadIdx.x] += dt * v;
+  const int sl = threadIdx.x & 7;
+  for (int a0 = 0; a0 < A; a0 += 32) {
+    const int a_idx = a0 + (threadIdx.x >> 3);
+    const bool aok = a_idx < A;
+    const uint16_t* wr = w_out + static_cast<int64_t>(aok ? a_idx : 0) * D;
+    float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll 4
+    for (int d = sl * 8; d < D; d += 64) {
+      float wv[8];
+      load8_f16(wr + d, wv);
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const float4 p0 = *reinterpret_cast<const float4*>(sh + rr * D + d);
+        const float4 p1 = *reinterpret_cast<const float4*>(sh + rr * D + d + 4);
+        acc[rr] = fmaf(p0.x, wv[0], fmaf(p0.y, wv[1], fmaf(p0.z, wv[2], fmaf(p0.w, wv[3], acc[rr]))));
+        acc[rr] = fmaf(p1.x, wv[4], fmaf(p1.y, wv[5], fmaf(p1.z, wv[6], fmaf(p1.w, wv[7], acc[rr]))));
+      }
+    }
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      float v = acc[rr];
+      v += __shfl_xor(v, 1, 64);
+      v += __shfl_xor(v, 2, 64);
+      v += __shfl_xor(v, 4, 64);
+      const int64_t m = m0 + rr;
+      if (aok && sl == 0 && m < M) x[m * A + a_idx] += dt * (v + h2f(b_out[a_idx]));
+    }
   }
 }
 
@@ -543,7 +595,7 @@ int validate_config(const oq_dit_config* c) {
   if (c->arch != OQ_DIT_PI && c->arch != OQ_DIT_GR00T) return OQ_ERR_ARG;
   if (c->n_blocks < 1 || c->steps < 1 || c->batch < 1 || c->tokens < 1 || c->prefix < 0) return OQ_ERR_SHAPE;
   if (c->hidden < 64 || c->hidden % 64 || c->mlp < 64 || c->mlp % 64) return OQ_ERR_SHAPE;
-  if (c->hidden > 16384 || c->mlp > 16384) return OQ_ERR_SHAPE;
+  if (c->hidden > 8192 || c->mlp > 16384) return OQ_ERR_SHAPE;
   if (c->n_heads < 1 || c->head_dim < 16 || c->head_dim > kMaxHeadDim || c->head_dim % 16 ||
       c->n_heads * c->head_dim != c->hidden)
     return OQ_ERR_SHAPE;
@@ -805,15 +857,16 @@ int run_step(oq_dit* h, float* x, int t, hipStream_t st) {
   for (int l = 0; l < c.n_blocks; ++l)
     if ((e = run_block(h, l, t, r, st)) != OQ_OK) return e;
   const float dt = (is_gr00t(c) ? 1.0f : -1.0f) / static_cast<float>(c.steps);
-  const size_t lds = (c.hidden + 256) * sizeof(float);
+  const size_t lds = static_cast<size_t>(4) * c.hidden * sizeof(float);
+  const dim3 fgrid(static_cast<unsigned>((M + 3) / 4));
   if (is_gr00t(c))
-    hipLaunchKernelGGL(final_kernel<true>, dim3(static_cast<unsigned>(M)), dim3(256), lds, st, r,
-                       static_cast<const uint16_t*>(h->w.g_f), static_cast<const uint16_t*>(h->w.w_out),
-                       static_cast<const uint16_t*>(h->w.b_out), x, c.hidden, c.action_dim, dt);
+    hipLaunchKernelGGL(final_kernel<true>, fgrid, dim3(256), lds, st, r, static_cast<const uint16_t*>(h->w.g_f),
+                       static_cast<const uint16_t*>(h->w.w_out), static_cast<const uint16_t*>(h->w.b_out), x, M,
+                       c.hidden, c.action_dim, dt);
   else
-    hipLaunchKernelGGL(final_kernel<false>, dim3(static_cast<unsigned>(M)), dim3(256), lds, st, r,
-                       static_cast<const uint16_t*>(h->w.g_f), static_cast<const uint16_t*>(h->w.w_out),
-                       static_cast<const uint16_t*>(h->w.b_out), x, c.hidden, c.action_dim, dt);
+    hipLaunchKernelGGL(final_kernel<false>, fgrid, dim3(256), lds, st, r, static_cast<const uint16_t*>(h->w.g_f),
+                       static_cast<const uint16_t*>(h->w.w_out), static_cast<const uint16_t*>(h->w.b_out), x, M,
+                       c.hidden, c.action_dim, dt);
   return launch_status();
 }
 
