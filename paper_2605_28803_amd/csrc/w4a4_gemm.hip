@@ -161,24 +161,25 @@ __global__ __launch_bounds__(256) void gemm_w4a4_kernel(GemmArgs a) {
 // ---------------------------------------------------------------------------
 // Large product (prefill / batched shapes): 256 x 256 output tile per
 // 512-thread workgroup of 8 waves (2 x 4), each wave a 128 x 64 tile (4 x 2
-// blocks of v_mfma_i32_32x32x32_i8, 128 accumulator registers), so two waves
-// share each SIMD and the hardware overlaps one wave's nibble widening and
-// LDS traffic with the other's MFMAs.  Codes stay packed in LDS (half the LDS
-// traffic of int8 tiles) and are widened to int8 after each 8-byte fragment
-// read.  K step 64 codes (32 packed bytes per row); LDS rows padded to 40
-// bytes (10 dwords: the 8-byte reads of 16 consecutive rows hit 16 distinct
-// bank pairs); two LDS buffers.  Global loads run three K steps ahead through
-// a ring of three register stages; rows past M (N) and steps past the last
-// read clamped addresses, so the loads are branch-free and the compiler
-// counts them exactly.  Tiles are visited XCD-major: consecutive workgroup
-// ids go to different XCDs, so ids are remapped so that each XCD works on a
-// compact group of tiles (shared A rows / B columns stay in that XCD's L2).
+// blocks of v_mfma_i32_32x32x32_i8, 128 accumulator registers), two waves per
+// SIMD.  Each LDS stage covers 128 codes of K: the packed codes are loaded
+// from global memory (32 bytes per thread and operand), widened once to int8
+// (16 * code) on the way into LDS, and read back as 16-byte fragments that
+// feed the matrix cores directly; the fragments of the next 32-code sub-step
+// are read while the current one is multiplied.  LDS rows are padded to 144
+// bytes (36 dwords: 16-byte reads and writes of 8 consecutive rows touch
+// distinct bank groups); two LDS buffers (144 KB).  Global loads run three
+// stages ahead through a ring of three register stages; rows past M (N) and
+// steps past the last read clamped addresses, so the loads are branch-free
+// and the compiler counts them exactly.  Tiles are visited XCD-major:
+// consecutive workgroup ids go to different XCDs, so ids are remapped so that
+// each XCD works on a compact group of tiles (shared A rows / B columns stay
+// in that XCD's L2).
 // ---------------------------------------------------------------------------
 
 constexpr int BIG = 256;
-constexpr int BIG_KSTAGE = 128;  // codes per LDS stage (64 packed bytes per row)
-constexpr int BIG_STRIDE = 72;   // packed bytes per LDS row (64 data + 8 pad): 18 dwords, so the
-                                 // 8-byte reads of 16 consecutive rows use 16 distinct bank pairs
+constexpr int BIG_KSTAGE = 128;    // codes per LDS stage (64 packed bytes per row in global memory)
+constexpr int BIG8_STRIDE = 144;   // int8 bytes per LDS row (128 + 16 pad)
 
 __device__ __forceinline__ v4i widen16_u2(uint2 p) {
   const uint32_t m = 0xF0F0F0F0u;
@@ -211,18 +212,19 @@ __device__ __forceinline__ void big_tile(int id, int tiles_m, int tiles_n, int* 
 
 template <int EPI>
 __global__ __launch_bounds__(512, 1) void gemm_big_kernel(GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) uint8_t sA[2][BIG * BIG_STRIDE];
-  __shared__ __attribute__((aligned(16))) uint8_t sB[2][BIG * BIG_STRIDE];
+  constexpr int BM = BIG;
+  __shared__ __attribute__((aligned(16))) uint8_t sA[2][BM * BIG8_STRIDE];
+  __shared__ __attribute__((aligned(16))) uint8_t sB[2][BIG * BIG8_STRIDE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm = wave >> 2, wn = wave & 3;  // 2 x 4 waves: rows wm*128, columns wn*64
-  const int tiles_m = static_cast<int>((a.M + BIG - 1) / BIG);
+  const int tiles_m = static_cast<int>((a.M + BM - 1) / BM);
   const int tiles_n = static_cast<int>((a.N + BIG - 1) / BIG);
   int tm, tn;
   big_tile(blockIdx.x, tiles_m, tiles_n, &tm, &tn);
-  const int64_t m0 = static_cast<int64_t>(tm) * BIG;
+  const int64_t m0 = static_cast<int64_t>(tm) * BM;
   const int64_t n0 = static_cast<int64_t>(tn) * BIG;
   const int64_t Kb = a.K / 2;
   const int nk = static_cast<int>((a.K + BIG_KSTAGE - 1) / BIG_KSTAGE);  // stages (the last may be half)
@@ -234,29 +236,32 @@ __global__ __launch_bounds__(512, 1) void gemm_big_kernel(GemmArgs a) {
   const int lr = tid >> 1, lh = tid & 1;
   const uint8_t* gA = a.A + min<int64_t>(m0 + lr, a.M - 1) * Kb + lh * 32;
   const uint8_t* gB = a.B + min<int64_t>(n0 + lr, a.N - 1) * Kb + lh * 32;
-  // Three register stages (plain variables: they must stay in VGPRs).
-  uint4 r0a, r0b, r0c, r0d, r1a, r1b, r1c, r1d, r2a, r2b, r2c, r2d;
-#define OQ_GLOAD(KS, RA, RA2, RB, RB2)                                            \
-  {                                                                               \
-    const int h_ = min(2 * (KS) + lh, nk64 - 1);                                  \
-    const int64_t off_ = static_cast<int64_t>(h_) * 32 - lh * 32;                 \
-    RA = *reinterpret_cast<const uint4*>(gA + off_);                              \
-    RA2 = *reinterpret_cast<const uint4*>(gA + off_ + 16);                        \
-    RB = *reinterpret_cast<const uint4*>(gB + off_);                              \
-    RB2 = *reinterpret_cast<const uint4*>(gB + off_ + 16);                        \
+  // Three register stages, indexed only by constants (they stay in VGPRs).
+  uint4 ra[3][2], rb[3][2];
+#define OQ_GLOAD(KS, S)                                                 \
+  {                                                                     \
+    const int h_ = min(2 * (KS) + lh, nk64 - 1);                        \
+    const int64_t off_ = static_cast<int64_t>(h_) * 32 - lh * 32;       \
+    ra[S][0] = *reinterpret_cast<const uint4*>(gA + off_);              \
+    ra[S][1] = *reinterpret_cast<const uint4*>(gA + off_ + 16);         \
+    rb[S][0] = *reinterpret_cast<const uint4*>(gB + off_);              \
+    rb[S][1] = *reinterpret_cast<const uint4*>(gB + off_ + 16);         \
   }
-#define OQ_ST16(P, V)                                                \
-  {                                                                  \
-    uint2* q_ = reinterpret_cast<uint2*>(P);                         \
-    q_[0] = make_uint2((V).x, (V).y);                                \
-    q_[1] = make_uint2((V).z, (V).w);                                \
+// Widen 16 packed bytes to 32 int8 (16 * code) and store them: the same
+// within-8-byte order for A and B, so the k order of every 16-code fragment
+// agrees between the operands.
+#define OQ_ST32(P, V)                                                   \
+  {                                                                     \
+    v4i* q_ = reinterpret_cast<v4i*>(P);                                \
+    q_[0] = widen16_u2(make_uint2((V).x, (V).y));                       \
+    q_[1] = widen16_u2(make_uint2((V).z, (V).w));                       \
   }
-#define OQ_LSTORE(BUF, RA, RA2, RB, RB2)                             \
-  {                                                                  \
-    OQ_ST16(&sA[(BUF)][lr * BIG_STRIDE + lh * 32], RA)               \
-    OQ_ST16(&sA[(BUF)][lr * BIG_STRIDE + lh * 32 + 16], RA2)         \
-    OQ_ST16(&sB[(BUF)][lr * BIG_STRIDE + lh * 32], RB)               \
-    OQ_ST16(&sB[(BUF)][lr * BIG_STRIDE + lh * 32 + 16], RB2)         \
+#define OQ_LSTORE(BUF, S)                                              \
+  {                                                                    \
+    OQ_ST32(&sA[(BUF)][lr * BIG8_STRIDE + lh * 64], ra[S][0])          \
+    OQ_ST32(&sA[(BUF)][lr * BIG8_STRIDE + lh * 64 + 32], ra[S][1])     \
+    OQ_ST32(&sB[(BUF)][lr * BIG8_STRIDE + lh * 64], rb[S][0])          \
+    OQ_ST32(&sB[(BUF)][lr * BIG8_STRIDE + lh * 64 + 32], rb[S][1])     \
   }
 
   v16i acc[4][2];
@@ -268,35 +273,33 @@ __global__ __launch_bounds__(512, 1) void gemm_big_kernel(GemmArgs a) {
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0;
 
   const int frow = lane & 31;
-  const int fofs = 8 * (lane >> 5);  // 8 packed bytes = 16 codes of a 32-code sub-step
-  const uint8_t* pA = &sA[0][(wm * 128 + frow) * BIG_STRIDE + fofs];
-  const uint8_t* pB = &sB[0][(wn * 64 + frow) * BIG_STRIDE + fofs];
-// The packed fragments of sub-step sub + 1 are read from LDS while sub-step
-// sub is widened and multiplied (two register sets of raw fragments).
+  const int fofs = 16 * (lane >> 5);  // 16 int8 codes of a 32-code sub-step
+  const uint8_t* pA = &sA[0][(wm * 128 + frow) * BIG8_STRIDE + fofs];
+  const uint8_t* pB = &sB[0][(wn * 64 + frow) * BIG8_STRIDE + fofs];
+  constexpr int ABUF = BM * BIG8_STRIDE, BBUF = BIG * BIG8_STRIDE;
+// The int8 fragments of sub-step sub + 1 are read from LDS while sub-step
+// sub is multiplied (two register sets).
 #define OQ_COMPUTE(BUF, NSUB)                                                                               \
   {                                                                                                         \
-    const int bo_ = (BUF) * BIG * BIG_STRIDE;                                                               \
-    uint2 ra_[2][4], rb_[2][2];                                                                             \
+    const int boa_ = (BUF) * ABUF, bob_ = (BUF) * BBUF;                                                      \
+    v4i fa_[2][4], fb_[2][2];                                                                               \
     _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                           \
-      ra_[0][i] = *reinterpret_cast<const uint2*>(pA + bo_ + i * 32 * BIG_STRIDE);                          \
+      fa_[0][i] = *reinterpret_cast<const v4i*>(pA + boa_ + i * 32 * BIG8_STRIDE);                          \
     _Pragma("unroll") for (int j = 0; j < 2; ++j)                                                           \
-      rb_[0][j] = *reinterpret_cast<const uint2*>(pB + bo_ + j * 32 * BIG_STRIDE);                          \
+      fb_[0][j] = *reinterpret_cast<const v4i*>(pB + bob_ + j * 32 * BIG8_STRIDE);                          \
     _Pragma("unroll") for (int sub = 0; sub < 4; ++sub) {                                                   \
       if (sub < (NSUB)) {                                                                                   \
         const int cur_ = sub & 1;                                                                           \
         if (sub + 1 < (NSUB)) {                                                                             \
           _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                     \
-            ra_[cur_ ^ 1][i] = *reinterpret_cast<const uint2*>(pA + bo_ + i * 32 * BIG_STRIDE + (sub + 1) * 16); \
+            fa_[cur_ ^ 1][i] = *reinterpret_cast<const v4i*>(pA + boa_ + i * 32 * BIG8_STRIDE + (sub + 1) * 32); \
           _Pragma("unroll") for (int j = 0; j < 2; ++j)                                                     \
-            rb_[cur_ ^ 1][j] = *reinterpret_cast<const uint2*>(pB + bo_ + j * 32 * BIG_STRIDE + (sub + 1) * 16); \
+            fb_[cur_ ^ 1][j] = *reinterpret_cast<const v4i*>(pB + bob_ + j * 32 * BIG8_STRIDE + (sub + 1) * 32); \
         }                                                                                                   \
         __builtin_amdgcn_sched_barrier(0);                                                                  \
-        v4i fa[4], fb[2];                                                                                   \
-        _Pragma("unroll") for (int i = 0; i < 4; ++i) fa[i] = widen16_u2(ra_[cur_][i]);                     \
-        _Pragma("unroll") for (int j = 0; j < 2; ++j) fb[j] = widen16_u2(rb_[cur_][j]);                     \
         _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                       \
         _Pragma("unroll") for (int j = 0; j < 2; ++j)                                                       \
-          acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[i], fb[j], acc[i][j], 0, 0, 0);               \
+          acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa_[cur_][i], fb_[cur_][j], acc[i][j], 0, 0, 0); \
         __builtin_amdgcn_sched_barrier(0);                                                                  \
       }                                                                                                     \
     }                                                                                                       \
@@ -304,38 +307,38 @@ __global__ __launch_bounds__(512, 1) void gemm_big_kernel(GemmArgs a) {
   // Sub-steps of 32 codes in stage ks: 4, or 2 for a final half stage.
 #define OQ_NSUB(KS) ((2 * (KS) + 2 <= nk64) ? 4 : 2)
 
-  OQ_GLOAD(0, r0a, r0b, r0c, r0d)
-  OQ_GLOAD(1, r1a, r1b, r1c, r1d)
-  OQ_GLOAD(2, r2a, r2b, r2c, r2d)
-  OQ_LSTORE(0, r0a, r0b, r0c, r0d)
+  OQ_GLOAD(0, 0)
+  OQ_GLOAD(1, 1)
+  OQ_GLOAD(2, 2)
+  OQ_LSTORE(0, 0)
   __syncthreads();
   // Stage kt: store stage kt+1 (loaded two stages ago) into the other
   // buffer, start the load of stage kt+3, run the MFMAs of stage kt, barrier.
   // At the top of each iteration ring slot 1 holds stage kt+1, slot 2 kt+2.
   int kt = 0;
   for (; kt + 3 <= nk; kt += 3) {
-    OQ_LSTORE((kt + 1) & 1, r1a, r1b, r1c, r1d)
-    OQ_GLOAD(kt + 3, r0a, r0b, r0c, r0d)
+    OQ_LSTORE((kt + 1) & 1, 1)
+    OQ_GLOAD(kt + 3, 0)
     OQ_COMPUTE(kt & 1, 4)
     __syncthreads();
-    OQ_LSTORE((kt + 2) & 1, r2a, r2b, r2c, r2d)
-    OQ_GLOAD(kt + 4, r1a, r1b, r1c, r1d)
+    OQ_LSTORE((kt + 2) & 1, 2)
+    OQ_GLOAD(kt + 4, 1)
     OQ_COMPUTE((kt + 1) & 1, 4)
     __syncthreads();
-    OQ_LSTORE((kt + 3) & 1, r0a, r0b, r0c, r0d)
-    OQ_GLOAD(kt + 5, r2a, r2b, r2c, r2d)
+    OQ_LSTORE((kt + 3) & 1, 0)
+    OQ_GLOAD(kt + 5, 2)
     OQ_COMPUTE((kt + 2) & 1, OQ_NSUB(kt + 2))
     __syncthreads();
   }
   if (kt < nk) {  // one or two stages left; stage kt is already in buffer kt & 1
-    if (kt + 1 < nk) OQ_LSTORE((kt + 1) & 1, r1a, r1b, r1c, r1d)
+    if (kt + 1 < nk) OQ_LSTORE((kt + 1) & 1, 1)
     OQ_COMPUTE(kt & 1, OQ_NSUB(kt))
     __syncthreads();
     if (kt + 1 < nk) OQ_COMPUTE((kt + 1) & 1, OQ_NSUB(kt + 1))
   }
 #undef OQ_NSUB
 #undef OQ_GLOAD
-#undef OQ_ST16
+#undef OQ_ST32
 #undef OQ_LSTORE
 #undef OQ_COMPUTE
 
@@ -583,6 +586,18 @@ int gemm_validate(const uint8_t* Xq, int64_t M, const uint8_t* Wq, int64_t N, in
   return OQ_OK;
 }
 
+int launch_big(const GemmArgs& a, Epilogue epi, int64_t tiles, hipStream_t stream) {
+  const dim3 g(static_cast<unsigned>(tiles)), b(512);
+  switch (epi) {
+    case EPI_I32: hipLaunchKernelGGL((gemm_big_kernel<EPI_I32>), g, b, 0, stream, a); break;
+    case EPI_F16: hipLaunchKernelGGL((gemm_big_kernel<EPI_F16>), g, b, 0, stream, a); break;
+    case EPI_BF16: hipLaunchKernelGGL((gemm_big_kernel<EPI_BF16>), g, b, 0, stream, a); break;
+    case EPI_RESID_F32: hipLaunchKernelGGL((gemm_big_kernel<EPI_RESID_F32>), g, b, 0, stream, a); break;
+    default: return OQ_ERR_ARG;
+  }
+  return launch_status();
+}
+
 int gemm_launch(const GemmArgs& a, Epilogue epi, hipStream_t stream) {
   if (a.M == 0) return OQ_OK;
   if (a.M <= 64) {
@@ -596,17 +611,7 @@ int gemm_launch(const GemmArgs& a, Epilogue epi, hipStream_t stream) {
   }
   // Large problems: 256 x 256 tiles when they still fill every CU.
   const int64_t big_tiles = ((a.M + BIG - 1) / BIG) * ((a.N + BIG - 1) / BIG);
-  if (big_tiles >= 256) {
-    const dim3 g(static_cast<unsigned>(big_tiles));
-    switch (epi) {
-      case EPI_I32: hipLaunchKernelGGL(gemm_big_kernel<EPI_I32>, g, dim3(512), 0, stream, a); break;
-      case EPI_F16: hipLaunchKernelGGL(gemm_big_kernel<EPI_F16>, g, dim3(512), 0, stream, a); break;
-      case EPI_BF16: hipLaunchKernelGGL(gemm_big_kernel<EPI_BF16>, g, dim3(512), 0, stream, a); break;
-      case EPI_RESID_F32: hipLaunchKernelGGL(gemm_big_kernel<EPI_RESID_F32>, g, dim3(512), 0, stream, a); break;
-      default: return OQ_ERR_ARG;
-    }
-    return launch_status();
-  }
+  if (big_tiles >= 256) return launch_big(a, epi, big_tiles, stream);
   const dim3 grid(static_cast<unsigned>((a.N + BN - 1) / BN), static_cast<unsigned>((a.M + BM - 1) / BM));
   switch (epi) {
     case EPI_I32: hipLaunchKernelGGL(gemm_w4a4_kernel<EPI_I32>, grid, dim3(256), 0, stream, a); break;
