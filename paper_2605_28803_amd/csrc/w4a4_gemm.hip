@@ -169,7 +169,8 @@ __global__ __launch_bounds__(256) void gemm_w4a4_kernel(GemmArgs a) {
 // are read while the current one is multiplied.  LDS rows are padded to 144
 // bytes (36 dwords: 16-byte reads and writes of 8 consecutive rows touch
 // distinct bank groups); two LDS buffers (144 KB).  Global loads run three
-// stages ahead through a ring of three register stages; rows past M (N) and
+// stages ahead through a ring of three register stages and each stage is
+// stored to LDS after the MFMAs of the previous one; rows past M (N) and
 // steps past the last read clamped addresses, so the loads are branch-free
 // and the compiler counts them exactly.  Tiles are visited XCD-major:
 // consecutive workgroup ids go to different XCDs, so ids are remapped so that
@@ -312,27 +313,28 @@ __global__ __launch_bounds__(512, 1) void gemm_big_kernel(GemmArgs a) {
   OQ_GLOAD(2, 2)
   OQ_LSTORE(0, 0)
   __syncthreads();
-  // Stage kt: store stage kt+1 (loaded two stages ago) into the other
-  // buffer, start the load of stage kt+3, run the MFMAs of stage kt, barrier.
-  // At the top of each iteration ring slot 1 holds stage kt+1, slot 2 kt+2.
+  // Stage kt: start the load of stage kt+3 into the free ring slot, run the
+  // MFMAs of stage kt, then store stage kt+1 (loaded two stages earlier) into
+  // the other LDS buffer and synchronize.  At the top of each iteration ring
+  // slot 1 holds stage kt+1 and slot 2 stage kt+2; stage kt is in LDS.
   int kt = 0;
   for (; kt + 3 <= nk; kt += 3) {
-    OQ_LSTORE((kt + 1) & 1, 1)
     OQ_GLOAD(kt + 3, 0)
     OQ_COMPUTE(kt & 1, 4)
+    OQ_LSTORE((kt + 1) & 1, 1)
     __syncthreads();
-    OQ_LSTORE((kt + 2) & 1, 2)
     OQ_GLOAD(kt + 4, 1)
     OQ_COMPUTE((kt + 1) & 1, 4)
+    OQ_LSTORE((kt + 2) & 1, 2)
     __syncthreads();
-    OQ_LSTORE((kt + 3) & 1, 0)
     OQ_GLOAD(kt + 5, 2)
     OQ_COMPUTE((kt + 2) & 1, OQ_NSUB(kt + 2))
+    OQ_LSTORE((kt + 3) & 1, 0)
     __syncthreads();
   }
   if (kt < nk) {  // one or two stages left; stage kt is already in buffer kt & 1
-    if (kt + 1 < nk) OQ_LSTORE((kt + 1) & 1, 1)
     OQ_COMPUTE(kt & 1, OQ_NSUB(kt))
+    if (kt + 1 < nk) OQ_LSTORE((kt + 1) & 1, 1)
     __syncthreads();
     if (kt + 1 < nk) OQ_COMPUTE((kt + 1) & 1, OQ_NSUB(kt + 1))
   }
