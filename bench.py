@@ -196,8 +196,9 @@ def prefill_kernels():
             e.synchronize()
             ts.append(s.elapsed_time(e))
         return float(np.median(ts))
-    t_r = cold(lambda: oq.rotate_quantize_act(X, K, Xq=Xq, x_scale=xs), 10)
-    t_g = cold(lambda: oq.w4a4_linear(Xq, xs, Wq, ws, Y=Y), 5)
+    oq.w4a4_linear(Xq, xs, Wq, ws, Y=Y)
+    t_r = cold(lambda: oq.rotate_quantize_act(X, K, Xq=Xq, x_scale=xs), 15)
+    t_g = cold(lambda: oq.w4a4_linear(Xq, xs, Wq, ws, Y=Y), 15)
     out = {"gemm_M16384_K16384_N16384": {"us": round(t_g * 1e3, 1),
                                          "TOPs": round(2 * M * N * K / (t_g * 1e-3) / 1e12, 1),
                                          "frac_int8_peak": round(2 * M * N * K / (t_g * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4)},
@@ -260,6 +261,111 @@ def cpu_baseline(cfg, inp, n_blocks_sample=3, min_seconds=10.0):
                       f"host cpus={len(os.sched_getaffinity(0))}"}
 
 
+def gr00t_step():
+    """The GR00T-shaped DiT step (16 blocks, hidden 1536, MLP 6144, 32 x 48
+    heads, batch 64 x 16 action tokens, 300 conditioning tokens, W4A4
+    throughout) timed warm over 20 steps; its W4A4 ops against the int8 MFMA
+    peak (the step's compute floor)."""
+    import torch
+    import paper_2605_28803_amd as oq
+    from workloads import configs, dit_inputs
+    cfg = configs.DIT_GR00T
+    inp = dit_inputs.make_dit_inputs(cfg)
+    model = oq.DiT(cfg, inp, device="cuda:0")
+    x = torch.from_numpy(inp["x0"].astype(np.float32)).cuda()
+    for t in range(cfg.steps):
+        model.step(x, t)
+    torch.cuda.synchronize()
+    s = torch.cuda.Event(enable_timing=True)
+    e = torch.cuda.Event(enable_timing=True)
+    s.record()
+    for i in range(20):
+        model.step(x, i % cfg.steps)
+    e.record()
+    e.synchronize()
+    ms = s.elapsed_time(e) / 20
+    model.close()
+    D, F, M = cfg.hidden, cfg.mlp, cfg.batch * cfg.tokens
+    ops = sum(2 * M * D * (D if l % 2 == 0 else 3 * D) + 2 * M * D * D + 4 * M * D * F for l in range(cfg.n_blocks))
+    return {"workload": "dit_gr00t: 16 blocks, hidden 1536, mlp 6144, 32x48 heads, batch 64 x 16 tokens, "
+                        "300 conditioning tokens, 4 steps",
+            "step_us": round(ms * 1e3, 1), "w4a4_GOP_per_step": round(ops / 1e9, 1),
+            "TOPs": round(ops / (ms * 1e-3) / 1e12, 1),
+            "frac_int8_peak": round(ops / (ms * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4)}
+
+
+def prefill_linears():
+    """The Gemma-2B-shaped prefill layer (816 tokens; q|k|v 2048 -> 2560, o,
+    gate|up 2048 -> 32768, down 16384 -> 2048), each linear's rotate-quantize
+    and GEMM timed cold (MALL flushed before each launch)."""
+    import torch
+    import paper_2605_28803_amd as oq
+    from workloads import configs
+    cfg = configs.PREFILL_GEMMA
+    dev = torch.device("cuda:0")
+    flush = torch.empty((512 << 20,), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def cold(fn, reps=10):
+        ts = []
+        for _ in range(reps):
+            flush.fill_(1)
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            b.synchronize()
+            ts.append(a.elapsed_time(b))
+        return float(np.median(ts))
+    out, tot_ops, tot_ms = {}, 0, 0.0
+    g = torch.Generator(device=dev).manual_seed(3)
+    for name, K, N in cfg.linears():
+        M = cfg.tokens
+        X = torch.randn((M, K), generator=g, device=dev).half()
+        W = (torch.randn((N, K), generator=g, device=dev) * cfg.w_std).half()
+        Wq, ws = oq.quantize_weights(W, K)
+        del W
+        Xq, xs = oq.rotate_quantize_act(X, K)
+        Y = torch.empty((M, N), dtype=torch.float16, device=dev)
+        t_r = cold(lambda: oq.rotate_quantize_act(X, K, Xq=Xq, x_scale=xs))
+        t_g = cold(lambda: oq.w4a4_linear(Xq, xs, Wq, ws, Y=Y))
+        ops = 2 * M * N * K
+        tot_ops += ops
+        tot_ms += t_r + t_g
+        out[name] = {"M": M, "K": K, "N": N, "rq_us": round(t_r * 1e3, 1), "gemm_us": round(t_g * 1e3, 1),
+                     "gemm_TOPs": round(ops / (t_g * 1e-3) / 1e12, 1)}
+    out["layer_us"] = round(tot_ms * 1e3, 1)
+    out["layer_TOPs"] = round(tot_ops / (tot_ms * 1e-3) / 1e12, 1)
+    del flush
+    torch.cuda.empty_cache()
+    return out
+
+
+def pi_step_without_graph(cfg, inp, steps=20):
+    """The same Pi-0.5-shaped step launched kernel by kernel (no HIP graph)."""
+    import torch
+    import paper_2605_28803_amd as oq
+    os.environ["OQ_DIT_NO_GRAPH"] = "1"
+    try:
+        model = oq.DiT(cfg, inp, device="cuda:0")
+    finally:
+        del os.environ["OQ_DIT_NO_GRAPH"]
+    x = torch.from_numpy(inp["x0"].astype(np.float32)).cuda()
+    for t in range(3):
+        model.step(x, t)
+    torch.cuda.synchronize()
+    s = torch.cuda.Event(enable_timing=True)
+    e = torch.cuda.Event(enable_timing=True)
+    s.record()
+    for i in range(steps):
+        model.step(x, i % cfg.steps)
+    e.record()
+    e.synchronize()
+    model.close()
+    return s.elapsed_time(e) / steps
+
+
 def run_dit(args):
     import torch
     import paper_2605_28803_amd as oq
@@ -294,6 +400,12 @@ def run_dit(args):
     assert torch.isfinite(x).all().item(), "non-finite action state"
     print(f"[bench] {args.steps} steps, {ms:.3f} ms/step", file=sys.stderr, flush=True)
 
+    nograph_ms = pi_step_without_graph(cfg, inp)
+    # Bytes a step must stream: every block's int4 weights and scales, and the
+    # prefix K/V.
+    D, F = cfg.hidden, cfg.mlp
+    step_bytes = cfg.n_blocks * ((3 * D * D + D * D + 2 * F * D + D * F) // 2 + 4 * (3 * D + D + 2 * F + D)
+                                 + 2 * 2 * cfg.prefix * D)
     kern, tot = time_linears(cfg, model.qweights, stream)
     rq_gbs = tot["rq_bytes"] / (tot["rq_ms"] * 1e-3) / 1e9
     roof = roofline_gemm()
@@ -316,12 +428,19 @@ def run_dit(args):
                                "Hadamard 1024/4096, s_t log-uniform [0.5,4]",
                    "global_batch": 1, "seq_len": cfg.tokens, "timing": "warm (weights + prefix K/V fit the MALL)"},
         "dit_step_latency_us": round(ms * 1e3, 2),
+        "dit_step_without_graph_us": round(nograph_ms * 1e3, 2),
+        "dit_step_stream": {"bytes": int(step_bytes), "GBs": round(step_bytes / (ms * 1e-3) / 1e9, 1),
+                            "hbm_floor_us": round(step_bytes / HBM_PEAK_GBS / 1e3, 1)},
         "roofline": roof,
         "kernels": {"per_linear": kern, "prefill": prefill,
                     "rotate_quant_GBs": round(rq_gbs, 1),
                     "gemm_TOPs": round(tot["gemm_ops"] / (tot["gemm_ms"] * 1e-3) / 1e12, 3),
                     "gemm_frac_int8_peak": round(tot["gemm_ops"] / (tot["gemm_ms"] * 1e-3) / 1e12 / INT8_PEAK_TOPS, 5)},
     }
+    if not args.no_prefill:
+        print("[bench] gr00t-shaped step, prefill layer", file=sys.stderr, flush=True)
+        line["dit_gr00t"] = gr00t_step()
+        line["prefill_gemma2b_layer"] = prefill_linears()
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle sample)", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(cfg, inp)
