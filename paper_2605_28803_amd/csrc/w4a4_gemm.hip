@@ -214,8 +214,11 @@ __device__ __forceinline__ void big_tile(int id, int tiles_m, int tiles_n, int* 
 template <int EPI>
 __global__ __launch_bounds__(512, 1) void gemm_big_kernel(GemmArgs a) {
   constexpr int BM = BIG;
-  __shared__ __attribute__((aligned(16))) uint8_t sA[2][BM * BIG8_STRIDE];
-  __shared__ __attribute__((aligned(16))) uint8_t sB[2][BIG * BIG8_STRIDE];
+  // Two LDS buffers per operand; after the K loop the same memory holds the
+  // 2-byte output tile of the staged epilogue.
+  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * (BM + BIG) * BIG8_STRIDE];
+  uint8_t (*sA)[BM * BIG8_STRIDE] = reinterpret_cast<uint8_t (*)[BM * BIG8_STRIDE]>(smem);
+  uint8_t (*sB)[BIG * BIG8_STRIDE] = reinterpret_cast<uint8_t (*)[BIG * BIG8_STRIDE]>(smem + 2 * BM * BIG8_STRIDE);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -346,9 +349,17 @@ __global__ __launch_bounds__(512, 1) void gemm_big_kernel(GemmArgs a) {
 
   // Epilogue (32 x 32 layout: element e of lane l is row 8*(e/4) + 4*(l/32) + e%4, column l%32).
   // Each lane's rows come in runs of four consecutive rows: their token scales
-  // are read as one float4 per run (rows past M read as 0).
+  // are read as one float4 per run (rows past M read as 0).  fp16 / bf16
+  // outputs are staged through LDS as a 256 x 256 tile and written as
+  // 16-byte row pieces (whole cache lines); int32 and residual outputs are
+  // written from the accumulator layout directly.
   const int col_in = lane & 31;
   const int row_grp = 4 * (lane >> 5);
+  constexpr bool STAGED = EPI == EPI_F16 || EPI == EPI_BF16;
+  constexpr int TP = BIG + 8;  // halves per staged row (528 bytes)
+  static_assert(!STAGED || BM * TP * 2 <= 2 * (BM + BIG) * BIG8_STRIDE, "staged tile exceeds LDS");
+  uint16_t* tile = reinterpret_cast<uint16_t*>(smem);
+  if (STAGED) __syncthreads();  // every fragment read of the last stage is done
   float wsc[2], bias[2], gate[2];
   int64_t gcs[2];
 #pragma unroll
@@ -367,7 +378,8 @@ __global__ __launch_bounds__(512, 1) void gemm_big_kernel(GemmArgs a) {
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int64_t r0 = m0 + wm * 128 + i * 32 + 8 * q + row_grp;
+      const int lr0 = wm * 128 + i * 32 + 8 * q + row_grp;  // row within the tile
+      const int64_t r0 = m0 + lr0;
       float xr[4] = {0.0f, 0.0f, 0.0f, 0.0f};
       if (EPI != EPI_I32) {
         if (r0 + 3 < a.M && (reinterpret_cast<uintptr_t>(a.xs + r0) & 15) == 0) {
@@ -381,6 +393,16 @@ __global__ __launch_bounds__(512, 1) void gemm_big_kernel(GemmArgs a) {
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const int64_t gc = gcs[j];
+        if (STAGED) {
+          // Rows / columns past the edge hold zeros and are not written back.
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const float y = static_cast<float>(acc[i][j][4 * q + u] >> 8) * xr[u] * wsc[j] + bias[j];
+            tile[(lr0 + u) * TP + wn * 64 + j * 32 + col_in] =
+                EPI == EPI_F16 ? __builtin_bit_cast(uint16_t, static_cast<_Float16>(y)) : f32_to_bf16_rne(y);
+          }
+          continue;
+        }
         if (gc >= a.N) continue;
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
@@ -392,18 +414,34 @@ __global__ __launch_bounds__(512, 1) void gemm_big_kernel(GemmArgs a) {
             static_cast<int32_t*>(a.C)[off] = v;
           } else {
             const float y = static_cast<float>(v) * xr[u] * wsc[j] + bias[j];
-            if (EPI == EPI_F16) {
-              static_cast<_Float16*>(a.C)[off] = static_cast<_Float16>(y);
-            } else if (EPI == EPI_BF16) {
-              static_cast<uint16_t*>(a.C)[off] = f32_to_bf16_rne(y);
-            } else {
-              float* rp = static_cast<float*>(a.C) + off;
-              *rp = fmaf(gate[j], y, *rp);
-            }
+            float* rp = static_cast<float*>(a.C) + off;
+            *rp = fmaf(gate[j], y, *rp);
           }
         }
       }
     }
+  if (STAGED) {
+    __syncthreads();
+    // 256 rows x 32 pieces of 8 outputs; thread t writes pieces t + 512 c.
+    uint16_t* C = static_cast<uint16_t*>(a.C);
+#pragma unroll
+    for (int c = 0; c < (BM * BIG / 8) / 512; ++c) {
+      const int id = tid + 512 * c;
+      const int lr = id >> 5, pc = (id & 31) * 8;
+      const int64_t gr = m0 + lr, gc = n0 + pc;
+      if (gr >= a.M || gc >= a.N) continue;
+      const uint4 v = *reinterpret_cast<const uint4*>(&tile[lr * TP + pc]);
+      if (gc + 8 <= a.N) {
+        *reinterpret_cast<uint4*>(C + gr * a.ldc + gc) = v;  // ldc % 8 == 0: 16-byte aligned
+      } else {
+        const uint16_t h[8] = {static_cast<uint16_t>(v.x), static_cast<uint16_t>(v.x >> 16),
+                               static_cast<uint16_t>(v.y), static_cast<uint16_t>(v.y >> 16),
+                               static_cast<uint16_t>(v.z), static_cast<uint16_t>(v.z >> 16),
+                               static_cast<uint16_t>(v.w), static_cast<uint16_t>(v.w >> 16)};
+        for (int e = 0; e < 8 && gc + e < a.N; ++e) C[gr * a.ldc + gc + e] = h[e];
+      }
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------

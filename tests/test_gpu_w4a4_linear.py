@@ -187,3 +187,30 @@ def test_prefill_layer_linears(name, K, N):
     print(f"  rel_l2 vs oracle on GPU codes {err:.2e}; vs independent oracle "
           f"{parity.rel_l2(Y.float().cpu().numpy()[rows], y_ind):.2e}")
     assert err <= parity.REL_L2_OUT
+
+
+@pytest.mark.parametrize("out_dtype", [oq.OUT_F16, oq.OUT_BF16])
+def test_large_tile_epilogue_ragged_strided(out_dtype):
+    """fp16 / bf16 outputs of the 256 x 256 tile path (staged through LDS and
+    written as 16-byte row pieces) with ragged rows and columns (M = N = 4100)
+    into a row-strided output (ldy = 4104): every output against the oracle
+    on the same codes, and the padding columns untouched."""
+    M = N = 4100
+    K = 256
+    rng = np.random.default_rng(17)
+    q, qw = _codes(rng, M, K), _codes(rng, N, K)
+    xs = rng.uniform(0.01, 2.0, M).astype(np.float32)
+    ws = rng.uniform(1e-4, 1e-2, N).astype(np.float32)
+    bias = (rng.standard_normal(N) * 0.1).astype(np.float16)
+    dt = torch.float16 if out_dtype == oq.OUT_F16 else torch.bfloat16
+    buf = torch.full((M, 4104), 7.0, dtype=dt, device=DEV)
+    Y = buf[:, :N]
+    oq.w4a4_linear(torch.from_numpy(parity.pack_int4(q)).to(DEV), torch.from_numpy(xs).to(DEV),
+                   torch.from_numpy(parity.pack_int4(qw)).to(DEV), torch.from_numpy(ws).to(DEV),
+                   bias=torch.from_numpy(bias).to(DEV), out_dtype=out_dtype, Y=Y)
+    torch.cuda.synchronize()
+    ref = linear.dequant(linear.int_gemm(q, qw), xs, ws, bias.astype(np.float64))
+    err = parity.rel_l2(Y.float().cpu().numpy(), ref)
+    print(f"large-tile ragged epilogue rel_l2={err:.3e}")
+    assert err <= parity.REL_L2_OUT
+    assert torch.all(buf[:, N:] == 7.0).item()
