@@ -29,20 +29,7 @@ namespace {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 
-constexpr int BM = 128, BN = 128, BK = 64;  // BK in codes (32 packed bytes per row)
-constexpr int LDS_STRIDE = 80;              // bytes per LDS row: 64 int8 + 16 pad
-
-__device__ __forceinline__ void unpack_store(uint8_t* dst, uint4 w) {
-  const uint32_t m = 0xF0F0F0F0u;
-  // Per packed dword: even-channel codes, then odd-channel codes.
-  uint4 p0, p1;
-  p0.x = (w.x << 4) & m; p0.y = w.x & m;
-  p0.z = (w.y << 4) & m; p0.w = w.y & m;
-  p1.x = (w.z << 4) & m; p1.y = w.z & m;
-  p1.z = (w.w << 4) & m; p1.w = w.w & m;
-  reinterpret_cast<uint4*>(dst)[0] = p0;
-  reinterpret_cast<uint4*>(dst)[1] = p1;
-}
+constexpr int BK = 64;  // K granularity in codes (one MFMA k step of 64 codes = 32 packed bytes)
 
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   uint32_t b = __float_as_uint(f);
@@ -50,135 +37,29 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   return static_cast<uint16_t>(b >> 16);
 }
 
-template <int EPI>
-__global__ __launch_bounds__(256) void gemm_w4a4_kernel(GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) uint8_t sA[2][BM * LDS_STRIDE];
-  __shared__ __attribute__((aligned(16))) uint8_t sB[2][BN * LDS_STRIDE];
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int64_t m0 = static_cast<int64_t>(blockIdx.y) * BM;
-  const int64_t n0 = static_cast<int64_t>(blockIdx.x) * BN;
-  const int64_t Kb = a.K / 2;
-  const int nk = static_cast<int>(a.K / BK);
-
-  // Global -> LDS assignment: thread loads 16 packed bytes (32 codes) of one row.
-  const int lr = tid >> 1, lh = tid & 1;
-  const bool a_ok = m0 + lr < a.M;
-  const bool b_ok = n0 + lr < a.N;
-  const uint8_t* gA = a.A + (a_ok ? (m0 + lr) : 0) * Kb + lh * 16;
-  const uint8_t* gB = a.B + (b_ok ? (n0 + lr) : 0) * Kb + lh * 16;
-  const int st_off = lr * LDS_STRIDE + lh * 32;
-
-  uint4 ra = make_uint4(0, 0, 0, 0), rb = make_uint4(0, 0, 0, 0);
-  if (a_ok) ra = *reinterpret_cast<const uint4*>(gA);
-  if (b_ok) rb = *reinterpret_cast<const uint4*>(gB);
-  unpack_store(&sA[0][st_off], ra);
-  unpack_store(&sB[0][st_off], rb);
-  __syncthreads();
-
-  v16i acc[2][2];
-#pragma unroll
-  for (int r = 0; r < 2; ++r)
-#pragma unroll
-    for (int s = 0; s < 2; ++s)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[r][s][e] = 0;
-
-  const int frag_row = lane & 31;
-  const int frag_k = 16 * (lane >> 5);
-
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    const bool more = kt + 1 < nk;
-    if (more) {
-      if (a_ok) ra = *reinterpret_cast<const uint4*>(gA + (kt + 1) * (BK / 2));
-      if (b_ok) rb = *reinterpret_cast<const uint4*>(gB + (kt + 1) * (BK / 2));
-    }
-#pragma unroll
-    for (int kk = 0; kk < BK; kk += 32) {
-      v4i fa[2], fb[2];
-#pragma unroll
-      for (int r = 0; r < 2; ++r)
-        fa[r] = *reinterpret_cast<const v4i*>(&sA[buf][(wm * 64 + r * 32 + frag_row) * LDS_STRIDE + kk + frag_k]);
-#pragma unroll
-      for (int s = 0; s < 2; ++s)
-        fb[s] = *reinterpret_cast<const v4i*>(&sB[buf][(wn * 64 + s * 32 + frag_row) * LDS_STRIDE + kk + frag_k]);
-#pragma unroll
-      for (int r = 0; r < 2; ++r)
-#pragma unroll
-        for (int s = 0; s < 2; ++s)
-          acc[r][s] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[r], fb[s], acc[r][s], 0, 0, 0);
-    }
-    if (more) {
-      unpack_store(&sA[buf ^ 1][st_off], ra);
-      unpack_store(&sB[buf ^ 1][st_off], rb);
-    }
-    __syncthreads();
-  }
-
-  // Epilogue.  32x32 accumulator layout: element e of lane l is row
-  // 8*(e/4) + 4*(l/32) + e%4, column l%32 of the block.
-  const int col_in = lane & 31;
-  const int row_grp = 4 * (lane >> 5);
-#pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    const int64_t gc = n0 + wn * 64 + s * 32 + col_in;
-    if (gc >= a.N) continue;
-    float wsc = 0.0f, bias = 0.0f, gate = 1.0f;
-    if (EPI != EPI_I32) {
-      wsc = a.ws[gc];
-      if (a.bias) bias = static_cast<float>(__builtin_bit_cast(_Float16, a.bias[gc]));
-      if (EPI == EPI_RESID_F32 && a.gate) gate = static_cast<float>(__builtin_bit_cast(_Float16, a.gate[gc]));
-    }
-#pragma unroll
-    for (int r = 0; r < 2; ++r)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int64_t gr = m0 + wm * 64 + r * 32 + 8 * (e >> 2) + row_grp + (e & 3);
-        if (gr >= a.M) continue;
-        const int v = acc[r][s][e] >> 8;
-        const int64_t off = gr * a.ldc + gc;
-        if (EPI == EPI_I32) {
-          static_cast<int32_t*>(a.C)[off] = v;
-        } else {
-          const float y = static_cast<float>(v) * a.xs[gr] * wsc + bias;
-          if (EPI == EPI_F16) {
-            static_cast<_Float16*>(a.C)[off] = static_cast<_Float16>(y);
-          } else if (EPI == EPI_BF16) {
-            static_cast<uint16_t*>(a.C)[off] = f32_to_bf16_rne(y);
-          } else {
-            float* rp = static_cast<float*>(a.C) + off;
-            *rp = fmaf(gate, y, *rp);
-          }
-        }
-      }
-  }
-}
-
 // ---------------------------------------------------------------------------
-// Large product (prefill / batched shapes): 256 x 256 output tile per
-// 512-thread workgroup of 8 waves (2 x 4), each wave a 128 x 64 tile (4 x 2
-// blocks of v_mfma_i32_32x32x32_i8, 128 accumulator registers), two waves per
-// SIMD.  Each LDS stage covers 128 codes of K: the packed codes are loaded
-// from global memory (32 bytes per thread and operand), widened once to int8
-// (16 * code) on the way into LDS, and read back as 16-byte fragments that
-// feed the matrix cores directly; the fragments of the next 32-code sub-step
-// are read while the current one is multiplied.  LDS rows are padded to 144
-// bytes (36 dwords: 16-byte reads and writes of 8 consecutive rows touch
-// distinct bank groups); two LDS buffers (144 KB).  Global loads run three
+// Products with M > 64 (prefill / batched shapes).  A workgroup of WM x WN
+// waves owns a (32 TM WM) x (32 TN WN) output tile; each wave a (32 TM) x
+// (32 TN) tile of v_mfma_i32_32x32x32_i8 blocks.  Two instances: 256 x 256
+// (8 waves of 128 x 64, one workgroup per CU) for large problems and 128 x
+// 128 (4 waves of 64 x 64, two workgroups per CU) when the large tiles would
+// not fill the CUs.  Each LDS stage covers 128 codes of K: the packed codes
+// are loaded from global memory (32 bytes per thread and row), widened once
+// to int8 (16 * code) on the way into LDS, and read back as 16-byte fragments
+// that feed the matrix cores directly; the fragments of the next 32-code
+// sub-step are read while the current one is multiplied.  LDS rows are
+// padded to 144 bytes (36 dwords: 16-byte reads and writes of 8 consecutive
+// rows touch distinct bank groups); two LDS buffers.  Global loads run three
 // stages ahead through a ring of three register stages and each stage is
 // stored to LDS after the MFMAs of the previous one; rows past M (N) and
 // steps past the last read clamped addresses, so the loads are branch-free
-// and the compiler counts them exactly.  Tiles are visited XCD-major:
-// consecutive workgroup ids go to different XCDs, so ids are remapped so that
-// each XCD works on a compact group of tiles (shared A rows / B columns stay
-// in that XCD's L2).
+// and the compiler counts them exactly.  fp16 / bf16 results are staged
+// through the freed LDS and written as 16-byte row pieces.  Tiles are visited
+// XCD-major: consecutive workgroup ids go to different XCDs, so ids are
+// remapped so that each XCD works on a compact group of tiles (shared A rows /
+// B columns stay in that XCD's L2).
 // ---------------------------------------------------------------------------
 
-constexpr int BIG = 256;
 constexpr int BIG_KSTAGE = 128;    // codes per LDS stage (64 packed bytes per row in global memory)
 constexpr int BIG8_STRIDE = 144;   // int8 bytes per LDS row (128 + 16 pad)
 
@@ -211,45 +92,57 @@ __device__ __forceinline__ void big_tile(int id, int tiles_m, int tiles_n, int* 
   *tn = in / gsize;
 }
 
-template <int EPI>
-__global__ __launch_bounds__(512, 1) void gemm_big_kernel(GemmArgs a) {
-  constexpr int BM = BIG;
+template <int EPI, int WM, int WN, int TM, int TN>
+__global__ __launch_bounds__(64 * WM * WN, 512 / (64 * WM * WN)) void gemm_big_kernel(GemmArgs a) {
+  // WM x WN waves, each a (32 TM) x (32 TN) tile of v_mfma_i32_32x32x32_i8 blocks.
+  constexpr int NT = 64 * WM * WN;          // threads
+  constexpr int BM = 32 * TM * WM, BN = 32 * TN * WN;
+  constexpr int PA = 2 * BM / NT, PB = 2 * BN / NT;  // rows each thread loads per stage
+  static_assert(PA >= 1 && PB >= 1 && 2 * BM % NT == 0 && 2 * BN % NT == 0, "load split");
   // Two LDS buffers per operand; after the K loop the same memory holds the
   // 2-byte output tile of the staged epilogue.
-  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * (BM + BIG) * BIG8_STRIDE];
+  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * (BM + BN) * BIG8_STRIDE];
   uint8_t (*sA)[BM * BIG8_STRIDE] = reinterpret_cast<uint8_t (*)[BM * BIG8_STRIDE]>(smem);
-  uint8_t (*sB)[BIG * BIG8_STRIDE] = reinterpret_cast<uint8_t (*)[BIG * BIG8_STRIDE]>(smem + 2 * BM * BIG8_STRIDE);
+  uint8_t (*sB)[BN * BIG8_STRIDE] = reinterpret_cast<uint8_t (*)[BN * BIG8_STRIDE]>(smem + 2 * BM * BIG8_STRIDE);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave >> 2, wn = wave & 3;  // 2 x 4 waves: rows wm*128, columns wn*64
+  const int wm = wave / WN, wn = wave % WN;  // rows wm * 32 TM, columns wn * 32 TN
   const int tiles_m = static_cast<int>((a.M + BM - 1) / BM);
-  const int tiles_n = static_cast<int>((a.N + BIG - 1) / BIG);
+  const int tiles_n = static_cast<int>((a.N + BN - 1) / BN);
   int tm, tn;
   big_tile(blockIdx.x, tiles_m, tiles_n, &tm, &tn);
   const int64_t m0 = static_cast<int64_t>(tm) * BM;
-  const int64_t n0 = static_cast<int64_t>(tn) * BIG;
+  const int64_t n0 = static_cast<int64_t>(tn) * BN;
   const int64_t Kb = a.K / 2;
   const int nk = static_cast<int>((a.K + BIG_KSTAGE - 1) / BIG_KSTAGE);  // stages (the last may be half)
   const int nk64 = static_cast<int>(a.K / 64);                            // 64-code halves in total
 
-  // Global -> LDS: a stage is 256 rows x 64 packed bytes per operand; thread
-  // loads 32 packed bytes (two 16-byte pieces) of row tid/2 of A and of B.
+  // Global -> LDS: a stage is BM (A) and BN (B) rows x 64 packed bytes; a
+  // thread loads 32 packed bytes (two 16-byte pieces) of rows tid/2 + r NT/2.
   // A half stage past K reads a clamped address; its MFMAs are skipped.
   const int lr = tid >> 1, lh = tid & 1;
-  const uint8_t* gA = a.A + min<int64_t>(m0 + lr, a.M - 1) * Kb + lh * 32;
-  const uint8_t* gB = a.B + min<int64_t>(n0 + lr, a.N - 1) * Kb + lh * 32;
+  const uint8_t* gA[PA];
+  const uint8_t* gB[PB];
+#pragma unroll
+  for (int r = 0; r < PA; ++r) gA[r] = a.A + min<int64_t>(m0 + lr + r * (NT / 2), a.M - 1) * Kb + lh * 32;
+#pragma unroll
+  for (int r = 0; r < PB; ++r) gB[r] = a.B + min<int64_t>(n0 + lr + r * (NT / 2), a.N - 1) * Kb + lh * 32;
   // Three register stages, indexed only by constants (they stay in VGPRs).
-  uint4 ra[3][2], rb[3][2];
-#define OQ_GLOAD(KS, S)                                                 \
-  {                                                                     \
-    const int h_ = min(2 * (KS) + lh, nk64 - 1);                        \
-    const int64_t off_ = static_cast<int64_t>(h_) * 32 - lh * 32;       \
-    ra[S][0] = *reinterpret_cast<const uint4*>(gA + off_);              \
-    ra[S][1] = *reinterpret_cast<const uint4*>(gA + off_ + 16);         \
-    rb[S][0] = *reinterpret_cast<const uint4*>(gB + off_);              \
-    rb[S][1] = *reinterpret_cast<const uint4*>(gB + off_ + 16);         \
+  uint4 ra[3][2 * PA], rb[3][2 * PB];
+#define OQ_GLOAD(KS, S)                                                          \
+  {                                                                              \
+    const int h_ = min(2 * (KS) + lh, nk64 - 1);                                 \
+    const int64_t off_ = static_cast<int64_t>(h_) * 32 - lh * 32;                \
+    _Pragma("unroll") for (int r_ = 0; r_ < PA; ++r_) {                          \
+      ra[S][2 * r_] = *reinterpret_cast<const uint4*>(gA[r_] + off_);            \
+      ra[S][2 * r_ + 1] = *reinterpret_cast<const uint4*>(gA[r_] + off_ + 16);   \
+    }                                                                            \
+    _Pragma("unroll") for (int r_ = 0; r_ < PB; ++r_) {                          \
+      rb[S][2 * r_] = *reinterpret_cast<const uint4*>(gB[r_] + off_);            \
+      rb[S][2 * r_ + 1] = *reinterpret_cast<const uint4*>(gB[r_] + off_ + 16);   \
+    }                                                                            \
   }
 // Widen 16 packed bytes to 32 int8 (16 * code) and store them: the same
 // within-8-byte order for A and B, so the k order of every 16-code fragment
@@ -260,49 +153,53 @@ __global__ __launch_bounds__(512, 1) void gemm_big_kernel(GemmArgs a) {
     q_[0] = widen16_u2(make_uint2((V).x, (V).y));                       \
     q_[1] = widen16_u2(make_uint2((V).z, (V).w));                       \
   }
-#define OQ_LSTORE(BUF, S)                                              \
-  {                                                                    \
-    OQ_ST32(&sA[(BUF)][lr * BIG8_STRIDE + lh * 64], ra[S][0])          \
-    OQ_ST32(&sA[(BUF)][lr * BIG8_STRIDE + lh * 64 + 32], ra[S][1])     \
-    OQ_ST32(&sB[(BUF)][lr * BIG8_STRIDE + lh * 64], rb[S][0])          \
-    OQ_ST32(&sB[(BUF)][lr * BIG8_STRIDE + lh * 64 + 32], rb[S][1])     \
+#define OQ_LSTORE(BUF, S)                                                                          \
+  {                                                                                                \
+    _Pragma("unroll") for (int r_ = 0; r_ < PA; ++r_) {                                            \
+      OQ_ST32(&sA[(BUF)][(lr + r_ * (NT / 2)) * BIG8_STRIDE + lh * 64], ra[S][2 * r_])             \
+      OQ_ST32(&sA[(BUF)][(lr + r_ * (NT / 2)) * BIG8_STRIDE + lh * 64 + 32], ra[S][2 * r_ + 1])    \
+    }                                                                                              \
+    _Pragma("unroll") for (int r_ = 0; r_ < PB; ++r_) {                                            \
+      OQ_ST32(&sB[(BUF)][(lr + r_ * (NT / 2)) * BIG8_STRIDE + lh * 64], rb[S][2 * r_])             \
+      OQ_ST32(&sB[(BUF)][(lr + r_ * (NT / 2)) * BIG8_STRIDE + lh * 64 + 32], rb[S][2 * r_ + 1])    \
+    }                                                                                              \
   }
 
-  v16i acc[4][2];
+  v16i acc[TM][TN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0;
 
   const int frow = lane & 31;
   const int fofs = 16 * (lane >> 5);  // 16 int8 codes of a 32-code sub-step
-  const uint8_t* pA = &sA[0][(wm * 128 + frow) * BIG8_STRIDE + fofs];
-  const uint8_t* pB = &sB[0][(wn * 64 + frow) * BIG8_STRIDE + fofs];
-  constexpr int ABUF = BM * BIG8_STRIDE, BBUF = BIG * BIG8_STRIDE;
+  const uint8_t* pA = &sA[0][(wm * 32 * TM + frow) * BIG8_STRIDE + fofs];
+  const uint8_t* pB = &sB[0][(wn * 32 * TN + frow) * BIG8_STRIDE + fofs];
+  constexpr int ABUF = BM * BIG8_STRIDE, BBUF = BN * BIG8_STRIDE;
 // The int8 fragments of sub-step sub + 1 are read from LDS while sub-step
 // sub is multiplied (two register sets).
 #define OQ_COMPUTE(BUF, NSUB)                                                                               \
   {                                                                                                         \
     const int boa_ = (BUF) * ABUF, bob_ = (BUF) * BBUF;                                                      \
-    v4i fa_[2][4], fb_[2][2];                                                                               \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                           \
+    v4i fa_[2][TM], fb_[2][TN];                                                                                  \
+    _Pragma("unroll") for (int i = 0; i < TM; ++i)                                                           \
       fa_[0][i] = *reinterpret_cast<const v4i*>(pA + boa_ + i * 32 * BIG8_STRIDE);                          \
-    _Pragma("unroll") for (int j = 0; j < 2; ++j)                                                           \
+    _Pragma("unroll") for (int j = 0; j < TN; ++j)                                                           \
       fb_[0][j] = *reinterpret_cast<const v4i*>(pB + bob_ + j * 32 * BIG8_STRIDE);                          \
     _Pragma("unroll") for (int sub = 0; sub < 4; ++sub) {                                                   \
       if (sub < (NSUB)) {                                                                                   \
         const int cur_ = sub & 1;                                                                           \
         if (sub + 1 < (NSUB)) {                                                                             \
-          _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                     \
+          _Pragma("unroll") for (int i = 0; i < TM; ++i)                                                     \
             fa_[cur_ ^ 1][i] = *reinterpret_cast<const v4i*>(pA + boa_ + i * 32 * BIG8_STRIDE + (sub + 1) * 32); \
-          _Pragma("unroll") for (int j = 0; j < 2; ++j)                                                     \
+          _Pragma("unroll") for (int j = 0; j < TN; ++j)                                                     \
             fb_[cur_ ^ 1][j] = *reinterpret_cast<const v4i*>(pB + bob_ + j * 32 * BIG8_STRIDE + (sub + 1) * 32); \
         }                                                                                                   \
         __builtin_amdgcn_sched_barrier(0);                                                                  \
-        _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                       \
-        _Pragma("unroll") for (int j = 0; j < 2; ++j)                                                       \
+        _Pragma("unroll") for (int i = 0; i < TM; ++i)                                                       \
+        _Pragma("unroll") for (int j = 0; j < TN; ++j)                                                       \
           acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa_[cur_][i], fb_[cur_][j], acc[i][j], 0, 0, 0); \
         __builtin_amdgcn_sched_barrier(0);                                                                  \
       }                                                                                                     \
@@ -356,15 +253,15 @@ __global__ __launch_bounds__(512, 1) void gemm_big_kernel(GemmArgs a) {
   const int col_in = lane & 31;
   const int row_grp = 4 * (lane >> 5);
   constexpr bool STAGED = EPI == EPI_F16 || EPI == EPI_BF16;
-  constexpr int TP = BIG + 8;  // halves per staged row (528 bytes)
-  static_assert(!STAGED || BM * TP * 2 <= 2 * (BM + BIG) * BIG8_STRIDE, "staged tile exceeds LDS");
+  constexpr int TP = BN + 8;  // halves per staged row
+  static_assert(!STAGED || BM * TP * 2 <= 2 * (BM + BN) * BIG8_STRIDE, "staged tile exceeds LDS");
   uint16_t* tile = reinterpret_cast<uint16_t*>(smem);
   if (STAGED) __syncthreads();  // every fragment read of the last stage is done
-  float wsc[2], bias[2], gate[2];
-  int64_t gcs[2];
+  float wsc[TN], bias[TN], gate[TN];
+  int64_t gcs[TN];
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    gcs[j] = n0 + wn * 64 + j * 32 + col_in;
+  for (int j = 0; j < TN; ++j) {
+    gcs[j] = n0 + wn * 32 * TN + j * 32 + col_in;
     wsc[j] = 0.0f;
     bias[j] = 0.0f;
     gate[j] = 1.0f;
@@ -375,10 +272,10 @@ __global__ __launch_bounds__(512, 1) void gemm_big_kernel(GemmArgs a) {
     }
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int lr0 = wm * 128 + i * 32 + 8 * q + row_grp;  // row within the tile
+      const int lr0 = wm * 32 * TM + i * 32 + 8 * q + row_grp;  // row within the tile
       const int64_t r0 = m0 + lr0;
       float xr[4] = {0.0f, 0.0f, 0.0f, 0.0f};
       if (EPI != EPI_I32) {
@@ -391,14 +288,14 @@ __global__ __launch_bounds__(512, 1) void gemm_big_kernel(GemmArgs a) {
         }
       }
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
+      for (int j = 0; j < TN; ++j) {
         const int64_t gc = gcs[j];
         if (STAGED) {
           // Rows / columns past the edge hold zeros and are not written back.
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
             const float y = static_cast<float>(acc[i][j][4 * q + u] >> 8) * xr[u] * wsc[j] + bias[j];
-            tile[(lr0 + u) * TP + wn * 64 + j * 32 + col_in] =
+            tile[(lr0 + u) * TP + wn * 32 * TN + j * 32 + col_in] =
                 EPI == EPI_F16 ? __builtin_bit_cast(uint16_t, static_cast<_Float16>(y)) : f32_to_bf16_rne(y);
           }
           continue;
@@ -422,12 +319,12 @@ __global__ __launch_bounds__(512, 1) void gemm_big_kernel(GemmArgs a) {
     }
   if (STAGED) {
     __syncthreads();
-    // 256 rows x 32 pieces of 8 outputs; thread t writes pieces t + 512 c.
+    // BM rows x BN/8 pieces of 8 outputs; thread t writes pieces t + NT c.
     uint16_t* C = static_cast<uint16_t*>(a.C);
 #pragma unroll
-    for (int c = 0; c < (BM * BIG / 8) / 512; ++c) {
-      const int id = tid + 512 * c;
-      const int lr = id >> 5, pc = (id & 31) * 8;
+    for (int c = 0; c < (BM * BN / 8) / NT; ++c) {
+      const int id = tid + NT * c;
+      const int lr = id / (BN / 8), pc = (id % (BN / 8)) * 8;
       const int64_t gr = m0 + lr, gc = n0 + pc;
       if (gr >= a.M || gc >= a.N) continue;
       const uint4 v = *reinterpret_cast<const uint4*>(&tile[lr * TP + pc]);
@@ -626,13 +523,14 @@ int gemm_validate(const uint8_t* Xq, int64_t M, const uint8_t* Wq, int64_t N, in
   return OQ_OK;
 }
 
+template <int WM, int WN, int TM, int TN>
 int launch_big(const GemmArgs& a, Epilogue epi, int64_t tiles, hipStream_t stream) {
-  const dim3 g(static_cast<unsigned>(tiles)), b(512);
+  const dim3 g(static_cast<unsigned>(tiles)), b(64 * WM * WN);
   switch (epi) {
-    case EPI_I32: hipLaunchKernelGGL((gemm_big_kernel<EPI_I32>), g, b, 0, stream, a); break;
-    case EPI_F16: hipLaunchKernelGGL((gemm_big_kernel<EPI_F16>), g, b, 0, stream, a); break;
-    case EPI_BF16: hipLaunchKernelGGL((gemm_big_kernel<EPI_BF16>), g, b, 0, stream, a); break;
-    case EPI_RESID_F32: hipLaunchKernelGGL((gemm_big_kernel<EPI_RESID_F32>), g, b, 0, stream, a); break;
+    case EPI_I32: hipLaunchKernelGGL((gemm_big_kernel<EPI_I32, WM, WN, TM, TN>), g, b, 0, stream, a); break;
+    case EPI_F16: hipLaunchKernelGGL((gemm_big_kernel<EPI_F16, WM, WN, TM, TN>), g, b, 0, stream, a); break;
+    case EPI_BF16: hipLaunchKernelGGL((gemm_big_kernel<EPI_BF16, WM, WN, TM, TN>), g, b, 0, stream, a); break;
+    case EPI_RESID_F32: hipLaunchKernelGGL((gemm_big_kernel<EPI_RESID_F32, WM, WN, TM, TN>), g, b, 0, stream, a); break;
     default: return OQ_ERR_ARG;
   }
   return launch_status();
@@ -649,18 +547,13 @@ int gemm_launch(const GemmArgs& a, Epilogue epi, hipStream_t stream) {
       default: return OQ_ERR_ARG;
     }
   }
-  // Large problems: 256 x 256 tiles when they still fill every CU.
-  const int64_t big_tiles = ((a.M + BIG - 1) / BIG) * ((a.N + BIG - 1) / BIG);
-  if (big_tiles >= 256) return launch_big(a, epi, big_tiles, stream);
-  const dim3 grid(static_cast<unsigned>((a.N + BN - 1) / BN), static_cast<unsigned>((a.M + BM - 1) / BM));
-  switch (epi) {
-    case EPI_I32: hipLaunchKernelGGL(gemm_w4a4_kernel<EPI_I32>, grid, dim3(256), 0, stream, a); break;
-    case EPI_F16: hipLaunchKernelGGL(gemm_w4a4_kernel<EPI_F16>, grid, dim3(256), 0, stream, a); break;
-    case EPI_BF16: hipLaunchKernelGGL(gemm_w4a4_kernel<EPI_BF16>, grid, dim3(256), 0, stream, a); break;
-    case EPI_RESID_F32: hipLaunchKernelGGL(gemm_w4a4_kernel<EPI_RESID_F32>, grid, dim3(256), 0, stream, a); break;
-    default: return OQ_ERR_ARG;
-  }
-  return launch_status();
+  // Large problems: 256 x 256 tiles (8 waves of 128 x 64) when they still
+  // fill every CU, else 128 x 128 tiles (4 waves of 64 x 64, two workgroups
+  // per CU).
+  const int64_t big_tiles = ((a.M + 255) / 256) * ((a.N + 255) / 256);
+  if (big_tiles >= 256) return launch_big<2, 4, 4, 2>(a, epi, big_tiles, stream);
+  const int64_t mid_tiles = ((a.M + 127) / 128) * ((a.N + 127) / 128);
+  return launch_big<2, 2, 2, 2>(a, epi, mid_tiles, stream);
 }
 
 }  // namespace oq
