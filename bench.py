@@ -106,12 +106,19 @@ def time_linears(cfg, qweights, stream):
     for name, K, N, M in dit_linears(cfg):
         X = (torch.randn((M, K), generator=g) * 2).half().to(dev)
         Wq, ws = qweights[0][names[name]]
-        Xq, xs = oq.rotate_quantize_act(X, K & -K, stream=stream)
         # Every linear is timed with the fp16-store epilogue; inside the step the
-        # o and down projections add into the fp32 residual instead.
+        # o and down projections add into the fp32 residual instead.  Up to 64
+        # tokens the step keeps the token codes in the 16-row tiled layout, and
+        # so do these timings.
         Y = torch.empty((M, N), dtype=torch.float16, device=dev)
-        gemm = lambda: oq.w4a4_linear(Xq, xs, Wq, ws, Y=Y)
-        rq = lambda: oq.rotate_quantize_act(X, K & -K, Xq=Xq, x_scale=xs)
+        if M <= 64 and K % 128 == 0:
+            Xq, xs = oq.rotate_quantize_act_tiled(X, K & -K, stream=stream)
+            gemm = lambda: oq.w4a4_linear_tiled(Xq, xs, Wq, ws, Y=Y)
+            rq = lambda: oq.rotate_quantize_act_tiled(X, K & -K, Xt=Xq, x_scale=xs)
+        else:
+            Xq, xs = oq.rotate_quantize_act(X, K & -K, stream=stream)
+            gemm = lambda: oq.w4a4_linear(Xq, xs, Wq, ws, Y=Y)
+            rq = lambda: oq.rotate_quantize_act(X, K & -K, Xq=Xq, x_scale=xs)
         t_rq = _graph_time(rq)
         t_g = _graph_time(gemm)
         b_g = gemm_bytes(M, N, K, 2)
@@ -130,13 +137,14 @@ def time_linears(cfg, qweights, stream):
 
 
 ROOFLINE_SHAPE = {"name": "gate_up", "M": 50, "N": 8192, "K": 1024}
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_skinny_gate_up_M50_traffic.txt")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_small_gate_up_M50_traffic.txt")
 
 
 def roofline_gemm(stream=None):
     """The roofline kernel: the W4A4 GEMM of the DiT block's gate|up projection
-    (M = 50 tokens, N = 2 x 4096, K = 1024, fp16 out) on seeded weights of
-    block 0, timed alone with HIP events around graph replays (no host launch
+    (M = 50 tokens, N = 2 x 4096, K = 1024, fp16 out, token codes in the
+    16-row tiled layout as inside the step) on seeded weights of block 0,
+    timed alone with HIP events around graph replays (no host launch
     overhead), and its rotate-quantize producer likewise.  Returns a dict."""
     import torch
     import paper_2605_28803_amd as oq
@@ -147,19 +155,19 @@ def roofline_gemm(stream=None):
     W = torch.from_numpy(G.gaussian(cfg.seed, "blk0/wgu", (N, K), cfg.w_std).astype(np.float16)).to(dev)
     Wq, ws = oq.quantize_weights(W, K & -K)
     X = torch.from_numpy(G.gaussian(cfg.seed, "roofline/x", (M, K)).astype(np.float16)).to(dev)
-    Xq, xs = oq.rotate_quantize_act(X, K & -K)
+    Xt, xs = oq.rotate_quantize_act_tiled(X, K & -K)
     Y = torch.empty((M, N), dtype=torch.float16, device=dev)
     torch.cuda.synchronize()
-    t_g = _graph_time(lambda: oq.w4a4_linear(Xq, xs, Wq, ws, Y=Y), reps=50, replays=20)
-    t_r = _graph_time(lambda: oq.rotate_quantize_act(X, K & -K, Xq=Xq, x_scale=xs), reps=50, replays=20)
+    t_g = _graph_time(lambda: oq.w4a4_linear_tiled(Xt, xs, Wq, ws, Y=Y), reps=50, replays=20)
+    t_r = _graph_time(lambda: oq.rotate_quantize_act_tiled(X, K & -K, Xt=Xt, x_scale=xs), reps=50, replays=20)
     b = gemm_bytes(M, N, K, 2)
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
         for line in open(TRAFFIC_FILE):
             if line.startswith("traffic_bytes_per_launch"):
                 traffic = int(float(line.split("=")[1]))
-    return {"kernel": "gemm_skinny_kernel<fp16 out, 32 columns, 4 waves> (W4A4 gate|up of a DiT block: "
-                      f"M={M}, N={N}, K={K})",
+    return {"kernel": "gemm_small_kernel<fp16 out, 32 columns, 8 waves, tiled token codes> (W4A4 gate|up of a "
+                      f"DiT block: M={M}, N={N}, K={K})",
             "bound": "hbm", "achieved": round(b / (t_g * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(b / (t_g * 1e-3) / 1e9 / HBM_PEAK_GBS, 4), "traffic": traffic,
             "avg_launch_us": round(t_g * 1e3, 3), "algorithmic_bytes_per_launch": int(b),

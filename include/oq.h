@@ -153,6 +153,53 @@ int oq_w4a4_gemm_i32(const uint8_t* Xq, int64_t M, const uint8_t* Wq, int64_t N,
                      int64_t K, int32_t* acc, int64_t ldc, void* stream);
 
 /*
+ * 16-row tiled token codes.  With few tokens (the DiT's action tokens, decode)
+ * the product of eq:lowbit_linear is bound by how fast every workgroup can
+ * re-read the token codes; this layout makes each 16-byte-per-lane load of a
+ * 16-row operand fragment one contiguous kilobyte.  It holds the same codes
+ * as Xq (K % 128 == 0):
+ *   rows padded to R16 = 16 * ceil(R / 16); total R16 * K / 2 bytes;
+ *   packed byte p (0 <= p < K/2) of row r is stored at byte
+ *   ((r / 16) * (K / 128) + p / 64) * 1024 + ((p / 16) % 4) * 256
+ *     + (r % 16) * 16 + p % 16.
+ * Bytes of padding rows are never read into a result (they may hold anything).
+ */
+
+/*
+ * oq_codes_to_tiled -- re-layout of packed codes Q [rows][K/2] (device) into
+ * the tiled layout T (device, R16 * K / 2 bytes; padding rows written as 0).
+ * rows >= 0, 128 <= K <= 16384, K % 128 == 0; Q, T 16-byte aligned.
+ * Errors: OQ_ERR_NULL, OQ_ERR_SHAPE, OQ_ERR_ALIGN, OQ_ERR_DEVICE, OQ_ERR_HIP.
+ */
+int oq_codes_to_tiled(const uint8_t* Q, int64_t rows, int64_t K, uint8_t* T, void* stream);
+
+/*
+ * oq_rotate_quantize_act_tiled -- oq_rotate_quantize_act (the same rotation,
+ * step scale and quantizer, identical codes and x_scale) writing the codes
+ * in the tiled layout: Xt device, R16 * K / 2 bytes with R = M (padding rows
+ * are left untouched).  Additionally K % 128 == 0.  Arguments and errors as
+ * oq_rotate_quantize_act.
+ */
+int oq_rotate_quantize_act_tiled(const void* X, int64_t M, int64_t K, int64_t ldx,
+                                 int32_t had_block, const float* s_table, int32_t t,
+                                 uint8_t* Xt, float* x_scale, void* stream);
+
+/*
+ * oq_w4a4_linear_tiled / oq_w4a4_gemm_i32_tiled -- oq_w4a4_linear and
+ * oq_w4a4_gemm_i32 (same results, bit for bit) with the token codes Xt in the
+ * tiled layout (R = M); Wq stays [N][K/2].  Additionally K % 128 == 0.  Meant
+ * for M <= 64; larger M is computed correctly in row groups of 64 but
+ * without the large-tile kernel of the row-layout calls.  Arguments and
+ * errors as the row-layout calls.
+ */
+int oq_w4a4_linear_tiled(const uint8_t* Xt, const float* x_scale, int64_t M,
+                         const uint8_t* Wq, const float* w_scale, const void* bias,
+                         int64_t N, int64_t K, void* Y, int64_t ldy, int32_t out_dtype,
+                         void* stream);
+int oq_w4a4_gemm_i32_tiled(const uint8_t* Xt, int64_t M, const uint8_t* Wq, int64_t N,
+                           int64_t K, int32_t* acc, int64_t ldc, void* stream);
+
+/*
  * oq_quantize_weights -- offline weight preparation on the device: fold the
  * Hadamard half of the rotation into the weight and quantize it per output
  * channel with round-to-nearest (eq:transform W' = R^T W in the output-major

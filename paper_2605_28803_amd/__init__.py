@@ -75,6 +75,35 @@ def rotate_quantize_act(X, had_block, s_table=None, t=0, Xq=None, x_scale=None, 
     return Xq, x_scale
 
 
+def tiled_bytes(rows: int, K: int) -> int:
+    """Size of the 16-row tiled code layout of a rows x K code matrix."""
+    return (rows + 15) // 16 * 16 * (K // 2)
+
+
+def rotate_quantize_act_tiled(X, had_block, s_table=None, t=0, Xt=None, x_scale=None, stream=None):
+    """As rotate_quantize_act, codes in the 16-row tiled layout (uint8 [tiled_bytes(M, K)])."""
+    M, K = X.shape
+    if Xt is None:
+        Xt = torch.empty((tiled_bytes(M, K),), dtype=torch.uint8, device=X.device)
+    if x_scale is None:
+        x_scale = torch.empty((M,), dtype=torch.float32, device=X.device)
+    keep, sp = _s_table(s_table)
+    _check(lib().oq_rotate_quantize_act_tiled(_ptr(X), M, K, X.stride(0), had_block, sp, t, _ptr(Xt),
+                                              _ptr(x_scale), _stream(stream)), "oq_rotate_quantize_act_tiled")
+    del keep
+    return Xt, x_scale
+
+
+def codes_to_tiled(Q, K=None, T=None, stream=None):
+    """Packed codes uint8 [R, K/2] -> the 16-row tiled layout (uint8 [tiled_bytes(R, K)])."""
+    R, Kh = Q.shape
+    K = 2 * Kh if K is None else K
+    if T is None:
+        T = torch.empty((tiled_bytes(R, K),), dtype=torch.uint8, device=Q.device)
+    _check(lib().oq_codes_to_tiled(_ptr(Q), R, K, _ptr(T), _stream(stream)), "oq_codes_to_tiled")
+    return T
+
+
 def rotate_debug_f32(X, had_block, s_table=None, t=0, stream=None):
     """Pre-rounding ratios z/Delta (f32 [M, K]) and x_scale."""
     M, K = X.shape
@@ -107,6 +136,28 @@ def w4a4_gemm_i32(Xq, Wq, acc=None, stream=None):
         acc = torch.empty((M, N), dtype=torch.int32, device=Xq.device)
     _check(lib().oq_w4a4_gemm_i32(_ptr(Xq), M, _ptr(Wq), N, 2 * Kh, _ptr(acc), acc.stride(0),
                                   _stream(stream)), "oq_w4a4_gemm_i32")
+    return acc
+
+
+def w4a4_linear_tiled(Xt, x_scale, Wq, w_scale, bias=None, out_dtype=OUT_F16, Y=None, stream=None):
+    """As w4a4_linear with the token codes in the 16-row tiled layout (M = len(x_scale))."""
+    M = x_scale.shape[0]
+    N, Kh = Wq.shape
+    K = 2 * Kh
+    if Y is None:
+        dt = torch.float16 if out_dtype == OUT_F16 else torch.bfloat16
+        Y = torch.empty((M, N), dtype=dt, device=Wq.device)
+    _check(lib().oq_w4a4_linear_tiled(_ptr(Xt), _ptr(x_scale), M, _ptr(Wq), _ptr(w_scale), _ptr(bias), N, K,
+                                      _ptr(Y), Y.stride(0), out_dtype, _stream(stream)), "oq_w4a4_linear_tiled")
+    return Y
+
+
+def w4a4_gemm_i32_tiled(Xt, M, Wq, acc=None, stream=None):
+    N, Kh = Wq.shape
+    if acc is None:
+        acc = torch.empty((M, N), dtype=torch.int32, device=Wq.device)
+    _check(lib().oq_w4a4_gemm_i32_tiled(_ptr(Xt), M, _ptr(Wq), N, 2 * Kh, _ptr(acc), acc.stride(0),
+                                        _stream(stream)), "oq_w4a4_gemm_i32_tiled")
     return acc
 
 

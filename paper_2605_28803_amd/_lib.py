@@ -40,9 +40,13 @@ SIGNATURES = {
     "oq_version": (C.c_char_p, []),
     "oq_check_device": (i32, []),
     "oq_rotate_quantize_act": (i32, [vp, i64, i64, i64, i32, fp, i32, vp, vp, vp]),
+    "oq_rotate_quantize_act_tiled": (i32, [vp, i64, i64, i64, i32, fp, i32, vp, vp, vp]),
     "oq_rotate_debug_f32": (i32, [vp, i64, i64, i64, i32, fp, i32, vp, vp, vp]),
     "oq_w4a4_linear": (i32, [vp, vp, i64, vp, vp, vp, i64, i64, vp, i64, i32, vp]),
     "oq_w4a4_gemm_i32": (i32, [vp, i64, vp, i64, i64, vp, i64, vp]),
+    "oq_w4a4_linear_tiled": (i32, [vp, vp, i64, vp, vp, vp, i64, i64, vp, i64, i32, vp]),
+    "oq_w4a4_gemm_i32_tiled": (i32, [vp, i64, vp, i64, i64, vp, i64, vp]),
+    "oq_codes_to_tiled": (i32, [vp, i64, i64, vp, vp]),
     "oq_quantize_weights": (i32, [vp, i64, i64, i64, i32, vp, vp, vp]),
     "oq_quantize_weights_host": (i32, [vp, i64, i64, i32, vp, vp]),
     "oq_dit_workspace_bytes": (i32, [C.POINTER(oq_dit_config), C.POINTER(C.c_size_t)]),

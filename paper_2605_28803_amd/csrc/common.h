@@ -24,6 +24,20 @@ inline int launch_status() {
   return e == hipSuccess ? OQ_OK : OQ_ERR_HIP;
 }
 
+// ---- 16-row tiled code layout -----------------------------------------------
+// Packed int4 codes of an R x K matrix (K % 128 == 0) stored for the small-M
+// product: rows are grouped in blocks of 16 (R rounded up to a multiple of 16),
+// each row in units of 64 packed bytes (128 codes).  Block (row block rb, unit
+// u) is 1024 contiguous bytes laid out as [piece 0..3][row 0..15][16 bytes]:
+// lane l of a wave loads bytes 16 l .. 16 l + 15 of a block and receives the
+// 16-byte piece l / 16 of row l % 16, which is the operand layout of
+// v_mfma_i32_16x16x64_i8.  Byte p of row r lives at
+//   ((r / 16) * (K / 128) + p / 64) * 1024 + ((p / 16) % 4) * 256 + (r % 16) * 16 + p % 16.
+__host__ __device__ inline int64_t tiled_offset(int64_t r, int64_t p, int64_t units) {
+  return (((r >> 4) * units + (p >> 6)) << 10) + (((p >> 4) & 3) << 8) + ((r & 15) << 4) + (p & 15);
+}
+inline int64_t tiled_bytes(int64_t rows, int64_t K) { return ((rows + 15) / 16) * 16 * (K / 2); }
+
 // ---- rotate-quantize ------------------------------------------------------
 struct RQPlan {
   int chunks;   // 16-byte vectors (8 channels) per thread: 1, 2, 3, 4, 6 or 8
@@ -33,8 +47,9 @@ struct RQPlan {
 bool rq_plan(int64_t K, RQPlan* p);
 
 // Validated launch (no argument checks); ratio != nullptr selects the debug output.
+// tiled: Xq is in the 16-row tiled layout (K % 128 == 0) instead of [M][K/2].
 int rq_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block, float s_t,
-              uint8_t* Xq, float* x_scale, float* ratio, hipStream_t stream);
+              uint8_t* Xq, float* x_scale, float* ratio, hipStream_t stream, bool tiled = false);
 
 // Shape/alignment validation shared by every rotate-quantize entry point.
 int rq_validate(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block,
@@ -52,6 +67,7 @@ struct GemmArgs {
   void* C;               // output
   const uint16_t* gate;  // EPI_RESID_F32: fp16 [N] per-channel multiplier (null = 1)
   int64_t M, N, K, ldc;
+  bool a_tiled;          // A is in the 16-row tiled layout (K % 128 == 0)
 };
 
 int gemm_validate(const uint8_t* Xq, int64_t M, const uint8_t* Wq, int64_t N, int64_t K,

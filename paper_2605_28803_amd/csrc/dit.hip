@@ -73,6 +73,7 @@ struct RQOut {
   float* xs;
   int logT, logb;
   float s_t, s_over_sqrtb;
+  bool tiled;  // codes in the 16-row tiled layout (the small-M product's operand)
 };
 
 // r = x W_in^T + b_in
@@ -152,7 +153,7 @@ __global__ __launch_bounds__(256) void norm_rq_kernel(const float* __restrict__ 
     }
     if (m.valid) store8_f16(h + m.row * D + k, v[c]);
   }
-  rqd::rq_core<C>(v, m, D, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr);
+  rqd::rq_core<C>(v, m, D, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr, o.tiled);
 }
 
 __device__ __forceinline__ float gelu_tanh(float x) {
@@ -187,7 +188,7 @@ __global__ __launch_bounds__(256) void gelu_rq_kernel(const uint16_t* __restrict
     for (int j = 0; j < 8; ++j) v[c][j] = GATED ? f16r(gelu_tanh(ga[j]) * up[j]) : f16r(gelu_tanh(ga[j]));
     if (m.valid) store8_f16(act + m.row * F + k, v[c]);
   }
-  rqd::rq_core<C>(v, m, F, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr);
+  rqd::rq_core<C>(v, m, F, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr, o.tiled);
 }
 
 struct AttnArgs {
@@ -424,7 +425,7 @@ __global__ __launch_bounds__(256) void combine_rq_kernel(AttnArgs a, int64_t M, 
     for (int j = 0; j < 8; ++j) v[c][j] = m.valid ? f16r(num[j] * inv) : 0.0f;
     if (m.valid) store8_f16(a.out + m.row * a.out_ld + k, v[c]);
   }
-  rqd::rq_core<C>(v, m, a.D, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr);
+  rqd::rq_core<C>(v, m, a.D, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr, o.tiled);
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
@@ -565,7 +566,7 @@ Layout layout_for(const oq_dit_config& c) {
   L.h2 = off; off += align256(M * D * 2);
   L.gu = off; off += align256(M * 2 * F * 2);
   L.act = off; off += align256(M * F * 2);
-  L.xq = off; off += align256(std::max(M * Kmax, MC * D) / 2);
+  L.xq = off; off += align256(std::max(tiled_bytes(M, Kmax), MC * D / 2));
   L.xs = off; off += align256(std::max(M, MC) * 4);
   L.part_o = off; off += align256(BH * nsplit * c.tokens * c.head_dim * 4);
   L.part_ml = off; off += align256(BH * nsplit * c.tokens * 2 * 4);
@@ -631,6 +632,7 @@ struct oq_dit {
   hipStream_t cap = nullptr;  // capture stream (graphs are replayed on the caller's stream)
   std::vector<oq_dit_graph> graphs;
   bool use_graphs = true;
+  bool tiled = false;  // block linears' token codes in the 16-row tiled layout (M <= 64)
 };
 
 namespace oq {
@@ -657,6 +659,7 @@ RQOut rq_out(oq_dit* h, int64_t K, float s, RQPlan* p) {
   o.logb = ilog2(b);
   o.s_t = s;
   o.s_over_sqrtb = static_cast<float>(static_cast<double>(s) / std::sqrt(static_cast<double>(b)));
+  o.tiled = h->tiled;
   return o;
 }
 
@@ -734,7 +737,8 @@ int gelu_rq(oq_dit* h, const uint16_t* in, uint16_t* act, float s, hipStream_t s
 int gemm(oq_dit* h, const oq_qweight& wt, int64_t K, int64_t N, Epilogue epi, void* out, int64_t ldc,
          const uint16_t* gate, hipStream_t st) {
   const int64_t M = static_cast<int64_t>(h->cfg.batch) * h->cfg.tokens;
-  GemmArgs a{at<uint8_t>(h, h->lay.xq), wt.wq, at<float>(h, h->lay.xs), wt.w_scale, nullptr, out, gate, M, N, K, ldc};
+  GemmArgs a{at<uint8_t>(h, h->lay.xq), wt.wq, at<float>(h, h->lay.xs), wt.w_scale, nullptr, out, gate, M, N, K, ldc,
+             h->tiled};
   return gemm_launch(a, epi, st);
 }
 
@@ -985,6 +989,10 @@ extern "C" int oq_dit_create(const oq_dit_config* cfg, const oq_dit_weights* w, 
   h->cap = cap;
   const char* env = std::getenv("OQ_DIT_NO_GRAPH");
   h->use_graphs = !(env && env[0] == '1');
+  // Up to 64 tokens the block products run on the small-M kernel, which reads
+  // the token codes fastest in the tiled layout; the fused producers write it.
+  const int64_t M = static_cast<int64_t>(cfg->batch) * cfg->tokens;
+  h->tiled = M <= 64 && cfg->hidden % 128 == 0 && cfg->mlp % 128 == 0;
   *out = h;
   return OQ_OK;
 }

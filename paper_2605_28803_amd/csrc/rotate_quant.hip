@@ -33,24 +33,37 @@
 namespace oq {
 namespace {
 
+// Re-layout of packed codes [R][K/2] into the 16-row tiled layout: one thread
+// per 16-byte piece; rows past R in the last block are written as zeros.
+__global__ __launch_bounds__(256) void tile_codes_kernel(const uint8_t* __restrict__ Q, int64_t R, int64_t K,
+                                                         uint8_t* __restrict__ T) {
+  const int64_t pieces_per_row = K / 32;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t rows16 = (R + 15) / 16 * 16;
+  if (i >= rows16 * pieces_per_row) return;
+  const int64_t r = i / pieces_per_row, p = (i % pieces_per_row) * 16;
+  const uint4 v = r < R ? *reinterpret_cast<const uint4*>(Q + r * (K / 2) + p) : make_uint4(0, 0, 0, 0);
+  *reinterpret_cast<uint4*>(T + tiled_offset(r, p, K / 128)) = v;
+}
+
 template <int C>
 __global__ __launch_bounds__(256) void rq_kernel(const uint16_t* __restrict__ X, int64_t M, int K,
                                                  int64_t ldx, int logT, int logb, float s_t,
                                                  float s_over_sqrtb, uint8_t* __restrict__ Xq,
-                                                 float* __restrict__ xs, float* __restrict__ ratio) {
+                                                 float* __restrict__ xs, float* __restrict__ ratio, bool tiled) {
   extern __shared__ float lds[];  // [rows_per_wg][K] when a row spans several waves
   __shared__ float red[4];
   const rqd::RowMap m = rqd::row_map(logT, M);
   float v[C][8];
   rqd::load_row_f16<C>(v, X, ldx, m);
-  rqd::rq_core<C>(v, m, K, logb, s_t, s_over_sqrtb, lds, red, Xq, xs, ratio);
+  rqd::rq_core<C>(v, m, K, logb, s_t, s_over_sqrtb, lds, red, Xq, xs, ratio, tiled);
 }
 
 // One row per wave (W = 1) or per workgroup (W > 1).
 template <int NG, int W, bool FULL>
 __global__ __launch_bounds__(256) void rq_mfma_kernel(const uint16_t* __restrict__ X, int64_t M, int64_t ldx, int logb,
                                                       float s_t, float s_over_sqrtb, uint8_t* __restrict__ Xq,
-                                                      float* __restrict__ xs, float* __restrict__ ratio) {
+                                                      float* __restrict__ xs, float* __restrict__ ratio, bool tiled) {
   // W > 1: [4 waves][NG groups][2 halves][64 lanes] float4 (consecutive lanes
   // hit consecutive 16-byte words: no bank conflicts on either side).
   extern __shared__ float4 xch[];
@@ -66,7 +79,7 @@ __global__ __launch_bounds__(256) void rq_mfma_kernel(const uint16_t* __restrict
     cur[g] = valid ? *reinterpret_cast<const rqm::rv8h*>(xr + rqm::chan0<NG>(wr, g, lane)) : rqm::rv8h{};
   rqm::rv8h a1, a2;
   rqm::hadamard_frags(lane, a1, a2);
-  rqm::rq_row<NG, W, FULL>(cur, a1, a2, row, valid, lane, wv, logb, s_t, s_over_sqrtb, Xq, xs, ratio, xch, red);
+  rqm::rq_row<NG, W, FULL>(cur, a1, a2, row, valid, lane, wv, logb, s_t, s_over_sqrtb, Xq, xs, ratio, xch, red, tiled);
 }
 
 // (NG, W) of the matrix-core variant for K channels, or false.
@@ -85,7 +98,7 @@ bool rq_mfma_shape(int64_t K, int* ng, int* w) {
 }
 
 int rq_mfma_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block, float s_t, uint8_t* Xq,
-                   float* x_scale, float* ratio, hipStream_t stream) {
+                   float* x_scale, float* ratio, hipStream_t stream, bool tiled) {
   int ng = 0, w = 0;
   rq_mfma_shape(K, &ng, &w);
   const int logb = ilog2(had_block);
@@ -99,10 +112,10 @@ int rq_mfma_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_blo
   if (ng == NG && w == W) {                                                                                   \
     if (had_block == K)                                                                                       \
       hipLaunchKernelGGL((rq_mfma_kernel<NG, W, true>), dim3(grid), dim3(256), lds, stream, x, M, ldx, logb,  \
-                         s_t, s_over_sqrtb, Xq, x_scale, ratio);                                              \
+                         s_t, s_over_sqrtb, Xq, x_scale, ratio, tiled);                                       \
     else                                                                                                      \
       hipLaunchKernelGGL((rq_mfma_kernel<NG, W, false>), dim3(grid), dim3(256), lds, stream, x, M, ldx, logb, \
-                         s_t, s_over_sqrtb, Xq, x_scale, ratio);                                              \
+                         s_t, s_over_sqrtb, Xq, x_scale, ratio, tiled);                                       \
     return launch_status();                                                                                   \
   }
   OQ_RQM(1, 1)
@@ -148,11 +161,11 @@ int rq_validate(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block,
 }
 
 int rq_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block, float s_t, uint8_t* Xq,
-              float* x_scale, float* ratio, hipStream_t stream) {
+              float* x_scale, float* ratio, hipStream_t stream, bool tiled) {
   if (M == 0) return OQ_OK;
   int ng = 0, w = 0;
   if (had_block >= 32 && rq_mfma_shape(K, &ng, &w))
-    return rq_mfma_launch(X, M, K, ldx, had_block, s_t, Xq, x_scale, ratio, stream);
+    return rq_mfma_launch(X, M, K, ldx, had_block, s_t, Xq, x_scale, ratio, stream, tiled);
   RQPlan p;
   rq_plan(K, &p);
   const int T = 1 << p.logT;
@@ -166,7 +179,8 @@ int rq_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block, f
 #define OQ_RQ_CASE(CH)                                                                                 \
   case CH:                                                                                             \
     hipLaunchKernelGGL(rq_kernel<CH>, dim3(static_cast<unsigned>(grid)), dim3(threads), lds, stream, x, \
-                       M, static_cast<int>(K), ldx, p.logT, logb, s_t, s_over_sqrtb, Xq, x_scale, ratio); \
+                       M, static_cast<int>(K), ldx, p.logT, logb, s_t, s_over_sqrtb, Xq, x_scale, ratio, \
+                       tiled);                                                                         \
     break;
   switch (p.chunks) {
     OQ_RQ_CASE(1)
@@ -197,6 +211,20 @@ extern "C" int oq_rotate_quantize_act(const void* X, int64_t M, int64_t K, int64
   return oq::rq_launch(X, M, K, ldx, had_block, s, Xq, x_scale, nullptr, static_cast<hipStream_t>(stream));
 }
 
+extern "C" int oq_rotate_quantize_act_tiled(const void* X, int64_t M, int64_t K, int64_t ldx, int32_t had_block,
+                                            const float* s_table, int32_t t, uint8_t* Xt, float* x_scale,
+                                            void* stream) {
+  int st = oq::rq_validate(X, M, K, ldx, had_block, Xt, x_scale);
+  if (st != OQ_OK) return st;
+  if (K % 128 != 0) return OQ_ERR_SHAPE;
+  if (t < 0) return OQ_ERR_ARG;
+  if (M == 0) return OQ_OK;
+  const float s = s_table ? s_table[t] : 1.0f;
+  if (!(s > 0.0f) || !std::isfinite(s)) return OQ_ERR_ARG;
+  if ((st = oq::device_check()) != OQ_OK) return st;
+  return oq::rq_launch(X, M, K, ldx, had_block, s, Xt, x_scale, nullptr, static_cast<hipStream_t>(stream), true);
+}
+
 extern "C" int oq_rotate_debug_f32(const void* X, int64_t M, int64_t K, int64_t ldx, int32_t had_block,
                                    const float* s_table, int32_t t, float* ratio, float* x_scale,
                                    void* stream) {
@@ -216,4 +244,17 @@ extern "C" int oq_quantize_weights(const void* W_u, int64_t N, int64_t K, int64_
   if (st != OQ_OK || N == 0) return st;
   if ((st = oq::device_check()) != OQ_OK) return st;
   return oq::rq_launch(W_u, N, K, ldw, had_block, 1.0f, Wq, w_scale, nullptr, static_cast<hipStream_t>(stream));
+}
+
+extern "C" int oq_codes_to_tiled(const uint8_t* Q, int64_t rows, int64_t K, uint8_t* T, void* stream) {
+  if (rows < 0 || K < 128 || K % 128 != 0 || K > 16384) return OQ_ERR_SHAPE;
+  if (rows == 0) return OQ_OK;
+  if (!Q || !T) return OQ_ERR_NULL;
+  if (!oq::aligned(Q, 16) || !oq::aligned(T, 16)) return OQ_ERR_ALIGN;
+  int st = oq::device_check();
+  if (st != OQ_OK) return st;
+  const int64_t pieces = (rows + 15) / 16 * 16 * (K / 32);
+  hipLaunchKernelGGL(oq::tile_codes_kernel, dim3(static_cast<unsigned>((pieces + 255) / 256)), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), Q, rows, K, T);
+  return oq::launch_status();
 }

@@ -15,6 +15,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "common.h"
+
 namespace oq {
 namespace rqd {
 
@@ -178,11 +180,12 @@ __device__ __forceinline__ uint32_t pack8(const uint32_t (&b)[8]) {
 // The rest of the fused pass once the row's fp32 values are in registers:
 // butterflies, row maximum, scales, codes.  `lds` must hold rows_per_wg * K
 // floats when logT > 6; `red` is a 4-float shared array.  Every thread of the
-// workgroup must call it.  ratio != nullptr writes z / Delta instead of codes.
+// workgroup must call it.  ratio != nullptr writes z / Delta instead of codes;
+// tiled selects the 16-row tiled code layout for Xq (K % 128 == 0).
 template <int C>
 __device__ __forceinline__ void rq_core(float (&v)[C][8], const RowMap& m, int K, int logb, float s_t,
                                         float s_over_sqrtb, float* lds, float* red, uint8_t* __restrict__ Xq,
-                                        float* __restrict__ xs, float* __restrict__ ratio) {
+                                        float* __restrict__ xs, float* __restrict__ ratio, bool tiled = false) {
   // Bits 0..2: inside each 8-channel chunk.
 #pragma unroll
   for (int q = 0; q < 3; ++q) {
@@ -304,7 +307,9 @@ __device__ __forceinline__ void rq_core(float (&v)[C][8], const RowMap& m, int K
     uint32_t b[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) b[j] = __float_as_uint(fmaf(v[c][j], g, kRoundMagic));
-    *reinterpret_cast<uint32_t*>(qr + chan(m, c, 0) / 2) = pack8(b);
+    const int p = chan(m, c, 0) / 2;  // a multiple of 4: the dword stays inside one 16-byte piece
+    uint8_t* dst = tiled ? Xq + tiled_offset(m.row, p, K / 128) : qr + p;
+    *reinterpret_cast<uint32_t*>(dst) = pack8(b);
   }
 }
 

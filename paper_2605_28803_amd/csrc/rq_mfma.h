@@ -75,7 +75,7 @@ template <int NG, int W, bool FULL>
 __device__ __forceinline__ void rq_row(const rv8h (&cur)[NG], const rv8h& a1, const rv8h& a2, int64_t row, bool valid,
                                        int lane, int wv, int logb, float s_t, float s_over_sqrtb,
                                        uint8_t* __restrict__ Xq, float* __restrict__ xs, float* __restrict__ ratio,
-                                       float4* xch, float* red) {
+                                       float4* xch, float* red, bool tiled) {
   using S = Shape<NG, W>;
   constexpr int K = S::K, LOGNG = S::LOGNG, LOGW = S::LOGW, GW = S::GW;
   const int rsub = wv / W, wr = wv % W;
@@ -200,7 +200,9 @@ __device__ __forceinline__ void rq_row(const rv8h (&cur)[NG], const rv8h& a1, co
     uint32_t b[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) b[e] = __float_as_uint(fmaf(v[s][e], gm, rqd::kRoundMagic));
-    *reinterpret_cast<uint32_t*>(qr + (group_of(s) * 16 + cl) * 16 + 4 * q) = rqd::pack8(b);
+    const int p = (group_of(s) * 16 + cl) * 16 + 4 * q;
+    uint8_t* dst = tiled ? Xq + tiled_offset(row, p, K / 128) : qr + p;
+    *reinterpret_cast<uint32_t*>(dst) = rqd::pack8(b);
   }
 }
 

@@ -342,26 +342,21 @@ __global__ __launch_bounds__(64 * WM * WN, 512 / (64 * WM * WN)) void gemm_big_k
 }
 
 // ---------------------------------------------------------------------------
-// Skinny product, M <= 64 (the DiT's 50 action tokens, single-token decode):
-// weight-bandwidth and latency bound, so the work is spread over many small
-// workgroups.  A workgroup owns an N tile of 16 * NB columns; its WAVES waves
-// split the K steps (interleaved) and each loads its A (token codes, 64 rows)
-// and B (weight codes) fragments straight from global memory into registers,
-// widening nibbles to int8 there, for v_mfma_i32_16x16x64_i8.  The partial
-// accumulators are summed through LDS before the shared epilogue.
+// Small-M product (the DiT's 50 action tokens, decode): weight-bandwidth and
+// latency bound, so the weight is spread over many small workgroups.  A
+// workgroup owns 16 MB rows x 16 NB columns of the output and all of K; its
+// WAVES waves take contiguous ranges of 128-code units (64 packed bytes per
+// row).  Every operand fragment is one 16-byte load per lane that feeds two
+// v_mfma_i32_16x16x64_i8 steps (the two 8-byte halves, widened to int8 in
+// registers); all of a wave's loads of UB units are issued before the first
+// MFMA.  A comes either from the 16-row tiled layout -- one load is 1024
+// contiguous bytes, 8 whole cache lines -- or from [M][K/2] rows (16 rows x
+// 64 bytes per load).  The token codes are re-read by every workgroup, so the
+// tiled form is what the DiT's fused producers write.  K % 128 == 64 (row
+// layout only) ends with one 64-code step in 8-byte pieces on the last wave.
+// The waves' partial accumulators are summed through LDS before the shared
+// epilogue.
 // ---------------------------------------------------------------------------
-
-__device__ __forceinline__ v4i widen16(uint2 w) {
-  // 8 packed bytes (16 codes) -> 16 int8 lanes holding 16 * code; even
-  // channels first within each packed dword (the same order for A and B).
-  const uint32_t m = 0xF0F0F0F0u;
-  v4i r;
-  r[0] = static_cast<int>((w.x << 4) & m);
-  r[1] = static_cast<int>(w.x & m);
-  r[2] = static_cast<int>((w.y << 4) & m);
-  r[3] = static_cast<int>(w.y & m);
-  return r;
-}
 
 // Epilogue of one output from the exact accumulator; the per-row / per-column
 // operands are passed in (loaded early by the caller).
@@ -382,113 +377,137 @@ __device__ __forceinline__ void store_out(const GemmArgs& a, int64_t off, int v,
   }
 }
 
-template <int EPI, int NB, int WAVES, int UNROLL>
-__global__ __launch_bounds__(64 * WAVES) void gemm_skinny_kernel(GemmArgs a) {
-  constexpr int BNs = 16 * NB;
-  constexpr int KSTEP = 64;                         // codes per MFMA
-  constexpr int OUT_PER_THREAD = 64 * BNs / (64 * WAVES);
-  __shared__ int red[WAVES][64 * BNs];
+template <int EPI, int NB, int WAVES, int MB, int UB, bool TILED>
+__global__ __launch_bounds__(64 * WAVES) void gemm_small_kernel(GemmArgs a) {
+  constexpr int BNs = 16 * NB, ROWS = 16 * MB, NOUT = ROWS * BNs, NT = 64 * WAVES;
+  constexpr int OPT = (NOUT + NT - 1) / NT;  // outputs per thread
+  static_assert(NT % BNs == 0, "a thread keeps one output column");
+  __shared__ int red[WAVES][NOUT];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int64_t n0 = static_cast<int64_t>(blockIdx.x) * BNs;
+  const int64_t m0 = static_cast<int64_t>(blockIdx.y) * ROWS;
   const int64_t Kb = a.K / 2;
-  const int nk = static_cast<int>(a.K / KSTEP);
-  const int koff = 8 * (lane >> 4);  // packed-byte offset of this lane's 16 codes in a k step
+  const int nu = static_cast<int>(a.K / 128);
+  const int ubeg = (nu * wave) / WAVES, uend = (nu * (wave + 1)) / WAVES;
 
-  // Epilogue operands of this thread's outputs (row i / BNs, column i % BNs
-  // for i = tid + u * blockDim): loaded before the main loop.
+  // Epilogue operands of this thread's outputs (row (tid + u NT) / BNs,
+  // column tid % BNs), loaded before the main loop.
   const int ecol = tid % BNs;
   const int64_t egc = n0 + ecol;
   const bool ecol_ok = egc < a.N;
   float e_ws = 0.0f, e_bias = 0.0f, e_gate = 1.0f;
-  float e_xs[OUT_PER_THREAD], e_res[OUT_PER_THREAD];
+  float e_xs[OPT], e_res[OPT];
   if (EPI != EPI_I32 && ecol_ok) {
     e_ws = a.ws[egc];
     if (a.bias) e_bias = static_cast<float>(__builtin_bit_cast(_Float16, a.bias[egc]));
     if (EPI == EPI_RESID_F32 && a.gate) e_gate = static_cast<float>(__builtin_bit_cast(_Float16, a.gate[egc]));
   }
 #pragma unroll
-  for (int u = 0; u < OUT_PER_THREAD; ++u) {
-    const int64_t gr = (tid + u * 64 * WAVES) / BNs;
+  for (int u = 0; u < OPT; ++u) {
+    const int64_t gr = m0 + (tid + u * NT) / BNs;
     e_xs[u] = 0.0f;
     e_res[u] = 0.0f;
-    if (EPI != EPI_I32 && gr < a.M) {
+    if (EPI != EPI_I32 && gr < a.M && tid + u * NT < NOUT) {
       e_xs[u] = a.xs[gr];
       if (EPI == EPI_RESID_F32 && ecol_ok) e_res[u] = static_cast<const float*>(a.C)[gr * a.ldc + egc];
     }
   }
 
-  const uint8_t* arow[4];
-  bool aok[4];
+  // Row-block bases: tiled -> block (m0 / 16 + rb) at unit 0 plus this lane's
+  // 16 bytes; rows -> row m0 + 16 rb + lane % 16 (clamped) at byte 0.
+  const uint8_t* abase[MB];
+  bool aok[MB];
 #pragma unroll
-  for (int rb = 0; rb < 4; ++rb) {
-    const int64_t r = rb * 16 + (lane & 15);
-    aok[rb] = r < a.M;
-    arow[rb] = a.A + (aok[rb] ? r : 0) * Kb + koff;
+  for (int rb = 0; rb < MB; ++rb) {
+    if (TILED) {
+      const int64_t blk = m0 / 16 + rb;
+      aok[rb] = blk * 16 < a.M;
+      abase[rb] = a.A + (aok[rb] ? blk : 0) * nu * 1024 + lane * 16;
+    } else {
+      const int64_t r = m0 + rb * 16 + (lane & 15);
+      aok[rb] = r < a.M;
+      abase[rb] = a.A + (aok[rb] ? r : 0) * Kb;
+    }
   }
-  const uint8_t* brow[NB];
-  bool bok[NB];
+  const uint8_t* bbase[NB];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const int64_t n = n0 + nb * 16 + (lane & 15);
-    bok[nb] = n < a.N;
-    brow[nb] = a.B + (bok[nb] ? n : 0) * Kb + koff;
-  }
+  for (int nb = 0; nb < NB; ++nb) bbase[nb] = a.B + min<int64_t>(n0 + nb * 16 + (lane & 15), a.N - 1) * Kb;
+  const int piece = 16 * (lane >> 4);  // this lane's 16 bytes of a 64-byte unit (row layout)
 
-  v4i acc[4][NB];
+  v4i acc[MB][NB];
 #pragma unroll
-  for (int rb = 0; rb < 4; ++rb)
+  for (int rb = 0; rb < MB; ++rb)
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[rb][nb] = v4i{0, 0, 0, 0};
 
-  for (int k0 = wave; k0 < nk; k0 += WAVES * UNROLL) {
-    uint2 fa[UNROLL][4], fb[UNROLL][NB];
+  for (int u0 = ubeg; u0 < uend; u0 += UB) {
+    uint4 fa[UB][MB], fb[UB][NB];
 #pragma unroll
-    for (int u = 0; u < UNROLL; ++u) {
-      const int ks = k0 + u * WAVES;
-      const bool kin = ks < nk;
-      const int64_t off = static_cast<int64_t>(ks) * (KSTEP / 2);
-#pragma unroll
-      for (int rb = 0; rb < 4; ++rb)
-        fa[u][rb] = (kin && aok[rb]) ? *reinterpret_cast<const uint2*>(arow[rb] + off) : make_uint2(0, 0);
+    for (int u = 0; u < UB; ++u) {
+      const int uu = u0 + u;
+      const bool in = uu < uend;
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
-        fb[u][nb] = (kin && bok[nb]) ? *reinterpret_cast<const uint2*>(brow[nb] + off) : make_uint2(0, 0);
+        fb[u][nb] = in ? *reinterpret_cast<const uint4*>(bbase[nb] + uu * 64 + piece) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int rb = 0; rb < MB; ++rb) {
+        const uint8_t* p = TILED ? abase[rb] + static_cast<int64_t>(uu) * 1024 : abase[rb] + uu * 64 + piece;
+        fa[u][rb] = (in && aok[rb]) ? *reinterpret_cast<const uint4*>(p) : make_uint4(0, 0, 0, 0);
+      }
     }
 #pragma unroll
-    for (int u = 0; u < UNROLL; ++u) {
-      v4i wb[NB];
+    for (int u = 0; u < UB; ++u) {
+      if (u0 + u < uend) {
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) wb[nb] = widen16(fb[u][nb]);
+        for (int h = 0; h < 2; ++h) {
+          v4i wb[NB];
 #pragma unroll
-      for (int rb = 0; rb < 4; ++rb) {
-        const v4i xa = widen16(fa[u][rb]);
+          for (int nb = 0; nb < NB; ++nb)
+            wb[nb] = widen16_u2(h ? make_uint2(fb[u][nb].z, fb[u][nb].w) : make_uint2(fb[u][nb].x, fb[u][nb].y));
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-          acc[rb][nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(xa, wb[nb], acc[rb][nb], 0, 0, 0);
+          for (int rb = 0; rb < MB; ++rb) {
+            const v4i xa =
+                widen16_u2(h ? make_uint2(fa[u][rb].z, fa[u][rb].w) : make_uint2(fa[u][rb].x, fa[u][rb].y));
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+              acc[rb][nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(xa, wb[nb], acc[rb][nb], 0, 0, 0);
+          }
+        }
       }
+    }
+  }
+  if (!TILED && (a.K & 127) && wave == WAVES - 1) {
+    // Final 64 codes: 32 packed bytes per row, 8 per lane.
+    const int64_t off = static_cast<int64_t>(nu) * 64 + 8 * (lane >> 4);
+    v4i wb[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) wb[nb] = widen16_u2(*reinterpret_cast<const uint2*>(bbase[nb] + off));
+#pragma unroll
+    for (int rb = 0; rb < MB; ++rb) {
+      const v4i xa = widen16_u2(aok[rb] ? *reinterpret_cast<const uint2*>(abase[rb] + off) : make_uint2(0, 0));
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        acc[rb][nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(xa, wb[nb], acc[rb][nb], 0, 0, 0);
     }
   }
 
   // 16x16 accumulator layout: element e of lane l is row 4*(l/16) + e, column l%16.
 #pragma unroll
-  for (int rb = 0; rb < 4; ++rb)
+  for (int rb = 0; rb < MB; ++rb)
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int row = rb * 16 + 4 * (lane >> 4) + e;
-        const int col = nb * 16 + (lane & 15);
-        red[wave][row * BNs + col] = acc[rb][nb][e];
-      }
+      for (int e = 0; e < 4; ++e)
+        red[wave][(rb * 16 + 4 * (lane >> 4) + e) * BNs + nb * 16 + (lane & 15)] = acc[rb][nb][e];
   __syncthreads();
 #pragma unroll
-  for (int u = 0; u < OUT_PER_THREAD; ++u) {
-    const int i = tid + u * 64 * WAVES;
-    const int64_t gr = i / BNs;
-    if (gr >= a.M || !ecol_ok) continue;
+  for (int u = 0; u < OPT; ++u) {
+    const int i = tid + u * NT;
+    const int64_t gr = m0 + i / BNs;
+    if (i >= NOUT || gr >= a.M || !ecol_ok) continue;
     int sum = 0;
 #pragma unroll
     for (int w = 0; w < WAVES; ++w) sum += red[w][i];
@@ -496,19 +515,30 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_skinny_kernel(GemmArgs a) {
   }
 }
 
-template <int EPI>
-int launch_skinny(const GemmArgs& a, hipStream_t stream) {
-  // Narrow tiles when N is small so that enough workgroups stream the weight;
-  // deep K gets eight waves, each with all of its k steps in flight.
-  const bool narrow = a.N <= 2048;
-  const bool deep = a.K >= 4096;
-  const unsigned nb = narrow ? 16 : 32;
-  const dim3 grid(static_cast<unsigned>((a.N + nb - 1) / nb));
-  if (narrow && deep) hipLaunchKernelGGL((gemm_skinny_kernel<EPI, 1, 8, 8>), grid, dim3(512), 0, stream, a);
-  else if (narrow) hipLaunchKernelGGL((gemm_skinny_kernel<EPI, 1, 4, 4>), grid, dim3(256), 0, stream, a);
-  else if (deep) hipLaunchKernelGGL((gemm_skinny_kernel<EPI, 2, 8, 8>), grid, dim3(512), 0, stream, a);
-  else hipLaunchKernelGGL((gemm_skinny_kernel<EPI, 2, 4, 4>), grid, dim3(256), 0, stream, a);
+// Tile shape of the small-M product: 32 columns per workgroup when N is wide
+// enough to keep more than 256 workgroups busy, else 16; waves sized so that
+// each takes one or two 128-code units of K (deeper K loops over UB units).
+template <int EPI, bool TILED, int MB>
+int launch_small_mb(const GemmArgs& a, hipStream_t stream) {
+  const bool wide = a.N > 4096;
+  const bool shallow = a.K <= 1024;
+  const int bn = wide ? 32 : 16;
+  const dim3 grid(static_cast<unsigned>((a.N + bn - 1) / bn), static_cast<unsigned>((a.M + 16 * MB - 1) / (16 * MB)));
+  if (wide && shallow) hipLaunchKernelGGL((gemm_small_kernel<EPI, 2, 8, MB, 1, TILED>), grid, dim3(512), 0, stream, a);
+  else if (wide) hipLaunchKernelGGL((gemm_small_kernel<EPI, 2, 8, MB, 2, TILED>), grid, dim3(512), 0, stream, a);
+  else if (shallow) hipLaunchKernelGGL((gemm_small_kernel<EPI, 1, 4, MB, 2, TILED>), grid, dim3(256), 0, stream, a);
+  else hipLaunchKernelGGL((gemm_small_kernel<EPI, 1, 16, MB, 2, TILED>), grid, dim3(1024), 0, stream, a);
   return launch_status();
+}
+
+template <int EPI, bool TILED>
+int launch_small(const GemmArgs& a, hipStream_t stream) {
+  return a.M <= 16 ? launch_small_mb<EPI, TILED, 1>(a, stream) : launch_small_mb<EPI, TILED, 4>(a, stream);
+}
+
+template <int EPI>
+int launch_small_any(const GemmArgs& a, hipStream_t stream) {
+  return a.a_tiled ? launch_small<EPI, true>(a, stream) : launch_small<EPI, false>(a, stream);
 }
 
 }  // namespace
@@ -538,12 +568,14 @@ int launch_big(const GemmArgs& a, Epilogue epi, int64_t tiles, hipStream_t strea
 
 int gemm_launch(const GemmArgs& a, Epilogue epi, hipStream_t stream) {
   if (a.M == 0) return OQ_OK;
-  if (a.M <= 64) {
+  // Tiled token codes always take the small-M kernel (row groups of 64 along
+  // grid.y when M > 64); row-layout codes take it up to M = 64.
+  if (a.M <= 64 || a.a_tiled) {
     switch (epi) {
-      case EPI_I32: return launch_skinny<EPI_I32>(a, stream);
-      case EPI_F16: return launch_skinny<EPI_F16>(a, stream);
-      case EPI_BF16: return launch_skinny<EPI_BF16>(a, stream);
-      case EPI_RESID_F32: return launch_skinny<EPI_RESID_F32>(a, stream);
+      case EPI_I32: return launch_small_any<EPI_I32>(a, stream);
+      case EPI_F16: return launch_small_any<EPI_F16>(a, stream);
+      case EPI_BF16: return launch_small_any<EPI_BF16>(a, stream);
+      case EPI_RESID_F32: return launch_small_any<EPI_RESID_F32>(a, stream);
       default: return OQ_ERR_ARG;
     }
   }
@@ -577,5 +609,31 @@ extern "C" int oq_w4a4_gemm_i32(const uint8_t* Xq, int64_t M, const uint8_t* Wq,
   if (st != OQ_OK || M == 0) return st;
   if ((st = oq::device_check()) != OQ_OK) return st;
   oq::GemmArgs a{Xq, Wq, nullptr, nullptr, nullptr, acc, nullptr, M, N, K, ldc};
+  return oq::gemm_launch(a, oq::EPI_I32, static_cast<hipStream_t>(stream));
+}
+
+extern "C" int oq_w4a4_linear_tiled(const uint8_t* Xt, const float* x_scale, int64_t M, const uint8_t* Wq,
+                                    const float* w_scale, const void* bias, int64_t N, int64_t K, void* Y,
+                                    int64_t ldy, int32_t out_dtype, void* stream) {
+  int st = oq::gemm_validate(Xt, M, Wq, N, K, Y, ldy, 8);
+  if (st != OQ_OK) return st;
+  if (K % 128 != 0) return OQ_ERR_SHAPE;
+  if (M == 0) return OQ_OK;
+  if (!x_scale || !w_scale) return OQ_ERR_NULL;
+  if (out_dtype != OQ_OUT_F16 && out_dtype != OQ_OUT_BF16) return OQ_ERR_ARG;
+  if (!oq::aligned(x_scale, 4) || !oq::aligned(w_scale, 4) || (bias && !oq::aligned(bias, 2))) return OQ_ERR_ALIGN;
+  if ((st = oq::device_check()) != OQ_OK) return st;
+  oq::GemmArgs a{Xt, Wq, x_scale, w_scale, static_cast<const uint16_t*>(bias), Y, nullptr, M, N, K, ldy, true};
+  return oq::gemm_launch(a, out_dtype == OQ_OUT_F16 ? oq::EPI_F16 : oq::EPI_BF16, static_cast<hipStream_t>(stream));
+}
+
+extern "C" int oq_w4a4_gemm_i32_tiled(const uint8_t* Xt, int64_t M, const uint8_t* Wq, int64_t N, int64_t K,
+                                      int32_t* acc, int64_t ldc, void* stream) {
+  int st = oq::gemm_validate(Xt, M, Wq, N, K, acc, ldc, 4);
+  if (st != OQ_OK) return st;
+  if (K % 128 != 0) return OQ_ERR_SHAPE;
+  if (M == 0) return OQ_OK;
+  if ((st = oq::device_check()) != OQ_OK) return st;
+  oq::GemmArgs a{Xt, Wq, nullptr, nullptr, nullptr, acc, nullptr, M, N, K, ldc, true};
   return oq::gemm_launch(a, oq::EPI_I32, static_cast<hipStream_t>(stream));
 }

@@ -72,6 +72,26 @@ def test_gemm_rejects_bad_arguments(lib):
     assert h(P16, 4, P16, 64, 64, P16, 66, None) == ALIGN
 
 
+def test_tiled_calls_reject_bad_arguments(lib):
+    # the tiled layout needs K % 128 == 0
+    g = lib.oq_w4a4_linear_tiled
+    assert g(P16, P16, 4, P16, P16, None, 64, 192, P16, 64, 0, None) == SHAPE
+    assert g(None, P16, 4, P16, P16, None, 64, 128, P16, 64, 0, None) == NULL
+    assert g(P16, P16, 4, P16, P16, None, 64, 128, P16, 64, 9, None) == ARG
+    h = lib.oq_w4a4_gemm_i32_tiled
+    assert h(P16, 4, P16, 64, 64, P16, 64, None) == SHAPE
+    assert h(P4, 4, P16, 64, 128, P16, 64, None) == ALIGN
+    r = lib.oq_rotate_quantize_act_tiled
+    assert r(P16, 4, 64, 64, 64, None, 0, P16, P16, None) == SHAPE
+    assert r(P16, 4, 128, 128, 128, None, -1, P16, P16, None) == ARG
+    c = lib.oq_codes_to_tiled
+    assert c(P16, 4, 192, P16, None) == SHAPE
+    assert c(P16, -1, 128, P16, None) == SHAPE
+    assert c(None, 4, 128, P16, None) == NULL
+    assert c(P16, 4, 128, P4, None) == ALIGN
+    assert c(None, 0, 128, None, None) == OK
+
+
 def test_valid_call_without_gpu_fails_cleanly(lib):
     try:
         import torch

@@ -22,7 +22,11 @@ def _codes(rng, R, K):
 
 @pytest.mark.parametrize("M,N,K", [(1, 64, 64), (50, 1024, 1024), (64, 128, 128), (200, 320, 1024),
                                    (257, 192, 1536), (130, 3072, 1024), (33, 256, 4096),
-                                   (300, 512, 6144)])
+                                   (300, 512, 6144),
+                                   # small-M row-layout kernel: a final 64-code step (K % 128 == 64),
+                                   # 16-row and 64-row groups, 16- and 32-column tiles
+                                   (50, 1024, 1088), (17, 2048, 320), (64, 520, 4160), (3, 100, 64),
+                                   (16, 4160, 2112), (50, 8192, 1024), (50, 1024, 4096)])
 def test_i32_accumulators_bit_exact(M, N, K):
     print(f"gemm i32 M={M} N={N} K={K}", flush=True)
     rng = np.random.default_rng(M + N + K)
