@@ -393,29 +393,6 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_small_kernel(GemmArgs a) {
   const int nu = static_cast<int>(a.K / 128);
   const int ubeg = (nu * wave) / WAVES, uend = (nu * (wave + 1)) / WAVES;
 
-  // Epilogue operands of this thread's outputs (row (tid + u NT) / BNs,
-  // column tid % BNs), loaded before the main loop.
-  const int ecol = tid % BNs;
-  const int64_t egc = n0 + ecol;
-  const bool ecol_ok = egc < a.N;
-  float e_ws = 0.0f, e_bias = 0.0f, e_gate = 1.0f;
-  float e_xs[OPT], e_res[OPT];
-  if (EPI != EPI_I32 && ecol_ok) {
-    e_ws = a.ws[egc];
-    if (a.bias) e_bias = static_cast<float>(__builtin_bit_cast(_Float16, a.bias[egc]));
-    if (EPI == EPI_RESID_F32 && a.gate) e_gate = static_cast<float>(__builtin_bit_cast(_Float16, a.gate[egc]));
-  }
-#pragma unroll
-  for (int u = 0; u < OPT; ++u) {
-    const int64_t gr = m0 + (tid + u * NT) / BNs;
-    e_xs[u] = 0.0f;
-    e_res[u] = 0.0f;
-    if (EPI != EPI_I32 && gr < a.M && tid + u * NT < NOUT) {
-      e_xs[u] = a.xs[gr];
-      if (EPI == EPI_RESID_F32 && ecol_ok) e_res[u] = static_cast<const float*>(a.C)[gr * a.ldc + egc];
-    }
-  }
-
   // Row-block bases: tiled -> block (m0 / 16 + rb) at unit 0 plus this lane's
   // 16 bytes; rows -> row m0 + 16 rb + lane % 16 (clamped) at byte 0.
   const uint8_t* abase[MB];
@@ -437,14 +414,9 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_small_kernel(GemmArgs a) {
   for (int nb = 0; nb < NB; ++nb) bbase[nb] = a.B + min<int64_t>(n0 + nb * 16 + (lane & 15), a.N - 1) * Kb;
   const int piece = 16 * (lane >> 4);  // this lane's 16 bytes of a 64-byte unit (row layout)
 
-  v4i acc[MB][NB];
-#pragma unroll
-  for (int rb = 0; rb < MB; ++rb)
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) acc[rb][nb] = v4i{0, 0, 0, 0};
-
-  for (int u0 = ubeg; u0 < uend; u0 += UB) {
-    uint4 fa[UB][MB], fb[UB][NB];
+  // Fragments of UB units starting at u0 (units past uend read as zeros).
+  uint4 fa[UB][MB], fb[UB][NB];
+  auto load_units = [&](int u0) {
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
       const int uu = u0 + u;
@@ -458,6 +430,39 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_small_kernel(GemmArgs a) {
         fa[u][rb] = (in && aok[rb]) ? *reinterpret_cast<const uint4*>(p) : make_uint4(0, 0, 0, 0);
       }
     }
+  };
+  // The first units' loads go out before anything else.
+  load_units(ubeg);
+
+  // Epilogue operands of this thread's outputs (row (tid + u NT) / BNs,
+  // column tid % BNs), loaded while the fragments are in flight.
+  const int ecol = tid % BNs;
+  const int64_t egc = n0 + ecol;
+  const bool ecol_ok = egc < a.N;
+  float e_ws = 0.0f, e_bias = 0.0f, e_gate = 1.0f;
+  float e_xs[OPT], e_res[OPT];
+  if (EPI != EPI_I32 && ecol_ok) {
+    e_ws = a.ws[egc];
+    if (a.bias) e_bias = static_cast<float>(__builtin_bit_cast(_Float16, a.bias[egc]));
+    if (EPI == EPI_RESID_F32 && a.gate) e_gate = static_cast<float>(__builtin_bit_cast(_Float16, a.gate[egc]));
+  }
+#pragma unroll
+  for (int u = 0; u < OPT; ++u) {
+    const int64_t gr = m0 + (tid + u * NT) / BNs;
+    e_xs[u] = 0.0f;
+    e_res[u] = 0.0f;
+    if (EPI != EPI_I32 && gr < a.M && tid + u * NT < NOUT) {
+      e_xs[u] = a.xs[gr];
+      if (EPI == EPI_RESID_F32 && ecol_ok) e_res[u] = static_cast<const float*>(a.C)[gr * a.ldc + egc];
+    }
+  }
+
+  v4i acc[MB][NB];
+#pragma unroll
+  for (int rb = 0; rb < MB; ++rb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[rb][nb] = v4i{0, 0, 0, 0};
+  auto mfma_units = [&](int u0) {
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
       if (u0 + u < uend) {
@@ -478,6 +483,13 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_small_kernel(GemmArgs a) {
         }
       }
     }
+  };
+  // First round straight-line (the MFMAs of a unit wait only for that unit's
+  // loads); deeper K continues in rounds of UB units.
+  mfma_units(ubeg);
+  for (int u0 = ubeg + UB; u0 < uend; u0 += UB) {
+    load_units(u0);
+    mfma_units(u0);
   }
   if (!TILED && (a.K & 127) && wave == WAVES - 1) {
     // Final 64 codes: 32 packed bytes per row, 8 per lane.
@@ -517,7 +529,9 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_small_kernel(GemmArgs a) {
 
 // Tile shape of the small-M product: 32 columns per workgroup when N is wide
 // enough to keep more than 256 workgroups busy, else 16; waves sized so that
-// each takes one or two 128-code units of K (deeper K loops over UB units).
+// each takes one or two 128-code units of K at K <= 1024 and up to 2 (16
+// columns) or 4 (32 columns) at K <= 4096 in its first round; deeper K runs
+// more rounds.
 template <int EPI, bool TILED, int MB>
 int launch_small_mb(const GemmArgs& a, hipStream_t stream) {
   const bool wide = a.N > 4096;
@@ -525,7 +539,7 @@ int launch_small_mb(const GemmArgs& a, hipStream_t stream) {
   const int bn = wide ? 32 : 16;
   const dim3 grid(static_cast<unsigned>((a.N + bn - 1) / bn), static_cast<unsigned>((a.M + 16 * MB - 1) / (16 * MB)));
   if (wide && shallow) hipLaunchKernelGGL((gemm_small_kernel<EPI, 2, 8, MB, 1, TILED>), grid, dim3(512), 0, stream, a);
-  else if (wide) hipLaunchKernelGGL((gemm_small_kernel<EPI, 2, 8, MB, 2, TILED>), grid, dim3(512), 0, stream, a);
+  else if (wide) hipLaunchKernelGGL((gemm_small_kernel<EPI, 2, 8, MB, 4, TILED>), grid, dim3(512), 0, stream, a);
   else if (shallow) hipLaunchKernelGGL((gemm_small_kernel<EPI, 1, 4, MB, 2, TILED>), grid, dim3(256), 0, stream, a);
   else hipLaunchKernelGGL((gemm_small_kernel<EPI, 1, 16, MB, 2, TILED>), grid, dim3(1024), 0, stream, a);
   return launch_status();
