@@ -93,9 +93,10 @@ __global__ __launch_bounds__(256) void inproj_kernel(const float* __restrict__ x
 }
 
 // h = fp16(norm(r) g (1 + sc) + sh), then rotate + quantize h.  norm is the
-// RMS norm (LN = false) or the layer norm (LN = true); sc and sh may be null
-// (zero).
-template <int C, bool LN>
+// RMS norm (LN = false) or the layer norm (LN = true); SC = false means no
+// scale vector (sc is not read, taken as zero); sh is always read.  Every
+// load of the row is issued before the first reduction.
+template <int C, bool LN, bool SC>
 __global__ __launch_bounds__(256) void norm_rq_kernel(const float* __restrict__ r, const uint16_t* __restrict__ g,
                                                       const uint16_t* __restrict__ sc,
                                                       const uint16_t* __restrict__ sh, uint16_t* __restrict__ h,
@@ -106,33 +107,37 @@ __global__ __launch_bounds__(256) void norm_rq_kernel(const float* __restrict__ 
   __shared__ float red3[4];
   const rqd::RowMap m = rqd::row_map(o.logT, M);
   float v[C][8];
-  float sum = 0.0f;
   const float* rr = r + (m.valid ? m.row : 0) * D;
 #pragma unroll
   for (int c = 0; c < C; ++c) {
     const int k = rqd::chan(m, c, 0);
-    float4 p0 = make_float4(0, 0, 0, 0), p1 = p0;
-    if (m.valid) {
-      p0 = *reinterpret_cast<const float4*>(rr + k);
-      p1 = *reinterpret_cast<const float4*>(rr + k + 4);
-    }
+    const float4 p0 = *reinterpret_cast<const float4*>(rr + k);
+    const float4 p1 = *reinterpret_cast<const float4*>(rr + k + 4);
     v[c][0] = p0.x; v[c][1] = p0.y; v[c][2] = p0.z; v[c][3] = p0.w;
     v[c][4] = p1.x; v[c][5] = p1.y; v[c][6] = p1.z; v[c][7] = p1.w;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) sum += v[c][j];
   }
   float gg[C][8], s1[C][8], s2[C][8];
 #pragma unroll
   for (int c = 0; c < C; ++c) {
     const int k = rqd::chan(m, c, 0);
     load8_f16(g + k, gg[c]);
+    load8_f16(sh + k, s2[c]);
+    if (SC) {
+      load8_f16(sc + k, s1[c]);
+    } else {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) s1[c][j] = s2[c][j] = 0.0f;
-    if (sc) load8_f16(sc + k, s1[c]);
-    if (sh) load8_f16(sh + k, s2[c]);
+      for (int j = 0; j < 8; ++j) s1[c][j] = 0.0f;
+    }
   }
   float mu = 0.0f;
-  if constexpr (LN) mu = rqd::row_reduce<false>(sum, m, red3) / static_cast<float>(D);
+  if constexpr (LN) {
+    float sum = 0.0f;
+#pragma unroll
+    for (int c = 0; c < C; ++c)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) sum += v[c][j];
+    mu = rqd::row_reduce<false>(sum, m, red3) / static_cast<float>(D);
+  }
   float ss = 0.0f;
 #pragma unroll
   for (int c = 0; c < C; ++c)
@@ -156,10 +161,16 @@ __global__ __launch_bounds__(256) void norm_rq_kernel(const float* __restrict__ 
   rqd::rq_core<C>(v, m, D, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr, o.tiled);
 }
 
+// gelu_tanh(x) = 0.5 x (1 + tanh(u)), u = sqrt(2/pi) (x + 0.044715 x^3).
+// Since 0.5 (1 + tanh(u)) = 1 / (1 + e^(-2u)), this is x / (1 + e^(-2u)):
+// one hardware exp and one reciprocal (each within a few fp32 ulp; the result
+// is rounded to fp16 by the caller).  e^(-2u) -> inf gives -0 for very
+// negative x, e^(-2u) -> 0 gives x.
 __device__ __forceinline__ float gelu_tanh(float x) {
   const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
   const float k1 = 0.044715f;
-  return 0.5f * x * (1.0f + tanhf(k0 * fmaf(k1 * x * x, x, x)));
+  const float u = k0 * fmaf(k1 * x * x, x, x);
+  return x * __builtin_amdgcn_rcpf(1.0f + __expf(-2.0f * u));
 }
 
 // GATED: a = fp16(gelu_tanh(gate) up) from gu = [gate | up] (fp16 [M][2F]);
@@ -235,34 +246,44 @@ __global__ __launch_bounds__(64 * WAVES) void attn_partial_kernel(AttnArgs a) {
   const int nk = min(KS, n_keys - k0);
   const int hd = HD > 0 ? HD : a.hd;
 
-  auto key_ptr = [&](int j, const uint16_t* pre, const uint16_t* own) -> const uint16_t* {
+  __builtin_assume(tid < 64 * WAVES);
+  // Row base of key j of this split: the first P keys are prefix rows, the
+  // rest the sample's own rows.  Both candidate addresses are formed in full
+  // and the per-lane choice selects between them (a select between two
+  // argument fields would become a per-lane load from the selected argument
+  // address, in front of every K / V load).
+  const uint16_t* const k_pre = a.k_pre;
+  const uint16_t* const v_pre = a.v_pre;
+  const uint16_t* const k_own = a.k_own;
+  const uint16_t* const v_own = a.v_own;
+  const int64_t pre_ld = a.pre_ld, own_ld = a.own_ld;
+  const int P = a.P, own_keys = a.own_keys;
+  auto key_row = [&](int j, const uint16_t* pre_base, const uint16_t* own_base) -> const uint16_t* {
     const int key = k0 + j;
-    if (key < a.P) return pre + (static_cast<int64_t>(b) * a.P + key) * a.pre_ld + h * hd;
-    return own + (static_cast<int64_t>(b) * a.own_keys + (key - a.P)) * a.own_ld + h * hd;
+    const uint16_t* pre_p = pre_base + (static_cast<int64_t>(b) * P + key) * pre_ld + h * hd;
+    const uint16_t* own_p = own_base + (static_cast<int64_t>(b) * own_keys + (key - P)) * own_ld + h * hd;
+    return key < P ? pre_p : own_p;
   };
 
-  // Loads are branch-free so that they issue together: an out-of-range key,
-  // query row or head dimension reads a clamped valid address and the value
-  // is replaced by zeros.
-  // Stage V^T: thread (key j = tid % 64, dim group) loads 8 dims of one key.
+  // Every global load of the workgroup is issued before the first LDS write
+  // or MFMA.  Loads are branch-free: an out-of-range key, query row or head
+  // dimension reads a clamped valid address, and its value is replaced by
+  // zero where it is used (never by overwriting a register a load is still
+  // filling, which would stall on that load).
+  // V: thread (key j = tid % 64, dims d8 = 8 (tid / 64) + 8 WAVES i) loads 8 dims.
+  constexpr int VIT = HD > 0 ? (HD + 8 * WAVES - 1) / (8 * WAVES) : kMaxHeadDim / (8 * WAVES);
+  const int vj = tid & 63;
+  const bool vjok = vj < nk;
+  uint4 vraw[VIT];
   {
-    const int j = tid & 63;
-    const bool jok = j < nk;
-    const uint16_t* vp = key_ptr(jok ? j : 0, a.v_pre, a.v_own);
+    const uint16_t* vp = key_row(vjok ? vj : 0, v_pre, v_own);
 #pragma unroll
-    for (int d8 = (tid >> 6) * 8; d8 < hd; d8 += 8 * WAVES) {
-      uint4 raw = *reinterpret_cast<const uint4*>(vp + d8);
-      if (!jok) raw = make_uint4(0, 0, 0, 0);
-      const uint32_t wv[4] = {raw.x, raw.y, raw.z, raw.w};
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        sVt[d8 + 2 * q][j] = static_cast<uint16_t>(wv[q] & 0xFFFFu);
-        sVt[d8 + 2 * q + 1][j] = static_cast<uint16_t>(wv[q] >> 16);
-      }
+    for (int i = 0; i < VIT; ++i) {
+      const int d8 = (tid >> 6) * 8 + i * 8 * WAVES;
+      vraw[i] = *reinterpret_cast<const uint4*>(vp + (d8 < hd ? d8 : 0));
     }
   }
-
-  // S = Q K^T for this wave's 16 rows.
+  // Q (this wave's 16 rows) and K (the split's 64 keys) fragments.
   const int qrow = 16 * w + (lane & 15);
   const bool qok = qrow < a.S;
   const int kq = 8 * (lane >> 4);
@@ -275,23 +296,42 @@ __global__ __launch_bounds__(64 * WAVES) void attn_partial_kernel(AttnArgs a) {
   for (int nb = 0; nb < KS / 16; ++nb) {
     const int j = nb * 16 + (lane & 15);
     kok[nb] = j < nk;
-    kp[nb] = key_ptr(kok[nb] ? j : 0, a.k_pre, a.k_own);
+    kp[nb] = key_row(kok[nb] ? j : 0, k_pre, k_own);
   }
-  // Issue every Q and K load of the wave before the first MFMA.
-  v8h qa[KKMAX], kb[KKMAX][KS / 16];
+  v8h qraw[KKMAX], kraw[KKMAX][KS / 16];
+  bool dok[KKMAX];
 #pragma unroll
   for (int kk = 0; kk < KKMAX; ++kk) {
     // hd % 8 == 0: a chunk of 8 dims is wholly inside or outside the head.
-    const bool dok = kk < nkk && kk * 32 + kq < hd;
-    const int d = dok ? kk * 32 + kq : 0;
-    qa[kk] = *reinterpret_cast<const v8h*>(qp + d);
-    if (!(dok && qok)) qa[kk] = v8h{};
+    dok[kk] = kk < nkk && kk * 32 + kq < hd;
+    const int d = dok[kk] ? kk * 32 + kq : 0;
+    qraw[kk] = *reinterpret_cast<const v8h*>(qp + d);
 #pragma unroll
-    for (int nb = 0; nb < KS / 16; ++nb) {
-      kb[kk][nb] = *reinterpret_cast<const v8h*>(kp[nb] + d);
-      if (!(dok && kok[nb])) kb[kk][nb] = v8h{};
+    for (int nb = 0; nb < KS / 16; ++nb) kraw[kk][nb] = *reinterpret_cast<const v8h*>(kp[nb] + d);
+  }
+
+  // Stage V^T [dim][key] in LDS.
+#pragma unroll
+  for (int i = 0; i < VIT; ++i) {
+    const int d8 = (tid >> 6) * 8 + i * 8 * WAVES;
+    if (d8 < hd) {
+      const uint32_t wv[4] = {vjok ? vraw[i].x : 0u, vjok ? vraw[i].y : 0u, vjok ? vraw[i].z : 0u,
+                              vjok ? vraw[i].w : 0u};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        sVt[d8 + 2 * q][vj] = static_cast<uint16_t>(wv[q] & 0xFFFFu);
+        sVt[d8 + 2 * q + 1][vj] = static_cast<uint16_t>(wv[q] >> 16);
+      }
     }
   }
+  v8h qa[KKMAX], kb[KKMAX][KS / 16];
+#pragma unroll
+  for (int kk = 0; kk < KKMAX; ++kk) {
+    qa[kk] = (dok[kk] && qok) ? qraw[kk] : v8h{};
+#pragma unroll
+    for (int nb = 0; nb < KS / 16; ++nb) kb[kk][nb] = (dok[kk] && kok[nb]) ? kraw[kk][nb] : v8h{};
+  }
+
   v4f sc[KS / 16];
 #pragma unroll
   for (int nb = 0; nb < KS / 16; ++nb) {
@@ -694,7 +734,7 @@ bool with_chunks(int chunks, F&& f) {
   }
 }
 
-// h = fp16(norm(r) g (1 + sc) + sh) and its codes (sc, sh may be null).
+// h = fp16(norm(r) g (1 + sc) + sh) and its codes (sc may be null: no scale).
 int norm_rq(oq_dit* h, const float* r, const void* g, const uint16_t* sc, const uint16_t* sh, uint16_t* out,
             float s, hipStream_t st) {
   const int64_t M = static_cast<int64_t>(h->cfg.batch) * h->cfg.tokens;
@@ -704,13 +744,21 @@ int norm_rq(oq_dit* h, const float* r, const void* g, const uint16_t* sc, const 
   const FusedLaunch fl = fused_launch(M, D, p);
   const uint16_t* gg = static_cast<const uint16_t*>(g);
   const bool ln = is_gr00t(h->cfg);
+  if (!sh) return OQ_ERR_NULL;
   const bool ok = with_chunks(p.chunks, [&](auto C) {
-    if (ln)
-      hipLaunchKernelGGL((norm_rq_kernel<decltype(C)::value, true>), fl.grid, fl.block, fl.lds, st, r, gg, sc, sh,
-                         out, M, static_cast<int>(D), o);
+    constexpr int CC = decltype(C)::value;
+    if (ln && sc)
+      hipLaunchKernelGGL((norm_rq_kernel<CC, true, true>), fl.grid, fl.block, fl.lds, st, r, gg, sc, sh, out, M,
+                         static_cast<int>(D), o);
+    else if (ln)
+      hipLaunchKernelGGL((norm_rq_kernel<CC, true, false>), fl.grid, fl.block, fl.lds, st, r, gg, sc, sh, out, M,
+                         static_cast<int>(D), o);
+    else if (sc)
+      hipLaunchKernelGGL((norm_rq_kernel<CC, false, true>), fl.grid, fl.block, fl.lds, st, r, gg, sc, sh, out, M,
+                         static_cast<int>(D), o);
     else
-      hipLaunchKernelGGL((norm_rq_kernel<decltype(C)::value, false>), fl.grid, fl.block, fl.lds, st, r, gg, sc, sh,
-                         out, M, static_cast<int>(D), o);
+      hipLaunchKernelGGL((norm_rq_kernel<CC, false, false>), fl.grid, fl.block, fl.lds, st, r, gg, sc, sh, out, M,
+                         static_cast<int>(D), o);
   });
   return ok ? launch_status() : OQ_ERR_SHAPE;
 }
