@@ -185,20 +185,39 @@ __global__ __launch_bounds__(256) void gelu_rq_kernel(const uint16_t* __restrict
   float v[C][8];
   const int64_t ld = GATED ? 2 * static_cast<int64_t>(F) : F;
   const uint16_t* gr = gu + (m.valid ? m.row : 0) * ld;
+  // Every chunk's loads first (one round trip), then the arithmetic.
+  uint4 graw[C], uraw[C];
 #pragma unroll
   for (int c = 0; c < C; ++c) {
     const int k = rqd::chan(m, c, 0);
-    float ga[8], up[8];
+    graw[c] = *reinterpret_cast<const uint4*>(gr + k);
+    if (GATED) uraw[c] = *reinterpret_cast<const uint4*>(gr + F + k);
+  }
 #pragma unroll
-    for (int j = 0; j < 8; ++j) ga[j] = 0.0f, up[j] = 1.0f;
-    if (m.valid) {
-      load8_f16(gr + k, ga);
-      if (GATED) load8_f16(gr + F + k, up);
+  for (int c = 0; c < C; ++c) {
+    const uint32_t gw[4] = {graw[c].x, graw[c].y, graw[c].z, graw[c].w};
+    float up[8] = {1, 1, 1, 1, 1, 1, 1, 1};
+    if (GATED) {
+      const uint32_t uw[4] = {uraw[c].x, uraw[c].y, uraw[c].z, uraw[c].w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        up[2 * q] = h2f(uw[q] & 0xFFFFu);
+        up[2 * q + 1] = h2f(uw[q] >> 16);
+      }
     }
 #pragma unroll
-    for (int j = 0; j < 8; ++j) v[c][j] = GATED ? f16r(gelu_tanh(ga[j]) * up[j]) : f16r(gelu_tanh(ga[j]));
-    if (m.valid) store8_f16(act + m.row * F + k, v[c]);
+    for (int q = 0; q < 4; ++q) {
+      v[c][2 * q] = f16r(gelu_tanh(h2f(gw[q] & 0xFFFFu)) * up[2 * q]);
+      v[c][2 * q + 1] = f16r(gelu_tanh(h2f(gw[q] >> 16)) * up[2 * q + 1]);
+    }
+    if (!m.valid) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[c][j] = 0.0f;
+    }
   }
+#pragma unroll
+  for (int c = 0; c < C; ++c)
+    if (m.valid) store8_f16(act + m.row * F + rqd::chan(m, c, 0), v[c]);
   rqd::rq_core<C>(v, m, F, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr, o.tiled);
 }
 

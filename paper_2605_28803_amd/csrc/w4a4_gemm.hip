@@ -394,7 +394,11 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_small_kernel(GemmArgs a) {
   const int ubeg = (nu * wave) / WAVES, uend = (nu * (wave + 1)) / WAVES;
 
   // Row-block bases: tiled -> block (m0 / 16 + rb) at unit 0 plus this lane's
-  // 16 bytes; rows -> row m0 + 16 rb + lane % 16 (clamped) at byte 0.
+  // 16 bytes; rows -> row m0 + 16 rb + lane % 16 at byte 0.  Out-of-range
+  // blocks / rows read a clamped valid address; their fragments are replaced
+  // by zeros where they are used.  Every load is unconditional, so the
+  // compiler counts them exactly and each MFMA waits only for its own
+  // operands.
   const uint8_t* abase[MB];
   bool aok[MB];
 #pragma unroll
@@ -414,46 +418,47 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_small_kernel(GemmArgs a) {
   for (int nb = 0; nb < NB; ++nb) bbase[nb] = a.B + min<int64_t>(n0 + nb * 16 + (lane & 15), a.N - 1) * Kb;
   const int piece = 16 * (lane >> 4);  // this lane's 16 bytes of a 64-byte unit (row layout)
 
-  // Fragments of UB units starting at u0 (units past uend read as zeros).
+  // Fragments of UB units starting at u0 (a unit past uend reads unit uend - 1
+  // or 0 again; its MFMAs are skipped).
   uint4 fa[UB][MB], fb[UB][NB];
   auto load_units = [&](int u0) {
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
-      const int uu = u0 + u;
-      const bool in = uu < uend;
+      const int uu = u0 + u < uend ? u0 + u : max(uend - 1, 0);
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-        fb[u][nb] = in ? *reinterpret_cast<const uint4*>(bbase[nb] + uu * 64 + piece) : make_uint4(0, 0, 0, 0);
+      for (int nb = 0; nb < NB; ++nb) fb[u][nb] = *reinterpret_cast<const uint4*>(bbase[nb] + uu * 64 + piece);
 #pragma unroll
-      for (int rb = 0; rb < MB; ++rb) {
-        const uint8_t* p = TILED ? abase[rb] + static_cast<int64_t>(uu) * 1024 : abase[rb] + uu * 64 + piece;
-        fa[u][rb] = (in && aok[rb]) ? *reinterpret_cast<const uint4*>(p) : make_uint4(0, 0, 0, 0);
-      }
+      for (int rb = 0; rb < MB; ++rb)
+        fa[u][rb] = *reinterpret_cast<const uint4*>(TILED ? abase[rb] + static_cast<int64_t>(uu) * 1024
+                                                           : abase[rb] + uu * 64 + piece);
     }
   };
   // The first units' loads go out before anything else.
   load_units(ubeg);
 
   // Epilogue operands of this thread's outputs (row (tid + u NT) / BNs,
-  // column tid % BNs), loaded while the fragments are in flight.
+  // column tid % BNs), loaded while the fragments are in flight, from clamped
+  // addresses (the values of outputs that are not stored do not matter).
   const int ecol = tid % BNs;
   const int64_t egc = n0 + ecol;
   const bool ecol_ok = egc < a.N;
+  const int64_t egc_c = ecol_ok ? egc : 0;
   float e_ws = 0.0f, e_bias = 0.0f, e_gate = 1.0f;
   float e_xs[OPT], e_res[OPT];
-  if (EPI != EPI_I32 && ecol_ok) {
-    e_ws = a.ws[egc];
-    if (a.bias) e_bias = static_cast<float>(__builtin_bit_cast(_Float16, a.bias[egc]));
-    if (EPI == EPI_RESID_F32 && a.gate) e_gate = static_cast<float>(__builtin_bit_cast(_Float16, a.gate[egc]));
+  if (EPI != EPI_I32) {
+    e_ws = a.ws[egc_c];
+    if (a.bias) e_bias = static_cast<float>(__builtin_bit_cast(_Float16, a.bias[egc_c]));
+    if (EPI == EPI_RESID_F32 && a.gate) e_gate = static_cast<float>(__builtin_bit_cast(_Float16, a.gate[egc_c]));
   }
 #pragma unroll
   for (int u = 0; u < OPT; ++u) {
     const int64_t gr = m0 + (tid + u * NT) / BNs;
+    const int64_t gr_c = gr < a.M ? gr : 0;
     e_xs[u] = 0.0f;
     e_res[u] = 0.0f;
-    if (EPI != EPI_I32 && gr < a.M && tid + u * NT < NOUT) {
-      e_xs[u] = a.xs[gr];
-      if (EPI == EPI_RESID_F32 && ecol_ok) e_res[u] = static_cast<const float*>(a.C)[gr * a.ldc + egc];
+    if (EPI != EPI_I32) {
+      e_xs[u] = a.xs[gr_c];
+      if (EPI == EPI_RESID_F32) e_res[u] = static_cast<const float*>(a.C)[gr_c * a.ldc + egc_c];
     }
   }
 
@@ -474,8 +479,8 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_small_kernel(GemmArgs a) {
             wb[nb] = widen16_u2(h ? make_uint2(fb[u][nb].z, fb[u][nb].w) : make_uint2(fb[u][nb].x, fb[u][nb].y));
 #pragma unroll
           for (int rb = 0; rb < MB; ++rb) {
-            const v4i xa =
-                widen16_u2(h ? make_uint2(fa[u][rb].z, fa[u][rb].w) : make_uint2(fa[u][rb].x, fa[u][rb].y));
+            const uint2 pa = h ? make_uint2(fa[u][rb].z, fa[u][rb].w) : make_uint2(fa[u][rb].x, fa[u][rb].y);
+            const v4i xa = widen16_u2(aok[rb] ? pa : make_uint2(0, 0));
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
               acc[rb][nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(xa, wb[nb], acc[rb][nb], 0, 0, 0);
