@@ -25,7 +25,8 @@ Also reported (same JSON line):
 JSON lines to gpurun_out/sweep.jsonl instead; --roofline-only runs just the
 roofline kernel measurement (the command the committed rocprofv3 summaries of
 that kernel were taken with); --copy-calibration runs a plain copy of known
-size (the counter calibration reference).
+size (the counter calibration reference); --gr00t-only times just the
+GR00T-shaped step.
 """
 from __future__ import annotations
 
@@ -525,6 +526,7 @@ def main():
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--roofline-only", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--gr00t-only", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (--gpus must be 1)", file=sys.stderr)
@@ -535,6 +537,8 @@ def main():
         print(json.dumps({"roofline": roofline_gemm()}), flush=True)
     elif args.copy_calibration:
         copy_calibration()
+    elif args.gr00t_only:
+        print(json.dumps({"dit_gr00t": gr00t_step()}), flush=True)
     else:
         run_dit(args)
 

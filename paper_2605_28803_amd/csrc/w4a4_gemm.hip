@@ -257,44 +257,57 @@ __global__ __launch_bounds__(64 * WM * WN, 512 / (64 * WM * WN)) void gemm_big_k
   static_assert(!STAGED || BM * TP * 2 <= 2 * (BM + BN) * BIG8_STRIDE, "staged tile exceeds LDS");
   uint16_t* tile = reinterpret_cast<uint16_t*>(smem);
   if (STAGED) __syncthreads();  // every fragment read of the last stage is done
+  // Per-column operands, then per 32-row block: every load of the block
+  // (token scales, and for the residual epilogue the old residual values) is
+  // issued from clamped addresses before the block's first store, so that the
+  // in-order memory counter never makes a load wait behind a store.
   float wsc[TN], bias[TN], gate[TN];
   int64_t gcs[TN];
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
     gcs[j] = n0 + wn * 32 * TN + j * 32 + col_in;
+    const int64_t gcc = gcs[j] < a.N ? gcs[j] : a.N - 1;
     wsc[j] = 0.0f;
     bias[j] = 0.0f;
     gate[j] = 1.0f;
-    if (EPI != EPI_I32 && gcs[j] < a.N) {
-      wsc[j] = a.ws[gcs[j]];
-      if (a.bias) bias[j] = static_cast<float>(__builtin_bit_cast(_Float16, a.bias[gcs[j]]));
-      if (EPI == EPI_RESID_F32 && a.gate) gate[j] = static_cast<float>(__builtin_bit_cast(_Float16, a.gate[gcs[j]]));
+    if (EPI != EPI_I32) {
+      wsc[j] = a.ws[gcc];
+      if (a.bias) bias[j] = static_cast<float>(__builtin_bit_cast(_Float16, a.bias[gcc]));
+      if (EPI == EPI_RESID_F32 && a.gate) gate[j] = static_cast<float>(__builtin_bit_cast(_Float16, a.gate[gcc]));
     }
   }
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+  for (int i = 0; i < TM; ++i) {
+    float xr[4][4];
+    float rold[4][TN][4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int64_t r0 = m0 + wm * 32 * TM + i * 32 + 8 * q + row_grp;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int64_t gr = r0 + u < a.M ? r0 + u : a.M - 1;
+        xr[q][u] = EPI != EPI_I32 ? a.xs[gr] : 0.0f;
+        if (EPI == EPI_RESID_F32) {
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            const int64_t gcc = gcs[j] < a.N ? gcs[j] : a.N - 1;
+            rold[q][j][u] = static_cast<const float*>(a.C)[gr * a.ldc + gcc];
+          }
+        }
+      }
+    }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int lr0 = wm * 32 * TM + i * 32 + 8 * q + row_grp;  // row within the tile
       const int64_t r0 = m0 + lr0;
-      float xr[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-      if (EPI != EPI_I32) {
-        if (r0 + 3 < a.M && (reinterpret_cast<uintptr_t>(a.xs + r0) & 15) == 0) {
-          const float4 t = *reinterpret_cast<const float4*>(a.xs + r0);
-          xr[0] = t.x; xr[1] = t.y; xr[2] = t.z; xr[3] = t.w;
-        } else {
-#pragma unroll
-          for (int u = 0; u < 4; ++u) xr[u] = r0 + u < a.M ? a.xs[r0 + u] : 0.0f;
-        }
-      }
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int64_t gc = gcs[j];
         if (STAGED) {
-          // Rows / columns past the edge hold zeros and are not written back.
+          // Rows / columns past the edge are staged but not written back.
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
-            const float y = static_cast<float>(acc[i][j][4 * q + u] >> 8) * xr[u] * wsc[j] + bias[j];
+            const float y = static_cast<float>(acc[i][j][4 * q + u] >> 8) * xr[q][u] * wsc[j] + bias[j];
             tile[(lr0 + u) * TP + wn * 32 * TN + j * 32 + col_in] =
                 EPI == EPI_F16 ? __builtin_bit_cast(uint16_t, static_cast<_Float16>(y)) : f32_to_bf16_rne(y);
           }
@@ -310,13 +323,13 @@ __global__ __launch_bounds__(64 * WM * WN, 512 / (64 * WM * WN)) void gemm_big_k
           if (EPI == EPI_I32) {
             static_cast<int32_t*>(a.C)[off] = v;
           } else {
-            const float y = static_cast<float>(v) * xr[u] * wsc[j] + bias[j];
-            float* rp = static_cast<float*>(a.C) + off;
-            *rp = fmaf(gate[j], y, *rp);
+            const float y = static_cast<float>(v) * xr[q][u] * wsc[j] + bias[j];
+            static_cast<float*>(a.C)[off] = fmaf(gate[j], y, rold[q][j][u]);
           }
         }
       }
     }
+  }
   if (STAGED) {
     __syncthreads();
     // BM rows x BN/8 pieces of 8 outputs; thread t writes pieces t + NT c.
