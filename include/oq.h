@@ -354,6 +354,15 @@ int oq_dit_denoise(oq_dit* h, float* x, int32_t n_steps, void* stream);
  * for per-block parity checks with a teacher-forced input. */
 int oq_dit_run_block(oq_dit* h, int32_t l, int32_t t, float* resid, void* stream);
 
+/* Parity check of the fused producers (each writes a linear's fp16 input and
+ * quantizes it in the same kernel, eq:scale / eq:quant after the rotation of
+ * eq:blockdiag): run block l of step t only up to and including the producer
+ * of quantization site `site` (0: the q|k|v (q) input, 1: the o input, 2:
+ * the gate|up (ff0) input, 3: the down (ff2) input).  That site's codes and
+ * token scales are then in the workspace (oq_dit_intermediates.codes,
+ * .x_scale).  Errors: as oq_dit_run_block; OQ_ERR_ARG for a bad site. */
+int oq_dit_run_block_until(oq_dit* h, int32_t l, int32_t t, float* resid, int32_t site, void* stream);
+
 /* Intermediate tensors of the most recent block the handle ran (fp16,
  * row-major, M = batch * tokens rows), for per-site parity checks: every
  * quantized linear's fp16 input and every fp16 output of the block can be
@@ -370,6 +379,12 @@ typedef struct {
                             its last block (oq_dit_run_block uses the caller's) */
   const void* cond_kv;   /* gr00t: [n_blocks/2 rounded up][B*P][2D] k|v of the
                             conditioning tokens per even block; pi: NULL       */
+  const void* codes;     /* packed codes of the last quantization site the
+                            handle produced (its fp16 input is h1, attn, h2 or
+                            act): [M][K/2], or the 16-row tiled layout when
+                            codes_tiled is 1                                  */
+  const float* x_scale;  /* [M] token scales of the same site                 */
+  int32_t codes_tiled;   /* 1: codes in the 16-row tiled layout (M <= 64)      */
 } oq_dit_intermediates;
 
 /* Fill *out with the intermediate pointers.  Errors: OQ_ERR_NULL, OQ_ERR_WORKSPACE. */

@@ -31,7 +31,8 @@ class oq_dit_weights(C.Structure):
 
 
 class oq_dit_intermediates(C.Structure):
-    _fields_ = [(n, vp) for n in ("h1", "qkv", "attn", "h2", "gate_up", "act", "resid", "cond_kv")]
+    _fields_ = [(n, vp) for n in ("h1", "qkv", "attn", "h2", "gate_up", "act", "resid", "cond_kv", "codes",
+                                  "x_scale")] + [("codes_tiled", i32)]
 
 
 # name -> (restype, argtypes)
@@ -56,6 +57,7 @@ SIGNATURES = {
     "oq_dit_step": (i32, [vp, vp, i32, vp]),
     "oq_dit_denoise": (i32, [vp, vp, i32, vp]),
     "oq_dit_run_block": (i32, [vp, i32, i32, vp, vp]),
+    "oq_dit_run_block_until": (i32, [vp, i32, i32, vp, i32, vp]),
     "oq_dit_get_intermediates": (i32, [vp, C.POINTER(oq_dit_intermediates)]),
     "oq_dit_destroy": (None, [vp]),
 }

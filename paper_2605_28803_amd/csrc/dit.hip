@@ -253,8 +253,11 @@ template <int WAVES, int HD>
 __global__ __launch_bounds__(64 * WAVES) void attn_partial_kernel(AttnArgs a) {
   constexpr int KS = kAttnKS;            // 64 keys
   constexpr int PAD = KS + 8;            // padded row (halves): 16-byte reads of 16 rows hit distinct banks
-  __shared__ __attribute__((aligned(16))) uint16_t sVt[kMaxHeadDim][PAD];  // V^T [dim][key]
-  __shared__ __attribute__((aligned(16))) uint16_t sP[4][16][PAD];         // per-wave P [row][key]
+  constexpr int HDL = HD > 0 ? HD : kMaxHeadDim;
+  // LDS sized for this instance (one wave and 48 dims need 9 KB, so many
+  // workgroups share a CU).
+  __shared__ __attribute__((aligned(16))) uint16_t sVt[HDL][PAD];      // V^T [dim][key]
+  __shared__ __attribute__((aligned(16))) uint16_t sP[WAVES][16][PAD];  // per-wave P [row][key]
 
   const int bh = blockIdx.x, split = blockIdx.y;
   const int b = bh / a.H, h = bh % a.H;
@@ -856,7 +859,10 @@ int attention_rq(oq_dit* h, const uint16_t* q, int64_t q_ld, const uint16_t* k_p
   return ok ? launch_status() : OQ_ERR_SHAPE;
 }
 
-int run_block_pi(oq_dit* h, int l, int t, float* r, hipStream_t st) {
+// until: stop after the fused producer of quantization site `until` (0: the
+// q|k|v input, 1: the o input, 2: the gate|up input, 3: the down input), or
+// run the whole block (until = 4).
+int run_block_pi(oq_dit* h, int l, int t, float* r, hipStream_t st, int until) {
   const oq_dit_config& c = h->cfg;
   const oq_dit_block& bw = h->blocks[l];
   const int64_t D = c.hidden, F = c.mlp;
@@ -868,19 +874,23 @@ int run_block_pi(oq_dit* h, int l, int t, float* r, hipStream_t st) {
   uint16_t* act = at<uint16_t>(h, h->lay.act);
   int e;
   if ((e = norm_rq(h, r, bw.g1, mod_ptr(h, l, t, 0), mod_ptr(h, l, t, 1), h1, s[0], st)) != OQ_OK) return e;
+  if (until == 0) return OQ_OK;
   if ((e = gemm(h, bw.qkv, D, 3 * D, EPI_F16, qkv, 3 * D, nullptr, st)) != OQ_OK) return e;
   if ((e = attention_rq(h, qkv, 3 * D, static_cast<const uint16_t*>(bw.prefix_k),
                         static_cast<const uint16_t*>(bw.prefix_v), c.prefix, D, qkv + D, qkv + 2 * D, 3 * D,
                         c.tokens, s[1], st)) != OQ_OK)
     return e;
+  if (until == 1) return OQ_OK;
   if ((e = gemm(h, bw.o, D, D, EPI_RESID_F32, r, D, mod_ptr(h, l, t, 2), st)) != OQ_OK) return e;
   if ((e = norm_rq(h, r, bw.g2, mod_ptr(h, l, t, 3), mod_ptr(h, l, t, 4), h2, s[2], st)) != OQ_OK) return e;
+  if (until == 2) return OQ_OK;
   if ((e = gemm(h, bw.gate_up, D, 2 * F, EPI_F16, gu, 2 * F, nullptr, st)) != OQ_OK) return e;
   if ((e = gelu_rq(h, gu, act, s[3], st)) != OQ_OK) return e;
+  if (until == 3) return OQ_OK;
   return gemm(h, bw.down, F, D, EPI_RESID_F32, r, D, mod_ptr(h, l, t, 5), st);
 }
 
-int run_block_gr00t(oq_dit* h, int l, int t, float* r, hipStream_t st) {
+int run_block_gr00t(oq_dit* h, int l, int t, float* r, hipStream_t st, int until) {
   const oq_dit_config& c = h->cfg;
   const oq_dit_block& bw = h->blocks[l];
   const int64_t D = c.hidden, F = c.mlp;
@@ -892,6 +902,7 @@ int run_block_gr00t(oq_dit* h, int l, int t, float* r, hipStream_t st) {
   uint16_t* act = at<uint16_t>(h, h->lay.act);
   int e;
   if ((e = norm_rq(h, r, bw.g1, mod_ptr(h, l, t, 0), mod_ptr(h, l, t, 1), h1, s[0], st)) != OQ_OK) return e;
+  if (until == 0) return OQ_OK;
   if (l % 2 == 0) {
     // Cross-attention to the conditioning k|v of this block ([B][P][2D]).
     if ((e = gemm(h, bw.qkv, D, D, EPI_F16, qkv, D, nullptr, st)) != OQ_OK) return e;
@@ -905,15 +916,18 @@ int run_block_gr00t(oq_dit* h, int l, int t, float* r, hipStream_t st) {
                           st)) != OQ_OK)
       return e;
   }
+  if (until == 1) return OQ_OK;
   if ((e = gemm(h, bw.o, D, D, EPI_RESID_F32, r, D, nullptr, st)) != OQ_OK) return e;
   if ((e = norm_rq(h, r, bw.g2, nullptr, static_cast<const uint16_t*>(bw.b2), h2, s[2], st)) != OQ_OK) return e;
+  if (until == 2) return OQ_OK;
   if ((e = gemm(h, bw.gate_up, D, F, EPI_F16, ff, F, nullptr, st)) != OQ_OK) return e;
   if ((e = gelu_rq(h, ff, act, s[3], st)) != OQ_OK) return e;
+  if (until == 3) return OQ_OK;
   return gemm(h, bw.down, F, D, EPI_RESID_F32, r, D, nullptr, st);
 }
 
-int run_block(oq_dit* h, int l, int t, float* r, hipStream_t st) {
-  return is_gr00t(h->cfg) ? run_block_gr00t(h, l, t, r, st) : run_block_pi(h, l, t, r, st);
+int run_block(oq_dit* h, int l, int t, float* r, hipStream_t st, int until = 4) {
+  return is_gr00t(h->cfg) ? run_block_gr00t(h, l, t, r, st, until) : run_block_pi(h, l, t, r, st, until);
 }
 
 int run_step(oq_dit* h, float* x, int t, hipStream_t st) {
@@ -1120,6 +1134,14 @@ extern "C" int oq_dit_run_block(oq_dit* h, int32_t l, int32_t t, float* resid, v
   return oq::run_block(h, l, t, resid, static_cast<hipStream_t>(stream));
 }
 
+extern "C" int oq_dit_run_block_until(oq_dit* h, int32_t l, int32_t t, float* resid, int32_t site, void* stream) {
+  if (!h || !resid) return OQ_ERR_NULL;
+  int e = step_ready(h);
+  if (e != OQ_OK) return e;
+  if (l < 0 || l >= h->cfg.n_blocks || t < 0 || t >= h->cfg.steps || site < 0 || site > 3) return OQ_ERR_ARG;
+  return oq::run_block(h, l, t, resid, static_cast<hipStream_t>(stream), site);
+}
+
 extern "C" int oq_dit_get_intermediates(const oq_dit* h, oq_dit_intermediates* out) {
   if (!h || !out) return OQ_ERR_NULL;
   if (!h->ws) return OQ_ERR_WORKSPACE;
@@ -1131,6 +1153,9 @@ extern "C" int oq_dit_get_intermediates(const oq_dit* h, oq_dit_intermediates* o
   out->act = h->ws + h->lay.act;
   out->resid = reinterpret_cast<const float*>(h->ws + h->lay.r);
   out->cond_kv = oq::is_gr00t(h->cfg) ? h->ws + h->lay.ckv : nullptr;
+  out->codes = h->ws + h->lay.xq;
+  out->x_scale = reinterpret_cast<const float*>(h->ws + h->lay.xs);
+  out->codes_tiled = h->tiled ? 1 : 0;
   return OQ_OK;
 }
 

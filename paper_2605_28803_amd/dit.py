@@ -136,6 +136,43 @@ class DiT:
                "oq_dit_run_block")
         return resid
 
+    def run_block_until(self, l, t, resid, site, stream=None):
+        """Block l of step t up to and including the fused producer of
+        quantization site `site` (0 q|k|v input, 1 o input, 2 gate|up input,
+        3 down input); resid is updated as far as the block got."""
+        from . import _check
+        _check(self.lib.oq_dit_run_block_until(self.handle, l, t, resid.data_ptr(), site, self._stream(stream)),
+               "oq_dit_run_block_until")
+        return resid
+
+    def site_codes(self, K):
+        """(codes int64 [M, K], x_scale float64 [M]) of the last quantization
+        site, read from the workspace (either code layout)."""
+        from . import _check
+        it = _lib.oq_dit_intermediates()
+        _check(self.lib.oq_dit_get_intermediates(self.handle, C.byref(it)), "oq_dit_get_intermediates")
+        torch.cuda.synchronize(self.device)
+        M = self.M
+        base = self.workspace.data_ptr()
+        off = it.codes - base
+        rows = (M + 15) // 16 * 16 if it.codes_tiled else M
+        raw = self.workspace[off: off + rows * K // 2].cpu().numpy()
+        if it.codes_tiled:
+            r = np.arange(M)[:, None]
+            p = np.arange(K // 2)[None, :]
+            idx = ((r // 16) * (K // 128) + p // 64) * 1024 + ((p // 16) % 4) * 256 + (r % 16) * 16 + p % 16
+            packed = raw[idx]
+        else:
+            packed = raw.reshape(M, K // 2)
+        lo = (packed & 0xF).astype(np.int64)
+        hi = (packed >> 4).astype(np.int64)
+        q = np.empty((M, K), dtype=np.int64)
+        q[:, 0::2] = np.where(lo >= 8, lo - 16, lo)
+        q[:, 1::2] = np.where(hi >= 8, hi - 16, hi)
+        xoff = it.x_scale - base
+        xs = self.workspace[xoff: xoff + 4 * M].cpu().numpy().view(np.float32).astype(np.float64)
+        return q, xs
+
     def intermediates(self):
         """fp16 intermediates of the last block run, as numpy float64 arrays:
         h1 [M,D], qkv [M,3D], attn [M,D], h2 [M,D], gate_up [M,2F] (gr00t:
