@@ -16,6 +16,8 @@ quant     symmetric uniform quantizer, per-token activation and per-output-
           channel weight quantization, the per-step activation scale
           (Section 4.2, eq:scale, eq:quant, eq:perstep_scale).
 linear    exact integer GEMM and the dequantizing epilogue (eq:lowbit_linear).
+composite the full composite rotation: zigzag channel permutation, per-block
+          SVD factor times Hadamard (eq:blockdiag, eq:transform).
 dit       one DiT denoising step built from the pieces above (Experimental
           Settings; Appendix "Necessity of Per-Step Activation Scaling").
 
@@ -25,4 +27,4 @@ case the value is rounded to fp16 exactly there.  Parity status of every
 function is stated in its docstring; all are pinned by tests that do not call
 the function they check.
 """
-from . import hadamard, quant, linear, dit  # noqa: F401
+from . import hadamard, quant, linear, dit, composite  # noqa: F401

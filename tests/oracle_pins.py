@@ -217,3 +217,125 @@ def check_worked_example_gemm(int_gemm):
     q = g["q"].astype(np.int64)[None, :]
     qw = np.stack([g["qw0"], g["qw1"]]).astype(np.int64)
     assert np.array_equal(int_gemm(q, qw)[0], g["acc"].astype(np.int64))
+
+
+# --------------------------------------------------------------------------
+# Full composite rotation (zigzag permutation, per-block SVD factor, Hadamard)
+# --------------------------------------------------------------------------
+
+def random_orthogonal(rng, n):
+    a = rng.standard_normal((n, n))
+    q, r = np.linalg.qr(a)
+    return q * np.sign(np.diag(r))
+
+
+def check_zigzag(zigzag_permutation, seed=20):
+    g = load_golden_rows("zigzag_example.txt")
+    perm = zigzag_permutation(g["energy"], 2)
+    assert np.array_equal(np.asarray(perm), g["perm"].astype(np.int64))
+    rng = np.random.default_rng(seed)
+    for K, B in ((64, 4), (96, 3), (128, 16), (256, 4)):
+        e = rng.exponential(size=K)
+        e[rng.choice(K, 5, replace=False)] = e[0]  # ties
+        perm = np.asarray(zigzag_permutation(e, B))
+        c = K // B
+        assert np.array_equal(np.sort(perm), np.arange(K)), "not a permutation"
+        # every block takes exactly one channel from each run of B consecutive
+        # ranks of the descending order
+        rank = np.empty(K, dtype=np.int64)
+        rank[np.array(sorted(range(K), key=lambda j: (-e[j], j)))] = np.arange(K)
+        for b in range(B):
+            rounds = np.sort(rank[perm[b * c:(b + 1) * c]] // B)
+            assert np.array_equal(rounds, np.arange(c)), "a block skips a round"
+        # block energies differ by at most the spread of all energies
+        sums = np.array([e[perm[b * c:(b + 1) * c]].sum() for b in range(B)])
+        assert sums.max() - sums.min() <= e.max() - e.min() + 1e-12
+
+
+def check_block_svd(block_svd_factors, seed=21):
+    """The paper's statement after the SVD rotation: row i of U_b^T W_b has
+    squared norm sigma_i^2, with sigma_i^2 taken here from the eigenvalues of
+    W_b W_b^T (a different routine); U_b orthogonal."""
+    rng = np.random.default_rng(seed)
+    N, K, c = 40, 32, 8
+    w = rng.standard_normal((N, K)) * np.exp(rng.standard_normal(K))[None, :]
+    perm = rng.permutation(K)
+    u, _ = block_svd_factors(w, perm, c)
+    u = np.asarray(u)
+    assert u.shape == (K // c, c, c)
+    for b in range(K // c):
+        wb = w[:, perm][:, b * c:(b + 1) * c].T
+        assert np.allclose(u[b].T @ u[b], np.eye(c), atol=1e-12)
+        energy = np.sum((u[b].T @ wb) ** 2, axis=1)
+        ev = np.sort(np.linalg.eigvalsh(wb @ wb.T))[::-1]
+        assert np.allclose(energy, ev, rtol=1e-10, atol=1e-10)
+
+
+def check_block_rotations(block_rotations, seed=22):
+    rng = np.random.default_rng(seed)
+    for c in (8, 64):
+        u = np.stack([random_orthogonal(rng, c) for _ in range(3)])
+        r = np.asarray(block_rotations(u))
+        for b in range(3):
+            assert np.allclose(r[b] @ r[b].T, np.eye(c), atol=1e-12), "not orthogonal"
+        # U = I leaves the normalized Hadamard matrix: a spike maps to +-1/sqrt(c)
+        ri = np.asarray(block_rotations(np.eye(c)[None]))[0]
+        assert np.allclose(np.abs(ri), 1.0 / np.sqrt(c), atol=1e-15)
+        assert np.allclose(ri[0], 1.0 / np.sqrt(c)) and np.allclose(ri[:, 0], 1.0 / np.sqrt(c))
+
+
+def check_rotate_composite(rotate_composite, block_rotations, fwht, seed=23):
+    rng = np.random.default_rng(seed)
+    M, N, K, c = 6, 20, 256, 64
+    x = rng.standard_normal((M, K))
+    # identity permutation with U_b = I is the block Walsh-Hadamard transform
+    r_id = np.asarray(block_rotations(np.stack([np.eye(c)] * (K // c))))
+    assert np.allclose(rotate_composite(x, np.arange(K), r_id), fwht(x, c), atol=1e-12)
+    # R_b = I leaves the gather (X P)[:, k] = X[:, perm[k]]
+    perm = rng.permutation(K)
+    eye = np.stack([np.eye(c)] * (K // c))
+    assert np.array_equal(rotate_composite(x, perm, eye), x[:, perm])
+    # invariance of the linear: (X P R)(W P R)^T = X W^T for orthogonal R
+    u = np.stack([random_orthogonal(rng, c) for _ in range(K // c)])
+    r = np.asarray(block_rotations(u))
+    w = rng.standard_normal((N, K))
+    lhs = rotate_composite(x, perm, r) @ rotate_composite(w, perm, r).T
+    ref = x @ w.T
+    assert np.max(np.abs(lhs - ref)) <= 1e-12 * np.max(np.abs(ref)) * K
+    # energy equalization (the purpose of U_b H_c): with U_b the left singular
+    # vectors of the block's weight rows (here eigenvectors of W_b W_b^T), every
+    # rotated weight row of the block carries the block's mean sigma^2
+    wp = w[:, perm]
+    ub = []
+    for b in range(K // c):
+        wb = wp[:, b * c:(b + 1) * c].T
+        ev, vec = np.linalg.eigh(wb @ wb.T)
+        ub.append(vec[:, ::-1])
+    r = np.asarray(block_rotations(np.stack(ub)))
+    wr = rotate_composite(w, perm, r)
+    for b in range(K // c):
+        wb = wp[:, b * c:(b + 1) * c].T
+        energy = np.sum(wr[:, b * c:(b + 1) * c] ** 2, axis=0)
+        assert np.allclose(energy, np.trace(wb @ wb.T) / c, rtol=1e-10), "block energy not equalized"
+
+
+def check_rotate_quantize_composite(rqc, rotate_quantize_act, seed=24):
+    """Identity permutation and U_b = I: the composite path is the Hadamard
+    path (block c); quantizer bound |z - Delta q| <= Delta / 2 in general."""
+    rng = np.random.default_rng(seed)
+    M, K, c = 5, 128, 64
+    x = rng.standard_normal((M, K))
+    h = np.array([[1.0]])
+    while h.shape[0] < c:
+        h = np.block([[h, h], [h, -h]])
+    r_id = np.stack([h / np.sqrt(c)] * (K // c))
+    q1, xs1, _ = rqc(x, np.arange(K), r_id, 2.5)
+    q2, xs2, _ = rotate_quantize_act(x, c, 2.5)
+    assert np.array_equal(q1, q2) and np.allclose(xs1, xs2, rtol=1e-14)
+    perm = rng.permutation(K)
+    r = np.stack([random_orthogonal(rng, c) for _ in range(K // c)])
+    q, xs, _ = rqc(x, perm, r, 1.0)
+    y = x[:, perm].reshape(M, K // c, c)
+    y = np.einsum("mbi,bij->mbj", y, r).reshape(M, K)
+    assert np.all(np.abs(y - xs[:, None] * q) <= xs[:, None] / 2 * (1 + 1e-12))
+    assert np.all(np.abs(q).max(axis=1) == 7)

@@ -1,0 +1,47 @@
+"""The composite-rotation oracle against facts outside it (CPU only)."""
+import numpy as np
+
+from oracle import composite, hadamard, quant
+from tests import oracle_pins as P
+
+
+def test_zigzag():
+    P.check_zigzag(composite.zigzag_permutation)
+
+
+def test_block_svd_row_energy():
+    P.check_block_svd(composite.block_svd_factors)
+
+
+def test_block_rotations():
+    P.check_block_rotations(composite.block_rotations)
+
+
+def test_rotate_composite():
+    P.check_rotate_composite(composite.rotate_composite, composite.block_rotations, hadamard.fwht)
+
+
+def test_rotate_quantize_composite():
+    P.check_rotate_quantize_composite(composite.rotate_quantize_composite, quant.rotate_quantize_act)
+
+
+def test_channel_energy_is_column_sum_of_squares():
+    w = np.arange(12, dtype=np.float64).reshape(3, 4)
+    assert np.array_equal(composite.channel_energy(w), np.array([0 + 16 + 64, 1 + 25 + 81, 4 + 36 + 100,
+                                                                 9 + 49 + 121], dtype=np.float64))
+
+
+def test_full_pipeline_invariance_from_svd():
+    """perm from column energies, U_b from the SVD, R_b = U_b H / 8: the folded
+    linear reproduces X W^T (float64)."""
+    rng = np.random.default_rng(30)
+    M, N, K, c = 8, 48, 256, 64
+    w = rng.standard_normal((N, K)) * 0.02
+    w[:, rng.choice(K, 4, replace=False)] *= 30
+    x = rng.standard_normal((M, K))
+    perm = composite.zigzag_permutation(composite.channel_energy(w), K // c)
+    u, _ = composite.block_svd_factors(w, perm, c)
+    r = composite.block_rotations(u)
+    lhs = composite.rotate_composite(x, perm, r) @ composite.rotate_composite(w, perm, r).T
+    ref = x @ w.T
+    assert np.max(np.abs(lhs - ref)) <= 1e-12 * np.max(np.abs(ref)) * K

@@ -3,7 +3,7 @@
 import numpy as np
 import pytest
 
-from oracle import hadamard, quant, linear
+from oracle import composite, hadamard, quant, linear
 from tests import oracle_pins as P
 
 
@@ -58,6 +58,65 @@ def sylvester_wrong_sign(n):
     if n > 1:
         h[-1, -1] *= -1
     return h
+
+
+def zigzag_ascending(energy, n_blocks):
+    return composite.zigzag_permutation(-np.asarray(energy, np.float64), n_blocks)
+
+
+def zigzag_round_robin(energy, n_blocks):
+    e = np.asarray(energy, np.float64)
+    K = e.shape[0]
+    c = K // n_blocks
+    order = sorted(range(K), key=lambda j: (-e[j], j))
+    perm = np.empty(K, dtype=np.int64)
+    for i, ch in enumerate(order):
+        r, p = divmod(i, n_blocks)
+        perm[p * c + r] = ch
+    return perm
+
+
+def svd_factor_transposed(w, perm, c):
+    u, s = composite.block_svd_factors(w, perm, c)
+    return np.transpose(u, (0, 2, 1)), s
+
+
+def rotations_unnormalized(u):
+    return composite.block_rotations(u) * np.sqrt(np.asarray(u).shape[-1])
+
+
+def rotate_inverse_gather(x, perm, r):
+    inv = np.empty_like(perm)
+    inv[perm] = np.arange(len(perm))
+    return composite.rotate_composite(x, inv, r)
+
+
+def rotate_transposed_blocks(x, perm, r):
+    return composite.rotate_composite(x, perm, np.transpose(np.asarray(r), (0, 2, 1)))
+
+
+def rqc_scale_not_divided(x, perm, r, s_t=1.0):
+    q, xs, ratio = composite.rotate_quantize_composite(x, perm, r, s_t)
+    return q, xs * s_t, ratio
+
+
+@pytest.mark.parametrize("check,impl", [
+    (P.check_zigzag, zigzag_ascending),
+    (P.check_zigzag, zigzag_round_robin),
+    (P.check_block_svd, svd_factor_transposed),
+    (P.check_block_rotations, rotations_unnormalized),
+])
+def test_composite_pin_rejects_mutant(check, impl):
+    with pytest.raises((AssertionError, ValueError)):
+        check(impl)
+
+
+def test_rotate_composite_pin_rejects_mutants():
+    for impl in (rotate_inverse_gather, rotate_transposed_blocks):
+        with pytest.raises(AssertionError):
+            P.check_rotate_composite(impl, composite.block_rotations, hadamard.fwht)
+    with pytest.raises(AssertionError):
+        P.check_rotate_quantize_composite(rqc_scale_not_divided, quant.rotate_quantize_act)
 
 
 @pytest.mark.parametrize("check,impl", [
