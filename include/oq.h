@@ -200,6 +200,70 @@ int oq_w4a4_gemm_i32_tiled(const uint8_t* Xt, int64_t M, const uint8_t* Wq, int6
                            int64_t K, int32_t* acc, int64_t ldc, void* stream);
 
 /*
+ * Full composite rotation (Section 4.1, "Block-wise Implementation";
+ * eq:blockdiag, eq:transform) with block size c = 64: X' = X P R_hat, where
+ * P permutes the channels (zigzag over the blocks by descending weight
+ * energy) and R_hat = BlockDiag(R_1 .. R_{K/64}), R_b = U_b H_64 / 8, U_b the
+ * left singular vectors of the block's weight rows.  Unlike the entry points
+ * above (whose input is already in the SVD basis, so only the Hadamard half
+ * runs online), the whole transform runs online here.
+ *
+ * oq_rotate_quantize_act_composite -- for each row i:
+ *   (X P)[i][k] = X[i][perm[k]];  y[i][64b + j] = sum_r (X P)[i][64b + r] R_b[r][j];
+ *   z = s_t y;  Delta_i = max|z| / 7;  q = round_half_even(z / Delta_i)
+ *   (|q| <= 7);  x_scale[i] = Delta_i / s_t.
+ * X        device fp16 [M][ldx], ldx >= K, ldx % 8 == 0, 16-byte aligned
+ * K        multiple of 64, 64 <= K <= 16384
+ * perm     device int32 [K], a permutation of 0 .. K-1, 16-byte aligned
+ *          (entries outside 0 .. K-1 are clamped into range; the result is
+ *          then unspecified but every access stays in bounds)
+ * Rt       device fp16 [K/64][64][64], block b column-major:
+ *          Rt[b][j][r] = R_b[r][j] (oq_block_rotations_host writes it), 16-byte
+ *          aligned.  The products are formed from these fp16 values exactly
+ *          and summed in fp32.
+ * s_table, t  as oq_rotate_quantize_act
+ * Xq       device [M][K/2] codes (8-byte aligned), x_scale device fp32 [M]
+ * Errors: OQ_ERR_NULL, OQ_ERR_SHAPE, OQ_ERR_ALIGN, OQ_ERR_ARG, OQ_ERR_DEVICE,
+ * OQ_ERR_HIP.
+ */
+int oq_rotate_quantize_act_composite(const void* X, int64_t M, int64_t K, int64_t ldx,
+                                     const int32_t* perm, const void* Rt, const float* s_table,
+                                     int32_t t, uint8_t* Xq, float* x_scale, void* stream);
+
+/*
+ * oq_zigzag_permutation_host -- perm (host int32 [K]) from per-channel weight
+ * energies ||W_{j,:}||^2 (host double [K]; for a weight stored [N][K] the sum
+ * of squares of column j): channels sorted by descending energy (ties keep
+ * the lower index first) and dealt to the K / block blocks in snake order --
+ * sorted position i goes to round r = i / n_blocks and block i % n_blocks
+ * (r even) or n_blocks - 1 - i % n_blocks (r odd), slot r; perm[b block + r]
+ * is that channel.  Errors: OQ_ERR_NULL, OQ_ERR_SHAPE.
+ */
+int oq_zigzag_permutation_host(const double* energy, int64_t K, int32_t block, int32_t* perm);
+
+/*
+ * oq_block_rotations_host -- Rt (host fp16 [K/block][block][block], each block
+ * column-major) = round_to_fp16(U_b H_block / sqrt(block)) from the row-major
+ * host double factors U [K/block][block][block].  block a power of two
+ * <= 4096 dividing K (the online kernel takes block 64).
+ * Errors: OQ_ERR_NULL, OQ_ERR_SHAPE.
+ */
+int oq_block_rotations_host(const double* U, int64_t K, int32_t block, uint16_t* Rt);
+
+/*
+ * oq_quantize_weights_composite_host -- the weight side of eq:transform in the
+ * output-major storage: W'[n] = (W[n] P) R_hat with the fp16 block matrices
+ * Rt as given (the same values the activation side uses), in float64, then
+ * per-output-channel RTN (eq:scale, eq:quant): Wq host [N][K/2], w_scale host
+ * fp32 [N].  W_u host double [N][K] row-major, perm host int32 [K], Rt host
+ * fp16 as above.  Runs on the calling thread's process (std::thread workers).
+ * Errors: OQ_ERR_NULL, OQ_ERR_SHAPE, OQ_ERR_ARG (perm entry out of range).
+ */
+int oq_quantize_weights_composite_host(const double* W_u, int64_t N, int64_t K, int32_t block,
+                                       const int32_t* perm, const uint16_t* Rt, uint8_t* Wq,
+                                       float* w_scale);
+
+/*
  * oq_quantize_weights -- offline weight preparation on the device: fold the
  * Hadamard half of the rotation into the weight and quantize it per output
  * channel with round-to-nearest (eq:transform W' = R^T W in the output-major

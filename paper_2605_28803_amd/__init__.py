@@ -104,6 +104,56 @@ def codes_to_tiled(Q, K=None, T=None, stream=None):
     return T
 
 
+def rotate_quantize_act_composite(X, perm, Rt, s_table=None, t=0, Xq=None, x_scale=None, stream=None):
+    """Full composite rotation (block 64) + step scale + per-token int4 codes.
+    X fp16 [M, K]; perm int32 [K] and Rt fp16 [K/64, 64, 64] (column-major
+    blocks) on the device.  Returns (Xq uint8 [M, K/2], x_scale f32 [M])."""
+    M, K = X.shape
+    if Xq is None:
+        Xq = torch.empty((M, K // 2), dtype=torch.uint8, device=X.device)
+    if x_scale is None:
+        x_scale = torch.empty((M,), dtype=torch.float32, device=X.device)
+    keep, sp = _s_table(s_table)
+    _check(lib().oq_rotate_quantize_act_composite(_ptr(X), M, K, X.stride(0), _ptr(perm), _ptr(Rt), sp, t,
+                                                  _ptr(Xq), _ptr(x_scale), _stream(stream)),
+           "oq_rotate_quantize_act_composite")
+    del keep
+    return Xq, x_scale
+
+
+def zigzag_permutation_host(energy: np.ndarray, block: int) -> np.ndarray:
+    """Zigzag channel permutation (int32 [K]) from per-channel weight energies."""
+    e = np.ascontiguousarray(energy, dtype=np.float64)
+    perm = np.empty(e.shape[0], dtype=np.int32)
+    _check(lib().oq_zigzag_permutation_host(e.ctypes.data, e.shape[0], block, perm.ctypes.data),
+           "oq_zigzag_permutation_host")
+    return perm
+
+
+def block_rotations_host(U: np.ndarray) -> np.ndarray:
+    """fp16 column-major blocks Rt [nb, c, c] (as uint16) of U_b H_c / sqrt(c)."""
+    u = np.ascontiguousarray(U, dtype=np.float64)
+    nb, c, _ = u.shape
+    Rt = np.empty((nb, c, c), dtype=np.uint16)
+    _check(lib().oq_block_rotations_host(u.ctypes.data, nb * c, c, Rt.ctypes.data), "oq_block_rotations_host")
+    return Rt
+
+
+def quantize_weights_composite_host(W_u: np.ndarray, perm: np.ndarray, Rt: np.ndarray):
+    """float64 host weight [N, K] folded with (perm, Rt) and RTN-quantized:
+    (Wq uint8 [N, K/2], w_scale f32 [N])."""
+    W = np.ascontiguousarray(W_u, dtype=np.float64)
+    N, K = W.shape
+    p = np.ascontiguousarray(perm, dtype=np.int32)
+    r = np.ascontiguousarray(Rt, dtype=np.uint16)
+    Wq = np.empty((N, K // 2), dtype=np.uint8)
+    ws = np.empty((N,), dtype=np.float32)
+    _check(lib().oq_quantize_weights_composite_host(W.ctypes.data, N, K, r.shape[-1], p.ctypes.data,
+                                                    r.ctypes.data, Wq.ctypes.data, ws.ctypes.data),
+           "oq_quantize_weights_composite_host")
+    return Wq, ws
+
+
 def rotate_debug_f32(X, had_block, s_table=None, t=0, stream=None):
     """Pre-rounding ratios z/Delta (f32 [M, K]) and x_scale."""
     M, K = X.shape

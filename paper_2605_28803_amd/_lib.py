@@ -48,6 +48,10 @@ SIGNATURES = {
     "oq_w4a4_linear_tiled": (i32, [vp, vp, i64, vp, vp, vp, i64, i64, vp, i64, i32, vp]),
     "oq_w4a4_gemm_i32_tiled": (i32, [vp, i64, vp, i64, i64, vp, i64, vp]),
     "oq_codes_to_tiled": (i32, [vp, i64, i64, vp, vp]),
+    "oq_rotate_quantize_act_composite": (i32, [vp, i64, i64, i64, vp, vp, fp, i32, vp, vp, vp]),
+    "oq_zigzag_permutation_host": (i32, [vp, i64, i32, vp]),
+    "oq_block_rotations_host": (i32, [vp, i64, i32, vp]),
+    "oq_quantize_weights_composite_host": (i32, [vp, i64, i64, i32, vp, vp, vp, vp]),
     "oq_quantize_weights": (i32, [vp, i64, i64, i64, i32, vp, vp, vp]),
     "oq_quantize_weights_host": (i32, [vp, i64, i64, i32, vp, vp]),
     "oq_dit_workspace_bytes": (i32, [C.POINTER(oq_dit_config), C.POINTER(C.c_size_t)]),
