@@ -26,7 +26,7 @@ JSON lines to gpurun_out/sweep.jsonl instead; --roofline-only runs just the
 roofline kernel measurement (the command the committed rocprofv3 summaries of
 that kernel were taken with); --copy-calibration runs a plain copy of known
 size (the counter calibration reference); --gr00t-only times just the
-GR00T-shaped step.
+GR00T-shaped step; --composite-only times just the full composite rotation.
 """
 from __future__ import annotations
 
@@ -215,6 +215,54 @@ def prefill_kernels():
                                           "GBs": round(rq_bytes(M, K) / (t_r * 1e-3) / 1e9, 1),
                                           "frac_hbm_peak": round(rq_bytes(M, K) / (t_r * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}}
     del X, Xq, Y, Wq, flush
+    torch.cuda.empty_cache()
+    return out
+
+
+def composite_kernels():
+    """The online full composite rotation (zigzag permutation + block-64
+    U_b H_64 on the fp16 matrix cores + per-token int4 codes), cold: at
+    M = 16384 x K = 1024 and 4096 against the HBM roofline (algorithmic bytes
+    2.5 K + 4 per row; perm and the fp16 block matrices, 128 bytes per
+    channel, are read once per launch and counted), and at the DiT shape
+    (M = 50, K = 1024), whose time is latency.  The permutation comes from
+    seeded synthetic weight energies and U_b are seeded random orthogonal
+    matrices (the kernel's work does not depend on their values)."""
+    import torch
+    import paper_2605_28803_amd as oq
+    from workloads import generators as G
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    flush = torch.empty((512 << 20,), dtype=torch.uint8, device=dev)
+
+    def cold(fn, reps):
+        ts = []
+        for _ in range(reps):
+            flush.fill_(1)
+            s = torch.cuda.Event(enable_timing=True)
+            e = torch.cuda.Event(enable_timing=True)
+            s.record(stream)
+            fn()
+            e.record(stream)
+            e.synchronize()
+            ts.append(s.elapsed_time(e))
+        return float(np.median(ts))
+
+    out = {}
+    for M, K in ((16384, 1024), (16384, 4096), (50, 1024)):
+        energy = G.gaussian(11, f"composite/energy{K}", (K,)) ** 2
+        perm = torch.from_numpy(oq.zigzag_permutation_host(energy, 64)).to(dev)
+        U = np.stack([G.random_orthogonal(11, f"composite/u{K}/{b}", 64) for b in range(K // 64)])
+        Rt = torch.from_numpy(oq.block_rotations_host(U).view(np.int16)).to(dev)
+        g = torch.Generator(device=dev).manual_seed(13)
+        X = torch.randn((M, K), generator=g, device=dev).half()
+        Xq, xs = oq.rotate_quantize_act_composite(X, perm, Rt)
+        t = cold(lambda: oq.rotate_quantize_act_composite(X, perm, Rt, Xq=Xq, x_scale=xs), 15)
+        b = rq_bytes(M, K) + K * 4 + K * 64 * 2
+        out[f"M{M}_K{K}"] = {"us": round(t * 1e3, 2), "GBs": round(b / (t * 1e-3) / 1e9, 1),
+                             "frac_hbm_peak": round(b / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+        del X, Xq, xs
+    del flush
     torch.cuda.empty_cache()
     return out
 
@@ -450,6 +498,7 @@ def run_dit(args):
         print("[bench] gr00t-shaped step, prefill layer", file=sys.stderr, flush=True)
         line["dit_gr00t"] = gr00t_step()
         line["prefill_gemma2b_layer"] = prefill_linears()
+        line["composite_rotate_quant"] = composite_kernels()
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle sample)", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(cfg, inp)
@@ -527,6 +576,7 @@ def main():
     ap.add_argument("--roofline-only", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--gr00t-only", action="store_true")
+    ap.add_argument("--composite-only", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (--gpus must be 1)", file=sys.stderr)
@@ -539,6 +589,8 @@ def main():
         copy_calibration()
     elif args.gr00t_only:
         print(json.dumps({"dit_gr00t": gr00t_step()}), flush=True)
+    elif args.composite_only:
+        print(json.dumps({"composite_rotate_quant": composite_kernels()}), flush=True)
     else:
         run_dit(args)
 

@@ -222,7 +222,7 @@ int oq_w4a4_gemm_i32_tiled(const uint8_t* Xt, int64_t M, const uint8_t* Wq, int6
  *          aligned.  The products are formed from these fp16 values exactly
  *          and summed in fp32.
  * s_table, t  as oq_rotate_quantize_act
- * Xq       device [M][K/2] codes (8-byte aligned), x_scale device fp32 [M]
+ * Xq       device [M][K/2] codes (16-byte aligned), x_scale device fp32 [M]
  * Errors: OQ_ERR_NULL, OQ_ERR_SHAPE, OQ_ERR_ALIGN, OQ_ERR_ARG, OQ_ERR_DEVICE,
  * OQ_ERR_HIP.
  */

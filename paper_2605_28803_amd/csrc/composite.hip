@@ -40,13 +40,17 @@ __device__ __forceinline__ uint32_t pack4codes(uint32_t d) {
   return (t & 0xFFu) | ((t >> 8) & 0xFF00u);
 }
 
-template <int RW, int KMAX>
+template <int RW, int KMAX, int G>
 __global__ __launch_bounds__(256) void rq_composite_kernel(const uint16_t* __restrict__ X, int64_t M, int K,
                                                            int64_t ldx, const int32_t* __restrict__ perm,
                                                            const uint16_t* __restrict__ Rt, float s_t,
                                                            uint8_t* __restrict__ Xq, float* __restrict__ xs) {
-  __shared__ __attribute__((aligned(16))) uint16_t sx[RW * KMAX];  // fp16 rows
-  __shared__ __attribute__((aligned(16))) int8_t sc[RW * KMAX];    // int8 codes
+  // fp16 rows, padded by 16 bytes: the 16 rows of a gather read the same
+  // permuted column, and the pad puts them in different LDS banks.
+  constexpr int XS = KMAX + 8;
+  __shared__ __attribute__((aligned(16))) uint16_t sx[RW * XS];
+  __shared__ __attribute__((aligned(16))) int32_t sp[KMAX];          // the permutation
+  __shared__ __attribute__((aligned(16))) uint8_t sc[RW * KMAX / 2];  // packed codes
   __shared__ float red[4][16];
   __shared__ float gscale[16];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -54,7 +58,8 @@ __global__ __launch_bounds__(256) void rq_composite_kernel(const uint16_t* __res
   const int nb = K / kCB;
   const int vpr = K / 8;  // 16-byte pieces per row
 
-  // Stage the rows (rows past M are zeros): 8 loads in flight per thread.
+  // Stage the rows (rows past M are zeros) and the permutation (clamped into
+  // range: a non-permutation keeps every access inside the staged rows).
   for (int p0 = tid; p0 < RW * vpr; p0 += 256 * 8) {
     uint4 v[8];
     bool ok[8];
@@ -70,44 +75,79 @@ __global__ __launch_bounds__(256) void rq_composite_kernel(const uint16_t* __res
     for (int u = 0; u < 8; ++u) {
       const int p = p0 + u * 256;
       const int r = p / vpr, c8 = p - r * vpr;
-      if (p < RW * vpr) *reinterpret_cast<uint4*>(&sx[r * KMAX + c8 * 8]) = ok[u] ? v[u] : make_uint4(0, 0, 0, 0);
+      if (p < RW * vpr) *reinterpret_cast<uint4*>(&sx[r * XS + c8 * 8]) = ok[u] ? v[u] : make_uint4(0, 0, 0, 0);
     }
+  }
+  for (int k4 = tid; k4 < K / 4; k4 += 256) {
+    int4 pv = *reinterpret_cast<const int4*>(perm + 4 * k4);
+    pv.x = min(max(pv.x, 0), K - 1);
+    pv.y = min(max(pv.y, 0), K - 1);
+    pv.z = min(max(pv.z, 0), K - 1);
+    pv.w = min(max(pv.w, 0), K - 1);
+    *reinterpret_cast<int4*>(&sp[4 * k4]) = pv;
   }
   __syncthreads();
 
   const int r16 = lane & 15, q = lane >> 4;
   const bool rok = r16 < RW;
-  const uint16_t* xrow = &sx[(rok ? r16 : 0) * KMAX];
+  const uint16_t* xrow = &sx[(rok ? r16 : 0) * XS];
 
-  // y of block b, column group cb for this lane: rows 4q + e, column r16.
+  // A fragment: rows x 32 permuted channels of block b, k step kk.
   auto gather = [&](int b, int kk) -> c8h {
     const int k0 = b * kCB + kk * 32 + 8 * q;
-    const int4 pa = *reinterpret_cast<const int4*>(perm + k0);
-    const int4 pb = *reinterpret_cast<const int4*>(perm + k0 + 4);
+    const int4 pa = *reinterpret_cast<const int4*>(&sp[k0]);
+    const int4 pb = *reinterpret_cast<const int4*>(&sp[k0 + 4]);
     const int idx[8] = {pa.x, pa.y, pa.z, pa.w, pb.x, pb.y, pb.z, pb.w};
     c8h a;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int src = min(max(idx[j], 0), K - 1);  // a non-permutation stays inside the staged row
-      a[j] = __builtin_bit_cast(_Float16, rok ? xrow[src] : uint16_t(0));
-    }
+    for (int j = 0; j < 8; ++j) a[j] = __builtin_bit_cast(_Float16, rok ? xrow[idx[j]] : uint16_t(0));
     return a;
   };
-  auto bfrag = [&](int b, int cb, int kk) -> c8h {
-    return *reinterpret_cast<const c8h*>(Rt + (static_cast<int64_t>(b) * kCB + cb * 16 + r16) * kCB + kk * 32 +
-                                         8 * q);
+  // B fragments of G consecutive blocks of this wave (blocks b0 + 4 g), all
+  // loads issued together; blocks past the end read block 0 and are skipped.
+  c8h bf[G][4][2];
+  auto load_b = [&](int b0) {
+#pragma unroll
+    for (int gi = 0; gi < G; ++gi) {
+      const int b = b0 + 4 * gi < nb ? b0 + 4 * gi : 0;
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+          bf[gi][cb][kk] = *reinterpret_cast<const c8h*>(
+              Rt + (static_cast<int64_t>(b) * kCB + cb * 16 + r16) * kCB + kk * 32 + 8 * q);
+    }
   };
 
-  // Pass 1: row maxima of |y|.
+  // Pass 1: row maxima of |y|.  The B fragments of the next group are in
+  // flight while the current group is multiplied (the scheduling barrier
+  // keeps the loads ahead of the products).
   float amax[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-  for (int b = wave; b < nb; b += 4) {
-    const c8h a0 = gather(b, 0), a1 = gather(b, 1);
+  load_b(wave);
+  for (int b0 = wave; b0 < nb; b0 += 4 * G) {
+    c8h cur[G][4][2];
 #pragma unroll
-    for (int cb = 0; cb < 4; ++cb) {
-      c4f acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, bfrag(b, cb, 0), c4f{0, 0, 0, 0}, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, bfrag(b, cb, 1), acc, 0, 0, 0);
+    for (int gi = 0; gi < G; ++gi)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) amax[e] = fmaxf(amax[e], fabsf(acc[e]));
+      for (int cb = 0; cb < 4; ++cb) {
+        cur[gi][cb][0] = bf[gi][cb][0];
+        cur[gi][cb][1] = bf[gi][cb][1];
+      }
+    if (b0 + 4 * G < nb) load_b(b0 + 4 * G);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int gi = 0; gi < G; ++gi) {
+      const int b = b0 + 4 * gi;
+      if (b < nb) {
+        const c8h a0 = gather(b, 0), a1 = gather(b, 1);
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) {
+          c4f acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, cur[gi][cb][0], c4f{0, 0, 0, 0}, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, cur[gi][cb][1], acc, 0, 0, 0);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) amax[e] = fmaxf(amax[e], fabsf(acc[e]));
+        }
+      }
     }
   }
 #pragma unroll
@@ -130,46 +170,228 @@ __global__ __launch_bounds__(256) void rq_composite_kernel(const uint16_t* __res
   }
   __syncthreads();
 
-  // Pass 2: codes into LDS.
+  // Pass 2: codes.  Lanes r16 and r16 ^ 1 hold channels 2i and 2i + 1 of
+  // the same row; the even lane packs both into one byte.
   float g[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) g[e] = gscale[4 * q + e];
-  for (int b = wave; b < nb; b += 4) {
-    const c8h a0 = gather(b, 0), a1 = gather(b, 1);
+  load_b(wave);
+  for (int b0 = wave; b0 < nb; b0 += 4 * G) {
+    c8h cur[G][4][2];
 #pragma unroll
-    for (int cb = 0; cb < 4; ++cb) {
-      c4f acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, bfrag(b, cb, 0), c4f{0, 0, 0, 0}, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, bfrag(b, cb, 1), acc, 0, 0, 0);
+    for (int gi = 0; gi < G; ++gi)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int row = 4 * q + e;
-        if (row < RW) {
-          const uint32_t bits = __float_as_uint(fmaf(acc[e], g[e], rqd::kRoundMagic));
-          sc[row * KMAX + b * kCB + cb * 16 + r16] = static_cast<int8_t>(bits & 0xFFu);
+      for (int cb = 0; cb < 4; ++cb) {
+        cur[gi][cb][0] = bf[gi][cb][0];
+        cur[gi][cb][1] = bf[gi][cb][1];
+      }
+    if (b0 + 4 * G < nb) load_b(b0 + 4 * G);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int gi = 0; gi < G; ++gi) {
+      const int b = b0 + 4 * gi;
+      if (b < nb) {
+        const c8h a0 = gather(b, 0), a1 = gather(b, 1);
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) {
+          c4f acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, cur[gi][cb][0], c4f{0, 0, 0, 0}, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, cur[gi][cb][1], acc, 0, 0, 0);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const uint32_t code = __float_as_uint(fmaf(acc[e], g[e], rqd::kRoundMagic)) & 0xFu;
+            const uint32_t other = __float_as_uint(rqd::lane_xor<1>(__uint_as_float(code)));
+            const int row = 4 * q + e;
+            if (row < RW && (r16 & 1) == 0)
+              sc[row * (KMAX / 2) + (b * kCB + cb * 16 + r16) / 2] = static_cast<uint8_t>(code | (other << 4));
+          }
         }
       }
     }
   }
   __syncthreads();
 
-  // Pack 16 codes per thread into 8 bytes.
-  const int ppr = K / 16;
+  // Store 16 packed bytes per thread.
+  const int ppr = K / 32;
   for (int p = tid; p < RW * ppr; p += 256) {
-    const int r = p / ppr, c16 = p - r * ppr;
+    const int r = p / ppr, c32 = p - r * ppr;
     if (row0 + r >= M) continue;
-    const uint4 w = *reinterpret_cast<const uint4*>(&sc[r * KMAX + c16 * 16]);
-    uint2 out;
-    out.x = pack4codes(w.x) | (pack4codes(w.y) << 16);
-    out.y = pack4codes(w.z) | (pack4codes(w.w) << 16);
-    *reinterpret_cast<uint2*>(Xq + (row0 + r) * static_cast<int64_t>(K / 2) + c16 * 8) = out;
+    *reinterpret_cast<uint4*>(Xq + (row0 + r) * static_cast<int64_t>(K / 2) + c32 * 16) =
+        *reinterpret_cast<const uint4*>(&sc[r * (KMAX / 2) + c32 * 16]);
   }
+}
+
+// Single pass for K <= 4096: eight waves, RG row groups of 16 rows (RW = 16 RG
+// rows per workgroup), every y value kept in registers until the row maxima
+// are known, so each block matrix is read once per workgroup and reused by
+// the RG row groups.  Codes are packed across lanes (channel pairs, then 4
+// and 8 channels) and stored as dwords by the lanes holding the first of 8
+// channels.
+template <int RG, int KMAX>
+__global__ __launch_bounds__(512) void rq_composite1_kernel(const uint16_t* __restrict__ X, int64_t M, int K,
+                                                            int64_t ldx, const int32_t* __restrict__ perm,
+                                                            const uint16_t* __restrict__ Rt, float s_t,
+                                                            uint8_t* __restrict__ Xq, float* __restrict__ xs) {
+  constexpr int WAVES = 8, RW = 16 * RG, XS = KMAX + 8;
+  constexpr int NBW = KMAX / kCB / WAVES;  // blocks per wave at K = KMAX
+  __shared__ __attribute__((aligned(16))) uint16_t sx[RW * XS];
+  __shared__ __attribute__((aligned(16))) int32_t sp[KMAX];
+  __shared__ float red[WAVES][RW];
+  __shared__ float gscale[RW];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t row0 = static_cast<int64_t>(blockIdx.x) * RW;
+  const int nb = K / kCB;
+  const int vpr = K / 8;
+
+  for (int p0 = tid; p0 < RW * vpr; p0 += 512 * 8) {
+    uint4 v[8];
+    bool ok[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int p = p0 + u * 512;
+      const int r = p / vpr, c8 = p - r * vpr;
+      ok[u] = p < RW * vpr && row0 + r < M;
+      const int64_t gr = ok[u] ? row0 + r : 0;
+      v[u] = *reinterpret_cast<const uint4*>(X + gr * ldx + (ok[u] ? c8 * 8 : 0));
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int p = p0 + u * 512;
+      const int r = p / vpr, c8 = p - r * vpr;
+      if (p < RW * vpr) *reinterpret_cast<uint4*>(&sx[r * XS + c8 * 8]) = ok[u] ? v[u] : make_uint4(0, 0, 0, 0);
+    }
+  }
+  for (int k4 = tid; k4 < K / 4; k4 += 512) {
+    int4 pv = *reinterpret_cast<const int4*>(perm + 4 * k4);
+    pv.x = min(max(pv.x, 0), K - 1);
+    pv.y = min(max(pv.y, 0), K - 1);
+    pv.z = min(max(pv.z, 0), K - 1);
+    pv.w = min(max(pv.w, 0), K - 1);
+    *reinterpret_cast<int4*>(&sp[4 * k4]) = pv;
+  }
+  __syncthreads();
+
+  const int r16 = lane & 15, q = lane >> 4;
+  auto gather = [&](int b, int kk, int rg) -> c8h {
+    const int k0 = b * kCB + kk * 32 + 8 * q;
+    const int4 pa = *reinterpret_cast<const int4*>(&sp[k0]);
+    const int4 pb = *reinterpret_cast<const int4*>(&sp[k0 + 4]);
+    const int idx[8] = {pa.x, pa.y, pa.z, pa.w, pb.x, pb.y, pb.z, pb.w};
+    const uint16_t* xrow = &sx[(rg * 16 + r16) * XS];
+    c8h a;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) a[j] = __builtin_bit_cast(_Float16, xrow[idx[j]]);
+    return a;
+  };
+
+  c4f y[NBW][4][RG];
+  float amax[RG][4];
+#pragma unroll
+  for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) amax[rg][e] = 0.0f;
+  // The block matrix fragments of block i + 1 are loaded while block i is
+  // multiplied (blocks past the end read block 0 and are not used).
+  auto load_b = [&](int b, c8h (&f)[4][2]) {
+    const int bb = b < nb ? b : 0;
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+        f[cb][kk] = *reinterpret_cast<const c8h*>(Rt + (static_cast<int64_t>(bb) * kCB + cb * 16 + r16) * kCB +
+                                                  kk * 32 + 8 * q);
+  };
+  c8h bnext[4][2];
+  load_b(wave, bnext);
+#pragma unroll
+  for (int i = 0; i < NBW; ++i) {
+    const int b = wave + WAVES * i;
+    c8h bf[4][2];
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) {
+      bf[cb][0] = bnext[cb][0];
+      bf[cb][1] = bnext[cb][1];
+    }
+    if (i + 1 < NBW) load_b(b + WAVES, bnext);
+    __builtin_amdgcn_sched_barrier(0);
+    if (b < nb) {
+#pragma unroll
+      for (int rg = 0; rg < RG; ++rg) {
+        const c8h a0 = gather(b, 0, rg), a1 = gather(b, 1, rg);
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) {
+          c4f acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, bf[cb][0], c4f{0, 0, 0, 0}, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, bf[cb][1], acc, 0, 0, 0);
+          y[i][cb][rg] = acc;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) amax[rg][e] = fmaxf(amax[rg][e], fabsf(acc[e]));
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float m = amax[rg][e];
+      m = fmaxf(m, rqd::lane_xor<1>(m));
+      m = fmaxf(m, rqd::lane_xor<2>(m));
+      m = fmaxf(m, rqd::lane_xor<4>(m));
+      m = fmaxf(m, rqd::lane_xor<8>(m));
+      if (r16 == 0) red[wave][rg * 16 + 4 * q + e] = m;
+    }
+  __syncthreads();
+  if (tid < RW) {
+    float m = red[0][tid];
+#pragma unroll
+    for (int w = 1; w < WAVES; ++w) m = fmaxf(m, red[w][tid]);
+    const float a_z = m * s_t;
+    const float delta = a_z / 7.0f;
+    gscale[tid] = delta > 0.0f ? s_t / delta : 0.0f;
+    if (row0 + tid < M) xs[row0 + tid] = delta / s_t;
+  }
+  __syncthreads();
+
+#pragma unroll
+  for (int i = 0; i < NBW; ++i) {
+    const int b = wave + WAVES * i;
+    if (b < nb) {
+#pragma unroll
+      for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int row = rg * 16 + 4 * q + e;
+          const float g = gscale[row];
+#pragma unroll
+          for (int cb = 0; cb < 4; ++cb) {
+            // code of channel b*64 + cb*16 + r16; pack 8 consecutive channels
+            uint32_t c = __float_as_uint(fmaf(y[i][cb][rg][e], g, rqd::kRoundMagic)) & 0xFu;
+            c |= __float_as_uint(rqd::lane_xor<1>(__uint_as_float(c))) << 4;
+            c |= __float_as_uint(rqd::lane_xor<2>(__uint_as_float(c))) << 8;
+            c |= __float_as_uint(rqd::lane_xor<4>(__uint_as_float(c))) << 16;
+            if ((r16 & 7) == 0 && row0 + row < M)
+              *reinterpret_cast<uint32_t*>(Xq + (row0 + row) * static_cast<int64_t>(K / 2) +
+                                           (b * kCB + cb * 16 + r16) / 2) = c;
+          }
+        }
+    }
+  }
+}
+
+template <int RG, int KMAX>
+int launch_composite1(const void* X, int64_t M, int64_t K, int64_t ldx, const int32_t* perm, const void* Rt,
+                      float s, uint8_t* Xq, float* x_scale, hipStream_t stream) {
+  const unsigned grid = static_cast<unsigned>((M + 16 * RG - 1) / (16 * RG));
+  hipLaunchKernelGGL((rq_composite1_kernel<RG, KMAX>), dim3(grid), dim3(512), 0, stream,
+                     static_cast<const uint16_t*>(X), M, static_cast<int>(K), ldx, perm,
+                     static_cast<const uint16_t*>(Rt), s, Xq, x_scale);
+  return launch_status();
 }
 
 template <int RW, int KMAX>
 int launch_composite(const void* X, int64_t M, int64_t K, int64_t ldx, const int32_t* perm, const void* Rt,
                      float s, uint8_t* Xq, float* x_scale, hipStream_t stream) {
   const unsigned grid = static_cast<unsigned>((M + RW - 1) / RW);
-  hipLaunchKernelGGL((rq_composite_kernel<RW, KMAX>), dim3(grid), dim3(256), 0, stream,
+  hipLaunchKernelGGL((rq_composite_kernel<RW, KMAX, 2>), dim3(grid), dim3(256), 0, stream,
                      static_cast<const uint16_t*>(X), M, static_cast<int>(K), ldx, perm,
                      static_cast<const uint16_t*>(Rt), s, Xq, x_scale);
   return launch_status();
@@ -186,7 +408,7 @@ extern "C" int oq_rotate_quantize_act_composite(const void* X, int64_t M, int64_
   if (t < 0) return OQ_ERR_ARG;
   if (M == 0) return OQ_OK;
   if (!X || !perm || !Rt || !Xq || !x_scale) return OQ_ERR_NULL;
-  if (!oq::aligned(X, 16) || !oq::aligned(perm, 16) || !oq::aligned(Rt, 16) || !oq::aligned(Xq, 8) ||
+  if (!oq::aligned(X, 16) || !oq::aligned(perm, 16) || !oq::aligned(Rt, 16) || !oq::aligned(Xq, 16) ||
       !oq::aligned(x_scale, 4))
     return OQ_ERR_ALIGN;
   const float s = s_table ? s_table[t] : 1.0f;
@@ -194,9 +416,13 @@ extern "C" int oq_rotate_quantize_act_composite(const void* X, int64_t M, int64_
   int st = oq::device_check();
   if (st != OQ_OK) return st;
   hipStream_t h = static_cast<hipStream_t>(stream);
-  if (K <= 1024) return oq::launch_composite<16, 1024>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
-  if (K <= 2048) return oq::launch_composite<16, 2048>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
-  if (K <= 4096) return oq::launch_composite<8, 4096>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+  // Single pass (y in registers) up to K = 4096, row groups sized to the
+  // LDS budget; deeper rows take the two-pass kernel.
+  // Few rows: one row group per workgroup, so the rows spread over more CUs.
+  if (M <= 1024 && K <= 2048) return oq::launch_composite1<1, 2048>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+  if (K <= 1024) return oq::launch_composite1<4, 1024>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+  if (K <= 2048) return oq::launch_composite1<2, 2048>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+  if (K <= 4096) return oq::launch_composite1<1, 4096>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
   if (K <= 8192) return oq::launch_composite<4, 8192>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
   return oq::launch_composite<2, 16384>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
 }
