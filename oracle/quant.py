@@ -71,3 +71,54 @@ def quantize_weights(w_u: np.ndarray, b: int):
     """
     wf = fwht(np.asarray(w_u, dtype=np.float64), b)
     return quantize_sym(wf)
+
+
+# ---------------------------------------------------------------------------
+# Per-step static activation scales (eq:perstep_scale, the per-(layer, step,
+# channel) table of the paper's text).  Reading: sigma_hat is the 99.9th
+# percentile of the magnitudes of the rotated activation over the calibration
+# rows (nearest rank: the k-th smallest |y| with k = ceil(p/100 n)), Delta_j =
+# sigma_hat_j / q_max, and at inference q = clamp(round(y_j / Delta_j), -7, 7)
+# with the table in place of the per-token maximum (clipping is live).  The
+# per-channel step cannot be factored out of the sum over channels, so it is
+# folded into the weight's input channels: W''[n][j] = W'[n][j] Delta_j,
+# quantized per output channel; the token scale is then 1.
+# ---------------------------------------------------------------------------
+
+def percentile_abs(y: np.ndarray, p: float) -> np.ndarray:
+    """Nearest-rank p-th percentile of |y| over rows, per column (float64 [K])."""
+    a = np.abs(np.asarray(y, dtype=np.float64))
+    n = a.shape[0]
+    k = int(np.ceil(p / 100.0 * n))
+    k = min(max(k, 1), n)
+    return np.sort(a, axis=0)[k - 1]
+
+
+def calibrate_step_scales(y: np.ndarray, p: float = 99.9, qmax: int = QMAX4) -> np.ndarray:
+    """Delta_j = percentile_abs(y, p) / q_max for the rotated calibration rows y [n, K]."""
+    return percentile_abs(y, p) / float(qmax)
+
+
+def quantize_static(y: np.ndarray, delta: np.ndarray, qmax: int = QMAX4):
+    """Codes with a static per-channel step: q = clamp(round(y / Delta_j), -q_max, q_max);
+    a channel with Delta_j = 0 gets code 0.  Returns (q, ratio)."""
+    y = np.asarray(y, dtype=np.float64)
+    d = np.asarray(delta, dtype=np.float64)
+    nz = d > 0
+    ratio = np.where(nz[None, :], y / np.where(nz, d, 1.0)[None, :], 0.0)
+    q = np.clip(np.rint(ratio), -qmax, qmax).astype(np.int64)
+    return q, ratio
+
+
+def rotate_quantize_static(x: np.ndarray, b: int, delta: np.ndarray):
+    """Hadamard rotation (as rotate_quantize_act) followed by the static
+    per-channel quantizer; token scale 1.  Returns (q, x_scale, ratio)."""
+    y = fwht(np.asarray(x, dtype=np.float64), b)
+    q, ratio = quantize_static(y, delta)
+    return q, np.ones(y.shape[0]), ratio
+
+
+def fold_weights_step(w_u: np.ndarray, b: int, delta: np.ndarray):
+    """W' = rotated weight (as quantize_weights), W'' = W' diag(Delta), per-row RTN."""
+    wf = fwht(np.asarray(w_u, dtype=np.float64), b) * np.asarray(delta, dtype=np.float64)[None, :]
+    return quantize_sym(wf)

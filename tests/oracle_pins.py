@@ -339,3 +339,68 @@ def check_rotate_quantize_composite(rqc, rotate_quantize_act, seed=24):
     y = np.einsum("mbi,bij->mbj", y, r).reshape(M, K)
     assert np.all(np.abs(y - xs[:, None] * q) <= xs[:, None] / 2 * (1 + 1e-12))
     assert np.all(np.abs(q).max(axis=1) == 7)
+
+
+# --------------------------------------------------------------------------
+# Per-step static scales
+# --------------------------------------------------------------------------
+
+def check_percentile(percentile_abs, seed=50):
+    rng = np.random.default_rng(seed)
+    for n in (1, 7, 1000, 1001):
+        y = rng.standard_normal((n, 5)) * np.array([1, 10, 0.1, 3, 0])
+        for p in (50.0, 99.9, 100.0):
+            v = np.asarray(percentile_abs(y, p))
+            a = np.abs(y)
+            for j in range(5):
+                # nearest rank: at least ceil(p n / 100) values <= v, fewer below v
+                k = max(1, int(np.ceil(p / 100.0 * n)))
+                assert np.count_nonzero(a[:, j] <= v[j]) >= k
+                assert np.count_nonzero(a[:, j] < v[j]) < k
+                assert v[j] in a[:, j]
+            if p == 100.0:
+                assert np.array_equal(v, a.max(axis=0))
+
+
+def check_quantize_static(quantize_static, seed=51):
+    rng = np.random.default_rng(seed)
+    y = rng.standard_normal((64, 32)) * 3
+    d = np.abs(rng.standard_normal(32)) * 0.5 + 0.05
+    d[3] = 0.0
+    q, _ = quantize_static(y, d)
+    q = np.asarray(q)
+    assert q.min() >= -7 and q.max() <= 7
+    assert not q[:, 3].any()
+    live = np.abs(y) <= 7 * d[None, :]
+    live[:, 3] = False
+    err = np.abs(y - d[None, :] * q)
+    assert np.all(err[live] <= d[None, :].repeat(64, 0)[live] / 2 + 1e-15), "unclipped error above Delta/2"
+    big = np.abs(y) >= 7.5 * d[None, :]
+    big[:, 3] = False
+    assert np.all(np.abs(q[big]) == 7) and np.all(np.sign(q[big]) == np.sign(y[big])), "clipping"
+    # a constant step equal to the row maximum / 7 is the per-token quantizer on that row
+    row = y[:1]
+    dd = np.full(32, np.abs(row).max() / 7)
+    qs, _ = quantize_static(row, dd)
+    qt = np.clip(np.rint(row / dd[0]), -7, 7)
+    assert np.array_equal(np.asarray(qs), qt)
+
+
+def check_fold_step(fold_weights_step, fwht, seed=52):
+    """Activations on the step grid (y = Delta_j * integer, no activation
+    error): the folded weight applied to the integer codes reproduces y W'^T
+    up to the weight's own RTN error bound; folding into the wrong axis fails."""
+    rng = np.random.default_rng(seed)
+    M, N, K, b = 6, 40, 64, 64
+    d = np.exp(rng.standard_normal(K))
+    q = rng.integers(-7, 8, size=(M, K))
+    y = q * d[None, :]
+    w = rng.standard_normal((N, K))
+    qw, ws, _ = fold_weights_step(w, b, d)
+    out = (q @ np.asarray(qw).T) * np.asarray(ws)[None, :]
+    wp = fwht(w, b)
+    ref = y @ wp.T
+    # |W'' - ws qw| <= ws / 2 elementwise, so the output error is bounded by
+    # sum_j |q_j| ws / 2
+    bound = np.abs(q).sum(axis=1)[:, None] * np.asarray(ws)[None, :] / 2
+    assert np.all(np.abs(out - ref) <= bound * (1 + 1e-12))
