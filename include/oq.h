@@ -289,6 +289,85 @@ int oq_quantize_weights_host(const double* W_u, int64_t N, int64_t K, int32_t ha
                              uint8_t* Wq, float* w_scale);
 
 /* ------------------------------------------------------------------------ */
+/* Static per-step, per-channel activation steps (Section 4.2,               */
+/* eq:perstep_scale with the per-(layer, step, channel) table)               */
+/* ------------------------------------------------------------------------ */
+/*
+ * The table holds Delta_{l,t,j} = sigma_hat(X'_{t,:,j}) / q_max for the
+ * rotated activation X' of layer l at denoising step t, sigma_hat the
+ * nearest-rank 99.9th percentile of the magnitudes over the calibration rows.
+ * At inference the codes are q = clamp(round(y_j / Delta_j), -7, 7) (clipping
+ * is live; round half to even) and the token scale is 1.  A per-channel step
+ * cannot leave the sum over channels, so it is folded into the weight's input
+ * channels per step: W''[n][j] = W'[n][j] Delta_j, quantized per output
+ * channel (one weight copy per (layer, step)); the products are then the
+ * ordinary oq_w4a4_linear / _tiled calls with x_scale = 1.
+ */
+
+/*
+ * oq_rotate_act_f32 -- the rotated activation of eq:transform alone:
+ * Y[i][k] = (x_i H_b / sqrt(b))[k] in fp32, Y device [M][K] contiguous,
+ * 16-byte aligned (the calibration input of oq_calibrate_step_scales).
+ * Arguments and shape limits as oq_rotate_quantize_act.  Errors: OQ_ERR_NULL,
+ * OQ_ERR_SHAPE, OQ_ERR_ALIGN, OQ_ERR_DEVICE, OQ_ERR_HIP.
+ */
+int oq_rotate_act_f32(const void* X, int64_t M, int64_t K, int64_t ldx, int32_t had_block,
+                      float* Y, void* stream);
+
+/*
+ * oq_calibrate_workspace_bytes -- device workspace needed by
+ * oq_calibrate_step_scales for K channels (K * 1032 bytes).
+ */
+size_t oq_calibrate_workspace_bytes(int64_t K);
+
+/*
+ * oq_calibrate_step_scales -- delta[j] = v_j / qmax, v_j the nearest-rank
+ * p-th percentile of |Y[:, j]| over the n rows: the k-th smallest magnitude
+ * with k = ceil(p / 100 * n) evaluated in double precision and clamped to
+ * [1, n].  v_j is exact (an element of the column; selection over the bit
+ * patterns, NaN ordered above +inf); the division is done in double and
+ * rounded once to fp32.
+ * Y device fp32 [n][ldy]; delta device fp32 [K]; work device, 16-byte
+ * aligned, at least oq_calibrate_workspace_bytes(K) bytes, owned by the
+ * caller and overwritten (calls that share it must not overlap).
+ * p in (0, 100]; qmax > 0 (7 for int4 codes).
+ * Errors: OQ_ERR_NULL, OQ_ERR_SHAPE (n == 0 with K > 0, ldy < K, workspace
+ * too small), OQ_ERR_ARG (p, qmax), OQ_ERR_ALIGN, OQ_ERR_DEVICE, OQ_ERR_HIP.
+ */
+int oq_calibrate_step_scales(const float* Y, int64_t n, int64_t K, int64_t ldy, double p,
+                             float qmax, float* delta, void* work, size_t work_bytes,
+                             void* stream);
+
+/*
+ * oq_rotate_quantize_act_static -- Hadamard rotation (as
+ * oq_rotate_quantize_act) followed by the static quantizer with the step row
+ * delta (device fp32 [K], 16-byte aligned: the table's row for this layer
+ * and step): Xq[i][k] = clamp(round(y_ik / delta[k]), -7, 7), x_scale[i] = 1.
+ * A channel whose step is zero, negative, NaN or infinite gets code 0.  The
+ * ratio is formed in fp32 with the hardware reciprocal of delta (about one
+ * ulp), so only ratios within a few ulps of a half integer can round
+ * differently from exact arithmetic.
+ * Errors: as oq_rotate_quantize_act; OQ_ERR_NULL (delta), OQ_ERR_ALIGN.
+ */
+int oq_rotate_quantize_act_static(const void* X, int64_t M, int64_t K, int64_t ldx,
+                                  int32_t had_block, const float* delta, uint8_t* Xq,
+                                  float* x_scale, void* stream);
+
+/* The same with the codes in the 16-row tiled layout (K % 128 == 0). */
+int oq_rotate_quantize_act_static_tiled(const void* X, int64_t M, int64_t K, int64_t ldx,
+                                        int32_t had_block, const float* delta, uint8_t* Xt,
+                                        float* x_scale, void* stream);
+
+/*
+ * oq_quantize_weights_step_host -- oq_quantize_weights_host with the step
+ * folded in: row n of the quantized weight is RTN(W'[n][:] * delta[:]),
+ * W' = W_u rotated by H_b / sqrt(b), in float64.  delta host fp32 [K], every
+ * entry finite and >= 0.  Errors: OQ_ERR_NULL, OQ_ERR_SHAPE, OQ_ERR_ARG.
+ */
+int oq_quantize_weights_step_host(const double* W_u, int64_t N, int64_t K, int32_t had_block,
+                                  const float* delta, uint8_t* Wq, float* w_scale);
+
+/* ------------------------------------------------------------------------ */
 /* DiT denoising-step driver                                                 */
 /* ------------------------------------------------------------------------ */
 

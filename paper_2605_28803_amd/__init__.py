@@ -234,5 +234,68 @@ def quantize_weights_host(W_u: np.ndarray, had_block: int):
     return Wq, ws
 
 
+def rotate_act_f32(X, had_block, Y=None, stream=None):
+    """Rotated activation y = x H_b / sqrt(b) in fp32 [M, K] (calibration input)."""
+    M, K = X.shape
+    if Y is None:
+        Y = torch.empty((M, K), dtype=torch.float32, device=X.device)
+    _check(lib().oq_rotate_act_f32(_ptr(X), M, K, X.stride(0), had_block, _ptr(Y), _stream(stream)),
+           "oq_rotate_act_f32")
+    return Y
+
+
+def calibrate_workspace_bytes(K: int) -> int:
+    return int(lib().oq_calibrate_workspace_bytes(K))
+
+
+def calibrate_step_scales(Y, p=99.9, qmax=7.0, delta=None, work=None, stream=None):
+    """Static steps delta f32 [K] = nearest-rank p-th percentile of |Y[:, j]| / qmax."""
+    n, K = Y.shape
+    if delta is None:
+        delta = torch.empty((K,), dtype=torch.float32, device=Y.device)
+    if work is None:
+        work = torch.empty((max(calibrate_workspace_bytes(K), 16),), dtype=torch.uint8, device=Y.device)
+    _check(lib().oq_calibrate_step_scales(_ptr(Y), n, K, Y.stride(0), float(p), float(qmax), _ptr(delta),
+                                          _ptr(work), work.numel(), _stream(stream)), "oq_calibrate_step_scales")
+    return delta
+
+
+def rotate_quantize_act_static(X, had_block, delta, Xq=None, x_scale=None, stream=None):
+    """Rotation + static per-channel steps delta (f32 [K], device): (Xq uint8 [M, K/2], x_scale = 1)."""
+    M, K = X.shape
+    if Xq is None:
+        Xq = torch.empty((M, K // 2), dtype=torch.uint8, device=X.device)
+    if x_scale is None:
+        x_scale = torch.empty((M,), dtype=torch.float32, device=X.device)
+    _check(lib().oq_rotate_quantize_act_static(_ptr(X), M, K, X.stride(0), had_block, _ptr(delta), _ptr(Xq),
+                                               _ptr(x_scale), _stream(stream)), "oq_rotate_quantize_act_static")
+    return Xq, x_scale
+
+
+def rotate_quantize_act_static_tiled(X, had_block, delta, Xt=None, x_scale=None, stream=None):
+    """As rotate_quantize_act_static, codes in the 16-row tiled layout."""
+    M, K = X.shape
+    if Xt is None:
+        Xt = torch.empty((tiled_bytes(M, K),), dtype=torch.uint8, device=X.device)
+    if x_scale is None:
+        x_scale = torch.empty((M,), dtype=torch.float32, device=X.device)
+    _check(lib().oq_rotate_quantize_act_static_tiled(_ptr(X), M, K, X.stride(0), had_block, _ptr(delta),
+                                                     _ptr(Xt), _ptr(x_scale), _stream(stream)),
+           "oq_rotate_quantize_act_static_tiled")
+    return Xt, x_scale
+
+
+def quantize_weights_step_host(W_u: np.ndarray, had_block: int, delta: np.ndarray):
+    """float64 host weight [N, K] rotated, scaled by the step row delta [K] per
+    input channel and RTN-quantized: (Wq uint8 [N, K/2], w_scale f32 [N])."""
+    W = np.ascontiguousarray(W_u, dtype=np.float64)
+    N, K = W.shape
+    d = np.ascontiguousarray(delta, dtype=np.float32)
+    Wq = np.empty((N, K // 2), dtype=np.uint8)
+    ws = np.empty((N,), dtype=np.float32)
+    _check(lib().oq_quantize_weights_step_host(W.ctypes.data, N, K, had_block, d.ctypes.data, Wq.ctypes.data,
+                                               ws.ctypes.data), "oq_quantize_weights_step_host")
+    return Wq, ws
+
 
 from .dit import DiT  # noqa: E402,F401

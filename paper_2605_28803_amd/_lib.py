@@ -54,6 +54,12 @@ SIGNATURES = {
     "oq_quantize_weights_composite_host": (i32, [vp, i64, i64, i32, vp, vp, vp, vp]),
     "oq_quantize_weights": (i32, [vp, i64, i64, i64, i32, vp, vp, vp]),
     "oq_quantize_weights_host": (i32, [vp, i64, i64, i32, vp, vp]),
+    "oq_rotate_act_f32": (i32, [vp, i64, i64, i64, i32, vp, vp]),
+    "oq_calibrate_workspace_bytes": (C.c_size_t, [i64]),
+    "oq_calibrate_step_scales": (i32, [vp, i64, i64, i64, C.c_double, C.c_float, vp, vp, C.c_size_t, vp]),
+    "oq_rotate_quantize_act_static": (i32, [vp, i64, i64, i64, i32, vp, vp, vp, vp]),
+    "oq_rotate_quantize_act_static_tiled": (i32, [vp, i64, i64, i64, i32, vp, vp, vp, vp]),
+    "oq_quantize_weights_step_host": (i32, [vp, i64, i64, i32, vp, vp, vp]),
     "oq_dit_workspace_bytes": (i32, [C.POINTER(oq_dit_config), C.POINTER(C.c_size_t)]),
     "oq_dit_create": (i32, [C.POINTER(oq_dit_config), C.POINTER(oq_dit_weights), C.POINTER(vp)]),
     "oq_dit_set_workspace": (i32, [vp, vp, C.c_size_t]),

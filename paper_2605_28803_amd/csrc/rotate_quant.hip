@@ -50,20 +50,22 @@ template <int C>
 __global__ __launch_bounds__(256) void rq_kernel(const uint16_t* __restrict__ X, int64_t M, int K,
                                                  int64_t ldx, int logT, int logb, float s_t,
                                                  float s_over_sqrtb, uint8_t* __restrict__ Xq,
-                                                 float* __restrict__ xs, float* __restrict__ ratio, bool tiled) {
+                                                 float* __restrict__ xs, float* __restrict__ ratio, bool tiled,
+                                                 const float* __restrict__ sdelta, bool rotate_only) {
   extern __shared__ float lds[];  // [rows_per_wg][K] when a row spans several waves
   __shared__ float red[4];
   const rqd::RowMap m = rqd::row_map(logT, M);
   float v[C][8];
   rqd::load_row_f16<C>(v, X, ldx, m);
-  rqd::rq_core<C>(v, m, K, logb, s_t, s_over_sqrtb, lds, red, Xq, xs, ratio, tiled);
+  rqd::rq_core<C>(v, m, K, logb, s_t, s_over_sqrtb, lds, red, Xq, xs, ratio, tiled, sdelta, rotate_only);
 }
 
 // One row per wave (W = 1) or per workgroup (W > 1).
 template <int NG, int W, bool FULL>
 __global__ __launch_bounds__(256) void rq_mfma_kernel(const uint16_t* __restrict__ X, int64_t M, int64_t ldx, int logb,
                                                       float s_t, float s_over_sqrtb, uint8_t* __restrict__ Xq,
-                                                      float* __restrict__ xs, float* __restrict__ ratio, bool tiled) {
+                                                      float* __restrict__ xs, float* __restrict__ ratio, bool tiled,
+                                                      const float* __restrict__ sdelta, bool rotate_only) {
   // W > 1: [4 waves][NG groups][2 halves][64 lanes] float4 (consecutive lanes
   // hit consecutive 16-byte words: no bank conflicts on either side).
   extern __shared__ float4 xch[];
@@ -79,7 +81,8 @@ __global__ __launch_bounds__(256) void rq_mfma_kernel(const uint16_t* __restrict
     cur[g] = valid ? *reinterpret_cast<const rqm::rv8h*>(xr + rqm::chan0<NG>(wr, g, lane)) : rqm::rv8h{};
   rqm::rv8h a1, a2;
   rqm::hadamard_frags(lane, a1, a2);
-  rqm::rq_row<NG, W, FULL>(cur, a1, a2, row, valid, lane, wv, logb, s_t, s_over_sqrtb, Xq, xs, ratio, xch, red, tiled);
+  rqm::rq_row<NG, W, FULL>(cur, a1, a2, row, valid, lane, wv, logb, s_t, s_over_sqrtb, Xq, xs, ratio, xch, red, tiled,
+                           sdelta, rotate_only);
 }
 
 // (NG, W) of the matrix-core variant for K channels, or false.
@@ -98,7 +101,8 @@ bool rq_mfma_shape(int64_t K, int* ng, int* w) {
 }
 
 int rq_mfma_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block, float s_t, uint8_t* Xq,
-                   float* x_scale, float* ratio, hipStream_t stream, bool tiled) {
+                   float* x_scale, float* ratio, hipStream_t stream, bool tiled, const float* sdelta,
+                   bool rotate_only) {
   int ng = 0, w = 0;
   rq_mfma_shape(K, &ng, &w);
   const int logb = ilog2(had_block);
@@ -112,10 +116,10 @@ int rq_mfma_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_blo
   if (ng == NG && w == W) {                                                                                   \
     if (had_block == K)                                                                                       \
       hipLaunchKernelGGL((rq_mfma_kernel<NG, W, true>), dim3(grid), dim3(256), lds, stream, x, M, ldx, logb,  \
-                         s_t, s_over_sqrtb, Xq, x_scale, ratio, tiled);                                       \
+                         s_t, s_over_sqrtb, Xq, x_scale, ratio, tiled, sdelta, rotate_only);                  \
     else                                                                                                      \
       hipLaunchKernelGGL((rq_mfma_kernel<NG, W, false>), dim3(grid), dim3(256), lds, stream, x, M, ldx, logb, \
-                         s_t, s_over_sqrtb, Xq, x_scale, ratio, tiled);                                       \
+                         s_t, s_over_sqrtb, Xq, x_scale, ratio, tiled, sdelta, rotate_only);                  \
     return launch_status();                                                                                   \
   }
   OQ_RQM(1, 1)
@@ -161,11 +165,12 @@ int rq_validate(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block,
 }
 
 int rq_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block, float s_t, uint8_t* Xq,
-              float* x_scale, float* ratio, hipStream_t stream, bool tiled) {
+              float* x_scale, float* ratio, hipStream_t stream, bool tiled, const float* sdelta,
+              bool rotate_only) {
   if (M == 0) return OQ_OK;
   int ng = 0, w = 0;
   if (had_block >= 32 && rq_mfma_shape(K, &ng, &w))
-    return rq_mfma_launch(X, M, K, ldx, had_block, s_t, Xq, x_scale, ratio, stream, tiled);
+    return rq_mfma_launch(X, M, K, ldx, had_block, s_t, Xq, x_scale, ratio, stream, tiled, sdelta, rotate_only);
   RQPlan p;
   rq_plan(K, &p);
   const int T = 1 << p.logT;
@@ -180,7 +185,7 @@ int rq_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block, f
   case CH:                                                                                             \
     hipLaunchKernelGGL(rq_kernel<CH>, dim3(static_cast<unsigned>(grid)), dim3(threads), lds, stream, x, \
                        M, static_cast<int>(K), ldx, p.logT, logb, s_t, s_over_sqrtb, Xq, x_scale, ratio, \
-                       tiled);                                                                         \
+                       tiled, sdelta, rotate_only);                                                    \
     break;
   switch (p.chunks) {
     OQ_RQ_CASE(1)
@@ -257,4 +262,39 @@ extern "C" int oq_codes_to_tiled(const uint8_t* Q, int64_t rows, int64_t K, uint
   hipLaunchKernelGGL(oq::tile_codes_kernel, dim3(static_cast<unsigned>((pieces + 255) / 256)), dim3(256), 0,
                      static_cast<hipStream_t>(stream), Q, rows, K, T);
   return oq::launch_status();
+}
+
+extern "C" int oq_rotate_act_f32(const void* X, int64_t M, int64_t K, int64_t ldx, int32_t had_block, float* Y,
+                                 void* stream) {
+  int st = oq::rq_validate(X, M, K, ldx, had_block, Y, reinterpret_cast<const float*>(Y));
+  if (st != OQ_OK || M == 0) return st;
+  if ((st = oq::device_check()) != OQ_OK) return st;
+  return oq::rq_launch(X, M, K, ldx, had_block, 1.0f, nullptr, nullptr, Y, static_cast<hipStream_t>(stream), false,
+                       nullptr, true);
+}
+
+namespace {
+int rq_static(const void* X, int64_t M, int64_t K, int64_t ldx, int32_t had_block, const float* delta, uint8_t* Xq,
+              float* x_scale, void* stream, bool tiled) {
+  int st = oq::rq_validate(X, M, K, ldx, had_block, Xq, x_scale);
+  if (st != OQ_OK) return st;
+  if (tiled && K % 128 != 0) return OQ_ERR_SHAPE;
+  if (M == 0) return OQ_OK;
+  if (!delta) return OQ_ERR_NULL;
+  if (!oq::aligned(delta, 16)) return OQ_ERR_ALIGN;
+  if ((st = oq::device_check()) != OQ_OK) return st;
+  return oq::rq_launch(X, M, K, ldx, had_block, 1.0f, Xq, x_scale, nullptr, static_cast<hipStream_t>(stream), tiled,
+                       delta, false);
+}
+}  // namespace
+
+extern "C" int oq_rotate_quantize_act_static(const void* X, int64_t M, int64_t K, int64_t ldx, int32_t had_block,
+                                             const float* delta, uint8_t* Xq, float* x_scale, void* stream) {
+  return rq_static(X, M, K, ldx, had_block, delta, Xq, x_scale, stream, false);
+}
+
+extern "C" int oq_rotate_quantize_act_static_tiled(const void* X, int64_t M, int64_t K, int64_t ldx,
+                                                   int32_t had_block, const float* delta, uint8_t* Xt,
+                                                   float* x_scale, void* stream) {
+  return rq_static(X, M, K, ldx, had_block, delta, Xt, x_scale, stream, true);
 }

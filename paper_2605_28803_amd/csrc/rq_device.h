@@ -177,15 +177,32 @@ __device__ __forceinline__ uint32_t pack8(const uint32_t (&b)[8]) {
   return (e & 0x0F0F0F0Fu) | ((o << 4) & 0xF0F0F0F0u);
 }
 
+// Static per-channel quantizer (eq:perstep_scale with the per-channel table
+// in place of the token step, eq:quant): code = clamp(rne(y / Delta), -7, 7)
+// for the unnormalized butterfly output u = y * sqrt(b) (inv_sqrtb =
+// 1 / sqrt(b)), returned as the bit pattern of (code + 1.5 * 2^23) for pack8.
+// A channel whose step is not a positive number (zero, negative, NaN) and
+// one with an infinite step get code 0.  Clamping the ratio to [-7, 7]
+// before rounding equals clamping the rounded code, the bounds being integers.
+__device__ __forceinline__ uint32_t static_code(float u, float delta, float inv_sqrtb) {
+  const float g = delta > 0.0f ? inv_sqrtb * __builtin_amdgcn_rcpf(delta) : 0.0f;
+  const float r = __builtin_amdgcn_fmed3f(u * g, -7.0f, 7.0f);
+  return __float_as_uint(r + kRoundMagic);
+}
+
 // The rest of the fused pass once the row's fp32 values are in registers:
 // butterflies, row maximum, scales, codes.  `lds` must hold rows_per_wg * K
 // floats when logT > 6; `red` is a 4-float shared array.  Every thread of the
 // workgroup must call it.  ratio != nullptr writes z / Delta instead of codes;
 // tiled selects the 16-row tiled code layout for Xq (K % 128 == 0).
+// sdelta != nullptr selects the static per-channel quantizer (step
+// sdelta[k] of channel k, token scale 1, see static_code); rotate_only
+// writes the normalized rotation s_t * y in fp32 to `ratio` and nothing else.
 template <int C>
 __device__ __forceinline__ void rq_core(float (&v)[C][8], const RowMap& m, int K, int logb, float s_t,
                                         float s_over_sqrtb, float* lds, float* red, uint8_t* __restrict__ Xq,
-                                        float* __restrict__ xs, float* __restrict__ ratio, bool tiled = false) {
+                                        float* __restrict__ xs, float* __restrict__ ratio, bool tiled = false,
+                                        const float* __restrict__ sdelta = nullptr, bool rotate_only = false) {
   // Bits 0..2: inside each 8-channel chunk.
 #pragma unroll
   for (int q = 0; q < 3; ++q) {
@@ -270,6 +287,39 @@ __device__ __forceinline__ void rq_core(float (&v)[C][8], const RowMap& m, int K
             }
       }
     }
+  }
+
+  // Rotation only, or the static quantizer: no row maximum (the branch is
+  // uniform over the grid, so skipping row_reduce's barrier is safe).
+  if (rotate_only) {
+    if (!m.valid) return;
+    float* yr = ratio + m.row * static_cast<int64_t>(K);
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      float4* dst = reinterpret_cast<float4*>(yr + chan(m, c, 0));
+      const float g = s_over_sqrtb;
+      dst[0] = make_float4(v[c][0] * g, v[c][1] * g, v[c][2] * g, v[c][3] * g);
+      dst[1] = make_float4(v[c][4] * g, v[c][5] * g, v[c][6] * g, v[c][7] * g);
+    }
+    return;
+  }
+  if (sdelta != nullptr) {
+    if (!m.valid) return;
+    if (m.t == 0) xs[m.row] = 1.0f;
+    uint8_t* qr = Xq + m.row * static_cast<int64_t>(K / 2);
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      const float4* dp = reinterpret_cast<const float4*>(sdelta + chan(m, c, 0));
+      const float4 d0 = dp[0], d1 = dp[1];
+      const float d[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+      uint32_t b[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) b[j] = static_code(v[c][j], d[j], s_over_sqrtb);
+      const int p = chan(m, c, 0) / 2;
+      uint8_t* dst = tiled ? Xq + tiled_offset(m.row, p, K / 128) : qr + p;
+      *reinterpret_cast<uint32_t*>(dst) = pack8(b);
+    }
+    return;
   }
 
   // Row absolute maximum of the unnormalized transform.

@@ -70,12 +70,14 @@ __device__ __forceinline__ int chan0(int wr, int g, int lane) {
 // ratio != nullptr, the fp32 ratios z / Delta).  cur[g] holds channels
 // chan0(wr, g, lane) .. + 7.  Every wave of the workgroup calls it: it
 // synchronizes when W > 1 (xch: [4][NG][2][64] float4 of LDS), and `red` is
-// a 4-float shared array.
+// a 4-float shared array.  sdelta / rotate_only: the static per-channel
+// quantizer and the fp32 rotation output, as in rqd::rq_core.
 template <int NG, int W, bool FULL>
 __device__ __forceinline__ void rq_row(const rv8h (&cur)[NG], const rv8h& a1, const rv8h& a2, int64_t row, bool valid,
                                        int lane, int wv, int logb, float s_t, float s_over_sqrtb,
                                        uint8_t* __restrict__ Xq, float* __restrict__ xs, float* __restrict__ ratio,
-                                       float4* xch, float* red, bool tiled) {
+                                       float4* xch, float* red, bool tiled,
+                                       const float* __restrict__ sdelta = nullptr, bool rotate_only = false) {
   using S = Shape<NG, W>;
   constexpr int K = S::K, LOGNG = S::LOGNG, LOGW = S::LOGW, GW = S::GW;
   const int rsub = wv / W, wr = wv % W;
@@ -159,6 +161,40 @@ __device__ __forceinline__ void rq_row(const rv8h (&cur)[NG], const rv8h& a1, co
     }
   }
 
+  auto group_of = [&](int s) { return xpose ? (s % W) * NG + wr * GW + s / W : wr * NG + s; };
+  // Rotation only, or the static quantizer: no row maximum (uniform branch;
+  // no barrier follows).
+  if (rotate_only) {
+    if (!valid) return;
+#pragma unroll
+    for (int s = 0; s < NG; ++s) {
+      float* yr = ratio + row * K + (group_of(s) * 16 + cl) * 32 + 8 * q;
+      const float g = s_over_sqrtb;
+      reinterpret_cast<float4*>(yr)[0] = make_float4(v[s][0] * g, v[s][1] * g, v[s][2] * g, v[s][3] * g);
+      reinterpret_cast<float4*>(yr)[1] = make_float4(v[s][4] * g, v[s][5] * g, v[s][6] * g, v[s][7] * g);
+    }
+    return;
+  }
+  if (sdelta != nullptr) {
+    if (!valid) return;
+    if (wr == 0 && lane == 0) xs[row] = 1.0f;
+    uint8_t* qr = Xq + row * (K / 2);
+#pragma unroll
+    for (int s = 0; s < NG; ++s) {
+      const int c0 = (group_of(s) * 16 + cl) * 32 + 8 * q;
+      const float4 d0 = reinterpret_cast<const float4*>(sdelta + c0)[0];
+      const float4 d1 = reinterpret_cast<const float4*>(sdelta + c0)[1];
+      const float d[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+      uint32_t b[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) b[e] = rqd::static_code(v[s][e], d[e], s_over_sqrtb);
+      const int p = c0 / 2;
+      uint8_t* dst = tiled ? Xq + tiled_offset(row, p, K / 128) : qr + p;
+      *reinterpret_cast<uint32_t*>(dst) = rqd::pack8(b);
+    }
+    return;
+  }
+
   // Row maximum: registers, lanes, then the W waves of the row.
   float amax = 0.0f;
 #pragma unroll
@@ -184,7 +220,6 @@ __device__ __forceinline__ void rq_row(const rv8h (&cur)[NG], const rv8h& a1, co
   const float gm = delta > 0.0f ? s_over_sqrtb / delta : 0.0f;
   if (!valid) return;
   if (wr == 0 && lane == 0) xs[row] = delta / s_t;
-  auto group_of = [&](int s) { return xpose ? (s % W) * NG + wr * GW + s / W : wr * NG + s; };
   if (ratio != nullptr) {
 #pragma unroll
     for (int s = 0; s < NG; ++s) {

@@ -3,6 +3,12 @@
 // round-to-nearest (eq:transform, eq:scale, eq:quant; RTN as in the
 // Implementation Details for the DiT side).  Rows are independent and split
 // across std::thread workers.
+//
+// With a static per-channel activation step Delta_j (eq:perstep_scale, the
+// per-channel table), the step multiplies input channel j of the rotated
+// weight before the per-row quantization, W''[n][j] = W'[n][j] Delta_j, so
+// that sum_j (Delta_j q_j) W'[n][j] = sum_j q_j W''[n][j] keeps an integer
+// product with token scale 1.
 #include <algorithm>
 #include <cmath>
 #include <thread>
@@ -12,7 +18,8 @@
 
 namespace {
 
-void prepare_rows(const double* W, int64_t r0, int64_t r1, int64_t K, int b, uint8_t* Wq, float* ws) {
+void prepare_rows(const double* W, int64_t r0, int64_t r1, int64_t K, int b, const float* delta, uint8_t* Wq,
+                  float* ws) {
   std::vector<double> y(static_cast<size_t>(K));
   const double norm = 1.0 / std::sqrt(static_cast<double>(b));
   for (int64_t n = r0; n < r1; ++n) {
@@ -28,6 +35,7 @@ void prepare_rows(const double* W, int64_t r0, int64_t r1, int64_t K, int b, uin
     double amax = 0.0;
     for (int64_t k = 0; k < K; ++k) {
       y[k] *= norm;
+      if (delta) y[k] *= static_cast<double>(delta[k]);
       amax = std::max(amax, std::fabs(y[k]));
     }
     const double delta = amax / 7.0;
@@ -47,8 +55,10 @@ void prepare_rows(const double* W, int64_t r0, int64_t r1, int64_t K, int b, uin
 
 }  // namespace
 
-extern "C" int oq_quantize_weights_host(const double* W_u, int64_t N, int64_t K, int32_t had_block, uint8_t* Wq,
-                                        float* w_scale) {
+namespace {
+
+int quantize_rows(const double* W_u, int64_t N, int64_t K, int32_t had_block, const float* delta, uint8_t* Wq,
+                  float* w_scale) {
   if (!W_u || !Wq || !w_scale) return OQ_ERR_NULL;
   if (N < 1 || K < 2 || K % 2 != 0 || !oq::is_pow2(had_block) || had_block > OQ_MAX_HAD_BLOCK ||
       K % had_block != 0)
@@ -58,8 +68,23 @@ extern "C" int oq_quantize_weights_host(const double* W_u, int64_t N, int64_t K,
   std::vector<std::thread> pool;
   for (int64_t i = 0; i < nt; ++i) {
     const int64_t r0 = N * i / nt, r1 = N * (i + 1) / nt;
-    pool.emplace_back(prepare_rows, W_u, r0, r1, K, had_block, Wq, w_scale);
+    pool.emplace_back(prepare_rows, W_u, r0, r1, K, had_block, delta, Wq, w_scale);
   }
   for (auto& th : pool) th.join();
   return OQ_OK;
+}
+
+}  // namespace
+
+extern "C" int oq_quantize_weights_host(const double* W_u, int64_t N, int64_t K, int32_t had_block, uint8_t* Wq,
+                                        float* w_scale) {
+  return quantize_rows(W_u, N, K, had_block, nullptr, Wq, w_scale);
+}
+
+extern "C" int oq_quantize_weights_step_host(const double* W_u, int64_t N, int64_t K, int32_t had_block,
+                                             const float* delta, uint8_t* Wq, float* w_scale) {
+  if (!delta) return OQ_ERR_NULL;
+  for (int64_t k = 0; k < K; ++k)
+    if (!(delta[k] >= 0.0f) || !std::isfinite(delta[k])) return OQ_ERR_ARG;
+  return quantize_rows(W_u, N, K, had_block, delta, Wq, w_scale);
 }

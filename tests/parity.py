@@ -56,6 +56,38 @@ def tau_rows(x: np.ndarray, b: int) -> np.ndarray:
     return np.where(umax > 0, 14 * gamma * l1 / safe + 21 * U32, 0.0)
 
 
+def block_l1(x: np.ndarray, b: int) -> np.ndarray:
+    """Per element: the sum of |x| over the Hadamard block that holds it [M, K]."""
+    x = np.asarray(x, dtype=np.float64)
+    M, K = x.shape
+    l1 = np.abs(x).reshape(M, K // b, b).sum(axis=2)
+    return np.repeat(l1, b, axis=1)
+
+
+def tau_rotate(x: np.ndarray, b: int, y_ref: np.ndarray) -> np.ndarray:
+    """Elementwise bound on |y_gpu - y_exact| for the fp32 rotation output:
+    the butterfly error gamma_d l1 / sqrt(b) and two roundings of the
+    normalization (the factor 1 / sqrt(b) and the product)."""
+    d = int(np.log2(b)) + 32
+    gamma = d * U32 / (1 - d * U32)
+    return gamma * block_l1(x, b) / np.sqrt(b) + 2 * U32 * np.abs(y_ref)
+
+
+def tau_static(x: np.ndarray, b: int, delta: np.ndarray, r_ref: np.ndarray) -> np.ndarray:
+    """Elementwise bound on |r_gpu - r_exact| of the static quantizer, r =
+    y / Delta_j formed as u * (fl(1 / sqrt(b)) * rcp(Delta_j)): the butterfly
+    error divided by sqrt(b) Delta_j, plus relative roundings of the factor,
+    the hardware reciprocal (one ulp), their product and the final product
+    (at most 6 * 2^-24 |r| together).  Zero where the step is not positive."""
+    d = int(np.log2(b)) + 32
+    gamma = d * U32 / (1 - d * U32)
+    dl = np.asarray(delta, dtype=np.float64)
+    ok = (dl > 0) & np.isfinite(dl)
+    safe = np.where(ok, dl, 1.0)
+    t = gamma * block_l1(x, b) / (np.sqrt(b) * safe[None, :]) + 6 * U32 * np.abs(r_ref)
+    return np.where(ok[None, :], t, 0.0)
+
+
 def dist_to_boundary(r: np.ndarray) -> np.ndarray:
     """Distance of each ratio to the nearest half integer."""
     return np.abs(np.abs(r - np.floor(r)) - 0.5)
@@ -68,7 +100,8 @@ def check_codes(q_gpu, q_ref, r_ref, tau_row):
     mism = q_gpu != q_ref
     n = int(mism.sum())
     total = q_ref.size
-    near = dist_to_boundary(r_ref) <= tau_row[:, None]
+    tau = np.asarray(tau_row, dtype=np.float64)
+    near = dist_to_boundary(r_ref) <= (tau if tau.ndim == 2 else tau[:, None])
     if n:
         assert np.all(np.abs(q_gpu[mism] - q_ref[mism]) == 1), "a code differs by more than one step"
         assert np.all(near[mism]), "a code differs away from a rounding boundary"
