@@ -9,15 +9,15 @@ acc[i, n] (+ bias[n]).
 
 The integer product is evaluated as a float64 matrix product of the integer
 codes.  That is exact: every product and every partial sum is an integer of
-magnitude at most 49*K < 2^53, and float64 adds such integers without
-rounding in any order.  Pins: an int64 triple loop on tiny shapes, +-identity
+magnitude at most max|q| max|qw| K (49 K for W4A4, 889 K for W4A8) < 2^53,
+and float64 adds such integers without rounding in any order.  Pins: an int64 triple loop on tiny shapes, +-identity
 and all-ones weights, and unit-scale epilogue.
 """
 from __future__ import annotations
 
 import numpy as np
 
-from .quant import rotate_quantize_act, quantize_weights
+from .quant import QMAX8, rotate_quantize_act, quantize_weights
 
 
 def int_gemm(q: np.ndarray, qw: np.ndarray) -> np.ndarray:
@@ -27,7 +27,9 @@ def int_gemm(q: np.ndarray, qw: np.ndarray) -> np.ndarray:
     if q.shape[-1] != qw.shape[-1]:
         raise ValueError("inner dimensions differ")
     K = q.shape[-1]
-    if 49 * K >= 2 ** 53:
+    mq = int(np.max(np.abs(q))) if q.size else 0
+    mw = int(np.max(np.abs(qw))) if qw.size else 0
+    if mq * mw * K >= 2 ** 53:
         raise ValueError("K too large for exact float64 accumulation")
     acc = q.astype(np.float64) @ qw.astype(np.float64).T
     out = acc.astype(np.int64)
@@ -51,6 +53,22 @@ def w4a4_linear(x: np.ndarray, w_u: np.ndarray, b: int, s_t: float = 1.0, bias=N
     quantized), integer product, dequantize.  Returns a dict of every
     intermediate."""
     q, xs, ratio = rotate_quantize_act(x, b, s_t)
+    if weights is None:
+        qw, ws, wratio = quantize_weights(w_u, b)
+    else:
+        qw, ws = weights
+        wratio = None
+    acc = int_gemm(q, qw)
+    y = dequant(acc, xs, ws, bias)
+    return {"q": q, "x_scale": xs, "ratio": ratio, "qw": qw, "w_scale": ws,
+            "wratio": wratio, "acc": acc, "y": y}
+
+
+def w4a8_linear(x: np.ndarray, w_u: np.ndarray, b: int, s_t: float = 1.0, bias=None, weights=None):
+    """Rotated W4A8 linear: as w4a4_linear with the activation quantized per
+    token to 8 bits (q_max = 127); the weight stays int4.  Returns a dict of
+    every intermediate."""
+    q, xs, ratio = rotate_quantize_act(x, b, s_t, QMAX8)
     if weights is None:
         qw, ws, wratio = quantize_weights(w_u, b)
     else:

@@ -15,9 +15,13 @@ test pins exactly that.
 Rounding: round half to even (numpy.rint).  A row whose maximum magnitude is
 0 gets Delta = 0 and all-zero codes (the division is not performed).
 
+The paper's own deployment mode is W4A8 (4-bit weights, 8-bit per-token
+activations): the same quantizer with k = 8, q_max = 127, for the activation.
+
 Pins: the quantizer error bound |z - Delta q| <= Delta/2, the absmax element
 maps to +-q_max, no code equals -8, zero / spike / constant rows, a worked
-example computed by hand, and the s_t invariance.
+example computed by hand (one for W4A4, one for W4A8), and the s_t
+invariance.
 """
 from __future__ import annotations
 
@@ -26,6 +30,7 @@ import numpy as np
 from .hadamard import fwht
 
 QMAX4 = 7
+QMAX8 = 127
 
 
 def quantize_sym(z: np.ndarray, qmax: int = QMAX4):
@@ -45,18 +50,19 @@ def quantize_sym(z: np.ndarray, qmax: int = QMAX4):
     return q, delta, ratio
 
 
-def rotate_quantize_act(x: np.ndarray, b: int, s_t: float = 1.0):
+def rotate_quantize_act(x: np.ndarray, b: int, s_t: float = 1.0, qmax: int = QMAX4):
     """Online rotation, step scale and per-token int4 quantization of an activation.
 
     x: [M, K] activation already in the U (SVD) basis, any float dtype (fp16
     inputs are converted exactly).  Steps: y = x . blockdiag(H_b)/sqrt(b)
     (eq:transform, eq:blockdiag); z = s_t * y; per-token quantizer (eq:scale,
-    eq:quant).  Returns (q [M,K] int64, x_scale [M] = Delta/s_t, ratio [M,K]).
+    eq:quant) with q_max = qmax (7 for int4, 127 for the 8-bit activations of
+    W4A8).  Returns (q [M,K] int64, x_scale [M] = Delta/s_t, ratio [M,K]).
     """
     y = fwht(np.asarray(x, dtype=np.float64), b)
     s = float(s_t)
     z = s * y
-    q, delta, ratio = quantize_sym(z)
+    q, delta, ratio = quantize_sym(z, qmax)
     return q, delta / s, ratio
 
 

@@ -113,25 +113,30 @@ def check_fwht_blockwise(fwht, seed=3):
 # Quantizer
 # --------------------------------------------------------------------------
 
-def check_quantizer(quantize_sym, seed=4):
+def check_quantizer(quantize_sym, seed=4, qmax=7):
+    """quantize_sym(z) at bit width log2(qmax + 1) + 1 (qmax 7 or 127)."""
     rng = np.random.default_rng(seed)
     z = rng.standard_normal((64, 256)) * rng.uniform(0.01, 100, size=(64, 1))
     q, d, _ = quantize_sym(z)
     # Error bound |z - Delta q| <= Delta/2 (absmax scaling never clips).
     err = np.abs(z - d[:, None] * q)
     assert np.all(err <= d[:, None] / 2 * (1 + 1e-12))
-    # The absmax element maps to +-7, and -8 never appears.
+    # The absmax element maps to +-q_max, and -(q_max + 1) never appears.
     idx = np.argmax(np.abs(z), axis=1)
-    assert np.array_equal(np.abs(q[np.arange(64), idx]), np.full(64, 7))
-    assert q.min() >= -7 and q.max() <= 7
-    assert np.allclose(d, np.max(np.abs(z), axis=1) / 7, rtol=1e-15, atol=0)
+    assert np.array_equal(np.abs(q[np.arange(64), idx]), np.full(64, qmax))
+    assert q.min() >= -qmax and q.max() <= qmax
+    assert np.allclose(d, np.max(np.abs(z), axis=1) / qmax, rtol=1e-15, atol=0)
     # Zero row -> zero codes and zero scale.
     q0, d0, _ = quantize_sym(np.zeros((2, 16)))
     assert np.all(q0 == 0) and np.all(d0 == 0)
-    # All-equal-magnitude row -> every code +-7.
+    # All-equal-magnitude row -> every code +-q_max.
     s = np.sign(rng.standard_normal((1, 32))) * 2.5
     qs, _, _ = quantize_sym(s)
-    assert np.array_equal(qs, (7 * np.sign(s)).astype(np.int64))
+    assert np.array_equal(qs, (qmax * np.sign(s)).astype(np.int64))
+    # Every code value is reachable: a ramp over [-max, max] hits all 2 q_max + 1 codes.
+    ramp = np.linspace(-1.0, 1.0, 8 * qmax + 1)[None, :]
+    qr, _, _ = quantize_sym(ramp)
+    assert np.array_equal(np.unique(qr), np.arange(-qmax, qmax + 1))
 
 
 def check_worked_example_activation(rotate_quantize_act):
@@ -404,3 +409,42 @@ def check_fold_step(fold_weights_step, fwht, seed=52):
     # sum_j |q_j| ws / 2
     bound = np.abs(q).sum(axis=1)[:, None] * np.asarray(ws)[None, :] / 2
     assert np.all(np.abs(out - ref) <= bound * (1 + 1e-12))
+
+
+# --------------------------------------------------------------------------
+# W4A8 (8-bit per-token activations against int4 weights)
+# --------------------------------------------------------------------------
+
+def check_w4a8_worked_example(w4a8_linear):
+    g = load_golden_rows("w4a8_example.txt")
+    x = g["x"][None, :]
+    b = int(g["b"][0])
+    w = np.stack([g["w0"], g["w1"]])
+    r = w4a8_linear(x, w, b)
+    assert np.array_equal(r["q"][0], g["q"].astype(np.int64))
+    assert abs(r["x_scale"][0] - g["x_scale"][0]) <= 1e-17
+    assert np.array_equal(r["qw"], np.stack([g["qw0"], g["qw1"]]).astype(np.int64))
+    assert np.allclose(r["w_scale"], g["ws"], rtol=1e-15, atol=0)
+    assert np.array_equal(r["acc"][0], g["acc"].astype(np.int64))
+    assert np.allclose(r["y"][0], g["out"], rtol=1e-14, atol=0)
+    # s_t invariance carries over to the 8-bit quantizer
+    r2 = w4a8_linear(x, w, b, s_t=2.0)
+    assert np.array_equal(r2["q"], r["q"]) and abs(r2["x_scale"][0] - r["x_scale"][0]) <= 1e-17
+
+
+def check_w4a8_error_bound(w4a8_linear, fwht, seed=60):
+    """|y - x W'^T| is bounded by the two rounding errors: per element
+    |y_k - Delta_x q_k| <= Delta_x / 2 and |w'_nk - Delta_w qw_nk| <= Delta_w / 2,
+    so |err_in| <= sum_k (Delta_x/2 |w'_nk| + |x'_k| Delta_w/2 + Delta_x Delta_w / 4).
+    An 8-bit activation must also beat the 4-bit one on the same inputs."""
+    rng = np.random.default_rng(seed)
+    M, N, K, b = 8, 16, 256, 64
+    x = rng.standard_normal((M, K))
+    w = rng.standard_normal((N, K)) * 0.1
+    r = w4a8_linear(x, w, b)
+    xp, wp = fwht(x, b), fwht(w, b)
+    exact = xp @ wp.T
+    dx, dw = r["x_scale"][:, None], r["w_scale"][None, :]
+    bound = (dx / 2) * np.abs(wp).sum(1)[None, :] + (dw / 2) * np.abs(xp).sum(1)[:, None] + K * dx * dw / 4
+    assert np.all(np.abs(r["y"] - exact) <= bound * (1 + 1e-12))
+    assert np.abs(r["q"]).max() == 127
