@@ -289,6 +289,35 @@ int oq_quantize_weights_host(const double* W_u, int64_t N, int64_t K, int32_t ha
                              uint8_t* Wq, float* w_scale);
 
 /* ------------------------------------------------------------------------ */
+/* W4A8: 8-bit per-token activations against the int4 weights (the paper's   */
+/* deployment mode, Appendix: W4A8 real-quantization latency)                */
+/* ------------------------------------------------------------------------ */
+/*
+ * oq_rotate_quantize_act_i8 -- oq_rotate_quantize_act with the symmetric
+ * quantizer at 8 bits (eq:scale, eq:quant with k = 8): Delta_i = max|z_i| /
+ * 127, codes in [-127, 127] (-128 never occurs), one signed byte per code.
+ * Xq8 device int8 [M][K] row-major, 16-byte aligned; x_scale as before.
+ * Arguments, limits and errors as oq_rotate_quantize_act.
+ */
+int oq_rotate_quantize_act_i8(const void* X, int64_t M, int64_t K, int64_t ldx,
+                              int32_t had_block, const float* s_table, int32_t t,
+                              int8_t* Xq8, float* x_scale, void* stream);
+
+/*
+ * oq_w4a8_linear / oq_w4a8_gemm_i32 -- oq_w4a4_linear / oq_w4a4_gemm_i32 with
+ * the token operand in 8-bit codes (Xq8 [M][K], as written by
+ * oq_rotate_quantize_act_i8) and the weight unchanged (packed int4 [N][K/2]):
+ * acc[i][n] = sum_k q8[i][k] * wq[n][k] exactly in int32 (|acc| <= 889 K),
+ * then the same epilogue.  Shapes, alignment and errors as the W4A4 calls.
+ */
+int oq_w4a8_linear(const int8_t* Xq8, const float* x_scale, int64_t M,
+                   const uint8_t* Wq, const float* w_scale, const void* bias,
+                   int64_t N, int64_t K, void* Y, int64_t ldy, int32_t out_dtype,
+                   void* stream);
+int oq_w4a8_gemm_i32(const int8_t* Xq8, int64_t M, const uint8_t* Wq, int64_t N, int64_t K,
+                     int32_t* acc, int64_t ldc, void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Static per-step, per-channel activation steps (Section 4.2,               */
 /* eq:perstep_scale with the per-(layer, step, channel) table)               */
 /* ------------------------------------------------------------------------ */

@@ -234,6 +234,42 @@ def quantize_weights_host(W_u: np.ndarray, had_block: int):
     return Wq, ws
 
 
+def rotate_quantize_act_i8(X, had_block, s_table=None, t=0, Xq8=None, x_scale=None, stream=None):
+    """W4A8 activation side: 8-bit per-token codes (int8 [M, K]) and x_scale f32 [M]."""
+    M, K = X.shape
+    if Xq8 is None:
+        Xq8 = torch.empty((M, K), dtype=torch.int8, device=X.device)
+    if x_scale is None:
+        x_scale = torch.empty((M,), dtype=torch.float32, device=X.device)
+    keep, sp = _s_table(s_table)
+    _check(lib().oq_rotate_quantize_act_i8(_ptr(X), M, K, X.stride(0), had_block, sp, t, _ptr(Xq8),
+                                           _ptr(x_scale), _stream(stream)), "oq_rotate_quantize_act_i8")
+    del keep
+    return Xq8, x_scale
+
+
+def w4a8_linear(Xq8, x_scale, Wq, w_scale, bias=None, out_dtype=OUT_F16, Y=None, stream=None):
+    """Y [M, N] = dequant(Xq8 . Wq^T) with 8-bit token codes and int4 weights."""
+    M, K = Xq8.shape
+    N = Wq.shape[0]
+    if Y is None:
+        dt = torch.float16 if out_dtype == OUT_F16 else torch.bfloat16
+        Y = torch.empty((M, N), dtype=dt, device=Xq8.device)
+    _check(lib().oq_w4a8_linear(_ptr(Xq8), _ptr(x_scale), M, _ptr(Wq), _ptr(w_scale), _ptr(bias), N, K,
+                                _ptr(Y), Y.stride(0), out_dtype, _stream(stream)), "oq_w4a8_linear")
+    return Y
+
+
+def w4a8_gemm_i32(Xq8, Wq, acc=None, stream=None):
+    M, K = Xq8.shape
+    N = Wq.shape[0]
+    if acc is None:
+        acc = torch.empty((M, N), dtype=torch.int32, device=Xq8.device)
+    _check(lib().oq_w4a8_gemm_i32(_ptr(Xq8), M, _ptr(Wq), N, K, _ptr(acc), acc.stride(0), _stream(stream)),
+           "oq_w4a8_gemm_i32")
+    return acc
+
+
 def rotate_act_f32(X, had_block, Y=None, stream=None):
     """Rotated activation y = x H_b / sqrt(b) in fp32 [M, K] (calibration input)."""
     M, K = X.shape

@@ -55,6 +55,9 @@ SIGNATURES = {
     "oq_quantize_weights": (i32, [vp, i64, i64, i64, i32, vp, vp, vp]),
     "oq_quantize_weights_host": (i32, [vp, i64, i64, i32, vp, vp]),
     "oq_rotate_act_f32": (i32, [vp, i64, i64, i64, i32, vp, vp]),
+    "oq_rotate_quantize_act_i8": (i32, [vp, i64, i64, i64, i32, fp, i32, vp, vp, vp]),
+    "oq_w4a8_linear": (i32, [vp, vp, i64, vp, vp, vp, i64, i64, vp, i64, i32, vp]),
+    "oq_w4a8_gemm_i32": (i32, [vp, i64, vp, i64, i64, vp, i64, vp]),
     "oq_calibrate_workspace_bytes": (C.c_size_t, [i64]),
     "oq_calibrate_step_scales": (i32, [vp, i64, i64, i64, C.c_double, C.c_float, vp, vp, C.c_size_t, vp]),
     "oq_rotate_quantize_act_static": (i32, [vp, i64, i64, i64, i32, vp, vp, vp, vp]),

@@ -49,10 +49,11 @@ bool rq_plan(int64_t K, RQPlan* p);
 // Validated launch (no argument checks); ratio != nullptr selects the debug output.
 // tiled: Xq is in the 16-row tiled layout (K % 128 == 0) instead of [M][K/2].
 // sdelta: static per-channel steps [K] (token scale 1) instead of the
-// per-token maximum; rotate_only: write s_t * y in fp32 to `ratio` only.
+// per-token maximum; rotate_only: write s_t * y in fp32 to `ratio` only;
+// i8: 8-bit codes (q_max = 127), one byte per code, Xq [M][K].
 int rq_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block, float s_t,
               uint8_t* Xq, float* x_scale, float* ratio, hipStream_t stream, bool tiled = false,
-              const float* sdelta = nullptr, bool rotate_only = false);
+              const float* sdelta = nullptr, bool rotate_only = false, bool i8 = false);
 
 // Shape/alignment validation shared by every rotate-quantize entry point.
 int rq_validate(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block,
@@ -71,6 +72,7 @@ struct GemmArgs {
   const uint16_t* gate;  // EPI_RESID_F32: fp16 [N] per-channel multiplier (null = 1)
   int64_t M, N, K, ldc;
   bool a_tiled;          // A is in the 16-row tiled layout (K % 128 == 0)
+  bool a_i8;             // A holds 8-bit codes, one byte each, [M][K] (W4A8)
 };
 
 int gemm_validate(const uint8_t* Xq, int64_t M, const uint8_t* Wq, int64_t N, int64_t K,

@@ -190,6 +190,16 @@ __device__ __forceinline__ uint32_t static_code(float u, float delta, float inv_
   return __float_as_uint(r + kRoundMagic);
 }
 
+// Eight 8-bit codes, given as the bit patterns of (ratio + 1.5*2^23), as two
+// dwords: channel j in byte j (two's complement, |code| <= 127).
+__device__ __forceinline__ uint2 pack8_i8(const uint32_t (&b)[8]) {
+  const uint32_t lo = __builtin_amdgcn_perm(__builtin_amdgcn_perm(b[3], b[2], 0x0c0c0400u),
+                                            __builtin_amdgcn_perm(b[1], b[0], 0x0c0c0400u), 0x05040100u);
+  const uint32_t hi = __builtin_amdgcn_perm(__builtin_amdgcn_perm(b[7], b[6], 0x0c0c0400u),
+                                            __builtin_amdgcn_perm(b[5], b[4], 0x0c0c0400u), 0x05040100u);
+  return make_uint2(lo, hi);
+}
+
 // The rest of the fused pass once the row's fp32 values are in registers:
 // butterflies, row maximum, scales, codes.  `lds` must hold rows_per_wg * K
 // floats when logT > 6; `red` is a 4-float shared array.  Every thread of the
@@ -197,12 +207,15 @@ __device__ __forceinline__ uint32_t static_code(float u, float delta, float inv_
 // tiled selects the 16-row tiled code layout for Xq (K % 128 == 0).
 // sdelta != nullptr selects the static per-channel quantizer (step
 // sdelta[k] of channel k, token scale 1, see static_code); rotate_only
-// writes the normalized rotation s_t * y in fp32 to `ratio` and nothing else.
+// writes the normalized rotation s_t * y in fp32 to `ratio` and nothing else;
+// i8 quantizes to 8 bits (q_max = 127) and writes one byte per code, Xq
+// [M][K] row-major.
 template <int C>
 __device__ __forceinline__ void rq_core(float (&v)[C][8], const RowMap& m, int K, int logb, float s_t,
                                         float s_over_sqrtb, float* lds, float* red, uint8_t* __restrict__ Xq,
                                         float* __restrict__ xs, float* __restrict__ ratio, bool tiled = false,
-                                        const float* __restrict__ sdelta = nullptr, bool rotate_only = false) {
+                                        const float* __restrict__ sdelta = nullptr, bool rotate_only = false,
+                                        bool i8 = false) {
   // Bits 0..2: inside each 8-channel chunk.
 #pragma unroll
   for (int q = 0; q < 3; ++q) {
@@ -330,12 +343,12 @@ __device__ __forceinline__ void rq_core(float (&v)[C][8], const RowMap& m, int K
     for (int j = 0; j < 8; ++j) amax = fmaxf(amax, fabsf(v[c][j]));
   amax = row_reduce<true>(amax, m, red);
 
-  // Scalars: a_z = max|s_t y|, Delta = a_z / 7, x_scale = Delta / s_t, and the
-  // multiplier g = (s_t / sqrt(b)) / Delta taking the unnormalized butterfly
-  // output u to z / Delta.  |u g| <= 7 up to rounding, so round-half-even of
-  // u g never leaves [-7, 7] and needs no clamp.
+  // Scalars: a_z = max|s_t y|, Delta = a_z / q_max, x_scale = Delta / s_t,
+  // and the multiplier g = (s_t / sqrt(b)) / Delta taking the unnormalized
+  // butterfly output u to z / Delta.  |u g| <= q_max up to rounding, so
+  // round-half-even of u g never leaves [-q_max, q_max] and needs no clamp.
   const float a_z = amax * s_over_sqrtb;
-  const float delta = a_z / 7.0f;
+  const float delta = a_z / (i8 ? 127.0f : 7.0f);
   const float g = delta > 0.0f ? s_over_sqrtb / delta : 0.0f;
   if (m.valid && m.t == 0) xs[m.row] = delta / s_t;
   if (!m.valid) return;
@@ -351,6 +364,17 @@ __device__ __forceinline__ void rq_core(float (&v)[C][8], const RowMap& m, int K
     return;
   }
 
+  if (i8) {
+    uint8_t* qr8 = Xq + m.row * static_cast<int64_t>(K);
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      uint32_t b[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) b[j] = __float_as_uint(fmaf(v[c][j], g, kRoundMagic));
+      *reinterpret_cast<uint2*>(qr8 + chan(m, c, 0)) = pack8_i8(b);
+    }
+    return;
+  }
   uint8_t* qr = Xq + m.row * static_cast<int64_t>(K / 2);
 #pragma unroll
   for (int c = 0; c < C; ++c) {

@@ -71,13 +71,15 @@ __device__ __forceinline__ int chan0(int wr, int g, int lane) {
 // chan0(wr, g, lane) .. + 7.  Every wave of the workgroup calls it: it
 // synchronizes when W > 1 (xch: [4][NG][2][64] float4 of LDS), and `red` is
 // a 4-float shared array.  sdelta / rotate_only: the static per-channel
-// quantizer and the fp32 rotation output, as in rqd::rq_core.
+// quantizer and the fp32 rotation output, as in rqd::rq_core; i8: 8-bit codes
+// (q_max = 127), one byte per code in [M][K].
 template <int NG, int W, bool FULL>
 __device__ __forceinline__ void rq_row(const rv8h (&cur)[NG], const rv8h& a1, const rv8h& a2, int64_t row, bool valid,
                                        int lane, int wv, int logb, float s_t, float s_over_sqrtb,
                                        uint8_t* __restrict__ Xq, float* __restrict__ xs, float* __restrict__ ratio,
                                        float4* xch, float* red, bool tiled,
-                                       const float* __restrict__ sdelta = nullptr, bool rotate_only = false) {
+                                       const float* __restrict__ sdelta = nullptr, bool rotate_only = false,
+                                       bool i8 = false) {
   using S = Shape<NG, W>;
   constexpr int K = S::K, LOGNG = S::LOGNG, LOGW = S::LOGW, GW = S::GW;
   const int rsub = wv / W, wr = wv % W;
@@ -216,7 +218,7 @@ __device__ __forceinline__ void rq_row(const rv8h (&cur)[NG], const rv8h& a1, co
   }
 
   const float a_z = amax * s_over_sqrtb;
-  const float delta = a_z / 7.0f;
+  const float delta = a_z / (i8 ? 127.0f : 7.0f);
   const float gm = delta > 0.0f ? s_over_sqrtb / delta : 0.0f;
   if (!valid) return;
   if (wr == 0 && lane == 0) xs[row] = delta / s_t;
@@ -226,6 +228,16 @@ __device__ __forceinline__ void rq_row(const rv8h (&cur)[NG], const rv8h& a1, co
       float* rr = ratio + row * K + (group_of(s) * 16 + cl) * 32 + 8 * q;
       reinterpret_cast<float4*>(rr)[0] = make_float4(v[s][0] * gm, v[s][1] * gm, v[s][2] * gm, v[s][3] * gm);
       reinterpret_cast<float4*>(rr)[1] = make_float4(v[s][4] * gm, v[s][5] * gm, v[s][6] * gm, v[s][7] * gm);
+    }
+    return;
+  }
+  if (i8) {
+#pragma unroll
+    for (int s = 0; s < NG; ++s) {
+      uint32_t b[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) b[e] = __float_as_uint(fmaf(v[s][e], gm, rqd::kRoundMagic));
+      *reinterpret_cast<uint2*>(Xq + row * K + (group_of(s) * 16 + cl) * 32 + 8 * q) = rqd::pack8_i8(b);
     }
     return;
   }

@@ -73,6 +73,19 @@ __device__ __forceinline__ v4i widen16_u2(uint2 p) {
   return r;
 }
 
+// 16 bytes of 8-bit codes (natural channel order) in the order that
+// widen16_u2 gives packed codes: within each group of 8 channels the even
+// channels first, [0 2 4 6 1 3 5 7], so that a W4A8 A operand meets the
+// widened weight fragment channel for channel.
+__device__ __forceinline__ v4i order16_i8(uint4 p) {
+  v4i r;
+  r[0] = static_cast<int>(__builtin_amdgcn_perm(p.y, p.x, 0x06040200u));
+  r[1] = static_cast<int>(__builtin_amdgcn_perm(p.y, p.x, 0x07050301u));
+  r[2] = static_cast<int>(__builtin_amdgcn_perm(p.w, p.z, 0x06040200u));
+  r[3] = static_cast<int>(__builtin_amdgcn_perm(p.w, p.z, 0x07050301u));
+  return r;
+}
+
 // Map a linear workgroup id to an output tile (tm, tn): the grid is cut into
 // 8 contiguous chunks, one per XCD (hardware dispatches id i to XCD i % 8),
 // and each chunk is walked in groups of GM tile rows.
@@ -92,7 +105,10 @@ __device__ __forceinline__ void big_tile(int id, int tiles_m, int tiles_n, int* 
   *tn = in / gsize;
 }
 
-template <int EPI, int WM, int WN, int TM, int TN>
+// A8: the token operand holds 8-bit codes (W4A8), one byte each, loaded 64
+// bytes per thread and row per stage and reordered (not widened) into LDS;
+// the products are then 16 * q * wq and the accumulator is shifted by 4.
+template <int EPI, int WM, int WN, int TM, int TN, bool A8>
 __global__ __launch_bounds__(64 * WM * WN, 512 / (64 * WM * WN)) void gemm_big_kernel(GemmArgs a) {
   // WM x WN waves, each a (32 TM) x (32 TN) tile of v_mfma_i32_32x32x32_i8 blocks.
   constexpr int NT = 64 * WM * WN;          // threads
@@ -116,6 +132,8 @@ __global__ __launch_bounds__(64 * WM * WN, 512 / (64 * WM * WN)) void gemm_big_k
   const int64_t m0 = static_cast<int64_t>(tm) * BM;
   const int64_t n0 = static_cast<int64_t>(tn) * BN;
   const int64_t Kb = a.K / 2;
+  constexpr int AW = A8 ? 2 : 1;  // A bytes per packed B byte
+  const int64_t Ka = Kb * AW;
   const int nk = static_cast<int>((a.K + BIG_KSTAGE - 1) / BIG_KSTAGE);  // stages (the last may be half)
   const int nk64 = static_cast<int>(a.K / 64);                            // 64-code halves in total
 
@@ -126,19 +144,18 @@ __global__ __launch_bounds__(64 * WM * WN, 512 / (64 * WM * WN)) void gemm_big_k
   const uint8_t* gA[PA];
   const uint8_t* gB[PB];
 #pragma unroll
-  for (int r = 0; r < PA; ++r) gA[r] = a.A + min<int64_t>(m0 + lr + r * (NT / 2), a.M - 1) * Kb + lh * 32;
+  for (int r = 0; r < PA; ++r) gA[r] = a.A + min<int64_t>(m0 + lr + r * (NT / 2), a.M - 1) * Ka + lh * 32 * AW;
 #pragma unroll
   for (int r = 0; r < PB; ++r) gB[r] = a.B + min<int64_t>(n0 + lr + r * (NT / 2), a.N - 1) * Kb + lh * 32;
   // Three register stages, indexed only by constants (they stay in VGPRs).
-  uint4 ra[3][2 * PA], rb[3][2 * PB];
-#define OQ_GLOAD(KS, S)                                                          \
-  {                                                                              \
-    const int h_ = min(2 * (KS) + lh, nk64 - 1);                                 \
-    const int64_t off_ = static_cast<int64_t>(h_) * 32 - lh * 32;                \
-    _Pragma("unroll") for (int r_ = 0; r_ < PA; ++r_) {                          \
-      ra[S][2 * r_] = *reinterpret_cast<const uint4*>(gA[r_] + off_);            \
-      ra[S][2 * r_ + 1] = *reinterpret_cast<const uint4*>(gA[r_] + off_ + 16);   \
-    }                                                                            \
+  uint4 ra[3][2 * AW * PA], rb[3][2 * PB];
+#define OQ_GLOAD(KS, S)                                                                \
+  {                                                                                    \
+    const int h_ = min(2 * (KS) + lh, nk64 - 1);                                       \
+    const int64_t off_ = static_cast<int64_t>(h_) * 32 - lh * 32;                      \
+    _Pragma("unroll") for (int r_ = 0; r_ < PA; ++r_)                                  \
+    _Pragma("unroll") for (int c_ = 0; c_ < 2 * AW; ++c_)                              \
+      ra[S][2 * AW * r_ + c_] = *reinterpret_cast<const uint4*>(gA[r_] + AW * off_ + 16 * c_); \
     _Pragma("unroll") for (int r_ = 0; r_ < PB; ++r_) {                          \
       rb[S][2 * r_] = *reinterpret_cast<const uint4*>(gB[r_] + off_);            \
       rb[S][2 * r_ + 1] = *reinterpret_cast<const uint4*>(gB[r_] + off_ + 16);   \
@@ -156,8 +173,14 @@ __global__ __launch_bounds__(64 * WM * WN, 512 / (64 * WM * WN)) void gemm_big_k
 #define OQ_LSTORE(BUF, S)                                                                          \
   {                                                                                                \
     _Pragma("unroll") for (int r_ = 0; r_ < PA; ++r_) {                                            \
-      OQ_ST32(&sA[(BUF)][(lr + r_ * (NT / 2)) * BIG8_STRIDE + lh * 64], ra[S][2 * r_])             \
-      OQ_ST32(&sA[(BUF)][(lr + r_ * (NT / 2)) * BIG8_STRIDE + lh * 64 + 32], ra[S][2 * r_ + 1])    \
+      if constexpr (A8) {                                                                          \
+        _Pragma("unroll") for (int c_ = 0; c_ < 4; ++c_)                                           \
+          *reinterpret_cast<v4i*>(&sA[(BUF)][(lr + r_ * (NT / 2)) * BIG8_STRIDE + lh * 64 + 16 * c_]) = \
+              order16_i8(ra[S][4 * r_ + c_]);                                                      \
+      } else {                                                                                     \
+        OQ_ST32(&sA[(BUF)][(lr + r_ * (NT / 2)) * BIG8_STRIDE + lh * 64], ra[S][2 * r_])           \
+        OQ_ST32(&sA[(BUF)][(lr + r_ * (NT / 2)) * BIG8_STRIDE + lh * 64 + 32], ra[S][2 * r_ + 1])  \
+      }                                                                                            \
     }                                                                                              \
     _Pragma("unroll") for (int r_ = 0; r_ < PB; ++r_) {                                            \
       OQ_ST32(&sB[(BUF)][(lr + r_ * (NT / 2)) * BIG8_STRIDE + lh * 64], rb[S][2 * r_])             \
@@ -307,7 +330,7 @@ __global__ __launch_bounds__(64 * WM * WN, 512 / (64 * WM * WN)) void gemm_big_k
           // Rows / columns past the edge are staged but not written back.
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
-            const float y = static_cast<float>(acc[i][j][4 * q + u] >> 8) * xr[q][u] * wsc[j] + bias[j];
+            const float y = static_cast<float>(acc[i][j][4 * q + u] >> (A8 ? 4 : 8)) * xr[q][u] * wsc[j] + bias[j];
             tile[(lr0 + u) * TP + wn * 32 * TN + j * 32 + col_in] =
                 EPI == EPI_F16 ? __builtin_bit_cast(uint16_t, static_cast<_Float16>(y)) : f32_to_bf16_rne(y);
           }
@@ -318,7 +341,7 @@ __global__ __launch_bounds__(64 * WM * WN, 512 / (64 * WM * WN)) void gemm_big_k
         for (int u = 0; u < 4; ++u) {
           const int64_t gr = r0 + u;
           if (gr >= a.M) continue;
-          const int v = acc[i][j][4 * q + u] >> 8;
+          const int v = acc[i][j][4 * q + u] >> (A8 ? 4 : 8);
           const int64_t off = gr * a.ldc + gc;
           if (EPI == EPI_I32) {
             static_cast<int32_t*>(a.C)[off] = v;
@@ -390,8 +413,11 @@ __device__ __forceinline__ void store_out(const GemmArgs& a, int64_t off, int v,
   }
 }
 
-template <int EPI, int NB, int WAVES, int MB, int UB, bool TILED>
+// A8 (row layout only): 8-bit token codes, 32 bytes per lane and unit,
+// reordered in registers; the accumulator is shifted by 4.
+template <int EPI, int NB, int WAVES, int MB, int UB, bool TILED, bool A8 = false>
 __global__ __launch_bounds__(64 * WAVES) void gemm_small_kernel(GemmArgs a) {
+  static_assert(!(A8 && TILED), "8-bit token codes use the row layout");
   constexpr int BNs = 16 * NB, ROWS = 16 * MB, NOUT = ROWS * BNs, NT = 64 * WAVES;
   constexpr int OPT = (NOUT + NT - 1) / NT;  // outputs per thread
   static_assert(NT % BNs == 0, "a thread keeps one output column");
@@ -423,7 +449,7 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_small_kernel(GemmArgs a) {
     } else {
       const int64_t r = m0 + rb * 16 + (lane & 15);
       aok[rb] = r < a.M;
-      abase[rb] = a.A + (aok[rb] ? r : 0) * Kb;
+      abase[rb] = a.A + (aok[rb] ? r : 0) * Kb * (A8 ? 2 : 1);
     }
   }
   const uint8_t* bbase[NB];
@@ -433,7 +459,8 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_small_kernel(GemmArgs a) {
 
   // Fragments of UB units starting at u0 (a unit past uend reads unit uend - 1
   // or 0 again; its MFMAs are skipped).
-  uint4 fa[UB][MB], fb[UB][NB];
+  constexpr int AH = A8 ? 2 : 1;  // 16-byte A loads per unit and row block
+  uint4 fa[UB][MB][AH], fb[UB][NB];
   auto load_units = [&](int u0) {
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
@@ -442,8 +469,11 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_small_kernel(GemmArgs a) {
       for (int nb = 0; nb < NB; ++nb) fb[u][nb] = *reinterpret_cast<const uint4*>(bbase[nb] + uu * 64 + piece);
 #pragma unroll
       for (int rb = 0; rb < MB; ++rb)
-        fa[u][rb] = *reinterpret_cast<const uint4*>(TILED ? abase[rb] + static_cast<int64_t>(uu) * 1024
-                                                           : abase[rb] + uu * 64 + piece);
+#pragma unroll
+        for (int c = 0; c < AH; ++c)
+          fa[u][rb][c] = *reinterpret_cast<const uint4*>(
+              TILED ? abase[rb] + static_cast<int64_t>(uu) * 1024
+                    : abase[rb] + uu * 64 * AH + piece * AH + 16 * c);
     }
   };
   // The first units' loads go out before anything else.
@@ -492,8 +522,13 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_small_kernel(GemmArgs a) {
             wb[nb] = widen16_u2(h ? make_uint2(fb[u][nb].z, fb[u][nb].w) : make_uint2(fb[u][nb].x, fb[u][nb].y));
 #pragma unroll
           for (int rb = 0; rb < MB; ++rb) {
-            const uint2 pa = h ? make_uint2(fa[u][rb].z, fa[u][rb].w) : make_uint2(fa[u][rb].x, fa[u][rb].y);
-            const v4i xa = widen16_u2(aok[rb] ? pa : make_uint2(0, 0));
+            v4i xa;
+            if constexpr (A8) {
+              xa = order16_i8(aok[rb] ? fa[u][rb][h] : make_uint4(0, 0, 0, 0));
+            } else {
+              const uint2 pa = h ? make_uint2(fa[u][rb][0].z, fa[u][rb][0].w) : make_uint2(fa[u][rb][0].x, fa[u][rb][0].y);
+              xa = widen16_u2(aok[rb] ? pa : make_uint2(0, 0));
+            }
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
               acc[rb][nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(xa, wb[nb], acc[rb][nb], 0, 0, 0);
@@ -517,7 +552,11 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_small_kernel(GemmArgs a) {
     for (int nb = 0; nb < NB; ++nb) wb[nb] = widen16_u2(*reinterpret_cast<const uint2*>(bbase[nb] + off));
 #pragma unroll
     for (int rb = 0; rb < MB; ++rb) {
-      const v4i xa = widen16_u2(aok[rb] ? *reinterpret_cast<const uint2*>(abase[rb] + off) : make_uint2(0, 0));
+      v4i xa;
+      if constexpr (A8)
+        xa = order16_i8(aok[rb] ? *reinterpret_cast<const uint4*>(abase[rb] + 2 * off) : make_uint4(0, 0, 0, 0));
+      else
+        xa = widen16_u2(aok[rb] ? *reinterpret_cast<const uint2*>(abase[rb] + off) : make_uint2(0, 0));
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
         acc[rb][nb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(xa, wb[nb], acc[rb][nb], 0, 0, 0);
@@ -541,7 +580,7 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_small_kernel(GemmArgs a) {
     int sum = 0;
 #pragma unroll
     for (int w = 0; w < WAVES; ++w) sum += red[w][i];
-    store_out<EPI>(a, gr * a.ldc + egc, sum >> 8, e_xs[u], e_ws, e_bias, e_gate, e_res[u]);
+    store_out<EPI>(a, gr * a.ldc + egc, sum >> (A8 ? 4 : 8), e_xs[u], e_ws, e_bias, e_gate, e_res[u]);
   }
 }
 
@@ -550,16 +589,19 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_small_kernel(GemmArgs a) {
 // each takes one or two 128-code units of K at K <= 1024 and up to 2 (16
 // columns) or 4 (32 columns) at K <= 4096 in its first round; deeper K runs
 // more rounds.
-template <int EPI, bool TILED, int MB>
+template <int EPI, bool TILED, int MB, bool A8 = false>
 int launch_small_mb(const GemmArgs& a, hipStream_t stream) {
   const bool wide = a.N > 4096;
   const bool shallow = a.K <= 1024;
   const int bn = wide ? 32 : 16;
+  // 8-bit token codes take twice the registers per unit: half the units per
+  // round in the deep cases (1024 threads leave 128 registers per lane).
+  constexpr int UBW = A8 ? 2 : 4;
   const dim3 grid(static_cast<unsigned>((a.N + bn - 1) / bn), static_cast<unsigned>((a.M + 16 * MB - 1) / (16 * MB)));
-  if (wide && shallow) hipLaunchKernelGGL((gemm_small_kernel<EPI, 2, 8, MB, 1, TILED>), grid, dim3(512), 0, stream, a);
-  else if (wide) hipLaunchKernelGGL((gemm_small_kernel<EPI, 2, 8, MB, 4, TILED>), grid, dim3(512), 0, stream, a);
-  else if (shallow) hipLaunchKernelGGL((gemm_small_kernel<EPI, 1, 4, MB, 2, TILED>), grid, dim3(256), 0, stream, a);
-  else hipLaunchKernelGGL((gemm_small_kernel<EPI, 1, 16, MB, 2, TILED>), grid, dim3(1024), 0, stream, a);
+  if (wide && shallow) hipLaunchKernelGGL((gemm_small_kernel<EPI, 2, 8, MB, 1, TILED, A8>), grid, dim3(512), 0, stream, a);
+  else if (wide) hipLaunchKernelGGL((gemm_small_kernel<EPI, 2, 8, MB, UBW, TILED, A8>), grid, dim3(512), 0, stream, a);
+  else if (shallow) hipLaunchKernelGGL((gemm_small_kernel<EPI, 1, 4, MB, 2, TILED, A8>), grid, dim3(256), 0, stream, a);
+  else hipLaunchKernelGGL((gemm_small_kernel<EPI, 1, 16, MB, A8 ? 1 : 2, TILED, A8>), grid, dim3(1024), 0, stream, a);
   return launch_status();
 }
 
@@ -570,6 +612,8 @@ int launch_small(const GemmArgs& a, hipStream_t stream) {
 
 template <int EPI>
 int launch_small_any(const GemmArgs& a, hipStream_t stream) {
+  if (a.a_i8)
+    return a.M <= 16 ? launch_small_mb<EPI, false, 1, true>(a, stream) : launch_small_mb<EPI, false, 4, true>(a, stream);
   return a.a_tiled ? launch_small<EPI, true>(a, stream) : launch_small<EPI, false>(a, stream);
 }
 
@@ -585,23 +629,35 @@ int gemm_validate(const uint8_t* Xq, int64_t M, const uint8_t* Wq, int64_t N, in
   return OQ_OK;
 }
 
-template <int WM, int WN, int TM, int TN>
-int launch_big(const GemmArgs& a, Epilogue epi, int64_t tiles, hipStream_t stream) {
+template <int WM, int WN, int TM, int TN, bool A8>
+int launch_big_a(const GemmArgs& a, Epilogue epi, int64_t tiles, hipStream_t stream) {
   const dim3 g(static_cast<unsigned>(tiles)), b(64 * WM * WN);
   switch (epi) {
-    case EPI_I32: hipLaunchKernelGGL((gemm_big_kernel<EPI_I32, WM, WN, TM, TN>), g, b, 0, stream, a); break;
-    case EPI_F16: hipLaunchKernelGGL((gemm_big_kernel<EPI_F16, WM, WN, TM, TN>), g, b, 0, stream, a); break;
-    case EPI_BF16: hipLaunchKernelGGL((gemm_big_kernel<EPI_BF16, WM, WN, TM, TN>), g, b, 0, stream, a); break;
-    case EPI_RESID_F32: hipLaunchKernelGGL((gemm_big_kernel<EPI_RESID_F32, WM, WN, TM, TN>), g, b, 0, stream, a); break;
+    case EPI_I32: hipLaunchKernelGGL((gemm_big_kernel<EPI_I32, WM, WN, TM, TN, A8>), g, b, 0, stream, a); break;
+    case EPI_F16: hipLaunchKernelGGL((gemm_big_kernel<EPI_F16, WM, WN, TM, TN, A8>), g, b, 0, stream, a); break;
+    case EPI_BF16: hipLaunchKernelGGL((gemm_big_kernel<EPI_BF16, WM, WN, TM, TN, A8>), g, b, 0, stream, a); break;
+    case EPI_RESID_F32:
+      if constexpr (A8) return OQ_ERR_ARG;  // the residual epilogue is a W4A4 DiT path only
+      else hipLaunchKernelGGL((gemm_big_kernel<EPI_RESID_F32, WM, WN, TM, TN, A8>), g, b, 0, stream, a);
+      break;
     default: return OQ_ERR_ARG;
   }
   return launch_status();
+}
+
+template <int WM, int WN, int TM, int TN>
+int launch_big(const GemmArgs& a, Epilogue epi, int64_t tiles, hipStream_t stream) {
+  if constexpr (WM * WN * TM * TN <= 16) {
+    if (a.a_i8) return launch_big_a<WM, WN, TM, TN, true>(a, epi, tiles, stream);
+  }
+  return launch_big_a<WM, WN, TM, TN, false>(a, epi, tiles, stream);
 }
 
 int gemm_launch(const GemmArgs& a, Epilogue epi, hipStream_t stream) {
   if (a.M == 0) return OQ_OK;
   // Tiled token codes always take the small-M kernel (row groups of 64 along
   // grid.y when M > 64); row-layout codes take it up to M = 64.
+  if (a.a_i8 && epi == EPI_RESID_F32) return OQ_ERR_ARG;
   if (a.M <= 64 || a.a_tiled) {
     switch (epi) {
       case EPI_I32: return launch_small_any<EPI_I32>(a, stream);
@@ -614,8 +670,10 @@ int gemm_launch(const GemmArgs& a, Epilogue epi, hipStream_t stream) {
   // Large problems: 256 x 256 tiles (8 waves of 128 x 64) when they still
   // fill every CU, else 128 x 128 tiles (4 waves of 64 x 64, two workgroups
   // per CU).
+  // 8-bit token codes double the A register ring, which the 256 x 256 tile
+  // cannot hold without spilling: they always take the 128 x 128 tile.
   const int64_t big_tiles = ((a.M + 255) / 256) * ((a.N + 255) / 256);
-  if (big_tiles >= 256) return launch_big<2, 4, 4, 2>(a, epi, big_tiles, stream);
+  if (big_tiles >= 256 && !a.a_i8) return launch_big<2, 4, 4, 2>(a, epi, big_tiles, stream);
   const int64_t mid_tiles = ((a.M + 127) / 128) * ((a.N + 127) / 128);
   return launch_big<2, 2, 2, 2>(a, epi, mid_tiles, stream);
 }
@@ -667,5 +725,29 @@ extern "C" int oq_w4a4_gemm_i32_tiled(const uint8_t* Xt, int64_t M, const uint8_
   if (M == 0) return OQ_OK;
   if ((st = oq::device_check()) != OQ_OK) return st;
   oq::GemmArgs a{Xt, Wq, nullptr, nullptr, nullptr, acc, nullptr, M, N, K, ldc, true};
+  return oq::gemm_launch(a, oq::EPI_I32, static_cast<hipStream_t>(stream));
+}
+
+extern "C" int oq_w4a8_linear(const int8_t* Xq8, const float* x_scale, int64_t M, const uint8_t* Wq,
+                              const float* w_scale, const void* bias, int64_t N, int64_t K, void* Y,
+                              int64_t ldy, int32_t out_dtype, void* stream) {
+  const uint8_t* A = reinterpret_cast<const uint8_t*>(Xq8);
+  int st = oq::gemm_validate(A, M, Wq, N, K, Y, ldy, 8);
+  if (st != OQ_OK || M == 0) return st;
+  if (!x_scale || !w_scale) return OQ_ERR_NULL;
+  if (out_dtype != OQ_OUT_F16 && out_dtype != OQ_OUT_BF16) return OQ_ERR_ARG;
+  if (!oq::aligned(x_scale, 4) || !oq::aligned(w_scale, 4) || (bias && !oq::aligned(bias, 2))) return OQ_ERR_ALIGN;
+  if ((st = oq::device_check()) != OQ_OK) return st;
+  oq::GemmArgs a{A, Wq, x_scale, w_scale, static_cast<const uint16_t*>(bias), Y, nullptr, M, N, K, ldy, false, true};
+  return oq::gemm_launch(a, out_dtype == OQ_OUT_F16 ? oq::EPI_F16 : oq::EPI_BF16, static_cast<hipStream_t>(stream));
+}
+
+extern "C" int oq_w4a8_gemm_i32(const int8_t* Xq8, int64_t M, const uint8_t* Wq, int64_t N, int64_t K,
+                                int32_t* acc, int64_t ldc, void* stream) {
+  const uint8_t* A = reinterpret_cast<const uint8_t*>(Xq8);
+  int st = oq::gemm_validate(A, M, Wq, N, K, acc, ldc, 4);
+  if (st != OQ_OK || M == 0) return st;
+  if ((st = oq::device_check()) != OQ_OK) return st;
+  oq::GemmArgs a{A, Wq, nullptr, nullptr, nullptr, acc, nullptr, M, N, K, ldc, false, true};
   return oq::gemm_launch(a, oq::EPI_I32, static_cast<hipStream_t>(stream));
 }

@@ -42,8 +42,10 @@ def unpack_int4(packed: np.ndarray) -> np.ndarray:
     return out
 
 
-def tau_rows(x: np.ndarray, b: int) -> np.ndarray:
-    """Per-row bound on |r_gpu - r_exact| for activation rows x [M, K]."""
+def tau_rows(x: np.ndarray, b: int, qmax: int = 7) -> np.ndarray:
+    """Per-row bound on |r_gpu - r_exact| for activation rows x [M, K]; the
+    constants 14 = 2 q_max and 21 = 3 q_max scale with q_max (127 for the
+    8-bit activations of W4A8)."""
     x = np.asarray(x, dtype=np.float64)
     M, K = x.shape
     d = int(np.log2(b)) + 32
@@ -53,7 +55,7 @@ def tau_rows(x: np.ndarray, b: int) -> np.ndarray:
     from oracle.hadamard import fwht  # the oracle's transform, exact to ~1e-15
     umax = np.abs(fwht(x, b)).max(axis=1) * np.sqrt(b)
     safe = np.where(umax > 0, umax, 1.0)
-    return np.where(umax > 0, 14 * gamma * l1 / safe + 21 * U32, 0.0)
+    return np.where(umax > 0, 2 * qmax * gamma * l1 / safe + 3 * qmax * U32, 0.0)
 
 
 def block_l1(x: np.ndarray, b: int) -> np.ndarray:
@@ -93,7 +95,7 @@ def dist_to_boundary(r: np.ndarray) -> np.ndarray:
     return np.abs(np.abs(r - np.floor(r)) - 0.5)
 
 
-def check_codes(q_gpu, q_ref, r_ref, tau_row):
+def check_codes(q_gpu, q_ref, r_ref, tau_row, qmax: int = 7):
     """Returns (n_mismatch, n_boundary_1ulp) and asserts the code criterion."""
     q_gpu = np.asarray(q_gpu)
     q_ref = np.asarray(q_ref)
@@ -106,7 +108,7 @@ def check_codes(q_gpu, q_ref, r_ref, tau_row):
         assert np.all(np.abs(q_gpu[mism] - q_ref[mism]) == 1), "a code differs by more than one step"
         assert np.all(near[mism]), "a code differs away from a rounding boundary"
     assert n <= CODE_MISMATCH_FRAC * total, f"{n} code mismatches of {total}"
-    assert q_gpu.min() >= -7 and q_gpu.max() <= 7, "code outside [-7, 7]"
+    assert q_gpu.min() >= -qmax and q_gpu.max() <= qmax, f"code outside [-{qmax}, {qmax}]"
     ulp = np.spacing(np.abs(r_ref).astype(np.float32)).astype(np.float64)
     n_ulp = int((dist_to_boundary(r_ref) <= ulp).sum())
     return n, n_ulp
