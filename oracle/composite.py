@@ -74,6 +74,21 @@ def block_svd_factors(w_ours: np.ndarray, perm: np.ndarray, c: int):
     return np.stack(us), ss
 
 
+def canonical_signs(u: np.ndarray) -> np.ndarray:
+    """Each column of u (or of every matrix in a stack) multiplied by -1 when
+    its entry of largest magnitude (the first one on ties) is negative.  A
+    singular vector is defined up to its sign; this fixes one representative
+    so that two computations of U_b can be compared column by column."""
+    u = np.array(u, dtype=np.float64, copy=True)
+    mats = u if u.ndim == 3 else u[None]
+    for m in mats:
+        for j in range(m.shape[1]):
+            r = int(np.argmax(np.abs(m[:, j])))
+            if m[r, j] < 0:
+                m[:, j] = -m[:, j]
+    return u
+
+
 def block_rotations(u_blocks: np.ndarray) -> np.ndarray:
     """R_b = U_b . H_c / sqrt(c) for every block (float64 [K/c, c, c])."""
     u = np.asarray(u_blocks, dtype=np.float64)

@@ -274,6 +274,28 @@ def check_block_svd(block_svd_factors, seed=21):
         energy = np.sum((u[b].T @ wb) ** 2, axis=1)
         ev = np.sort(np.linalg.eigvalsh(wb @ wb.T))[::-1]
         assert np.allclose(energy, ev, rtol=1e-10, atol=1e-10)
+        # U_b^T W_b = Sigma V^T has mutually orthogonal rows: U_b diagonalizes W_b W_b^T
+        g = (u[b].T @ wb) @ (u[b].T @ wb).T
+        assert np.max(np.abs(g - np.diag(np.diag(g)))) <= 1e-10 * np.max(np.abs(g))
+
+
+def check_canonical_signs(canonical_signs, seed=25):
+    """Hand example, then: the largest-magnitude entry of every column is
+    positive, columns equal +-the input's, orthogonality kept, idempotent."""
+    u = np.array([[0.6, -0.8], [-0.8, -0.6]])
+    assert np.array_equal(np.asarray(canonical_signs(u)), np.array([[-0.6, 0.8], [0.8, 0.6]]))
+    tie = np.array([[-0.5, 1.0], [0.5, 0.0]])  # first entry wins a magnitude tie
+    assert np.array_equal(np.asarray(canonical_signs(tie)), np.array([[0.5, 1.0], [-0.5, 0.0]]))
+    rng = np.random.default_rng(seed)
+    q = np.stack([random_orthogonal(rng, 16) for _ in range(3)])
+    c = np.asarray(canonical_signs(q))
+    for b in range(3):
+        idx = np.argmax(np.abs(c[b]), axis=0)
+        assert np.all(c[b][idx, np.arange(16)] > 0)
+        assert np.allclose(np.abs(c[b]), np.abs(q[b]), atol=0)
+        assert np.all(np.isin(np.sign(c[b] * q[b]).sum(0) / 16, [-1.0, 1.0]))
+        assert np.allclose(c[b].T @ c[b], np.eye(16), atol=1e-12)
+    assert np.array_equal(np.asarray(canonical_signs(c)), c)
 
 
 def check_block_rotations(block_rotations, seed=22):

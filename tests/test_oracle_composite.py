@@ -45,3 +45,35 @@ def test_full_pipeline_invariance_from_svd():
     lhs = composite.rotate_composite(x, perm, r) @ composite.rotate_composite(w, perm, r).T
     ref = x @ w.T
     assert np.max(np.abs(lhs - ref)) <= 1e-12 * np.max(np.abs(ref)) * K
+
+
+def test_canonical_signs():
+    P.check_canonical_signs(composite.canonical_signs)
+
+
+def test_canonical_signs_mutants_rejected():
+    import pytest
+
+    def by_first_entry(u):  # sign of the first entry instead of the largest
+        u = np.array(u, dtype=np.float64, copy=True)
+        mats = u if u.ndim == 3 else u[None]
+        for m in mats:
+            for j in range(m.shape[1]):
+                if m[0, j] < 0:
+                    m[:, j] = -m[:, j]
+        return u
+
+    def last_on_ties(u):
+        u = np.array(u, dtype=np.float64, copy=True)
+        mats = u if u.ndim == 3 else u[None]
+        for m in mats:
+            for j in range(m.shape[1]):
+                a = np.abs(m[:, j])
+                r = len(a) - 1 - int(np.argmax(a[::-1]))
+                if m[r, j] < 0:
+                    m[:, j] = -m[:, j]
+        return u
+    with pytest.raises(AssertionError):
+        P.check_canonical_signs(by_first_entry)
+    with pytest.raises(AssertionError):
+        P.check_canonical_signs(last_on_ties)
