@@ -289,6 +289,65 @@ int oq_quantize_weights_host(const double* W_u, int64_t N, int64_t K, int32_t ha
                              uint8_t* Wq, float* w_scale);
 
 /* ------------------------------------------------------------------------ */
+/* Offline preparation of the composite-rotation weight on the GPU           */
+/* (Section 4.1: zigzag P, per-block SVD factor U_b, R_b = U_b H_64 / 8,      */
+/* fold and RTN)                                                              */
+/* ------------------------------------------------------------------------ */
+/*
+ * The weight W is device fp16 [N][ldw] (row n = output channel n, K input
+ * channels); block b is input channels perm[64 b .. 64 b + 63].  The steps
+ * can be called one by one or through oq_prepare_weights_composite.
+ *
+ * oq_channel_energy -- energy[j] = sum_n W[n][j]^2 in fp64 (device [K]); a
+ *   fixed summation order, so equal columns give equal energies.
+ *   Errors: OQ_ERR_NULL, OQ_ERR_SHAPE, OQ_ERR_ALIGN, OQ_ERR_DEVICE, OQ_ERR_HIP.
+ *
+ * oq_zigzag_permutation -- perm (device int32 [K]) from device energies: the
+ *   descending order of the energy (ties to the lower channel index) dealt
+ *   to K / block blocks in snake order: sorted position i goes to round
+ *   r = i / n_b and to block i mod n_b on even rounds, n_b - 1 - (i mod n_b)
+ *   on odd rounds, slot r; perm[b * block + r] is the source channel.
+ *   K % block == 0, K <= 65536.
+ *
+ * oq_block_svd -- for each block (block must be 64): U (device fp64
+ *   [K/64][64][64], row-major, U_b[r][i]) holds the left singular vectors of
+ *   W_b (64 x N, the block's input-channel rows) as columns, ordered by
+ *   descending singular value (ties to the lower index), each column's
+ *   largest-magnitude entry (the first on ties) positive; sigma2 (device fp64
+ *   [K/64][64]) the squared singular values.  Computed as the eigenvectors of
+ *   the fp64 Gram matrix W_b W_b^T by cyclic Jacobi in fp64; vectors of
+ *   (numerically) repeated singular values, including a null space when
+ *   N < 64, are an orthonormal basis of their eigenspace, not unique.
+ *   perm entries out of [0, K) are clamped.
+ *
+ * oq_block_rotations -- Rt (device fp16 [K/64][64][64], column-major blocks:
+ *   Rt[b][j][r] = R_b[r][j]) with R_b = U_b H_64 / 8 evaluated in fp64 and
+ *   rounded once to fp16 (half to even): the operand of
+ *   oq_rotate_quantize_act_composite.
+ *
+ * oq_prepare_weights_composite -- all of the above, then the fold and RTN:
+ *   Wq, w_scale = oq_rotate_quantize_act_composite(W, perm, Rt) with s_t = 1
+ *   (the weight rows rotated by P R_hat and quantized per output channel).
+ *   perm device int32 [K]; Rt device [K/64][64][64] fp16, 16-byte aligned;
+ *   Wq device [N][K/2]; w_scale device fp32 [N]; work device, 16-byte
+ *   aligned, at least oq_prepare_weights_workspace_bytes(K) = 528 K bytes.
+ *   ldw % 8 == 0 and W 16-byte aligned (the fold's row loads).
+ *   Errors: OQ_ERR_NULL, OQ_ERR_SHAPE (K % 64, K > 16384, workspace),
+ *   OQ_ERR_ALIGN, OQ_ERR_DEVICE, OQ_ERR_HIP.
+ */
+int oq_channel_energy(const void* W, int64_t N, int64_t K, int64_t ldw, double* energy,
+                      void* stream);
+int oq_zigzag_permutation(const double* energy, int64_t K, int32_t block, int32_t* perm,
+                          void* stream);
+int oq_block_svd(const void* W, int64_t N, int64_t K, int64_t ldw, const int32_t* perm,
+                 int32_t block, double* U, double* sigma2, void* stream);
+int oq_block_rotations(const double* U, int64_t K, int32_t block, uint16_t* Rt, void* stream);
+size_t oq_prepare_weights_workspace_bytes(int64_t K);
+int oq_prepare_weights_composite(const void* W, int64_t N, int64_t K, int64_t ldw,
+                                 int32_t* perm, uint16_t* Rt, uint8_t* Wq, float* w_scale,
+                                 void* work, size_t work_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* W4A8: 8-bit per-token activations against the int4 weights (the paper's   */
 /* deployment mode, Appendix: W4A8 real-quantization latency)                */
 /* ------------------------------------------------------------------------ */

@@ -270,6 +270,63 @@ def w4a8_gemm_i32(Xq8, Wq, acc=None, stream=None):
     return acc
 
 
+def channel_energy(W, energy=None, stream=None):
+    """fp64 [K] column energies sum_n W[n][j]^2 of a device fp16 weight [N, K]."""
+    N, K = W.shape
+    if energy is None:
+        energy = torch.empty((K,), dtype=torch.float64, device=W.device)
+    _check(lib().oq_channel_energy(_ptr(W), N, K, W.stride(0), _ptr(energy), _stream(stream)), "oq_channel_energy")
+    return energy
+
+
+def zigzag_permutation(energy, block=64, perm=None, stream=None):
+    """Device zigzag permutation (int32 [K]) from device fp64 energies."""
+    K = energy.shape[0]
+    if perm is None:
+        perm = torch.empty((K,), dtype=torch.int32, device=energy.device)
+    _check(lib().oq_zigzag_permutation(_ptr(energy), K, block, _ptr(perm), _stream(stream)), "oq_zigzag_permutation")
+    return perm
+
+
+def block_svd(W, perm, block=64, U=None, sigma2=None, stream=None):
+    """(U fp64 [K/64, 64, 64], sigma2 fp64 [K/64, 64]) of every block of the permuted weight."""
+    N, K = W.shape
+    nb = K // block
+    if U is None:
+        U = torch.empty((nb, block, block), dtype=torch.float64, device=W.device)
+    if sigma2 is None:
+        sigma2 = torch.empty((nb, block), dtype=torch.float64, device=W.device)
+    _check(lib().oq_block_svd(_ptr(W), N, K, W.stride(0), _ptr(perm), block, _ptr(U), _ptr(sigma2),
+                              _stream(stream)), "oq_block_svd")
+    return U, sigma2
+
+
+def block_rotations(U, Rt=None, stream=None):
+    """fp16 column-major blocks (int16 [nb, 64, 64]) of U_b H_64 / 8."""
+    nb, c, _ = U.shape
+    if Rt is None:
+        Rt = torch.empty((nb, c, c), dtype=torch.int16, device=U.device)
+    _check(lib().oq_block_rotations(_ptr(U), nb * c, c, _ptr(Rt), _stream(stream)), "oq_block_rotations")
+    return Rt
+
+
+def prepare_weights_composite(W, stream=None):
+    """Device fp16 weight [N, K] -> (perm int32 [K], Rt int16 [K/64, 64, 64],
+    Wq uint8 [N, K/2], w_scale f32 [N]), all on the device."""
+    N, K = W.shape
+    dev = W.device
+    perm = torch.empty((K,), dtype=torch.int32, device=dev)
+    Rt = torch.empty((K // 64, 64, 64), dtype=torch.int16, device=dev)
+    Wq = torch.empty((N, K // 2), dtype=torch.uint8, device=dev)
+    ws = torch.empty((N,), dtype=torch.float32, device=dev)
+    nbytes = int(lib().oq_prepare_weights_workspace_bytes(K))
+    work = torch.empty((max(nbytes, 16),), dtype=torch.uint8, device=dev)
+    _check(lib().oq_prepare_weights_composite(_ptr(W), N, K, W.stride(0), _ptr(perm), _ptr(Rt), _ptr(Wq), _ptr(ws),
+                                              _ptr(work), work.numel(), _stream(stream)),
+           "oq_prepare_weights_composite")
+    return perm, Rt, Wq, ws
+
+
 def rotate_act_f32(X, had_block, Y=None, stream=None):
     """Rotated activation y = x H_b / sqrt(b) in fp32 [M, K] (calibration input)."""
     M, K = X.shape

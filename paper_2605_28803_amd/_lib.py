@@ -55,6 +55,12 @@ SIGNATURES = {
     "oq_quantize_weights": (i32, [vp, i64, i64, i64, i32, vp, vp, vp]),
     "oq_quantize_weights_host": (i32, [vp, i64, i64, i32, vp, vp]),
     "oq_rotate_act_f32": (i32, [vp, i64, i64, i64, i32, vp, vp]),
+    "oq_channel_energy": (i32, [vp, i64, i64, i64, vp, vp]),
+    "oq_zigzag_permutation": (i32, [vp, i64, i32, vp, vp]),
+    "oq_block_svd": (i32, [vp, i64, i64, i64, vp, i32, vp, vp, vp]),
+    "oq_block_rotations": (i32, [vp, i64, i32, vp, vp]),
+    "oq_prepare_weights_workspace_bytes": (C.c_size_t, [i64]),
+    "oq_prepare_weights_composite": (i32, [vp, i64, i64, i64, vp, vp, vp, vp, vp, C.c_size_t, vp]),
     "oq_rotate_quantize_act_i8": (i32, [vp, i64, i64, i64, i32, fp, i32, vp, vp, vp]),
     "oq_w4a8_linear": (i32, [vp, vp, i64, vp, vp, vp, i64, i64, vp, i64, i32, vp]),
     "oq_w4a8_gemm_i32": (i32, [vp, i64, vp, i64, i64, vp, i64, vp]),

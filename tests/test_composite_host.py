@@ -85,3 +85,31 @@ def test_composite_call_rejects_bad_arguments():
     wd = np.zeros((1, 4)); rt = np.zeros((1, 4, 4), dtype=np.uint16)
     out = np.zeros(2, dtype=np.uint8); ws = np.zeros(1, dtype=np.float32)
     assert wq(wd.ctypes.data, 1, 4, 4, bad.ctypes.data, rt.ctypes.data, out.ctypes.data, ws.ctypes.data) == ARG
+
+
+def test_prepare_calls_reject_bad_arguments():
+    lib = _lib.load()
+    e = lib.oq_channel_energy
+    assert e(None, 4, 64, 64, P16, None) == NULL
+    assert e(P16, 0, 64, 64, P16, None) == SHAPE
+    assert e(P16, 4, 64, 32, P16, None) == SHAPE
+    assert e(P16, 4, 64, 64, P4, None) == ALIGN                  # fp64 output 8-byte aligned
+    z = lib.oq_zigzag_permutation
+    assert z(P16, 96, 64, P16, None) == SHAPE                    # K % block
+    assert z(P16, 1 << 17, 64, P16, None) == SHAPE               # K limit
+    assert z(None, 128, 64, P16, None) == NULL
+    s = lib.oq_block_svd
+    assert s(P16, 8, 128, 128, P16, 32, P16, P16, None) == SHAPE  # block must be 64
+    assert s(P16, 8, 96, 96, P16, 64, P16, P16, None) == SHAPE
+    assert s(P16, 8, 128, 128, None, 64, P16, P16, None) == NULL
+    assert s(P16, 8, 128, 128, P16, 64, P4, P16, None) == ALIGN
+    r = lib.oq_block_rotations
+    assert r(P16, 100, 64, P16, None) == SHAPE
+    assert r(None, 128, 64, P16, None) == NULL
+    ws = lib.oq_prepare_weights_workspace_bytes(1024)
+    assert ws == 1024 * 66 * 8 and lib.oq_prepare_weights_workspace_bytes(0) == 0
+    f = lib.oq_prepare_weights_composite
+    assert f(P16, 8, 1024, 1024, P16, P16, P16, P16, P16, ws - 1, None) == SHAPE
+    assert f(P16, 8, 1024, 1028, P16, P16, P16, P16, P16, ws, None) == ALIGN  # ldw % 8
+    assert f(P16, 8, 1024, 1024, P16, P16, None, P16, P16, ws, None) == NULL
+    assert f(P16, 8, 1000, 1000, P16, P16, P16, P16, P16, ws, None) == SHAPE  # K % 64
