@@ -26,7 +26,10 @@ JSON lines to gpurun_out/sweep.jsonl instead; --roofline-only runs just the
 roofline kernel measurement (the command the committed rocprofv3 summaries of
 that kernel were taken with); --copy-calibration runs a plain copy of known
 size (the counter calibration reference); --gr00t-only times just the
-GR00T-shaped step; --composite-only times just the full composite rotation.
+GR00T-shaped step; --composite-only times just the full composite rotation;
+--static-only times the static per-channel step path and its calibration;
+--w4a8-only times the W4A8 mode beside W4A4; --prepare-only times the GPU
+weight preparation for the composite rotation.
 """
 from __future__ import annotations
 
@@ -267,6 +270,180 @@ def composite_kernels():
     return out
 
 
+def static_scale_kernels():
+    """The static per-step, per-channel path, cold: rotate-quantize against a
+    step row (algorithmic bytes 2.5 K + 4 per row + 4 K for the row of
+    steps) at M = 16384 x K = 1024 / 4096 and at the DiT shape M = 50 (tiled
+    codes); the per-token kernel on the same inputs beside it; and the
+    calibration collector on n = 16384 rotated rows (fp32 rotation output,
+    6 K bytes per row, and the exact column percentile, which reads the
+    n x K fp32 rows once per radix pass, 4 passes)."""
+    import torch
+    import paper_2605_28803_amd as oq
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    flush = torch.empty((512 << 20,), dtype=torch.uint8, device=dev)
+
+    def cold(fn, reps):
+        ts = []
+        for _ in range(reps):
+            flush.fill_(1)
+            s = torch.cuda.Event(enable_timing=True)
+            e = torch.cuda.Event(enable_timing=True)
+            s.record(stream)
+            fn()
+            e.record(stream)
+            e.synchronize()
+            ts.append(s.elapsed_time(e))
+        return float(np.median(ts))
+
+    def rate(b, t):
+        return {"us": round(t * 1e3, 2), "GBs": round(b / (t * 1e-3) / 1e9, 1),
+                "frac_hbm_peak": round(b / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+
+    out = {}
+    g = torch.Generator(device=dev).manual_seed(17)
+    for M, K in ((16384, 1024), (16384, 4096), (50, 1024)):
+        X = torch.randn((M, K), generator=g, device=dev).half()
+        n = 16384
+        Yc = oq.rotate_act_f32(torch.randn((n, K), generator=g, device=dev).half(), K)
+        delta = oq.calibrate_step_scales(Yc, 99.9, 7.0)
+        work = torch.empty((oq.calibrate_workspace_bytes(K),), dtype=torch.uint8, device=dev)
+        tiled = M <= 64
+        if tiled:
+            Xq, xs = oq.rotate_quantize_act_static_tiled(X, K, delta)
+            f_static = lambda: oq.rotate_quantize_act_static_tiled(X, K, delta, Xt=Xq, x_scale=xs)
+            Xp, xp = oq.rotate_quantize_act_tiled(X, K)
+            f_tok = lambda: oq.rotate_quantize_act_tiled(X, K, Xt=Xp, x_scale=xp)
+        else:
+            Xq, xs = oq.rotate_quantize_act_static(X, K, delta)
+            f_static = lambda: oq.rotate_quantize_act_static(X, K, delta, Xq=Xq, x_scale=xs)
+            Xp, xp = oq.rotate_quantize_act(X, K)
+            f_tok = lambda: oq.rotate_quantize_act(X, K, Xq=Xp, x_scale=xp)
+        t_s = cold(f_static, 15)
+        t_t = cold(f_tok, 15)
+        rec = {"static": rate(rq_bytes(M, K) + 4 * K, t_s), "per_token": rate(rq_bytes(M, K), t_t)}
+        if M > 64:
+            Y = torch.empty((n, K), dtype=torch.float32, device=dev)
+            Xc = torch.randn((n, K), generator=g, device=dev).half()
+            t_rot = cold(lambda: oq.rotate_act_f32(Xc, K, Y=Y), 10)
+            t_cal = cold(lambda: oq.calibrate_step_scales(Yc, 99.9, 7.0, delta=delta, work=work), 10)
+            rec["calib_rotate_f32_n16384"] = rate(n * K * 6, t_rot)
+            rec["calib_percentile_n16384"] = dict(rate(n * K * 4, t_cal), passes=4,
+                                                  pass_GBs=round(4 * n * K * 4 / (t_cal * 1e-3) / 1e9, 1))
+            del Y, Xc
+        out[f"M{M}_K{K}"] = rec
+        del X, Xq, xs, Xp, xp, Yc, work
+    del flush
+    torch.cuda.empty_cache()
+    return out
+
+
+def w4a8_kernels():
+    """The W4A8 mode, cold: the 8-bit rotate-quantize at M = K = 16384
+    (algorithmic bytes 2 K + K + 4 per row), the W4A8 GEMM at M = K = N = 16384
+    (2 M N K ops against the int8 MFMA peak) and at the DiT gate|up shape
+    (M = 50, N = 8192, K = 1024: bytes M K + N K / 2 + 4 (M + N) + 2 M N
+    against HBM), each beside its W4A4 counterpart on the same inputs."""
+    import torch
+    import paper_2605_28803_amd as oq
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    flush = torch.empty((512 << 20,), dtype=torch.uint8, device=dev)
+
+    def cold(fn, reps):
+        ts = []
+        for _ in range(reps):
+            flush.fill_(1)
+            s = torch.cuda.Event(enable_timing=True)
+            e = torch.cuda.Event(enable_timing=True)
+            s.record(stream)
+            fn()
+            e.record(stream)
+            e.synchronize()
+            ts.append(s.elapsed_time(e))
+        return float(np.median(ts))
+
+    out = {}
+    g = torch.Generator(device=dev).manual_seed(19)
+    for M, N, K in ((16384, 16384, 16384), (50, 8192, 1024)):
+        X = torch.randn((M, K), generator=g, device=dev).half()
+        W = (torch.randn((N, K), generator=g, device=dev) * 0.02).half()
+        Wq, ws = oq.quantize_weights(W, K)
+        del W
+        X8, xs8 = oq.rotate_quantize_act_i8(X, K)
+        X4, xs4 = oq.rotate_quantize_act(X, K)
+        Y = torch.empty((M, N), dtype=torch.float16, device=dev)
+        reps = 10 if M > 64 else 30
+        t_r8 = cold(lambda: oq.rotate_quantize_act_i8(X, K, Xq8=X8, x_scale=xs8), reps)
+        t_g8 = cold(lambda: oq.w4a8_linear(X8, xs8, Wq, ws, Y=Y), reps)
+        t_g4 = cold(lambda: oq.w4a4_linear(X4, xs4, Wq, ws, Y=Y), reps)
+        ops = 2 * M * N * K
+        rec = {"rotate_quant_i8_us": round(t_r8 * 1e3, 2),
+               "rotate_quant_i8_GBs": round(M * (3 * K + 4) / (t_r8 * 1e-3) / 1e9, 1),
+               "w4a8_gemm_us": round(t_g8 * 1e3, 2), "w4a4_gemm_us": round(t_g4 * 1e3, 2),
+               "w4a8_TOPs": round(ops / (t_g8 * 1e-3) / 1e12, 1),
+               "w4a8_frac_int8_peak": round(ops / (t_g8 * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4)}
+        if M <= 64:
+            b = M * K + N * K // 2 + 4 * (M + N) + 2 * M * N
+            rec["w4a8_gemm_GBs"] = round(b / (t_g8 * 1e-3) / 1e9, 1)
+        out[f"M{M}_N{N}_K{K}"] = rec
+        del X, Wq, ws, X8, X4, Y
+    del flush
+    torch.cuda.empty_cache()
+    return out
+
+
+def prepare_kernels():
+    """Offline composite-rotation weight preparation on the GPU, per weight
+    of the Pi-0.5 DiT block (qkv 3072 x 1024, o 1024 x 1024, gate|up 8192 x
+    1024, down 1024 x 4096) and the Gemma-2B-shaped gate|up (32768 x 2048):
+    the whole oq_prepare_weights_composite call and its steps (energies,
+    zigzag ranks, block Gram + Jacobi, fp16 R_b, fold + RTN), warm, median
+    of 5.  The energies read N K fp16 once; the Gram kernel reads them once
+    more, gathered; the Jacobi sweeps are LDS / latency bound."""
+    import torch
+    import paper_2605_28803_amd as oq
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+
+    def timed(fn, reps=5):
+        fn()
+        ts = []
+        for _ in range(reps):
+            s = torch.cuda.Event(enable_timing=True)
+            e = torch.cuda.Event(enable_timing=True)
+            s.record(stream)
+            fn()
+            e.record(stream)
+            e.synchronize()
+            ts.append(s.elapsed_time(e))
+        return round(float(np.median(ts)) * 1e3, 1)
+
+    out = {}
+    g = torch.Generator(device=dev).manual_seed(23)
+    for name, N, K in (("qkv", 3072, 1024), ("o", 1024, 1024), ("gate_up", 8192, 1024), ("down", 1024, 4096),
+                       ("gemma_gate_up", 32768, 2048)):
+        W = (torch.randn((N, K), generator=g, device=dev) * 0.02).half()
+        e = oq.channel_energy(W)
+        perm = oq.zigzag_permutation(e)
+        U, lam = oq.block_svd(W, perm)
+        Rt = oq.block_rotations(U)
+        Wq = torch.empty((N, K // 2), dtype=torch.uint8, device=dev)
+        ws = torch.empty((N,), dtype=torch.float32, device=dev)
+        out[f"{name}_N{N}_K{K}"] = {
+            "total_us": timed(lambda: oq.prepare_weights_composite(W)),
+            "energy_us": timed(lambda: oq.channel_energy(W, energy=e)),
+            "zigzag_us": timed(lambda: oq.zigzag_permutation(e, perm=perm)),
+            "block_svd_us": timed(lambda: oq.block_svd(W, perm, U=U, sigma2=lam)),
+            "rotations_us": timed(lambda: oq.block_rotations(U, Rt=Rt)),
+            "fold_rtn_us": timed(lambda: oq.rotate_quantize_act_composite(W, perm, Rt, Xq=Wq, x_scale=ws)),
+        }
+        del W, e, perm, U, lam, Rt, Wq, ws
+    torch.cuda.empty_cache()
+    return out
+
+
 def copy_calibration():
     """A plain device copy of a known size (256 MiB read + 256 MiB written), the
     reference for scaling the FETCH_SIZE / WRITE_SIZE counters."""
@@ -499,6 +676,9 @@ def run_dit(args):
         line["dit_gr00t"] = gr00t_step()
         line["prefill_gemma2b_layer"] = prefill_linears()
         line["composite_rotate_quant"] = composite_kernels()
+        line["static_step_scales"] = static_scale_kernels()
+        line["w4a8"] = w4a8_kernels()
+        line["weight_preparation"] = prepare_kernels()
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle sample)", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(cfg, inp)
@@ -577,6 +757,9 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--gr00t-only", action="store_true")
     ap.add_argument("--composite-only", action="store_true")
+    ap.add_argument("--static-only", action="store_true")
+    ap.add_argument("--w4a8-only", action="store_true")
+    ap.add_argument("--prepare-only", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (--gpus must be 1)", file=sys.stderr)
@@ -591,6 +774,12 @@ def main():
         print(json.dumps({"dit_gr00t": gr00t_step()}), flush=True)
     elif args.composite_only:
         print(json.dumps({"composite_rotate_quant": composite_kernels()}), flush=True)
+    elif args.static_only:
+        print(json.dumps({"static_step_scales": static_scale_kernels()}), flush=True)
+    elif args.w4a8_only:
+        print(json.dumps({"w4a8": w4a8_kernels()}), flush=True)
+    elif args.prepare_only:
+        print(json.dumps({"weight_preparation": prepare_kernels()}), flush=True)
     else:
         run_dit(args)
 
