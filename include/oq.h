@@ -455,6 +455,16 @@ int oq_rotate_quantize_act_static_tiled(const void* X, int64_t M, int64_t K, int
 int oq_quantize_weights_step_host(const double* W_u, int64_t N, int64_t K, int32_t had_block,
                                   const float* delta, uint8_t* Wq, float* w_scale);
 
+/*
+ * oq_quantize_weights_step -- the same fold on the device from an fp16
+ * weight (as oq_quantize_weights, with channel j of each rotated row
+ * multiplied by delta[j] before the row's maximum), in fp32.  delta device
+ * fp32 [K], 16-byte aligned.  Errors: as oq_quantize_weights; OQ_ERR_NULL
+ * (delta), OQ_ERR_ALIGN.
+ */
+int oq_quantize_weights_step(const void* W_u, int64_t N, int64_t K, int64_t ldw, int32_t had_block,
+                             const float* delta, uint8_t* Wq, float* w_scale, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* DiT denoising-step driver                                                 */
 /* ------------------------------------------------------------------------ */
@@ -593,6 +603,27 @@ int oq_dit_run_block(oq_dit* h, int32_t l, int32_t t, float* resid, void* stream
  * token scales are then in the workspace (oq_dit_intermediates.codes,
  * .x_scale).  Errors: as oq_dit_run_block; OQ_ERR_ARG for a bad site. */
 int oq_dit_run_block_until(oq_dit* h, int32_t l, int32_t t, float* resid, int32_t site, void* stream);
+
+/* Static per-step, per-channel steps inside the driver (eq:perstep_scale with
+ * the per-(layer, step, channel) table; the scalar s_t of oq_dit_weights is
+ * then unused for the four block sites).  delta: device fp32
+ * [n_blocks][steps][3 D + F], 16-byte aligned: for block l and step t the step
+ * rows of the q|k|v (q) input [D], the o input [D], the gate|up (ff0) input
+ * [D] and the down (ff2) input [F], in that order.  step_weights: host array
+ * [n_blocks][steps][4] of the same four linears folded with their step rows
+ * (oq_quantize_weights_step: W''[n][j] = W'[n][j] Delta_j, RTN per output
+ * channel), device pointers borrowed until the mode is cleared.  Each site's
+ * producer then writes codes clamp(round(y_j / Delta_j), +-7) with token
+ * scale 1 and each linear uses its step's folded weight.  delta = NULL
+ * returns the handle to the per-token quantizer.  The array is copied; the
+ * captured steps are dropped.  Not for the gr00t conditioning k|v linear
+ * (step-invariant, computed once).  Errors: OQ_ERR_NULL, OQ_ERR_ALIGN. */
+int oq_dit_set_static_steps(oq_dit* h, const float* delta, const oq_qweight* step_weights);
+
+/* The step's in-projection alone: resid [M][D] fp32 = x W_in^T + b_in (the
+ * residual at the input of block 0), for a caller that runs blocks one by
+ * one (calibration rollouts).  Errors: OQ_ERR_NULL, OQ_ERR_ALIGN, OQ_ERR_HIP. */
+int oq_dit_in_projection(oq_dit* h, const float* x, float* resid, void* stream);
 
 /* Intermediate tensors of the most recent block the handle ran (fp16,
  * row-major, M = batch * tokens rows), for per-site parity checks: every

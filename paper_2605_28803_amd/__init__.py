@@ -378,6 +378,19 @@ def rotate_quantize_act_static_tiled(X, had_block, delta, Xt=None, x_scale=None,
     return Xt, x_scale
 
 
+def quantize_weights_step(W_u, had_block, delta, Wq=None, w_scale=None, stream=None):
+    """Device fp16 weight [N, K] rotated, scaled by the device step row delta
+    (f32 [K]) per input channel and RTN-quantized: (Wq uint8 [N, K/2], w_scale f32 [N])."""
+    N, K = W_u.shape
+    if Wq is None:
+        Wq = torch.empty((N, K // 2), dtype=torch.uint8, device=W_u.device)
+    if w_scale is None:
+        w_scale = torch.empty((N,), dtype=torch.float32, device=W_u.device)
+    _check(lib().oq_quantize_weights_step(_ptr(W_u), N, K, W_u.stride(0), had_block, _ptr(delta), _ptr(Wq),
+                                          _ptr(w_scale), _stream(stream)), "oq_quantize_weights_step")
+    return Wq, w_scale
+
+
 def quantize_weights_step_host(W_u: np.ndarray, had_block: int, delta: np.ndarray):
     """float64 host weight [N, K] rotated, scaled by the step row delta [K] per
     input channel and RTN-quantized: (Wq uint8 [N, K/2], w_scale f32 [N])."""

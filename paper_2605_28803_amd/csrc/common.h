@@ -50,10 +50,12 @@ bool rq_plan(int64_t K, RQPlan* p);
 // tiled: Xq is in the 16-row tiled layout (K % 128 == 0) instead of [M][K/2].
 // sdelta: static per-channel steps [K] (token scale 1) instead of the
 // per-token maximum; rotate_only: write s_t * y in fp32 to `ratio` only;
-// i8: 8-bit codes (q_max = 127), one byte per code, Xq [M][K].
+// i8: 8-bit codes (q_max = 127), one byte per code, Xq [M][K]; cmul:
+// per-channel multiplier of the rotated row before its maximum.
 int rq_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block, float s_t,
               uint8_t* Xq, float* x_scale, float* ratio, hipStream_t stream, bool tiled = false,
-              const float* sdelta = nullptr, bool rotate_only = false, bool i8 = false);
+              const float* sdelta = nullptr, bool rotate_only = false, bool i8 = false,
+              const float* cmul = nullptr);
 
 // Shape/alignment validation shared by every rotate-quantize entry point.
 int rq_validate(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block,

@@ -74,6 +74,7 @@ struct RQOut {
   int logT, logb;
   float s_t, s_over_sqrtb;
   bool tiled;  // codes in the 16-row tiled layout (the small-M product's operand)
+  const float* sdelta;  // static per-channel steps of this site and step (null: per-token quantizer)
 };
 
 // r = x W_in^T + b_in
@@ -158,7 +159,7 @@ __global__ __launch_bounds__(256) void norm_rq_kernel(const float* __restrict__ 
     }
     if (m.valid) store8_f16(h + m.row * D + k, v[c]);
   }
-  rqd::rq_core<C>(v, m, D, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr, o.tiled);
+  rqd::rq_core<C>(v, m, D, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr, o.tiled, o.sdelta);
 }
 
 // gelu_tanh(x) = 0.5 x (1 + tanh(u)), u = sqrt(2/pi) (x + 0.044715 x^3).
@@ -218,7 +219,7 @@ __global__ __launch_bounds__(256) void gelu_rq_kernel(const uint16_t* __restrict
 #pragma unroll
   for (int c = 0; c < C; ++c)
     if (m.valid) store8_f16(act + m.row * F + rqd::chan(m, c, 0), v[c]);
-  rqd::rq_core<C>(v, m, F, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr, o.tiled);
+  rqd::rq_core<C>(v, m, F, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr, o.tiled, o.sdelta);
 }
 
 struct AttnArgs {
@@ -487,7 +488,7 @@ __global__ __launch_bounds__(256) void combine_rq_kernel(AttnArgs a, int64_t M, 
     for (int j = 0; j < 8; ++j) v[c][j] = m.valid ? f16r(num[j] * inv) : 0.0f;
     if (m.valid) store8_f16(a.out + m.row * a.out_ld + k, v[c]);
   }
-  rqd::rq_core<C>(v, m, a.D, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr, o.tiled);
+  rqd::rq_core<C>(v, m, a.D, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr, o.tiled, o.sdelta);
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
@@ -695,6 +696,11 @@ struct oq_dit {
   std::vector<oq_dit_graph> graphs;
   bool use_graphs = true;
   bool tiled = false;  // block linears' token codes in the 16-row tiled layout (M <= 64)
+  // Static per-step, per-channel steps (null: the per-token quantizer with
+  // the scalar step scale): device table [n_blocks][steps][3D + F] and the
+  // per-(block, step) folded weights of the four block linears.
+  const float* static_delta = nullptr;
+  std::vector<oq_qweight> static_w;
 };
 
 namespace oq {
@@ -711,9 +717,11 @@ const uint16_t* mod_ptr(oq_dit* h, int l, int t, int k) {
   return static_cast<const uint16_t*>(h->w.mod) + ((static_cast<int64_t>(l) * h->cfg.steps + t) * nm + k) * D;
 }
 
-RQOut rq_out(oq_dit* h, int64_t K, float s, RQPlan* p) {
+RQOut rq_out(oq_dit* h, int64_t K, float s, RQPlan* p, const float* sdelta = nullptr) {
   fused_plan(K, p);
   RQOut o;
+  o.sdelta = sdelta;
+  if (sdelta) s = 1.0f;  // the static steps replace the token step and its scale
   o.xq = at<uint8_t>(h, h->lay.xq);
   o.xs = at<float>(h, h->lay.xs);
   o.logT = p->logT;
@@ -758,11 +766,11 @@ bool with_chunks(int chunks, F&& f) {
 
 // h = fp16(norm(r) g (1 + sc) + sh) and its codes (sc may be null: no scale).
 int norm_rq(oq_dit* h, const float* r, const void* g, const uint16_t* sc, const uint16_t* sh, uint16_t* out,
-            float s, hipStream_t st) {
+            float s, hipStream_t st, const float* sdelta) {
   const int64_t M = static_cast<int64_t>(h->cfg.batch) * h->cfg.tokens;
   const int64_t D = h->cfg.hidden;
   RQPlan p;
-  const RQOut o = rq_out(h, D, s, &p);
+  const RQOut o = rq_out(h, D, s, &p, sdelta);
   const FusedLaunch fl = fused_launch(M, D, p);
   const uint16_t* gg = static_cast<const uint16_t*>(g);
   const bool ln = is_gr00t(h->cfg);
@@ -786,11 +794,11 @@ int norm_rq(oq_dit* h, const float* r, const void* g, const uint16_t* sc, const 
 }
 
 // a = fp16(gelu(...)) of the MLP's first linear output and its codes.
-int gelu_rq(oq_dit* h, const uint16_t* in, uint16_t* act, float s, hipStream_t st) {
+int gelu_rq(oq_dit* h, const uint16_t* in, uint16_t* act, float s, hipStream_t st, const float* sdelta) {
   const int64_t M = static_cast<int64_t>(h->cfg.batch) * h->cfg.tokens;
   const int64_t F = h->cfg.mlp;
   RQPlan p;
-  const RQOut o = rq_out(h, F, s, &p);
+  const RQOut o = rq_out(h, F, s, &p, sdelta);
   const FusedLaunch fl = fused_launch(M, F, p);
   const bool gated = !is_gr00t(h->cfg);
   const bool ok = with_chunks(p.chunks, [&](auto C) {
@@ -817,7 +825,7 @@ int gemm(oq_dit* h, const oq_qweight& wt, int64_t K, int64_t N, Epilogue epi, vo
 // pre_ld) followed by `own` rows of the q|k|v buffer.
 int attention_rq(oq_dit* h, const uint16_t* q, int64_t q_ld, const uint16_t* k_pre, const uint16_t* v_pre,
                  int P, int64_t pre_ld, const uint16_t* k_own, const uint16_t* v_own, int64_t own_ld, int own,
-                 float s, hipStream_t st) {
+                 float s, hipStream_t st, const float* sdelta) {
   const oq_dit_config& c = h->cfg;
   const int64_t M = static_cast<int64_t>(c.batch) * c.tokens;
   const int64_t D = c.hidden;
@@ -851,7 +859,7 @@ int attention_rq(oq_dit* h, const uint16_t* q, int64_t q_ld, const uint16_t* k_p
   int e = launch_status();
   if (e != OQ_OK) return e;
   RQPlan p;
-  const RQOut ro = rq_out(h, D, s, &p);
+  const RQOut ro = rq_out(h, D, s, &p, sdelta);
   const FusedLaunch fl = fused_launch(M, D, p);
   const bool ok = with_chunks(p.chunks, [&](auto C) {
     hipLaunchKernelGGL((combine_rq_kernel<decltype(C)::value>), fl.grid, fl.block, fl.lds, st, a, M, ro);
@@ -862,32 +870,54 @@ int attention_rq(oq_dit* h, const uint16_t* q, int64_t q_ld, const uint16_t* k_p
 // until: stop after the fused producer of quantization site `until` (0: the
 // q|k|v input, 1: the o input, 2: the gate|up input, 3: the down input), or
 // run the whole block (until = 4).
+// Per-site static steps and the linears' weights of block l at step t: the
+// per-step folded copies in the static mode, else the block's weights.
+struct SiteSet {
+  const float* d[4];
+  const oq_qweight* w[4];
+};
+
+SiteSet site_set(oq_dit* h, int l, int t) {
+  const oq_dit_config& c = h->cfg;
+  const oq_dit_block& bw = h->blocks[l];
+  SiteSet ss;
+  const oq_qweight* own[4] = {&bw.qkv, &bw.o, &bw.gate_up, &bw.down};
+  const size_t lt = static_cast<size_t>(l) * c.steps + t;
+  const int64_t D = c.hidden;
+  for (int i = 0; i < 4; ++i) {
+    ss.d[i] = h->static_delta ? h->static_delta + lt * (3 * D + c.mlp) + i * D : nullptr;
+    ss.w[i] = h->static_delta ? &h->static_w[lt * 4 + i] : own[i];
+  }
+  return ss;
+}
+
 int run_block_pi(oq_dit* h, int l, int t, float* r, hipStream_t st, int until) {
   const oq_dit_config& c = h->cfg;
   const oq_dit_block& bw = h->blocks[l];
   const int64_t D = c.hidden, F = c.mlp;
   const float* s = &h->s_table[(static_cast<size_t>(l) * c.steps + t) * 4];
+  const SiteSet ss = site_set(h, l, t);
   uint16_t* h1 = at<uint16_t>(h, h->lay.h1);
   uint16_t* qkv = at<uint16_t>(h, h->lay.qkv);
   uint16_t* h2 = at<uint16_t>(h, h->lay.h2);
   uint16_t* gu = at<uint16_t>(h, h->lay.gu);
   uint16_t* act = at<uint16_t>(h, h->lay.act);
   int e;
-  if ((e = norm_rq(h, r, bw.g1, mod_ptr(h, l, t, 0), mod_ptr(h, l, t, 1), h1, s[0], st)) != OQ_OK) return e;
+  if ((e = norm_rq(h, r, bw.g1, mod_ptr(h, l, t, 0), mod_ptr(h, l, t, 1), h1, s[0], st, ss.d[0])) != OQ_OK) return e;
   if (until == 0) return OQ_OK;
-  if ((e = gemm(h, bw.qkv, D, 3 * D, EPI_F16, qkv, 3 * D, nullptr, st)) != OQ_OK) return e;
+  if ((e = gemm(h, *ss.w[0], D, 3 * D, EPI_F16, qkv, 3 * D, nullptr, st)) != OQ_OK) return e;
   if ((e = attention_rq(h, qkv, 3 * D, static_cast<const uint16_t*>(bw.prefix_k),
                         static_cast<const uint16_t*>(bw.prefix_v), c.prefix, D, qkv + D, qkv + 2 * D, 3 * D,
-                        c.tokens, s[1], st)) != OQ_OK)
+                        c.tokens, s[1], st, ss.d[1])) != OQ_OK)
     return e;
   if (until == 1) return OQ_OK;
-  if ((e = gemm(h, bw.o, D, D, EPI_RESID_F32, r, D, mod_ptr(h, l, t, 2), st)) != OQ_OK) return e;
-  if ((e = norm_rq(h, r, bw.g2, mod_ptr(h, l, t, 3), mod_ptr(h, l, t, 4), h2, s[2], st)) != OQ_OK) return e;
+  if ((e = gemm(h, *ss.w[1], D, D, EPI_RESID_F32, r, D, mod_ptr(h, l, t, 2), st)) != OQ_OK) return e;
+  if ((e = norm_rq(h, r, bw.g2, mod_ptr(h, l, t, 3), mod_ptr(h, l, t, 4), h2, s[2], st, ss.d[2])) != OQ_OK) return e;
   if (until == 2) return OQ_OK;
-  if ((e = gemm(h, bw.gate_up, D, 2 * F, EPI_F16, gu, 2 * F, nullptr, st)) != OQ_OK) return e;
-  if ((e = gelu_rq(h, gu, act, s[3], st)) != OQ_OK) return e;
+  if ((e = gemm(h, *ss.w[2], D, 2 * F, EPI_F16, gu, 2 * F, nullptr, st)) != OQ_OK) return e;
+  if ((e = gelu_rq(h, gu, act, s[3], st, ss.d[3])) != OQ_OK) return e;
   if (until == 3) return OQ_OK;
-  return gemm(h, bw.down, F, D, EPI_RESID_F32, r, D, mod_ptr(h, l, t, 5), st);
+  return gemm(h, *ss.w[3], F, D, EPI_RESID_F32, r, D, mod_ptr(h, l, t, 5), st);
 }
 
 int run_block_gr00t(oq_dit* h, int l, int t, float* r, hipStream_t st, int until) {
@@ -895,35 +925,38 @@ int run_block_gr00t(oq_dit* h, int l, int t, float* r, hipStream_t st, int until
   const oq_dit_block& bw = h->blocks[l];
   const int64_t D = c.hidden, F = c.mlp;
   const float* s = &h->s_table[(static_cast<size_t>(l) * c.steps + t) * 4];
+  const SiteSet ss = site_set(h, l, t);
   uint16_t* h1 = at<uint16_t>(h, h->lay.h1);
   uint16_t* qkv = at<uint16_t>(h, h->lay.qkv);
   uint16_t* h2 = at<uint16_t>(h, h->lay.h2);
   uint16_t* ff = at<uint16_t>(h, h->lay.gu);
   uint16_t* act = at<uint16_t>(h, h->lay.act);
   int e;
-  if ((e = norm_rq(h, r, bw.g1, mod_ptr(h, l, t, 0), mod_ptr(h, l, t, 1), h1, s[0], st)) != OQ_OK) return e;
+  if ((e = norm_rq(h, r, bw.g1, mod_ptr(h, l, t, 0), mod_ptr(h, l, t, 1), h1, s[0], st, ss.d[0])) != OQ_OK) return e;
   if (until == 0) return OQ_OK;
   if (l % 2 == 0) {
     // Cross-attention to the conditioning k|v of this block ([B][P][2D]).
-    if ((e = gemm(h, bw.qkv, D, D, EPI_F16, qkv, D, nullptr, st)) != OQ_OK) return e;
+    if ((e = gemm(h, *ss.w[0], D, D, EPI_F16, qkv, D, nullptr, st)) != OQ_OK) return e;
     const int64_t MC = static_cast<int64_t>(c.batch) * c.prefix;
     const uint16_t* kv = at<uint16_t>(h, h->lay.ckv) + static_cast<int64_t>(l / 2) * MC * 2 * D;
-    if ((e = attention_rq(h, qkv, D, kv, kv + D, c.prefix, 2 * D, nullptr, nullptr, 0, 0, s[1], st)) != OQ_OK)
+    if ((e = attention_rq(h, qkv, D, kv, kv + D, c.prefix, 2 * D, nullptr, nullptr, 0, 0, s[1], st, ss.d[1])) !=
+        OQ_OK)
       return e;
   } else {
-    if ((e = gemm(h, bw.qkv, D, 3 * D, EPI_F16, qkv, 3 * D, nullptr, st)) != OQ_OK) return e;
-    if ((e = attention_rq(h, qkv, 3 * D, nullptr, nullptr, 0, 0, qkv + D, qkv + 2 * D, 3 * D, c.tokens, s[1],
-                          st)) != OQ_OK)
+    if ((e = gemm(h, *ss.w[0], D, 3 * D, EPI_F16, qkv, 3 * D, nullptr, st)) != OQ_OK) return e;
+    if ((e = attention_rq(h, qkv, 3 * D, nullptr, nullptr, 0, 0, qkv + D, qkv + 2 * D, 3 * D, c.tokens, s[1], st,
+                          ss.d[1])) != OQ_OK)
       return e;
   }
   if (until == 1) return OQ_OK;
-  if ((e = gemm(h, bw.o, D, D, EPI_RESID_F32, r, D, nullptr, st)) != OQ_OK) return e;
-  if ((e = norm_rq(h, r, bw.g2, nullptr, static_cast<const uint16_t*>(bw.b2), h2, s[2], st)) != OQ_OK) return e;
+  if ((e = gemm(h, *ss.w[1], D, D, EPI_RESID_F32, r, D, nullptr, st)) != OQ_OK) return e;
+  if ((e = norm_rq(h, r, bw.g2, nullptr, static_cast<const uint16_t*>(bw.b2), h2, s[2], st, ss.d[2])) != OQ_OK)
+    return e;
   if (until == 2) return OQ_OK;
-  if ((e = gemm(h, bw.gate_up, D, F, EPI_F16, ff, F, nullptr, st)) != OQ_OK) return e;
-  if ((e = gelu_rq(h, ff, act, s[3], st)) != OQ_OK) return e;
+  if ((e = gemm(h, *ss.w[2], D, F, EPI_F16, ff, F, nullptr, st)) != OQ_OK) return e;
+  if ((e = gelu_rq(h, ff, act, s[3], st, ss.d[3])) != OQ_OK) return e;
   if (until == 3) return OQ_OK;
-  return gemm(h, bw.down, F, D, EPI_RESID_F32, r, D, nullptr, st);
+  return gemm(h, *ss.w[3], F, D, EPI_RESID_F32, r, D, nullptr, st);
 }
 
 int run_block(oq_dit* h, int l, int t, float* r, hipStream_t st, int until = 4) {
@@ -1140,6 +1173,37 @@ extern "C" int oq_dit_run_block_until(oq_dit* h, int32_t l, int32_t t, float* re
   if (e != OQ_OK) return e;
   if (l < 0 || l >= h->cfg.n_blocks || t < 0 || t >= h->cfg.steps || site < 0 || site > 3) return OQ_ERR_ARG;
   return oq::run_block(h, l, t, resid, static_cast<hipStream_t>(stream), site);
+}
+
+extern "C" int oq_dit_set_static_steps(oq_dit* h, const float* delta, const oq_qweight* step_weights) {
+  if (!h) return OQ_ERR_NULL;
+  oq::drop_graphs(h);  // captured steps hold the previous tables and weights
+  if (!delta) {
+    h->static_delta = nullptr;
+    h->static_w.clear();
+    return OQ_OK;
+  }
+  if (!step_weights) return OQ_ERR_NULL;
+  if (!oq::aligned(delta, 16)) return OQ_ERR_ALIGN;
+  const size_t n = static_cast<size_t>(h->cfg.n_blocks) * h->cfg.steps * 4;
+  for (size_t i = 0; i < n; ++i) {
+    if (!step_weights[i].wq || !step_weights[i].w_scale) return OQ_ERR_NULL;
+    if (!oq::aligned(step_weights[i].wq, 16) || !oq::aligned(step_weights[i].w_scale, 4)) return OQ_ERR_ALIGN;
+  }
+  h->static_w.assign(step_weights, step_weights + n);
+  h->static_delta = delta;
+  return OQ_OK;
+}
+
+extern "C" int oq_dit_in_projection(oq_dit* h, const float* x, float* resid, void* stream) {
+  if (!h || !x || !resid) return OQ_ERR_NULL;
+  if (!oq::aligned(x, 4) || !oq::aligned(resid, 4)) return OQ_ERR_ALIGN;
+  const oq_dit_config& c = h->cfg;
+  const int64_t M = static_cast<int64_t>(c.batch) * c.tokens;
+  hipLaunchKernelGGL(oq::inproj_kernel, dim3(static_cast<unsigned>(M)), dim3(256), c.action_dim * sizeof(float),
+                     static_cast<hipStream_t>(stream), x, static_cast<const uint16_t*>(h->w.w_in),
+                     static_cast<const uint16_t*>(h->w.b_in), resid, c.action_dim, c.hidden);
+  return oq::launch_status();
 }
 
 extern "C" int oq_dit_get_intermediates(const oq_dit* h, oq_dit_intermediates* out) {

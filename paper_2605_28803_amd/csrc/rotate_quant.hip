@@ -51,13 +51,14 @@ __global__ __launch_bounds__(256) void rq_kernel(const uint16_t* __restrict__ X,
                                                  int64_t ldx, int logT, int logb, float s_t,
                                                  float s_over_sqrtb, uint8_t* __restrict__ Xq,
                                                  float* __restrict__ xs, float* __restrict__ ratio, bool tiled,
-                                                 const float* __restrict__ sdelta, bool rotate_only, bool i8) {
+                                                 const float* __restrict__ sdelta, bool rotate_only, bool i8,
+                                                 const float* __restrict__ cmul) {
   extern __shared__ float lds[];  // [rows_per_wg][K] when a row spans several waves
   __shared__ float red[4];
   const rqd::RowMap m = rqd::row_map(logT, M);
   float v[C][8];
   rqd::load_row_f16<C>(v, X, ldx, m);
-  rqd::rq_core<C>(v, m, K, logb, s_t, s_over_sqrtb, lds, red, Xq, xs, ratio, tiled, sdelta, rotate_only, i8);
+  rqd::rq_core<C>(v, m, K, logb, s_t, s_over_sqrtb, lds, red, Xq, xs, ratio, tiled, sdelta, rotate_only, i8, cmul);
 }
 
 // One row per wave (W = 1) or per workgroup (W > 1).
@@ -65,7 +66,8 @@ template <int NG, int W, bool FULL>
 __global__ __launch_bounds__(256) void rq_mfma_kernel(const uint16_t* __restrict__ X, int64_t M, int64_t ldx, int logb,
                                                       float s_t, float s_over_sqrtb, uint8_t* __restrict__ Xq,
                                                       float* __restrict__ xs, float* __restrict__ ratio, bool tiled,
-                                                      const float* __restrict__ sdelta, bool rotate_only, bool i8) {
+                                                      const float* __restrict__ sdelta, bool rotate_only, bool i8,
+                                                 const float* __restrict__ cmul) {
   // W > 1: [4 waves][NG groups][2 halves][64 lanes] float4 (consecutive lanes
   // hit consecutive 16-byte words: no bank conflicts on either side).
   extern __shared__ float4 xch[];
@@ -82,7 +84,7 @@ __global__ __launch_bounds__(256) void rq_mfma_kernel(const uint16_t* __restrict
   rqm::rv8h a1, a2;
   rqm::hadamard_frags(lane, a1, a2);
   rqm::rq_row<NG, W, FULL>(cur, a1, a2, row, valid, lane, wv, logb, s_t, s_over_sqrtb, Xq, xs, ratio, xch, red, tiled,
-                           sdelta, rotate_only, i8);
+                           sdelta, rotate_only, i8, cmul);
 }
 
 // (NG, W) of the matrix-core variant for K channels, or false.
@@ -102,7 +104,7 @@ bool rq_mfma_shape(int64_t K, int* ng, int* w) {
 
 int rq_mfma_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block, float s_t, uint8_t* Xq,
                    float* x_scale, float* ratio, hipStream_t stream, bool tiled, const float* sdelta,
-                   bool rotate_only, bool i8) {
+                   bool rotate_only, bool i8, const float* cmul) {
   int ng = 0, w = 0;
   rq_mfma_shape(K, &ng, &w);
   const int logb = ilog2(had_block);
@@ -116,10 +118,10 @@ int rq_mfma_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_blo
   if (ng == NG && w == W) {                                                                                   \
     if (had_block == K)                                                                                       \
       hipLaunchKernelGGL((rq_mfma_kernel<NG, W, true>), dim3(grid), dim3(256), lds, stream, x, M, ldx, logb,  \
-                         s_t, s_over_sqrtb, Xq, x_scale, ratio, tiled, sdelta, rotate_only, i8);              \
+                         s_t, s_over_sqrtb, Xq, x_scale, ratio, tiled, sdelta, rotate_only, i8, cmul);        \
     else                                                                                                      \
       hipLaunchKernelGGL((rq_mfma_kernel<NG, W, false>), dim3(grid), dim3(256), lds, stream, x, M, ldx, logb, \
-                         s_t, s_over_sqrtb, Xq, x_scale, ratio, tiled, sdelta, rotate_only, i8);              \
+                         s_t, s_over_sqrtb, Xq, x_scale, ratio, tiled, sdelta, rotate_only, i8, cmul);        \
     return launch_status();                                                                                   \
   }
   OQ_RQM(1, 1)
@@ -166,12 +168,12 @@ int rq_validate(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block,
 
 int rq_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block, float s_t, uint8_t* Xq,
               float* x_scale, float* ratio, hipStream_t stream, bool tiled, const float* sdelta,
-              bool rotate_only, bool i8) {
+              bool rotate_only, bool i8, const float* cmul) {
   if (M == 0) return OQ_OK;
   int ng = 0, w = 0;
   if (had_block >= 32 && rq_mfma_shape(K, &ng, &w))
     return rq_mfma_launch(X, M, K, ldx, had_block, s_t, Xq, x_scale, ratio, stream, tiled, sdelta, rotate_only,
-                          i8);
+                          i8, cmul);
   RQPlan p;
   rq_plan(K, &p);
   const int T = 1 << p.logT;
@@ -186,7 +188,7 @@ int rq_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block, f
   case CH:                                                                                             \
     hipLaunchKernelGGL(rq_kernel<CH>, dim3(static_cast<unsigned>(grid)), dim3(threads), lds, stream, x, \
                        M, static_cast<int>(K), ldx, p.logT, logb, s_t, s_over_sqrtb, Xq, x_scale, ratio, \
-                       tiled, sdelta, rotate_only, i8);                                                \
+                       tiled, sdelta, rotate_only, i8, cmul);                                          \
     break;
   switch (p.chunks) {
     OQ_RQ_CASE(1)
@@ -312,4 +314,15 @@ extern "C" int oq_rotate_quantize_act_i8(const void* X, int64_t M, int64_t K, in
   if ((st = oq::device_check()) != OQ_OK) return st;
   return oq::rq_launch(X, M, K, ldx, had_block, s, reinterpret_cast<uint8_t*>(Xq8), x_scale, nullptr,
                        static_cast<hipStream_t>(stream), false, nullptr, false, true);
+}
+
+extern "C" int oq_quantize_weights_step(const void* W_u, int64_t N, int64_t K, int64_t ldw, int32_t had_block,
+                                        const float* delta, uint8_t* Wq, float* w_scale, void* stream) {
+  int st = oq::rq_validate(W_u, N, K, ldw, had_block, Wq, w_scale);
+  if (st != OQ_OK || N == 0) return st;
+  if (!delta) return OQ_ERR_NULL;
+  if (!oq::aligned(delta, 16)) return OQ_ERR_ALIGN;
+  if ((st = oq::device_check()) != OQ_OK) return st;
+  return oq::rq_launch(W_u, N, K, ldw, had_block, 1.0f, Wq, w_scale, nullptr, static_cast<hipStream_t>(stream), false,
+                       nullptr, false, false, delta);
 }

@@ -209,13 +209,14 @@ __device__ __forceinline__ uint2 pack8_i8(const uint32_t (&b)[8]) {
 // sdelta[k] of channel k, token scale 1, see static_code); rotate_only
 // writes the normalized rotation s_t * y in fp32 to `ratio` and nothing else;
 // i8 quantizes to 8 bits (q_max = 127) and writes one byte per code, Xq
-// [M][K] row-major.
+// [M][K] row-major; cmul != nullptr multiplies channel k of the rotated row
+// by cmul[k] before the row maximum (the per-step weight fold W' diag(Delta)).
 template <int C>
 __device__ __forceinline__ void rq_core(float (&v)[C][8], const RowMap& m, int K, int logb, float s_t,
                                         float s_over_sqrtb, float* lds, float* red, uint8_t* __restrict__ Xq,
                                         float* __restrict__ xs, float* __restrict__ ratio, bool tiled = false,
                                         const float* __restrict__ sdelta = nullptr, bool rotate_only = false,
-                                        bool i8 = false) {
+                                        bool i8 = false, const float* __restrict__ cmul = nullptr) {
   // Bits 0..2: inside each 8-channel chunk.
 #pragma unroll
   for (int q = 0; q < 3; ++q) {
@@ -299,6 +300,16 @@ __device__ __forceinline__ void rq_core(float (&v)[C][8], const RowMap& m, int K
               v[c + h][j] = a - b;
             }
       }
+    }
+  }
+
+  if (cmul != nullptr) {
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      const float4* mp = reinterpret_cast<const float4*>(cmul + chan(m, c, 0));
+      const float4 a = mp[0], b = mp[1];
+      v[c][0] *= a.x; v[c][1] *= a.y; v[c][2] *= a.z; v[c][3] *= a.w;
+      v[c][4] *= b.x; v[c][5] *= b.y; v[c][6] *= b.z; v[c][7] *= b.w;
     }
   }
 

@@ -72,14 +72,15 @@ __device__ __forceinline__ int chan0(int wr, int g, int lane) {
 // synchronizes when W > 1 (xch: [4][NG][2][64] float4 of LDS), and `red` is
 // a 4-float shared array.  sdelta / rotate_only: the static per-channel
 // quantizer and the fp32 rotation output, as in rqd::rq_core; i8: 8-bit codes
-// (q_max = 127), one byte per code in [M][K].
+// (q_max = 127), one byte per code in [M][K]; cmul: per-channel multiplier
+// before the row maximum, as in rqd::rq_core.
 template <int NG, int W, bool FULL>
 __device__ __forceinline__ void rq_row(const rv8h (&cur)[NG], const rv8h& a1, const rv8h& a2, int64_t row, bool valid,
                                        int lane, int wv, int logb, float s_t, float s_over_sqrtb,
                                        uint8_t* __restrict__ Xq, float* __restrict__ xs, float* __restrict__ ratio,
                                        float4* xch, float* red, bool tiled,
                                        const float* __restrict__ sdelta = nullptr, bool rotate_only = false,
-                                       bool i8 = false) {
+                                       bool i8 = false, const float* __restrict__ cmul = nullptr) {
   using S = Shape<NG, W>;
   constexpr int K = S::K, LOGNG = S::LOGNG, LOGW = S::LOGW, GW = S::GW;
   const int rsub = wv / W, wr = wv % W;
@@ -164,6 +165,15 @@ __device__ __forceinline__ void rq_row(const rv8h (&cur)[NG], const rv8h& a1, co
   }
 
   auto group_of = [&](int s) { return xpose ? (s % W) * NG + wr * GW + s / W : wr * NG + s; };
+  if (cmul != nullptr) {  // per-channel multiplier before the row maximum (the per-step weight fold)
+#pragma unroll
+    for (int s = 0; s < NG; ++s) {
+      const float4* mp = reinterpret_cast<const float4*>(cmul + (group_of(s) * 16 + cl) * 32 + 8 * q);
+      const float4 a = mp[0], b = mp[1];
+      v[s][0] *= a.x; v[s][1] *= a.y; v[s][2] *= a.z; v[s][3] *= a.w;
+      v[s][4] *= b.x; v[s][5] *= b.y; v[s][6] *= b.z; v[s][7] *= b.w;
+    }
+  }
   // Rotation only, or the static quantizer: no row maximum (uniform branch;
   // no barrier follows).
   if (rotate_only) {

@@ -204,6 +204,112 @@ class DiT:
             out["cond_kv"] = view(it.cond_kv, nc * self.MC * 2 * D, np.float16, (nc, self.MC, 2 * D))
         return out
 
+    # ------------------------------------------------------------------
+    # Static per-step, per-channel steps (the per-(layer, step, channel)
+    # table of eq:perstep_scale): calibration rollouts and the driver's
+    # static mode.  Every computation runs in the library's kernels.
+    # ------------------------------------------------------------------
+
+    SITE_WEIGHTS = {"pi": (("wqkv",), ("wo",), ("wgu",), ("wd",)),
+                    "gr00t": (("wq", "wqkv"), ("wo",), ("wff0",), ("wff2",))}
+
+    def site_inputs(self):
+        """Device fp16 views of the four quantization sites' inputs of the
+        last block run: h1 [M, D], attn [M, D], h2 [M, D], act [M, F]."""
+        from . import _check
+        it = _lib.oq_dit_intermediates()
+        _check(self.lib.oq_dit_get_intermediates(self.handle, C.byref(it)), "oq_dit_get_intermediates")
+        D, F, M = self.cfg_c.hidden, self.cfg_c.mlp, self.M
+        base = self.workspace.data_ptr()
+        views = []
+        for ptr, K in ((it.h1, D), (it.attn, D), (it.h2, D), (it.act, F)):
+            off = ptr - base
+            views.append(self.workspace[off: off + 2 * M * K].view(torch.float16).view(M, K))
+        return views
+
+    def in_projection(self, x, resid=None, stream=None):
+        """resid fp32 [M, D] = x W_in^T + b_in for the state x (fp32 [B, S, A])."""
+        from . import _check
+        if resid is None:
+            resid = torch.empty((self.M, self.cfg_c.hidden), dtype=torch.float32, device=self.device)
+        _check(self.lib.oq_dit_in_projection(self.handle, x.data_ptr(), resid.data_ptr(), self._stream(stream)),
+               "oq_dit_in_projection")
+        return resid
+
+    def site_dims(self):
+        D, F = self.cfg_c.hidden, self.cfg_c.mlp
+        return (D, D, D, F), (0, D, 2 * D, 3 * D), 3 * D + F
+
+    def calibrate_static_steps(self, x0s, p=99.9, samples=False):
+        """Calibration rollouts from the initial states x0s (fp32 device
+        tensors [B, S, A]) with the handle's per-token quantizer: at every
+        step t and block l, each site's fp16 input is rotated (fp32) and
+        collected; the step table is then the nearest-rank p-th percentile of
+        the collected magnitudes per channel over q_max = 7.  Returns the
+        device table fp32 [L, T, 3D + F] (and the collected rows per
+        (l, t, site) if samples)."""
+        from . import calibrate_step_scales, calibrate_workspace_bytes, rotate_act_f32
+        L, T, M = self.cfg_c.n_blocks, self.cfg_c.steps, self.M
+        Ks, offs, width = self.site_dims()
+        n = len(x0s)
+        dev = self.device
+        Y = {(l, t, i): torch.empty((n * M, Ks[i]), dtype=torch.float32, device=dev)
+             for l in range(L) for t in range(T) for i in range(4)}
+        r = torch.empty((M, self.cfg_c.hidden), dtype=torch.float32, device=dev)
+        for j, x0 in enumerate(x0s):
+            x = x0.clone()
+            for t in range(T):
+                self.in_projection(x, r)
+                for l in range(L):
+                    self.run_block(l, t, r)
+                    for i, xin in enumerate(self.site_inputs()):
+                        rotate_act_f32(xin, _pow2_divisor(Ks[i]), Y=Y[(l, t, i)][j * M:(j + 1) * M])
+                self.step(x, t)
+        table = torch.empty((L, T, width), dtype=torch.float32, device=dev)
+        work = torch.empty((calibrate_workspace_bytes(max(Ks)),), dtype=torch.uint8, device=dev)
+        for (l, t, i), y in Y.items():
+            calibrate_step_scales(y, p, 7.0, delta=table[l, t, offs[i]:offs[i] + Ks[i]], work=work)
+        torch.cuda.synchronize(dev)
+        return (table, Y) if samples else table
+
+    def set_static_steps(self, inp, table):
+        """Fold every block linear with its step rows on the device
+        (oq_quantize_weights_step, one weight copy per (block, step)) and put
+        the handle into the static mode with the table (fp32 device [L, T,
+        3D + F], kept referenced)."""
+        from . import _check, quantize_weights_step
+        L, T = self.cfg_c.n_blocks, self.cfg_c.steps
+        Ks, offs, _ = self.site_dims()
+        names = self.SITE_WEIGHTS[self.arch]
+        arr = (_lib.oq_qweight * (L * T * 4))()
+        folded = []
+        for l in range(L):
+            bw = inp["w"]["blocks"][l]
+            for i in range(4):
+                nm = next(n for n in names[i] if n in bw)
+                W = torch.from_numpy(np.ascontiguousarray(bw[nm], dtype=np.float16)).to(self.device)
+                for t in range(T):
+                    Wq, ws = quantize_weights_step(W, _pow2_divisor(Ks[i]), table[l, t, offs[i]:offs[i] + Ks[i]])
+                    folded.append((Wq, ws))
+                    arr[(l * T + t) * 4 + i] = _lib.oq_qweight(Wq.data_ptr(), ws.data_ptr())
+                del W
+        _check(self.lib.oq_dit_set_static_steps(self.handle, C.c_void_p(table.data_ptr()), arr),
+               "oq_dit_set_static_steps")
+        self._static = (table, folded, arr)
+        torch.cuda.synchronize(self.device)
+        return folded
+
+    def static_weight(self, l, t, site):
+        """(Wq, w_scale) device tensors of the folded linear of (block, step, site)."""
+        T = self.cfg_c.steps
+        order = [(ll, i, tt) for ll in range(self.cfg_c.n_blocks) for i in range(4) for tt in range(T)]
+        return self._static[1][order.index((l, site, t))]
+
+    def clear_static_steps(self):
+        from . import _check
+        _check(self.lib.oq_dit_set_static_steps(self.handle, None, None), "oq_dit_set_static_steps")
+        self._static = None
+
     def close(self):
         if getattr(self, "handle", None):
             self.lib.oq_dit_destroy(self.handle)

@@ -90,6 +90,24 @@ def tau_static(x: np.ndarray, b: int, delta: np.ndarray, r_ref: np.ndarray) -> n
     return np.where(ok[None, :], t, 0.0)
 
 
+def tau_rows_scaled(x: np.ndarray, b: int, cm: np.ndarray) -> np.ndarray:
+    """Per-row bound for the per-row quantizer of the rotated row scaled by
+    cm per channel (the per-step weight fold): the fp32 butterfly error
+    gamma_d l1 of each channel's block, times cm_j, relative to the row
+    maximum of |u cm|, plus one more rounding (the product by cm) on top of
+    the per-token kernel's 21 * 2^-24."""
+    x = np.asarray(x, dtype=np.float64)
+    cm = np.asarray(cm, dtype=np.float64)
+    M, K = x.shape
+    d = int(np.log2(b)) + 32
+    gamma = d * U32 / (1 - d * U32)
+    l1 = block_l1(x, b) * cm[None, :]
+    from oracle.hadamard import fwht
+    umax = np.abs(fwht(x, b) * cm[None, :]).max(axis=1) * np.sqrt(b)
+    safe = np.where(umax > 0, umax, 1.0)
+    return np.where(umax > 0, 14 * gamma * l1.max(axis=1) / safe + 28 * U32, 0.0)
+
+
 def dist_to_boundary(r: np.ndarray) -> np.ndarray:
     """Distance of each ratio to the nearest half integer."""
     return np.abs(np.abs(r - np.floor(r)) - 0.5)

@@ -179,3 +179,21 @@ def test_static_linear(M, N, K, b):
     print(f"static linear rel_l2 vs oracle {err:.2e}, vs float linear {qual:.3f}")
     assert err <= parity.REL_L2_OUT
     assert np.isfinite(qual) and qual < 1.0
+
+
+@pytest.mark.parametrize("N,K,b", [(96, 1024, 1024), (3072, 1024, 1024), (1024, 4096, 4096), (200, 1536, 512),
+                                   (33, 256, 8)])
+def test_quantize_weights_step_device(N, K, b):
+    """The device fold W' diag(Delta) + RTN against the oracle's fold of the
+    same fp16 weight: codes by the boundary rule, scales to the fp32 bound."""
+    print(f"weight step fold N={N} K={K} b={b}", flush=True)
+    rng = np.random.default_rng(N + K)
+    w16 = (rng.standard_normal((N, K)) * 0.02).astype(np.float16)
+    d = np.exp(rng.standard_normal(K) * 0.5).astype(np.float32)
+    d[rng.choice(K, 2, replace=False)] = 0.0
+    Wq, ws = oq.quantize_weights_step(torch.from_numpy(w16).to(DEV), b, torch.from_numpy(d).to(DEV))
+    torch.cuda.synchronize()
+    qo, wso, ro = quant.fold_weights_step(w16.astype(np.float64), b, d.astype(np.float64))
+    tau = parity.tau_rows_scaled(w16, b, d)
+    parity.check_codes(parity.unpack_int4(Wq.cpu().numpy()), qo, ro, tau)
+    assert np.allclose(ws.cpu().numpy(), wso, rtol=1e-5, atol=0)

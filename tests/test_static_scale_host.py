@@ -72,3 +72,15 @@ def test_static_calls_reject_bad_arguments():
     assert h(w.ctypes.data, 1, 8, 8, None, out.ctypes.data, sc.ctypes.data) == NULL
     assert h(w.ctypes.data, 1, 8, 8, bad.ctypes.data, out.ctypes.data, sc.ctypes.data) == ARG
     assert h(w.ctypes.data, 1, 8, 8, nan.ctypes.data, out.ctypes.data, sc.ctypes.data) == ARG
+
+
+def test_step_fold_device_and_dit_static_calls_reject_bad_arguments():
+    lib = _lib.load()
+    f = lib.oq_quantize_weights_step
+    assert f(P16, 4, 1024, 1024, 1024, None, P16, P16, None) == NULL      # delta
+    assert f(P16, 4, 1024, 1024, 1024, P4, P16, P16, None) == ALIGN       # delta 16-byte
+    assert f(P16, 4, 1024, 1000, 1024, P16, P16, P16, None) == SHAPE      # ldw < K
+    assert f(None, 0, 1024, 1024, 1024, None, None, None, None) == OK     # no rows
+    s = lib.oq_dit_set_static_steps
+    assert s(None, P16, None) == NULL
+    assert lib.oq_dit_in_projection(None, P16, P16, None) == NULL
