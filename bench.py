@@ -600,6 +600,54 @@ def pi_step_without_graph(cfg, inp, steps=20):
     return s.elapsed_time(e) / steps
 
 
+def dit_static_step(cfg, inp, model, n_traj=4, steps=50):
+    """The Pi-0.5 step with the paper-literal static per-step, per-channel
+    steps: calibration rollouts (n_traj seeded synthetic initial states, all
+    10 denoising steps, every block and site), the per-(block, step) weight
+    folds on the device, then the step timed as the main line (graph replay,
+    t cycling) -- ten weight copies per block, so the step's weights are no
+    longer MALL-resident across steps.  Also reports how far a full
+    10-step denoise moves from the per-token driver's (relative L2, not a
+    parity figure: both are quantized models)."""
+    import torch
+    from workloads import generators as G
+    stream = torch.cuda.current_stream()
+    x0s = [torch.from_numpy(G.gaussian(900 + j, "calib/x0", inp["x0"].shape).astype(np.float32)).cuda()
+           for j in range(n_traj)]
+    t0 = time.perf_counter()
+    table = model.calibrate_static_steps(x0s)
+    t_cal = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    model.set_static_steps(inp, table)
+    t_fold = time.perf_counter() - t0
+    x = torch.from_numpy(inp["x0"].astype(np.float32)).cuda()
+    for k in range(10):
+        model.step(x, k % cfg.steps, stream=stream)
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for k in range(steps):
+        model.step(x, k % cfg.steps, stream=stream)
+    end.record(stream)
+    end.synchronize()
+    ms = start.elapsed_time(end) / steps
+    xs = torch.from_numpy(inp["x0"].astype(np.float32)).cuda()
+    model.denoise(xs, cfg.steps, stream=stream)
+    model.clear_static_steps()
+    xt = torch.from_numpy(inp["x0"].astype(np.float32)).cuda()
+    model.denoise(xt, cfg.steps, stream=stream)
+    torch.cuda.synchronize()
+    x0 = torch.from_numpy(inp["x0"].astype(np.float32)).cuda()
+    dev = float(torch.linalg.norm(xs - xt) / torch.linalg.norm(xt - x0))
+    del table
+    torch.cuda.empty_cache()
+    return {"step_us": round(ms * 1e3, 2), "steps_per_s": round(1000.0 / ms, 1),
+            "calibration_s": round(t_cal, 2), "calibration_trajectories": n_traj,
+            "weight_folds_s": round(t_fold, 2), "folded_weight_copies": cfg.n_blocks * cfg.steps * 4,
+            "denoise_vs_per_token_rel_l2": round(dev, 4)}
+
+
 def run_dit(args):
     import torch
     import paper_2605_28803_amd as oq
@@ -679,6 +727,8 @@ def run_dit(args):
         line["static_step_scales"] = static_scale_kernels()
         line["w4a8"] = w4a8_kernels()
         line["weight_preparation"] = prepare_kernels()
+        print("[bench] static per-step steps (calibration + step)", file=sys.stderr, flush=True)
+        line["dit_static_steps"] = dit_static_step(cfg, inp, model)
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle sample)", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(cfg, inp)
