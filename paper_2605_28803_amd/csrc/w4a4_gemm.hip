@@ -16,11 +16,13 @@
 // are stored even-channels-first; A and B use the same order, so the dot
 // products are unchanged.
 //
-// Tiling: 128 x 128 output tile per 256-thread workgroup, 2 x 2 waves of
-// 64 x 64 (2 x 2 MFMA blocks of 32 x 32), K step 64 codes, two LDS buffers
-// (global loads of step k+1 are in flight while step k runs on the matrix
-// cores).  LDS rows are padded to 80 bytes so the 16-byte fragment reads of 16
-// consecutive rows hit disjoint banks.
+// Two kernels.  M > 64: LDS-staged tiles of 256 x 256, 128 x 128 or 64 x 64
+// outputs on v_mfma_i32_32x32x32_i8, the largest tile that still gives every
+// CU a workgroup (details at gemm_big_kernel).  M <= 64 (and token codes in
+// the 16-row tiled layout): a weight-streaming kernel on
+// v_mfma_i32_16x16x64_i8 with the operands loaded straight into registers
+// (details at gemm_small_kernel).  8-bit token codes (W4A8) use both with
+// the A operand loaded as bytes.
 #include "common.h"
 
 namespace oq {
@@ -669,13 +671,17 @@ int gemm_launch(const GemmArgs& a, Epilogue epi, hipStream_t stream) {
   }
   // Large problems: 256 x 256 tiles (8 waves of 128 x 64) when they still
   // fill every CU, else 128 x 128 tiles (4 waves of 64 x 64, two workgroups
-  // per CU).
+  // per CU), else 64 x 64 tiles (2 waves of 64 x 32, four workgroups per CU).
   // 8-bit token codes double the A register ring, which the 256 x 256 tile
   // cannot hold without spilling: they always take the 128 x 128 tile.
   const int64_t big_tiles = ((a.M + 255) / 256) * ((a.N + 255) / 256);
   if (big_tiles >= 256 && !a.a_i8) return launch_big<2, 4, 4, 2>(a, epi, big_tiles, stream);
   const int64_t mid_tiles = ((a.M + 127) / 128) * ((a.N + 127) / 128);
-  return launch_big<2, 2, 2, 2>(a, epi, mid_tiles, stream);
+  if (mid_tiles >= 256) return launch_big<2, 2, 2, 2>(a, epi, mid_tiles, stream);
+  // Fewer 128 x 128 tiles than CUs (prefill-sized M with N ~ 2048): 64 x 64
+  // tiles of two waves (64 x 32 each), several workgroups per CU.
+  const int64_t small_tiles = ((a.M + 63) / 64) * ((a.N + 63) / 64);
+  return launch_big<1, 2, 2, 1>(a, epi, small_tiles, stream);
 }
 
 }  // namespace oq
