@@ -68,8 +68,8 @@ __global__ __launch_bounds__(256) void rq_mfma_kernel(const uint16_t* __restrict
                                                       float* __restrict__ xs, float* __restrict__ ratio, bool tiled,
                                                       const float* __restrict__ sdelta, bool rotate_only, bool i8,
                                                  const float* __restrict__ cmul) {
-  // W > 1: [4 waves][NG groups][2 halves][64 lanes] float4 (consecutive lanes
-  // hit consecutive 16-byte words: no bank conflicts on either side).
+  // W > 1: [4 waves][NG groups][2 halves][32 lanes] float4, one half of the
+  // lanes at a time (consecutive lanes hit consecutive 16-byte words).
   extern __shared__ float4 xch[];
   __shared__ float red[4];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
@@ -110,7 +110,7 @@ int rq_mfma_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_blo
   const int logb = ilog2(had_block);
   const float s_over_sqrtb = static_cast<float>(static_cast<double>(s_t) / std::sqrt(static_cast<double>(had_block)));
   const int rpb = 4 / w;
-  const size_t lds = w > 1 ? static_cast<size_t>(4) * ng * 128 * sizeof(float4) : 0;
+  const size_t lds = w > 1 ? static_cast<size_t>(4) * ng * 64 * sizeof(float4) : 0;
   // One row per wave (W = 1) or per workgroup (W > 1).
   const unsigned grid = static_cast<unsigned>((M + rpb - 1) / rpb);
   const uint16_t* x = static_cast<const uint16_t*>(X);

@@ -69,7 +69,7 @@ __device__ __forceinline__ int chan0(int wr, int g, int lane) {
 // remaining butterflies, the row maximum, the scale and the codes (or, with
 // ratio != nullptr, the fp32 ratios z / Delta).  cur[g] holds channels
 // chan0(wr, g, lane) .. + 7.  Every wave of the workgroup calls it: it
-// synchronizes when W > 1 (xch: [4][NG][2][64] float4 of LDS), and `red` is
+// synchronizes when W > 1 (xch: [4][NG][2][32] float4 of LDS), and `red` is
 // a 4-float shared array.  sdelta / rotate_only: the static per-channel
 // quantizer and the fp32 rotation output, as in rqd::rq_core; i8: 8-bit codes
 // (q_max = 127), one byte per code in [M][K]; cmul: per-channel multiplier
@@ -128,23 +128,36 @@ __device__ __forceinline__ void rq_row(const rv8h (&cur)[NG], const rv8h& a1, co
   const bool xpose = W > 1 && need(wbit0);
   if constexpr (W > 1) {
     if (xpose) {
-      float4* mine = xch + static_cast<int64_t>(wv) * NG * 128 + lane;
+      // Two rounds, one per half of the lanes: the transpose only moves a
+      // value between waves at the same lane, so each round needs half the
+      // LDS (more workgroups per CU) and a lane overwrites only its own
+      // registers after its own values are written.
+      const int lh = lane & 31;
 #pragma unroll
-      for (int g = 0; g < NG; ++g) {
-        mine[g * 128] = make_float4(v[g][0], v[g][1], v[g][2], v[g][3]);
-        mine[g * 128 + 64] = make_float4(v[g][4], v[g][5], v[g][6], v[g][7]);
-      }
-      __syncthreads();
+      for (int half = 0; half < 2; ++half) {
+        if ((lane >> 5) == half) {
+          float4* mine = xch + static_cast<int64_t>(wv) * NG * 64 + lh;
 #pragma unroll
-      for (int gi = 0; gi < GW; ++gi)
-#pragma unroll
-        for (int u = 0; u < W; ++u) {
-          const float4* src = xch + static_cast<int64_t>((rsub * W + u) * NG + wr * GW + gi) * 128 + lane;
-          const float4 p0 = src[0], p1 = src[64];
-          float* d = v[gi * W + u];
-          d[0] = p0.x; d[1] = p0.y; d[2] = p0.z; d[3] = p0.w;
-          d[4] = p1.x; d[5] = p1.y; d[6] = p1.z; d[7] = p1.w;
+          for (int g = 0; g < NG; ++g) {
+            mine[g * 64] = make_float4(v[g][0], v[g][1], v[g][2], v[g][3]);
+            mine[g * 64 + 32] = make_float4(v[g][4], v[g][5], v[g][6], v[g][7]);
+          }
         }
+        __syncthreads();
+        if ((lane >> 5) == half) {
+#pragma unroll
+          for (int gi = 0; gi < GW; ++gi)
+#pragma unroll
+            for (int u = 0; u < W; ++u) {
+              const float4* src = xch + static_cast<int64_t>((rsub * W + u) * NG + wr * GW + gi) * 64 + lh;
+              const float4 p0 = src[0], p1 = src[32];
+              float* d = v[gi * W + u];
+              d[0] = p0.x; d[1] = p0.y; d[2] = p0.z; d[3] = p0.w;
+              d[4] = p1.x; d[5] = p1.y; d[6] = p1.z; d[7] = p1.w;
+            }
+        }
+        __syncthreads();
+      }
       // Wave bits in registers: slot bits 0 .. log2(W) - 1 are u.
 #pragma unroll
       for (int t = 0; t < LOGW; ++t) {
