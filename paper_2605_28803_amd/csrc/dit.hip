@@ -426,6 +426,178 @@ __global__ __launch_bounds__(64 * WAVES) void attn_partial_kernel(AttnArgs a) {
   }
 }
 
+// Conditioning k|v rows [B*P][2D] (head h at columns h*hd of each half)
+// rewritten head-major, [B][H][2][P][hd], so that the cross-attention of one
+// (sample, head) reads its keys and values as two contiguous blocks.  One
+// thread per 16-byte piece (hd % 8 == 0).
+__global__ __launch_bounds__(256) void kv_head_major_kernel(const uint16_t* __restrict__ rows,
+                                                            uint16_t* __restrict__ hm, int64_t B, int P, int H,
+                                                            int hd) {
+  const int64_t D = static_cast<int64_t>(H) * hd;
+  const int64_t pieces = B * P * 2 * D / 8;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= pieces) return;
+  const int64_t row = i / (2 * D / 8), c = (i % (2 * D / 8)) * 8;  // row b * P + p, column c of 2D
+  const int64_t b = row / P, p = row % P;
+  const int64_t half = c / D, h = (c % D) / hd, d = (c % D) % hd;
+  const uint4 v = *reinterpret_cast<const uint4*>(rows + row * 2 * D + c);
+  *reinterpret_cast<uint4*>(hm + (((b * H + h) * 2 + half) * P + p) * hd + d) = v;
+}
+
+// Cross-attention of one (sample b, head h) over all P conditioning keys,
+// read head-major (K then V blocks of P x hd).  The keys are taken 64 at a
+// time with the same matrix-core steps as attn_partial_kernel, and the
+// splits are merged on the fly (running maximum m, sum l and output O per
+// query row, rescaled by e^{m_old - m_new}); the normalized output is written
+// as fp16 to its head's columns of `out`.  WAVES = ceil(S / 16).
+template <int WAVES, int HD>
+__global__ __launch_bounds__(64 * WAVES) void attn_cross_kernel(const uint16_t* __restrict__ q, int64_t q_ld,
+                                                                const uint16_t* __restrict__ kvh, int P, int S,
+                                                                int H, float scale, uint16_t* __restrict__ out,
+                                                                int64_t out_ld) {
+  constexpr int KS = kAttnKS;
+  constexpr int PAD = KS + 8;
+  static_assert(HD % 16 == 0 && HD <= kMaxHeadDim, "head_dim");
+  constexpr int KK = (HD + 31) / 32;               // 32-wide k steps of q.k (zero-padded)
+  constexpr int VIT = (HD + 8 * WAVES - 1) / (8 * WAVES);
+  __shared__ __attribute__((aligned(16))) uint16_t sVt[HD][PAD];
+  __shared__ __attribute__((aligned(16))) uint16_t sP[WAVES][16][PAD];
+  const int bh = blockIdx.x;
+  const int b = bh / H, h = bh % H;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  __builtin_assume(tid < 64 * WAVES);
+  const uint16_t* kb_base = kvh + static_cast<int64_t>(bh) * 2 * P * HD;
+  const uint16_t* vb_base = kb_base + static_cast<int64_t>(P) * HD;
+  const int qrow = 16 * w + (lane & 15);
+  const bool qok = qrow < S;
+  const int kq = 8 * (lane >> 4);
+  const uint16_t* qp = q + (static_cast<int64_t>(b) * S + (qok ? qrow : 0)) * q_ld + h * HD;
+  v8h qa[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    const bool dok = kk * 32 + kq < HD;
+    const v8h raw = *reinterpret_cast<const v8h*>(qp + (dok ? kk * 32 + kq : 0));
+    qa[kk] = (dok && qok) ? raw : v8h{};
+  }
+  float m[4], l[4];
+  v4f o[HD / 16];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    m[e] = -INFINITY;
+    l[e] = 0.0f;
+  }
+#pragma unroll
+  for (int nb = 0; nb < HD / 16; ++nb) o[nb] = v4f{0, 0, 0, 0};
+
+  const int nsplit = (P + KS - 1) / KS;
+  for (int sp = 0; sp < nsplit; ++sp) {
+    const int k0 = sp * KS;
+    const int nk = min(KS, P - k0);
+    // Loads first (clamped rows; values of keys past P are masked at use).
+    const int vj = tid & 63;
+    const bool vjok = vj < nk;
+    uint4 vraw[VIT];
+    {
+      const uint16_t* vp = vb_base + static_cast<int64_t>(k0 + (vjok ? vj : 0)) * HD;
+#pragma unroll
+      for (int i = 0; i < VIT; ++i) {
+        const int d8 = w * 8 + i * 8 * WAVES;
+        vraw[i] = *reinterpret_cast<const uint4*>(vp + (d8 < HD ? d8 : 0));
+      }
+    }
+    v8h kraw[KK][KS / 16];
+    bool kok[KS / 16];
+#pragma unroll
+    for (int nb = 0; nb < KS / 16; ++nb) {
+      const int j = nb * 16 + (lane & 15);
+      kok[nb] = j < nk;
+      const uint16_t* kp = kb_base + static_cast<int64_t>(k0 + (kok[nb] ? j : 0)) * HD;
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        const bool dok = kk * 32 + kq < HD;
+        kraw[kk][nb] = *reinterpret_cast<const v8h*>(kp + (dok ? kk * 32 + kq : 0));
+      }
+    }
+    __syncthreads();  // the previous split's P and V^T reads are done
+#pragma unroll
+    for (int i = 0; i < VIT; ++i) {
+      const int d8 = w * 8 + i * 8 * WAVES;
+      if (d8 < HD) {
+        const uint32_t wv[4] = {vjok ? vraw[i].x : 0u, vjok ? vraw[i].y : 0u, vjok ? vraw[i].z : 0u,
+                                vjok ? vraw[i].w : 0u};
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          sVt[d8 + 2 * t][vj] = static_cast<uint16_t>(wv[t] & 0xFFFFu);
+          sVt[d8 + 2 * t + 1][vj] = static_cast<uint16_t>(wv[t] >> 16);
+        }
+      }
+    }
+    v4f sc[KS / 16];
+#pragma unroll
+    for (int nb = 0; nb < KS / 16; ++nb) {
+      sc[nb] = v4f{0, 0, 0, 0};
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        const bool dok = kk * 32 + kq < HD;
+        const v8h kb = (dok && kok[nb]) ? kraw[kk][nb] : v8h{};
+        sc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(qa[kk], kb, sc[nb], 0, 0, 0);
+      }
+    }
+    // Running softmax per row 4 (lane / 16) + e.
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int nb = 0; nb < KS / 16; ++nb) {
+        const int j = nb * 16 + (lane & 15);
+        const float v = j < nk ? sc[nb][e] * scale : -INFINITY;
+        sc[nb][e] = v;
+        mx = fmaxf(mx, v);
+      }
+      mx = fmaxf(mx, rqd::lane_xor<1>(mx));
+      mx = fmaxf(mx, rqd::lane_xor<2>(mx));
+      mx = fmaxf(mx, rqd::lane_xor<4>(mx));
+      mx = fmaxf(mx, rqd::lane_xor<8>(mx));
+      const float mn = fmaxf(m[e], mx);
+      const float alpha = __expf(m[e] - mn);  // 0 on the first split (m = -inf)
+      float sum = 0.0f;
+#pragma unroll
+      for (int nb = 0; nb < KS / 16; ++nb) {
+        const float pv = __expf(sc[nb][e] - mn);
+        sum += pv;
+        sP[w][4 * (lane >> 4) + e][nb * 16 + (lane & 15)] = f2h(pv);
+      }
+      sum += rqd::lane_xor<1>(sum);
+      sum += rqd::lane_xor<2>(sum);
+      sum += rqd::lane_xor<4>(sum);
+      sum += rqd::lane_xor<8>(sum);
+      l[e] = l[e] * alpha + sum;
+      m[e] = mn;
+#pragma unroll
+      for (int nb = 0; nb < HD / 16; ++nb) o[nb][e] *= alpha;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int nb = 0; nb < HD / 16; ++nb) {
+#pragma unroll
+      for (int ks = 0; ks < KS / 32; ++ks) {
+        const v8h pa = *reinterpret_cast<const v8h*>(&sP[w][lane & 15][ks * 32 + kq]);
+        const v8h vb = *reinterpret_cast<const v8h*>(&sVt[nb * 16 + (lane & 15)][ks * 32 + kq]);
+        o[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(pa, vb, o[nb], 0, 0, 0);
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int row = 16 * w + 4 * (lane >> 4) + e;
+    if (row >= S) continue;
+    const float inv = 1.0f / l[e];
+    uint16_t* orow = out + (static_cast<int64_t>(b) * S + row) * out_ld + h * HD;
+#pragma unroll
+    for (int nb = 0; nb < HD / 16; ++nb) orow[nb * 16 + (lane & 15)] = f2h(o[nb][e] * inv);
+  }
+}
+
 // Token row (b, s): out = sum_s e^{m_s - M} o_s / sum_s e^{m_s - M} l_s per
 // head, rounded to fp16, then rotate + quantize the row.
 template <int C>
@@ -607,7 +779,7 @@ bool is_gr00t(const oq_dit_config& c) { return c.arch == OQ_DIT_GR00T; }
 int n_cross(const oq_dit_config& c) { return is_gr00t(c) ? (c.n_blocks + 1) / 2 : 0; }
 
 struct Layout {
-  size_t r, h1, qkv, o, h2, gu, act, xq, xs, part_o, part_ml, ckv, total;
+  size_t r, h1, qkv, o, h2, gu, act, xq, xs, part_o, part_ml, ckv, ckvh, total;
 };
 
 Layout layout_for(const oq_dit_config& c) {
@@ -634,6 +806,7 @@ Layout layout_for(const oq_dit_config& c) {
   L.part_o = off; off += align256(BH * nsplit * c.tokens * c.head_dim * 4);
   L.part_ml = off; off += align256(BH * nsplit * c.tokens * 2 * 4);
   L.ckv = off; off += align256(static_cast<size_t>(n_cross(c)) * MC * 2 * D * 2);
+  L.ckvh = off; off += align256(static_cast<size_t>(n_cross(c)) * MC * 2 * D * 2);  // the same, head-major
   L.total = off;
   return L;
 }
@@ -867,6 +1040,52 @@ int attention_rq(oq_dit* h, const uint16_t* q, int64_t q_ld, const uint16_t* k_p
   return ok ? launch_status() : OQ_ERR_SHAPE;
 }
 
+// gr00t cross-attention of block l over the head-major conditioning k|v,
+// then the o linear's rotate-quantize of the fp16 output rows.
+int cross_attention_rq(oq_dit* h, const uint16_t* q, int64_t q_ld, int l, float s, hipStream_t st,
+                       const float* sdelta) {
+  const oq_dit_config& c = h->cfg;
+  const int64_t M = static_cast<int64_t>(c.batch) * c.tokens;
+  const int64_t D = c.hidden;
+  const int64_t MC = static_cast<int64_t>(c.batch) * c.prefix;
+  const uint16_t* kvh = at<uint16_t>(h, h->lay.ckvh) + static_cast<int64_t>(l / 2) * MC * 2 * D;
+  uint16_t* out = at<uint16_t>(h, h->lay.o);
+  const float scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(c.head_dim)));
+  const unsigned waves = static_cast<unsigned>((c.tokens + 15) / 16);
+  const dim3 grid(static_cast<unsigned>(c.batch * c.n_heads));
+  auto launch = [&](auto W, auto HDc) {
+    constexpr int WV = decltype(W)::value, HD = decltype(HDc)::value;
+    hipLaunchKernelGGL((attn_cross_kernel<WV, HD>), grid, dim3(64 * WV), 0, st, q, q_ld, kvh, c.prefix,
+                       c.tokens, c.n_heads, scale, out, D);
+  };
+  auto by_hd = [&](auto W) {
+    switch (c.head_dim) {  // every multiple of 16 up to kMaxHeadDim (validate_config)
+      case 16: launch(W, std::integral_constant<int, 16>{}); return true;
+      case 32: launch(W, std::integral_constant<int, 32>{}); return true;
+      case 48: launch(W, std::integral_constant<int, 48>{}); return true;
+      case 64: launch(W, std::integral_constant<int, 64>{}); return true;
+      case 80: launch(W, std::integral_constant<int, 80>{}); return true;
+      case 96: launch(W, std::integral_constant<int, 96>{}); return true;
+      case 112: launch(W, std::integral_constant<int, 112>{}); return true;
+      case 128: launch(W, std::integral_constant<int, 128>{}); return true;
+      default: return false;
+    }
+  };
+  bool ok;
+  switch (waves) {
+    case 1: ok = by_hd(std::integral_constant<int, 1>{}); break;
+    case 2: ok = by_hd(std::integral_constant<int, 2>{}); break;
+    case 3: ok = by_hd(std::integral_constant<int, 3>{}); break;
+    default: ok = by_hd(std::integral_constant<int, 4>{}); break;
+  }
+  if (!ok) return OQ_ERR_SHAPE;
+  int e = launch_status();
+  if (e != OQ_OK) return e;
+  const int b = pow2_divisor(static_cast<int>(D));
+  return rq_launch(out, M, D, D, b, sdelta ? 1.0f : s, at<uint8_t>(h, h->lay.xq), at<float>(h, h->lay.xs), nullptr,
+                   st, h->tiled, sdelta);
+}
+
 // until: stop after the fused producer of quantization site `until` (0: the
 // q|k|v input, 1: the o input, 2: the gate|up input, 3: the down input), or
 // run the whole block (until = 4).
@@ -937,11 +1156,7 @@ int run_block_gr00t(oq_dit* h, int l, int t, float* r, hipStream_t st, int until
   if (l % 2 == 0) {
     // Cross-attention to the conditioning k|v of this block ([B][P][2D]).
     if ((e = gemm(h, *ss.w[0], D, D, EPI_F16, qkv, D, nullptr, st)) != OQ_OK) return e;
-    const int64_t MC = static_cast<int64_t>(c.batch) * c.prefix;
-    const uint16_t* kv = at<uint16_t>(h, h->lay.ckv) + static_cast<int64_t>(l / 2) * MC * 2 * D;
-    if ((e = attention_rq(h, qkv, D, kv, kv + D, c.prefix, 2 * D, nullptr, nullptr, 0, 0, s[1], st, ss.d[1])) !=
-        OQ_OK)
-      return e;
+    if ((e = cross_attention_rq(h, qkv, D, l, s[1], st, ss.d[1])) != OQ_OK) return e;
   } else {
     if ((e = gemm(h, *ss.w[0], D, 3 * D, EPI_F16, qkv, 3 * D, nullptr, st)) != OQ_OK) return e;
     if ((e = attention_rq(h, qkv, 3 * D, nullptr, nullptr, 0, 0, qkv + D, qkv + 2 * D, 3 * D, c.tokens, s[1], st,
@@ -1002,6 +1217,11 @@ int set_condition(oq_dit* h, const uint16_t* cond, hipStream_t st) {
     const oq_qweight& wt = h->blocks[l].cross_kv;
     GemmArgs a{xq, wt.wq, xs, wt.w_scale, nullptr, kv, nullptr, MC, 2 * D, D, 2 * D};
     if ((e = gemm_launch(a, EPI_F16, st)) != OQ_OK) return e;
+    uint16_t* kvh = at<uint16_t>(h, h->lay.ckvh) + static_cast<int64_t>(l / 2) * MC * 2 * D;
+    const int64_t pieces = MC * 2 * D / 8;
+    hipLaunchKernelGGL(kv_head_major_kernel, dim3(static_cast<unsigned>((pieces + 255) / 256)), dim3(256), 0, st,
+                       kv, kvh, static_cast<int64_t>(c.batch), c.prefix, c.n_heads, c.head_dim);
+    if ((e = launch_status()) != OQ_OK) return e;
   }
   return OQ_OK;
 }
