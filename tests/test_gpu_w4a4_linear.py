@@ -40,7 +40,8 @@ def test_i32_accumulators_bit_exact(M, N, K):
 @pytest.mark.parametrize("M,N,K", [(4096, 4096, 256), (4100, 4160, 192), (8192, 2048, 128), (2048, 8320, 64),
                                    (4096, 4096, 320), (2100, 4160, 192), (8192, 4096, 448), (1100, 8200, 128)])
 def test_i32_bit_exact_large_tiles(M, N, K):
-    """Shapes that take the 256 x 256 and the 128 x 256 tile paths, with ragged edges."""
+    """Shapes that take the 256 x 256 and the 128 x 128 tile paths, with ragged edges (the 64 x 64 tile
+    is taken by the M > 64 shapes of test_i32_accumulators_bit_exact)."""
     print(f"gemm i32 large M={M} N={N} K={K}", flush=True)
     rng = np.random.default_rng(M + 3 * N + 7 * K)
     q, qw = _codes(rng, M, K), _codes(rng, N, K)
