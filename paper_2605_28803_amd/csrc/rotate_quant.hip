@@ -81,10 +81,27 @@ __global__ __launch_bounds__(256) void rq_mfma_kernel(const uint16_t* __restrict
 #pragma unroll
   for (int g = 0; g < NG; ++g)
     cur[g] = valid ? *reinterpret_cast<const rqm::rv8h*>(xr + rqm::chan0<NG>(wr, g, lane)) : rqm::rv8h{};
+  // Static steps with one row per wave: the workgroup forms the K
+  // multipliers once in LDS while the rows' loads are in flight.
+  const float* sg = nullptr;
+  if constexpr (W == 1) {
+    if (sdelta != nullptr) {
+      float* gt = reinterpret_cast<float*>(xch);
+      constexpr int K = rqm::Shape<NG, W>::K;
+      for (int k4 = threadIdx.x; k4 < K / 4; k4 += 256) {
+        const float4 d = reinterpret_cast<const float4*>(sdelta)[k4];
+        reinterpret_cast<float4*>(gt)[k4] =
+            make_float4(rqd::static_mult(d.x, s_over_sqrtb), rqd::static_mult(d.y, s_over_sqrtb),
+                        rqd::static_mult(d.z, s_over_sqrtb), rqd::static_mult(d.w, s_over_sqrtb));
+      }
+      __syncthreads();
+      sg = gt;
+    }
+  }
   rqm::rv8h a1, a2;
   rqm::hadamard_frags(lane, a1, a2);
   rqm::rq_row<NG, W, FULL>(cur, a1, a2, row, valid, lane, wv, logb, s_t, s_over_sqrtb, Xq, xs, ratio, xch, red, tiled,
-                           sdelta, rotate_only, i8, cmul);
+                           sdelta, rotate_only, i8, cmul, sg);
 }
 
 // (NG, W) of the matrix-core variant for K channels, or false.
@@ -110,7 +127,8 @@ int rq_mfma_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_blo
   const int logb = ilog2(had_block);
   const float s_over_sqrtb = static_cast<float>(static_cast<double>(s_t) / std::sqrt(static_cast<double>(had_block)));
   const int rpb = 4 / w;
-  const size_t lds = w > 1 ? static_cast<size_t>(4) * ng * 64 * sizeof(float4) : 0;
+  const size_t lds = w > 1 ? static_cast<size_t>(4) * ng * 64 * sizeof(float4)
+                           : (sdelta != nullptr ? static_cast<size_t>(K) * sizeof(float) : 0);
   // One row per wave (W = 1) or per workgroup (W > 1).
   const unsigned grid = static_cast<unsigned>((M + rpb - 1) / rpb);
   const uint16_t* x = static_cast<const uint16_t*>(X);

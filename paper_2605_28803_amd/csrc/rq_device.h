@@ -200,6 +200,16 @@ __device__ __forceinline__ uint2 pack8_i8(const uint32_t (&b)[8]) {
   return make_uint2(lo, hi);
 }
 
+// The same with the multiplier g = inv_sqrtb * rcp(delta) (0 for a step
+// that is not positive) already formed, as static_code forms it.
+__device__ __forceinline__ float static_mult(float delta, float inv_sqrtb) {
+  return delta > 0.0f ? inv_sqrtb * __builtin_amdgcn_rcpf(delta) : 0.0f;
+}
+__device__ __forceinline__ uint32_t static_code_g(float u, float g) {
+  const float r = __builtin_amdgcn_fmed3f(u * g, -7.0f, 7.0f);
+  return __float_as_uint(r + kRoundMagic);
+}
+
 // The rest of the fused pass once the row's fp32 values are in registers:
 // butterflies, row maximum, scales, codes.  `lds` must hold rows_per_wg * K
 // floats when logT > 6; `red` is a 4-float shared array.  Every thread of the

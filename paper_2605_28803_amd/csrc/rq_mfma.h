@@ -73,14 +73,16 @@ __device__ __forceinline__ int chan0(int wr, int g, int lane) {
 // a 4-float shared array.  sdelta / rotate_only: the static per-channel
 // quantizer and the fp32 rotation output, as in rqd::rq_core; i8: 8-bit codes
 // (q_max = 127), one byte per code in [M][K]; cmul: per-channel multiplier
-// before the row maximum, as in rqd::rq_core.
+// before the row maximum, as in rqd::rq_core; sg (with sdelta): the static
+// multipliers rqd::static_mult already formed per channel (in LDS).
 template <int NG, int W, bool FULL>
 __device__ __forceinline__ void rq_row(const rv8h (&cur)[NG], const rv8h& a1, const rv8h& a2, int64_t row, bool valid,
                                        int lane, int wv, int logb, float s_t, float s_over_sqrtb,
                                        uint8_t* __restrict__ Xq, float* __restrict__ xs, float* __restrict__ ratio,
                                        float4* xch, float* red, bool tiled,
                                        const float* __restrict__ sdelta = nullptr, bool rotate_only = false,
-                                       bool i8 = false, const float* __restrict__ cmul = nullptr) {
+                                       bool i8 = false, const float* __restrict__ cmul = nullptr,
+                                       const float* sg = nullptr) {
   using S = Shape<NG, W>;
   constexpr int K = S::K, LOGNG = S::LOGNG, LOGW = S::LOGW, GW = S::GW;
   const int rsub = wv / W, wr = wv % W;
@@ -207,12 +209,20 @@ __device__ __forceinline__ void rq_row(const rv8h (&cur)[NG], const rv8h& a1, co
 #pragma unroll
     for (int s = 0; s < NG; ++s) {
       const int c0 = (group_of(s) * 16 + cl) * 32 + 8 * q;
-      const float4 d0 = reinterpret_cast<const float4*>(sdelta + c0)[0];
-      const float4 d1 = reinterpret_cast<const float4*>(sdelta + c0)[1];
-      const float d[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
       uint32_t b[8];
+      if (sg != nullptr) {
+        const float4 g0 = reinterpret_cast<const float4*>(sg + c0)[0];
+        const float4 g1 = reinterpret_cast<const float4*>(sg + c0)[1];
+        const float g[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
 #pragma unroll
-      for (int e = 0; e < 8; ++e) b[e] = rqd::static_code(v[s][e], d[e], s_over_sqrtb);
+        for (int e = 0; e < 8; ++e) b[e] = rqd::static_code_g(v[s][e], g[e]);
+      } else {
+        const float4 d0 = reinterpret_cast<const float4*>(sdelta + c0)[0];
+        const float4 d1 = reinterpret_cast<const float4*>(sdelta + c0)[1];
+        const float d[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) b[e] = rqd::static_code(v[s][e], d[e], s_over_sqrtb);
+      }
       const int p = c0 / 2;
       uint8_t* dst = tiled ? Xq + tiled_offset(row, p, K / 128) : qr + p;
       *reinterpret_cast<uint32_t*>(dst) = rqd::pack8(b);
