@@ -181,7 +181,8 @@ def roofline_gemm(stream=None):
 def prefill_kernels():
     """One large shape of each kernel, cold (MALL flushed before each launch):
     W4A4 GEMM at M = K = N = 16384 (int8-MFMA roofline) and rotate-quantize at
-    M = K = 16384 (HBM roofline)."""
+    M = K = 16384 (HBM roofline); and rotate-quantize back to back on 1.3 GB
+    inputs (the flush's own write-back no longer overlaps the timed launch)."""
     import torch
     import paper_2605_28803_amd as oq
     dev = torch.device("cuda:0")
@@ -218,6 +219,30 @@ def prefill_kernels():
                                           "GBs": round(rq_bytes(M, K) / (t_r * 1e-3) / 1e9, 1),
                                           "frac_hbm_peak": round(rq_bytes(M, K) / (t_r * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}}
     del X, Xq, Y, Wq, flush
+    torch.cuda.empty_cache()
+    # Back to back on 1.3 GB (beyond the 256 MB MALL, so every launch streams
+    # from HBM): rotate-quantize at M = 131072, K = 4096 and M = 32768, K =
+    # 16384, median of 20 launches.
+    for Mw, Kw in ((131072, 4096), (32768, 16384)):
+        X = torch.randn((Mw, Kw), generator=g, device=dev).half()
+        Xq = torch.empty((Mw, Kw // 2), dtype=torch.uint8, device=dev)
+        xsw = torch.empty((Mw,), dtype=torch.float32, device=dev)
+        f = lambda: oq.rotate_quantize_act(X, Kw, Xq=Xq, x_scale=xsw)
+        f()
+        ts = []
+        for _ in range(20):
+            s = torch.cuda.Event(enable_timing=True)
+            e = torch.cuda.Event(enable_timing=True)
+            s.record(stream)
+            f()
+            e.record(stream)
+            e.synchronize()
+            ts.append(s.elapsed_time(e))
+        t = float(np.median(ts))
+        gbs = rq_bytes(Mw, Kw) / (t * 1e-3) / 1e9
+        out[f"rotate_quant_M{Mw}_K{Kw}_back_to_back"] = {"us": round(t * 1e3, 1), "GBs": round(gbs, 1),
+                                                          "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)}
+        del X, Xq, xsw
     torch.cuda.empty_cache()
     return out
 
