@@ -236,11 +236,11 @@ struct AttnArgs {
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 
-// One (sample b, head h, 64-key split) on the fp16 matrix cores
-// (v_mfma_f32_16x16x32_f16), ceil(S / 16) waves.  Wave w owns query rows
-// 16w .. 16w+15 (head_dim a multiple of 16; the q.k contraction is padded with
-// zeros to a multiple of 32):
-//   S = Q K^T (16 x 64, fp32), scaled; split maximum m and sum l per row;
+// One (sample b, head h, split of KS keys, KS a multiple of 64) on the fp16
+// matrix cores (v_mfma_f32_16x16x32_f16), ceil(S / 16) waves.  Wave w owns
+// query rows 16w .. 16w+15 (head_dim a multiple of 16; the q.k contraction is
+// padded with zeros to a multiple of 32):
+//   S = Q K^T (16 x KS, fp32), scaled; split maximum m and sum l per row;
 //   P = exp(S - m) (fp16, staged in LDS as the next A operand);
 //   O = P V (16 x hd, fp32) with V^T staged in LDS.
 // O, m and l go to the workspace; combine_rq_kernel merges the splits.
@@ -250,15 +250,25 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 // l % 16 in element e.  WAVES = ceil(S / 16) waves; HD = head_dim when it is
 // one of the compiled sizes (the loops then unroll completely), 0 otherwise
 // (a.hd at run time).
-template <int WAVES, int HD>
+//
+// The split's K and V blocks are read from global memory once per workgroup
+// (every wave needs all of K): K in 16-byte pieces along its rows (a wave
+// reads whole rows) into LDS as [key][dim]; V as pairs of keys (2j, 2j + 1)
+// by 8 dims, written to V^T [dim][key] as 4-byte key pairs.  Keys past the
+// split and dims past head_dim are staged as zeros.
+template <int WAVES, int HD, int KS>
 __global__ __launch_bounds__(64 * WAVES) void attn_partial_kernel(AttnArgs a) {
-  constexpr int KS = kAttnKS;            // 64 keys
+  static_assert(KS % 64 == 0, "keys per split");
+  constexpr int NT = 64 * WAVES;
   constexpr int PAD = KS + 8;            // padded row (halves): 16-byte reads of 16 rows hit distinct banks
   constexpr int HDL = HD > 0 ? HD : kMaxHeadDim;
-  // LDS sized for this instance (one wave and 48 dims need 9 KB, so many
+  constexpr int KPAD = HDL + 8;          // padded K row (halves), likewise
+  constexpr int C8 = HDL / 8;            // 8-dim pieces per row
+  // LDS sized for this instance (one wave and 48 dims need 16 KB, so many
   // workgroups share a CU).
   __shared__ __attribute__((aligned(16))) uint16_t sVt[HDL][PAD];      // V^T [dim][key]
   __shared__ __attribute__((aligned(16))) uint16_t sP[WAVES][16][PAD];  // per-wave P [row][key]
+  __shared__ __attribute__((aligned(16))) uint16_t sK[KS][KPAD];        // K [key][dim]
 
   const int bh = blockIdx.x, split = blockIdx.y;
   const int b = bh / a.H, h = bh % a.H;
@@ -269,7 +279,7 @@ __global__ __launch_bounds__(64 * WAVES) void attn_partial_kernel(AttnArgs a) {
   const int nk = min(KS, n_keys - k0);
   const int hd = HD > 0 ? HD : a.hd;
 
-  __builtin_assume(tid < 64 * WAVES);
+  __builtin_assume(tid < NT);
   // Row base of key j of this split: the first P keys are prefix rows, the
   // rest the sample's own rows.  Both candidate addresses are formed in full
   // and the per-lane choice selects between them (a select between two
@@ -291,69 +301,85 @@ __global__ __launch_bounds__(64 * WAVES) void attn_partial_kernel(AttnArgs a) {
   // Every global load of the workgroup is issued before the first LDS write
   // or MFMA.  Loads are branch-free: an out-of-range key, query row or head
   // dimension reads a clamped valid address, and its value is replaced by
-  // zero where it is used (never by overwriting a register a load is still
-  // filling, which would stall on that load).
-  // V: thread (key j = tid % 64, dims d8 = 8 (tid / 64) + 8 WAVES i) loads 8 dims.
-  constexpr int VIT = HD > 0 ? (HD + 8 * WAVES - 1) / (8 * WAVES) : kMaxHeadDim / (8 * WAVES);
-  const int vj = tid & 63;
-  const bool vjok = vj < nk;
-  uint4 vraw[VIT];
-  {
-    const uint16_t* vp = key_row(vjok ? vj : 0, v_pre, v_own);
+  // zero where it is staged or used (never by overwriting a register a load
+  // is still filling, which would stall on that load).
+  // K: piece p = tid + NT i is key p / C8, dims 8 (p % C8) .. + 7.
+  constexpr int KIT = (KS * C8 + NT - 1) / NT;
+  uint4 kraw[KIT];
 #pragma unroll
-    for (int i = 0; i < VIT; ++i) {
-      const int d8 = (tid >> 6) * 8 + i * 8 * WAVES;
-      vraw[i] = *reinterpret_cast<const uint4*>(vp + (d8 < hd ? d8 : 0));
+  for (int i = 0; i < KIT; ++i) {
+    const int p = tid + NT * i;
+    const int j = p / C8, c8 = (p % C8) * 8;
+    const bool ok = p < KS * C8 && j < nk && c8 < hd;
+    kraw[i] = *reinterpret_cast<const uint4*>(key_row(ok ? j : 0, k_pre, k_own) + (ok ? c8 : 0));
+  }
+  // V: unit u = tid + NT i is keys 2 (u % (KS/2)) + {0, 1}, dims 8 (u / (KS/2)) .. + 7.
+  constexpr int VIT = (KS / 2 * C8 + NT - 1) / NT;
+  uint4 vraw[VIT][2];
+#pragma unroll
+  for (int i = 0; i < VIT; ++i) {
+    const int u = tid + NT * i;
+    const int j = 2 * (u % (KS / 2)), c8 = (u / (KS / 2)) * 8;
+    const bool ok = u < KS / 2 * C8 && c8 < hd;
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const bool oke = ok && j + e < nk;
+      vraw[i][e] = *reinterpret_cast<const uint4*>(key_row(oke ? j + e : 0, v_pre, v_own) + (ok ? c8 : 0));
     }
   }
-  // Q (this wave's 16 rows) and K (the split's 64 keys) fragments.
+  // Q (this wave's 16 rows).
   const int qrow = 16 * w + (lane & 15);
   const bool qok = qrow < a.S;
   const int kq = 8 * (lane >> 4);
   const int nkk = (hd + 31) / 32;  // 32-wide k steps over the head dimension (zero-padded)
   constexpr int KKMAX = HD > 0 ? (HD + 31) / 32 : kMaxHeadDim / 32;
   const uint16_t* qp = a.q + (static_cast<int64_t>(b) * a.S + (qok ? qrow : 0)) * a.q_ld + h * hd;
-  const uint16_t* kp[KS / 16];
-  bool kok[KS / 16];
-#pragma unroll
-  for (int nb = 0; nb < KS / 16; ++nb) {
-    const int j = nb * 16 + (lane & 15);
-    kok[nb] = j < nk;
-    kp[nb] = key_row(kok[nb] ? j : 0, k_pre, k_own);
-  }
-  v8h qraw[KKMAX], kraw[KKMAX][KS / 16];
+  v8h qraw[KKMAX];
   bool dok[KKMAX];
 #pragma unroll
   for (int kk = 0; kk < KKMAX; ++kk) {
     // hd % 8 == 0: a chunk of 8 dims is wholly inside or outside the head.
     dok[kk] = kk < nkk && kk * 32 + kq < hd;
-    const int d = dok[kk] ? kk * 32 + kq : 0;
-    qraw[kk] = *reinterpret_cast<const v8h*>(qp + d);
-#pragma unroll
-    for (int nb = 0; nb < KS / 16; ++nb) kraw[kk][nb] = *reinterpret_cast<const v8h*>(kp[nb] + d);
+    qraw[kk] = *reinterpret_cast<const v8h*>(qp + (dok[kk] ? kk * 32 + kq : 0));
   }
 
-  // Stage V^T [dim][key] in LDS.
+  // Stage K [key][dim] and V^T [dim][key] in LDS.
+#pragma unroll
+  for (int i = 0; i < KIT; ++i) {
+    const int p = tid + NT * i;
+    const int j = p / C8, c8 = (p % C8) * 8;
+    if (p < KS * C8) {
+      const bool ok = j < nk && c8 < hd;
+      const uint4 v = ok ? kraw[i] : make_uint4(0, 0, 0, 0);
+      uint32_t* d = reinterpret_cast<uint32_t*>(&sK[j][c8]);
+      d[0] = v.x;
+      d[1] = v.y;
+      d[2] = v.z;
+      d[3] = v.w;
+    }
+  }
 #pragma unroll
   for (int i = 0; i < VIT; ++i) {
-    const int d8 = (tid >> 6) * 8 + i * 8 * WAVES;
-    if (d8 < hd) {
-      const uint32_t wv[4] = {vjok ? vraw[i].x : 0u, vjok ? vraw[i].y : 0u, vjok ? vraw[i].z : 0u,
-                              vjok ? vraw[i].w : 0u};
+    const int u = tid + NT * i;
+    const int j = 2 * (u % (KS / 2)), c8 = (u / (KS / 2)) * 8;
+    if (u < KS / 2 * C8) {
+      const bool ok0 = c8 < hd && j < nk, ok1 = c8 < hd && j + 1 < nk;
+      const uint32_t w0[4] = {ok0 ? vraw[i][0].x : 0u, ok0 ? vraw[i][0].y : 0u, ok0 ? vraw[i][0].z : 0u,
+                              ok0 ? vraw[i][0].w : 0u};
+      const uint32_t w1[4] = {ok1 ? vraw[i][1].x : 0u, ok1 ? vraw[i][1].y : 0u, ok1 ? vraw[i][1].z : 0u,
+                              ok1 ? vraw[i][1].w : 0u};
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        sVt[d8 + 2 * q][vj] = static_cast<uint16_t>(wv[q] & 0xFFFFu);
-        sVt[d8 + 2 * q + 1][vj] = static_cast<uint16_t>(wv[q] >> 16);
+        // dims c8 + 2q (low halves) and c8 + 2q + 1 (high halves) of keys j, j + 1
+        *reinterpret_cast<uint32_t*>(&sVt[c8 + 2 * q][j]) = (w0[q] & 0xFFFFu) | (w1[q] << 16);
+        *reinterpret_cast<uint32_t*>(&sVt[c8 + 2 * q + 1][j]) = (w0[q] >> 16) | (w1[q] & 0xFFFF0000u);
       }
     }
   }
-  v8h qa[KKMAX], kb[KKMAX][KS / 16];
+  v8h qa[KKMAX];
 #pragma unroll
-  for (int kk = 0; kk < KKMAX; ++kk) {
-    qa[kk] = (dok[kk] && qok) ? qraw[kk] : v8h{};
-#pragma unroll
-    for (int nb = 0; nb < KS / 16; ++nb) kb[kk][nb] = (dok[kk] && kok[nb]) ? kraw[kk][nb] : v8h{};
-  }
+  for (int kk = 0; kk < KKMAX; ++kk) qa[kk] = (dok[kk] && qok) ? qraw[kk] : v8h{};
+  __syncthreads();
 
   v4f sc[KS / 16];
 #pragma unroll
@@ -361,7 +387,10 @@ __global__ __launch_bounds__(64 * WAVES) void attn_partial_kernel(AttnArgs a) {
     sc[nb] = v4f{0, 0, 0, 0};
 #pragma unroll
     for (int kk = 0; kk < KKMAX; ++kk)
-      if (kk < nkk) sc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(qa[kk], kb[kk][nb], sc[nb], 0, 0, 0);
+      if (kk < nkk) {
+        const v8h kb = *reinterpret_cast<const v8h*>(&sK[nb * 16 + (lane & 15)][dok[kk] ? kk * 32 + kq : 0]);
+        sc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(qa[kk], kb, sc[nb], 0, 0, 0);
+      }
   }
 
   // Softmax statistics per row (row 4*(lane/16) + e, keys across the 16 lanes
@@ -1017,10 +1046,10 @@ int attention_rq(oq_dit* h, const uint16_t* q, int64_t q_ld, const uint16_t* k_p
   auto launch = [&](auto W) {
     constexpr int WV = decltype(W)::value;
     switch (c.head_dim) {
-      case 48: hipLaunchKernelGGL((attn_partial_kernel<WV, 48>), grid, dim3(64 * WV), 0, st, a); break;
-      case 64: hipLaunchKernelGGL((attn_partial_kernel<WV, 64>), grid, dim3(64 * WV), 0, st, a); break;
-      case 128: hipLaunchKernelGGL((attn_partial_kernel<WV, 128>), grid, dim3(64 * WV), 0, st, a); break;
-      default: hipLaunchKernelGGL((attn_partial_kernel<WV, 0>), grid, dim3(64 * WV), 0, st, a); break;
+      case 48: hipLaunchKernelGGL((attn_partial_kernel<WV, 48, kAttnKS>), grid, dim3(64 * WV), 0, st, a); break;
+      case 64: hipLaunchKernelGGL((attn_partial_kernel<WV, 64, kAttnKS>), grid, dim3(64 * WV), 0, st, a); break;
+      case 128: hipLaunchKernelGGL((attn_partial_kernel<WV, 128, kAttnKS>), grid, dim3(64 * WV), 0, st, a); break;
+      default: hipLaunchKernelGGL((attn_partial_kernel<WV, 0, kAttnKS>), grid, dim3(64 * WV), 0, st, a); break;
     }
   };
   switch (waves) {
