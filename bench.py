@@ -255,7 +255,10 @@ def composite_kernels():
     channel, are read once per launch and counted), and at the DiT shape
     (M = 50, K = 1024), whose time is latency.  The permutation comes from
     seeded synthetic weight energies and U_b are seeded random orthogonal
-    matrices (the kernel's work does not depend on their values)."""
+    matrices (the kernel's work does not depend on their values).  Beside each
+    online figure: the same transform with P folded into the producer (the
+    input already in the permuted order, perm = None), and K = 16384, where
+    the online gather stages only 2 rows per workgroup."""
     import torch
     import paper_2605_28803_amd as oq
     from workloads import generators as G
@@ -277,7 +280,7 @@ def composite_kernels():
         return float(np.median(ts))
 
     out = {}
-    for M, K in ((16384, 1024), (16384, 4096), (50, 1024)):
+    for M, K in ((16384, 1024), (16384, 4096), (16384, 16384), (50, 1024)):
         energy = G.gaussian(11, f"composite/energy{K}", (K,)) ** 2
         perm = torch.from_numpy(oq.zigzag_permutation_host(energy, 64)).to(dev)
         U = np.stack([G.random_orthogonal(11, f"composite/u{K}/{b}", 64) for b in range(K // 64)])
@@ -286,9 +289,15 @@ def composite_kernels():
         X = torch.randn((M, K), generator=g, device=dev).half()
         Xq, xs = oq.rotate_quantize_act_composite(X, perm, Rt)
         t = cold(lambda: oq.rotate_quantize_act_composite(X, perm, Rt, Xq=Xq, x_scale=xs), 15)
+        # the same transform with P folded into the producer (perm = None: the
+        # input is taken to be in the permuted order already)
+        tf = cold(lambda: oq.rotate_quantize_act_composite(X, None, Rt, Xq=Xq, x_scale=xs), 15)
         b = rq_bytes(M, K) + K * 4 + K * 64 * 2
+        bf = rq_bytes(M, K) + K * 64 * 2
         out[f"M{M}_K{K}"] = {"us": round(t * 1e3, 2), "GBs": round(b / (t * 1e-3) / 1e9, 1),
-                             "frac_hbm_peak": round(b / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+                             "frac_hbm_peak": round(b / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                             "perm_folded_us": round(tf * 1e3, 2),
+                             "perm_folded_GBs": round(bf / (tf * 1e-3) / 1e9, 1)}
         del X, Xq, xs
     del flush
     torch.cuda.empty_cache()

@@ -216,7 +216,11 @@ int oq_w4a4_gemm_i32_tiled(const uint8_t* Xt, int64_t M, const uint8_t* Wq, int6
  * K        multiple of 64, 64 <= K <= 16384
  * perm     device int32 [K], a permutation of 0 .. K-1, 16-byte aligned
  *          (entries outside 0 .. K-1 are clamped into range; the result is
- *          then unspecified but every access stays in bounds)
+ *          then unspecified but every access stays in bounds); or NULL: X is
+ *          already in the permuted channel order (P folded into the
+ *          producer of X, as U is for the Hadamard path), so (X P) = X and
+ *          the rows go straight from global memory into the matrix-core
+ *          operands without a gather
  * Rt       device fp16 [K/64][64][64], block b column-major:
  *          Rt[b][j][r] = R_b[r][j] (oq_block_rotations_host writes it), 16-byte
  *          aligned.  The products are formed from these fp16 values exactly

@@ -38,6 +38,14 @@ def _stream(stream=None):
     return C.c_void_p(s.cuda_stream)
 
 
+def _ld(t):
+    """Leading dimension (elements from one row to the next) of a 2-D tensor.
+    The stride of a single row is unconstrained (numpy and torch may give it
+    any value), and only row 0 is read, so its leading dimension is the row
+    length."""
+    return t.stride(0) if t.shape[0] > 1 else t.shape[1]
+
+
 def _ptr(t):
     return None if t is None else C.c_void_p(t.data_ptr())
 
@@ -62,14 +70,14 @@ def status_string(code: int) -> str:
 
 
 def rotate_quantize_act(X, had_block, s_table=None, t=0, Xq=None, x_scale=None, stream=None):
-    """X: fp16 [M, K] (row stride X.stride(0)).  Returns (Xq uint8 [M, K/2], x_scale f32 [M])."""
+    """X: fp16 [M, K] (row stride X.stride(0); any stride for a single row).  Returns (Xq uint8 [M, K/2], x_scale f32 [M])."""
     M, K = X.shape
     if Xq is None:
         Xq = torch.empty((M, K // 2), dtype=torch.uint8, device=X.device)
     if x_scale is None:
         x_scale = torch.empty((M,), dtype=torch.float32, device=X.device)
     keep, sp = _s_table(s_table)
-    _check(lib().oq_rotate_quantize_act(_ptr(X), M, K, X.stride(0), had_block, sp, t, _ptr(Xq),
+    _check(lib().oq_rotate_quantize_act(_ptr(X), M, K, _ld(X), had_block, sp, t, _ptr(Xq),
                                         _ptr(x_scale), _stream(stream)), "oq_rotate_quantize_act")
     del keep
     return Xq, x_scale
@@ -88,7 +96,7 @@ def rotate_quantize_act_tiled(X, had_block, s_table=None, t=0, Xt=None, x_scale=
     if x_scale is None:
         x_scale = torch.empty((M,), dtype=torch.float32, device=X.device)
     keep, sp = _s_table(s_table)
-    _check(lib().oq_rotate_quantize_act_tiled(_ptr(X), M, K, X.stride(0), had_block, sp, t, _ptr(Xt),
+    _check(lib().oq_rotate_quantize_act_tiled(_ptr(X), M, K, _ld(X), had_block, sp, t, _ptr(Xt),
                                               _ptr(x_scale), _stream(stream)), "oq_rotate_quantize_act_tiled")
     del keep
     return Xt, x_scale
@@ -106,15 +114,16 @@ def codes_to_tiled(Q, K=None, T=None, stream=None):
 
 def rotate_quantize_act_composite(X, perm, Rt, s_table=None, t=0, Xq=None, x_scale=None, stream=None):
     """Full composite rotation (block 64) + step scale + per-token int4 codes.
-    X fp16 [M, K]; perm int32 [K] and Rt fp16 [K/64, 64, 64] (column-major
-    blocks) on the device.  Returns (Xq uint8 [M, K/2], x_scale f32 [M])."""
+    X fp16 [M, K]; perm int32 [K] (None: X is already in the permuted channel
+    order) and Rt fp16 [K/64, 64, 64] (column-major blocks) on the device.
+    Returns (Xq uint8 [M, K/2], x_scale f32 [M])."""
     M, K = X.shape
     if Xq is None:
         Xq = torch.empty((M, K // 2), dtype=torch.uint8, device=X.device)
     if x_scale is None:
         x_scale = torch.empty((M,), dtype=torch.float32, device=X.device)
     keep, sp = _s_table(s_table)
-    _check(lib().oq_rotate_quantize_act_composite(_ptr(X), M, K, X.stride(0), _ptr(perm), _ptr(Rt), sp, t,
+    _check(lib().oq_rotate_quantize_act_composite(_ptr(X), M, K, _ld(X), _ptr(perm), _ptr(Rt), sp, t,
                                                   _ptr(Xq), _ptr(x_scale), _stream(stream)),
            "oq_rotate_quantize_act_composite")
     del keep
@@ -160,7 +169,7 @@ def rotate_debug_f32(X, had_block, s_table=None, t=0, stream=None):
     ratio = torch.empty((M, K), dtype=torch.float32, device=X.device)
     x_scale = torch.empty((M,), dtype=torch.float32, device=X.device)
     keep, sp = _s_table(s_table)
-    _check(lib().oq_rotate_debug_f32(_ptr(X), M, K, X.stride(0), had_block, sp, t, _ptr(ratio),
+    _check(lib().oq_rotate_debug_f32(_ptr(X), M, K, _ld(X), had_block, sp, t, _ptr(ratio),
                                      _ptr(x_scale), _stream(stream)), "oq_rotate_debug_f32")
     del keep
     return ratio, x_scale
@@ -175,7 +184,7 @@ def w4a4_linear(Xq, x_scale, Wq, w_scale, bias=None, out_dtype=OUT_F16, Y=None, 
         dt = torch.float16 if out_dtype == OUT_F16 else torch.bfloat16
         Y = torch.empty((M, N), dtype=dt, device=Xq.device)
     _check(lib().oq_w4a4_linear(_ptr(Xq), _ptr(x_scale), M, _ptr(Wq), _ptr(w_scale), _ptr(bias), N, K,
-                                _ptr(Y), Y.stride(0), out_dtype, _stream(stream)), "oq_w4a4_linear")
+                                _ptr(Y), _ld(Y), out_dtype, _stream(stream)), "oq_w4a4_linear")
     return Y
 
 
@@ -184,7 +193,7 @@ def w4a4_gemm_i32(Xq, Wq, acc=None, stream=None):
     N, Kh = Wq.shape
     if acc is None:
         acc = torch.empty((M, N), dtype=torch.int32, device=Xq.device)
-    _check(lib().oq_w4a4_gemm_i32(_ptr(Xq), M, _ptr(Wq), N, 2 * Kh, _ptr(acc), acc.stride(0),
+    _check(lib().oq_w4a4_gemm_i32(_ptr(Xq), M, _ptr(Wq), N, 2 * Kh, _ptr(acc), _ld(acc),
                                   _stream(stream)), "oq_w4a4_gemm_i32")
     return acc
 
@@ -198,7 +207,7 @@ def w4a4_linear_tiled(Xt, x_scale, Wq, w_scale, bias=None, out_dtype=OUT_F16, Y=
         dt = torch.float16 if out_dtype == OUT_F16 else torch.bfloat16
         Y = torch.empty((M, N), dtype=dt, device=Wq.device)
     _check(lib().oq_w4a4_linear_tiled(_ptr(Xt), _ptr(x_scale), M, _ptr(Wq), _ptr(w_scale), _ptr(bias), N, K,
-                                      _ptr(Y), Y.stride(0), out_dtype, _stream(stream)), "oq_w4a4_linear_tiled")
+                                      _ptr(Y), _ld(Y), out_dtype, _stream(stream)), "oq_w4a4_linear_tiled")
     return Y
 
 
@@ -206,7 +215,7 @@ def w4a4_gemm_i32_tiled(Xt, M, Wq, acc=None, stream=None):
     N, Kh = Wq.shape
     if acc is None:
         acc = torch.empty((M, N), dtype=torch.int32, device=Wq.device)
-    _check(lib().oq_w4a4_gemm_i32_tiled(_ptr(Xt), M, _ptr(Wq), N, 2 * Kh, _ptr(acc), acc.stride(0),
+    _check(lib().oq_w4a4_gemm_i32_tiled(_ptr(Xt), M, _ptr(Wq), N, 2 * Kh, _ptr(acc), _ld(acc),
                                         _stream(stream)), "oq_w4a4_gemm_i32_tiled")
     return acc
 
@@ -218,7 +227,7 @@ def quantize_weights(W_u, had_block, Wq=None, w_scale=None, stream=None):
         Wq = torch.empty((N, K // 2), dtype=torch.uint8, device=W_u.device)
     if w_scale is None:
         w_scale = torch.empty((N,), dtype=torch.float32, device=W_u.device)
-    _check(lib().oq_quantize_weights(_ptr(W_u), N, K, W_u.stride(0), had_block, _ptr(Wq), _ptr(w_scale),
+    _check(lib().oq_quantize_weights(_ptr(W_u), N, K, _ld(W_u), had_block, _ptr(Wq), _ptr(w_scale),
                                      _stream(stream)), "oq_quantize_weights")
     return Wq, w_scale
 
@@ -242,7 +251,7 @@ def rotate_quantize_act_i8(X, had_block, s_table=None, t=0, Xq8=None, x_scale=No
     if x_scale is None:
         x_scale = torch.empty((M,), dtype=torch.float32, device=X.device)
     keep, sp = _s_table(s_table)
-    _check(lib().oq_rotate_quantize_act_i8(_ptr(X), M, K, X.stride(0), had_block, sp, t, _ptr(Xq8),
+    _check(lib().oq_rotate_quantize_act_i8(_ptr(X), M, K, _ld(X), had_block, sp, t, _ptr(Xq8),
                                            _ptr(x_scale), _stream(stream)), "oq_rotate_quantize_act_i8")
     del keep
     return Xq8, x_scale
@@ -256,7 +265,7 @@ def w4a8_linear(Xq8, x_scale, Wq, w_scale, bias=None, out_dtype=OUT_F16, Y=None,
         dt = torch.float16 if out_dtype == OUT_F16 else torch.bfloat16
         Y = torch.empty((M, N), dtype=dt, device=Xq8.device)
     _check(lib().oq_w4a8_linear(_ptr(Xq8), _ptr(x_scale), M, _ptr(Wq), _ptr(w_scale), _ptr(bias), N, K,
-                                _ptr(Y), Y.stride(0), out_dtype, _stream(stream)), "oq_w4a8_linear")
+                                _ptr(Y), _ld(Y), out_dtype, _stream(stream)), "oq_w4a8_linear")
     return Y
 
 
@@ -265,7 +274,7 @@ def w4a8_gemm_i32(Xq8, Wq, acc=None, stream=None):
     N = Wq.shape[0]
     if acc is None:
         acc = torch.empty((M, N), dtype=torch.int32, device=Xq8.device)
-    _check(lib().oq_w4a8_gemm_i32(_ptr(Xq8), M, _ptr(Wq), N, K, _ptr(acc), acc.stride(0), _stream(stream)),
+    _check(lib().oq_w4a8_gemm_i32(_ptr(Xq8), M, _ptr(Wq), N, K, _ptr(acc), _ld(acc), _stream(stream)),
            "oq_w4a8_gemm_i32")
     return acc
 
@@ -275,7 +284,7 @@ def channel_energy(W, energy=None, stream=None):
     N, K = W.shape
     if energy is None:
         energy = torch.empty((K,), dtype=torch.float64, device=W.device)
-    _check(lib().oq_channel_energy(_ptr(W), N, K, W.stride(0), _ptr(energy), _stream(stream)), "oq_channel_energy")
+    _check(lib().oq_channel_energy(_ptr(W), N, K, _ld(W), _ptr(energy), _stream(stream)), "oq_channel_energy")
     return energy
 
 
@@ -296,7 +305,7 @@ def block_svd(W, perm, block=64, U=None, sigma2=None, stream=None):
         U = torch.empty((nb, block, block), dtype=torch.float64, device=W.device)
     if sigma2 is None:
         sigma2 = torch.empty((nb, block), dtype=torch.float64, device=W.device)
-    _check(lib().oq_block_svd(_ptr(W), N, K, W.stride(0), _ptr(perm), block, _ptr(U), _ptr(sigma2),
+    _check(lib().oq_block_svd(_ptr(W), N, K, _ld(W), _ptr(perm), block, _ptr(U), _ptr(sigma2),
                               _stream(stream)), "oq_block_svd")
     return U, sigma2
 
@@ -321,7 +330,7 @@ def prepare_weights_composite(W, stream=None):
     ws = torch.empty((N,), dtype=torch.float32, device=dev)
     nbytes = int(lib().oq_prepare_weights_workspace_bytes(K))
     work = torch.empty((max(nbytes, 16),), dtype=torch.uint8, device=dev)
-    _check(lib().oq_prepare_weights_composite(_ptr(W), N, K, W.stride(0), _ptr(perm), _ptr(Rt), _ptr(Wq), _ptr(ws),
+    _check(lib().oq_prepare_weights_composite(_ptr(W), N, K, _ld(W), _ptr(perm), _ptr(Rt), _ptr(Wq), _ptr(ws),
                                               _ptr(work), work.numel(), _stream(stream)),
            "oq_prepare_weights_composite")
     return perm, Rt, Wq, ws
@@ -332,7 +341,7 @@ def rotate_act_f32(X, had_block, Y=None, stream=None):
     M, K = X.shape
     if Y is None:
         Y = torch.empty((M, K), dtype=torch.float32, device=X.device)
-    _check(lib().oq_rotate_act_f32(_ptr(X), M, K, X.stride(0), had_block, _ptr(Y), _stream(stream)),
+    _check(lib().oq_rotate_act_f32(_ptr(X), M, K, _ld(X), had_block, _ptr(Y), _stream(stream)),
            "oq_rotate_act_f32")
     return Y
 
@@ -348,7 +357,7 @@ def calibrate_step_scales(Y, p=99.9, qmax=7.0, delta=None, work=None, stream=Non
         delta = torch.empty((K,), dtype=torch.float32, device=Y.device)
     if work is None:
         work = torch.empty((max(calibrate_workspace_bytes(K), 16),), dtype=torch.uint8, device=Y.device)
-    _check(lib().oq_calibrate_step_scales(_ptr(Y), n, K, Y.stride(0), float(p), float(qmax), _ptr(delta),
+    _check(lib().oq_calibrate_step_scales(_ptr(Y), n, K, _ld(Y), float(p), float(qmax), _ptr(delta),
                                           _ptr(work), work.numel(), _stream(stream)), "oq_calibrate_step_scales")
     return delta
 
@@ -360,7 +369,7 @@ def rotate_quantize_act_static(X, had_block, delta, Xq=None, x_scale=None, strea
         Xq = torch.empty((M, K // 2), dtype=torch.uint8, device=X.device)
     if x_scale is None:
         x_scale = torch.empty((M,), dtype=torch.float32, device=X.device)
-    _check(lib().oq_rotate_quantize_act_static(_ptr(X), M, K, X.stride(0), had_block, _ptr(delta), _ptr(Xq),
+    _check(lib().oq_rotate_quantize_act_static(_ptr(X), M, K, _ld(X), had_block, _ptr(delta), _ptr(Xq),
                                                _ptr(x_scale), _stream(stream)), "oq_rotate_quantize_act_static")
     return Xq, x_scale
 
@@ -372,7 +381,7 @@ def rotate_quantize_act_static_tiled(X, had_block, delta, Xt=None, x_scale=None,
         Xt = torch.empty((tiled_bytes(M, K),), dtype=torch.uint8, device=X.device)
     if x_scale is None:
         x_scale = torch.empty((M,), dtype=torch.float32, device=X.device)
-    _check(lib().oq_rotate_quantize_act_static_tiled(_ptr(X), M, K, X.stride(0), had_block, _ptr(delta),
+    _check(lib().oq_rotate_quantize_act_static_tiled(_ptr(X), M, K, _ld(X), had_block, _ptr(delta),
                                                      _ptr(Xt), _ptr(x_scale), _stream(stream)),
            "oq_rotate_quantize_act_static_tiled")
     return Xt, x_scale
@@ -386,7 +395,7 @@ def quantize_weights_step(W_u, had_block, delta, Wq=None, w_scale=None, stream=N
         Wq = torch.empty((N, K // 2), dtype=torch.uint8, device=W_u.device)
     if w_scale is None:
         w_scale = torch.empty((N,), dtype=torch.float32, device=W_u.device)
-    _check(lib().oq_quantize_weights_step(_ptr(W_u), N, K, W_u.stride(0), had_block, _ptr(delta), _ptr(Wq),
+    _check(lib().oq_quantize_weights_step(_ptr(W_u), N, K, _ld(W_u), had_block, _ptr(delta), _ptr(Wq),
                                           _ptr(w_scale), _stream(stream)), "oq_quantize_weights_step")
     return Wq, w_scale
 

@@ -40,7 +40,7 @@ __device__ __forceinline__ uint32_t pack4codes(uint32_t d) {
   return (t & 0xFFu) | ((t >> 8) & 0xFF00u);
 }
 
-template <int RW, int KMAX, int G>
+template <int RW, int KMAX, int G, bool GATHER>
 __global__ __launch_bounds__(256) void rq_composite_kernel(const uint16_t* __restrict__ X, int64_t M, int K,
                                                            int64_t ldx, const int32_t* __restrict__ perm,
                                                            const uint16_t* __restrict__ Rt, float s_t,
@@ -48,8 +48,8 @@ __global__ __launch_bounds__(256) void rq_composite_kernel(const uint16_t* __res
   // fp16 rows, padded by 16 bytes: the 16 rows of a gather read the same
   // permuted column, and the pad puts them in different LDS banks.
   constexpr int XS = KMAX + 8;
-  __shared__ __attribute__((aligned(16))) uint16_t sx[RW * XS];
-  __shared__ __attribute__((aligned(16))) int32_t sp[KMAX];          // the permutation
+  __shared__ __attribute__((aligned(16))) uint16_t sx[GATHER ? RW * XS : 8];
+  __shared__ __attribute__((aligned(16))) int32_t sp[GATHER ? KMAX : 4];  // the permutation
   __shared__ __attribute__((aligned(16))) uint8_t sc[RW * KMAX / 2];  // packed codes
   __shared__ float red[4][16];
   __shared__ float gscale[16];
@@ -60,40 +60,49 @@ __global__ __launch_bounds__(256) void rq_composite_kernel(const uint16_t* __res
 
   // Stage the rows (rows past M are zeros) and the permutation (clamped into
   // range: a non-permutation keeps every access inside the staged rows).
-  for (int p0 = tid; p0 < RW * vpr; p0 += 256 * 8) {
-    uint4 v[8];
-    bool ok[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int p = p0 + u * 256;
-      const int r = p / vpr, c8 = p - r * vpr;
-      ok[u] = p < RW * vpr && row0 + r < M;
-      const int64_t gr = ok[u] ? row0 + r : 0;
-      v[u] = *reinterpret_cast<const uint4*>(X + gr * ldx + (ok[u] ? c8 * 8 : 0));
+  if constexpr (GATHER) {
+    for (int p0 = tid; p0 < RW * vpr; p0 += 256 * 8) {
+      uint4 v[8];
+      bool ok[8];
+  #pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int p = p0 + u * 256;
+        const int r = p / vpr, c8 = p - r * vpr;
+        ok[u] = p < RW * vpr && row0 + r < M;
+        const int64_t gr = ok[u] ? row0 + r : 0;
+        v[u] = *reinterpret_cast<const uint4*>(X + gr * ldx + (ok[u] ? c8 * 8 : 0));
+      }
+  #pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int p = p0 + u * 256;
+        const int r = p / vpr, c8 = p - r * vpr;
+        if (p < RW * vpr) *reinterpret_cast<uint4*>(&sx[r * XS + c8 * 8]) = ok[u] ? v[u] : make_uint4(0, 0, 0, 0);
+      }
     }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int p = p0 + u * 256;
-      const int r = p / vpr, c8 = p - r * vpr;
-      if (p < RW * vpr) *reinterpret_cast<uint4*>(&sx[r * XS + c8 * 8]) = ok[u] ? v[u] : make_uint4(0, 0, 0, 0);
+    for (int k4 = tid; k4 < K / 4; k4 += 256) {
+      int4 pv = *reinterpret_cast<const int4*>(perm + 4 * k4);
+      pv.x = min(max(pv.x, 0), K - 1);
+      pv.y = min(max(pv.y, 0), K - 1);
+      pv.z = min(max(pv.z, 0), K - 1);
+      pv.w = min(max(pv.w, 0), K - 1);
+      *reinterpret_cast<int4*>(&sp[4 * k4]) = pv;
     }
-  }
-  for (int k4 = tid; k4 < K / 4; k4 += 256) {
-    int4 pv = *reinterpret_cast<const int4*>(perm + 4 * k4);
-    pv.x = min(max(pv.x, 0), K - 1);
-    pv.y = min(max(pv.y, 0), K - 1);
-    pv.z = min(max(pv.z, 0), K - 1);
-    pv.w = min(max(pv.w, 0), K - 1);
-    *reinterpret_cast<int4*>(&sp[4 * k4]) = pv;
   }
   __syncthreads();
 
   const int r16 = lane & 15, q = lane >> 4;
   const bool rok = r16 < RW;
-  const uint16_t* xrow = &sx[(rok ? r16 : 0) * XS];
+  const uint16_t* xrow = &sx[GATHER && rok ? r16 * XS : 0];
 
-  // A fragment: rows x 32 permuted channels of block b, k step kk.
+  // A fragment: rows x 32 permuted channels of block b, k step kk (without a
+  // permutation: one 16-byte load per lane from global memory, rows past RW
+  // or M zero).
+  const bool gok = rok && row0 + r16 < M;
   auto gather = [&](int b, int kk) -> c8h {
+    if constexpr (!GATHER) {
+      const c8h v = *reinterpret_cast<const c8h*>(X + (gok ? row0 + r16 : 0) * ldx + b * kCB + kk * 32 + 8 * q);
+      return gok ? v : c8h{};
+    }
     const int k0 = b * kCB + kk * 32 + 8 * q;
     const int4 pa = *reinterpret_cast<const int4*>(&sp[k0]);
     const int4 pb = *reinterpret_cast<const int4*>(&sp[k0 + 4]);
@@ -226,15 +235,15 @@ __global__ __launch_bounds__(256) void rq_composite_kernel(const uint16_t* __res
 // the RG row groups.  Codes are packed across lanes (channel pairs, then 4
 // and 8 channels) and stored as dwords by the lanes holding the first of 8
 // channels.
-template <int RG, int KMAX>
+template <int RG, int KMAX, bool GATHER>
 __global__ __launch_bounds__(512) void rq_composite1_kernel(const uint16_t* __restrict__ X, int64_t M, int K,
                                                             int64_t ldx, const int32_t* __restrict__ perm,
                                                             const uint16_t* __restrict__ Rt, float s_t,
                                                             uint8_t* __restrict__ Xq, float* __restrict__ xs) {
   constexpr int WAVES = 8, RW = 16 * RG, XS = KMAX + 8;
   constexpr int NBW = KMAX / kCB / WAVES;  // blocks per wave at K = KMAX
-  __shared__ __attribute__((aligned(16))) uint16_t sx[RW * XS];
-  __shared__ __attribute__((aligned(16))) int32_t sp[KMAX];
+  __shared__ __attribute__((aligned(16))) uint16_t sx[GATHER ? RW * XS : 8];
+  __shared__ __attribute__((aligned(16))) int32_t sp[GATHER ? KMAX : 4];
   __shared__ float red[WAVES][RW];
   __shared__ float gscale[RW];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -242,35 +251,54 @@ __global__ __launch_bounds__(512) void rq_composite1_kernel(const uint16_t* __re
   const int nb = K / kCB;
   const int vpr = K / 8;
 
-  for (int p0 = tid; p0 < RW * vpr; p0 += 512 * 8) {
-    uint4 v[8];
-    bool ok[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int p = p0 + u * 512;
-      const int r = p / vpr, c8 = p - r * vpr;
-      ok[u] = p < RW * vpr && row0 + r < M;
-      const int64_t gr = ok[u] ? row0 + r : 0;
-      v[u] = *reinterpret_cast<const uint4*>(X + gr * ldx + (ok[u] ? c8 * 8 : 0));
+  if constexpr (GATHER) {
+    for (int p0 = tid; p0 < RW * vpr; p0 += 512 * 8) {
+      uint4 v[8];
+      bool ok[8];
+  #pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int p = p0 + u * 512;
+        const int r = p / vpr, c8 = p - r * vpr;
+        ok[u] = p < RW * vpr && row0 + r < M;
+        const int64_t gr = ok[u] ? row0 + r : 0;
+        v[u] = *reinterpret_cast<const uint4*>(X + gr * ldx + (ok[u] ? c8 * 8 : 0));
+      }
+  #pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int p = p0 + u * 512;
+        const int r = p / vpr, c8 = p - r * vpr;
+        if (p < RW * vpr) *reinterpret_cast<uint4*>(&sx[r * XS + c8 * 8]) = ok[u] ? v[u] : make_uint4(0, 0, 0, 0);
+      }
     }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int p = p0 + u * 512;
-      const int r = p / vpr, c8 = p - r * vpr;
-      if (p < RW * vpr) *reinterpret_cast<uint4*>(&sx[r * XS + c8 * 8]) = ok[u] ? v[u] : make_uint4(0, 0, 0, 0);
+    for (int k4 = tid; k4 < K / 4; k4 += 512) {
+      int4 pv = *reinterpret_cast<const int4*>(perm + 4 * k4);
+      pv.x = min(max(pv.x, 0), K - 1);
+      pv.y = min(max(pv.y, 0), K - 1);
+      pv.z = min(max(pv.z, 0), K - 1);
+      pv.w = min(max(pv.w, 0), K - 1);
+      *reinterpret_cast<int4*>(&sp[4 * k4]) = pv;
     }
-  }
-  for (int k4 = tid; k4 < K / 4; k4 += 512) {
-    int4 pv = *reinterpret_cast<const int4*>(perm + 4 * k4);
-    pv.x = min(max(pv.x, 0), K - 1);
-    pv.y = min(max(pv.y, 0), K - 1);
-    pv.z = min(max(pv.z, 0), K - 1);
-    pv.w = min(max(pv.w, 0), K - 1);
-    *reinterpret_cast<int4*>(&sp[4 * k4]) = pv;
   }
   __syncthreads();
 
   const int r16 = lane & 15, q = lane >> 4;
+  // Without a permutation (X already in the permuted channel order): the A
+  // fragment of rows rg*16 .. + 15 and k step kk of block b is one 16-byte
+  // load per lane straight from global memory; rows past M read row 0 and
+  // are zeroed where used.
+  bool rv[RG];
+#pragma unroll
+  for (int rg = 0; rg < RG; ++rg) rv[rg] = row0 + rg * 16 + r16 < M;
+  auto load_a = [&](int b, c8h (&f)[RG][2]) {
+    const int bb = b < nb ? b : 0;
+#pragma unroll
+    for (int rg = 0; rg < RG; ++rg) {
+      const int64_t gr = rv[rg] ? row0 + rg * 16 + r16 : 0;
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+        f[rg][kk] = *reinterpret_cast<const c8h*>(X + gr * ldx + bb * kCB + kk * 32 + 8 * q);
+    }
+  };
   auto gather = [&](int b, int kk, int rg) -> c8h {
     const int k0 = b * kCB + kk * 32 + 8 * q;
     const int4 pa = *reinterpret_cast<const int4*>(&sp[k0]);
@@ -301,7 +329,9 @@ __global__ __launch_bounds__(512) void rq_composite1_kernel(const uint16_t* __re
                                                   kk * 32 + 8 * q);
   };
   c8h bnext[4][2];
+  c8h anext[GATHER ? 1 : RG][2];
   load_b(wave, bnext);
+  if constexpr (!GATHER) load_a(wave, anext);
 #pragma unroll
   for (int i = 0; i < NBW; ++i) {
     const int b = wave + WAVES * i;
@@ -311,12 +341,30 @@ __global__ __launch_bounds__(512) void rq_composite1_kernel(const uint16_t* __re
       bf[cb][0] = bnext[cb][0];
       bf[cb][1] = bnext[cb][1];
     }
-    if (i + 1 < NBW) load_b(b + WAVES, bnext);
+    c8h af[GATHER ? 1 : RG][2];
+    if constexpr (!GATHER) {
+#pragma unroll
+      for (int rg = 0; rg < RG; ++rg) {
+        af[rg][0] = anext[rg][0];
+        af[rg][1] = anext[rg][1];
+      }
+    }
+    if (i + 1 < NBW) {
+      load_b(b + WAVES, bnext);
+      if constexpr (!GATHER) load_a(b + WAVES, anext);
+    }
     __builtin_amdgcn_sched_barrier(0);
     if (b < nb) {
 #pragma unroll
       for (int rg = 0; rg < RG; ++rg) {
-        const c8h a0 = gather(b, 0, rg), a1 = gather(b, 1, rg);
+        c8h a0, a1;
+        if constexpr (GATHER) {
+          a0 = gather(b, 0, rg);
+          a1 = gather(b, 1, rg);
+        } else {
+          a0 = rv[rg] ? af[rg][0] : c8h{};
+          a1 = rv[rg] ? af[rg][1] : c8h{};
+        }
 #pragma unroll
         for (int cb = 0; cb < 4; ++cb) {
           c4f acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, bf[cb][0], c4f{0, 0, 0, 0}, 0, 0, 0);
@@ -377,21 +425,21 @@ __global__ __launch_bounds__(512) void rq_composite1_kernel(const uint16_t* __re
   }
 }
 
-template <int RG, int KMAX>
+template <int RG, int KMAX, bool GATHER = true>
 int launch_composite1(const void* X, int64_t M, int64_t K, int64_t ldx, const int32_t* perm, const void* Rt,
                       float s, uint8_t* Xq, float* x_scale, hipStream_t stream) {
   const unsigned grid = static_cast<unsigned>((M + 16 * RG - 1) / (16 * RG));
-  hipLaunchKernelGGL((rq_composite1_kernel<RG, KMAX>), dim3(grid), dim3(512), 0, stream,
+  hipLaunchKernelGGL((rq_composite1_kernel<RG, KMAX, GATHER>), dim3(grid), dim3(512), 0, stream,
                      static_cast<const uint16_t*>(X), M, static_cast<int>(K), ldx, perm,
                      static_cast<const uint16_t*>(Rt), s, Xq, x_scale);
   return launch_status();
 }
 
-template <int RW, int KMAX>
+template <int RW, int KMAX, bool GATHER = true>
 int launch_composite(const void* X, int64_t M, int64_t K, int64_t ldx, const int32_t* perm, const void* Rt,
                      float s, uint8_t* Xq, float* x_scale, hipStream_t stream) {
   const unsigned grid = static_cast<unsigned>((M + RW - 1) / RW);
-  hipLaunchKernelGGL((rq_composite_kernel<RW, KMAX, 2>), dim3(grid), dim3(256), 0, stream,
+  hipLaunchKernelGGL((rq_composite_kernel<RW, KMAX, 2, GATHER>), dim3(grid), dim3(256), 0, stream,
                      static_cast<const uint16_t*>(X), M, static_cast<int>(K), ldx, perm,
                      static_cast<const uint16_t*>(Rt), s, Xq, x_scale);
   return launch_status();
@@ -407,8 +455,8 @@ extern "C" int oq_rotate_quantize_act_composite(const void* X, int64_t M, int64_
   if (ldx % 8 != 0) return OQ_ERR_ALIGN;
   if (t < 0) return OQ_ERR_ARG;
   if (M == 0) return OQ_OK;
-  if (!X || !perm || !Rt || !Xq || !x_scale) return OQ_ERR_NULL;
-  if (!oq::aligned(X, 16) || !oq::aligned(perm, 16) || !oq::aligned(Rt, 16) || !oq::aligned(Xq, 16) ||
+  if (!X || !Rt || !Xq || !x_scale) return OQ_ERR_NULL;
+  if (!oq::aligned(X, 16) || (perm && !oq::aligned(perm, 16)) || !oq::aligned(Rt, 16) || !oq::aligned(Xq, 16) ||
       !oq::aligned(x_scale, 4))
     return OQ_ERR_ALIGN;
   const float s = s_table ? s_table[t] : 1.0f;
@@ -416,6 +464,15 @@ extern "C" int oq_rotate_quantize_act_composite(const void* X, int64_t M, int64_
   int st = oq::device_check();
   if (st != OQ_OK) return st;
   hipStream_t h = static_cast<hipStream_t>(stream);
+  // Without a permutation the rows are read straight into the MFMA operands
+  // (no LDS staging): row groups sized to the register budget.
+  if (!perm) {
+    if (K <= 1024) return oq::launch_composite1<2, 1024, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+    if (K <= 2048) return oq::launch_composite1<2, 2048, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+    if (K <= 4096) return oq::launch_composite1<1, 4096, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+    if (K <= 8192) return oq::launch_composite<16, 8192, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+    return oq::launch_composite<16, 16384, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+  }
   // Single pass (y in registers) up to K = 4096, row groups sized to the
   // LDS budget; deeper rows take the two-pass kernel.
   // Few rows: one row group per workgroup, so the rows spread over more CUs.

@@ -1,5 +1,7 @@
 """Online full composite rotation (zigzag permutation, block 64 SVD factor
-times Hadamard) + step scale + per-token int4 codes against the oracle (GPU).
+times Hadamard) + step scale + per-token int4 codes against the oracle (GPU),
+with the permutation applied online and with it folded into the producer
+(perm = NULL, the input already in the permuted order).
 
 The oracle is fed the same fp16 activation and the same fp16 block matrices
 (as float64).  The GPU forms the exact fp16 x fp16 products and sums each
@@ -74,6 +76,39 @@ def test_composite_codes(M, K, s):
     rel = np.abs(xs.cpu().numpy().astype(np.float64) - xs_o) / np.where(xs_o > 0, xs_o, 1.0)
     assert np.all(rel <= tau / 7 + 4 * U32)
     print(f"  boundary code differences {n_mis} of {M * K}")
+
+
+@pytest.mark.parametrize("M,K,s", CASES)
+def test_composite_prepermuted_codes(M, K, s):
+    """perm = NULL: the activation arrives already in the permuted channel
+    order (P folded into its producer); the codes of X P through R_hat equal
+    the oracle's composite transform of X with P (same boundary rule)."""
+    print(f"composite prepermuted M={M} K={K} s={s}", flush=True)
+    x16, _, perm, r16 = _operands(5100 + M + K, M, 96, K)
+    _, rt = _device(perm, r16)
+    Xp = torch.from_numpy(np.ascontiguousarray(x16[:, perm])).to(DEV)
+    Xq, xs = oq.rotate_quantize_act_composite(Xp, None, rt, s_table=np.array([s], np.float32), t=0)
+    torch.cuda.synchronize()
+    q_o, xs_o, r_o = composite.rotate_quantize_composite(x16, perm, r16.astype(np.float64), float(np.float32(s)))
+    tau = _tau(x16, perm, r16)
+    n_mis, _ = parity.check_codes(parity.unpack_int4(Xq.cpu().numpy()), q_o, r_o, tau)
+    rel = np.abs(xs.cpu().numpy().astype(np.float64) - xs_o) / np.where(xs_o > 0, xs_o, 1.0)
+    assert np.all(rel <= tau / 7 + 4 * U32)
+    print(f"  boundary code differences {n_mis} of {M * K}")
+
+
+def test_composite_prepermuted_strided_rows_and_zero_row():
+    M, K = 40, 2048
+    x16, _, perm, r16 = _operands(78, M, 64, K)
+    x16[7] = 0
+    buf = torch.zeros((M, K + 64), dtype=torch.float16, device=DEV)
+    buf[:, :K] = torch.from_numpy(np.ascontiguousarray(x16[:, perm])).to(DEV)
+    _, rt = _device(perm, r16)
+    Xq, xs = oq.rotate_quantize_act_composite(buf[:, :K], None, rt)
+    torch.cuda.synchronize()
+    q_o, xs_o, r_o = composite.rotate_quantize_composite(x16, perm, r16.astype(np.float64))
+    parity.check_codes(parity.unpack_int4(Xq.cpu().numpy()), q_o, r_o, _tau(x16, perm, r16))
+    assert xs.cpu().numpy()[7] == 0 and not Xq.cpu().numpy()[7].any()
 
 
 def test_composite_strided_rows_and_zero_row():

@@ -2,7 +2,8 @@
 the GPU weight preparation, in the configurations bench.py times, checked
 on sampled outputs that the oracle computes one by one (GPU).
 
-  * composite rotate-quantize at M = 16384, K = 1024 and 4096: sampled rows'
+  * composite rotate-quantize at M = 16384, K = 1024 and 4096 (and with the
+    permutation folded into the input, K = 1024, 4096, 16384): sampled rows'
     codes by the boundary rule against the oracle fed the same fp16 R_b;
   * static rotate-quantize at M = 16384, K = 4096: sampled rows by the
     static boundary rule;
@@ -32,10 +33,12 @@ def _rows(M, n, seed):
     return np.unique(np.concatenate([rng.choice(M, n, replace=False), [0, M - 1]]))
 
 
-@pytest.mark.parametrize("K", [1024, 4096])
-def test_composite_full_size_sampled(K):
+@pytest.mark.parametrize("K,folded", [(1024, False), (4096, False), (1024, True), (4096, True), (16384, True)])
+def test_composite_full_size_sampled(K, folded):
+    """folded: perm = None on the input already in the permuted order (the
+    GPU is handed X P, the oracle X and P)."""
     M = 16384
-    print(f"composite full size M={M} K={K}", flush=True)
+    print(f"composite full size M={M} K={K} folded={folded}", flush=True)
     energy = G.gaussian(11, f"composite/energy{K}", (K,)) ** 2
     perm = composite.zigzag_permutation(energy, K // 64)
     u = np.stack([G.random_orthogonal(11, f"composite/u{K}/{b}", 64) for b in range(K // 64)])
@@ -44,7 +47,10 @@ def test_composite_full_size_sampled(K):
     X = torch.randn((M, K), generator=g, device=DEV).half()
     p = torch.from_numpy(perm.astype(np.int32)).to(DEV)
     rt = torch.from_numpy(np.ascontiguousarray(np.transpose(r16, (0, 2, 1))).view(np.int16)).to(DEV)
-    Xq, xs = oq.rotate_quantize_act_composite(X, p, rt)
+    if folded:
+        Xq, xs = oq.rotate_quantize_act_composite(X[:, p.long()].contiguous(), None, rt)
+    else:
+        Xq, xs = oq.rotate_quantize_act_composite(X, p, rt)
     torch.cuda.synchronize()
     rows = _rows(M, 48, K)
     ri = torch.from_numpy(rows).to(DEV)
