@@ -467,6 +467,9 @@ extern "C" int oq_rotate_quantize_act_composite(const void* X, int64_t M, int64_
   // Without a permutation the rows are read straight into the MFMA operands
   // (no LDS staging): row groups sized to the register budget.
   if (!perm) {
+    // Few rows: one row group per workgroup, so the rows spread over more CUs.
+    if (M <= 1024 && K <= 1024) return oq::launch_composite1<1, 1024, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+    if (M <= 1024 && K <= 2048) return oq::launch_composite1<1, 2048, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
     if (K <= 1024) return oq::launch_composite1<2, 1024, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
     if (K <= 2048) return oq::launch_composite1<2, 2048, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
     if (K <= 4096) return oq::launch_composite1<1, 4096, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
