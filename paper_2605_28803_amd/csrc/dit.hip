@@ -942,7 +942,9 @@ struct FusedLaunch {
 
 FusedLaunch fused_launch(int64_t M, int64_t K, const RQPlan& p) {
   const int T = 1 << p.logT;
-  const int threads = T >= 256 ? T : 256;
+  // Few rows (the action tokens): one row per workgroup, so the rows spread
+  // over as many CUs as there are rows; else 256-thread workgroups.
+  const int threads = T >= 256 || M <= 256 ? T : 256;
   const int rows_per_wg = threads / T;
   FusedLaunch f;
   f.grid = dim3(static_cast<unsigned>((M + rows_per_wg - 1) / rows_per_wg));
