@@ -633,7 +633,11 @@ int oq_dit_in_projection(oq_dit* h, const float* x, float* resid, void* stream);
  * row-major, M = batch * tokens rows), for per-site parity checks: every
  * quantized linear's fp16 input and every fp16 output of the block can be
  * compared with the oracle fed the GPU's own upstream values.  Pointers into
- * the workspace, valid until the next call on the handle. */
+ * the workspace, valid until the next call on the handle.  The fp16 linear
+ * inputs h1, attn, h2 and act are written by oq_dit_run_block and
+ * oq_dit_run_block_until only (oq_dit_step and oq_dit_denoise produce their
+ * codes without storing them; gr00t's cross-attention output, which its
+ * quantizer reads back, is the exception). */
 typedef struct {
   const void* h1;        /* [M][D]  norm output, input of the q|k|v (q) linear  */
   const void* qkv;       /* [M][3D] q|k|v linear output (gr00t even: q, [M][D]) */

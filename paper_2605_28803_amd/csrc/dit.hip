@@ -157,7 +157,7 @@ __global__ __launch_bounds__(256) void norm_rq_kernel(const float* __restrict__ 
       const float y = (v[c][j] - mu) * inv * gg[c][j];
       v[c][j] = f16r(fmaf(y, s1[c][j], y) + s2[c][j]);
     }
-    if (m.valid) store8_f16(h + m.row * D + k, v[c]);
+    if (m.valid && h) store8_f16(h + m.row * D + k, v[c]);
   }
   rqd::rq_core<C>(v, m, D, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr, o.tiled, o.sdelta);
 }
@@ -218,7 +218,7 @@ __global__ __launch_bounds__(256) void gelu_rq_kernel(const uint16_t* __restrict
   }
 #pragma unroll
   for (int c = 0; c < C; ++c)
-    if (m.valid) store8_f16(act + m.row * F + rqd::chan(m, c, 0), v[c]);
+    if (m.valid && act) store8_f16(act + m.row * F + rqd::chan(m, c, 0), v[c]);
   rqd::rq_core<C>(v, m, F, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr, o.tiled, o.sdelta);
 }
 
@@ -687,7 +687,7 @@ __global__ __launch_bounds__(256) void combine_rq_kernel(AttnArgs a, int64_t M, 
     const float inv = 1.0f / den;
 #pragma unroll
     for (int j = 0; j < 8; ++j) v[c][j] = m.valid ? f16r(num[j] * inv) : 0.0f;
-    if (m.valid) store8_f16(a.out + m.row * a.out_ld + k, v[c]);
+    if (m.valid && a.out) store8_f16(a.out + m.row * a.out_ld + k, v[c]);
   }
   rqd::rq_core<C>(v, m, a.D, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr, o.tiled, o.sdelta);
 }
@@ -1029,7 +1029,7 @@ int gemm(oq_dit* h, const oq_qweight& wt, int64_t K, int64_t N, Epilogue epi, vo
 // pre_ld) followed by `own` rows of the q|k|v buffer.
 int attention_rq(oq_dit* h, const uint16_t* q, int64_t q_ld, const uint16_t* k_pre, const uint16_t* v_pre,
                  int P, int64_t pre_ld, const uint16_t* k_own, const uint16_t* v_own, int64_t own_ld, int own,
-                 float s, hipStream_t st, const float* sdelta) {
+                 float s, hipStream_t st, const float* sdelta, bool keep) {
   const oq_dit_config& c = h->cfg;
   const int64_t M = static_cast<int64_t>(c.batch) * c.tokens;
   const int64_t D = c.hidden;
@@ -1039,7 +1039,7 @@ int attention_rq(oq_dit* h, const uint16_t* q, int64_t q_ld, const uint16_t* k_p
   a.k_own = k_own; a.v_own = v_own; a.own_ld = own_ld; a.own_keys = own;
   a.part_o = at<float>(h, h->lay.part_o);
   a.part_ml = at<float>(h, h->lay.part_ml);
-  a.out = at<uint16_t>(h, h->lay.o); a.out_ld = D;
+  a.out = keep ? at<uint16_t>(h, h->lay.o) : nullptr; a.out_ld = D;
   a.S = c.tokens; a.H = c.n_heads; a.hd = c.head_dim; a.D = static_cast<int>(D);
   a.nsplit = (P + own + kAttnKS - 1) / kAttnKS;
   a.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(c.head_dim)));
@@ -1141,24 +1141,26 @@ SiteSet site_set(oq_dit* h, int l, int t) {
   return ss;
 }
 
-int run_block_pi(oq_dit* h, int l, int t, float* r, hipStream_t st, int until) {
+int run_block_pi(oq_dit* h, int l, int t, float* r, hipStream_t st, int until, bool keep) {
   const oq_dit_config& c = h->cfg;
   const oq_dit_block& bw = h->blocks[l];
   const int64_t D = c.hidden, F = c.mlp;
   const float* s = &h->s_table[(static_cast<size_t>(l) * c.steps + t) * 4];
   const SiteSet ss = site_set(h, l, t);
-  uint16_t* h1 = at<uint16_t>(h, h->lay.h1);
+  // The fp16 site inputs are kept in the workspace for the parity calls
+  // only; the producers write just the codes otherwise.
+  uint16_t* h1 = keep ? at<uint16_t>(h, h->lay.h1) : nullptr;
   uint16_t* qkv = at<uint16_t>(h, h->lay.qkv);
-  uint16_t* h2 = at<uint16_t>(h, h->lay.h2);
+  uint16_t* h2 = keep ? at<uint16_t>(h, h->lay.h2) : nullptr;
   uint16_t* gu = at<uint16_t>(h, h->lay.gu);
-  uint16_t* act = at<uint16_t>(h, h->lay.act);
+  uint16_t* act = keep ? at<uint16_t>(h, h->lay.act) : nullptr;
   int e;
   if ((e = norm_rq(h, r, bw.g1, mod_ptr(h, l, t, 0), mod_ptr(h, l, t, 1), h1, s[0], st, ss.d[0])) != OQ_OK) return e;
   if (until == 0) return OQ_OK;
   if ((e = gemm(h, *ss.w[0], D, 3 * D, EPI_F16, qkv, 3 * D, nullptr, st)) != OQ_OK) return e;
   if ((e = attention_rq(h, qkv, 3 * D, static_cast<const uint16_t*>(bw.prefix_k),
                         static_cast<const uint16_t*>(bw.prefix_v), c.prefix, D, qkv + D, qkv + 2 * D, 3 * D,
-                        c.tokens, s[1], st, ss.d[1])) != OQ_OK)
+                        c.tokens, s[1], st, ss.d[1], keep)) != OQ_OK)
     return e;
   if (until == 1) return OQ_OK;
   if ((e = gemm(h, *ss.w[1], D, D, EPI_RESID_F32, r, D, mod_ptr(h, l, t, 2), st)) != OQ_OK) return e;
@@ -1170,17 +1172,17 @@ int run_block_pi(oq_dit* h, int l, int t, float* r, hipStream_t st, int until) {
   return gemm(h, *ss.w[3], F, D, EPI_RESID_F32, r, D, mod_ptr(h, l, t, 5), st);
 }
 
-int run_block_gr00t(oq_dit* h, int l, int t, float* r, hipStream_t st, int until) {
+int run_block_gr00t(oq_dit* h, int l, int t, float* r, hipStream_t st, int until, bool keep) {
   const oq_dit_config& c = h->cfg;
   const oq_dit_block& bw = h->blocks[l];
   const int64_t D = c.hidden, F = c.mlp;
   const float* s = &h->s_table[(static_cast<size_t>(l) * c.steps + t) * 4];
   const SiteSet ss = site_set(h, l, t);
-  uint16_t* h1 = at<uint16_t>(h, h->lay.h1);
+  uint16_t* h1 = keep ? at<uint16_t>(h, h->lay.h1) : nullptr;
   uint16_t* qkv = at<uint16_t>(h, h->lay.qkv);
-  uint16_t* h2 = at<uint16_t>(h, h->lay.h2);
+  uint16_t* h2 = keep ? at<uint16_t>(h, h->lay.h2) : nullptr;
   uint16_t* ff = at<uint16_t>(h, h->lay.gu);
-  uint16_t* act = at<uint16_t>(h, h->lay.act);
+  uint16_t* act = keep ? at<uint16_t>(h, h->lay.act) : nullptr;
   int e;
   if ((e = norm_rq(h, r, bw.g1, mod_ptr(h, l, t, 0), mod_ptr(h, l, t, 1), h1, s[0], st, ss.d[0])) != OQ_OK) return e;
   if (until == 0) return OQ_OK;
@@ -1191,7 +1193,7 @@ int run_block_gr00t(oq_dit* h, int l, int t, float* r, hipStream_t st, int until
   } else {
     if ((e = gemm(h, *ss.w[0], D, 3 * D, EPI_F16, qkv, 3 * D, nullptr, st)) != OQ_OK) return e;
     if ((e = attention_rq(h, qkv, 3 * D, nullptr, nullptr, 0, 0, qkv + D, qkv + 2 * D, 3 * D, c.tokens, s[1], st,
-                          ss.d[1])) != OQ_OK)
+                          ss.d[1], keep)) != OQ_OK)
       return e;
   }
   if (until == 1) return OQ_OK;
@@ -1205,8 +1207,8 @@ int run_block_gr00t(oq_dit* h, int l, int t, float* r, hipStream_t st, int until
   return gemm(h, *ss.w[3], F, D, EPI_RESID_F32, r, D, nullptr, st);
 }
 
-int run_block(oq_dit* h, int l, int t, float* r, hipStream_t st, int until = 4) {
-  return is_gr00t(h->cfg) ? run_block_gr00t(h, l, t, r, st, until) : run_block_pi(h, l, t, r, st, until);
+int run_block(oq_dit* h, int l, int t, float* r, hipStream_t st, int until = 4, bool keep = true) {
+  return is_gr00t(h->cfg) ? run_block_gr00t(h, l, t, r, st, until, keep) : run_block_pi(h, l, t, r, st, until, keep);
 }
 
 int run_step(oq_dit* h, float* x, int t, hipStream_t st) {
@@ -1219,7 +1221,7 @@ int run_step(oq_dit* h, float* x, int t, hipStream_t st) {
   int e = launch_status();
   if (e != OQ_OK) return e;
   for (int l = 0; l < c.n_blocks; ++l)
-    if ((e = run_block(h, l, t, r, st)) != OQ_OK) return e;
+    if ((e = run_block(h, l, t, r, st, 4, false)) != OQ_OK) return e;
   const float dt = (is_gr00t(c) ? 1.0f : -1.0f) / static_cast<float>(c.steps);
   const size_t lds = static_cast<size_t>(4) * c.hidden * sizeof(float);
   const dim3 fgrid(static_cast<unsigned>((M + 3) / 4));
