@@ -150,3 +150,18 @@ def test_dit_config_validation_without_gpu(lib):
     assert lib.oq_dit_set_condition(None, P16, None) == NULL
     assert lib.oq_dit_step(None, P16, 0, None) == NULL
     assert lib.oq_dit_create(C.byref(good), None, C.byref(C.c_void_p())) == NULL
+
+
+def test_leading_dimension_of_single_rows():
+    """A single row may carry any row stride (numpy gives the size-1 axis of
+    a fancy-indexed copy its own value, which torch.from_numpy keeps); the
+    binding then passes the row length as the leading dimension, and the row
+    stride otherwise."""
+    import torch
+    perm = np.random.default_rng(0).permutation(64)
+    one = torch.from_numpy(np.ascontiguousarray(np.zeros((1, 64), np.float16)[:, perm]))
+    assert oq._ld(one) == 64
+    assert oq._ld(torch.zeros((3, 64), dtype=torch.float16)) == 64
+    assert oq._ld(torch.zeros((3, 80), dtype=torch.float16)[:, :64]) == 80
+    assert oq._ld(torch.zeros((1, 80), dtype=torch.float16)[:, :64]) == 64
+    assert oq._ld(torch.zeros((0, 64), dtype=torch.float16)) == 64
