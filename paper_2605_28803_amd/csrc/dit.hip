@@ -162,6 +162,142 @@ __global__ __launch_bounds__(256) void norm_rq_kernel(const float* __restrict__ 
   rqd::rq_core<C>(v, m, D, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr, o.tiled, o.sdelta);
 }
 
+// ---------------------------------------------------------------------------
+// The RMS-norm producer for 1024-channel rows with few rows (the Pi-0.5 action
+// tokens, per-token quantizer, Hadamard block = the row): 256 threads per row,
+// 4 consecutive channels per thread (channel 4 t + j), so each thread's chain
+// of arithmetic is half that of the 128-thread generic layout.  Channel bits
+// 0-1 are in registers, bits 2-7 across the lanes of a wave, bits 8-9 across
+// the four waves (one exchange through LDS).  Same arithmetic as
+// norm_rq_kernel and rqd::rq_core; only the order of the fp32 sums differs.
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float wave_sum64(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+  return v;
+}
+
+template <int H>
+__device__ __forceinline__ void lane_stage4(float (&x)[4], int lane) {
+  const float sgn = (lane & H) ? -1.0f : 1.0f;
+  float p[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) p[j] = rqd::lane_xor<H>(x[j]);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) x[j] = fmaf(sgn, x[j], p[j]);  // upper: p - x, lower: p + x
+}
+
+template <int H>
+__device__ __forceinline__ void lane_stage4_swap(float (&x)[4]) {
+#pragma unroll
+  for (int j = 0; j < 4; j += 2) {
+    float a = x[j], b = x[j + 1];
+    rqd::permlane_swap<H>(a, b);
+    const float sm = a + b, df = a - b;
+    a = sm;
+    b = df;
+    rqd::permlane_swap<H>(a, b);
+    x[j] = a;
+    x[j + 1] = b;
+  }
+}
+
+template <bool SC>
+__global__ __launch_bounds__(256) void norm_rq1024_kernel(const float* __restrict__ r,
+                                                          const uint16_t* __restrict__ g,
+                                                          const uint16_t* __restrict__ sc,
+                                                          const uint16_t* __restrict__ sh, uint16_t* __restrict__ h,
+                                                          int64_t M, RQOut o) {
+  constexpr int D = 1024;
+  __shared__ __attribute__((aligned(16))) float xch[D];
+  __shared__ float red[2][4];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int64_t row = blockIdx.x;
+  const bool valid = row < M;
+  const int k0 = 4 * t;
+  const float4 rv = *reinterpret_cast<const float4*>(r + (valid ? row : 0) * D + k0);
+  const uint2 gq = *reinterpret_cast<const uint2*>(g + k0);
+  const uint2 hq = *reinterpret_cast<const uint2*>(sh + k0);
+  uint2 cq = make_uint2(0, 0);
+  if (SC) cq = *reinterpret_cast<const uint2*>(sc + k0);
+  const float v[4] = {rv.x, rv.y, rv.z, rv.w};
+  const float gg[4] = {h2f(gq.x & 0xFFFFu), h2f(gq.x >> 16), h2f(gq.y & 0xFFFFu), h2f(gq.y >> 16)};
+  const float s2[4] = {h2f(hq.x & 0xFFFFu), h2f(hq.x >> 16), h2f(hq.y & 0xFFFFu), h2f(hq.y >> 16)};
+  const float s1[4] = {SC ? h2f(cq.x & 0xFFFFu) : 0.0f, SC ? h2f(cq.x >> 16) : 0.0f,
+                       SC ? h2f(cq.y & 0xFFFFu) : 0.0f, SC ? h2f(cq.y >> 16) : 0.0f};
+  float ss = 0.0f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) ss = fmaf(v[j], v[j], ss);
+  ss = wave_sum64(ss);
+  if (lane == 0) red[0][w] = ss;
+  __syncthreads();
+  ss = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
+  const float inv = 1.0f / sqrtf(ss / static_cast<float>(D) + kEps);
+  float x[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const float y = v[j] * inv * gg[j];
+    x[j] = valid ? f16r(fmaf(y, s1[j], y) + s2[j]) : 0.0f;
+  }
+  if (valid && h)
+    *reinterpret_cast<uint2*>(h + row * D + k0) =
+        make_uint2(static_cast<uint32_t>(f2h(x[0])) | (static_cast<uint32_t>(f2h(x[1])) << 16),
+                   static_cast<uint32_t>(f2h(x[2])) | (static_cast<uint32_t>(f2h(x[3])) << 16));
+  // Channel bits 0-1.
+  {
+    const float a0 = x[0] + x[1], a1 = x[0] - x[1], a2 = x[2] + x[3], a3 = x[2] - x[3];
+    x[0] = a0 + a2;
+    x[2] = a0 - a2;
+    x[1] = a1 + a3;
+    x[3] = a1 - a3;
+  }
+  // Channel bits 2-7: lane bits 0-5.
+  lane_stage4<1>(x, lane);
+  lane_stage4<2>(x, lane);
+  lane_stage4<4>(x, lane);
+  lane_stage4<8>(x, lane);
+  lane_stage4_swap<16>(x);
+  lane_stage4_swap<32>(x);
+  // Channel bits 8-9: the four waves.
+  *reinterpret_cast<float4*>(&xch[k0]) = make_float4(x[0], x[1], x[2], x[3]);
+  __syncthreads();
+  {
+    float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float sg = (__popc(w & u) & 1) ? -1.0f : 1.0f;
+      const float4 q = *reinterpret_cast<const float4*>(&xch[(u * 64 + lane) * 4]);
+      acc[0] = fmaf(sg, q.x, acc[0]);
+      acc[1] = fmaf(sg, q.y, acc[1]);
+      acc[2] = fmaf(sg, q.z, acc[2]);
+      acc[3] = fmaf(sg, q.w, acc[3]);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) x[j] = acc[j];
+  }
+  // Row maximum of the unnormalized transform, scales, codes (as rq_core).
+  float amax = fmaxf(fmaxf(fabsf(x[0]), fabsf(x[1])), fmaxf(fabsf(x[2]), fabsf(x[3])));
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) amax = fmaxf(amax, __shfl_xor(amax, m, 64));
+  if (lane == 0) red[1][w] = amax;
+  __syncthreads();
+  amax = fmaxf(fmaxf(red[1][0], red[1][1]), fmaxf(red[1][2], red[1][3]));
+  const float a_z = amax * o.s_over_sqrtb;
+  const float delta = a_z / 7.0f;
+  const float gm = delta > 0.0f ? o.s_over_sqrtb / delta : 0.0f;
+  if (!valid) return;
+  if (t == 0) o.xs[row] = delta / o.s_t;
+  uint32_t c[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) c[j] = __float_as_uint(fmaf(x[j], gm, rqd::kRoundMagic)) & 0xFu;
+  // Byte i: channel 2i in the low nibble, 2i + 1 in the high nibble.
+  const uint16_t packed = static_cast<uint16_t>(c[0] | (c[1] << 4) | (c[2] << 8) | (c[3] << 12));
+  const int p = k0 / 2;  // even: both bytes in one 16-byte piece of the tiled layout
+  uint8_t* dst = o.tiled ? o.xq + tiled_offset(row, p, D / 128) : o.xq + row * (D / 2) + p;
+  *reinterpret_cast<uint16_t*>(dst) = packed;
+}
+
 // gelu_tanh(x) = 0.5 x (1 + tanh(u)), u = sqrt(2/pi) (x + 0.044715 x^3).
 // Since 0.5 (1 + tanh(u)) = 1 / (1 + e^(-2u)), this is x / (1 + e^(-2u)):
 // one hardware exp and one reciprocal (each within a few fp32 ulp; the result
@@ -979,6 +1115,15 @@ int norm_rq(oq_dit* h, const float* r, const void* g, const uint16_t* sc, const 
   const uint16_t* gg = static_cast<const uint16_t*>(g);
   const bool ln = is_gr00t(h->cfg);
   if (!sh) return OQ_ERR_NULL;
+  if (!ln && !sdelta && D == 1024 && o.logb == 10 && M <= 256) {
+    if (sc)
+      hipLaunchKernelGGL(norm_rq1024_kernel<true>, dim3(static_cast<unsigned>(M)), dim3(256), 0, st, r, gg, sc, sh,
+                         out, M, o);
+    else
+      hipLaunchKernelGGL(norm_rq1024_kernel<false>, dim3(static_cast<unsigned>(M)), dim3(256), 0, st, r, gg, sc, sh,
+                         out, M, o);
+    return launch_status();
+  }
   const bool ok = with_chunks(p.chunks, [&](auto C) {
     constexpr int CC = decltype(C)::value;
     if (ln && sc)
