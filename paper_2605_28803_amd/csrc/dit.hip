@@ -203,6 +203,71 @@ __device__ __forceinline__ void lane_stage4_swap(float (&x)[4]) {
   }
 }
 
+// Rotation over the whole 1024-channel row (Hadamard block = K) and the
+// per-token int4 codes of a row held as 4 channels per thread (channel
+// 4 t + j) by a 256-thread workgroup: channel bits 0-1 in registers, bits 2-7
+// across the lanes, bits 8-9 across the four waves through LDS (xch: 1024
+// floats; red: 4 floats, both unused by the caller meanwhile).  Every thread
+// calls it.
+__device__ __forceinline__ void rq1024_row(float (&x)[4], int64_t row, bool valid, const RQOut& o, float* xch,
+                                           float* red) {
+  constexpr int D = 1024;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int k0 = 4 * t;
+  // Channel bits 0-1.
+  {
+    const float a0 = x[0] + x[1], a1 = x[0] - x[1], a2 = x[2] + x[3], a3 = x[2] - x[3];
+    x[0] = a0 + a2;
+    x[2] = a0 - a2;
+    x[1] = a1 + a3;
+    x[3] = a1 - a3;
+  }
+  // Channel bits 2-7: lane bits 0-5.
+  lane_stage4<1>(x, lane);
+  lane_stage4<2>(x, lane);
+  lane_stage4<4>(x, lane);
+  lane_stage4<8>(x, lane);
+  lane_stage4_swap<16>(x);
+  lane_stage4_swap<32>(x);
+  // Channel bits 8-9: the four waves.
+  *reinterpret_cast<float4*>(&xch[k0]) = make_float4(x[0], x[1], x[2], x[3]);
+  __syncthreads();
+  {
+    float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float sg = (__popc(w & u) & 1) ? -1.0f : 1.0f;
+      const float4 q = *reinterpret_cast<const float4*>(&xch[(u * 64 + lane) * 4]);
+      acc[0] = fmaf(sg, q.x, acc[0]);
+      acc[1] = fmaf(sg, q.y, acc[1]);
+      acc[2] = fmaf(sg, q.z, acc[2]);
+      acc[3] = fmaf(sg, q.w, acc[3]);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) x[j] = acc[j];
+  }
+  // Row maximum of the unnormalized transform, scales, codes (as rq_core).
+  float amax = fmaxf(fmaxf(fabsf(x[0]), fabsf(x[1])), fmaxf(fabsf(x[2]), fabsf(x[3])));
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) amax = fmaxf(amax, __shfl_xor(amax, m, 64));
+  if (lane == 0) red[w] = amax;
+  __syncthreads();
+  amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  const float a_z = amax * o.s_over_sqrtb;
+  const float delta = a_z / 7.0f;
+  const float gm = delta > 0.0f ? o.s_over_sqrtb / delta : 0.0f;
+  if (!valid) return;
+  if (t == 0) o.xs[row] = delta / o.s_t;
+  uint32_t c[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) c[j] = __float_as_uint(fmaf(x[j], gm, rqd::kRoundMagic)) & 0xFu;
+  // Byte i: channel 2i in the low nibble, 2i + 1 in the high nibble.
+  const uint16_t packed = static_cast<uint16_t>(c[0] | (c[1] << 4) | (c[2] << 8) | (c[3] << 12));
+  const int p = k0 / 2;  // even: both bytes in one 16-byte piece of the tiled layout
+  uint8_t* dst = o.tiled ? o.xq + tiled_offset(row, p, D / 128) : o.xq + row * (D / 2) + p;
+  *reinterpret_cast<uint16_t*>(dst) = packed;
+}
+
 template <bool SC>
 __global__ __launch_bounds__(256) void norm_rq1024_kernel(const float* __restrict__ r,
                                                           const uint16_t* __restrict__ g,
@@ -244,58 +309,7 @@ __global__ __launch_bounds__(256) void norm_rq1024_kernel(const float* __restric
     *reinterpret_cast<uint2*>(h + row * D + k0) =
         make_uint2(static_cast<uint32_t>(f2h(x[0])) | (static_cast<uint32_t>(f2h(x[1])) << 16),
                    static_cast<uint32_t>(f2h(x[2])) | (static_cast<uint32_t>(f2h(x[3])) << 16));
-  // Channel bits 0-1.
-  {
-    const float a0 = x[0] + x[1], a1 = x[0] - x[1], a2 = x[2] + x[3], a3 = x[2] - x[3];
-    x[0] = a0 + a2;
-    x[2] = a0 - a2;
-    x[1] = a1 + a3;
-    x[3] = a1 - a3;
-  }
-  // Channel bits 2-7: lane bits 0-5.
-  lane_stage4<1>(x, lane);
-  lane_stage4<2>(x, lane);
-  lane_stage4<4>(x, lane);
-  lane_stage4<8>(x, lane);
-  lane_stage4_swap<16>(x);
-  lane_stage4_swap<32>(x);
-  // Channel bits 8-9: the four waves.
-  *reinterpret_cast<float4*>(&xch[k0]) = make_float4(x[0], x[1], x[2], x[3]);
-  __syncthreads();
-  {
-    float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const float sg = (__popc(w & u) & 1) ? -1.0f : 1.0f;
-      const float4 q = *reinterpret_cast<const float4*>(&xch[(u * 64 + lane) * 4]);
-      acc[0] = fmaf(sg, q.x, acc[0]);
-      acc[1] = fmaf(sg, q.y, acc[1]);
-      acc[2] = fmaf(sg, q.z, acc[2]);
-      acc[3] = fmaf(sg, q.w, acc[3]);
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) x[j] = acc[j];
-  }
-  // Row maximum of the unnormalized transform, scales, codes (as rq_core).
-  float amax = fmaxf(fmaxf(fabsf(x[0]), fabsf(x[1])), fmaxf(fabsf(x[2]), fabsf(x[3])));
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) amax = fmaxf(amax, __shfl_xor(amax, m, 64));
-  if (lane == 0) red[1][w] = amax;
-  __syncthreads();
-  amax = fmaxf(fmaxf(red[1][0], red[1][1]), fmaxf(red[1][2], red[1][3]));
-  const float a_z = amax * o.s_over_sqrtb;
-  const float delta = a_z / 7.0f;
-  const float gm = delta > 0.0f ? o.s_over_sqrtb / delta : 0.0f;
-  if (!valid) return;
-  if (t == 0) o.xs[row] = delta / o.s_t;
-  uint32_t c[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) c[j] = __float_as_uint(fmaf(x[j], gm, rqd::kRoundMagic)) & 0xFu;
-  // Byte i: channel 2i in the low nibble, 2i + 1 in the high nibble.
-  const uint16_t packed = static_cast<uint16_t>(c[0] | (c[1] << 4) | (c[2] << 8) | (c[3] << 12));
-  const int p = k0 / 2;  // even: both bytes in one 16-byte piece of the tiled layout
-  uint8_t* dst = o.tiled ? o.xq + tiled_offset(row, p, D / 128) : o.xq + row * (D / 2) + p;
-  *reinterpret_cast<uint16_t*>(dst) = packed;
+  rq1024_row(x, row, valid, o, xch, red[1]);
 }
 
 // gelu_tanh(x) = 0.5 x (1 + tanh(u)), u = sqrt(2/pi) (x + 0.044715 x^3).
@@ -828,6 +842,58 @@ __global__ __launch_bounds__(256) void combine_rq_kernel(AttnArgs a, int64_t M, 
   rqd::rq_core<C>(v, m, a.D, o.logb, o.s_t, o.s_over_sqrtb, lds, red, o.xq, o.xs, nullptr, o.tiled, o.sdelta);
 }
 
+// combine_rq_kernel for 1024-channel rows with few rows (the Pi-0.5 action
+// tokens, per-token quantizer, Hadamard block = the row): 256 threads per row,
+// 4 consecutive channels (one head's) per thread; every split's statistics
+// and values are loaded before the first use (split indices past nsplit
+// reread the last split and get weight 0), then rq1024_row.
+__global__ __launch_bounds__(256) void combine_rq1024_kernel(AttnArgs a, int64_t M, RQOut o) {
+  __shared__ __attribute__((aligned(16))) float xch[1024];
+  __shared__ float red[4];
+  const int t = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  const bool valid = row < M;
+  const int64_t rr = valid ? row : 0;
+  const int b = static_cast<int>(rr / a.S), q = static_cast<int>(rr % a.S);
+  const int k0 = 4 * t;
+  const int h = k0 / a.hd, d = k0 - h * a.hd;
+  const int64_t bh = static_cast<int64_t>(b) * a.H + h;
+  const float* ml = a.part_ml + bh * a.nsplit * a.S * 2 + 2 * q;
+  const float* po = a.part_o + bh * a.nsplit * a.S * a.hd + static_cast<int64_t>(q) * a.hd + d;
+  const int slast = a.nsplit - 1;
+  float2 st[kMaxSplits];
+  float4 pv[kMaxSplits];
+#pragma unroll
+  for (int s = 0; s < kMaxSplits; ++s) {
+    const int sc = min(s, slast);
+    st[s] = *reinterpret_cast<const float2*>(ml + static_cast<int64_t>(sc) * a.S * 2);
+    pv[s] = *reinterpret_cast<const float4*>(po + static_cast<int64_t>(sc) * a.S * a.hd);
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int s = 0; s < kMaxSplits; ++s) mx = fmaxf(mx, s < a.nsplit ? st[s].x : -INFINITY);
+  float den = 0.0f;
+  float num[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int s = 0; s < kMaxSplits; ++s) {
+    const float wgt = s < a.nsplit ? __expf(st[s].x - mx) : 0.0f;
+    den = fmaf(wgt, st[s].y, den);
+    num[0] = fmaf(wgt, pv[s].x, num[0]);
+    num[1] = fmaf(wgt, pv[s].y, num[1]);
+    num[2] = fmaf(wgt, pv[s].z, num[2]);
+    num[3] = fmaf(wgt, pv[s].w, num[3]);
+  }
+  const float inv = 1.0f / den;
+  float x[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) x[j] = valid ? f16r(num[j] * inv) : 0.0f;
+  if (valid && a.out)
+    *reinterpret_cast<uint2*>(a.out + row * a.out_ld + k0) =
+        make_uint2(static_cast<uint32_t>(f2h(x[0])) | (static_cast<uint32_t>(f2h(x[1])) << 16),
+                   static_cast<uint32_t>(f2h(x[2])) | (static_cast<uint32_t>(f2h(x[3])) << 16));
+  rq1024_row(x, row, valid, o, xch, red);
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
   for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
   return v;
@@ -1209,6 +1275,10 @@ int attention_rq(oq_dit* h, const uint16_t* q, int64_t q_ld, const uint16_t* k_p
   if (e != OQ_OK) return e;
   RQPlan p;
   const RQOut ro = rq_out(h, D, s, &p, sdelta);
+  if (!sdelta && D == 1024 && ro.logb == 10 && M <= 256 && c.head_dim % 4 == 0) {
+    hipLaunchKernelGGL(combine_rq1024_kernel, dim3(static_cast<unsigned>(M)), dim3(256), 0, st, a, M, ro);
+    return launch_status();
+  }
   const FusedLaunch fl = fused_launch(M, D, p);
   const bool ok = with_chunks(p.chunks, [&](auto C) {
     hipLaunchKernelGGL((combine_rq_kernel<decltype(C)::value>), fl.grid, fl.block, fl.lds, st, a, M, ro);
