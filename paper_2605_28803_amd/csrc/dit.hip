@@ -164,7 +164,7 @@ __global__ __launch_bounds__(256) void norm_rq_kernel(const float* __restrict__ 
 
 // ---------------------------------------------------------------------------
 // The RMS-norm producer for 1024-channel rows with few rows (the Pi-0.5 action
-// tokens, per-token quantizer, Hadamard block = the row): 256 threads per row,
+// tokens, Hadamard block = the row; per-token or static steps): 256 threads per row,
 // 4 consecutive channels per thread (channel 4 t + j), so each thread's chain
 // of arithmetic is half that of the 128-thread generic layout.  Channel bits
 // 0-1 are in registers, bits 2-7 across the lanes of a wave, bits 8-9 across
@@ -203,12 +203,12 @@ __device__ __forceinline__ void lane_stage4_swap(float (&x)[4]) {
   }
 }
 
-// Rotation over the whole 1024-channel row (Hadamard block = K) and the
-// per-token int4 codes of a row held as 4 channels per thread (channel
-// 4 t + j) by a 256-thread workgroup: channel bits 0-1 in registers, bits 2-7
-// across the lanes, bits 8-9 across the four waves through LDS (xch: 1024
-// floats; red: 4 floats, both unused by the caller meanwhile).  Every thread
-// calls it.
+// Rotation over the whole 1024-channel row (Hadamard block = K) and the int4
+// codes (per-token, or with the static steps o.sdelta) of a row held as 4
+// channels per thread (channel 4 t + j) by a 256-thread workgroup: channel
+// bits 0-1 in registers, bits 2-7 across the lanes, bits 8-9 across the four
+// waves through LDS (xch: 1024 floats; red: 4 floats, both unused by the
+// caller meanwhile).  Every thread calls it.
 __device__ __forceinline__ void rq1024_row(float (&x)[4], int64_t row, bool valid, const RQOut& o, float* xch,
                                            float* red) {
   constexpr int D = 1024;
@@ -246,6 +246,22 @@ __device__ __forceinline__ void rq1024_row(float (&x)[4], int64_t row, bool vali
 #pragma unroll
     for (int j = 0; j < 4; ++j) x[j] = acc[j];
   }
+  const int p = k0 / 2;  // even: both bytes in one 16-byte piece of the tiled layout
+  uint8_t* dst = o.tiled ? o.xq + tiled_offset(row, p, D / 128) : o.xq + row * (D / 2) + p;
+  uint32_t c[4];
+  if (o.sdelta != nullptr) {
+    // Static per-channel steps (as rq_core): token scale 1, no row maximum
+    // (the branch is uniform over the grid).
+    if (!valid) return;
+    if (t == 0) o.xs[row] = 1.0f;
+    const float4 d = *reinterpret_cast<const float4*>(o.sdelta + k0);
+    c[0] = rqd::static_code(x[0], d.x, o.s_over_sqrtb) & 0xFu;
+    c[1] = rqd::static_code(x[1], d.y, o.s_over_sqrtb) & 0xFu;
+    c[2] = rqd::static_code(x[2], d.z, o.s_over_sqrtb) & 0xFu;
+    c[3] = rqd::static_code(x[3], d.w, o.s_over_sqrtb) & 0xFu;
+    *reinterpret_cast<uint16_t*>(dst) = static_cast<uint16_t>(c[0] | (c[1] << 4) | (c[2] << 8) | (c[3] << 12));
+    return;
+  }
   // Row maximum of the unnormalized transform, scales, codes (as rq_core).
   float amax = fmaxf(fmaxf(fabsf(x[0]), fabsf(x[1])), fmaxf(fabsf(x[2]), fabsf(x[3])));
 #pragma unroll
@@ -258,14 +274,10 @@ __device__ __forceinline__ void rq1024_row(float (&x)[4], int64_t row, bool vali
   const float gm = delta > 0.0f ? o.s_over_sqrtb / delta : 0.0f;
   if (!valid) return;
   if (t == 0) o.xs[row] = delta / o.s_t;
-  uint32_t c[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) c[j] = __float_as_uint(fmaf(x[j], gm, rqd::kRoundMagic)) & 0xFu;
   // Byte i: channel 2i in the low nibble, 2i + 1 in the high nibble.
-  const uint16_t packed = static_cast<uint16_t>(c[0] | (c[1] << 4) | (c[2] << 8) | (c[3] << 12));
-  const int p = k0 / 2;  // even: both bytes in one 16-byte piece of the tiled layout
-  uint8_t* dst = o.tiled ? o.xq + tiled_offset(row, p, D / 128) : o.xq + row * (D / 2) + p;
-  *reinterpret_cast<uint16_t*>(dst) = packed;
+  *reinterpret_cast<uint16_t*>(dst) = static_cast<uint16_t>(c[0] | (c[1] << 4) | (c[2] << 8) | (c[3] << 12));
 }
 
 template <bool SC>
@@ -843,7 +855,7 @@ __global__ __launch_bounds__(256) void combine_rq_kernel(AttnArgs a, int64_t M, 
 }
 
 // combine_rq_kernel for 1024-channel rows with few rows (the Pi-0.5 action
-// tokens, per-token quantizer, Hadamard block = the row): 256 threads per row,
+// tokens, Hadamard block = the row; per-token or static steps): 256 threads per row,
 // 4 consecutive channels (one head's) per thread; every split's statistics
 // and values are loaded before the first use (split indices past nsplit
 // reread the last split and get weight 0), then rq1024_row.
@@ -1181,7 +1193,7 @@ int norm_rq(oq_dit* h, const float* r, const void* g, const uint16_t* sc, const 
   const uint16_t* gg = static_cast<const uint16_t*>(g);
   const bool ln = is_gr00t(h->cfg);
   if (!sh) return OQ_ERR_NULL;
-  if (!ln && !sdelta && D == 1024 && o.logb == 10 && M <= 256) {
+  if (!ln && D == 1024 && o.logb == 10 && M <= 256) {
     if (sc)
       hipLaunchKernelGGL(norm_rq1024_kernel<true>, dim3(static_cast<unsigned>(M)), dim3(256), 0, st, r, gg, sc, sh,
                          out, M, o);
@@ -1275,7 +1287,7 @@ int attention_rq(oq_dit* h, const uint16_t* q, int64_t q_ld, const uint16_t* k_p
   if (e != OQ_OK) return e;
   RQPlan p;
   const RQOut ro = rq_out(h, D, s, &p, sdelta);
-  if (!sdelta && D == 1024 && ro.logb == 10 && M <= 256 && c.head_dim % 4 == 0) {
+  if (D == 1024 && ro.logb == 10 && M <= 256 && c.head_dim % 4 == 0) {
     hipLaunchKernelGGL(combine_rq1024_kernel, dim3(static_cast<unsigned>(M)), dim3(256), 0, st, a, M, ro);
     return launch_status();
   }
