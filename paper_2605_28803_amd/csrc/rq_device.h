@@ -78,6 +78,16 @@ __device__ __forceinline__ void permlane_swap(float& a, float& b) {
   b = __int_as_float(y);
 }
 
+// The same swap on two dwords: afterwards the lower half-group holds
+// (a[l], a[l+H]) and the upper half-group (b[l-H], b[l]).
+template <int H>
+__device__ __forceinline__ void dword_swap(uint32_t& a, uint32_t& b) {
+  float x = __uint_as_float(a), y = __uint_as_float(b);
+  permlane_swap<H>(x, y);
+  a = __float_as_uint(x);
+  b = __float_as_uint(y);
+}
+
 template <int H, int C>
 __device__ __forceinline__ void lane_stage_swap(float (&v)[C][8]) {
 #pragma unroll

@@ -275,14 +275,39 @@ __device__ __forceinline__ void rq_row(const rv8h (&cur)[NG], const rv8h& a1, co
     return;
   }
   uint8_t* qr = Xq + row * (K / 2);
+  if constexpr (NG % 4 == 0) {
+    // Four slots at a time: lane (cl, q) packs one dword (8 codes) of each,
+    // then a 4 x 4 transpose between the slot index and lane bits 4-5 (two
+    // permlane32 swaps, then two permlane16 swaps) leaves lane q with all four
+    // dwords of slot 4a + q -- the 32 codes of chunk cl, one 16-byte store.
 #pragma unroll
-  for (int s = 0; s < NG; ++s) {
-    uint32_t b[8];
+    for (int a = 0; a < NG / 4; ++a) {
+      uint32_t d[4];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) b[e] = __float_as_uint(fmaf(v[s][e], gm, rqd::kRoundMagic));
-    const int p = (group_of(s) * 16 + cl) * 16 + 4 * q;
-    uint8_t* dst = tiled ? Xq + tiled_offset(row, p, K / 128) : qr + p;
-    *reinterpret_cast<uint32_t*>(dst) = rqd::pack8(b);
+      for (int i = 0; i < 4; ++i) {
+        uint32_t b[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) b[e] = __float_as_uint(fmaf(v[4 * a + i][e], gm, rqd::kRoundMagic));
+        d[i] = rqd::pack8(b);
+      }
+      rqd::dword_swap<32>(d[0], d[2]);
+      rqd::dword_swap<32>(d[1], d[3]);
+      rqd::dword_swap<16>(d[0], d[1]);
+      rqd::dword_swap<16>(d[2], d[3]);
+      const int p = (group_of(4 * a + q) * 16 + cl) * 16;
+      uint8_t* dst = tiled ? Xq + tiled_offset(row, p, K / 128) : qr + p;
+      *reinterpret_cast<uint4*>(dst) = make_uint4(d[0], d[1], d[2], d[3]);
+    }
+  } else {
+#pragma unroll
+    for (int s = 0; s < NG; ++s) {
+      uint32_t b[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) b[e] = __float_as_uint(fmaf(v[s][e], gm, rqd::kRoundMagic));
+      const int p = (group_of(s) * 16 + cl) * 16 + 4 * q;
+      uint8_t* dst = tiled ? Xq + tiled_offset(row, p, K / 128) : qr + p;
+      *reinterpret_cast<uint32_t*>(dst) = rqd::pack8(b);
+    }
   }
 }
 
