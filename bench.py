@@ -85,6 +85,16 @@ def dit_linears(cfg):
     return [("qkv", D, 3 * D, M), ("o", D, D, M), ("gate_up", D, 2 * F, M), ("down", F, D, M)]
 
 
+def evict_mall(flush):
+    """Make the next launch cold: read a 512 MB buffer, twice the 256 MB MALL,
+    so that the cache holds clean lines of it and none of the timed kernel's
+    inputs.  A write of the buffer would do the same but leave up to 256 MB of
+    dirty lines whose write-back to HBM then overlaps the timed launch (for
+    rotate-quantize at M = 16384 that added 23-33 us)."""
+    import torch
+    flush.view(torch.int32).amax()
+
+
 def gemm_bytes(M, N, K, out_bytes):
     """Algorithmic HBM bytes of one W4A4 GEMM launch: packed codes of both
     operands, both scale vectors, the output (fp16 store, or fp32 residual
@@ -179,15 +189,16 @@ def roofline_gemm(stream=None):
 
 
 def prefill_kernels():
-    """One large shape of each kernel, cold (MALL flushed before each launch):
+    """One large shape of each kernel, cold (MALL evicted by a read before each launch):
     W4A4 GEMM at M = K = N = 16384 (int8-MFMA roofline) and rotate-quantize at
     M = K = 16384 (HBM roofline); and rotate-quantize back to back on 1.3 GB
-    inputs (the flush's own write-back no longer overlaps the timed launch)."""
+    inputs (every launch streams from HBM; its own outputs' write-back overlaps
+    the next launch as it would in a pipeline)."""
     import torch
     import paper_2605_28803_amd as oq
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
-    flush = torch.empty((512 << 20,), dtype=torch.uint8, device=dev)
+    flush = torch.ones((512 << 20,), dtype=torch.uint8, device=dev)
     M = K = N = 16384
     g = torch.Generator(device=dev).manual_seed(7)
     X = torch.randn((M, K), generator=g, device=dev).half()
@@ -200,7 +211,7 @@ def prefill_kernels():
     def cold(fn, reps):
         ts = []
         for _ in range(reps):
-            flush.fill_(1)
+            evict_mall(flush)
             s = torch.cuda.Event(enable_timing=True)
             e = torch.cuda.Event(enable_timing=True)
             s.record(stream)
@@ -211,13 +222,25 @@ def prefill_kernels():
         return float(np.median(ts))
     oq.w4a4_linear(Xq, xs, Wq, ws, Y=Y)
     t_r = cold(lambda: oq.rotate_quantize_act(X, K, Xq=Xq, x_scale=xs), 15)
+    ts = []
+    for _ in range(15):  # the same launch after a write flush, for comparison
+        flush.fill_(1)
+        s = torch.cuda.Event(enable_timing=True)
+        e = torch.cuda.Event(enable_timing=True)
+        s.record(stream)
+        oq.rotate_quantize_act(X, K, Xq=Xq, x_scale=xs)
+        e.record(stream)
+        e.synchronize()
+        ts.append(s.elapsed_time(e))
+    t_rw = float(np.median(ts))
     t_g = cold(lambda: oq.w4a4_linear(Xq, xs, Wq, ws, Y=Y), 15)
     out = {"gemm_M16384_K16384_N16384": {"us": round(t_g * 1e3, 1),
                                          "TOPs": round(2 * M * N * K / (t_g * 1e-3) / 1e12, 1),
                                          "frac_int8_peak": round(2 * M * N * K / (t_g * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4)},
            "rotate_quant_M16384_K16384": {"us": round(t_r * 1e3, 1),
                                           "GBs": round(rq_bytes(M, K) / (t_r * 1e-3) / 1e9, 1),
-                                          "frac_hbm_peak": round(rq_bytes(M, K) / (t_r * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}}
+                                          "frac_hbm_peak": round(rq_bytes(M, K) / (t_r * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                                          "after_write_flush_us": round(t_rw * 1e3, 1)}}
     del X, Xq, Y, Wq, flush
     torch.cuda.empty_cache()
     # Back to back on 1.3 GB (beyond the 256 MB MALL, so every launch streams
@@ -264,12 +287,12 @@ def composite_kernels():
     from workloads import generators as G
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
-    flush = torch.empty((512 << 20,), dtype=torch.uint8, device=dev)
+    flush = torch.ones((512 << 20,), dtype=torch.uint8, device=dev)
 
     def cold(fn, reps):
         ts = []
         for _ in range(reps):
-            flush.fill_(1)
+            evict_mall(flush)
             s = torch.cuda.Event(enable_timing=True)
             e = torch.cuda.Event(enable_timing=True)
             s.record(stream)
@@ -316,12 +339,12 @@ def static_scale_kernels():
     import paper_2605_28803_amd as oq
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
-    flush = torch.empty((512 << 20,), dtype=torch.uint8, device=dev)
+    flush = torch.ones((512 << 20,), dtype=torch.uint8, device=dev)
 
     def cold(fn, reps):
         ts = []
         for _ in range(reps):
-            flush.fill_(1)
+            evict_mall(flush)
             s = torch.cuda.Event(enable_timing=True)
             e = torch.cuda.Event(enable_timing=True)
             s.record(stream)
@@ -383,12 +406,12 @@ def w4a8_kernels():
     import paper_2605_28803_amd as oq
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
-    flush = torch.empty((512 << 20,), dtype=torch.uint8, device=dev)
+    flush = torch.ones((512 << 20,), dtype=torch.uint8, device=dev)
 
     def cold(fn, reps):
         ts = []
         for _ in range(reps):
-            flush.fill_(1)
+            evict_mall(flush)
             s = torch.cuda.Event(enable_timing=True)
             e = torch.cuda.Event(enable_timing=True)
             s.record(stream)
@@ -565,19 +588,19 @@ def gr00t_step():
 def prefill_linears():
     """The Gemma-2B-shaped prefill layer (816 tokens; q|k|v 2048 -> 2560, o,
     gate|up 2048 -> 32768, down 16384 -> 2048), each linear's rotate-quantize
-    and GEMM timed cold (MALL flushed before each launch)."""
+    and GEMM timed cold (MALL evicted by a read before each launch)."""
     import torch
     import paper_2605_28803_amd as oq
     from workloads import configs
     cfg = configs.PREFILL_GEMMA
     dev = torch.device("cuda:0")
-    flush = torch.empty((512 << 20,), dtype=torch.uint8, device=dev)
+    flush = torch.ones((512 << 20,), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
     def cold(fn, reps=10):
         ts = []
         for _ in range(reps):
-            flush.fill_(1)
+            evict_mall(flush)
             a = torch.cuda.Event(enable_timing=True)
             b = torch.cuda.Event(enable_timing=True)
             a.record(stream)
@@ -771,14 +794,14 @@ def run_dit(args):
 
 
 def run_sweep(args):
-    """Rotate-quantize and GEMM roofline sweep over M x (K = N); cold-ish timing
-    (a 512 MB buffer is rewritten between timed launches to evict the MALL)."""
+    """Rotate-quantize and GEMM roofline sweep over M x (K = N); cold timing
+    (a 512 MB buffer is read between timed launches to evict the MALL)."""
     import torch
     import paper_2605_28803_amd as oq
     from workloads import configs
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
-    flush = torch.empty((512 << 20,), dtype=torch.uint8, device=dev)
+    flush = torch.ones((512 << 20,), dtype=torch.uint8, device=dev)
     os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
     path = os.path.join(ROOT, "gpurun_out", "sweep.jsonl")
     Ms = [int(m) for m in args.sweep_m.split(",")] if args.sweep_m else list(configs.SWEEP.Ms)
@@ -798,7 +821,7 @@ def run_sweep(args):
                 def timed(fn, reps):
                     ts = []
                     for _ in range(reps):
-                        flush.fill_(1)
+                        evict_mall(flush)
                         s = torch.cuda.Event(enable_timing=True)
                         e = torch.cuda.Event(enable_timing=True)
                         s.record(stream)
