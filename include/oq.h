@@ -415,8 +415,9 @@ size_t oq_calibrate_workspace_bytes(int64_t K);
 /*
  * oq_calibrate_step_scales -- delta[j] = v_j / qmax, v_j the nearest-rank
  * p-th percentile of |Y[:, j]| over the n rows: the k-th smallest magnitude
- * with k = ceil(p / 100 * n) evaluated in double precision and clamped to
- * [1, n].  v_j is exact (an element of the column; selection over the bit
+ * with k = ceil(p n / 100) clamped to [1, n], p taken to 1e-6 percent and
+ * the product formed in integers (p = 99.9, n = 1000 gives k = 999, not the
+ * maximum).  v_j is exact (an element of the column; selection over the bit
  * patterns, NaN ordered above +inf); the division is done in double and
  * rounded once to fp32.
  * Y device fp32 [n][ldy]; delta device fp32 [K]; work device, 16-byte

@@ -40,14 +40,20 @@ written.  The Hadamard block of a linear is the largest power of two dividing
 its input size (the block-wise form of eq:blockdiag).
 
 Parity: the norms, the attention and the activation are pinned by closed
-forms and library routines in the tests; the step composes pinned pieces.
+forms and library routines in the tests.  The composition of a block (where
+the modulation scale, shift and gates act, which residual branch each gate
+scales, the prefix keys ahead of the own keys, per-sample attention, the
+conditioning k|v of the cross-attention blocks, gate against up) is pinned by
+two tiny blocks worked by hand (tests/golden/dit_block_pi.txt,
+dit_block_gr00t.txt) whose every quantization is exact, so their outputs are
+plain numbers; planted mistakes in each of those places fail that pin.
 """
 from __future__ import annotations
 
 import numpy as np
 
-from .linear import w4a4_linear
-from .quant import quantize_weights
+from .linear import dequant, int_gemm, w4a4_linear
+from .quant import quantize_weights, rotate_quantize_act, rotate_quantize_static
 
 EPS = 1e-6
 
@@ -127,14 +133,60 @@ def cond_kv(cfg, qblocks, cond):
     return out
 
 
-def block(cfg, w, qblocks, mod, s_table, r, l, t, B, S, prefix=None, ckv=None):
-    """Block l at step t on the residual r [B*S, D] (float64); returns the new residual."""
+def block_trace(cfg, w, qblocks, mod, s_table, r, l, t, B, S, prefix=None, ckv=None, forced=None,
+                static=None):
+    """Block l at step t on the residual r [B*S, D] (float64), every
+    intermediate returned in a dict.
+
+    Names: "h1" (first norm output), "qkv" (pi and odd gr00t blocks) or "q"
+    (even gr00t blocks), "attn", "r1" (residual after the attention branch),
+    "h2" (second norm output), "gate_up" (pi: [gate | up]; gr00t: the ff0
+    output before the GELU), "act", "r_out"; for each quantization site i
+    (0: q|k|v input, 1: o input, 2: gate|up / ff0 input, 3: down / ff2 input)
+    "codes{i}" = (q, x_scale, ratio) and "y{i}" = the linear's output before
+    fp16 rounding or the residual update.
+
+    forced (teacher forcing): a dict that may hold values another
+    implementation produced under the names "h1", "qkv", "q", "attn", "h2",
+    "gate_up", "act" and "codes{i}" = (q, x_scale).  A forced value is what
+    everything downstream of it uses; under its own name the result keeps
+    the oracle's value computed from the (forced) inputs upstream of it.  So
+    each operation is evaluated on the other implementation's own input.
+
+    static: None (per-token quantizer with the scalar step s_table[l, t, i])
+    or (delta, qweights_t): the per-channel static steps delta[i] of the four
+    sites at (l, t) and the weights folded with them, a dict like qblocks[l]
+    (eq:perstep_scale with the per-channel table; token scale 1)."""
     D, H, F = cfg.hidden, cfg.n_heads, cfg.mlp
-    blk, qb, m = w["blocks"][l], qblocks[l], mod[l][t]
+    blk, m = w["blocks"][l], mod[l][t]
     st = s_table[l, t]
+    fz = forced or {}
+    out = {}
+
+    def tf(name, own):
+        out[name] = own
+        v = fz.get(name)
+        return own if v is None else np.asarray(v, dtype=np.float64)
+
+    def site(i, x, name):
+        b = hadamard_block(x.shape[1])
+        if static is None:
+            q, xs, ratio = rotate_quantize_act(x, b, st[i])
+            qw, ws = qblocks[l][name]
+        else:
+            q, xs, ratio = rotate_quantize_static(x, b, static[0][i])
+            qw, ws = static[1][name]
+        out[f"codes{i}"] = (q, xs, ratio)
+        fq = fz.get(f"codes{i}")
+        if fq is not None:
+            q, xs = fq
+        y = dequant(int_gemm(q, qw), xs, ws)
+        out[f"y{i}"] = y
+        return y
+
     if cfg.arch == "pi":
-        h = f16(rms_norm(r) * blk["g1"] * (1.0 + m["sc1"]) + m["sh1"])
-        qkv = f16(_lin(h, qb, "wqkv", st[0]))
+        h = tf("h1", f16(rms_norm(r) * blk["g1"] * (1.0 + m["sc1"]) + m["sh1"]))
+        qkv = tf("qkv", f16(site(0, h, "wqkv")))
         o = np.empty((B * S, D))
         Kp, Vp = prefix
         for b in range(B):
@@ -142,31 +194,42 @@ def block(cfg, w, qblocks, mod, s_table, r, l, t, B, S, prefix=None, ckv=None):
             kk = np.concatenate([Kp[l, b], qkv[rows, D:2 * D]], axis=0)
             vv = np.concatenate([Vp[l, b], qkv[rows, 2 * D:]], axis=0)
             o[rows] = attention(qkv[rows, :D], kk, vv, H)
-        o = f16(o)
-        r = r + m["gt1"] * _lin(o, qb, "wo", st[1])
-        h2 = f16(rms_norm(r) * blk["g2"] * (1.0 + m["sc2"]) + m["sh2"])
-        gu = f16(_lin(h2, qb, "wgu", st[2]))
-        a = f16(gelu_tanh(gu[:, :F]) * gu[:, F:])
-        return r + m["gt2"] * _lin(a, qb, "wd", st[3])
+        o = tf("attn", f16(o))
+        r = r + m["gt1"] * site(1, o, "wo")
+        out["r1"] = r
+        h2 = tf("h2", f16(rms_norm(r) * blk["g2"] * (1.0 + m["sc2"]) + m["sh2"]))
+        gu = tf("gate_up", f16(site(2, h2, "wgu")))
+        a = tf("act", f16(gelu_tanh(gu[:, :F]) * gu[:, F:]))
+        out["r_out"] = r + m["gt2"] * site(3, a, "wd")
+        return out
     if cfg.arch == "gr00t":
-        h = f16(layer_norm(r) * blk["g1"] * (1.0 + m["sc1"]) + m["sh1"])
+        h = tf("h1", f16(layer_norm(r) * blk["g1"] * (1.0 + m["sc1"]) + m["sh1"]))
         o = np.empty((B * S, D))
         if l % 2 == 0:
-            q = f16(_lin(h, qb, "wq", st[0]))
+            q = tf("q", f16(site(0, h, "wq")))
+            kv = ckv[l]
             for b in range(B):
                 rows = slice(b * S, (b + 1) * S)
-                o[rows] = attention(q[rows], ckv[l][b, :, :D], ckv[l][b, :, D:], H)
+                o[rows] = attention(q[rows], kv[b, :, :D], kv[b, :, D:], H)
         else:
-            qkv = f16(_lin(h, qb, "wqkv", st[0]))
+            qkv = tf("qkv", f16(site(0, h, "wqkv")))
             for b in range(B):
                 rows = slice(b * S, (b + 1) * S)
                 o[rows] = attention(qkv[rows, :D], qkv[rows, D:2 * D], qkv[rows, 2 * D:], H)
-        o = f16(o)
-        r = r + _lin(o, qb, "wo", st[1])
-        h3 = f16(layer_norm(r) * blk["g3"] + blk["beta3"])
-        f = f16(gelu_tanh(_lin(h3, qb, "wff0", st[2])))
-        return r + _lin(f, qb, "wff2", st[3])
+        o = tf("attn", f16(o))
+        r = r + site(1, o, "wo")
+        out["r1"] = r
+        h3 = tf("h2", f16(layer_norm(r) * blk["g3"] + blk["beta3"]))
+        ff = tf("gate_up", f16(site(2, h3, "wff0")))
+        f = tf("act", f16(gelu_tanh(ff)))
+        out["r_out"] = r + site(3, f, "wff2")
+        return out
     raise ValueError(cfg.arch)
+
+
+def block(cfg, w, qblocks, mod, s_table, r, l, t, B, S, prefix=None, ckv=None):
+    """Block l at step t on the residual r [B*S, D] (float64); returns the new residual."""
+    return block_trace(cfg, w, qblocks, mod, s_table, r, l, t, B, S, prefix=prefix, ckv=ckv)["r_out"]
 
 
 def in_projection(w, x_t):

@@ -83,7 +83,8 @@ def quantize_weights(w_u: np.ndarray, b: int):
 # Per-step static activation scales (eq:perstep_scale, the per-(layer, step,
 # channel) table of the paper's text).  Reading: sigma_hat is the 99.9th
 # percentile of the magnitudes of the rotated activation over the calibration
-# rows (nearest rank: the k-th smallest |y| with k = ceil(p/100 n)), Delta_j =
+# rows (nearest rank: the k-th smallest |y| with k = ceil(p n / 100), p to
+# 1e-6 percent so that k is exact), Delta_j =
 # sigma_hat_j / q_max, and at inference q = clamp(round(y_j / Delta_j), -7, 7)
 # with the table in place of the per-token maximum (clipping is live).  The
 # per-channel step cannot be factored out of the sum over channels, so it is
@@ -91,12 +92,21 @@ def quantize_weights(w_u: np.ndarray, b: int):
 # quantized per output channel; the token scale is then 1.
 # ---------------------------------------------------------------------------
 
+def nearest_rank(p: float, n: int) -> int:
+    """k = ceil(p n / 100) clamped to [1, n], with p taken to a resolution of
+    1e-6 percent so that the product is formed exactly in integers: p = 99.9
+    and n = 1000 give k = 999 (the float product 99.9 / 100 * 1000 is
+    999.0000000000001, whose ceiling would be the maximum)."""
+    pm = int(round(float(p) * 1e6))  # p in units of 1e-6 percent
+    k = -(-(pm * int(n)) // 10 ** 8)
+    return min(max(k, 1), int(n))
+
+
 def percentile_abs(y: np.ndarray, p: float) -> np.ndarray:
     """Nearest-rank p-th percentile of |y| over rows, per column (float64 [K])."""
     a = np.abs(np.asarray(y, dtype=np.float64))
     n = a.shape[0]
-    k = int(np.ceil(p / 100.0 * n))
-    k = min(max(k, 1), n)
+    k = nearest_rank(p, n)
     return np.sort(a, axis=0)[k - 1]
 
 

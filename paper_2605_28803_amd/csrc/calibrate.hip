@@ -142,8 +142,12 @@ extern "C" int oq_calibrate_step_scales(const float* Y, int64_t n, int64_t K, in
   if (!oq::aligned(Y, 4) || !oq::aligned(delta, 4) || !oq::aligned(work, 16)) return OQ_ERR_ALIGN;
   int st = oq::device_check();
   if (st != OQ_OK) return st;
-  // Nearest rank: the k-th smallest with k = ceil(p / 100 * n), in [1, n].
-  int64_t k = static_cast<int64_t>(std::ceil(p / 100.0 * static_cast<double>(n)));
+  // Nearest rank: the k-th smallest with k = ceil(p n / 100), in [1, n].  p is
+  // taken to 1e-6 percent and the product formed in integers (pm n <= 1e8 *
+  // INT32_MAX < 2^63): in floating point 99.9 / 100 * 1000 = 999.0000000000001
+  // would round up to the maximum.
+  const int64_t pm = std::llround(p * 1e6);
+  int64_t k = (pm * n + 99999999) / 100000000;
   if (k < 1) k = 1;
   if (k > n) k = n;
   hipStream_t s = static_cast<hipStream_t>(stream);

@@ -372,19 +372,35 @@ def check_rotate_quantize_composite(rqc, rotate_quantize_act, seed=24):
 # Per-step static scales
 # --------------------------------------------------------------------------
 
+# Nearest ranks k = ceil(p n / 100) worked out by hand: p = 99.9 selects the
+# 999th of 1000, the 1998th of 2000, the 9990th of 10000 (never the maximum
+# when p n / 100 is a whole number), the 1000th of 1001 (1000.0 -> 1000 ...
+# 99.9 * 1001 / 100 = 999.999 -> 1000), the 7th of 7 and the 1st of 1; p = 50
+# the 500th of 1000 and the 4th of 7; p = 100 the last.
+PERCENTILE_RANKS = {(99.9, 1000): 999, (99.9, 2000): 1998, (99.9, 10000): 9990, (99.9, 1001): 1000,
+                    (99.9, 7): 7, (99.9, 1): 1, (50.0, 1000): 500, (50.0, 7): 4, (100.0, 1001): 1001}
+
+
 def check_percentile(percentile_abs, seed=50):
     rng = np.random.default_rng(seed)
+    for (p, n), k in PERCENTILE_RANKS.items():
+        # distinct magnitudes 1..n in a random order: the k-th smallest is k
+        y = (rng.permutation(n) + 1.0) * np.where(rng.random(n) < 0.5, -1.0, 1.0)
+        v = np.asarray(percentile_abs(y[:, None], p))
+        assert v.shape == (1,) and v[0] == float(k), (p, n, v, k)
     for n in (1, 7, 1000, 1001):
         y = rng.standard_normal((n, 5)) * np.array([1, 10, 0.1, 3, 0])
         for p in (50.0, 99.9, 100.0):
             v = np.asarray(percentile_abs(y, p))
             a = np.abs(y)
+            k = PERCENTILE_RANKS.get((p, n))
             for j in range(5):
-                # nearest rank: at least ceil(p n / 100) values <= v, fewer below v
-                k = max(1, int(np.ceil(p / 100.0 * n)))
-                assert np.count_nonzero(a[:, j] <= v[j]) >= k
-                assert np.count_nonzero(a[:, j] < v[j]) < k
+                # v is an element of the column; with the hand-worked rank, at
+                # least k values are <= v and fewer than k below it
                 assert v[j] in a[:, j]
+                if k is not None:
+                    assert np.count_nonzero(a[:, j] <= v[j]) >= k
+                    assert np.count_nonzero(a[:, j] < v[j]) < k
             if p == 100.0:
                 assert np.array_equal(v, a.max(axis=0))
 
@@ -470,3 +486,60 @@ def check_w4a8_error_bound(w4a8_linear, fwht, seed=60):
     bound = (dx / 2) * np.abs(wp).sum(1)[None, :] + (dw / 2) * np.abs(xp).sum(1)[:, None] + K * dx * dw / 4
     assert np.all(np.abs(r["y"] - exact) <= bound * (1 + 1e-12))
     assert np.abs(r["q"]).max() == 127
+
+
+# --------------------------------------------------------------------------
+# DiT block composition (two tiny blocks worked by hand, every quantization
+# exact; tests/golden/dit_block_pi.txt and dit_block_gr00t.txt)
+# --------------------------------------------------------------------------
+
+def _tiny_dit_cfg(arch):
+    from types import SimpleNamespace
+    return SimpleNamespace(arch=arch, hidden=4, mlp=4, n_heads=1, head_dim=4, steps=1)
+
+
+def _mat(v, cols):
+    return np.asarray(v, dtype=np.float64).reshape(-1, cols)
+
+
+def _check_named(out, g, prefix, names, tag):
+    for nm in names:
+        exp = _mat(g[prefix + nm], len(out[nm][0]) if np.ndim(out[nm]) == 2 else 1)
+        got = np.asarray(out[nm], dtype=np.float64).reshape(exp.shape)
+        assert np.allclose(got, exp, rtol=1e-12, atol=1e-12), (tag, nm, got, exp)
+
+
+def check_dit_block_pi(block_trace, quantize_block_weights):
+    g = load_golden_rows("dit_block_pi.txt")
+    cfg = _tiny_dit_cfg("pi")
+    blk = {"g1": g["g1"], "g2": g["g2"], "wqkv": _mat(g["wqkv"], 4), "wo": _mat(g["wo"], 4),
+           "wgu": _mat(g["wgu"], 4), "wd": _mat(g["wd"], 4)}
+    w = {"blocks": [blk]}
+    mod = [[{k: g[k] for k in ("sc1", "sh1", "gt1", "sc2", "sh2", "gt2")}]]
+    s_table = g["s"].reshape(1, 1, 4)
+    prefix = (g["kp"].reshape(1, 1, 2, 4), g["vp"].reshape(1, 1, 2, 4))
+    qb = quantize_block_weights(cfg, w["blocks"])
+    out = block_trace(cfg, w, qb, mod, s_table, _mat(g["r"], 4), 0, 0, 1, 1, prefix=prefix)
+    _check_named(out, g, "", ("h1", "qkv", "attn", "r1", "h2", "gate_up", "act", "r_out"), "pi")
+
+
+def check_dit_block_gr00t(block_trace, quantize_block_weights, cond_kv):
+    g = load_golden_rows("dit_block_gr00t.txt")
+    cfg = _tiny_dit_cfg("gr00t")
+    blocks, mod = [], []
+    for l, lin in ((0, ("wq", "wkv", "wo", "wff0", "wff2")), (1, ("wqkv", "wo", "wff0", "wff2"))):
+        p = f"b{l}_"
+        blk = {"g1": g[p + "g1"], "g3": g[p + "g3"], "beta3": g[p + "beta3"]}
+        for nm in lin:
+            blk[nm] = _mat(g[p + nm], 4)
+        blocks.append(blk)
+        mod.append([{"sc1": g[p + "sc1"], "sh1": g[p + "sh1"]}])
+    w = {"blocks": blocks}
+    s_table = np.stack([g["s"], g["s"][::-1]]).reshape(2, 1, 4)
+    qb = quantize_block_weights(cfg, blocks)
+    ckv = cond_kv(cfg, qb, g["cond"].reshape(2, 2, 4))
+    assert np.allclose(ckv[0].reshape(-1), g["ckv"], rtol=0, atol=1e-12), ckv[0]
+    for l, site0 in ((0, "q"), (1, "qkv")):
+        out = block_trace(cfg, w, qb, mod, s_table, _mat(g[f"b{l}_r"], 4), l, 0, 2, 1, ckv=ckv)
+        _check_named(out, g, f"b{l}_", ("h1", site0, "attn", "r1", "h2", "gate_up", "act", "r_out"),
+                     f"gr00t block {l}")

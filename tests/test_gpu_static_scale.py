@@ -84,6 +84,20 @@ def test_calibrate_exact_order_statistic(n, K, p):
     assert np.array_equal(d7.cpu().numpy(), d7_ref)
 
 
+@pytest.mark.parametrize("n,p,k", [(1000, 99.9, 999), (2000, 99.9, 1998), (10000, 99.9, 9990), (1001, 99.9, 1000)])
+def test_calibrate_literal_rank(n, p, k):
+    """Columns holding the magnitudes 1..n in random orders and signs: the
+    nearest rank worked by hand selects the value k (never the maximum when
+    p n / 100 is whole)."""
+    print(f"calibrate literal rank n={n} p={p}", flush=True)
+    rng = np.random.default_rng(n)
+    y = np.stack([(rng.permutation(n) + 1.0) * np.where(rng.random(n) < 0.5, -1.0, 1.0) for _ in range(64)], axis=1)
+    Y = torch.from_numpy(y.astype(np.float32)).to(DEV)
+    d = oq.calibrate_step_scales(Y, p=p, qmax=1.0)
+    torch.cuda.synchronize()
+    assert np.array_equal(d.cpu().numpy(), np.full(64, float(k), np.float32))
+
+
 def test_calibrate_strided_rows_and_repeat_calls():
     """Y with ldy > K (a column slice of a wider buffer); the workspace is
     reused by a second call of another size."""

@@ -4,6 +4,7 @@ import torch
 import torch.nn.functional as Fn
 
 from oracle import dit, quant
+from tests import oracle_pins as P
 from workloads import configs, dit_inputs
 
 
@@ -155,3 +156,31 @@ def test_step_scale_changes_only_boundary_codes():
     q2, xs2, _ = quant.rotate_quantize_act(x, 4096, 3.25)
     assert np.mean(q1 != q2) < 1e-5
     assert np.allclose(xs1, xs2, rtol=1e-14)
+
+
+def test_block_composition_golden_pi():
+    """A tiny Pi-style block worked by hand (every quantization exact)."""
+    P.check_dit_block_pi(dit.block_trace, dit.quantize_block_weights)
+
+
+def test_block_composition_golden_gr00t():
+    """Tiny GR00T-style cross- and self-attention blocks worked by hand."""
+    P.check_dit_block_gr00t(dit.block_trace, dit.quantize_block_weights, dit.cond_kv)
+
+
+def test_block_is_block_trace_output():
+    cfg = configs.DIT_PI
+    inp = dit_inputs.make_dit_inputs(cfg, n_blocks=1)
+    w = inp["w"]
+    qb = dit.quantize_block_weights(cfg, w["blocks"])
+    r = dit.in_projection(w, inp["x0"])
+    a = dit.block(cfg, w, qb, inp["mod"], inp["s_table"], r, 0, 2, 1, cfg.tokens, prefix=(inp["kp"], inp["vp"]))
+    tr = dit.block_trace(cfg, w, qb, inp["mod"], inp["s_table"], r, 0, 2, 1, cfg.tokens,
+                         prefix=(inp["kp"], inp["vp"]))
+    assert np.array_equal(a, tr["r_out"])
+    # Forcing every value with the oracle's own changes nothing.
+    forced = {k: tr[k] for k in ("h1", "qkv", "attn", "h2", "gate_up", "act")}
+    forced.update({f"codes{i}": tr[f"codes{i}"][:2] for i in range(4)})
+    tf = dit.block_trace(cfg, w, qb, inp["mod"], inp["s_table"], r, 0, 2, 1, cfg.tokens,
+                         prefix=(inp["kp"], inp["vp"]), forced=forced)
+    assert np.array_equal(tf["r_out"], a)

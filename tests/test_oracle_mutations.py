@@ -4,6 +4,7 @@ import numpy as np
 import pytest
 
 from oracle import composite, hadamard, quant, linear
+from oracle import dit as odit
 from tests import oracle_pins as P
 
 
@@ -143,3 +144,105 @@ def test_worked_example_rejects_qmax8():
         return q, d / s_t, r
     with pytest.raises(AssertionError):
         P.check_worked_example_activation(rq)
+
+
+# --------------------------------------------------------------------------
+# DiT block composition: each mutant is the oracle's block with one planted
+# misreading (of the modulation, a gate, the prefix keys, gate against up,
+# the conditioning tokens, the LayerNorm affine) or one misplaced operation.
+# --------------------------------------------------------------------------
+
+def _with_mod(fn):
+    def mutant(cfg, w, qb, mod, s_table, r, l, t, B, S, **kw):
+        mm = [[dict(x) for x in row] for row in mod]
+        fn(mm[l][t])
+        return odit.block_trace(cfg, w, qb, mm, s_table, r, l, t, B, S, **kw)
+    return mutant
+
+
+def _swap(a, b):
+    def f(m):
+        m[a], m[b] = m[b], m[a]
+    return f
+
+
+def _ones(name):
+    def f(m):
+        m[name] = np.ones_like(m[name])
+    return f
+
+
+def block_no_prefix(cfg, w, qb, mod, s_table, r, l, t, B, S, prefix=None, **kw):
+    kp, vp = prefix
+    return odit.block_trace(cfg, w, qb, mod, s_table, r, l, t, B, S, prefix=(kp[:, :, :0], vp[:, :, :0]), **kw)
+
+
+def block_gate_up_swapped(cfg, w, qb, mod, s_table, r, l, t, B, S, **kw):
+    F = cfg.mlp
+    qq = [dict(x) for x in qb]
+    qw, ws = qq[l]["wgu"]
+    order = np.r_[F:2 * F, 0:F]
+    qq[l]["wgu"] = (qw[order], ws[order])
+    return odit.block_trace(cfg, w, qq, mod, s_table, r, l, t, B, S, **kw)
+
+
+def block_pi_norm2_on_block_input(cfg, w, qb, mod, s_table, r, l, t, B, S, prefix=None, **kw):
+    """The second norm reads the block's input residual instead of the residual
+    after the attention branch."""
+    out = odit.block_trace(cfg, w, qb, mod, s_table, r, l, t, B, S, prefix=prefix)
+    blk, m = w["blocks"][l], mod[l][t]
+    h2 = odit.f16(odit.rms_norm(r) * blk["g2"] * (1.0 + m["sc2"]) + m["sh2"])
+    return odit.block_trace(cfg, w, qb, mod, s_table, r, l, t, B, S, prefix=prefix,
+                            forced={"h2": h2, "attn": out["attn"]})
+
+
+def block_gr00t_cond_of_sample0(cfg, w, qb, mod, s_table, r, l, t, B, S, ckv=None, **kw):
+    c = {k: np.repeat(v[:1], v.shape[0], axis=0) for k, v in ckv.items()}
+    return odit.block_trace(cfg, w, qb, mod, s_table, r, l, t, B, S, ckv=c, **kw)
+
+
+def block_gr00t_cond_k_v_swapped(cfg, w, qb, mod, s_table, r, l, t, B, S, ckv=None, **kw):
+    D = cfg.hidden
+    c = {k: np.concatenate([v[..., D:], v[..., :D]], axis=-1) for k, v in ckv.items()}
+    return odit.block_trace(cfg, w, qb, mod, s_table, r, l, t, B, S, ckv=c, **kw)
+
+
+def block_gr00t_attention_across_batch(cfg, w, qb, mod, s_table, r, l, t, B, S, **kw):
+    if l % 2 == 0:
+        return odit.block_trace(cfg, w, qb, mod, s_table, r, l, t, B, S, **kw)
+    return odit.block_trace(cfg, w, qb, mod, s_table, r, l, t, 1, B * S, **kw)
+
+
+def block_gr00t_ln3_affine_swapped(cfg, w, qb, mod, s_table, r, l, t, B, S, **kw):
+    ww = {"blocks": [dict(b) for b in w["blocks"]]}
+    b = ww["blocks"][l]
+    b["g3"], b["beta3"] = b["beta3"], b["g3"]
+    return odit.block_trace(cfg, ww, qb, mod, s_table, r, l, t, B, S, **kw)
+
+
+@pytest.mark.parametrize("impl", [
+    _with_mod(_swap("sc1", "sh1")),
+    _with_mod(_swap("sc2", "sh2")),
+    _with_mod(_ones("gt1")),
+    _with_mod(_ones("gt2")),
+    _with_mod(_swap("gt1", "gt2")),
+    block_no_prefix,
+    block_gate_up_swapped,
+    block_pi_norm2_on_block_input,
+], ids=["sc1_sh1", "sc2_sh2", "no_gt1", "no_gt2", "gates_swapped", "no_prefix", "gate_up_swapped",
+        "norm2_on_block_input"])
+def test_dit_block_pi_pin_rejects_mutant(impl):
+    with pytest.raises(AssertionError):
+        P.check_dit_block_pi(impl, odit.quantize_block_weights)
+
+
+@pytest.mark.parametrize("impl", [
+    _with_mod(_swap("sc1", "sh1")),
+    block_gr00t_cond_of_sample0,
+    block_gr00t_cond_k_v_swapped,
+    block_gr00t_attention_across_batch,
+    block_gr00t_ln3_affine_swapped,
+], ids=["sc1_sh1", "cond_of_sample0", "cond_k_v_swapped", "attention_across_batch", "ln3_affine_swapped"])
+def test_dit_block_gr00t_pin_rejects_mutant(impl):
+    with pytest.raises(AssertionError):
+        P.check_dit_block_gr00t(impl, odit.quantize_block_weights, odit.cond_kv)

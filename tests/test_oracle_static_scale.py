@@ -46,8 +46,16 @@ def test_static_pins_reject_mutants():
         wf = hadamard.fwht(w, b) * np.asarray(d)[: w.shape[0], None] if w.shape[0] <= len(d) else None
         return quant.quantize_sym(wf)
 
+    def pct_float_rank(y, p):
+        # the rank formed in floating point: 99.9 / 100 * 1000 = 999.0000000000001 -> 1000
+        a = np.sort(np.abs(np.asarray(y, np.float64)), axis=0)
+        n = a.shape[0]
+        return a[min(max(int(np.ceil(p / 100.0 * n)), 1), n) - 1]
+
     with pytest.raises(AssertionError):
         P.check_percentile(pct_wrong_rank)
+    with pytest.raises(AssertionError):
+        P.check_percentile(pct_float_rank)
     with pytest.raises(AssertionError):
         P.check_quantize_static(qs_no_clip)
     with pytest.raises((AssertionError, ValueError, TypeError)):
