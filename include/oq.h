@@ -630,6 +630,15 @@ int oq_dit_set_static_steps(oq_dit* h, const float* delta, const oq_qweight* ste
  * one (calibration rollouts).  Errors: OQ_ERR_NULL, OQ_ERR_ALIGN, OQ_ERR_HIP. */
 int oq_dit_in_projection(oq_dit* h, const float* x, float* resid, void* stream);
 
+/* The last stage of a step alone, on a caller residual (device fp32 [M][D],
+ * 16-byte aligned, read only): v = fp16(norm(resid) g_f) W_out^T + b_out and
+ * the Euler update x += dt v with dt = -1/T (pi) or +1/T (gr00t), x device
+ * fp32 [B][S][A] in place (Experimental Settings: T Euler steps).  With
+ * oq_dit_in_projection and oq_dit_run_block it rebuilds a step from its
+ * parts, for checking oq_dit_step against them bit for bit.
+ * Errors: OQ_ERR_NULL, OQ_ERR_ALIGN, OQ_ERR_HIP. */
+int oq_dit_final_stage(oq_dit* h, const float* resid, float* x, void* stream);
+
 /* Intermediate tensors of the most recent block the handle ran (fp16,
  * row-major, M = batch * tokens rows), for per-site parity checks: every
  * quantized linear's fp16 input and every fp16 output of the block can be

@@ -80,6 +80,7 @@ SIGNATURES = {
     "oq_dit_get_intermediates": (i32, [vp, C.POINTER(oq_dit_intermediates)]),
     "oq_dit_set_static_steps": (i32, [vp, vp, C.POINTER(oq_qweight)]),
     "oq_dit_in_projection": (i32, [vp, vp, vp, vp]),
+    "oq_dit_final_stage": (i32, [vp, vp, vp, vp]),
     "oq_quantize_weights_step": (i32, [vp, i64, i64, i64, i32, vp, vp, vp, vp]),
     "oq_dit_destroy": (None, [vp]),
 }

@@ -1097,6 +1097,7 @@ struct oq_dit_graph {
   float* x;
   int t0, n;
   hipGraphExec_t exec;
+  uint64_t last_use;
 };
 
 struct oq_dit {
@@ -1109,7 +1110,8 @@ struct oq_dit {
   size_t ws_bytes = 0;
   bool cond_ready = false;    // gr00t: conditioning k|v computed into this workspace
   hipStream_t cap = nullptr;  // capture stream (graphs are replayed on the caller's stream)
-  std::vector<oq_dit_graph> graphs;
+  std::vector<oq_dit_graph> graphs;  // at most kMaxGraphs, least recently used dropped
+  uint64_t graph_clock = 0;
   bool use_graphs = true;
   bool tiled = false;  // block linears' token codes in the 16-row tiled layout (M <= 64)
   // Static per-step, per-channel steps (null: the per-token quantizer with
@@ -1438,6 +1440,8 @@ int run_block(oq_dit* h, int l, int t, float* r, hipStream_t st, int until = 4, 
   return is_gr00t(h->cfg) ? run_block_gr00t(h, l, t, r, st, until, keep) : run_block_pi(h, l, t, r, st, until, keep);
 }
 
+int final_stage(oq_dit* h, const float* r, float* x, hipStream_t st);
+
 int run_step(oq_dit* h, float* x, int t, hipStream_t st) {
   const oq_dit_config& c = h->cfg;
   const int64_t M = static_cast<int64_t>(c.batch) * c.tokens;
@@ -1449,6 +1453,14 @@ int run_step(oq_dit* h, float* x, int t, hipStream_t st) {
   if (e != OQ_OK) return e;
   for (int l = 0; l < c.n_blocks; ++l)
     if ((e = run_block(h, l, t, r, st, 4, false)) != OQ_OK) return e;
+  return final_stage(h, r, x, st);
+}
+
+// x += dt * (fp16(norm(r) g_f) W_out^T + b_out): the final norm, the
+// out-projection and the Euler update of a step.
+int final_stage(oq_dit* h, const float* r, float* x, hipStream_t st) {
+  const oq_dit_config& c = h->cfg;
+  const int64_t M = static_cast<int64_t>(c.batch) * c.tokens;
   const float dt = (is_gr00t(c) ? 1.0f : -1.0f) / static_cast<float>(c.steps);
   const size_t lds = static_cast<size_t>(4) * c.hidden * sizeof(float);
   const dim3 fgrid(static_cast<unsigned>((M + 3) / 4));
@@ -1486,13 +1498,22 @@ int set_condition(oq_dit* h, const uint16_t* cond, hipStream_t st) {
   return OQ_OK;
 }
 
+// Replays still in flight finish before their executable graphs go.
 void drop_graphs(oq_dit* h) {
+  if (h->graphs.empty()) return;
+  hipDeviceSynchronize();
   for (auto& g : h->graphs) hipGraphExecDestroy(g.exec);
   h->graphs.clear();
 }
 
+// Captured step graphs kept per handle (keyed by state pointer, first step
+// and count); a denoising loop over one state buffer uses at most its T
+// single steps plus one whole-loop graph.
+constexpr size_t kMaxGraphs = 16;
+
 // Steps t0 .. t0+n-1 on x: replay the cached graph for (x, t0, n), capturing it
-// on the internal stream the first time.
+// on the internal stream the first time (that first call instantiates the
+// graph, a host-side allocation of the runtime; later calls allocate nothing).
 int run_steps(oq_dit* h, float* x, int t0, int n, hipStream_t st) {
   if (!h->use_graphs) {
     for (int t = t0; t < t0 + n; ++t) {
@@ -1501,9 +1522,21 @@ int run_steps(oq_dit* h, float* x, int t0, int n, hipStream_t st) {
     }
     return OQ_OK;
   }
+  ++h->graph_clock;
   for (auto& g : h->graphs)
-    if (g.x == x && g.t0 == t0 && g.n == n)
+    if (g.x == x && g.t0 == t0 && g.n == n) {
+      g.last_use = h->graph_clock;
       return hipGraphLaunch(g.exec, st) == hipSuccess ? OQ_OK : OQ_ERR_HIP;
+    }
+  if (h->graphs.size() >= kMaxGraphs) {
+    // Drop the least recently used capture once its replays have finished
+    // (its last one may have been enqueued on another caller stream).
+    hipDeviceSynchronize();
+    auto lru = std::min_element(h->graphs.begin(), h->graphs.end(),
+                                [](const oq_dit_graph& a, const oq_dit_graph& b) { return a.last_use < b.last_use; });
+    hipGraphExecDestroy(lru->exec);
+    h->graphs.erase(lru);
+  }
   if (hipStreamBeginCapture(h->cap, hipStreamCaptureModeThreadLocal) != hipSuccess) return OQ_ERR_HIP;
   int e = OQ_OK;
   for (int t = t0; t < t0 + n && e == OQ_OK; ++t) e = run_step(h, x, t, h->cap);
@@ -1517,7 +1550,7 @@ int run_steps(oq_dit* h, float* x, int t0, int n, hipStream_t st) {
   const hipError_t ie = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
   hipGraphDestroy(graph);
   if (ie != hipSuccess) return OQ_ERR_HIP;
-  h->graphs.push_back({x, t0, n, exec});
+  h->graphs.push_back({x, t0, n, exec, h->graph_clock});
   return hipGraphLaunch(exec, st) == hipSuccess ? OQ_OK : OQ_ERR_HIP;
 }
 
@@ -1684,6 +1717,12 @@ extern "C" int oq_dit_in_projection(oq_dit* h, const float* x, float* resid, voi
                      static_cast<hipStream_t>(stream), x, static_cast<const uint16_t*>(h->w.w_in),
                      static_cast<const uint16_t*>(h->w.b_in), resid, c.action_dim, c.hidden);
   return oq::launch_status();
+}
+
+extern "C" int oq_dit_final_stage(oq_dit* h, const float* resid, float* x, void* stream) {
+  if (!h || !resid || !x) return OQ_ERR_NULL;
+  if (!oq::aligned(x, 4) || !oq::aligned(resid, 16)) return OQ_ERR_ALIGN;
+  return oq::final_stage(h, resid, x, static_cast<hipStream_t>(stream));
 }
 
 extern "C" int oq_dit_get_intermediates(const oq_dit* h, oq_dit_intermediates* out) {

@@ -178,8 +178,8 @@ class DiT:
         h1 [M,D], qkv [M,3D], attn [M,D], h2 [M,D], gate_up [M,2F] (gr00t:
         ff0 output [M,F]), act [M,F], resid [M,D] (fp32) and, for gr00t,
         q [M,D] (the q output of a cross-attention block, stored with row
-        stride D where the q|k|v output of a self-attention block starts)
-        and cond_kv [n_cross, B*P, 2D]."""
+        stride D where the q|k|v output of a self-attention block starts).
+        The conditioning k|v: cond_kv_block(l)."""
         from . import _check
         it = _lib.oq_dit_intermediates()
         _check(self.lib.oq_dit_get_intermediates(self.handle, C.byref(it)), "oq_dit_get_intermediates")
@@ -200,9 +200,30 @@ class DiT:
         out["resid"] = view(it.resid, M * D, np.float32, (M, D))
         if gr:
             out["q"] = view(it.qkv, M * D, np.float16, (M, D))
-            nc = (self.cfg_c.n_blocks + 1) // 2
-            out["cond_kv"] = view(it.cond_kv, nc * self.MC * 2 * D, np.float16, (nc, self.MC, 2 * D))
         return out
+
+    def step_residual(self):
+        """fp32 residual after the last block of the most recent step
+        (workspace), as float64 [M, D]."""
+        from . import _check
+        it = _lib.oq_dit_intermediates()
+        _check(self.lib.oq_dit_get_intermediates(self.handle, C.byref(it)), "oq_dit_get_intermediates")
+        torch.cuda.synchronize(self.device)
+        M, D = self.M, self.cfg_c.hidden
+        off = it.resid - self.workspace.data_ptr()
+        return self.workspace[off: off + 4 * M * D].cpu().numpy().view(np.float32).reshape(M, D).astype(np.float64)
+
+    def cond_kv_block(self, l):
+        """gr00t: the conditioning k|v of cross-attention block l (even), fp16
+        values as float64 [B*P, 2D]."""
+        from . import _check
+        it = _lib.oq_dit_intermediates()
+        _check(self.lib.oq_dit_get_intermediates(self.handle, C.byref(it)), "oq_dit_get_intermediates")
+        torch.cuda.synchronize(self.device)
+        n = self.MC * 2 * self.cfg_c.hidden
+        off = it.cond_kv - self.workspace.data_ptr() + (l // 2) * n * 2
+        raw = self.workspace[off: off + 2 * n].cpu().numpy().view(np.float16)
+        return raw.reshape(self.MC, 2 * self.cfg_c.hidden).astype(np.float64)
 
     # ------------------------------------------------------------------
     # Static per-step, per-channel steps (the per-(layer, step, channel)
@@ -236,6 +257,14 @@ class DiT:
                "oq_dit_in_projection")
         return resid
 
+    def final_stage(self, resid, x, stream=None):
+        """x (fp32 [B, S, A], in place) += dt * out-projection of the final
+        norm of resid (fp32 [M, D])."""
+        from . import _check
+        _check(self.lib.oq_dit_final_stage(self.handle, resid.data_ptr(), x.data_ptr(), self._stream(stream)),
+               "oq_dit_final_stage")
+        return x
+
     def site_dims(self):
         D, F = self.cfg_c.hidden, self.cfg_c.mlp
         return (D, D, D, F), (0, D, 2 * D, 3 * D), 3 * D + F
@@ -256,8 +285,9 @@ class DiT:
         Y = {(l, t, i): torch.empty((n * M, Ks[i]), dtype=torch.float32, device=dev)
              for l in range(L) for t in range(T) for i in range(4)}
         r = torch.empty((M, self.cfg_c.hidden), dtype=torch.float32, device=dev)
+        x = torch.empty_like(x0s[0])  # one state buffer: the captured steps are reused
         for j, x0 in enumerate(x0s):
-            x = x0.clone()
+            x.copy_(x0)
             for t in range(T):
                 self.in_projection(x, r)
                 for l in range(L):

@@ -26,3 +26,16 @@ def pytest_collection_modifyitems(config, items):
     for item in items:
         if "gpu" in item.keywords:
             item.add_marker(skip)
+
+
+def pytest_terminal_summary(terminalreporter):
+    """Totals of the int4 code comparisons made in this run (tests/parity.py)."""
+    parity = sys.modules.get("tests.parity")
+    if parity is None or not parity.STATS["elements"]:
+        return
+    s = parity.STATS
+    terminalreporter.write_line(
+        "int4 code parity: {elements} elements, {mismatches} mismatches ({frac:.2e}), "
+        "{mismatches_beyond_1ulp} of them beyond 1 fp32 ulp of the boundary; {within_1ulp} elements within "
+        "1 ulp of a boundary; max |r_gpu - r_exact| = {max_ratio_err_ulp:.1f} ulp over {ratio_elements} "
+        "ratios".format(frac=s["mismatches"] / s["elements"], **s))

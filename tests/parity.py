@@ -113,22 +113,51 @@ def dist_to_boundary(r: np.ndarray) -> np.ndarray:
     return np.abs(np.abs(r - np.floor(r)) - 0.5)
 
 
-def check_codes(q_gpu, q_ref, r_ref, tau_row, qmax: int = 7):
-    """Returns (n_mismatch, n_boundary_1ulp) and asserts the code criterion."""
+# Running totals over every check_codes call of the session (reported at the
+# end of the run by tests/conftest.py): elements compared, code mismatches,
+# mismatches whose exact ratio lies more than one fp32 ulp from the rounding
+# boundary, elements within one ulp of a boundary, and the largest measured
+# |r_gpu - r_exact| in fp32 ulps of r_exact (where the GPU's ratios are known).
+STATS = {"elements": 0, "mismatches": 0, "mismatches_beyond_1ulp": 0, "within_1ulp": 0,
+         "ratio_elements": 0, "max_ratio_err_ulp": 0.0}
+
+
+def ulp32(r) -> np.ndarray:
+    """One fp32 ulp at |r| (float64 array)."""
+    return np.spacing(np.abs(np.asarray(r, dtype=np.float64)).astype(np.float32)).astype(np.float64)
+
+
+def check_codes(q_gpu, q_ref, r_ref, tau_row, qmax: int = 7, r_gpu=None, record=True):
+    """Returns (n_mismatch, n_boundary_1ulp) and asserts the code criterion.
+    r_gpu: optionally the GPU's own pre-rounding ratios, to measure their
+    distance from the exact ones in fp32 ulps.  record: add to STATS (off
+    where q_ref is not the oracle's)."""
     q_gpu = np.asarray(q_gpu)
     q_ref = np.asarray(q_ref)
     mism = q_gpu != q_ref
     n = int(mism.sum())
     total = q_ref.size
     tau = np.asarray(tau_row, dtype=np.float64)
-    near = dist_to_boundary(r_ref) <= (tau if tau.ndim == 2 else tau[:, None])
+    dist = dist_to_boundary(r_ref)
+    near = dist <= (tau if tau.ndim == 2 else tau[:, None])
     if n:
         assert np.all(np.abs(q_gpu[mism] - q_ref[mism]) == 1), "a code differs by more than one step"
         assert np.all(near[mism]), "a code differs away from a rounding boundary"
     assert n <= CODE_MISMATCH_FRAC * total, f"{n} code mismatches of {total}"
     assert q_gpu.min() >= -qmax and q_gpu.max() <= qmax, f"code outside [-{qmax}, {qmax}]"
-    ulp = np.spacing(np.abs(r_ref).astype(np.float32)).astype(np.float64)
-    n_ulp = int((dist_to_boundary(r_ref) <= ulp).sum())
+    ulp = ulp32(r_ref)
+    within = dist <= ulp
+    n_ulp = int(within.sum())
+    if not record:
+        return n, n_ulp
+    STATS["elements"] += int(total)
+    STATS["mismatches"] += n
+    STATS["mismatches_beyond_1ulp"] += int((mism & ~within).sum())
+    STATS["within_1ulp"] += n_ulp
+    if r_gpu is not None:
+        err = np.abs(np.asarray(r_gpu, dtype=np.float64) - r_ref) / np.maximum(ulp, np.finfo(np.float32).tiny)
+        STATS["ratio_elements"] += int(err.size)
+        STATS["max_ratio_err_ulp"] = max(STATS["max_ratio_err_ulp"], float(err.max()) if err.size else 0.0)
     return n, n_ulp
 
 

@@ -5,9 +5,10 @@ flips at a rounding boundary moves that row of the output by about
 Delta / (sqrt(K) rms) ~ 1.5% at K = 1024.  Tiny fp32-vs-fp64 differences
 upstream (attention, norms) therefore make whole-block or whole-step
 comparisons unstable at the 2e-3 level.  Parity is established per site with
-teacher forcing: every quantized linear and every glue operation of a block is
-checked against the oracle fed the GPU's own fp16 input of that operation
-(read back from the driver's intermediates):
+teacher forcing (tests/dit_parity.py): the oracle's block (block_trace) is run
+with every GPU site value forced, so each quantized linear and each glue
+operation of a block is checked against the oracle fed the GPU's own input of
+that operation (read back from the driver's intermediates):
   * activation codes of each linear input: the boundary rule of the rotate-
     quantize tests (at most 1e-4 of the elements, each one step, each within
     the fp32 error bound of a half integer);
@@ -25,9 +26,7 @@ import torch
 
 import paper_2605_28803_amd as oq
 from oracle import dit as odit
-from oracle import linear as olin
-from oracle import quant as oquant
-from tests import parity
+from tests import dit_parity, parity
 from workloads import configs, dit_inputs
 
 pytestmark = pytest.mark.gpu
@@ -45,87 +44,13 @@ def _setup(n_blocks, batch=None, cfg=configs.DIT_PI, zero_blocks=False):
     return cfg, inp, model
 
 
-def _gpu_codes(x, s):
-    """The library's codes / scales of an fp16 input (same kernel the driver runs)."""
-    K = x.shape[1]
-    X = torch.from_numpy(x.astype(np.float16)).to(DEV)
-    Xq, xs = oq.rotate_quantize_act(X, K & -K, s_table=np.array([s], np.float32), t=0)
-    torch.cuda.synchronize()
-    return parity.unpack_int4(Xq.cpu().numpy()), xs.cpu().numpy().astype(np.float64)
-
-
-def _site(x_gpu, s, qw, ws, tag):
-    """Code check of one linear input; returns the oracle's output from the GPU's codes."""
-    K = x_gpu.shape[1]
-    b = K & -K
-    q_g, xs_g = _gpu_codes(x_gpu, s)
-    q_o, xs_o, r_o = oquant.rotate_quantize_act(x_gpu, b, float(np.float32(s)))
-    n_mis, _ = parity.check_codes(q_g, q_o, r_o, parity.tau_rows(x_gpu, b))
-    assert np.allclose(xs_g, xs_o, rtol=1e-5), tag
-    return olin.dequant(olin.int_gemm(q_g, qw), xs_g, ws), n_mis
-
-
-def _weights(model, l):
-    out = {}
-    for nm, (Wq, ws) in model.qweights[l].items():
-        out[nm] = (parity.unpack_int4(Wq.cpu().numpy()), ws.cpu().numpy().astype(np.float64))
-    return out
-
-
-def _check_block(cfg, inp, model, l, t, r_in):
-    D, F, H = cfg.hidden, cfg.mlp, cfg.n_heads
-    B, S = inp["batch"], cfg.tokens
-    blk, m, st = inp["w"]["blocks"][l], inp["mod"][l][t], inp["s_table"][l, t]
-    r_t = torch.from_numpy(r_in.astype(np.float32)).to(DEV)
-    model.run_block(l, t, r_t)
-    torch.cuda.synchronize()
-    r_out = r_t.cpu().numpy().astype(np.float64)
-    it = model.intermediates()
-    W = _weights(model, l)
-    r = r_in.astype(np.float32).astype(np.float64)
-    errs = {}
-    # Norm 1.
-    h1 = odit.f16(odit.rms_norm(r) * blk["g1"] * (1.0 + m["sc1"]) + m["sh1"])
-    errs["h1"] = parity.rel_l2(it["h1"], h1)
-    # q|k|v linear.
-    y, n1 = _site(it["h1"], st[0], *W["wqkv"], "qkv")
-    errs["qkv"] = parity.rel_l2(it["qkv"], odit.f16(y))
-    # Attention on the GPU's q|k|v.
-    qkv = it["qkv"]
-    att = np.empty((B * S, D))
-    for b in range(B):
-        rows = slice(b * S, (b + 1) * S)
-        kk = np.concatenate([inp["kp"][l, b], qkv[rows, D:2 * D]])
-        vv = np.concatenate([inp["vp"][l, b], qkv[rows, 2 * D:]])
-        att[rows] = odit.attention(qkv[rows, :D], kk, vv, H)
-    errs["attn"] = parity.rel_l2(it["attn"], odit.f16(att))
-    # o linear and residual.
-    y_o, n2 = _site(it["attn"], st[1], *W["wo"], "o")
-    r1 = r + m["gt1"] * y_o
-    h2 = odit.f16(odit.rms_norm(r1) * blk["g2"] * (1.0 + m["sc2"]) + m["sh2"])
-    errs["h2"] = parity.rel_l2(it["h2"], h2)
-    y_gu, n3 = _site(it["h2"], st[2], *W["wgu"], "gate_up")
-    errs["gate_up"] = parity.rel_l2(it["gate_up"], odit.f16(y_gu))
-    gu = it["gate_up"]
-    act = odit.f16(odit.gelu_tanh(gu[:, :F]) * gu[:, F:])
-    errs["act"] = parity.rel_l2(it["act"], act)
-    y_d, n4 = _site(it["act"], st[3], *W["wd"], "down")
-    r2 = r1 + m["gt2"] * y_d
-    errs["update"] = parity.rel_l2(r_out - r, r2 - r)
-    return errs, n1 + n2 + n3 + n4, r_out
-
-
 def test_blocks_teacher_forced_pi():
     cfg, inp, model = _setup(n_blocks=3)
     r0 = odit.in_projection(inp["w"], inp["x0"])
     for t in (0, 7):
         rr = r0
         for l in range(inp["n_blocks"]):
-            errs, n_mis, rr = _check_block(cfg, inp, model, l, t, rr)
-            print(f"block {l} step {t}: code mismatches {n_mis}; " +
-                  ", ".join(f"{k} {v:.2e}" for k, v in errs.items()), flush=True)
-            for k, v in errs.items():
-                assert v <= parity.REL_L2_OUT, (l, t, k, v)
+            rr = dit_parity.assert_block(cfg, inp, model, l, t, rr)
 
 
 def test_full_depth_sampled_blocks_pi():
@@ -138,11 +63,8 @@ def test_full_depth_sampled_blocks_pi():
     r = torch.from_numpy(odit.in_projection(inp["w"], inp["x0"]).astype(np.float32)).to(DEV)
     for l in range(cfg.n_blocks):
         if l in (0, 9, 17):
-            errs, n_mis, r_next = _check_block(cfg, inp, model, l, t, r.cpu().numpy().astype(np.float64))
-            print(f"full depth block {l}: code mismatches {n_mis}; " +
-                  ", ".join(f"{k} {v:.2e}" for k, v in errs.items()), flush=True)
-            for k, v in errs.items():
-                assert v <= parity.REL_L2_OUT, (l, k, v)
+            r_next = dit_parity.assert_block(cfg, inp, model, l, t, r.cpu().numpy().astype(np.float64),
+                                             tag="full depth ")
             r = torch.from_numpy(r_next.astype(np.float32)).to(DEV)
         else:
             model.run_block(l, t, r)

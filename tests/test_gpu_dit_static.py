@@ -18,10 +18,8 @@ import torch
 
 import paper_2605_28803_amd as oq
 from oracle import dit as odit
-from oracle import hadamard
-from oracle import linear as olin
 from oracle import quant as oquant
-from tests import parity
+from tests import dit_parity, parity
 from workloads import configs, dit_inputs
 from workloads import generators as G
 
@@ -100,51 +98,35 @@ def test_static_sites_gr00t():
     model.close()
 
 
-def _site_static(model, x_gpu, d, l, t, site):
-    """GPU codes of the fp16 input by the stand-alone static kernel, and the
-    oracle's product with the step's folded weight (teacher-forced)."""
-    K = x_gpu.shape[1]
-    X = torch.from_numpy(x_gpu.astype(np.float16)).to(DEV)
-    Xq, xs = oq.rotate_quantize_act_static(X, K & -K, torch.from_numpy(d.astype(np.float32)).to(DEV))
-    torch.cuda.synchronize()
-    q = parity.unpack_int4(Xq.cpu().numpy())
-    q_o, _, r_o = oquant.rotate_quantize_static(x_gpu, K & -K, d)
-    parity.check_codes(q, q_o, r_o, parity.tau_static(x_gpu, K & -K, d, r_o))
-    Wq, ws = model.static_weight(l, t, site)
-    qw = parity.unpack_int4(Wq.cpu().numpy())
-    return olin.dequant(olin.int_gemm(q, qw), np.ones(q.shape[0]), ws.cpu().numpy().astype(np.float64))
+def _deltas(model, table, l, t):
+    return [_row(model, table, l, t, i).astype(np.float64) for i in range(4)]
 
 
-def test_static_block_linears_teacher_forced_pi():
+def test_static_blocks_teacher_forced_pi():
+    """Every site of two blocks in the static mode against the oracle's block
+    with the same step rows and the library's step-folded weights, every GPU
+    site value forced (tests/dit_parity.py)."""
     cfg = configs.DIT_PI
     inp, model, table, _ = _model(cfg, n_blocks=2)
     model.set_static_steps(inp, table)
-    D, F = cfg.hidden, cfg.mlp
-    r_in = odit.in_projection(inp["w"], inp["x0"])
+    r0 = odit.in_projection(inp["w"], inp["x0"])
     for t in (0, 5):
-        l = 1
-        m = inp["mod"][l][t]
-        r_t = torch.from_numpy(r_in.astype(np.float32)).to(DEV)
-        model.run_block(l, t, r_t)
-        torch.cuda.synchronize()
-        r_out = r_t.cpu().numpy().astype(np.float64)
-        it = model.intermediates()
-        r = r_in.astype(np.float32).astype(np.float64)
-        row = lambda s: _row(model, table, l, t, s).astype(np.float64)
-        errs = {}
-        y = _site_static(model, it["h1"], row(0), l, t, 0)
-        errs["qkv"] = parity.rel_l2(it["qkv"], odit.f16(y))
-        y_o = _site_static(model, it["attn"], row(1), l, t, 1)
-        r1 = r + m["gt1"] * y_o
-        y_gu = _site_static(model, it["h2"], row(2), l, t, 2)
-        errs["gate_up"] = parity.rel_l2(it["gate_up"], odit.f16(y_gu))
-        y_d = _site_static(model, it["act"], row(3), l, t, 3)
-        # the o update is teacher-forced through h2 = norm(r1): check the whole residual update
-        r2 = r1 + m["gt2"] * y_d
-        errs["update"] = parity.rel_l2(r_out - r, r2 - r)
-        print(f"static block {l} step {t}: " + ", ".join(f"{k} {v:.2e}" for k, v in errs.items()), flush=True)
-        for k, v in errs.items():
-            assert v <= parity.REL_L2_OUT, (t, k, v)
+        rr = r0
+        for l in range(2):
+            rr = dit_parity.assert_block(cfg, inp, model, l, t, rr, tag="static ",
+                                         static_delta=_deltas(model, table, l, t))
+    model.close()
+
+
+def test_static_blocks_teacher_forced_gr00t():
+    cfg = configs.DIT_GR00T
+    inp, model, table, _ = _model(cfg, n_blocks=2, batch=2)
+    model.set_static_steps(inp, table)
+    r0 = odit.in_projection(inp["w"], inp["x0"])
+    rr = r0
+    for l in range(2):
+        rr = dit_parity.assert_block(cfg, inp, model, l, 1, rr, tag="gr00t static ",
+                                     static_delta=_deltas(model, table, l, 1))
     model.close()
 
 

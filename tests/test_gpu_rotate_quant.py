@@ -62,7 +62,7 @@ def _check(x16, b, s, Xq, xs, ratio, xs2):
     q_o, xs_o, r_o = quant.rotate_quantize_act(x, b, s32)
     tau = parity.tau_rows(x, b)
     q = parity.unpack_int4(Xq)
-    n_mis, n_ulp = parity.check_codes(q, q_o, r_o, tau)
+    n_mis, n_ulp = parity.check_codes(q, q_o, r_o, tau, r_gpu=ratio)
     assert np.all(np.abs(ratio - r_o) <= tau[:, None] + 1e-30), "pre-rounding ratio outside tau"
     rel = np.abs(xs.astype(np.float64) - xs_o) / np.where(xs_o > 0, xs_o, 1.0)
     assert np.all(rel <= tau / 7 + 4 * parity.U32)
@@ -109,7 +109,7 @@ def test_step_scale_invariance_on_gpu():
         qa, qb = parity.unpack_int4(a[0]), parity.unpack_int4(b_[0])
         _, _, r_o = quant.rotate_quantize_act(x16.astype(np.float64), 4096, 1.0)
         tau = parity.tau_rows(x16.astype(np.float64), 4096)
-        parity.check_codes(qb, qa, r_o, 2 * tau)
+        parity.check_codes(qb, qa, r_o, 2 * tau, record=False)
         assert np.allclose(a[1], b_[1], rtol=1e-5)
 
 
