@@ -123,8 +123,10 @@ STATS = {"elements": 0, "mismatches": 0, "mismatches_beyond_1ulp": 0, "within_1u
 
 
 def ulp32(r) -> np.ndarray:
-    """One fp32 ulp at |r| (float64 array)."""
-    return np.spacing(np.abs(np.asarray(r, dtype=np.float64)).astype(np.float32)).astype(np.float64)
+    """One fp32 ulp at |r|, taken at least at 0.5 (the nearest rounding
+    boundary of a ratio below 0.5 is 0.5 itself), as float64."""
+    a = np.maximum(np.abs(np.asarray(r, dtype=np.float64)), 0.5)
+    return np.spacing(a.astype(np.float32)).astype(np.float64)
 
 
 def check_codes(q_gpu, q_ref, r_ref, tau_row, qmax: int = 7, r_gpu=None, record=True):
@@ -155,7 +157,7 @@ def check_codes(q_gpu, q_ref, r_ref, tau_row, qmax: int = 7, r_gpu=None, record=
     STATS["mismatches_beyond_1ulp"] += int((mism & ~within).sum())
     STATS["within_1ulp"] += n_ulp
     if r_gpu is not None:
-        err = np.abs(np.asarray(r_gpu, dtype=np.float64) - r_ref) / np.maximum(ulp, np.finfo(np.float32).tiny)
+        err = np.abs(np.asarray(r_gpu, dtype=np.float64) - r_ref) / ulp
         STATS["ratio_elements"] += int(err.size)
         STATS["max_ratio_err_ulp"] = max(STATS["max_ratio_err_ulp"], float(err.max()) if err.size else 0.0)
     return n, n_ulp
