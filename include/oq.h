@@ -432,6 +432,24 @@ int oq_calibrate_step_scales(const float* Y, int64_t n, int64_t K, int64_t ldy, 
                              void* stream);
 
 /*
+ * oq_calibrate_step_scales_noalloc -- for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same computation and results as
+ * oq_calibrate_step_scales, bit for bit, with no workspace argument.  The
+ * histogram, prefixes and ranks live in a device array inside the library
+ * (16.9 MB per GPU, held until the process ends; its address is looked up
+ * once per device on the first call with that device current).  The call
+ * allocates nothing and clears what must start at zero with a kernel.
+ * K <= 16384 columns; a larger K returns OQ_ERR_WORKSPACE and writes nothing.
+ * The stream must belong to the current device.  Every call on one GPU
+ * shares that GPU's array: calls that overlap on one GPU (other streams or
+ * threads) race and must be serialized by the caller.
+ * Errors: as oq_calibrate_step_scales, and OQ_ERR_WORKSPACE for K > 16384.
+ */
+int oq_calibrate_step_scales_noalloc(const float* Y, int64_t n, int64_t K, int64_t ldy, double p,
+                                     float qmax, float* delta, void* stream);
+
+/*
  * oq_rotate_quantize_act_static -- Hadamard rotation (as
  * oq_rotate_quantize_act) followed by the static quantizer with the step row
  * delta (device fp32 [K], 16-byte aligned: the table's row for this layer

@@ -362,6 +362,18 @@ def calibrate_step_scales(Y, p=99.9, qmax=7.0, delta=None, work=None, stream=Non
     return delta
 
 
+def calibrate_step_scales_noalloc(Y, p=99.9, qmax=7.0, delta=None, stream=None):
+    """As calibrate_step_scales, with the library's own device scratch (K <=
+    16384; the call itself allocates nothing; pass delta to allocate nothing
+    here either)."""
+    n, K = Y.shape
+    if delta is None:
+        delta = torch.empty((K,), dtype=torch.float32, device=Y.device)
+    _check(lib().oq_calibrate_step_scales_noalloc(_ptr(Y), n, K, _ld(Y), float(p), float(qmax), _ptr(delta),
+                                                  _stream(stream)), "oq_calibrate_step_scales_noalloc")
+    return delta
+
+
 def rotate_quantize_act_static(X, had_block, delta, Xq=None, x_scale=None, stream=None):
     """Rotation + static per-channel steps delta (f32 [K], device): (Xq uint8 [M, K/2], x_scale = 1)."""
     M, K = X.shape

@@ -66,6 +66,7 @@ SIGNATURES = {
     "oq_w4a8_gemm_i32": (i32, [vp, i64, vp, i64, i64, vp, i64, vp]),
     "oq_calibrate_workspace_bytes": (C.c_size_t, [i64]),
     "oq_calibrate_step_scales": (i32, [vp, i64, i64, i64, C.c_double, C.c_float, vp, vp, C.c_size_t, vp]),
+    "oq_calibrate_step_scales_noalloc": (i32, [vp, i64, i64, i64, C.c_double, C.c_float, vp, vp]),
     "oq_rotate_quantize_act_static": (i32, [vp, i64, i64, i64, i32, vp, vp, vp, vp]),
     "oq_rotate_quantize_act_static_tiled": (i32, [vp, i64, i64, i64, i32, vp, vp, vp, vp]),
     "oq_quantize_weights_step_host": (i32, [vp, i64, i64, i32, vp, vp, vp]),

@@ -19,6 +19,7 @@
 // histogram [K][256] with one atomic per non-zero bin.  The row chunks give
 // the launch enough workgroups to fill the chip for any column count.
 #include <cmath>
+#include <mutex>
 
 #include "common.h"
 
@@ -123,6 +124,86 @@ __global__ __launch_bounds__(256) void quantile_select_kernel(uint32_t* __restri
   if (last) out[col] = static_cast<float>(static_cast<double>(__uint_as_float(p)) / qmax);
 }
 
+// Launches of one calibration: work = hist [K][256] | prefix [K] | rank [K].
+int calibrate_launch(const float* Y, int64_t n, int64_t K, int64_t ldy, double p, float qmax, float* delta,
+                     uint32_t* work, hipStream_t s) {
+  // Nearest rank: the k-th smallest with k = ceil(p n / 100), in [1, n].  p is
+  // taken to 1e-6 percent and the product formed in integers (pm n <= 1e8 *
+  // INT32_MAX < 2^63): in floating point 99.9 / 100 * 1000 = 999.0000000000001
+  // would round up to the maximum.
+  const int64_t pm = std::llround(p * 1e6);
+  int64_t k = (pm * n + 99999999) / 100000000;
+  if (k < 1) k = 1;
+  if (k > n) k = n;
+  uint32_t* hist = work;
+  uint32_t* prefix = hist + K * 256;
+  uint32_t* rank = prefix + K;
+  hipLaunchKernelGGL(quantile_init_kernel, dim3(static_cast<unsigned>((K * 64 + 255) / 256)), dim3(256), 0, s,
+                     hist, prefix, rank, K, static_cast<uint32_t>(k));
+  const int64_t slabs = (K + kSlab - 1) / kSlab;
+  // Enough row chunks for ~8 workgroups per CU over the slabs, at least 64
+  // rows per chunk.
+  int64_t splits = (2048 + slabs - 1) / slabs;
+  if (splits > kMaxRowSplits) splits = kMaxRowSplits;
+  if (splits > (n + 63) / 64) splits = (n + 63) / 64;
+  if (splits < 1) splits = 1;
+  const int64_t chunk = (n + splits - 1) / splits;
+  splits = (n + chunk - 1) / chunk;
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    hipLaunchKernelGGL(quantile_hist_kernel, dim3(static_cast<unsigned>(slabs), static_cast<unsigned>(splits)),
+                       dim3(256), 0, s, Y, n, K, ldy, chunk, shift, prefix, hist);
+    hipLaunchKernelGGL(quantile_select_kernel, dim3(static_cast<unsigned>((K + 3) / 4)), dim3(256), 0, s, hist,
+                       K, shift, prefix, rank, pass == 3, static_cast<double>(qmax), delta);
+  }
+  return launch_status();
+}
+
+// Argument checks shared by both entry points (before any launch).
+int calibrate_check(const float* Y, int64_t n, int64_t K, int64_t ldy, double p, float qmax, float* delta) {
+  if (n < 0 || K < 0 || n > INT32_MAX || K > (int64_t(1) << 24) || ldy < K) return OQ_ERR_SHAPE;
+  if (!(p > 0.0 && p <= 100.0) || !(qmax > 0.0f) || !std::isfinite(qmax)) return OQ_ERR_ARG;
+  if (K == 0) return OQ_OK;
+  if (n == 0) return OQ_ERR_SHAPE;  // no order statistic of an empty column
+  if (!Y || !delta) return OQ_ERR_NULL;
+  if (!aligned(Y, 4) || !aligned(delta, 4)) return OQ_ERR_ALIGN;
+  return OQ_OK;
+}
+
+// ---- the allocation-free variant -----------------------------------------
+// Its histogram, prefixes and ranks live in a file-scope device array, one
+// copy per GPU for the life of the process, sized for kScratchMaxK columns.
+constexpr int64_t kScratchMaxK = 16384;
+constexpr size_t kScratchWords = static_cast<size_t>(kScratchMaxK) * (256 + 2);  // 16.9 MB
+constexpr int kMaxDevices = 64;
+
+// The array's address on each device, from hipGetSymbolAddress with that
+// device current (the host-side name is not a device address).
+std::mutex g_scratch_mu;
+uint32_t* g_scratch_ptr[kMaxDevices] = {};
+
+}  // namespace
+}  // namespace oq
+
+static __device__ __align__(256) uint32_t scratch[oq::kScratchWords];
+
+namespace oq {
+namespace {
+
+int scratch_for_current_device(uint32_t** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return OQ_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return OQ_ERR_DEVICE;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return OQ_ERR_HIP;
+    g_scratch_ptr[dev] = static_cast<uint32_t*>(ptr);
+  }
+  *out = g_scratch_ptr[dev];
+  return OQ_OK;
+}
+
 }  // namespace
 }  // namespace oq
 
@@ -133,44 +214,23 @@ extern "C" size_t oq_calibrate_workspace_bytes(int64_t K) {
 
 extern "C" int oq_calibrate_step_scales(const float* Y, int64_t n, int64_t K, int64_t ldy, double p, float qmax,
                                         float* delta, void* work, size_t work_bytes, void* stream) {
-  if (n < 0 || K < 0 || n > INT32_MAX || K > (int64_t(1) << 24) || ldy < K) return OQ_ERR_SHAPE;
-  if (!(p > 0.0 && p <= 100.0) || !(qmax > 0.0f) || !std::isfinite(qmax)) return OQ_ERR_ARG;
-  if (K == 0) return OQ_OK;
-  if (n == 0) return OQ_ERR_SHAPE;  // no order statistic of an empty column
-  if (!Y || !delta || !work) return OQ_ERR_NULL;
+  int e = oq::calibrate_check(Y, n, K, ldy, p, qmax, delta);
+  if (e != OQ_OK || K == 0) return e;
+  if (!work) return OQ_ERR_NULL;
   if (work_bytes < oq_calibrate_workspace_bytes(K)) return OQ_ERR_SHAPE;
-  if (!oq::aligned(Y, 4) || !oq::aligned(delta, 4) || !oq::aligned(work, 16)) return OQ_ERR_ALIGN;
-  int st = oq::device_check();
-  if (st != OQ_OK) return st;
-  // Nearest rank: the k-th smallest with k = ceil(p n / 100), in [1, n].  p is
-  // taken to 1e-6 percent and the product formed in integers (pm n <= 1e8 *
-  // INT32_MAX < 2^63): in floating point 99.9 / 100 * 1000 = 999.0000000000001
-  // would round up to the maximum.
-  const int64_t pm = std::llround(p * 1e6);
-  int64_t k = (pm * n + 99999999) / 100000000;
-  if (k < 1) k = 1;
-  if (k > n) k = n;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  uint32_t* hist = static_cast<uint32_t*>(work);
-  uint32_t* prefix = hist + K * 256;
-  uint32_t* rank = prefix + K;
-  hipLaunchKernelGGL(oq::quantile_init_kernel, dim3(static_cast<unsigned>((K * 64 + 255) / 256)), dim3(256), 0, s,
-                     hist, prefix, rank, K, static_cast<uint32_t>(k));
-  const int64_t slabs = (K + oq::kSlab - 1) / oq::kSlab;
-  // Enough row chunks for ~8 workgroups per CU over the slabs, at least 64
-  // rows per chunk.
-  int64_t splits = (2048 + slabs - 1) / slabs;
-  if (splits > oq::kMaxRowSplits) splits = oq::kMaxRowSplits;
-  if (splits > (n + 63) / 64) splits = (n + 63) / 64;
-  if (splits < 1) splits = 1;
-  const int64_t chunk = (n + splits - 1) / splits;
-  splits = (n + chunk - 1) / chunk;
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
-    hipLaunchKernelGGL(oq::quantile_hist_kernel, dim3(static_cast<unsigned>(slabs), static_cast<unsigned>(splits)),
-                       dim3(256), 0, s, Y, n, K, ldy, chunk, shift, prefix, hist);
-    hipLaunchKernelGGL(oq::quantile_select_kernel, dim3(static_cast<unsigned>((K + 3) / 4)), dim3(256), 0, s, hist,
-                       K, shift, prefix, rank, pass == 3, static_cast<double>(qmax), delta);
-  }
-  return oq::launch_status();
+  if (!oq::aligned(work, 16)) return OQ_ERR_ALIGN;
+  if ((e = oq::device_check()) != OQ_OK) return e;
+  return oq::calibrate_launch(Y, n, K, ldy, p, qmax, delta, static_cast<uint32_t*>(work),
+                              static_cast<hipStream_t>(stream));
+}
+
+extern "C" int oq_calibrate_step_scales_noalloc(const float* Y, int64_t n, int64_t K, int64_t ldy, double p,
+                                                float qmax, float* delta, void* stream) {
+  int e = oq::calibrate_check(Y, n, K, ldy, p, qmax, delta);
+  if (e != OQ_OK || K == 0) return e;
+  if (K > oq::kScratchMaxK) return OQ_ERR_WORKSPACE;
+  if ((e = oq::device_check()) != OQ_OK) return e;
+  uint32_t* work = nullptr;
+  if ((e = oq::scratch_for_current_device(&work)) != OQ_OK) return e;
+  return oq::calibrate_launch(Y, n, K, ldy, p, qmax, delta, work, static_cast<hipStream_t>(stream));
 }
