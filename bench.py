@@ -19,7 +19,15 @@ Also reported (same JSON line):
   prefill    the GEMM at M=K=N=16384 against the int8 MFMA peak and the
              rotate-quantize at M=K=16384 against HBM peak, cold;
   cpu_baseline  the oracle on this host on a bounded sample (3 of 18 blocks of
-             one step), scaled to denoising steps per second.
+             one step), scaled to denoising steps per second;
+  single_linear_64x1024x1024  the single rotated linear, warm and cold;
+  sweep      rotate-quantize and GEMM at M in {1, 16, 256, 4096, 16384} x
+             K = N in {1024 .. 16384}, cold, each against its roofline (HBM
+             for rotate-quantize; min(int8 peak, intensity x HBM) for the GEMM);
+  static_footprint  int4 + scales against fp16 for the synthetic workloads'
+             linears, beside the paper's own figures (paper_context);
+  cpu_oracle_kernels  the oracle's rotate-quantize and GEMM on row samples of
+             the 16384^3 prefill shape, single-threaded and on every core.
 
 --sweep writes the rotate-quantize / GEMM roofline sweep (M x K = N grid) as
 JSON lines to gpurun_out/sweep.jsonl instead; --roofline-only runs just the
@@ -705,6 +713,233 @@ def dit_static_step(cfg, inp, model, n_traj=4, steps=50):
             "denoise_vs_per_token_rel_l2": round(dev, 4)}
 
 
+# The paper's own figures (context, not targets: other hardware, other
+# precision, whole-model storage), from its Table tab:memory_savings and
+# Appendix B Table tab:real_quant_latency.
+PAPER_CONTEXT = {
+    "static_memory_savings": {
+        "gr00t_n1.5": {"fp16_GB": 1.99, "quantized_MB": 586, "saving": 0.713, "q_layers": 180},
+        "pi0.5": {"fp16_GB": 4.27, "quantized_GB": 1.20, "saving": 0.720, "q_layers": 252},
+        "what": "whole-model static memory, W4 weights plus quantization metadata (storage, no hardware)",
+        "source": "Table tab:memory_savings"},
+    "per_step_latency_ms": {
+        "fp16": 32.2, "omega_qvla_w4a8": 26.7, "qvla_real": 27.1, "quantvla_real": 29.8,
+        "hardware": "NVIDIA H100", "precision": "W4A8 (INT8 tensor-core GEMM, packed INT4 weights)",
+        "workload": "Pi-0.5 policy, LIBERO Spatial task 0, 3 episodes (one policy call per step)",
+        "source": "Appendix B, Table tab:real_quant_latency"},
+}
+
+
+def static_footprint():
+    """Storage of every quantized linear of the synthetic workloads against
+    fp16: packed int4 codes + one fp32 scale per output channel (+ the fp32
+    step-scale table of the DiT sites), the analogue of the paper's static
+    memory saving (linears only: norms, embeddings and the rest of a real
+    policy stay outside this count)."""
+    from workloads import configs
+    out = {}
+
+    def entry(linears, extra_bytes=0):
+        fp16 = sum(2 * n * k for n, k in linears)
+        q = sum(n * k // 2 + 4 * n for n, k in linears) + extra_bytes
+        return {"fp16_MB": round(fp16 / 1e6, 1), "w4_MB": round(q / 1e6, 1), "saving": round(1 - q / fp16, 4),
+                "linears": len(linears)}
+
+    c = configs.DIT_PI
+    D, F = c.hidden, c.mlp
+    lin = [(3 * D, D), (D, D), (2 * F, D), (D, F)] * c.n_blocks
+    out["dit_pi05_expert"] = entry(lin, 4 * c.n_blocks * c.steps * 4)
+    c = configs.DIT_GR00T
+    D, F = c.hidden, c.mlp
+    lin = []
+    for l in range(c.n_blocks):
+        lin += ([(D, D), (2 * D, D)] if l % 2 == 0 else [(3 * D, D)]) + [(D, D), (F, D), (D, F)]
+    out["dit_gr00t"] = entry(lin, 4 * c.n_blocks * c.steps * 4)
+    p = configs.PREFILL_GEMMA
+    lin = [(n, k) for _, k, n in p.linears()] * p.n_layers
+    out["backbone_gemma2b_18_layers"] = entry(lin)
+    return out
+
+
+def single_linear(stream):
+    """The single rotated linear (64 x 1024 activation with 8 outlier channels
+    x50, 1024 x 1024 weight with a random orthogonal U folded in, b = 1024,
+    s_t = 1): rotate-quantize + W4A4 GEMM latency, warm (graph replays) and
+    cold (MALL evicted by a read before each pair)."""
+    import torch
+    import paper_2605_28803_amd as oq
+    from workloads import configs, linear_inputs
+    case = configs.LINEAR_1024
+    inp = linear_inputs.make_linear_inputs(case)
+    dev = torch.device("cuda:0")
+    X = torch.from_numpy(inp["x"].astype(np.float16)).to(dev)
+    W = torch.from_numpy((inp["w"] @ inp["u"]).astype(np.float16)).to(dev)  # U folded offline
+    Wq, ws = oq.quantize_weights(W, case.had_block)
+    Xq = torch.empty((case.M, case.K // 2), dtype=torch.uint8, device=dev)
+    xs = torch.empty((case.M,), dtype=torch.float32, device=dev)
+    Y = torch.empty((case.M, case.N), dtype=torch.float16, device=dev)
+
+    def pair():  # on the current stream (the capture stream inside _graph_time)
+        oq.rotate_quantize_act(X, case.had_block, Xq=Xq, x_scale=xs)
+        oq.w4a4_linear(Xq, xs, Wq, ws, Y=Y)
+
+    warm = _graph_time(pair, reps=50, replays=20)
+    flush = torch.ones((512 << 20,), dtype=torch.uint8, device=dev)
+    ts = []
+    for _ in range(30):
+        evict_mall(flush)
+        s = torch.cuda.Event(enable_timing=True)
+        e = torch.cuda.Event(enable_timing=True)
+        s.record(stream)
+        pair()
+        e.record(stream)
+        e.synchronize()
+        ts.append(s.elapsed_time(e))
+    del flush
+    return {"M": case.M, "K": case.K, "N": case.N, "warm_us": round(warm * 1e3, 2),
+            "cold_us": round(float(np.median(ts)) * 1e3, 2),
+            "note": "rotate-quantize + GEMM with epilogue, two launches; latency-bound (164 KB, 134 MOP)"}
+
+
+def gemm_roofline(M, N, K, t_ms):
+    """Achieved TOP/s of a W4A4 GEMM launch and its fraction of the roofline
+    min(int8 peak, arithmetic intensity x HBM bandwidth) over its algorithmic
+    bytes (fp16 output)."""
+    ops = 2.0 * M * N * K
+    b = gemm_bytes(M, N, K, 2)
+    ai = ops / b
+    roof = min(INT8_PEAK_TOPS, ai * HBM_PEAK_GBS / 1e3)
+    tops = ops / (t_ms * 1e-3) / 1e12
+    return {"gemm_us": round(t_ms * 1e3, 2), "gemm_TOPs": round(tops, 2),
+            "gemm_frac_int8": round(tops / INT8_PEAK_TOPS, 4),
+            "gemm_GBs": round(b / (t_ms * 1e-3) / 1e9, 1),
+            "gemm_bound": "hbm" if ai * HBM_PEAK_GBS / 1e3 < INT8_PEAK_TOPS else "mfma",
+            "gemm_roofline_TOPs": round(roof, 1), "gemm_frac_roofline": round(tops / roof, 4)}
+
+
+def sweep_records(Ms=None, Ks=None, reps=10, sink=None):
+    """Rotate-quantize and W4A4 GEMM at M x (K = N), cold (a 512 MB read
+    evicts the MALL before each timed launch).  Inputs per shape: seed 1000 +
+    10 iM + iK; X ~ N(0, 1) with round(0.01 K) outlier channels x50 and W ~
+    N(0, 0.02^2), drawn on the device with torch's generator under that seed;
+    Hadamard block K."""
+    import torch
+    import paper_2605_28803_amd as oq
+    from workloads import configs
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    flush = torch.ones((512 << 20,), dtype=torch.uint8, device=dev)
+    out = []
+    for case in configs.SWEEP.cases():
+        M, K, N = case.M, case.K, case.N
+        if (Ms and M not in Ms) or (Ks and K not in Ks):
+            continue
+        g = torch.Generator(device=dev).manual_seed(case.seed)
+        X = torch.randn((M, K), generator=g, device=dev)
+        ch = torch.randperm(K, generator=g, device=dev)[: case.outlier_count]
+        X[:, ch] *= case.outlier_factor
+        X = X.half()
+        W = (torch.randn((N, K), generator=g, device=dev) * case.w_std).half()
+        Wq, ws = oq.quantize_weights(W, K)
+        del W
+        Xq, xs = oq.rotate_quantize_act(X, K)
+        Y = torch.empty((M, N), dtype=torch.float16, device=dev)
+
+        def timed(fn):
+            ts = []
+            for _ in range(reps):
+                evict_mall(flush)
+                s = torch.cuda.Event(enable_timing=True)
+                e = torch.cuda.Event(enable_timing=True)
+                s.record(stream)
+                fn()
+                e.record(stream)
+                e.synchronize()
+                ts.append(s.elapsed_time(e))
+            return float(np.median(ts))
+
+        rq = lambda: oq.rotate_quantize_act(X, K, Xq=Xq, x_scale=xs, stream=stream)
+        gm = lambda: oq.w4a4_linear(Xq, xs, Wq, ws, Y=Y, stream=stream)
+        rq()
+        gm()
+        t_rq = timed(rq)
+        t_g = timed(gm)
+        rb = rq_bytes(M, K)
+        rec = {"M": M, "K": K, "N": N, "seed": case.seed, "rq_us": round(t_rq * 1e3, 2),
+               "rq_GBs": round(rb / (t_rq * 1e-3) / 1e9, 1),
+               "rq_frac_hbm": round(rb / (t_rq * 1e-3) / 1e9 / HBM_PEAK_GBS, 4), "rq_MB": round(rb / 1e6, 2)}
+        rec.update(gemm_roofline(M, N, K, t_g))
+        out.append(rec)
+        if sink is not None:
+            sink(rec)
+        del Xq, xs, Y, Wq, ws, X
+    del flush
+    torch.cuda.empty_cache()
+    return out
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_kernel_baselines(rq_rows=384, gemm_rows=32, M=16384, K=16384):
+    """The oracle's rotate-quantize and integer GEMM on this host at the
+    prefill shape M = K = N = 16384 (float64 / int64 numpy, untouched), each
+    on a bounded sample of rows, single-threaded (BLAS limited to one thread;
+    the rotate-quantize over the same row chunks, one after the other) and
+    with every host core (the row chunks on a thread pool for the
+    rotate-quantize, the BLAS thread pool for the GEMM), extrapolated x M /
+    rows to the whole launch."""
+    import concurrent.futures as cf
+    from threadpoolctl import threadpool_limits
+    from oracle import linear as olin
+    from oracle import quant as oquant
+    cores = len(os.sched_getaffinity(0))
+    rng = np.random.default_rng(2024)
+    x = rng.standard_normal((rq_rows, K)).astype(np.float16).astype(np.float64)
+    out = {"cpu_model": cpu_model(), "host_cores": cores}
+    # The same row chunks serially on one thread, then on a pool of every core.
+    chunks = np.array_split(np.arange(rq_rows), cores)
+    with threadpool_limits(1):
+        t0 = time.perf_counter()
+        q = np.concatenate([oquant.rotate_quantize_act(x[r], K, 1.0)[0] for r in chunks])
+        t1 = time.perf_counter() - t0
+    with threadpool_limits(1), cf.ThreadPoolExecutor(cores) as ex:
+        t0 = time.perf_counter()
+        list(ex.map(lambda r: oquant.rotate_quantize_act(x[r], K, 1.0), chunks))
+        tn = time.perf_counter() - t0
+    rb = rq_bytes(M, K)
+    out["rotate_quant"] = {"shape": f"M={M} K={K}", "rows_sampled": rq_rows,
+                           "single_thread_s": round(t1 * M / rq_rows, 2),
+                           "all_cores_s": round(tn * M / rq_rows, 2), "threads": cores,
+                           "single_thread_GBs": round(rb / (t1 * M / rq_rows) / 1e9, 4),
+                           "all_cores_GBs": round(rb / (tn * M / rq_rows) / 1e9, 4),
+                           "kind": "extrapolated x M/rows"}
+    qw = rng.integers(-7, 8, size=(K, K)).astype(np.int64)  # N = K weight codes (timing only)
+    qa = q[:gemm_rows]
+    with threadpool_limits(1):
+        t0 = time.perf_counter()
+        olin.int_gemm(qa, qw)
+        g1 = time.perf_counter() - t0
+    with threadpool_limits(cores):
+        t0 = time.perf_counter()
+        olin.int_gemm(qa, qw)
+        gn = time.perf_counter() - t0
+    ops = 2.0 * M * K * K
+    out["gemm"] = {"shape": f"M={M} N={K} K={K}", "rows_sampled": gemm_rows,
+                   "single_thread_s": round(g1 * M / gemm_rows, 1), "all_cores_s": round(gn * M / gemm_rows, 1),
+                   "threads": cores, "single_thread_TOPs": round(ops / (g1 * M / gemm_rows) / 1e12, 6),
+                   "all_cores_TOPs": round(ops / (gn * M / gemm_rows) / 1e12, 6),
+                   "kind": "extrapolated x M/rows (exact int GEMM as a float64 BLAS product of the codes)"}
+    return out
+
+
 def run_dit(args):
     import torch
     import paper_2605_28803_amd as oq
@@ -786,68 +1021,34 @@ def run_dit(args):
         line["weight_preparation"] = prepare_kernels()
         print("[bench] static per-step steps (calibration + step)", file=sys.stderr, flush=True)
         line["dit_static_steps"] = dit_static_step(cfg, inp, model)
+    line["single_linear_64x1024x1024"] = single_linear(stream)
+    if not args.no_prefill:
+        print("[bench] roofline sweep (25 shapes, cold)", file=sys.stderr, flush=True)
+        line["sweep"] = sweep_records()
+    line["static_footprint"] = static_footprint()
+    line["paper_context"] = PAPER_CONTEXT
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle sample)", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(cfg, inp)
+        print("[bench] cpu oracle kernels (rotate-quantize, GEMM samples)", file=sys.stderr, flush=True)
+        line["cpu_oracle_kernels"] = cpu_kernel_baselines()
     model.close()
     print(json.dumps(line), flush=True)
 
 
 def run_sweep(args):
-    """Rotate-quantize and GEMM roofline sweep over M x (K = N); cold timing
-    (a 512 MB buffer is read between timed launches to evict the MALL)."""
-    import torch
-    import paper_2605_28803_amd as oq
-    from workloads import configs
-    dev = torch.device("cuda:0")
-    stream = torch.cuda.current_stream()
-    flush = torch.ones((512 << 20,), dtype=torch.uint8, device=dev)
+    """The rotate-quantize / GEMM roofline sweep alone (sweep_records), as JSON
+    lines on stdout and in gpurun_out/sweep.jsonl."""
     os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
     path = os.path.join(ROOT, "gpurun_out", "sweep.jsonl")
-    Ms = [int(m) for m in args.sweep_m.split(",")] if args.sweep_m else list(configs.SWEEP.Ms)
-    Ks = [int(k) for k in args.sweep_k.split(",")] if args.sweep_k else list(configs.SWEEP.Ks)
+    Ms = [int(m) for m in args.sweep_m.split(",")] if args.sweep_m else None
+    Ks = [int(k) for k in args.sweep_k.split(",")] if args.sweep_k else None
     with open(path, "w") as f:
-        for M in Ms:
-            for K in Ks:
-                N = K
-                g = torch.Generator(device="cpu").manual_seed(1000 + M + K)
-                X = torch.randn((M, K), generator=g).half().to(dev)
-                W = (torch.randn((N, K), generator=g) * 0.02).half().to(dev)
-                Wq, ws = oq.quantize_weights(W, K)
-                del W
-                Xq, xs = oq.rotate_quantize_act(X, K)
-                Y = torch.empty((M, N), dtype=torch.float16, device=dev)
-
-                def timed(fn, reps):
-                    ts = []
-                    for _ in range(reps):
-                        evict_mall(flush)
-                        s = torch.cuda.Event(enable_timing=True)
-                        e = torch.cuda.Event(enable_timing=True)
-                        s.record(stream)
-                        fn()
-                        e.record(stream)
-                        e.synchronize()
-                        ts.append(s.elapsed_time(e))
-                    return float(np.median(ts))
-
-                rq = lambda: oq.rotate_quantize_act(X, K, Xq=Xq, x_scale=xs, stream=stream)
-                gm = lambda: oq.w4a4_linear(Xq, xs, Wq, ws, Y=Y, stream=stream)
-                rq(); gm()
-                reps = 20
-                t_rq = timed(rq, reps)
-                t_g = timed(gm, reps)
-                rec = {"M": M, "K": K, "N": N, "rq_us": round(t_rq * 1e3, 2),
-                       "rq_GBs": round(rq_bytes(M, K) / (t_rq * 1e-3) / 1e9, 1),
-                       "rq_frac_hbm": round(rq_bytes(M, K) / (t_rq * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-                       "gemm_us": round(t_g * 1e3, 2),
-                       "gemm_TOPs": round(2 * M * N * K / (t_g * 1e-3) / 1e12, 2),
-                       "gemm_frac_int8": round(2 * M * N * K / (t_g * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4),
-                       "gemm_GBs": round(gemm_bytes(M, N, K, 2) / (t_g * 1e-3) / 1e9, 1)}
-                f.write(json.dumps(rec) + "\n")
-                f.flush()
-                print(json.dumps(rec), flush=True)
-                del Xq, xs, Y, Wq, ws, X
+        def sink(rec):
+            f.write(json.dumps(rec) + "\n")
+            f.flush()
+            print(json.dumps(rec), flush=True)
+        sweep_records(Ms, Ks, reps=20, sink=sink)
 
 
 def main():
@@ -867,6 +1068,7 @@ def main():
     ap.add_argument("--static-only", action="store_true")
     ap.add_argument("--w4a8-only", action="store_true")
     ap.add_argument("--prepare-only", action="store_true")
+    ap.add_argument("--cpu-kernels-only", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (--gpus must be 1)", file=sys.stderr)
@@ -887,6 +1089,8 @@ def main():
         print(json.dumps({"w4a8": w4a8_kernels()}), flush=True)
     elif args.prepare_only:
         print(json.dumps({"weight_preparation": prepare_kernels()}), flush=True)
+    elif args.cpu_kernels_only:
+        print(json.dumps({"cpu_oracle_kernels": cpu_kernel_baselines()}), flush=True)
     else:
         run_dit(args)
 
