@@ -124,24 +124,34 @@ __device__ __forceinline__ void big_tile(int id, int tiles_m, int tiles_n, int* 
 // A8: the token operand holds 8-bit codes (W4A8), one byte each, loaded 64
 // bytes per thread and row per stage and reordered (not widened) into LDS;
 // the products are then 16 * q * wq and the accumulator is shifted by 4.
-template <int EPI, int WM, int WN, int TM, int TN, bool A8, int NS>
-__global__ __launch_bounds__(64 * WM * WN, 512 / (64 * WM * WN)) void gemm_big_kernel(GemmArgs a) {
+template <int EPI, int WM, int WN, int TM, int TN, bool A8, int NS, int KG>
+__global__ __launch_bounds__(64 * WM * WN * KG, (512 / (64 * WM * WN * KG) > 0 ? 512 / (64 * WM * WN * KG) : 1))
+void gemm_big_kernel(GemmArgs a) {
   static_assert(NS >= 2, "at least two register stages");
-  // WM x WN waves, each a (32 TM) x (32 TN) tile of v_mfma_i32_32x32x32_i8 blocks.
-  constexpr int NT = 64 * WM * WN;          // threads
+  // KG groups of WM x WN waves; in each group every wave owns a (32 TM) x
+  // (32 TN) tile of v_mfma_i32_32x32x32_i8 blocks.  Group g multiplies the
+  // stages g, g + KG, g + 2 KG, ... of K through its own LDS buffers; the
+  // groups' accumulators are summed through LDS before the epilogue (exact
+  // integer sums, so any KG gives the same result bit for bit).
+  constexpr int NTG = 64 * WM * WN;         // threads per group
+  constexpr int NT = NTG * KG;              // threads
   constexpr int BM = 32 * TM * WM, BN = 32 * TN * WN;
-  constexpr int PA = 2 * BM / NT, PB = 2 * BN / NT;  // rows each thread loads per stage
-  static_assert(PA >= 1 && PB >= 1 && 2 * BM % NT == 0 && 2 * BN % NT == 0, "load split");
-  // Two LDS buffers per operand; after the K loop the same memory holds the
-  // 2-byte output tile of the staged epilogue.
-  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * (BM + BN) * BIG8_STRIDE];
-  uint8_t (*sA)[BM * BIG8_STRIDE] = reinterpret_cast<uint8_t (*)[BM * BIG8_STRIDE]>(smem);
-  uint8_t (*sB)[BN * BIG8_STRIDE] = reinterpret_cast<uint8_t (*)[BN * BIG8_STRIDE]>(smem + 2 * BM * BIG8_STRIDE);
+  constexpr int PA = 2 * BM / NTG, PB = 2 * BN / NTG;  // rows each thread loads per stage
+  static_assert(PA >= 1 && PB >= 1 && 2 * BM % NTG == 0 && 2 * BN % NTG == 0, "load split");
+  // Per group two LDS buffers per operand; after the K loop the same memory
+  // holds the other groups' accumulators and the 2-byte output tile of the
+  // staged epilogue.
+  constexpr int GBYTES = 2 * (BM + BN) * BIG8_STRIDE;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[KG * GBYTES];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int grp = tid / NTG, tg = tid % NTG;
+  const int wave = tg >> 6;  // wave within the group
   const int wm = wave / WN, wn = wave % WN;  // rows wm * 32 TM, columns wn * 32 TN
+  uint8_t (*sA)[BM * BIG8_STRIDE] = reinterpret_cast<uint8_t (*)[BM * BIG8_STRIDE]>(smem + grp * GBYTES);
+  uint8_t (*sB)[BN * BIG8_STRIDE] =
+      reinterpret_cast<uint8_t (*)[BN * BIG8_STRIDE]>(smem + grp * GBYTES + 2 * BM * BIG8_STRIDE);
   const int tiles_m = static_cast<int>((a.M + BM - 1) / BM);
   const int tiles_n = static_cast<int>((a.N + BN - 1) / BN);
   int tm, tn;
@@ -155,20 +165,22 @@ __global__ __launch_bounds__(64 * WM * WN, 512 / (64 * WM * WN)) void gemm_big_k
   const int nk64 = static_cast<int>(a.K / 64);                            // 64-code halves in total
 
   // Global -> LDS: a stage is BM (A) and BN (B) rows x 64 packed bytes; a
-  // thread loads 32 packed bytes (two 16-byte pieces) of rows tid/2 + r NT/2.
-  // A half stage past K reads a clamped address; its MFMAs are skipped.
-  const int lr = tid >> 1, lh = tid & 1;
+  // thread loads 32 packed bytes (two 16-byte pieces) of rows tg/2 + r NTG/2.
+  // Local stage j of group grp is stage KG j + grp of K.  A half stage past K,
+  // and a stage past the end, read clamped addresses; their MFMAs are skipped.
+  const int lr = tg >> 1, lh = tg & 1;
+  const int njl = (nk + KG - 1) / KG;  // local stages (the same count in every group)
   const uint8_t* gA[PA];
   const uint8_t* gB[PB];
 #pragma unroll
-  for (int r = 0; r < PA; ++r) gA[r] = a.A + min<int64_t>(m0 + lr + r * (NT / 2), a.M - 1) * Ka + lh * 32 * AW;
+  for (int r = 0; r < PA; ++r) gA[r] = a.A + min<int64_t>(m0 + lr + r * (NTG / 2), a.M - 1) * Ka + lh * 32 * AW;
 #pragma unroll
-  for (int r = 0; r < PB; ++r) gB[r] = a.B + min<int64_t>(n0 + lr + r * (NT / 2), a.N - 1) * Kb + lh * 32;
+  for (int r = 0; r < PB; ++r) gB[r] = a.B + min<int64_t>(n0 + lr + r * (NTG / 2), a.N - 1) * Kb + lh * 32;
   // NS register stages, indexed only by constants (they stay in VGPRs).
   uint4 ra[NS][2 * AW * PA], rb[NS][2 * PB];
 #define OQ_GLOAD(KS, S)                                                                \
   {                                                                                    \
-    const int h_ = min(2 * (KS) + lh, nk64 - 1);                                       \
+    const int h_ = min(2 * (KG * (KS) + grp) + lh, nk64 - 1);                           \
     const int64_t off_ = static_cast<int64_t>(h_) * 32 - lh * 32;                      \
     _Pragma("unroll") for (int r_ = 0; r_ < PA; ++r_)                                  \
     _Pragma("unroll") for (int c_ = 0; c_ < 2 * AW; ++c_)                              \
@@ -192,16 +204,16 @@ __global__ __launch_bounds__(64 * WM * WN, 512 / (64 * WM * WN)) void gemm_big_k
     _Pragma("unroll") for (int r_ = 0; r_ < PA; ++r_) {                                            \
       if constexpr (A8) {                                                                          \
         _Pragma("unroll") for (int c_ = 0; c_ < 4; ++c_)                                           \
-          *reinterpret_cast<v4i*>(&sA[(BUF)][(lr + r_ * (NT / 2)) * BIG8_STRIDE + lh * 64 + 16 * c_]) = \
+          *reinterpret_cast<v4i*>(&sA[(BUF)][(lr + r_ * (NTG / 2)) * BIG8_STRIDE + lh * 64 + 16 * c_]) = \
               order16_i8(ra[S][4 * r_ + c_]);                                                      \
       } else {                                                                                     \
-        OQ_ST32(&sA[(BUF)][(lr + r_ * (NT / 2)) * BIG8_STRIDE + lh * 64], ra[S][2 * r_])           \
-        OQ_ST32(&sA[(BUF)][(lr + r_ * (NT / 2)) * BIG8_STRIDE + lh * 64 + 32], ra[S][2 * r_ + 1])  \
+        OQ_ST32(&sA[(BUF)][(lr + r_ * (NTG / 2)) * BIG8_STRIDE + lh * 64], ra[S][2 * r_])          \
+        OQ_ST32(&sA[(BUF)][(lr + r_ * (NTG / 2)) * BIG8_STRIDE + lh * 64 + 32], ra[S][2 * r_ + 1]) \
       }                                                                                            \
     }                                                                                              \
     _Pragma("unroll") for (int r_ = 0; r_ < PB; ++r_) {                                            \
-      OQ_ST32(&sB[(BUF)][(lr + r_ * (NT / 2)) * BIG8_STRIDE + lh * 64], rb[S][2 * r_])             \
-      OQ_ST32(&sB[(BUF)][(lr + r_ * (NT / 2)) * BIG8_STRIDE + lh * 64 + 32], rb[S][2 * r_ + 1])    \
+      OQ_ST32(&sB[(BUF)][(lr + r_ * (NTG / 2)) * BIG8_STRIDE + lh * 64], rb[S][2 * r_])            \
+      OQ_ST32(&sB[(BUF)][(lr + r_ * (NTG / 2)) * BIG8_STRIDE + lh * 64 + 32], rb[S][2 * r_ + 1])   \
     }                                                                                              \
   }
 
@@ -245,8 +257,9 @@ __global__ __launch_bounds__(64 * WM * WN, 512 / (64 * WM * WN)) void gemm_big_k
       }                                                                                                     \
     }                                                                                                       \
   }
-  // Sub-steps of 32 codes in stage ks: 4, or 2 for a final half stage.
-#define OQ_NSUB(KS) ((2 * (KS) + 2 <= nk64) ? 4 : 2)
+  // Sub-steps of 32 codes in local stage ks: 4, 2 for a final half stage, 0
+  // past the end of K.
+#define OQ_NSUB(KS) ((2 * (KG * (KS) + grp) + 2 <= nk64) ? 4 : (2 * (KG * (KS) + grp) < nk64 ? 2 : 0))
 
   // Global loads run NS - 1 stages ahead of the LDS stage being multiplied:
   // at the top of stage kt, ring slot (kt + i) % NS holds stage kt + i for
@@ -261,7 +274,7 @@ __global__ __launch_bounds__(64 * WM * WN, 512 / (64 * WM * WN)) void gemm_big_k
   OQ_LSTORE(0, 0)
   __syncthreads();
   int kt = 0;
-  for (; kt + NS <= nk; kt += NS) {
+  for (; kt + NS <= njl; kt += NS) {
     static_for<NS>([&](auto S_) {
       constexpr int SV = decltype(S_)::value;
       constexpr int SN = (SV + 1) % NS;
@@ -275,13 +288,42 @@ __global__ __launch_bounds__(64 * WM * WN, 512 / (64 * WM * WN)) void gemm_big_k
   static_for<NS>([&](auto S_) {
     constexpr int SV = decltype(S_)::value;
     constexpr int SN = (SV + 1) % NS;
-    if (kt + SV < nk) {
+    if (kt + SV < njl) {
       OQ_COMPUTE((kt + SV) & 1, OQ_NSUB(kt + SV))
-      if (kt + SV + 1 < nk) OQ_LSTORE((kt + SV + 1) & 1, SN)
+      if (kt + SV + 1 < njl) OQ_LSTORE((kt + SV + 1) & 1, SN)
       __syncthreads();
     }
   });
 #undef OQ_NSUB
+  if constexpr (KG > 1) {
+    // Groups 1 .. KG-1 leave their accumulators in their own (now unused)
+    // LDS buffers, lane-major; group 0 adds them in group order.
+    __syncthreads();
+    constexpr int WORDS = WM * WN * TM * TN * 16 * 64;  // one group's accumulators
+    static_assert(WORDS * 4 <= GBYTES, "accumulators exceed a group's buffers");
+    if (grp > 0) {
+      int32_t* red = reinterpret_cast<int32_t*>(smem + grp * GBYTES);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) red[((wave * TM + i) * TN + j) * 1024 + e * 64 + lane] = acc[i][j][e];
+    }
+    __syncthreads();
+    if (grp == 0) {
+#pragma unroll
+      for (int gg = 1; gg < KG; ++gg) {
+        const int32_t* red = reinterpret_cast<const int32_t*>(smem + gg * GBYTES);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][j][e] += red[((wave * TM + i) * TN + j) * 1024 + e * 64 + lane];
+      }
+    }
+  }
 #undef OQ_GLOAD
 #undef OQ_ST32
 #undef OQ_LSTORE
@@ -319,8 +361,10 @@ __global__ __launch_bounds__(64 * WM * WN, 512 / (64 * WM * WN)) void gemm_big_k
       if (EPI == EPI_RESID_F32 && a.gate) gate[j] = static_cast<float>(__builtin_bit_cast(_Float16, a.gate[gcc]));
     }
   }
+  // (Only group 0 holds the summed accumulators.)
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
+    if (grp != 0) break;
     float xr[4][4];
     float rold[4][TN][4];
 #pragma unroll
@@ -374,6 +418,7 @@ __global__ __launch_bounds__(64 * WM * WN, 512 / (64 * WM * WN)) void gemm_big_k
     }
   }
   if (STAGED) {
+    static_assert((BM * BN / 8) % NT == 0, "output pieces per thread");
     __syncthreads();
     // BM rows x BN/8 pieces of 8 outputs; thread t writes pieces t + NT c.
     uint16_t* C = static_cast<uint16_t*>(a.C);
@@ -649,28 +694,30 @@ int gemm_validate(const uint8_t* Xq, int64_t M, const uint8_t* Wq, int64_t N, in
   return OQ_OK;
 }
 
-template <int WM, int WN, int TM, int TN, bool A8, int NS>
+template <int WM, int WN, int TM, int TN, bool A8, int NS, int KG>
 int launch_big_a(const GemmArgs& a, Epilogue epi, int64_t tiles, hipStream_t stream) {
-  const dim3 g(static_cast<unsigned>(tiles)), b(64 * WM * WN);
+  const dim3 g(static_cast<unsigned>(tiles)), b(64 * WM * WN * KG);
   switch (epi) {
-    case EPI_I32: hipLaunchKernelGGL((gemm_big_kernel<EPI_I32, WM, WN, TM, TN, A8, NS>), g, b, 0, stream, a); break;
-    case EPI_F16: hipLaunchKernelGGL((gemm_big_kernel<EPI_F16, WM, WN, TM, TN, A8, NS>), g, b, 0, stream, a); break;
-    case EPI_BF16: hipLaunchKernelGGL((gemm_big_kernel<EPI_BF16, WM, WN, TM, TN, A8, NS>), g, b, 0, stream, a); break;
+    case EPI_I32: hipLaunchKernelGGL((gemm_big_kernel<EPI_I32, WM, WN, TM, TN, A8, NS, KG>), g, b, 0, stream, a); break;
+    case EPI_F16: hipLaunchKernelGGL((gemm_big_kernel<EPI_F16, WM, WN, TM, TN, A8, NS, KG>), g, b, 0, stream, a); break;
+    case EPI_BF16:
+      hipLaunchKernelGGL((gemm_big_kernel<EPI_BF16, WM, WN, TM, TN, A8, NS, KG>), g, b, 0, stream, a);
+      break;
     case EPI_RESID_F32:
       if constexpr (A8) return OQ_ERR_ARG;  // the residual epilogue is a W4A4 DiT path only
-      else hipLaunchKernelGGL((gemm_big_kernel<EPI_RESID_F32, WM, WN, TM, TN, A8, NS>), g, b, 0, stream, a);
+      else hipLaunchKernelGGL((gemm_big_kernel<EPI_RESID_F32, WM, WN, TM, TN, A8, NS, KG>), g, b, 0, stream, a);
       break;
     default: return OQ_ERR_ARG;
   }
   return launch_status();
 }
 
-template <int WM, int WN, int TM, int TN, int NS>
+template <int WM, int WN, int TM, int TN, int NS, int KG = 1>
 int launch_big(const GemmArgs& a, Epilogue epi, int64_t tiles, hipStream_t stream) {
   if constexpr (WM * WN * TM * TN <= 16) {
-    if (a.a_i8) return launch_big_a<WM, WN, TM, TN, true, NS>(a, epi, tiles, stream);
+    if (a.a_i8) return launch_big_a<WM, WN, TM, TN, true, NS, KG>(a, epi, tiles, stream);
   }
-  return launch_big_a<WM, WN, TM, TN, false, NS>(a, epi, tiles, stream);
+  return launch_big_a<WM, WN, TM, TN, false, NS, KG>(a, epi, tiles, stream);
 }
 
 int gemm_launch(const GemmArgs& a, Epilogue epi, hipStream_t stream) {
@@ -695,13 +742,26 @@ int gemm_launch(const GemmArgs& a, Epilogue epi, hipStream_t stream) {
   const int64_t big_tiles = ((a.M + 255) / 256) * ((a.N + 255) / 256);
   if (big_tiles >= 256 && !a.a_i8) return launch_big<2, 4, 4, 2, 3>(a, epi, big_tiles, stream);
   const int64_t mid_tiles = ((a.M + 127) / 128) * ((a.N + 127) / 128);
-  if (mid_tiles >= 256) return launch_big<2, 2, 2, 2, 3>(a, epi, mid_tiles, stream);
+  // Two K groups (two wave groups of one workgroup on alternate stages of K,
+  // summed through LDS) halve the serial stage chain of a tile; a K-grouped
+  // workgroup needs twice the LDS, so they are used only while its tiles
+  // still fit the CUs in one round: 128 x 128 tiles at one workgroup per CU,
+  // 64 x 64 tiles at two.  (Measured 12-34% faster at M = 256 - 1024 with N =
+  // 1536 - 8192; slower once a second round of workgroups is needed.)
+  const bool kgroups = !a.a_i8;
+  if (mid_tiles >= 256) {
+    if (kgroups && mid_tiles <= 256) return launch_big<2, 2, 2, 2, 3, 2>(a, epi, mid_tiles, stream);
+    return launch_big<2, 2, 2, 2, 3>(a, epi, mid_tiles, stream);
+  }
   // Fewer 128 x 128 tiles than CUs (prefill-sized M with N ~ 2048): 64 x 64
-  // tiles of two waves (64 x 32 each), several workgroups per CU.
+  // tiles of two waves (64 x 32 each), several workgroups per CU.  Deep K
+  // (K >= 6144) keeps more register stages in flight (twelve without K
+  // groups: 7-11% faster at M = 816 - 1024, N = 1536 - 2048).
   const int64_t small_tiles = ((a.M + 63) / 64) * ((a.N + 63) / 64);
-  // Deep K (K >= 6144) keeps twelve register stages in flight: 7-11% faster at
-  // M = 816 - 1024 with N = 1536 - 2048 (the loads of a 64 x 64 tile's long K
-  // loop are then issued far enough ahead); shorter K gains nothing from it.
+  if (kgroups && small_tiles <= 512) {
+    if (a.K >= 6144) return launch_big<1, 2, 2, 1, 4, 2>(a, epi, small_tiles, stream);
+    return launch_big<1, 2, 2, 1, 3, 2>(a, epi, small_tiles, stream);
+  }
   if (a.K >= 6144) return launch_big<1, 2, 2, 1, 12>(a, epi, small_tiles, stream);
   return launch_big<1, 2, 2, 1, 3>(a, epi, small_tiles, stream);
 }

@@ -26,7 +26,12 @@ def _codes(rng, R, K):
                                    # small-M row-layout kernel: a final 64-code step (K % 128 == 64),
                                    # 16-row and 64-row groups, 16- and 32-column tiles
                                    (50, 1024, 1088), (17, 2048, 320), (64, 520, 4160), (3, 100, 64),
-                                   (16, 4160, 2112), (50, 8192, 1024), (50, 1024, 4096)])
+                                   (16, 4160, 2112), (50, 8192, 1024), (50, 1024, 4096),
+                                   # two K groups (alternate 128-code stages summed through LDS):
+                                   # the second group's only stage a half stage, no stage at all, an
+                                   # odd stage count, deep K, and 256 128 x 128 tiles (ragged N)
+                                   (1000, 1000, 192), (130, 200, 64), (500, 700, 320), (520, 1000, 6208),
+                                   (250, 16376, 320), (256, 16384, 1536)])
 def test_i32_accumulators_bit_exact(M, N, K):
     print(f"gemm i32 M={M} N={N} K={K}", flush=True)
     rng = np.random.default_rng(M + N + K)
@@ -67,7 +72,8 @@ def test_i32_extreme_magnitudes():
 
 
 @pytest.mark.parametrize("out_dtype", [oq.OUT_F16, oq.OUT_BF16])
-@pytest.mark.parametrize("M,N,K", [(50, 1024, 1024), (200, 320, 2048), (77, 1000, 4096)])
+@pytest.mark.parametrize("M,N,K", [(50, 1024, 1024), (200, 320, 2048), (77, 1000, 4096), (250, 16376, 320),
+                                   (1000, 1000, 3072)])
 def test_dequant_epilogue(M, N, K, out_dtype):
     rng = np.random.default_rng(M * N + K)
     q, qw = _codes(rng, M, K), _codes(rng, N, K)
