@@ -675,8 +675,9 @@ typedef struct {
   const void* act;       /* [M][F]  input of the down / ff2 linear               */
   const float* resid;    /* [M][D]  fp32 residual of the last oq_dit_step after
                             its last block (oq_dit_run_block uses the caller's) */
-  const void* cond_kv;   /* gr00t: [n_blocks/2 rounded up][B*P][2D] k|v of the
-                            conditioning tokens per even block; pi: NULL       */
+  const void* cond_kv;   /* gr00t: k|v of the conditioning tokens of every
+                            even block, head-major [n_blocks/2 rounded up][B]
+                            [H][2 (k, v)][P][head_dim]; pi: NULL              */
   const void* codes;     /* packed codes of the last quantization site the
                             handle produced (its fp16 input is h1, attn, h2 or
                             act): [M][K/2], or the 16-row tiled layout when

@@ -1048,8 +1048,10 @@ Layout layout_for(const oq_dit_config& c) {
   L.xs = off; off += align256(std::max(M, MC) * 4);
   L.part_o = off; off += align256(BH * nsplit * c.tokens * c.head_dim * 4);
   L.part_ml = off; off += align256(BH * nsplit * c.tokens * 2 * 4);
-  L.ckv = off; off += align256(static_cast<size_t>(n_cross(c)) * MC * 2 * D * 2);
-  L.ckvh = off; off += align256(static_cast<size_t>(n_cross(c)) * MC * 2 * D * 2);  // the same, head-major
+  // The conditioning k|v: one block's linear output in row layout (staging),
+  // and every cross-attention block's values head-major.
+  L.ckv = off; off += align256(static_cast<size_t>(n_cross(c) > 0 ? 1 : 0) * MC * 2 * D * 2);
+  L.ckvh = off; off += align256(static_cast<size_t>(n_cross(c)) * MC * 2 * D * 2);
   L.total = off;
   return L;
 }
@@ -1485,7 +1487,7 @@ int set_condition(oq_dit* h, const uint16_t* cond, hipStream_t st) {
   int e = rq_launch(cond, MC, D, D, pow2_divisor(static_cast<int>(D)), 1.0f, xq, xs, nullptr, st);
   if (e != OQ_OK) return e;
   for (int l = 0; l < c.n_blocks; l += 2) {
-    uint16_t* kv = at<uint16_t>(h, h->lay.ckv) + static_cast<int64_t>(l / 2) * MC * 2 * D;
+    uint16_t* kv = at<uint16_t>(h, h->lay.ckv);  // staging, rewritten head-major below
     const oq_qweight& wt = h->blocks[l].cross_kv;
     GemmArgs a{xq, wt.wq, xs, wt.w_scale, nullptr, kv, nullptr, MC, 2 * D, D, 2 * D};
     if ((e = gemm_launch(a, EPI_F16, st)) != OQ_OK) return e;
@@ -1735,7 +1737,7 @@ extern "C" int oq_dit_get_intermediates(const oq_dit* h, oq_dit_intermediates* o
   out->gate_up = h->ws + h->lay.gu;
   out->act = h->ws + h->lay.act;
   out->resid = reinterpret_cast<const float*>(h->ws + h->lay.r);
-  out->cond_kv = oq::is_gr00t(h->cfg) ? h->ws + h->lay.ckv : nullptr;
+  out->cond_kv = oq::is_gr00t(h->cfg) ? h->ws + h->lay.ckvh : nullptr;
   out->codes = h->ws + h->lay.xq;
   out->x_scale = reinterpret_cast<const float*>(h->ws + h->lay.xs);
   out->codes_tiled = h->tiled ? 1 : 0;

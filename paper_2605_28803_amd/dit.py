@@ -220,10 +220,13 @@ class DiT:
         it = _lib.oq_dit_intermediates()
         _check(self.lib.oq_dit_get_intermediates(self.handle, C.byref(it)), "oq_dit_get_intermediates")
         torch.cuda.synchronize(self.device)
-        n = self.MC * 2 * self.cfg_c.hidden
+        D, H = self.cfg_c.hidden, self.cfg_c.n_heads
+        B, P, hd = self.cfg_c.batch, self.cfg_c.prefix, self.cfg_c.head_dim
+        n = self.MC * 2 * D
         off = it.cond_kv - self.workspace.data_ptr() + (l // 2) * n * 2
         raw = self.workspace[off: off + 2 * n].cpu().numpy().view(np.float16)
-        return raw.reshape(self.MC, 2 * self.cfg_c.hidden).astype(np.float64)
+        # head-major [B][H][2][P][hd] -> rows [B*P] of [k | v], head h at columns h*hd
+        return raw.reshape(B, H, 2, P, hd).transpose(0, 3, 2, 1, 4).reshape(B * P, 2 * D).astype(np.float64)
 
     # ------------------------------------------------------------------
     # Static per-step, per-channel steps (the per-(layer, step, channel)
