@@ -665,10 +665,12 @@ def pi_step_without_graph(cfg, inp, steps=20):
     return s.elapsed_time(e) / steps
 
 
-def dit_static_step(cfg, inp, model, n_traj=4, steps=50):
+def dit_static_step(cfg, inp, model, n_traj=24, steps=50):
     """The Pi-0.5 step with the paper-literal static per-step, per-channel
     steps: calibration rollouts (n_traj seeded synthetic initial states, all
-    10 denoising steps, every block and site), the per-(block, step) weight
+    10 denoising steps, every block and site; 24 x 50 = 1200 rows per
+    (block, step, site), so that the nearest-rank 99.9th percentile is the
+    second largest magnitude, not the largest), the per-(block, step) weight
     folds on the device, then the step timed as the main line (graph replay,
     t cycling) -- ten weight copies per block, so the step's weights are no
     longer MALL-resident across steps.  Also reports how far a full

@@ -134,7 +134,7 @@ def cond_kv(cfg, qblocks, cond):
 
 
 def block_trace(cfg, w, qblocks, mod, s_table, r, l, t, B, S, prefix=None, ckv=None, forced=None,
-                static=None):
+                static=None, unquantized=False):
     """Block l at step t on the residual r [B*S, D] (float64), every
     intermediate returned in a dict.
 
@@ -156,7 +156,11 @@ def block_trace(cfg, w, qblocks, mod, s_table, r, l, t, B, S, prefix=None, ckv=N
     static: None (per-token quantizer with the scalar step s_table[l, t, i])
     or (delta, qweights_t): the per-channel static steps delta[i] of the four
     sites at (l, t) and the weights folded with them, a dict like qblocks[l]
-    (eq:perstep_scale with the per-channel table; token scale 1)."""
+    (eq:perstep_scale with the per-channel table; token scale 1).
+
+    unquantized: every linear is the plain float64 product x W^T with the
+    block's weights as given (no rotation, no codes: the model the
+    quantization approximates); qblocks is then unused."""
     D, H, F = cfg.hidden, cfg.n_heads, cfg.mlp
     blk, m = w["blocks"][l], mod[l][t]
     st = s_table[l, t]
@@ -169,6 +173,10 @@ def block_trace(cfg, w, qblocks, mod, s_table, r, l, t, B, S, prefix=None, ckv=N
         return own if v is None else np.asarray(v, dtype=np.float64)
 
     def site(i, x, name):
+        if unquantized:
+            y = x @ np.asarray(w["blocks"][l][name], dtype=np.float64).T
+            out[f"y{i}"] = y
+            return y
         b = hadamard_block(x.shape[1])
         if static is None:
             q, xs, ratio = rotate_quantize_act(x, b, st[i])
@@ -227,9 +235,21 @@ def block_trace(cfg, w, qblocks, mod, s_table, r, l, t, B, S, prefix=None, ckv=N
     raise ValueError(cfg.arch)
 
 
-def block(cfg, w, qblocks, mod, s_table, r, l, t, B, S, prefix=None, ckv=None):
+def block(cfg, w, qblocks, mod, s_table, r, l, t, B, S, prefix=None, ckv=None, unquantized=False):
     """Block l at step t on the residual r [B*S, D] (float64); returns the new residual."""
-    return block_trace(cfg, w, qblocks, mod, s_table, r, l, t, B, S, prefix=prefix, ckv=ckv)["r_out"]
+    return block_trace(cfg, w, qblocks, mod, s_table, r, l, t, B, S, prefix=prefix, ckv=ckv,
+                       unquantized=unquantized)["r_out"]
+
+
+def cond_kv_unquantized(cfg, w, cond):
+    """gr00t: cond_kv with the k|v linear as the plain product (fp16 values)."""
+    out = {}
+    B, P, D = cond.shape
+    for l, blk in enumerate(w["blocks"]):
+        if cfg.arch == "gr00t" and l % 2 == 0:
+            kv = f16(cond.reshape(B * P, D) @ np.asarray(blk["wkv"], dtype=np.float64).T)
+            out[l] = kv.reshape(B, P, 2 * D)
+    return out
 
 
 def in_projection(w, x_t):
@@ -238,7 +258,7 @@ def in_projection(w, x_t):
     return x_t.reshape(B * S, A) @ np.asarray(w["w_in"], np.float64).T + w["b_in"][None, :]
 
 
-def step(cfg, w, qblocks, mod, s_table, x_t, t, prefix=None, ckv=None, trace=None):
+def step(cfg, w, qblocks, mod, s_table, x_t, t, prefix=None, ckv=None, trace=None, unquantized=False):
     """One Euler denoising step.  x_t [B, S, A] float64 -> x_{t+1}.
 
     w: dict with w_in [D, A], b_in [D], w_out [A, D], b_out [A], g_f [D] and
@@ -246,12 +266,13 @@ def step(cfg, w, qblocks, mod, s_table, x_t, t, prefix=None, ckv=None, trace=Non
     qblocks: output of quantize_block_weights.  mod[l][t]: dict of the per-step
     modulation vectors.  s_table [L, T, 4].  prefix: pi, (Kp, Vp) each
     [L, B, P, D]; ckv: gr00t, output of cond_kv.  trace: optional list that
-    receives the residual after each block.
+    receives the residual after each block.  unquantized: every block
+    linear as the plain float64 product (see block_trace).
     """
     B, S, A = x_t.shape
     r = in_projection(w, x_t)
     for l in range(len(w["blocks"])):
-        r = block(cfg, w, qblocks, mod, s_table, r, l, t, B, S, prefix=prefix, ckv=ckv)
+        r = block(cfg, w, qblocks, mod, s_table, r, l, t, B, S, prefix=prefix, ckv=ckv, unquantized=unquantized)
         if trace is not None:
             trace.append(r.copy())
     norm = rms_norm if cfg.arch == "pi" else layer_norm
@@ -261,11 +282,16 @@ def step(cfg, w, qblocks, mod, s_table, x_t, t, prefix=None, ckv=None, trace=Non
     return x_t + dt * v.reshape(B, S, A)
 
 
-def denoise(cfg, w, mod, s_table, x0, prefix=None, cond=None, n_steps=None):
-    """Full Euler loop from x0 over n_steps (default cfg.steps)."""
-    qblocks = quantize_block_weights(cfg, w["blocks"])
-    ckv = cond_kv(cfg, qblocks, cond) if cfg.arch == "gr00t" else None
+def denoise(cfg, w, mod, s_table, x0, prefix=None, cond=None, n_steps=None, unquantized=False):
+    """Full Euler loop from x0 over n_steps (default cfg.steps); unquantized:
+    the same loop with every block linear as the plain float64 product."""
+    if unquantized:
+        qblocks = None
+        ckv = cond_kv_unquantized(cfg, w, cond) if cfg.arch == "gr00t" else None
+    else:
+        qblocks = quantize_block_weights(cfg, w["blocks"])
+        ckv = cond_kv(cfg, qblocks, cond) if cfg.arch == "gr00t" else None
     x = np.asarray(x0, dtype=np.float64)
     for t in range(cfg.steps if n_steps is None else n_steps):
-        x = step(cfg, w, qblocks, mod, s_table, x, t, prefix=prefix, ckv=ckv)
+        x = step(cfg, w, qblocks, mod, s_table, x, t, prefix=prefix, ckv=ckv, unquantized=unquantized)
     return x

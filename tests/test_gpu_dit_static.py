@@ -144,3 +144,38 @@ def test_clearing_static_mode_restores_the_driver():
     assert not torch.equal(a, b)
     assert torch.isfinite(b).all()
     model.close()
+
+
+@pytest.mark.parametrize("arch", ["pi", "gr00t"])
+def test_deviation_from_unquantized_rollout(arch):
+    """Reported, not gated (both are quantized models): how far the full
+    denoising loop of the per-token driver and of the static-step driver
+    (calibrated on 24 trajectories, enough rows that the 99.9th percentile is
+    not the maximum) lands from the unquantized float64 rollout of the same
+    synthetic DiT (the oracle with every linear a plain product), as the
+    relative L2 of x_T - x_0; the oracle's own per-token model is shown
+    beside them.  Pi: 3 blocks; GR00T: 2 blocks at batch 4."""
+    cfg = configs.DIT_PI if arch == "pi" else configs.DIT_GR00T
+    inp = dit_inputs.make_dit_inputs(cfg, n_blocks=3 if arch == "pi" else 2, batch=None if arch == "pi" else 4)
+    model = oq.DiT(cfg, inp, device="cuda:0")
+    T = cfg.steps
+    x0 = torch.from_numpy(inp["x0"].astype(np.float32)).to(DEV)
+    xt = x0.clone()
+    model.denoise(xt, T)
+    table = model.calibrate_static_steps(_x0s(cfg, inp, 24))
+    model.set_static_steps(inp, table)
+    xs = x0.clone()
+    model.denoise(xs, T)
+    torch.cuda.synchronize()
+    x0n = inp["x0"].astype(np.float32).astype(np.float64)
+    kw = {"prefix": (inp["kp"], inp["vp"])} if arch == "pi" else {"cond": inp["cond"]}
+    ref = odit.denoise(cfg, inp["w"], inp["mod"], inp["s_table"], x0n, unquantized=True, **kw)
+    q_oracle = odit.denoise(cfg, inp["w"], inp["mod"], inp["s_table"], x0n, **kw)
+    dev = lambda x: parity.rel_l2(np.asarray(x, np.float64) - x0n, ref - x0n)
+    d_tok, d_static, d_oracle = dev(xt.cpu().numpy()), dev(xs.cpu().numpy()), dev(q_oracle)
+    d_between = parity.rel_l2(xs.cpu().numpy() - x0n, xt.cpu().numpy() - x0n)
+    print(f"{arch} {T}-step denoise, rel L2 of x_T - x_0 against the unquantized fp64 rollout: "
+          f"per-token driver {d_tok:.4f}, static-step driver {d_static:.4f}, oracle per-token model {d_oracle:.4f}; "
+          f"static against per-token {d_between:.4f}", flush=True)
+    assert np.isfinite([d_tok, d_static, d_oracle]).all()
+    model.close()

@@ -184,3 +184,20 @@ def test_block_is_block_trace_output():
     tf = dit.block_trace(cfg, w, qb, inp["mod"], inp["s_table"], r, 0, 2, 1, cfg.tokens,
                          prefix=(inp["kp"], inp["vp"]), forced=forced)
     assert np.array_equal(tf["r_out"], a)
+
+
+def test_unquantized_mode_on_the_golden_blocks():
+    """Every quantization of the hand-worked blocks is exact, so the oracle's
+    unquantized mode (plain float64 products) must give the same numbers."""
+    from functools import partial
+    P.check_dit_block_pi(partial(dit.block_trace, unquantized=True), dit.quantize_block_weights)
+    P.check_dit_block_gr00t(partial(dit.block_trace, unquantized=True), dit.quantize_block_weights, dit.cond_kv)
+
+
+def test_unquantized_conditioning_kv_is_the_plain_product():
+    cfg = configs.DIT_GR00T
+    inp = dit_inputs.make_dit_inputs(cfg, n_blocks=2, batch=2)
+    ckv = dit.cond_kv_unquantized(cfg, inp["w"], inp["cond"])
+    ref = torch.einsum("bpd,nd->bpn", _t(inp["cond"]), _t(inp["w"]["blocks"][0]["wkv"])).numpy()
+    assert np.allclose(ckv[0], dit.f16(ref), rtol=0, atol=1e-3)
+    assert set(ckv) == {0}
