@@ -671,7 +671,9 @@ typedef struct {
   const void* qkv;       /* [M][3D] q|k|v linear output (gr00t even: q, [M][D]) */
   const void* attn;      /* [M][D]  attention output, input of the o linear      */
   const void* h2;        /* [M][D]  norm output, input of the gate|up / ff0 linear */
-  const void* gate_up;   /* [M][2F] gate|up output (gr00t: ff0 output, [M][F])   */
+  const void* gate_up;   /* pi: [M][2F] gate|up output; gr00t: not written (the
+                            ff0 linear applies the GELU in its epilogue and
+                            writes act directly)                              */
   const void* act;       /* [M][F]  input of the down / ff2 linear               */
   const float* resid;    /* [M][D]  fp32 residual of the last oq_dit_step after
                             its last block (oq_dit_run_block uses the caller's) */

@@ -61,8 +61,23 @@ int rq_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block, f
 int rq_validate(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block,
                 const void* out, const float* x_scale);
 
+// ---- GELU (tanh form) ---------------------------------------------------------
+// gelu_tanh(x) = 0.5 x (1 + tanh(u)), u = sqrt(2/pi) (x + 0.044715 x^3).
+// Since 0.5 (1 + tanh(u)) = 1 / (1 + e^(-2u)), this is x / (1 + e^(-2u)):
+// one hardware exp and one reciprocal (each within a few fp32 ulp; the result
+// is rounded to fp16 by the caller).  e^(-2u) -> inf gives -0 for very
+// negative x, e^(-2u) -> 0 gives x.
+__device__ __forceinline__ float gelu_tanh(float x) {
+  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
+  const float k1 = 0.044715f;
+  const float u = k0 * fmaf(k1 * x * x, x, x);
+  return x * __builtin_amdgcn_rcpf(1.0f + __expf(-2.0f * u));
+}
+
 // ---- GEMM ------------------------------------------------------------------
-enum Epilogue { EPI_I32 = 0, EPI_F16 = 1, EPI_BF16 = 2, EPI_RESID_F32 = 3 };
+// EPI_GELU_F16: y = fp16(gelu_tanh(fp16(acc x_scale w_scale + bias))), the
+// activation of a non-gated MLP applied to the linear's fp16 output.
+enum Epilogue { EPI_I32 = 0, EPI_F16 = 1, EPI_BF16 = 2, EPI_RESID_F32 = 3, EPI_GELU_F16 = 4 };
 
 struct GemmArgs {
   const uint8_t* A;      // [M][K/2]

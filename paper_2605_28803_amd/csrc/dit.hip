@@ -324,18 +324,6 @@ __global__ __launch_bounds__(256) void norm_rq1024_kernel(const float* __restric
   rq1024_row(x, row, valid, o, xch, red[1]);
 }
 
-// gelu_tanh(x) = 0.5 x (1 + tanh(u)), u = sqrt(2/pi) (x + 0.044715 x^3).
-// Since 0.5 (1 + tanh(u)) = 1 / (1 + e^(-2u)), this is x / (1 + e^(-2u)):
-// one hardware exp and one reciprocal (each within a few fp32 ulp; the result
-// is rounded to fp16 by the caller).  e^(-2u) -> inf gives -0 for very
-// negative x, e^(-2u) -> 0 gives x.
-__device__ __forceinline__ float gelu_tanh(float x) {
-  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
-  const float k1 = 0.044715f;
-  const float u = k0 * fmaf(k1 * x * x, x, x);
-  return x * __builtin_amdgcn_rcpf(1.0f + __expf(-2.0f * u));
-}
-
 // GATED: a = fp16(gelu_tanh(gate) up) from gu = [gate | up] (fp16 [M][2F]);
 // otherwise a = fp16(gelu_tanh(u)) from u (fp16 [M][F]).  Then rotate +
 // quantize a.
@@ -1412,8 +1400,7 @@ int run_block_gr00t(oq_dit* h, int l, int t, float* r, hipStream_t st, int until
   uint16_t* h1 = keep ? at<uint16_t>(h, h->lay.h1) : nullptr;
   uint16_t* qkv = at<uint16_t>(h, h->lay.qkv);
   uint16_t* h2 = keep ? at<uint16_t>(h, h->lay.h2) : nullptr;
-  uint16_t* ff = at<uint16_t>(h, h->lay.gu);
-  uint16_t* act = keep ? at<uint16_t>(h, h->lay.act) : nullptr;
+  uint16_t* act = at<uint16_t>(h, h->lay.act);  // written by the ff0 epilogue, read by its quantizer
   int e;
   if ((e = norm_rq(h, r, bw.g1, mod_ptr(h, l, t, 0), mod_ptr(h, l, t, 1), h1, s[0], st, ss.d[0])) != OQ_OK) return e;
   if (until == 0) return OQ_OK;
@@ -1432,8 +1419,14 @@ int run_block_gr00t(oq_dit* h, int l, int t, float* r, hipStream_t st, int until
   if ((e = norm_rq(h, r, bw.g2, nullptr, static_cast<const uint16_t*>(bw.b2), h2, s[2], st, ss.d[2])) != OQ_OK)
     return e;
   if (until == 2) return OQ_OK;
-  if ((e = gemm(h, *ss.w[2], D, F, EPI_F16, ff, F, nullptr, st)) != OQ_OK) return e;
-  if ((e = gelu_rq(h, ff, act, s[3], st, ss.d[3])) != OQ_OK) return e;
+  // The non-gated GELU is elementwise: the ff0 linear applies it in its
+  // epilogue (act = fp16(gelu(fp16(y)))), and the activation rows are then
+  // rotated and quantized by the stand-alone kernel.
+  if ((e = gemm(h, *ss.w[2], D, F, EPI_GELU_F16, act, F, nullptr, st)) != OQ_OK) return e;
+  const int64_t M = static_cast<int64_t>(c.batch) * c.tokens;
+  if ((e = rq_launch(act, M, F, F, pow2_divisor(static_cast<int>(F)), ss.d[3] ? 1.0f : s[3],
+                     at<uint8_t>(h, h->lay.xq), at<float>(h, h->lay.xs), nullptr, st, h->tiled, ss.d[3])) != OQ_OK)
+    return e;
   if (until == 3) return OQ_OK;
   return gemm(h, *ss.w[3], F, D, EPI_RESID_F32, r, D, nullptr, st);
 }

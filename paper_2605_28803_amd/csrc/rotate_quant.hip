@@ -113,6 +113,7 @@ bool rq_mfma_shape(int64_t K, int* ng, int* w) {
     case 2048: *ng = 4; *w = 1; return true;
     case 3072: *ng = 6; *w = 1; return true;
     case 4096: *ng = 8; *w = 1; return true;
+    case 6144: *ng = 12; *w = 1; return true;  // the 6144-channel MLP input (blocks of <= 2048)
     case 8192: *ng = 4; *w = 4; return true;  // 68 VGPRs (7 waves per SIMD) against 136 for (8, 2)
     case 16384: *ng = 8; *w = 4; return true;
     default: return false;
@@ -148,6 +149,7 @@ int rq_mfma_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_blo
   OQ_RQM(4, 1)
   OQ_RQM(6, 1)
   OQ_RQM(8, 1)
+  OQ_RQM(12, 1)
   OQ_RQM(4, 4)
   OQ_RQM(8, 4)
 #undef OQ_RQM

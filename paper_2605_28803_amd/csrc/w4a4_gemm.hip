@@ -337,7 +337,7 @@ void gemm_big_kernel(GemmArgs a) {
   // written from the accumulator layout directly.
   const int col_in = lane & 31;
   const int row_grp = 4 * (lane >> 5);
-  constexpr bool STAGED = EPI == EPI_F16 || EPI == EPI_BF16;
+  constexpr bool STAGED = EPI == EPI_F16 || EPI == EPI_BF16 || EPI == EPI_GELU_F16;
   constexpr int TP = BN + 8;  // halves per staged row
   static_assert(!STAGED || BM * TP * 2 <= 2 * (BM + BN) * BIG8_STRIDE, "staged tile exceeds LDS");
   uint16_t* tile = reinterpret_cast<uint16_t*>(smem);
@@ -395,8 +395,16 @@ void gemm_big_kernel(GemmArgs a) {
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
             const float y = static_cast<float>(acc[i][j][4 * q + u] >> (A8 ? 4 : 8)) * xr[q][u] * wsc[j] + bias[j];
-            tile[(lr0 + u) * TP + wn * 32 * TN + j * 32 + col_in] =
-                EPI == EPI_F16 ? __builtin_bit_cast(uint16_t, static_cast<_Float16>(y)) : f32_to_bf16_rne(y);
+            uint16_t hv;
+            if constexpr (EPI == EPI_F16) {
+              hv = __builtin_bit_cast(uint16_t, static_cast<_Float16>(y));
+            } else if constexpr (EPI == EPI_GELU_F16) {
+              hv = __builtin_bit_cast(
+                  uint16_t, static_cast<_Float16>(gelu_tanh(static_cast<float>(static_cast<_Float16>(y)))));
+            } else {
+              hv = f32_to_bf16_rne(y);
+            }
+            tile[(lr0 + u) * TP + wn * 32 * TN + j * 32 + col_in] = hv;
           }
           continue;
         }
@@ -471,6 +479,9 @@ __device__ __forceinline__ void store_out(const GemmArgs& a, int64_t off, int v,
   const float y = static_cast<float>(v) * xs * ws + bias;
   if (EPI == EPI_F16) {
     static_cast<_Float16*>(a.C)[off] = static_cast<_Float16>(y);
+  } else if (EPI == EPI_GELU_F16) {
+    static_cast<_Float16*>(a.C)[off] =
+        static_cast<_Float16>(gelu_tanh(static_cast<float>(static_cast<_Float16>(y))));
   } else if (EPI == EPI_BF16) {
     static_cast<uint16_t*>(a.C)[off] = f32_to_bf16_rne(y);
   } else {
@@ -703,6 +714,10 @@ int launch_big_a(const GemmArgs& a, Epilogue epi, int64_t tiles, hipStream_t str
     case EPI_BF16:
       hipLaunchKernelGGL((gemm_big_kernel<EPI_BF16, WM, WN, TM, TN, A8, NS, KG>), g, b, 0, stream, a);
       break;
+    case EPI_GELU_F16:
+      if constexpr (A8) return OQ_ERR_ARG;  // a DiT path only
+      else hipLaunchKernelGGL((gemm_big_kernel<EPI_GELU_F16, WM, WN, TM, TN, A8, NS, KG>), g, b, 0, stream, a);
+      break;
     case EPI_RESID_F32:
       if constexpr (A8) return OQ_ERR_ARG;  // the residual epilogue is a W4A4 DiT path only
       else hipLaunchKernelGGL((gemm_big_kernel<EPI_RESID_F32, WM, WN, TM, TN, A8, NS, KG>), g, b, 0, stream, a);
@@ -724,13 +739,14 @@ int gemm_launch(const GemmArgs& a, Epilogue epi, hipStream_t stream) {
   if (a.M == 0) return OQ_OK;
   // Tiled token codes always take the small-M kernel (row groups of 64 along
   // grid.y when M > 64); row-layout codes take it up to M = 64.
-  if (a.a_i8 && epi == EPI_RESID_F32) return OQ_ERR_ARG;
+  if (a.a_i8 && (epi == EPI_RESID_F32 || epi == EPI_GELU_F16)) return OQ_ERR_ARG;
   if (a.M <= 64 || a.a_tiled) {
     switch (epi) {
       case EPI_I32: return launch_small_any<EPI_I32>(a, stream);
       case EPI_F16: return launch_small_any<EPI_F16>(a, stream);
       case EPI_BF16: return launch_small_any<EPI_BF16>(a, stream);
       case EPI_RESID_F32: return launch_small_any<EPI_RESID_F32>(a, stream);
+      case EPI_GELU_F16: return launch_small_any<EPI_GELU_F16>(a, stream);
       default: return OQ_ERR_ARG;
     }
   }

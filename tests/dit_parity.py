@@ -71,7 +71,9 @@ def check_block(cfg, inp, model, l, t, r_in, static_delta=None):
     r = np.asarray(r_in, dtype=np.float32).astype(np.float64)
     gr = cfg.arch == "gr00t"
     site0 = "q" if gr and l % 2 == 0 else "qkv"
-    names = ("h1", site0, "attn", "h2", "gate_up", "act")
+    # gr00t: the ff0 linear applies the GELU in its epilogue, so its fp16
+    # output before the activation is not kept; act is checked instead.
+    names = ("h1", site0, "attn", "h2", "act") if gr else ("h1", site0, "attn", "h2", "gate_up", "act")
     forced = {nm: it[nm] for nm in names}
     for i in range(4):
         forced[f"codes{i}"] = codes[i]
