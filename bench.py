@@ -880,6 +880,13 @@ def sweep_records(Ms=None, Ks=None, reps=10, sink=None):
     return out
 
 
+def prefill_gemms(reps=5):
+    """The six prefill GEMM shapes (M in {4096, 16384} x K = N in {4096, 8192,
+    16384}), cold, reps launches each: the command the MFMA counter summary
+    of the W4A4 GEMM is taken with (sweep inputs and timing)."""
+    return [r for r in sweep_records(Ms=[4096, 16384], Ks=[4096, 8192, 16384], reps=reps)]
+
+
 def cpu_model():
     try:
         for line in open("/proc/cpuinfo"):
@@ -1071,6 +1078,7 @@ def main():
     ap.add_argument("--w4a8-only", action="store_true")
     ap.add_argument("--prepare-only", action="store_true")
     ap.add_argument("--cpu-kernels-only", action="store_true")
+    ap.add_argument("--gemm-prefill-only", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (--gpus must be 1)", file=sys.stderr)
@@ -1091,6 +1099,9 @@ def main():
         print(json.dumps({"w4a8": w4a8_kernels()}), flush=True)
     elif args.prepare_only:
         print(json.dumps({"weight_preparation": prepare_kernels()}), flush=True)
+    elif args.gemm_prefill_only:
+        for rec in prefill_gemms():
+            print(json.dumps(rec), flush=True)
     elif args.cpu_kernels_only:
         print(json.dumps({"cpu_oracle_kernels": cpu_kernel_baselines()}), flush=True)
     else:
