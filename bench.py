@@ -289,7 +289,8 @@ def composite_kernels():
     matrices (the kernel's work does not depend on their values).  Beside each
     online figure: the same transform with P folded into the producer (the
     input already in the permuted order, perm = None), and K = 16384, where
-    the online gather stages only 2 rows per workgroup."""
+    each row is split into channel chunks whose workgroups exchange their row
+    maxima."""
     import torch
     import paper_2605_28803_amd as oq
     from workloads import generators as G

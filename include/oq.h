@@ -227,6 +227,16 @@ int oq_w4a4_gemm_i32_tiled(const uint8_t* Xt, int64_t M, const uint8_t* Wq, int6
  *          and summed in fp32.
  * s_table, t  as oq_rotate_quantize_act
  * Xq       device [M][K/2] codes (16-byte aligned), x_scale device fp32 [M]
+ * Device memory: above K = 4096 (and at K = 4096 with perm NULL and M > 1024)
+ * the rows are split into channel chunks whose workgroups exchange their
+ * partial row maxima through a library-owned device buffer (the inverse
+ * permutation and one float per row and chunk), allocated on the first call
+ * on a GPU, grown when a call needs more and kept until the process ends.
+ * Such calls therefore may allocate, and calls that overlap on one GPU (other
+ * streams, other host threads) share that buffer and must not run
+ * concurrently.  A token scale written as NaN reports that a chunk's
+ * exchange did not complete (never expected; the codes of that row are then
+ * unspecified).
  * Errors: OQ_ERR_NULL, OQ_ERR_SHAPE, OQ_ERR_ALIGN, OQ_ERR_ARG, OQ_ERR_DEVICE,
  * OQ_ERR_HIP.
  */

@@ -7,8 +7,14 @@
 // scalar form): z = s_t y, Delta = max|z| / 7, q = round_half_even(z / Delta),
 // x_scale = Delta / s_t.
 //
-// One workgroup of four waves owns RW rows.  The rows are staged in LDS as
-// fp16.  Pass 1: wave w takes the 64-channel blocks b = w, w + 4, ...; for
+// Three kernels.  Up to K = 4096, rq_composite1_kernel keeps whole rows in
+// LDS and every y value in registers (one pass).  Above, rq_composite_x_kernel
+// splits each row into chunks of channels whose workgroups exchange their
+// partial row maxima (one pass, each y computed once); K that no chunk width
+// divides takes the two-pass rq_composite_kernel described next.
+//
+// Two-pass kernel: one workgroup of four waves owns RW rows.  The rows are
+// staged in LDS as fp16.  Pass 1: wave w takes the 64-channel blocks b = w, w + 4, ...; for
 // each, the A fragment (rows x 32 permuted channels) is gathered from LDS
 // through perm (the v_mfma_f32_16x16x32_f16 operand layout: lane l holds row
 // l % 16 and the 8 consecutive k values 8 (l / 16) .. + 7), the B fragment is
@@ -19,7 +25,9 @@
 // writes int8 codes to LDS, which are packed two per byte and stored
 // coalesced.  fp16 x fp16 products are exact in fp32; the 64-term sums are
 // the only rounding of the transform.  Rows past RW in a fragment are zero.
+#include <algorithm>
 #include <cmath>
+#include <mutex>
 
 #include "common.h"
 #include "rq_device.h"
@@ -425,6 +433,358 @@ __global__ __launch_bounds__(512) void rq_composite1_kernel(const uint16_t* __re
   }
 }
 
+// ---------------------------------------------------------------------------
+// Rows wider than a workgroup can stage (K > 4096): the permuted channels of
+// a row are cut into nq = K / C chunks of C channels, and each (tile of R =
+// 16 RG rows, chunk) pair is one workgroup, so that each block matrix R_b is
+// read once per R rows instead of once per few rows.  The nq workgroups of a
+// tile exchange their rows' partial maxima through per-launch slots in global
+// memory (initialised to -1 by comp_prep_kernel; a published maximum is >= 0)
+// and each quantizes its own chunk, so every y value is computed once and
+// stays in registers.
+//
+// Staging: each thread owns K / 8 / 512 pieces of 8 input channels; with the
+// online permutation it looks up the permuted position j = P^-1(k) of each of
+// its channels once (pinv, written by comp_prep_kernel) and, for every row,
+// loads the piece with one 16-byte read and writes the channels whose j falls
+// in this chunk to LDS at j - qC.  The whole row is read by each of the nq
+// workgroups (from L2: the tile's workgroups are placed on one XCD, adjacent
+// in dispatch order).  Without a permutation the chunk's columns are copied
+// directly.
+//
+// Exchange: the tile's workgroups are dispatched together (ids x + 8 (nq t' +
+// q) for XCD x), so a workgroup only waits for partners dispatched at the same
+// time.  The wait polls with agent-scope atomic loads and is bounded; if the
+// bound is ever reached the tile's token scales are written as NaN (never a
+// silent result) and the workgroup finishes, so the grid always drains.
+// ---------------------------------------------------------------------------
+constexpr int kPollLimit = 1 << 20;
+
+__global__ __launch_bounds__(256) void comp_prep_kernel(const int32_t* __restrict__ perm, int K,
+                                                        uint16_t* __restrict__ pinv, float* __restrict__ slots,
+                                                        int64_t nslots) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  // A perm entry out of range is clamped, so every write stays inside pinv
+  // (a non-permutation gives wrong codes, never an access out of bounds).
+  if (perm && i < K) pinv[min(max(perm[i], 0), K - 1)] = static_cast<uint16_t>(i);
+  if (i < nslots) slots[i] = -1.0f;
+}
+
+template <int RG, int C, bool GATHER, int WAVES, int PF>
+__global__ __launch_bounds__(64 * WAVES) void rq_composite_x_kernel(
+    const uint16_t* __restrict__ X, int64_t M, int K, int64_t ldx, const uint16_t* __restrict__ pinv,
+    const uint16_t* __restrict__ Rt, float s_t, uint8_t* __restrict__ Xq, float* __restrict__ xs,
+    float* __restrict__ slots, int nq, int ntiles) {
+  constexpr int NT = 64 * WAVES;
+  constexpr int R = 16 * RG, XS = C + 8;
+  constexpr int NBC = C / kCB, NBW = NBC / WAVES;  // blocks per chunk, per wave
+  static_assert(NBW >= 1 && NBC % WAVES == 0, "chunk blocks per wave");
+  static_assert(PF >= 2, "block matrix ring depth");
+  __shared__ __attribute__((aligned(16))) uint16_t sx[R * XS];
+  __shared__ float red[WAVES][R];
+  __shared__ float gscale[R];
+  __shared__ int timed_out;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int xcd = blockIdx.x % 8, idx = blockIdx.x / 8;
+  const int q = idx % nq;
+  const int tile = (idx / nq) * 8 + xcd;
+  if (tile >= ntiles) return;  // every workgroup of such a tile id returns
+  const int64_t row0 = static_cast<int64_t>(tile) * R;
+  const int cbase = q * C;
+  if (tid == 0) timed_out = 0;
+
+  // ---- y = x_chunk . BlockDiag(R_b) for this wave's NBW blocks, kept in
+  // registers.  The block matrices run through a ring of PF register stages;
+  // the first PF - 1 are requested before the rows are staged.
+  const int r16 = lane & 15, qq = lane >> 4;
+  const int wb0 = wave * NBW;  // first block of this wave within the chunk
+  auto load_b = [&](int i, c8h (&f)[4][2]) {
+    const int64_t gb = static_cast<int64_t>(q) * NBC + wb0 + (i < NBW ? i : 0);
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+        f[cb][kk] = *reinterpret_cast<const c8h*>(Rt + (gb * kCB + cb * 16 + r16) * kCB + kk * 32 + 8 * qq);
+  };
+  c8h bring[PF][4][2];
+#pragma unroll
+  for (int i = 0; i < PF - 1; ++i)
+    if (i < NBW) load_b(i, bring[i]);
+  // ---- Stage the chunk of R rows in LDS (rows past M as zeros).
+  if constexpr (GATHER) {
+    const int npc = K / 8;                       // pieces per row
+    constexpr int PMAX = 16384 / 8 / NT;         // pieces per thread at K = 16384
+    const int ppc = (npc + NT - 1) / NT;         // pieces per thread here
+    uint32_t dst[PMAX][4];                       // local positions of the 8 channels, 2 per word, 0xFFFF = none
+#pragma unroll
+    for (int pi = 0; pi < PMAX; ++pi) {
+      const int p = tid + NT * pi;
+      uint4 pv = make_uint4(0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu);
+      if (pi < ppc && p < npc) pv = *reinterpret_cast<const uint4*>(pinv + 8 * p);
+      const uint32_t w[4] = {pv.x, pv.y, pv.z, pv.w};
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        uint32_t lo = (w[c] & 0xFFFFu) - cbase, hi = (w[c] >> 16) - cbase;
+        lo = (pi < ppc && p < npc && lo < static_cast<uint32_t>(C)) ? lo : 0xFFFFu;
+        hi = (pi < ppc && p < npc && hi < static_cast<uint32_t>(C)) ? hi : 0xFFFFu;
+        dst[pi][c] = lo | (hi << 16);
+      }
+    }
+    // Rows in batches of RB, double-buffered: the loads of batch b + 1 are
+    // issued before batch b is written to LDS.
+    constexpr int RB = 4;
+    static_assert(R % RB == 0, "row batches");
+    uint4 v[2][RB][PMAX];
+    auto load_rows = [&](int r0, uint4 (&buf)[RB][PMAX]) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const int64_t gr = row0 + r0 + rb;
+        const bool rok = gr < M;
+#pragma unroll
+        for (int pi = 0; pi < PMAX; ++pi) {
+          const int p = tid + NT * pi;
+          const bool ok = rok && pi < ppc && p < npc;
+          buf[rb][pi] = *reinterpret_cast<const uint4*>(X + (ok ? gr : 0) * ldx + (ok ? 8 * p : 0));
+          if (!ok) buf[rb][pi] = make_uint4(0, 0, 0, 0);
+        }
+      }
+    };
+    load_rows(0, v[0]);
+#pragma unroll
+    for (int bt = 0; bt < R / RB; ++bt) {
+      if (bt + 1 < R / RB) load_rows((bt + 1) * RB, v[(bt + 1) & 1]);
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        uint16_t* srow = sx + (bt * RB + rb) * XS;
+#pragma unroll
+        for (int pi = 0; pi < PMAX; ++pi) {
+          const uint4 x4 = v[bt & 1][rb][pi];
+          const uint32_t w[4] = {x4.x, x4.y, x4.z, x4.w};
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            const uint32_t lo = dst[pi][c] & 0xFFFFu, hi = dst[pi][c] >> 16;
+            if (lo != 0xFFFFu) srow[lo] = static_cast<uint16_t>(w[c]);
+            if (hi != 0xFFFFu) srow[hi] = static_cast<uint16_t>(w[c] >> 16);
+          }
+        }
+      }
+    }
+    // A permutation gives every position of the chunk exactly one channel, so
+    // every LDS element of the R rows is written (rows past M with zeros).
+  } else {
+    constexpr int PPR = C / 8;  // 16-byte pieces per row of the chunk
+    for (int p0 = tid; p0 < R * PPR; p0 += NT * 8) {
+      uint4 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int p = p0 + NT * u;
+        const int r = p / PPR, c8 = p % PPR;
+        const bool ok = p < R * PPR && row0 + r < M;
+        v[u] = *reinterpret_cast<const uint4*>(X + (ok ? row0 + r : 0) * ldx + cbase + (ok ? 8 * c8 : 0));
+        if (!ok) v[u] = make_uint4(0, 0, 0, 0);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int p = p0 + NT * u;
+        if (p < R * PPR) *reinterpret_cast<uint4*>(&sx[(p / PPR) * XS + 8 * (p % PPR)]) = v[u];
+      }
+    }
+  }
+  __syncthreads();
+
+  c4f y[NBW][4][RG];
+  float amax[RG][4];
+#pragma unroll
+  for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) amax[rg][e] = 0.0f;
+#pragma unroll
+  for (int i = 0; i < NBW; ++i) {
+    if (i + PF - 1 < NBW) load_b(i + PF - 1, bring[(i + PF - 1) % PF]);
+    __builtin_amdgcn_sched_barrier(0);
+    const c8h (&bf)[4][2] = bring[i % PF];
+#pragma unroll
+    for (int rg = 0; rg < RG; ++rg) {
+      const uint16_t* ap = &sx[(rg * 16 + r16) * XS + (wb0 + i) * kCB + 8 * qq];
+      const c8h a0 = *reinterpret_cast<const c8h*>(ap);
+      const c8h a1 = *reinterpret_cast<const c8h*>(ap + 32);
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) {
+        c4f acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, bf[cb][0], c4f{0, 0, 0, 0}, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, bf[cb][1], acc, 0, 0, 0);
+        y[i][cb][rg] = acc;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) amax[rg][e] = fmaxf(amax[rg][e], fabsf(acc[e]));
+      }
+    }
+  }
+  // Chunk maxima per row: across the 16 lanes of a row group, then the waves.
+#pragma unroll
+  for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float m = amax[rg][e];
+      m = fmaxf(m, rqd::lane_xor<1>(m));
+      m = fmaxf(m, rqd::lane_xor<2>(m));
+      m = fmaxf(m, rqd::lane_xor<4>(m));
+      m = fmaxf(m, rqd::lane_xor<8>(m));
+      if (r16 == 0) red[wave][rg * 16 + 4 * qq + e] = m;
+    }
+  __syncthreads();  // also: every wave's reads of sx are done (sx is reused for the codes)
+  float* tslots = slots + static_cast<int64_t>(tile) * nq * R;  // [nq][R] of this tile
+  if (tid < R) {
+    float m = red[0][tid];
+#pragma unroll
+    for (int w = 1; w < WAVES; ++w) m = fmaxf(m, red[w][tid]);
+    if (nq == 1) {
+      red[0][tid] = m;
+    } else {
+      __hip_atomic_store(&tslots[q * R + tid], m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+  if (nq > 1) {
+    // Thread t < nq R waits for partner t / R's maximum of row t % R (its own
+    // chunk's included).
+    for (int t = tid; t < nq * R; t += NT) {
+      float v = __hip_atomic_load(&tslots[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      for (int it = 0; !(v >= 0.0f) && it < kPollLimit; ++it) {
+        __builtin_amdgcn_s_sleep(2);
+        v = __hip_atomic_load(&tslots[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      if (!(v >= 0.0f)) timed_out = 1;
+    }
+    __syncthreads();
+    if (tid < R) {
+      float m = 0.0f;
+      for (int p = 0; p < nq; ++p)
+        m = fmaxf(m, __hip_atomic_load(&tslots[p * R + tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+      red[0][tid] = m;
+    }
+  }
+  __syncthreads();
+  if (tid < R) {
+    const float m = red[0][tid];
+    const float a_z = m * s_t;
+    const float delta = a_z / 7.0f;
+    gscale[tid] = delta > 0.0f ? s_t / delta : 0.0f;
+    if (q == 0 && row0 + tid < M) xs[row0 + tid] = timed_out ? __builtin_nanf("") : delta / s_t;
+  }
+  __syncthreads();
+
+  // ---- Codes: 8 consecutive channels packed into a dword across lanes and
+  // staged in LDS (the chunk's rows, C / 2 bytes each), then stored as 16-byte pieces.
+  uint32_t* scodes = reinterpret_cast<uint32_t*>(sx);  // [R][C / 8] dwords
+#pragma unroll
+  for (int i = 0; i < NBW; ++i)
+#pragma unroll
+    for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int row = rg * 16 + 4 * qq + e;
+        const float g = gscale[row];
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) {
+          uint32_t c = __float_as_uint(fmaf(y[i][cb][rg][e], g, rqd::kRoundMagic)) & 0xFu;
+          c |= __float_as_uint(rqd::lane_xor<1>(__uint_as_float(c))) << 4;
+          c |= __float_as_uint(rqd::lane_xor<2>(__uint_as_float(c))) << 8;
+          c |= __float_as_uint(rqd::lane_xor<4>(__uint_as_float(c))) << 16;
+          if ((r16 & 7) == 0) scodes[row * (C / 8) + ((wb0 + i) * kCB + cb * 16 + r16) / 8] = c;
+        }
+      }
+  __syncthreads();
+  constexpr int CPR = C / 32;  // 16-byte code pieces per row of the chunk
+  for (int p = tid; p < R * CPR; p += NT) {
+    const int r = p / CPR, c16 = p % CPR;
+    if (row0 + r >= M) continue;
+    *reinterpret_cast<uint4*>(Xq + (row0 + r) * static_cast<int64_t>(K / 2) + cbase / 2 + 16 * c16) =
+        *reinterpret_cast<const uint4*>(&scodes[r * (C / 8) + 4 * c16]);
+  }
+}
+
+// Device workspace of the chunked kernel (the inverse permutation and the
+// exchange slots), one per GPU, grown on demand and kept for the process.
+struct CompWork {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+};
+constexpr int kMaxDevices = 64;
+CompWork g_comp_work[kMaxDevices];
+std::mutex g_comp_mu;
+
+int comp_workspace(size_t bytes, void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return OQ_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_comp_mu);
+  CompWork& w = g_comp_work[dev];
+  if (w.bytes < bytes) {
+    // hipFree waits for the device, so no launch still uses the old buffer.
+    if (w.ptr && hipFree(w.ptr) != hipSuccess) return OQ_ERR_HIP;
+    w.ptr = nullptr;
+    w.bytes = 0;
+    const size_t grow = bytes + bytes / 2;
+    if (hipMalloc(&w.ptr, grow) != hipSuccess) {
+      w.ptr = nullptr;
+      return OQ_ERR_HIP;
+    }
+    w.bytes = grow;
+  }
+  *out = w.ptr;
+  return OQ_OK;
+}
+
+template <int RG, int C, bool GATHER, int WAVES = 8, int PF = 2>
+int launch_composite_x(const void* X, int64_t M, int64_t K, int64_t ldx, const int32_t* perm, const void* Rt,
+                       float s, uint8_t* Xq, float* x_scale, hipStream_t stream) {
+  constexpr int R = 16 * RG;
+  const int64_t ntiles = (M + R - 1) / R;
+  const int nq = static_cast<int>(K / C);
+  if (ntiles > (int64_t{1} << 26)) return OQ_ERR_SHAPE;
+  const size_t pinv_bytes = (static_cast<size_t>(K) * 2 + 255) / 256 * 256;
+  const int64_t nslots = nq > 1 ? ntiles * nq * R : 0;
+  void* ws = nullptr;
+  int st = comp_workspace(pinv_bytes + static_cast<size_t>(nslots) * 4 + 256, &ws);
+  if (st != OQ_OK) return st;
+  uint16_t* pinv = static_cast<uint16_t*>(ws);
+  float* slots = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + pinv_bytes);
+  const int64_t nprep = std::max<int64_t>(GATHER ? K : 0, nslots);
+  if (nprep > 0) {
+    hipLaunchKernelGGL(comp_prep_kernel, dim3(static_cast<unsigned>((nprep + 255) / 256)), dim3(256), 0, stream,
+                       GATHER ? perm : nullptr, static_cast<int>(K), pinv, slots, nslots);
+    if ((st = launch_status()) != OQ_OK) return st;
+  }
+  const int64_t grid = (ntiles + 7) / 8 * 8 * nq;
+  hipLaunchKernelGGL((rq_composite_x_kernel<RG, C, GATHER, WAVES, PF>), dim3(static_cast<unsigned>(grid)),
+                     dim3(64 * WAVES), 0, stream, static_cast<const uint16_t*>(X), M, static_cast<int>(K), ldx,
+                     pinv, static_cast<const uint16_t*>(Rt), s, Xq, x_scale, slots, nq,
+                     static_cast<int>(ntiles));
+  return launch_status();
+}
+
+// Chunk width above K = 4096: the widest of 4096 / 2048 / 1024 / 512 that
+// divides K, at most `cap` (0: none; the two-pass kernel is used).  With the
+// online permutation every chunk's workgroup reads whole rows, so the widest
+// chunk (fewest re-reads) is best; with P folded into the input a workgroup
+// reads only its chunk's columns and 2048-channel chunks (two workgroups per
+// CU) are faster (measured at K = 8192 and 16384).
+int comp_chunk(int64_t K, int cap) {
+  for (int c : {4096, 2048, 1024, 512})
+    if (c <= cap && K % c == 0) return c;
+  return 0;
+}
+
+template <bool GATHER>
+int launch_composite_chunked(int C, const void* X, int64_t M, int64_t K, int64_t ldx, const int32_t* perm,
+                             const void* Rt, float s, uint8_t* Xq, float* x_scale, hipStream_t h) {
+  switch (C) {
+    case 4096: return launch_composite_x<1, 4096, GATHER>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+    case 2048: return launch_composite_x<1, 2048, GATHER>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+    case 1024: return launch_composite_x<1, 1024, GATHER>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+    case 512: return launch_composite_x<1, 512, GATHER>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+    default: return OQ_ERR_SHAPE;
+  }
+}
+
 template <int RG, int KMAX, bool GATHER = true>
 int launch_composite1(const void* X, int64_t M, int64_t K, int64_t ldx, const int32_t* perm, const void* Rt,
                       float s, uint8_t* Xq, float* x_scale, hipStream_t stream) {
@@ -472,7 +832,13 @@ extern "C" int oq_rotate_quantize_act_composite(const void* X, int64_t M, int64_
     if (M <= 1024 && K <= 2048) return oq::launch_composite1<1, 2048, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
     if (K <= 1024) return oq::launch_composite1<2, 1024, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
     if (K <= 2048) return oq::launch_composite1<2, 2048, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+    // K = 4096 with many rows: two 2048-channel chunks (two workgroups per
+    // CU) beat one workgroup per 16 whole rows.
+    if (K == 4096 && M > 1024)
+      return oq::launch_composite_chunked<false>(2048, X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
     if (K <= 4096) return oq::launch_composite1<1, 4096, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+    if (const int c = oq::comp_chunk(K, 2048))
+      return oq::launch_composite_chunked<false>(c, X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
     if (K <= 8192) return oq::launch_composite<16, 8192, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
     return oq::launch_composite<16, 16384, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
   }
@@ -483,6 +849,8 @@ extern "C" int oq_rotate_quantize_act_composite(const void* X, int64_t M, int64_
   if (K <= 1024) return oq::launch_composite1<4, 1024>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
   if (K <= 2048) return oq::launch_composite1<2, 2048>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
   if (K <= 4096) return oq::launch_composite1<1, 4096>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+  if (const int c = oq::comp_chunk(K, 4096))
+    return oq::launch_composite_chunked<true>(c, X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
   if (K <= 8192) return oq::launch_composite<4, 8192>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
   return oq::launch_composite<2, 16384>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
 }

@@ -58,8 +58,12 @@ def _tau(x16, perm, r16):
     return np.where(amax > 0, 14 * gamma * S.max(axis=1) / safe + 21 * U32, 0.0)
 
 
+# Above K = 4096 the rows are split into chunks of C channels (C = 4096, 2048,
+# 1024 or 512, the widest dividing K) whose workgroups exchange row maxima:
+# several tiles of 16 rows, a partial last tile, and every chunk width.
 CASES = [(50, 1024, 1.0), (64, 1024, 2.3), (33, 2048, 0.7), (17, 4096, 1.0), (9, 6144, 3.1), (5, 8192, 1.0),
-         (3, 16384, 1.4), (1000, 1024, 1.0), (130, 1536, 0.9), (257, 4096, 1.0), (1, 64, 1.0)]
+         (3, 16384, 1.4), (1000, 1024, 1.0), (130, 1536, 0.9), (257, 4096, 1.0), (1, 64, 1.0),
+         (100, 8192, 1.0), (257, 16384, 0.8), (33, 6144, 1.2), (40, 4608, 1.0), (17, 5120, 2.0)]
 
 
 @pytest.mark.parametrize("M,K,s", CASES)
@@ -97,9 +101,10 @@ def test_composite_prepermuted_codes(M, K, s):
     print(f"  boundary code differences {n_mis} of {M * K}")
 
 
-def test_composite_prepermuted_strided_rows_and_zero_row():
-    M, K = 40, 2048
-    x16, _, perm, r16 = _operands(78, M, 64, K)
+@pytest.mark.parametrize("K", [2048, 8192])
+def test_composite_prepermuted_strided_rows_and_zero_row(K):
+    M = 40
+    x16, _, perm, r16 = _operands(78 + K, M, 64, K)
     x16[7] = 0
     buf = torch.zeros((M, K + 64), dtype=torch.float16, device=DEV)
     buf[:, :K] = torch.from_numpy(np.ascontiguousarray(x16[:, perm])).to(DEV)
@@ -111,9 +116,10 @@ def test_composite_prepermuted_strided_rows_and_zero_row():
     assert xs.cpu().numpy()[7] == 0 and not Xq.cpu().numpy()[7].any()
 
 
-def test_composite_strided_rows_and_zero_row():
-    M, K = 40, 2048
-    x16, _, perm, r16 = _operands(77, M, 64, K)
+@pytest.mark.parametrize("K", [2048, 8192])
+def test_composite_strided_rows_and_zero_row(K):
+    M = 40
+    x16, _, perm, r16 = _operands(77 + K, M, 64, K)
     x16[7] = 0
     buf = torch.zeros((M, K + 64), dtype=torch.float16, device=DEV)
     buf[:, :K] = torch.from_numpy(x16).to(DEV)
@@ -169,3 +175,23 @@ def test_composite_linear_end_to_end():
     # quantization quality on synthetic data is information, not parity (the
     # paper's quality numbers need its weights and activations)
     assert np.isfinite(err_c) and np.isfinite(err_h) and err_c < 1.0 and err_h < 1.0
+
+
+def test_chunked_calls_in_a_row():
+    """Consecutive calls above K = 4096 with growing, shrinking and growing M:
+    the exchange slots and the inverse permutation are re-initialised by every
+    call (a stale slot would release a tile early, or a stale permutation
+    would misplace channels)."""
+    K = 8192
+    x16, _, perm, r16 = _operands(4242, 3000, 64, K)
+    p, rt = _device(perm, r16)
+    X = torch.from_numpy(x16).to(DEV)
+    q_o, xs_o, r_o = composite.rotate_quantize_composite(x16, perm, r16.astype(np.float64))
+    tau = _tau(x16, perm, r16)
+    for M in (1000, 40, 3000):
+        print(f"composite chunked call M={M} K={K}", flush=True)
+        Xq, xs = oq.rotate_quantize_act_composite(X[:M], p, rt)
+        torch.cuda.synchronize()
+        parity.check_codes(parity.unpack_int4(Xq.cpu().numpy()), q_o[:M], r_o[:M], tau[:M])
+        rel = np.abs(xs.cpu().numpy().astype(np.float64) - xs_o[:M]) / np.where(xs_o[:M] > 0, xs_o[:M], 1.0)
+        assert np.all(rel <= tau[:M] / 7 + 4 * U32)

@@ -161,3 +161,21 @@ def test_composite_and_weight_preparation():
     Rt = oq.block_rotations(U)
     _twice(lambda v: oq.rotate_quantize_act_composite(X, perm, Rt, Xq=v[0], x_scale=v[1]),
            [("dense", (M, K // 2), torch.uint8), ("dense", (M,), torch.float32)])
+
+
+@pytest.mark.parametrize("K", [8192, 16384])
+def test_composite_chunked(K):
+    """The chunked composite kernel (row maxima exchanged between the chunks'
+    workgroups), with the online permutation and with it folded."""
+    M = 16384
+    print(f"determinism composite chunked K={K}", flush=True)
+    W = _w(1024, K, 11)
+    X = _x(M, K, 12)
+    e = oq.channel_energy(W)
+    perm = oq.zigzag_permutation(e, 64)
+    U, _ = oq.block_svd(W, perm, 64)
+    Rt = oq.block_rotations(U)
+    _twice(lambda v: oq.rotate_quantize_act_composite(X, perm, Rt, Xq=v[0], x_scale=v[1]),
+           [("dense", (M, K // 2), torch.uint8), ("dense", (M,), torch.float32)])
+    _twice(lambda v: oq.rotate_quantize_act_composite(X, None, Rt, Xq=v[0], x_scale=v[1]),
+           [("dense", (M, K // 2), torch.uint8), ("dense", (M,), torch.float32)])

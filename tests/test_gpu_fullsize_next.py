@@ -2,9 +2,9 @@
 the GPU weight preparation, in the configurations bench.py times, checked
 on sampled outputs that the oracle computes one by one (GPU).
 
-  * composite rotate-quantize at M = 16384, K = 1024 and 4096 (and with the
-    permutation folded into the input, K = 1024, 4096, 16384): sampled rows'
-    codes by the boundary rule against the oracle fed the same fp16 R_b;
+  * composite rotate-quantize at M = 16384, K = 1024, 4096, 8192 and 16384,
+    with the online permutation and with it folded into the input: sampled
+    rows' codes by the boundary rule against the oracle fed the same fp16 R_b;
   * static rotate-quantize at M = 16384, K = 4096: sampled rows by the
     static boundary rule;
   * W4A8 at M = K = N = 16384 (the 128 x 128 tiling with 8-bit token codes)
@@ -33,7 +33,8 @@ def _rows(M, n, seed):
     return np.unique(np.concatenate([rng.choice(M, n, replace=False), [0, M - 1]]))
 
 
-@pytest.mark.parametrize("K,folded", [(1024, False), (4096, False), (1024, True), (4096, True), (16384, True)])
+@pytest.mark.parametrize("K,folded", [(1024, False), (4096, False), (8192, False), (16384, False), (1024, True),
+                                      (4096, True), (8192, True), (16384, True)])
 def test_composite_full_size_sampled(K, folded):
     """folded: perm = None on the input already in the permuted order (the
     GPU is handed X P, the oracle X and P)."""
