@@ -40,6 +40,10 @@ typedef float c4f __attribute__((ext_vector_type(4)));
 
 constexpr int kCB = 64;  // block size c
 
+// Address-space-qualified pointers for the direct global -> LDS load builtin.
+typedef __attribute__((address_space(1))) void gmem_void;
+typedef __attribute__((address_space(3))) void lds_void;
+
 // Two nibbles per byte from 16 two's-complement int8 codes (even channel low).
 __device__ __forceinline__ uint32_t pack4codes(uint32_t d) {
   const uint32_t e = d & 0x000F000Fu;          // codes 0, 2 -> bits 0-3, 16-19
@@ -434,10 +438,11 @@ __global__ __launch_bounds__(512) void rq_composite1_kernel(const uint16_t* __re
 }
 
 // ---------------------------------------------------------------------------
-// Rows wider than a workgroup can stage (K > 4096): the permuted channels of
-// a row are cut into nq = K / C chunks of C channels, and each (tile of R =
-// 16 RG rows, chunk) pair is one workgroup, so that each block matrix R_b is
-// read once per R rows instead of once per few rows.  The nq workgroups of a
+// Rows wider than a workgroup can stage (K > 4096, and K = 4096 with P
+// folded): the permuted channels of a row are cut into nq = K / C chunks of C
+// channels, and each (tile of R = 16 RG rows, chunk) pair is one workgroup, so
+// that each block matrix R_b is read once per R rows instead of once per few
+// rows.  The nq workgroups of a
 // tile exchange their rows' partial maxima through per-launch slots in global
 // memory (initialised to -1 by comp_prep_kernel; a published maximum is >= 0)
 // and each quantizes its own chunk, so every y value is computed once and
@@ -573,23 +578,19 @@ __global__ __launch_bounds__(64 * WAVES) void rq_composite_x_kernel(
     // A permutation gives every position of the chunk exactly one channel, so
     // every LDS element of the R rows is written (rows past M with zeros).
   } else {
-    constexpr int PPR = C / 8;  // 16-byte pieces per row of the chunk
-    for (int p0 = tid; p0 < R * PPR; p0 += NT * 8) {
-      uint4 v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int p = p0 + NT * u;
-        const int r = p / PPR, c8 = p % PPR;
-        const bool ok = p < R * PPR && row0 + r < M;
-        v[u] = *reinterpret_cast<const uint4*>(X + (ok ? row0 + r : 0) * ldx + cbase + (ok ? 8 * c8 : 0));
-        if (!ok) v[u] = make_uint4(0, 0, 0, 0);
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int p = p0 + NT * u;
-        if (p < R * PPR) *reinterpret_cast<uint4*>(&sx[(p / PPR) * XS + 8 * (p % PPR)]) = v[u];
-      }
+    // The chunk's columns of each row go straight from global memory into
+    // LDS (global_load_lds_dwordx4: lane l's 16 bytes land at the given LDS
+    // address + 16 l), 1 KB (512 channels) per wave instruction, with no
+    // registers in between, so every row of the tile is in flight at once.
+    // Rows past M read row M - 1 (their results are not stored).
+    constexpr int PARTS = C / 512;
+    for (int j = wave; j < R * PARTS; j += WAVES) {
+      const int r = j / PARTS, h = j % PARTS;
+      const int64_t gr = row0 + r < M ? row0 + r : M - 1;
+      const uint16_t* src = X + gr * ldx + cbase + 512 * h + 8 * lane;
+      __builtin_amdgcn_global_load_lds((gmem_void*)src, (lds_void*)(sx + r * XS + 512 * h), 16, 0, 0);
     }
+    __builtin_amdgcn_s_waitcnt(0);
   }
   __syncthreads();
 
@@ -761,26 +762,35 @@ int launch_composite_x(const void* X, int64_t M, int64_t K, int64_t ldx, const i
   return launch_status();
 }
 
-// Chunk width above K = 4096: the widest of 4096 / 2048 / 1024 / 512 that
-// divides K, at most `cap` (0: none; the two-pass kernel is used).  With the
-// online permutation every chunk's workgroup reads whole rows, so the widest
-// chunk (fewest re-reads) is best; with P folded into the input a workgroup
-// reads only its chunk's columns and 2048-channel chunks (two workgroups per
-// CU) are faster (measured at K = 8192 and 16384).
+// Chunk width: the widest of 4096 / 2048 / 1024 / 512 that divides K, at
+// most `cap` (0: none; the two-pass kernel is used).  With the online
+// permutation every chunk's workgroup reads whole rows, so 16-row tiles of the
+// widest chunk (fewest re-reads) are best.  With P folded into the input a
+// workgroup reads only its chunk's columns and the block matrices dominate
+// the traffic from L2 (128 K / R bytes per row for R-row tiles), so 32-row
+// tiles of at most 1024 channels (64 KB of LDS, two workgroups per CU) are
+// best (measured at K = 4096 - 16384).
 int comp_chunk(int64_t K, int cap) {
   for (int c : {4096, 2048, 1024, 512})
     if (c <= cap && K % c == 0) return c;
   return 0;
 }
 
-template <bool GATHER>
-int launch_composite_chunked(int C, const void* X, int64_t M, int64_t K, int64_t ldx, const int32_t* perm,
-                             const void* Rt, float s, uint8_t* Xq, float* x_scale, hipStream_t h) {
+int launch_composite_chunked(bool gather, int C, const void* X, int64_t M, int64_t K, int64_t ldx,
+                             const int32_t* perm, const void* Rt, float s, uint8_t* Xq, float* x_scale,
+                             hipStream_t h) {
+  if (gather) {
+    switch (C) {
+      case 4096: return launch_composite_x<1, 4096, true>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+      case 2048: return launch_composite_x<1, 2048, true>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+      case 1024: return launch_composite_x<1, 1024, true>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+      case 512: return launch_composite_x<1, 512, true>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+      default: return OQ_ERR_SHAPE;
+    }
+  }
   switch (C) {
-    case 4096: return launch_composite_x<1, 4096, GATHER>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
-    case 2048: return launch_composite_x<1, 2048, GATHER>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
-    case 1024: return launch_composite_x<1, 1024, GATHER>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
-    case 512: return launch_composite_x<1, 512, GATHER>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+    case 1024: return launch_composite_x<2, 1024, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+    case 512: return launch_composite_x<2, 512, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
     default: return OQ_ERR_SHAPE;
   }
 }
@@ -832,13 +842,13 @@ extern "C" int oq_rotate_quantize_act_composite(const void* X, int64_t M, int64_
     if (M <= 1024 && K <= 2048) return oq::launch_composite1<1, 2048, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
     if (K <= 1024) return oq::launch_composite1<2, 1024, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
     if (K <= 2048) return oq::launch_composite1<2, 2048, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
-    // K = 4096 with many rows: two 2048-channel chunks (two workgroups per
-    // CU) beat one workgroup per 16 whole rows.
+    // K = 4096 with many rows: 1024-channel chunks of 32-row tiles beat one
+    // workgroup per 16 whole rows (78 vs 120 us at M = 16384).
     if (K == 4096 && M > 1024)
-      return oq::launch_composite_chunked<false>(2048, X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+      return oq::launch_composite_chunked(false, 1024, X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
     if (K <= 4096) return oq::launch_composite1<1, 4096, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
-    if (const int c = oq::comp_chunk(K, 2048))
-      return oq::launch_composite_chunked<false>(c, X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+    if (const int c = oq::comp_chunk(K, 1024))
+      return oq::launch_composite_chunked(false, c, X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
     if (K <= 8192) return oq::launch_composite<16, 8192, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
     return oq::launch_composite<16, 16384, false>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
   }
@@ -850,7 +860,7 @@ extern "C" int oq_rotate_quantize_act_composite(const void* X, int64_t M, int64_
   if (K <= 2048) return oq::launch_composite1<2, 2048>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
   if (K <= 4096) return oq::launch_composite1<1, 4096>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
   if (const int c = oq::comp_chunk(K, 4096))
-    return oq::launch_composite_chunked<true>(c, X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
+    return oq::launch_composite_chunked(true, c, X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
   if (K <= 8192) return oq::launch_composite<4, 8192>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
   return oq::launch_composite<2, 16384>(X, M, K, ldx, perm, Rt, s, Xq, x_scale, h);
 }

@@ -58,12 +58,15 @@ def _tau(x16, perm, r16):
     return np.where(amax > 0, 14 * gamma * S.max(axis=1) / safe + 21 * U32, 0.0)
 
 
-# Above K = 4096 the rows are split into chunks of C channels (C = 4096, 2048,
-# 1024 or 512, the widest dividing K) whose workgroups exchange row maxima:
-# several tiles of 16 rows, a partial last tile, and every chunk width.
+# Above K = 4096 (and at K = 4096 with P folded and M > 1024) the rows are
+# split into chunks of channels whose workgroups exchange row maxima: 16-row
+# tiles of up to 4096 channels with the online permutation, 32-row tiles of up
+# to 1024 channels with it folded; several tiles, a partial last tile, and
+# every chunk width.
 CASES = [(50, 1024, 1.0), (64, 1024, 2.3), (33, 2048, 0.7), (17, 4096, 1.0), (9, 6144, 3.1), (5, 8192, 1.0),
          (3, 16384, 1.4), (1000, 1024, 1.0), (130, 1536, 0.9), (257, 4096, 1.0), (1, 64, 1.0),
-         (100, 8192, 1.0), (257, 16384, 0.8), (33, 6144, 1.2), (40, 4608, 1.0), (17, 5120, 2.0)]
+         (100, 8192, 1.0), (257, 16384, 0.8), (33, 6144, 1.2), (40, 4608, 1.0), (17, 5120, 2.0),
+         (1500, 4096, 1.0)]
 
 
 @pytest.mark.parametrize("M,K,s", CASES)
