@@ -227,9 +227,12 @@ def prefill_kernels():
             e.record(stream)
             e.synchronize()
             ts.append(s.elapsed_time(e))
+        pct[0] = [round(float(np.percentile(ts, p)) * 1e3, 1) for p in (10, 90)]
         return float(np.median(ts))
+    pct = [None]
     oq.w4a4_linear(Xq, xs, Wq, ws, Y=Y)
     t_r = cold(lambda: oq.rotate_quantize_act(X, K, Xq=Xq, x_scale=xs), 15)
+    p_r = pct[0]
     ts = []
     for _ in range(15):  # the same launch after a write flush, for comparison
         flush.fill_(1)
@@ -242,10 +245,11 @@ def prefill_kernels():
         ts.append(s.elapsed_time(e))
     t_rw = float(np.median(ts))
     t_g = cold(lambda: oq.w4a4_linear(Xq, xs, Wq, ws, Y=Y), 15)
-    out = {"gemm_M16384_K16384_N16384": {"us": round(t_g * 1e3, 1),
+    p_g = pct[0]
+    out = {"gemm_M16384_K16384_N16384": {"us": round(t_g * 1e3, 1), "us_p10_p90": p_g,
                                          "TOPs": round(2 * M * N * K / (t_g * 1e-3) / 1e12, 1),
                                          "frac_int8_peak": round(2 * M * N * K / (t_g * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4)},
-           "rotate_quant_M16384_K16384": {"us": round(t_r * 1e3, 1),
+           "rotate_quant_M16384_K16384": {"us": round(t_r * 1e3, 1), "us_p10_p90": p_r,
                                           "GBs": round(rq_bytes(M, K) / (t_r * 1e-3) / 1e9, 1),
                                           "frac_hbm_peak": round(rq_bytes(M, K) / (t_r * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                                           "after_write_flush_us": round(t_rw * 1e3, 1)}}
@@ -859,19 +863,20 @@ def sweep_records(Ms=None, Ks=None, reps=10, sink=None):
                 e.record(stream)
                 e.synchronize()
                 ts.append(s.elapsed_time(e))
-            return float(np.median(ts))
+            return float(np.median(ts)), [round(float(np.percentile(ts, p)) * 1e3, 2) for p in (10, 90)]
 
         rq = lambda: oq.rotate_quantize_act(X, K, Xq=Xq, x_scale=xs, stream=stream)
         gm = lambda: oq.w4a4_linear(Xq, xs, Wq, ws, Y=Y, stream=stream)
         rq()
         gm()
-        t_rq = timed(rq)
-        t_g = timed(gm)
+        t_rq, rq_p = timed(rq)
+        t_g, g_p = timed(gm)
         rb = rq_bytes(M, K)
-        rec = {"M": M, "K": K, "N": N, "seed": case.seed, "rq_us": round(t_rq * 1e3, 2),
+        rec = {"M": M, "K": K, "N": N, "seed": case.seed, "rq_us": round(t_rq * 1e3, 2), "rq_us_p10_p90": rq_p,
                "rq_GBs": round(rb / (t_rq * 1e-3) / 1e9, 1),
                "rq_frac_hbm": round(rb / (t_rq * 1e-3) / 1e9 / HBM_PEAK_GBS, 4), "rq_MB": round(rb / 1e6, 2)}
         rec.update(gemm_roofline(M, N, K, t_g))
+        rec["gemm_us_p10_p90"] = g_p
         out.append(rec)
         if sink is not None:
             sink(rec)
@@ -983,6 +988,19 @@ def run_dit(args):
     ms = start.elapsed_time(end) / args.steps
     assert torch.isfinite(x).all().item(), "non-finite action state"
     print(f"[bench] {args.steps} steps, {ms:.3f} ms/step", file=sys.stderr, flush=True)
+    # Per-step latency distribution (after the timed region; not part of value):
+    # 50 single steps, each between its own events.
+    per = []
+    for k in range(50):
+        s_ev = torch.cuda.Event(enable_timing=True)
+        e_ev = torch.cuda.Event(enable_timing=True)
+        s_ev.record(stream)
+        model.step(x, k % cfg.steps, stream=stream)
+        e_ev.record(stream)
+        e_ev.synchronize()
+        per.append(s_ev.elapsed_time(e_ev) * 1e3)
+    step_dist = {"steps": 50, "median_us": round(float(np.median(per)), 2),
+                 "p10_us": round(float(np.percentile(per, 10)), 2), "p90_us": round(float(np.percentile(per, 90)), 2)}
 
     nograph_ms = pi_step_without_graph(cfg, inp)
     # Bytes a step must stream: every block's int4 weights and scales, and the
@@ -1012,6 +1030,7 @@ def run_dit(args):
                                "Hadamard 1024/4096, s_t log-uniform [0.5,4]",
                    "global_batch": 1, "seq_len": cfg.tokens, "timing": "warm (weights + prefix K/V fit the MALL)"},
         "dit_step_latency_us": round(ms * 1e3, 2),
+        "dit_step_single_launch_us": step_dist,
         "dit_step_without_graph_us": round(nograph_ms * 1e3, 2),
         "dit_step_stream": {"bytes": int(step_bytes), "GBs": round(step_bytes / (ms * 1e-3) / 1e9, 1),
                             "hbm_floor_us": round(step_bytes / HBM_PEAK_GBS / 1e3, 1)},

@@ -381,6 +381,7 @@ struct AttnArgs {
   uint16_t* out; int64_t out_ld;
   int S, H, hd, D, nsplit;
   float scale;
+  int direct;  // one split: write the normalized fp16 output to `out` instead of partials
 };
 
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
@@ -576,8 +577,13 @@ __global__ __launch_bounds__(64 * WAVES) void attn_partial_kernel(AttnArgs a) {
   }
   __syncthreads();
 
-  // O = P V, 16 x hd per wave.
+  // O = P V, 16 x hd per wave.  With a single split (a.direct) the row is
+  // complete: o / l, rounded to fp16, goes straight to the head's columns of
+  // `out` (the same fp32 operations as the merge of one split).
   float* po = a.part_o + (static_cast<int64_t>(bh) * a.nsplit + split) * a.S * hd;
+  float inv[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) inv[e] = 1.0f / l[e];
   for (int nb = 0; nb < hd / 16; ++nb) {
     v4f o = v4f{0, 0, 0, 0};
 #pragma unroll
@@ -589,9 +595,14 @@ __global__ __launch_bounds__(64 * WAVES) void attn_partial_kernel(AttnArgs a) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int row = 16 * w + 4 * (lane >> 4) + e;
-      if (row < a.S) po[static_cast<int64_t>(row) * hd + nb * 16 + (lane & 15)] = o[e];
+      if (row >= a.S) continue;
+      if (a.direct)
+        a.out[(static_cast<int64_t>(b) * a.S + row) * a.out_ld + h * hd + nb * 16 + (lane & 15)] = f2h(o[e] * inv[e]);
+      else
+        po[static_cast<int64_t>(row) * hd + nb * 16 + (lane & 15)] = o[e];
     }
   }
+  if (a.direct) return;
   float* ml = a.part_ml + (static_cast<int64_t>(bh) * a.nsplit + split) * a.S * 2;
   if ((lane & 15) == 0) {
 #pragma unroll
@@ -1240,7 +1251,8 @@ int gemm(oq_dit* h, const oq_qweight& wt, int64_t K, int64_t N, Epilogue epi, vo
 }
 
 // Attention (partials over 64-key splits, then the merge fused with the o
-// linear's rotate-quantize).  Keys: `P` rows of k_pre / v_pre (row stride
+// linear's rotate-quantize; with a single split the normalized rows and the
+// stand-alone rotate-quantize).  Keys: `P` rows of k_pre / v_pre (row stride
 // pre_ld) followed by `own` rows of the q|k|v buffer.
 int attention_rq(oq_dit* h, const uint16_t* q, int64_t q_ld, const uint16_t* k_pre, const uint16_t* v_pre,
                  int P, int64_t pre_ld, const uint16_t* k_own, const uint16_t* v_own, int64_t own_ld, int own,
@@ -1258,6 +1270,11 @@ int attention_rq(oq_dit* h, const uint16_t* q, int64_t q_ld, const uint16_t* k_p
   a.S = c.tokens; a.H = c.n_heads; a.hd = c.head_dim; a.D = static_cast<int>(D);
   a.nsplit = (P + own + kAttnKS - 1) / kAttnKS;
   a.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(c.head_dim)));
+  // One split (the GR00T self-attention over its 16 action tokens): the
+  // attention writes its normalized fp16 rows and the stand-alone
+  // rotate-quantize takes them (no partials, no merge).
+  a.direct = a.nsplit == 1 ? 1 : 0;
+  if (a.direct) a.out = at<uint16_t>(h, h->lay.o);
   const unsigned waves = static_cast<unsigned>((c.tokens + 15) / 16);
   const dim3 grid(c.batch * c.n_heads, a.nsplit);
   auto launch = [&](auto W) {
@@ -1277,6 +1294,9 @@ int attention_rq(oq_dit* h, const uint16_t* q, int64_t q_ld, const uint16_t* k_p
   }
   int e = launch_status();
   if (e != OQ_OK) return e;
+  if (a.direct)
+    return rq_launch(a.out, M, D, D, pow2_divisor(static_cast<int>(D)), sdelta ? 1.0f : s, at<uint8_t>(h, h->lay.xq),
+                     at<float>(h, h->lay.xs), nullptr, st, h->tiled, sdelta);
   RQPlan p;
   const RQOut ro = rq_out(h, D, s, &p, sdelta);
   if (D == 1024 && ro.logb == 10 && M <= 256 && c.head_dim % 4 == 0) {

@@ -61,7 +61,8 @@ __global__ __launch_bounds__(256) void rq_kernel(const uint16_t* __restrict__ X,
   rqd::rq_core<C>(v, m, K, logb, s_t, s_over_sqrtb, lds, red, Xq, xs, ratio, tiled, sdelta, rotate_only, i8, cmul);
 }
 
-// One row per wave (W = 1) or per workgroup (W > 1).
+// One row per wave (W = 1), per workgroup (W = 2, 4: four waves), or per
+// three-wave workgroup (W = 3).
 template <int NG, int W, bool FULL>
 __global__ __launch_bounds__(256) void rq_mfma_kernel(const uint16_t* __restrict__ X, int64_t M, int64_t ldx, int logb,
                                                       float s_t, float s_over_sqrtb, uint8_t* __restrict__ Xq,
@@ -109,11 +110,11 @@ bool rq_mfma_shape(int64_t K, int* ng, int* w) {
   switch (K) {
     case 512: *ng = 1; *w = 1; return true;
     case 1024: *ng = 2; *w = 1; return true;
-    case 1536: *ng = 3; *w = 1; return true;
+    case 1536: *ng = 1; *w = 3; return true;  // three waves per row, one 512-channel block each
     case 2048: *ng = 4; *w = 1; return true;
     case 3072: *ng = 6; *w = 1; return true;
     case 4096: *ng = 8; *w = 1; return true;
-    case 6144: *ng = 12; *w = 1; return true;  // the 6144-channel MLP input (blocks of <= 2048)
+    case 6144: *ng = 4; *w = 3; return true;  // the 6144-channel MLP input: three waves of one 2048-block each
     case 8192: *ng = 4; *w = 4; return true;  // 68 VGPRs (7 waves per SIMD) against 136 for (8, 2)
     case 16384: *ng = 8; *w = 4; return true;
     default: return false;
@@ -127,29 +128,30 @@ int rq_mfma_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_blo
   rq_mfma_shape(K, &ng, &w);
   const int logb = ilog2(had_block);
   const float s_over_sqrtb = static_cast<float>(static_cast<double>(s_t) / std::sqrt(static_cast<double>(had_block)));
-  const int rpb = 4 / w;
-  const size_t lds = w > 1 ? static_cast<size_t>(4) * ng * 64 * sizeof(float4)
-                           : (sdelta != nullptr ? static_cast<size_t>(K) * sizeof(float) : 0);
+  const int rpb = w == 3 ? 1 : 4 / w;
+  const unsigned threads = w == 3 ? 192 : 256;
+  const size_t lds = (w == 2 || w == 4) ? static_cast<size_t>(4) * ng * 64 * sizeof(float4)
+                                        : (w == 1 && sdelta != nullptr ? static_cast<size_t>(K) * sizeof(float) : 0);
   // One row per wave (W = 1) or per workgroup (W > 1).
   const unsigned grid = static_cast<unsigned>((M + rpb - 1) / rpb);
   const uint16_t* x = static_cast<const uint16_t*>(X);
 #define OQ_RQM(NG, W)                                                                                         \
   if (ng == NG && w == W) {                                                                                   \
     if (had_block == K)                                                                                       \
-      hipLaunchKernelGGL((rq_mfma_kernel<NG, W, true>), dim3(grid), dim3(256), lds, stream, x, M, ldx, logb,  \
+      hipLaunchKernelGGL((rq_mfma_kernel<NG, W, true>), dim3(grid), dim3(threads), lds, stream, x, M, ldx, logb, \
                          s_t, s_over_sqrtb, Xq, x_scale, ratio, tiled, sdelta, rotate_only, i8, cmul);        \
     else                                                                                                      \
-      hipLaunchKernelGGL((rq_mfma_kernel<NG, W, false>), dim3(grid), dim3(256), lds, stream, x, M, ldx, logb, \
+      hipLaunchKernelGGL((rq_mfma_kernel<NG, W, false>), dim3(grid), dim3(threads), lds, stream, x, M, ldx, logb, \
                          s_t, s_over_sqrtb, Xq, x_scale, ratio, tiled, sdelta, rotate_only, i8, cmul);        \
     return launch_status();                                                                                   \
   }
   OQ_RQM(1, 1)
   OQ_RQM(2, 1)
-  OQ_RQM(3, 1)
+  OQ_RQM(1, 3)
   OQ_RQM(4, 1)
   OQ_RQM(6, 1)
   OQ_RQM(8, 1)
-  OQ_RQM(12, 1)
+  OQ_RQM(4, 3)
   OQ_RQM(4, 4)
   OQ_RQM(8, 4)
 #undef OQ_RQM
@@ -191,7 +193,8 @@ int rq_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_block, f
               bool rotate_only, bool i8, const float* cmul) {
   if (M == 0) return OQ_OK;
   int ng = 0, w = 0;
-  if (had_block >= 32 && rq_mfma_shape(K, &ng, &w))
+  // (With three waves per row a Hadamard block must not span waves: b <= 512 NG.)
+  if (had_block >= 32 && rq_mfma_shape(K, &ng, &w) && (w != 3 || had_block <= 512 * ng))
     return rq_mfma_launch(X, M, K, ldx, had_block, s_t, Xq, x_scale, ratio, stream, tiled, sdelta, rotate_only,
                           i8, cmul);
   RQPlan p;

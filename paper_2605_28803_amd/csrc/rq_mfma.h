@@ -50,11 +50,14 @@ __device__ __forceinline__ void hadamard_frags(int lane, rv8h& a1, rv8h& a2) {
 template <int NG, int W>
 struct Shape {
   static constexpr int K = NG * W * 512;
-  static constexpr int RPB = 4 / W;  // rows per 256-thread workgroup
+  static constexpr int RPB = W == 3 ? 1 : 4 / W;  // rows per workgroup (256 threads; 192 when W = 3)
   static constexpr int LOGNG = NG >= 16 ? 4 : NG >= 8 ? 3 : NG >= 4 ? 2 : NG >= 2 ? 1 : 0;
   static constexpr int LOGW = W >= 4 ? 2 : W >= 2 ? 1 : 0;
   static constexpr int GW = NG / W;  // groups per wave after the transpose
-  static_assert(W == 1 || (NG % W == 0 && (NG & (NG - 1)) == 0), "NG must be a power of two >= W when W > 1");
+  // W = 3: three waves per row, each holding whole Hadamard blocks (b <= 512 NG, checked by the launcher),
+  // so no butterfly crosses a wave and only the row maximum is shared.
+  static_assert(W == 1 || W == 3 || (NG % W == 0 && (NG & (NG - 1)) == 0),
+                "NG must be a power of two >= W when W is 2 or 4");
   static_assert(NG <= 16, "at most 16 register groups");
 };
 
@@ -127,8 +130,8 @@ __device__ __forceinline__ void rq_row(const rv8h (&cur)[NG], const rv8h& a1, co
   // G = wr * NG + s without the wave transpose, and with it (s = gi * W + u)
   // G = u * NG + wr * GW + gi.
   const int wbit0 = 9 + LOGNG;
-  const bool xpose = W > 1 && need(wbit0);
-  if constexpr (W > 1) {
+  const bool xpose = W > 1 && W != 3 && need(wbit0);
+  if constexpr (W == 2 || W == 4) {
     if (xpose) {
       // Two rounds, one per half of the lanes: the transpose only moves a
       // value between waves at the same lane, so each round needs half the
