@@ -43,7 +43,8 @@ using rqd::f16r;
 using rqd::h2f;
 using rqd::f2h;
 
-constexpr int kAttnKS = 64;     // keys per attention split
+constexpr int kAttnKS = 64;     // keys per step of the cross-attention's running merge
+constexpr int kAttnSplit = 64;  // keys per split of the split attention (partials, then a merge)
 constexpr int kMaxTokens = 64;  // action tokens per sample handled by the attention kernels
 constexpr int kMaxHeadDim = 128;
 constexpr int kMaxSplits = 16;  // (prefix + tokens) <= 16 * 64 keys
@@ -1031,7 +1032,7 @@ Layout layout_for(const oq_dit_config& c) {
   // Keys per sample: pi attends to [prefix ; own], gr00t to the conditioning
   // tokens (even blocks) or to its own tokens (odd blocks).
   const int keys = is_gr00t(c) ? std::max(c.prefix, c.tokens) : c.prefix + c.tokens;
-  const int nsplit = (keys + kAttnKS - 1) / kAttnKS;
+  const int nsplit = (keys + kAttnSplit - 1) / kAttnSplit;
   const int64_t BH = static_cast<int64_t>(c.batch) * c.n_heads;
   const int64_t MC = is_gr00t(c) ? static_cast<int64_t>(c.batch) * c.prefix : 0;  // conditioning rows
   Layout L;
@@ -1082,7 +1083,7 @@ int validate_config(const oq_dit_config* c) {
     return OQ_ERR_SHAPE;
   if (c->tokens > kMaxTokens || c->action_dim < 1 || c->action_dim > 256) return OQ_ERR_SHAPE;
   const int keys = c->arch == OQ_DIT_GR00T ? std::max(c->prefix, c->tokens) : c->prefix + c->tokens;
-  if (keys > kMaxSplits * kAttnKS) return OQ_ERR_SHAPE;
+  if (keys > kMaxSplits * kAttnSplit) return OQ_ERR_SHAPE;
   if (c->arch == OQ_DIT_GR00T && c->prefix < 1) return OQ_ERR_SHAPE;
   RQPlan p;
   if (!fused_plan(c->hidden, &p) || !fused_plan(c->mlp, &p)) return OQ_ERR_SHAPE;
@@ -1268,7 +1269,7 @@ int attention_rq(oq_dit* h, const uint16_t* q, int64_t q_ld, const uint16_t* k_p
   a.part_ml = at<float>(h, h->lay.part_ml);
   a.out = keep ? at<uint16_t>(h, h->lay.o) : nullptr; a.out_ld = D;
   a.S = c.tokens; a.H = c.n_heads; a.hd = c.head_dim; a.D = static_cast<int>(D);
-  a.nsplit = (P + own + kAttnKS - 1) / kAttnKS;
+  a.nsplit = (P + own + kAttnSplit - 1) / kAttnSplit;
   a.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(c.head_dim)));
   // One split (the GR00T self-attention over its 16 action tokens): the
   // attention writes its normalized fp16 rows and the stand-alone
@@ -1280,10 +1281,10 @@ int attention_rq(oq_dit* h, const uint16_t* q, int64_t q_ld, const uint16_t* k_p
   auto launch = [&](auto W) {
     constexpr int WV = decltype(W)::value;
     switch (c.head_dim) {
-      case 48: hipLaunchKernelGGL((attn_partial_kernel<WV, 48, kAttnKS>), grid, dim3(64 * WV), 0, st, a); break;
-      case 64: hipLaunchKernelGGL((attn_partial_kernel<WV, 64, kAttnKS>), grid, dim3(64 * WV), 0, st, a); break;
-      case 128: hipLaunchKernelGGL((attn_partial_kernel<WV, 128, kAttnKS>), grid, dim3(64 * WV), 0, st, a); break;
-      default: hipLaunchKernelGGL((attn_partial_kernel<WV, 0, kAttnKS>), grid, dim3(64 * WV), 0, st, a); break;
+      case 48: hipLaunchKernelGGL((attn_partial_kernel<WV, 48, kAttnSplit>), grid, dim3(64 * WV), 0, st, a); break;
+      case 64: hipLaunchKernelGGL((attn_partial_kernel<WV, 64, kAttnSplit>), grid, dim3(64 * WV), 0, st, a); break;
+      case 128: hipLaunchKernelGGL((attn_partial_kernel<WV, 128, kAttnSplit>), grid, dim3(64 * WV), 0, st, a); break;
+      default: hipLaunchKernelGGL((attn_partial_kernel<WV, 0, kAttnSplit>), grid, dim3(64 * WV), 0, st, a); break;
     }
   };
   switch (waves) {

@@ -126,6 +126,9 @@ int rq_mfma_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_blo
                    bool rotate_only, bool i8, const float* cmul) {
   int ng = 0, w = 0;
   rq_mfma_shape(K, &ng, &w);
+  // Few rows (the action tokens): two waves per 4096-channel row halve the
+  // serial work of a wave; the grid is far below one wave per SIMD anyway.
+  if (K == 4096 && M <= 512) { ng = 4; w = 2; }
   const int logb = ilog2(had_block);
   const float s_over_sqrtb = static_cast<float>(static_cast<double>(s_t) / std::sqrt(static_cast<double>(had_block)));
   const int rpb = w == 3 ? 1 : 4 / w;
@@ -151,6 +154,7 @@ int rq_mfma_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_blo
   OQ_RQM(4, 1)
   OQ_RQM(6, 1)
   OQ_RQM(8, 1)
+  OQ_RQM(4, 2)
   OQ_RQM(4, 3)
   OQ_RQM(4, 4)
   OQ_RQM(8, 4)

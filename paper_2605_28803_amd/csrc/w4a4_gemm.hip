@@ -681,9 +681,21 @@ int launch_small_mb(const GemmArgs& a, hipStream_t stream) {
   return launch_status();
 }
 
+// Row blocks of 16 (one per workgroup) spread a small-M product over four
+// times the workgroups of 64-row blocks; that pays while the grid stays
+// within 16 waves per CU (the 50-row DiT linears: q|k|v, o and down, 1.5 to
+// 5 thousand waves; not the 8192-column gate|up, whose 32-column workgroups of
+// 8 waves would make 8 thousand).
+int small_row_blocks_of_16(const GemmArgs& a) {
+  const bool wide = a.N > 4096, shallow = a.K <= 1024;
+  const int64_t bn = wide ? 32 : 16, waves = wide ? 8 : (shallow ? 4 : 16);
+  const int64_t total = (a.N + bn - 1) / bn * ((a.M + 15) / 16) * waves;
+  return a.M <= 16 || total <= 4096;
+}
+
 template <int EPI, bool TILED>
 int launch_small(const GemmArgs& a, hipStream_t stream) {
-  return a.M <= 16 ? launch_small_mb<EPI, TILED, 1>(a, stream) : launch_small_mb<EPI, TILED, 4>(a, stream);
+  return small_row_blocks_of_16(a) ? launch_small_mb<EPI, TILED, 1>(a, stream) : launch_small_mb<EPI, TILED, 4>(a, stream);
 }
 
 template <int EPI>

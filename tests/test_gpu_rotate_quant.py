@@ -33,6 +33,9 @@ CASES = [
     (6000, 4096, 4096, 1.0), (6001, 4096, 1024, 1.3), (1100, 8192, 8192, 1.0), (1030, 16384, 16384, 0.9),
     # three waves per row, one Hadamard block (or several) each: K = 1536 / 6144
     (1024, 1536, 512, 1.0), (1025, 6144, 2048, 1.7), (130, 6144, 64, 1.0), (3, 1536, 32, 2.0),
+    # K = 4096 with at most 512 rows: two waves per row (odd M, the last
+    # two-wave row count, one wave stage or none)
+    (511, 4096, 4096, 1.1), (512, 4096, 2048, 0.9), (513, 4096, 4096, 1.0), (33, 4096, 128, 1.0),
 ]
 
 
