@@ -391,17 +391,26 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 // One (sample b, head h, split of KS keys, KS a multiple of 64) on the fp16
 // matrix cores (v_mfma_f32_16x16x32_f16), ceil(S / 16) waves.  Wave w owns
 // query rows 16w .. 16w+15 (head_dim a multiple of 16; the q.k contraction is
-// padded with zeros to a multiple of 32):
-//   S = Q K^T (16 x KS, fp32), scaled; split maximum m and sum l per row;
-//   P = exp(S - m) (fp16, staged in LDS as the next A operand);
-//   O = P V (16 x hd, fp32) with V^T staged in LDS.
+// padded with zeros to a multiple of 32).  Both products are taken transposed,
+// so that the probabilities never leave the registers:
+//   S^T = K Q^T (KS x 16, fp32), scaled: lane l holds query l % 16 against
+//     keys 16 nb + 4 (l / 16) + e (block nb, element e);
+//   split maximum m and sum l of each query: 16 values in the lane, then the
+//     four lanes l % 16 + 16 g;
+//   P^T = exp(S^T - m) in fp16 is directly the B operand of
+//   O^T = V^T P^T (hd x 16, fp32), V^T staged in LDS: the contraction index
+//     k = 8 g + j of a 32-key step s stands for key 32 s + 4 g + j (j < 4) or
+//     32 s + 16 + 4 g + j - 4 (j >= 4), the same keys in both operands (a
+//     sum over keys does not depend on their order);
+//   lane l then holds dims 16 nb + 4 (l / 16) .. + 3 of query l % 16: one
+//     16-byte partial store (or one 8-byte fp16 store) per dim block.
 // O, m and l go to the workspace; combine_rq_kernel merges the splits.
 // MFMA operand layout used (the same k order for both operands): lane l holds
-// row / column l % 16 and the 8 consecutive k values 8 * (l / 16) .. + 7 of a
-// 32-wide k step; the 16 x 16 fp32 result has row 4 * (l / 16) + e, column
-// l % 16 in element e.  WAVES = ceil(S / 16) waves; HD = head_dim when it is
-// one of the compiled sizes (the loops then unroll completely), 0 otherwise
-// (a.hd at run time).
+// row / column l % 16 and the 8 k values 8 * (l / 16) .. + 7 of a 32-wide k
+// step; the 16 x 16 fp32 result has row 4 * (l / 16) + e, column l % 16 in
+// element e.  WAVES = ceil(S / 16) waves; HD = head_dim when it is one of the
+// compiled sizes (the loops then unroll completely), 0 otherwise (a.hd at run
+// time).
 //
 // The split's K and V blocks are read from global memory once per workgroup
 // (every wave needs all of K): K in 16-byte pieces along its rows (a wave
@@ -418,9 +427,8 @@ __global__ __launch_bounds__(64 * WAVES) void attn_partial_kernel(AttnArgs a) {
   constexpr int C8 = HDL / 8;            // 8-dim pieces per row
   // LDS sized for this instance (one wave and 48 dims need 16 KB, so many
   // workgroups share a CU).
-  __shared__ __attribute__((aligned(16))) uint16_t sVt[HDL][PAD];      // V^T [dim][key]
-  __shared__ __attribute__((aligned(16))) uint16_t sP[WAVES][16][PAD];  // per-wave P [row][key]
-  __shared__ __attribute__((aligned(16))) uint16_t sK[KS][KPAD];        // K [key][dim]
+  __shared__ __attribute__((aligned(16))) uint16_t sVt[HDL][PAD];  // V^T [dim][key]
+  __shared__ __attribute__((aligned(16))) uint16_t sK[KS][KPAD];    // K [key][dim]
 
   const int bh = blockIdx.x, split = blockIdx.y;
   const int b = bh / a.H, h = bh % a.H;
@@ -533,6 +541,8 @@ __global__ __launch_bounds__(64 * WAVES) void attn_partial_kernel(AttnArgs a) {
   for (int kk = 0; kk < KKMAX; ++kk) qa[kk] = (dok[kk] && qok) ? qraw[kk] : v8h{};
   __syncthreads();
 
+  // S^T = K Q^T: block nb of 16 keys against this wave's 16 queries.
+  const int g = lane >> 4;
   v4f sc[KS / 16];
 #pragma unroll
   for (int nb = 0; nb < KS / 16; ++nb) {
@@ -540,80 +550,73 @@ __global__ __launch_bounds__(64 * WAVES) void attn_partial_kernel(AttnArgs a) {
 #pragma unroll
     for (int kk = 0; kk < KKMAX; ++kk)
       if (kk < nkk) {
-        const v8h kb = *reinterpret_cast<const v8h*>(&sK[nb * 16 + (lane & 15)][dok[kk] ? kk * 32 + kq : 0]);
-        sc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(qa[kk], kb, sc[nb], 0, 0, 0);
+        const v8h ka = *reinterpret_cast<const v8h*>(&sK[nb * 16 + (lane & 15)][dok[kk] ? kk * 32 + kq : 0]);
+        sc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ka, qa[kk], sc[nb], 0, 0, 0);
       }
   }
 
-  // Softmax statistics per row (row 4*(lane/16) + e, keys across the 16 lanes
-  // of the group and the KS/16 blocks).
-  float mx[4], l[4];
+  // Softmax statistics of query lane % 16: the lane's 16 keys, then the four
+  // lanes of the same query (lane bits 4 and 5).
+  float m_ = -INFINITY;
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    float m_ = -INFINITY;
+  for (int nb = 0; nb < KS / 16; ++nb)
 #pragma unroll
-    for (int nb = 0; nb < KS / 16; ++nb) {
-      const int j = nb * 16 + (lane & 15);
+    for (int e = 0; e < 4; ++e) {
+      const int j = nb * 16 + 4 * g + e;
       const float v = j < nk ? sc[nb][e] * a.scale : -INFINITY;
       sc[nb][e] = v;
       m_ = fmaxf(m_, v);
     }
-    m_ = fmaxf(m_, rqd::lane_xor<1>(m_));
-    m_ = fmaxf(m_, rqd::lane_xor<2>(m_));
-    m_ = fmaxf(m_, rqd::lane_xor<4>(m_));
-    m_ = fmaxf(m_, rqd::lane_xor<8>(m_));
-    float s_ = 0.0f;
+  m_ = fmaxf(m_, rqd::lane_xor<16>(m_));
+  m_ = fmaxf(m_, __shfl_xor(m_, 32, 64));
+  float l_ = 0.0f;
+  v8h pb[KS / 32];  // P^T fragments, one per 32-key step
 #pragma unroll
-    for (int nb = 0; nb < KS / 16; ++nb) {
-      const float p = __expf(sc[nb][e] - m_);
-      s_ += p;
-      sP[w][4 * (lane >> 4) + e][nb * 16 + (lane & 15)] = f2h(p);
+  for (int st = 0; st < KS / 32; ++st)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float p = __expf(sc[2 * st + (j >> 2)][j & 3] - m_);
+      l_ += p;
+      pb[st][j] = static_cast<_Float16>(p);
     }
-    s_ += rqd::lane_xor<1>(s_);
-    s_ += rqd::lane_xor<2>(s_);
-    s_ += rqd::lane_xor<4>(s_);
-    s_ += rqd::lane_xor<8>(s_);
-    mx[e] = m_;
-    l[e] = s_;
-  }
-  __syncthreads();
+  l_ += rqd::lane_xor<16>(l_);
+  l_ += __shfl_xor(l_, 32, 64);
 
-  // O = P V, 16 x hd per wave.  With a single split (a.direct) the row is
-  // complete: o / l, rounded to fp16, goes straight to the head's columns of
-  // `out` (the same fp32 operations as the merge of one split).
-  float* po = a.part_o + (static_cast<int64_t>(bh) * a.nsplit + split) * a.S * hd;
-  float inv[4];
+  // O^T = V^T P^T, 16 dims x 16 queries per block.  With a single split
+  // (a.direct) the row is complete: o / l, rounded to fp16, goes straight to
+  // the head's columns of `out` (the same fp32 operations as the merge of one
+  // split).
+  const int q = 16 * w + (lane & 15);
+  const bool qst = q < a.S;
+  const int64_t po_off = ((static_cast<int64_t>(bh) * a.nsplit + split) * a.S + (qst ? q : 0)) * hd + 4 * g;
+  const int64_t out_off = (static_cast<int64_t>(b) * a.S + (qst ? q : 0)) * a.out_ld + h * hd + 4 * g;
+  const float inv = 1.0f / l_;
+  constexpr int NBD = HDL / 16;
 #pragma unroll
-  for (int e = 0; e < 4; ++e) inv[e] = 1.0f / l[e];
-  for (int nb = 0; nb < hd / 16; ++nb) {
-    v4f o = v4f{0, 0, 0, 0};
+  for (int nb = 0; nb < NBD; ++nb) {
+    if (nb * 16 < hd) {
+      v4f o = v4f{0, 0, 0, 0};
 #pragma unroll
-    for (int ks = 0; ks < KS / 32; ++ks) {
-      const v8h pa = *reinterpret_cast<const v8h*>(&sP[w][lane & 15][ks * 32 + kq]);
-      const v8h vb = *reinterpret_cast<const v8h*>(&sVt[nb * 16 + (lane & 15)][ks * 32 + kq]);
-      o = __builtin_amdgcn_mfma_f32_16x16x32_f16(pa, vb, o, 0, 0, 0);
-    }
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int row = 16 * w + 4 * (lane >> 4) + e;
-      if (row >= a.S) continue;
-      if (a.direct)
-        a.out[(static_cast<int64_t>(b) * a.S + row) * a.out_ld + h * hd + nb * 16 + (lane & 15)] = f2h(o[e] * inv[e]);
-      else
-        po[static_cast<int64_t>(row) * hd + nb * 16 + (lane & 15)] = o[e];
+      for (int st = 0; st < KS / 32; ++st) {
+        const uint16_t* vr = &sVt[nb * 16 + (lane & 15)][st * 32 + 4 * g];
+        const uint2 lo = *reinterpret_cast<const uint2*>(vr), hi = *reinterpret_cast<const uint2*>(vr + 16);
+        const v8h va = __builtin_bit_cast(v8h, make_uint4(lo.x, lo.y, hi.x, hi.y));
+        o = __builtin_amdgcn_mfma_f32_16x16x32_f16(va, pb[st], o, 0, 0, 0);
+      }
+      if (qst) {
+        if (a.direct)
+          *reinterpret_cast<uint2*>(a.out + out_off + nb * 16) =
+              make_uint2(static_cast<uint32_t>(f2h(o[0] * inv)) | (static_cast<uint32_t>(f2h(o[1] * inv)) << 16),
+                         static_cast<uint32_t>(f2h(o[2] * inv)) | (static_cast<uint32_t>(f2h(o[3] * inv)) << 16));
+        else
+          *reinterpret_cast<float4*>(a.part_o + po_off + nb * 16) = make_float4(o[0], o[1], o[2], o[3]);
+      }
     }
   }
   if (a.direct) return;
-  float* ml = a.part_ml + (static_cast<int64_t>(bh) * a.nsplit + split) * a.S * 2;
-  if ((lane & 15) == 0) {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int row = 16 * w + 4 * (lane >> 4) + e;
-      if (row < a.S) {
-        ml[2 * row] = mx[e];
-        ml[2 * row + 1] = l[e];
-      }
-    }
+  if (g == 0 && qst) {
+    float* ml = a.part_ml + ((static_cast<int64_t>(bh) * a.nsplit + split) * a.S + q) * 2;
+    *reinterpret_cast<float2*>(ml) = make_float2(m_, l_);
   }
 }
 
