@@ -640,10 +640,12 @@ __global__ __launch_bounds__(256) void kv_head_major_kernel(const uint16_t* __re
 
 // Cross-attention of one (sample b, head h) over all P conditioning keys,
 // read head-major (K then V blocks of P x hd).  The keys are taken 64 at a
-// time with the same matrix-core steps as attn_partial_kernel, and the
-// splits are merged on the fly (running maximum m, sum l and output O per
-// query row, rescaled by e^{m_old - m_new}); the normalized output is written
-// as fp16 to its head's columns of `out`.  WAVES = ceil(S / 16).
+// time with the transposed matrix-core steps of attn_partial_kernel (S^T =
+// K Q^T, then O^T = V^T P^T with P^T in registers; K fragments are loaded
+// straight from global memory in the A operand layout), and the splits are
+// merged on the fly (running maximum m, sum l and output O per query, a
+// lane's own: rescaled by e^{m_old - m_new}); the normalized output is
+// written as fp16 to its head's columns of `out`.  WAVES = ceil(S / 16).
 template <int WAVES, int HD>
 __global__ __launch_bounds__(64 * WAVES) void attn_cross_kernel(const uint16_t* __restrict__ q, int64_t q_ld,
                                                                 const uint16_t* __restrict__ kvh, int P, int S,
@@ -655,16 +657,16 @@ __global__ __launch_bounds__(64 * WAVES) void attn_cross_kernel(const uint16_t* 
   constexpr int KK = (HD + 31) / 32;               // 32-wide k steps of q.k (zero-padded)
   constexpr int VIT = (HD + 8 * WAVES - 1) / (8 * WAVES);
   __shared__ __attribute__((aligned(16))) uint16_t sVt[HD][PAD];
-  __shared__ __attribute__((aligned(16))) uint16_t sP[WAVES][16][PAD];
   const int bh = blockIdx.x;
   const int b = bh / H, h = bh % H;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   __builtin_assume(tid < 64 * WAVES);
   const uint16_t* kb_base = kvh + static_cast<int64_t>(bh) * 2 * P * HD;
   const uint16_t* vb_base = kb_base + static_cast<int64_t>(P) * HD;
+  const int g = lane >> 4;
   const int qrow = 16 * w + (lane & 15);
   const bool qok = qrow < S;
-  const int kq = 8 * (lane >> 4);
+  const int kq = 8 * g;
   const uint16_t* qp = q + (static_cast<int64_t>(b) * S + (qok ? qrow : 0)) * q_ld + h * HD;
   v8h qa[KK];
 #pragma unroll
@@ -673,13 +675,9 @@ __global__ __launch_bounds__(64 * WAVES) void attn_cross_kernel(const uint16_t* 
     const v8h raw = *reinterpret_cast<const v8h*>(qp + (dok ? kk * 32 + kq : 0));
     qa[kk] = (dok && qok) ? raw : v8h{};
   }
-  float m[4], l[4];
+  // Running statistics of query lane % 16 and O^T: o[nb][e] = dim 16 nb + 4 g + e.
+  float m = -INFINITY, l = 0.0f;
   v4f o[HD / 16];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    m[e] = -INFINITY;
-    l[e] = 0.0f;
-  }
 #pragma unroll
   for (int nb = 0; nb < HD / 16; ++nb) o[nb] = v4f{0, 0, 0, 0};
 
@@ -699,6 +697,7 @@ __global__ __launch_bounds__(64 * WAVES) void attn_cross_kernel(const uint16_t* 
         vraw[i] = *reinterpret_cast<const uint4*>(vp + (d8 < HD ? d8 : 0));
       }
     }
+    // K fragments (A operand): key 16 nb + lane % 16, dims 32 kk + 8 g .. + 7.
     v8h kraw[KK][KS / 16];
     bool kok[KS / 16];
 #pragma unroll
@@ -712,7 +711,7 @@ __global__ __launch_bounds__(64 * WAVES) void attn_cross_kernel(const uint16_t* 
         kraw[kk][nb] = *reinterpret_cast<const v8h*>(kp + (dok ? kk * 32 + kq : 0));
       }
     }
-    __syncthreads();  // the previous split's P and V^T reads are done
+    __syncthreads();  // the previous split's V^T reads are done
 #pragma unroll
     for (int i = 0; i < VIT; ++i) {
       const int d8 = w * 8 + i * 8 * WAVES;
@@ -726,6 +725,7 @@ __global__ __launch_bounds__(64 * WAVES) void attn_cross_kernel(const uint16_t* 
         }
       }
     }
+    // S^T = K Q^T: sc[nb][e] = key 16 nb + 4 g + e against query lane % 16.
     v4f sc[KS / 16];
 #pragma unroll
     for (int nb = 0; nb < KS / 16; ++nb) {
@@ -733,63 +733,60 @@ __global__ __launch_bounds__(64 * WAVES) void attn_cross_kernel(const uint16_t* 
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
         const bool dok = kk * 32 + kq < HD;
-        const v8h kb = (dok && kok[nb]) ? kraw[kk][nb] : v8h{};
-        sc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(qa[kk], kb, sc[nb], 0, 0, 0);
+        const v8h ka = (dok && kok[nb]) ? kraw[kk][nb] : v8h{};
+        sc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ka, qa[kk], sc[nb], 0, 0, 0);
       }
     }
-    // Running softmax per row 4 (lane / 16) + e.
+    // Running softmax of the lane's query: its 16 keys, then lane bits 4, 5.
+    float mx = -INFINITY;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      float mx = -INFINITY;
+    for (int nb = 0; nb < KS / 16; ++nb)
 #pragma unroll
-      for (int nb = 0; nb < KS / 16; ++nb) {
-        const int j = nb * 16 + (lane & 15);
+      for (int e = 0; e < 4; ++e) {
+        const int j = nb * 16 + 4 * g + e;
         const float v = j < nk ? sc[nb][e] * scale : -INFINITY;
         sc[nb][e] = v;
         mx = fmaxf(mx, v);
       }
-      mx = fmaxf(mx, rqd::lane_xor<1>(mx));
-      mx = fmaxf(mx, rqd::lane_xor<2>(mx));
-      mx = fmaxf(mx, rqd::lane_xor<4>(mx));
-      mx = fmaxf(mx, rqd::lane_xor<8>(mx));
-      const float mn = fmaxf(m[e], mx);
-      const float alpha = __expf(m[e] - mn);  // 0 on the first split (m = -inf)
-      float sum = 0.0f;
+    mx = fmaxf(mx, rqd::lane_xor<16>(mx));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float mn = fmaxf(m, mx);
+    const float alpha = __expf(m - mn);  // 0 on the first split (m = -inf)
+    float sum = 0.0f;
+    v8h pb[KS / 32];
 #pragma unroll
-      for (int nb = 0; nb < KS / 16; ++nb) {
-        const float pv = __expf(sc[nb][e] - mn);
+    for (int st = 0; st < KS / 32; ++st)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float pv = __expf(sc[2 * st + (j >> 2)][j & 3] - mn);
         sum += pv;
-        sP[w][4 * (lane >> 4) + e][nb * 16 + (lane & 15)] = f2h(pv);
+        pb[st][j] = static_cast<_Float16>(pv);
       }
-      sum += rqd::lane_xor<1>(sum);
-      sum += rqd::lane_xor<2>(sum);
-      sum += rqd::lane_xor<4>(sum);
-      sum += rqd::lane_xor<8>(sum);
-      l[e] = l[e] * alpha + sum;
-      m[e] = mn;
-#pragma unroll
-      for (int nb = 0; nb < HD / 16; ++nb) o[nb][e] *= alpha;
-    }
-    __syncthreads();
+    sum += rqd::lane_xor<16>(sum);
+    sum += __shfl_xor(sum, 32, 64);
+    l = l * alpha + sum;
+    m = mn;
+    __syncthreads();  // V^T staged
 #pragma unroll
     for (int nb = 0; nb < HD / 16; ++nb) {
+      o[nb] *= alpha;
 #pragma unroll
-      for (int ks = 0; ks < KS / 32; ++ks) {
-        const v8h pa = *reinterpret_cast<const v8h*>(&sP[w][lane & 15][ks * 32 + kq]);
-        const v8h vb = *reinterpret_cast<const v8h*>(&sVt[nb * 16 + (lane & 15)][ks * 32 + kq]);
-        o[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(pa, vb, o[nb], 0, 0, 0);
+      for (int st = 0; st < KS / 32; ++st) {
+        const uint16_t* vr = &sVt[nb * 16 + (lane & 15)][st * 32 + 4 * g];
+        const uint2 lo = *reinterpret_cast<const uint2*>(vr), hi = *reinterpret_cast<const uint2*>(vr + 16);
+        const v8h va = __builtin_bit_cast(v8h, make_uint4(lo.x, lo.y, hi.x, hi.y));
+        o[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(va, pb[st], o[nb], 0, 0, 0);
       }
     }
   }
+  if (!qok) return;
+  const float inv = 1.0f / l;
+  uint16_t* orow = out + (static_cast<int64_t>(b) * S + qrow) * out_ld + h * HD + 4 * g;
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const int row = 16 * w + 4 * (lane >> 4) + e;
-    if (row >= S) continue;
-    const float inv = 1.0f / l[e];
-    uint16_t* orow = out + (static_cast<int64_t>(b) * S + row) * out_ld + h * HD;
-#pragma unroll
-    for (int nb = 0; nb < HD / 16; ++nb) orow[nb * 16 + (lane & 15)] = f2h(o[nb][e] * inv);
-  }
+  for (int nb = 0; nb < HD / 16; ++nb)
+    *reinterpret_cast<uint2*>(orow + nb * 16) =
+        make_uint2(static_cast<uint32_t>(f2h(o[nb][0] * inv)) | (static_cast<uint32_t>(f2h(o[nb][1] * inv)) << 16),
+                   static_cast<uint32_t>(f2h(o[nb][2] * inv)) | (static_cast<uint32_t>(f2h(o[nb][3] * inv)) << 16));
 }
 
 // Token row (b, s): out = sum_s e^{m_s - M} o_s / sum_s e^{m_s - M} l_s per
