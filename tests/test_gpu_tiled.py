@@ -85,6 +85,9 @@ GEMM_CASES = [
     (50, 3072, 1024), (50, 1024, 1024), (50, 8192, 1024), (50, 1024, 4096),
     (1, 2560, 2048), (16, 2048, 16384), (17, 200, 2048), (64, 4096, 128), (65, 320, 1536),
     (130, 1000, 1024), (33, 48, 6144), (8, 32768, 2048),
+    # M > 64 in 64-row blocks (wide or deep enough that 16-row blocks would
+    # exceed 4096 waves), ragged last block
+    (200, 8192, 1024), (100, 2048, 4096),
 ]
 
 
