@@ -378,7 +378,9 @@ struct AttnArgs {
   const uint16_t* k_pre; const uint16_t* v_pre; int P;  // [B][P][pre_ld] (P may be 0)
   int64_t pre_ld;
   const uint16_t* k_own; const uint16_t* v_own; int64_t own_ld; int own_keys;  // [B*S][..]
-  float* part_o; float* part_ml;                        // [B*H][nsplit][S][hd], [B*H][nsplit][S][2]
+  // Split partials: the split's normalized output o / l in fp16 (a convex
+  // combination of value rows, so it cannot overflow) and (m, l) in fp32.
+  uint16_t* part_o; float* part_ml;                     // [B*H][nsplit][S][hd], [B*H][nsplit][S][2]
   uint16_t* out; int64_t out_ld;
   int S, H, hd, D, nsplit;
   float scale;
@@ -403,8 +405,9 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 //     32 s + 16 + 4 g + j - 4 (j >= 4), the same keys in both operands (a
 //     sum over keys does not depend on their order);
 //   lane l then holds dims 16 nb + 4 (l / 16) .. + 3 of query l % 16: one
-//     16-byte partial store (or one 8-byte fp16 store) per dim block.
-// O, m and l go to the workspace; combine_rq_kernel merges the splits.
+//     8-byte store of fp16(O / l) per dim block.
+// The normalized O / l (fp16), m and l go to the workspace; combine_rq_kernel
+// merges the splits with weights e^{m_s - m} l_s.
 // MFMA operand layout used (the same k order for both operands): lane l holds
 // row / column l % 16 and the 8 k values 8 * (l / 16) .. + 7 of a 32-wide k
 // step; the 16 x 16 fp32 result has row 4 * (l / 16) + e, column l % 16 in
@@ -609,7 +612,9 @@ __global__ __launch_bounds__(64 * WAVES) void attn_partial_kernel(AttnArgs a) {
               make_uint2(static_cast<uint32_t>(f2h(o[0] * inv)) | (static_cast<uint32_t>(f2h(o[1] * inv)) << 16),
                          static_cast<uint32_t>(f2h(o[2] * inv)) | (static_cast<uint32_t>(f2h(o[3] * inv)) << 16));
         else
-          *reinterpret_cast<float4*>(a.part_o + po_off + nb * 16) = make_float4(o[0], o[1], o[2], o[3]);
+          *reinterpret_cast<uint2*>(a.part_o + po_off + nb * 16) =
+              make_uint2(static_cast<uint32_t>(f2h(o[0] * inv)) | (static_cast<uint32_t>(f2h(o[1] * inv)) << 16),
+                         static_cast<uint32_t>(f2h(o[2] * inv)) | (static_cast<uint32_t>(f2h(o[3] * inv)) << 16));
       }
     }
   }
@@ -805,9 +810,9 @@ __global__ __launch_bounds__(256) void combine_rq_kernel(AttnArgs a, int64_t M, 
     const int h = k / a.hd, d = k - h * a.hd;
     const int64_t bh = static_cast<int64_t>(b) * a.H + h;
     const float* ml = a.part_ml + bh * a.nsplit * a.S * 2 + 2 * q;
-    const float* po = a.part_o + bh * a.nsplit * a.S * a.hd + static_cast<int64_t>(q) * a.hd + d;
+    const uint16_t* po = a.part_o + bh * a.nsplit * a.S * a.hd + static_cast<int64_t>(q) * a.hd + d;
     // All split statistics first (independent loads), then the weighted values
-    // in groups of 8 splits.
+    // in groups of 8 splits (weight e^{m_s - m} l_s on the normalized o_s).
     float mv[kMaxSplits], lv[kMaxSplits];
 #pragma unroll
     for (int s = 0; s < kMaxSplits; ++s) {
@@ -826,24 +831,22 @@ __global__ __launch_bounds__(256) void combine_rq_kernel(AttnArgs a, int64_t M, 
     float num[8] = {0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
     for (int s0 = 0; s0 < kMaxSplits; s0 += 8) {
-      float4 p0[8], p1[8];
+      uint4 pr[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        p0[u] = p1[u] = make_float4(0, 0, 0, 0);
-        if (s0 + u < a.nsplit) {
-          const float* src = po + static_cast<int64_t>(s0 + u) * a.S * a.hd;
-          p0[u] = *reinterpret_cast<const float4*>(src);
-          p1[u] = *reinterpret_cast<const float4*>(src + 4);
-        }
+        pr[u] = make_uint4(0, 0, 0, 0);
+        if (s0 + u < a.nsplit) pr[u] = *reinterpret_cast<const uint4*>(po + static_cast<int64_t>(s0 + u) * a.S * a.hd);
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const float w = s0 + u < a.nsplit ? __expf(mv[s0 + u] - mx) : 0.0f;
-        den = fmaf(w, lv[s0 + u], den);
-        num[0] = fmaf(w, p0[u].x, num[0]); num[1] = fmaf(w, p0[u].y, num[1]);
-        num[2] = fmaf(w, p0[u].z, num[2]); num[3] = fmaf(w, p0[u].w, num[3]);
-        num[4] = fmaf(w, p1[u].x, num[4]); num[5] = fmaf(w, p1[u].y, num[5]);
-        num[6] = fmaf(w, p1[u].z, num[6]); num[7] = fmaf(w, p1[u].w, num[7]);
+        const float w = s0 + u < a.nsplit ? __expf(mv[s0 + u] - mx) * lv[s0 + u] : 0.0f;
+        den += w;
+        const uint32_t pw[4] = {pr[u].x, pr[u].y, pr[u].z, pr[u].w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          num[2 * j] = fmaf(w, h2f(pw[j] & 0xFFFFu), num[2 * j]);
+          num[2 * j + 1] = fmaf(w, h2f(pw[j] >> 16), num[2 * j + 1]);
+        }
       }
     }
     const float inv = 1.0f / den;
@@ -871,15 +874,15 @@ __global__ __launch_bounds__(256) void combine_rq1024_kernel(AttnArgs a, int64_t
   const int h = k0 / a.hd, d = k0 - h * a.hd;
   const int64_t bh = static_cast<int64_t>(b) * a.H + h;
   const float* ml = a.part_ml + bh * a.nsplit * a.S * 2 + 2 * q;
-  const float* po = a.part_o + bh * a.nsplit * a.S * a.hd + static_cast<int64_t>(q) * a.hd + d;
+  const uint16_t* po = a.part_o + bh * a.nsplit * a.S * a.hd + static_cast<int64_t>(q) * a.hd + d;
   const int slast = a.nsplit - 1;
   float2 st[kMaxSplits];
-  float4 pv[kMaxSplits];
+  uint2 pv[kMaxSplits];
 #pragma unroll
   for (int s = 0; s < kMaxSplits; ++s) {
     const int sc = min(s, slast);
     st[s] = *reinterpret_cast<const float2*>(ml + static_cast<int64_t>(sc) * a.S * 2);
-    pv[s] = *reinterpret_cast<const float4*>(po + static_cast<int64_t>(sc) * a.S * a.hd);
+    pv[s] = *reinterpret_cast<const uint2*>(po + static_cast<int64_t>(sc) * a.S * a.hd);
   }
   float mx = -INFINITY;
 #pragma unroll
@@ -888,12 +891,12 @@ __global__ __launch_bounds__(256) void combine_rq1024_kernel(AttnArgs a, int64_t
   float num[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
   for (int s = 0; s < kMaxSplits; ++s) {
-    const float wgt = s < a.nsplit ? __expf(st[s].x - mx) : 0.0f;
-    den = fmaf(wgt, st[s].y, den);
-    num[0] = fmaf(wgt, pv[s].x, num[0]);
-    num[1] = fmaf(wgt, pv[s].y, num[1]);
-    num[2] = fmaf(wgt, pv[s].z, num[2]);
-    num[3] = fmaf(wgt, pv[s].w, num[3]);
+    const float wgt = s < a.nsplit ? __expf(st[s].x - mx) * st[s].y : 0.0f;  // e^{m_s - m} l_s
+    den += wgt;
+    num[0] = fmaf(wgt, h2f(pv[s].x & 0xFFFFu), num[0]);
+    num[1] = fmaf(wgt, h2f(pv[s].x >> 16), num[1]);
+    num[2] = fmaf(wgt, h2f(pv[s].y & 0xFFFFu), num[2]);
+    num[3] = fmaf(wgt, h2f(pv[s].y >> 16), num[3]);
   }
   const float inv = 1.0f / den;
   float x[4];
@@ -1046,7 +1049,7 @@ Layout layout_for(const oq_dit_config& c) {
   L.act = off; off += align256(M * F * 2);
   L.xq = off; off += align256(std::max(tiled_bytes(M, Kmax), MC * D / 2));
   L.xs = off; off += align256(std::max(M, MC) * 4);
-  L.part_o = off; off += align256(BH * nsplit * c.tokens * c.head_dim * 4);
+  L.part_o = off; off += align256(BH * nsplit * c.tokens * c.head_dim * 2);
   L.part_ml = off; off += align256(BH * nsplit * c.tokens * 2 * 4);
   // The conditioning k|v: one block's linear output in row layout (staging),
   // and every cross-attention block's values head-major.
@@ -1265,7 +1268,7 @@ int attention_rq(oq_dit* h, const uint16_t* q, int64_t q_ld, const uint16_t* k_p
   a.q = q; a.q_ld = q_ld;
   a.k_pre = k_pre; a.v_pre = v_pre; a.P = P; a.pre_ld = pre_ld;
   a.k_own = k_own; a.v_own = v_own; a.own_ld = own_ld; a.own_keys = own;
-  a.part_o = at<float>(h, h->lay.part_o);
+  a.part_o = at<uint16_t>(h, h->lay.part_o);
   a.part_ml = at<float>(h, h->lay.part_ml);
   a.out = keep ? at<uint16_t>(h, h->lay.o) : nullptr; a.out_ld = D;
   a.S = c.tokens; a.H = c.n_heads; a.hd = c.head_dim; a.D = static_cast<int>(D);
