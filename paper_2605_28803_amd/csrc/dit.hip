@@ -78,6 +78,27 @@ struct RQOut {
   const float* sdelta;  // static per-channel steps of this site and step (null: per-token quantizer)
 };
 
+// One output of the action in-projection: sum over a ascending of
+// x[a] W_in[n][a] (fma chain); 16-byte weight loads when the row allows them
+// (the same sum either way).
+__device__ __forceinline__ float inproj_dot(const float* xsh, const uint16_t* __restrict__ wr, int A, bool vec) {
+  float acc = 0.0f;
+  if (vec) {
+    for (int a0 = 0; a0 < A; a0 += 8) {
+      const uint4 q = *reinterpret_cast<const uint4*>(wr + a0);
+      const uint32_t qw[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        acc = fmaf(xsh[a0 + 2 * j], h2f(qw[j] & 0xFFFFu), acc);
+        acc = fmaf(xsh[a0 + 2 * j + 1], h2f(qw[j] >> 16), acc);
+      }
+    }
+  } else {
+    for (int a = 0; a < A; ++a) acc = fmaf(xsh[a], h2f(wr[a]), acc);
+  }
+  return acc;
+}
+
 // r = x W_in^T + b_in
 __global__ __launch_bounds__(256) void inproj_kernel(const float* __restrict__ x, const uint16_t* __restrict__ w_in,
                                                      const uint16_t* __restrict__ b_in, float* __restrict__ r, int A,
@@ -86,12 +107,9 @@ __global__ __launch_bounds__(256) void inproj_kernel(const float* __restrict__ x
   const int m = blockIdx.x;
   for (int a = threadIdx.x; a < A; a += blockDim.x) xsh[a] = x[static_cast<int64_t>(m) * A + a];
   __syncthreads();
-  for (int n = threadIdx.x; n < D; n += blockDim.x) {
-    const uint16_t* wr = w_in + static_cast<int64_t>(n) * A;
-    float acc = 0.0f;
-    for (int a = 0; a < A; ++a) acc = fmaf(xsh[a], h2f(wr[a]), acc);
-    r[static_cast<int64_t>(m) * D + n] = acc + h2f(b_in[n]);
-  }
+  const bool vec = A % 8 == 0 && (reinterpret_cast<uintptr_t>(w_in) & 15) == 0;
+  for (int n = threadIdx.x; n < D; n += blockDim.x)
+    r[static_cast<int64_t>(m) * D + n] = inproj_dot(xsh, w_in + static_cast<int64_t>(n) * A, A, vec) + h2f(b_in[n]);
 }
 
 // h = fp16(norm(r) g (1 + sc) + sh), then rotate + quantize h.  norm is the
@@ -281,25 +299,21 @@ __device__ __forceinline__ void rq1024_row(float (&x)[4], int64_t row, bool vali
   *reinterpret_cast<uint16_t*>(dst) = static_cast<uint16_t>(c[0] | (c[1] << 4) | (c[2] << 8) | (c[3] << 12));
 }
 
+// RMS norm, modulation, fp16 rounding and rotate-quantize of one 1024-channel
+// row whose values v (channels 4 t .. 4 t + 3) thread t already holds; h
+// (optional) receives the fp16 row.
 template <bool SC>
-__global__ __launch_bounds__(256) void norm_rq1024_kernel(const float* __restrict__ r,
-                                                          const uint16_t* __restrict__ g,
-                                                          const uint16_t* __restrict__ sc,
-                                                          const uint16_t* __restrict__ sh, uint16_t* __restrict__ h,
-                                                          int64_t M, RQOut o) {
+__device__ __forceinline__ void norm1024_row(const float (&v)[4], const uint16_t* __restrict__ g,
+                                             const uint16_t* __restrict__ sc, const uint16_t* __restrict__ sh,
+                                             uint16_t* __restrict__ h, int64_t row, bool valid, const RQOut& o,
+                                             float* xch, float (&red)[2][4]) {
   constexpr int D = 1024;
-  __shared__ __attribute__((aligned(16))) float xch[D];
-  __shared__ float red[2][4];
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const int64_t row = blockIdx.x;
-  const bool valid = row < M;
   const int k0 = 4 * t;
-  const float4 rv = *reinterpret_cast<const float4*>(r + (valid ? row : 0) * D + k0);
   const uint2 gq = *reinterpret_cast<const uint2*>(g + k0);
   const uint2 hq = *reinterpret_cast<const uint2*>(sh + k0);
   uint2 cq = make_uint2(0, 0);
   if (SC) cq = *reinterpret_cast<const uint2*>(sc + k0);
-  const float v[4] = {rv.x, rv.y, rv.z, rv.w};
   const float gg[4] = {h2f(gq.x & 0xFFFFu), h2f(gq.x >> 16), h2f(gq.y & 0xFFFFu), h2f(gq.y >> 16)};
   const float s2[4] = {h2f(hq.x & 0xFFFFu), h2f(hq.x >> 16), h2f(hq.y & 0xFFFFu), h2f(hq.y >> 16)};
   const float s1[4] = {SC ? h2f(cq.x & 0xFFFFu) : 0.0f, SC ? h2f(cq.x >> 16) : 0.0f,
@@ -323,6 +337,55 @@ __global__ __launch_bounds__(256) void norm_rq1024_kernel(const float* __restric
         make_uint2(static_cast<uint32_t>(f2h(x[0])) | (static_cast<uint32_t>(f2h(x[1])) << 16),
                    static_cast<uint32_t>(f2h(x[2])) | (static_cast<uint32_t>(f2h(x[3])) << 16));
   rq1024_row(x, row, valid, o, xch, red[1]);
+}
+
+template <bool SC>
+__global__ __launch_bounds__(256) void norm_rq1024_kernel(const float* __restrict__ r,
+                                                          const uint16_t* __restrict__ g,
+                                                          const uint16_t* __restrict__ sc,
+                                                          const uint16_t* __restrict__ sh, uint16_t* __restrict__ h,
+                                                          int64_t M, RQOut o) {
+  constexpr int D = 1024;
+  __shared__ __attribute__((aligned(16))) float xch[D];
+  __shared__ float red[2][4];
+  const int64_t row = blockIdx.x;
+  const bool valid = row < M;
+  const float4 rv = *reinterpret_cast<const float4*>(r + (valid ? row : 0) * D + 4 * threadIdx.x);
+  const float v[4] = {rv.x, rv.y, rv.z, rv.w};
+  norm1024_row<SC>(v, g, sc, sh, h, row, valid, o, xch, red);
+}
+
+// The action in-projection r = x W_in^T + b_in (the same sums as
+// inproj_kernel) fused with the first block's norm producer (as
+// norm_rq1024_kernel): one 1024-channel row per 256-thread workgroup, thread
+// t computing channels 4 t .. 4 t + 3 (A <= 256 action channels).
+template <bool SC>
+__global__ __launch_bounds__(256) void inproj_norm_rq1024_kernel(const float* __restrict__ x,
+                                                                 const uint16_t* __restrict__ w_in,
+                                                                 const uint16_t* __restrict__ b_in,
+                                                                 float* __restrict__ r, int A,
+                                                                 const uint16_t* __restrict__ g,
+                                                                 const uint16_t* __restrict__ sc,
+                                                                 const uint16_t* __restrict__ sh,
+                                                                 uint16_t* __restrict__ h, int64_t M, RQOut o) {
+  constexpr int D = 1024;
+  __shared__ __attribute__((aligned(16))) float xch[D];
+  __shared__ float red[2][4];
+  __shared__ float xsh[256];
+  const int t = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  const bool valid = row < M;
+  if (t < A) xsh[t] = x[(valid ? row : 0) * A + t];
+  __syncthreads();
+  const bool vec = A % 8 == 0 && (reinterpret_cast<uintptr_t>(w_in) & 15) == 0;
+  float v[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int n = 4 * t + j;
+    v[j] = inproj_dot(xsh, w_in + static_cast<int64_t>(n) * A, A, vec) + h2f(b_in[n]);
+  }
+  if (valid) *reinterpret_cast<float4*>(r + row * D + 4 * t) = make_float4(v[0], v[1], v[2], v[3]);
+  norm1024_row<SC>(v, g, sc, sh, h, row, valid, o, xch, red);
 }
 
 // GATED: a = fp16(gelu_tanh(gate) up) from gu = [gate | up] (fp16 [M][2F]);
@@ -915,20 +978,36 @@ __device__ __forceinline__ float wave_sum(float v) {
 }
 
 // x[m][:] += dt * (fp16(norm(r[m]) g_f) W_out^T + b_out), norm = RMS norm or
-// (LN) layer norm.  Four rows per 256-thread workgroup: wave w normalizes row
-// m0 + w into LDS (reductions inside the wave), then thread t computes the
-// partial dot products of output a = t / 8 over the d-slice t % 8 for all
-// four rows (16-byte W_out loads shared by the rows), reduced over the 8
-// slices with lane shuffles (outputs in groups of 32).  D % 64 == 0.
-template <bool LN>
+// (LN) layer norm.  R (1 or 4) rows per 256-thread workgroup: wave w < R
+// normalizes row m0 + w into LDS (reductions inside the wave), then thread t
+// computes the partial dot products of output a = t / 8 over the d-slice
+// t % 8 for the R rows (16-byte W_out loads shared by the rows), reduced over
+// the 8 slices with lane shuffles (outputs in groups of 32).  D % 64 == 0.
+template <bool LN, int R>
 __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ r, const uint16_t* __restrict__ g_f,
                                                     const uint16_t* __restrict__ w_out,
                                                     const uint16_t* __restrict__ b_out, float* __restrict__ x,
                                                     int64_t M, int D, int A, float dt) {
-  extern __shared__ float sh[];  // [4][D] normalized rows
+  extern __shared__ float sh[];  // [R][D] normalized rows
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int64_t m0 = static_cast<int64_t>(blockIdx.x) * 4;
-  {
+  const int64_t m0 = static_cast<int64_t>(blockIdx.x) * R;
+  // Thread t takes output a = t / 8 over the dims 8 (t % 8) + 64 i.  With at
+  // most 32 outputs and D <= 64 NW its W_out slice is loaded into registers
+  // first, so that the loads overlap the norms.
+  constexpr int NW = 24;
+  const int sl = threadIdx.x & 7;
+  const bool pre = A <= 32 && D <= 64 * NW;
+  uint4 wreg[NW];
+  if (pre) {
+    const int a_idx = threadIdx.x >> 3;
+    const uint16_t* wr = w_out + static_cast<int64_t>(a_idx < A ? a_idx : 0) * D;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      const int d = sl * 8 + 64 * i;
+      wreg[i] = d < D ? *reinterpret_cast<const uint4*>(wr + d) : make_uint4(0, 0, 0, 0);
+    }
+  }
+  if (w < R) {
     const int64_t m = m0 + w;
     const bool ok = m < M;
     const float* rr = r + (ok ? m : 0) * D;
@@ -989,26 +1068,19 @@ __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ r,
     }
   }
   __syncthreads();
-  const int sl = threadIdx.x & 7;
-  for (int a0 = 0; a0 < A; a0 += 32) {
-    const int a_idx = a0 + (threadIdx.x >> 3);
-    const bool aok = a_idx < A;
-    const uint16_t* wr = w_out + static_cast<int64_t>(aok ? a_idx : 0) * D;
-    float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll 4
-    for (int d = sl * 8; d < D; d += 64) {
-      float wv[8];
-      load8_f16(wr + d, wv);
+  // The same sums in the same order on both paths (dims ascending per slice).
+  auto accumulate = [&](float (&acc)[R], const float (&wv)[8], int d) {
 #pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const float4 p0 = *reinterpret_cast<const float4*>(sh + rr * D + d);
-        const float4 p1 = *reinterpret_cast<const float4*>(sh + rr * D + d + 4);
-        acc[rr] = fmaf(p0.x, wv[0], fmaf(p0.y, wv[1], fmaf(p0.z, wv[2], fmaf(p0.w, wv[3], acc[rr]))));
-        acc[rr] = fmaf(p1.x, wv[4], fmaf(p1.y, wv[5], fmaf(p1.z, wv[6], fmaf(p1.w, wv[7], acc[rr]))));
-      }
+    for (int rr = 0; rr < R; ++rr) {
+      const float4 p0 = *reinterpret_cast<const float4*>(sh + rr * D + d);
+      const float4 p1 = *reinterpret_cast<const float4*>(sh + rr * D + d + 4);
+      acc[rr] = fmaf(p0.x, wv[0], fmaf(p0.y, wv[1], fmaf(p0.z, wv[2], fmaf(p0.w, wv[3], acc[rr]))));
+      acc[rr] = fmaf(p1.x, wv[4], fmaf(p1.y, wv[5], fmaf(p1.z, wv[6], fmaf(p1.w, wv[7], acc[rr]))));
     }
+  };
+  auto finish = [&](float (&acc)[R], int a_idx, bool aok) {
 #pragma unroll
-    for (int rr = 0; rr < 4; ++rr) {
+    for (int rr = 0; rr < R; ++rr) {
       float v = acc[rr];
       v += __shfl_xor(v, 1, 64);
       v += __shfl_xor(v, 2, 64);
@@ -1016,6 +1088,43 @@ __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ r,
       const int64_t m = m0 + rr;
       if (aok && sl == 0 && m < M) x[m * A + a_idx] += dt * (v + h2f(b_out[a_idx]));
     }
+  };
+  if (pre) {
+    const int a_idx = threadIdx.x >> 3;
+    float acc[R];
+#pragma unroll
+    for (int rr = 0; rr < R; ++rr) acc[rr] = 0.0f;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      const int d = sl * 8 + 64 * i;
+      if (d < D) {
+        const uint32_t q[4] = {wreg[i].x, wreg[i].y, wreg[i].z, wreg[i].w};
+        float wv[8];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          wv[2 * j] = h2f(q[j] & 0xFFFFu);
+          wv[2 * j + 1] = h2f(q[j] >> 16);
+        }
+        accumulate(acc, wv, d);
+      }
+    }
+    finish(acc, a_idx, a_idx < A);
+    return;
+  }
+  for (int a0 = 0; a0 < A; a0 += 32) {
+    const int a_idx = a0 + (threadIdx.x >> 3);
+    const bool aok = a_idx < A;
+    const uint16_t* wr = w_out + static_cast<int64_t>(aok ? a_idx : 0) * D;
+    float acc[R];
+#pragma unroll
+    for (int rr = 0; rr < R; ++rr) acc[rr] = 0.0f;
+#pragma unroll 4
+    for (int d = sl * 8; d < D; d += 64) {
+      float wv[8];
+      load8_f16(wr + d, wv);
+      accumulate(acc, wv, d);
+    }
+    finish(acc, a_idx, aok);
   }
 }
 
@@ -1384,7 +1493,9 @@ SiteSet site_set(oq_dit* h, int l, int t) {
   return ss;
 }
 
-int run_block_pi(oq_dit* h, int l, int t, float* r, hipStream_t st, int until, bool keep) {
+// norm1_done: the first norm producer already ran (fused with the action
+// in-projection of the step).
+int run_block_pi(oq_dit* h, int l, int t, float* r, hipStream_t st, int until, bool keep, bool norm1_done = false) {
   const oq_dit_config& c = h->cfg;
   const oq_dit_block& bw = h->blocks[l];
   const int64_t D = c.hidden, F = c.mlp;
@@ -1398,7 +1509,9 @@ int run_block_pi(oq_dit* h, int l, int t, float* r, hipStream_t st, int until, b
   uint16_t* gu = at<uint16_t>(h, h->lay.gu);
   uint16_t* act = keep ? at<uint16_t>(h, h->lay.act) : nullptr;
   int e;
-  if ((e = norm_rq(h, r, bw.g1, mod_ptr(h, l, t, 0), mod_ptr(h, l, t, 1), h1, s[0], st, ss.d[0])) != OQ_OK) return e;
+  if (!norm1_done &&
+      (e = norm_rq(h, r, bw.g1, mod_ptr(h, l, t, 0), mod_ptr(h, l, t, 1), h1, s[0], st, ss.d[0])) != OQ_OK)
+    return e;
   if (until == 0) return OQ_OK;
   if ((e = gemm(h, *ss.w[0], D, 3 * D, EPI_F16, qkv, 3 * D, nullptr, st)) != OQ_OK) return e;
   if ((e = attention_rq(h, qkv, 3 * D, static_cast<const uint16_t*>(bw.prefix_k),
@@ -1461,17 +1574,45 @@ int run_block(oq_dit* h, int l, int t, float* r, hipStream_t st, int until = 4, 
 
 int final_stage(oq_dit* h, const float* r, float* x, hipStream_t st);
 
+// Pi-0.5 with 1024-channel rows on the 1024-wide producer path (at most 256
+// rows, Hadamard block = the row): the step's in-projection and block 0's
+// first norm producer as one kernel (the same arithmetic as inproj_kernel
+// followed by norm_rq1024_kernel).  *fused = false when it does not apply.
+int inproj_norm1(oq_dit* h, const float* x, float* r, int t, hipStream_t st, bool* fused) {
+  const oq_dit_config& c = h->cfg;
+  const int64_t M = static_cast<int64_t>(c.batch) * c.tokens;
+  *fused = false;
+  if (is_gr00t(c) || c.hidden != 1024 || M > 256) return OQ_OK;
+  const float* s = &h->s_table[static_cast<size_t>(t) * 4];  // block 0
+  const SiteSet ss = site_set(h, 0, t);
+  RQPlan p;
+  const RQOut o = rq_out(h, c.hidden, s[0], &p, ss.d[0]);
+  if (o.logb != 10) return OQ_OK;
+  hipLaunchKernelGGL(inproj_norm_rq1024_kernel<true>, dim3(static_cast<unsigned>(M)), dim3(256), 0, st, x,
+                     static_cast<const uint16_t*>(h->w.w_in), static_cast<const uint16_t*>(h->w.b_in), r,
+                     c.action_dim, static_cast<const uint16_t*>(h->blocks[0].g1), mod_ptr(h, 0, t, 0),
+                     mod_ptr(h, 0, t, 1), nullptr, M, o);
+  *fused = true;
+  return launch_status();
+}
+
 int run_step(oq_dit* h, float* x, int t, hipStream_t st) {
   const oq_dit_config& c = h->cfg;
   const int64_t M = static_cast<int64_t>(c.batch) * c.tokens;
   float* r = at<float>(h, h->lay.r);
-  hipLaunchKernelGGL(inproj_kernel, dim3(static_cast<unsigned>(M)), dim3(256), c.action_dim * sizeof(float), st, x,
-                     static_cast<const uint16_t*>(h->w.w_in), static_cast<const uint16_t*>(h->w.b_in), r,
-                     c.action_dim, c.hidden);
-  int e = launch_status();
+  bool fused = false;
+  int e = inproj_norm1(h, x, r, t, st, &fused);
   if (e != OQ_OK) return e;
-  for (int l = 0; l < c.n_blocks; ++l)
-    if ((e = run_block(h, l, t, r, st, 4, false)) != OQ_OK) return e;
+  if (!fused) {
+    hipLaunchKernelGGL(inproj_kernel, dim3(static_cast<unsigned>(M)), dim3(256), c.action_dim * sizeof(float), st, x,
+                       static_cast<const uint16_t*>(h->w.w_in), static_cast<const uint16_t*>(h->w.b_in), r,
+                       c.action_dim, c.hidden);
+    if ((e = launch_status()) != OQ_OK) return e;
+  }
+  for (int l = 0; l < c.n_blocks; ++l) {
+    e = fused && l == 0 ? run_block_pi(h, 0, t, r, st, 4, false, true) : run_block(h, l, t, r, st, 4, false);
+    if (e != OQ_OK) return e;
+  }
   return final_stage(h, r, x, st);
 }
 
@@ -1481,16 +1622,25 @@ int final_stage(oq_dit* h, const float* r, float* x, hipStream_t st) {
   const oq_dit_config& c = h->cfg;
   const int64_t M = static_cast<int64_t>(c.batch) * c.tokens;
   const float dt = (is_gr00t(c) ? 1.0f : -1.0f) / static_cast<float>(c.steps);
-  const size_t lds = static_cast<size_t>(4) * c.hidden * sizeof(float);
-  const dim3 fgrid(static_cast<unsigned>((M + 3) / 4));
-  if (is_gr00t(c))
-    hipLaunchKernelGGL(final_kernel<true>, fgrid, dim3(256), lds, st, r, static_cast<const uint16_t*>(h->w.g_f),
-                       static_cast<const uint16_t*>(h->w.w_out), static_cast<const uint16_t*>(h->w.b_out), x, M,
-                       c.hidden, c.action_dim, dt);
-  else
-    hipLaunchKernelGGL(final_kernel<false>, fgrid, dim3(256), lds, st, r, static_cast<const uint16_t*>(h->w.g_f),
-                       static_cast<const uint16_t*>(h->w.w_out), static_cast<const uint16_t*>(h->w.b_out), x, M,
-                       c.hidden, c.action_dim, dt);
+  // Few rows (the Pi-0.5 action tokens): one row per workgroup, so the rows
+  // spread over as many CUs; else four (the weight slices are read once per
+  // workgroup).
+  auto launch = [&](auto LNc, auto Rc) {
+    constexpr bool LN = decltype(LNc)::value;
+    constexpr int R = decltype(Rc)::value;
+    const size_t lds = static_cast<size_t>(R) * c.hidden * sizeof(float);
+    hipLaunchKernelGGL((final_kernel<LN, R>), dim3(static_cast<unsigned>((M + R - 1) / R)), dim3(256), lds, st, r,
+                       static_cast<const uint16_t*>(h->w.g_f), static_cast<const uint16_t*>(h->w.w_out),
+                       static_cast<const uint16_t*>(h->w.b_out), x, M, c.hidden, c.action_dim, dt);
+  };
+  const bool few = M <= 256;
+  if (is_gr00t(c)) {
+    if (few) launch(std::true_type{}, std::integral_constant<int, 1>{});
+    else launch(std::true_type{}, std::integral_constant<int, 4>{});
+  } else {
+    if (few) launch(std::false_type{}, std::integral_constant<int, 1>{});
+    else launch(std::false_type{}, std::integral_constant<int, 4>{});
+  }
   return launch_status();
 }
 
