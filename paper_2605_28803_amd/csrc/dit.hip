@@ -35,6 +35,7 @@
 
 #include "common.h"
 #include "rq_device.h"
+#include "rq_mfma.h"
 
 namespace oq {
 namespace {
@@ -297,6 +298,72 @@ __device__ __forceinline__ void rq1024_row(float (&x)[4], int64_t row, bool vali
   for (int j = 0; j < 4; ++j) c[j] = __float_as_uint(fmaf(x[j], gm, rqd::kRoundMagic)) & 0xFu;
   // Byte i: channel 2i in the low nibble, 2i + 1 in the high nibble.
   *reinterpret_cast<uint16_t*>(dst) = static_cast<uint16_t>(c[0] | (c[1] << 4) | (c[2] << 8) | (c[3] << 12));
+}
+
+// h = fp16(norm(r) g (1 + sc) + sh) for 1536-channel rows (the GR00T hidden
+// size: three 512-channel Hadamard blocks), then rotate + quantize h: one row
+// per three-wave workgroup, wave w holding block w as 8 consecutive channels
+// per lane in the matrix-core layout of rqm::rq_row (H_32 on the fp16 matrix
+// cores, then the lane butterflies; only the row maximum is shared).  The norm
+// statistics are summed in each wave, then over the three waves in LDS.
+template <bool LN, bool SC>
+__global__ __launch_bounds__(192) void norm_rq1536_kernel(const float* __restrict__ r, const uint16_t* __restrict__ g,
+                                                          const uint16_t* __restrict__ sc,
+                                                          const uint16_t* __restrict__ sh, uint16_t* __restrict__ h,
+                                                          int64_t M, RQOut o) {
+  constexpr int D = 1536;
+  __shared__ float red[4];
+  __shared__ float rs[2][3];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int64_t row = blockIdx.x;
+  const bool valid = row < M;
+  const int k = rqm::chan0<1>(wv, 0, lane);
+  const float4* rr = reinterpret_cast<const float4*>(r + (valid ? row : 0) * D + k);
+  const float4 p0 = rr[0], p1 = rr[1];
+  const float v[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+  float gg[8], s1[8], s2[8];
+  load8_f16(g + k, gg);
+  load8_f16(sh + k, s2);
+  if (SC) {
+    load8_f16(sc + k, s1);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) s1[j] = 0.0f;
+  }
+  float mu = 0.0f;
+  if constexpr (LN) {
+    float sum = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) sum += v[j];
+    sum = wave_sum64(sum);
+    if (lane == 0) rs[0][wv] = sum;
+    __syncthreads();
+    mu = (rs[0][0] + rs[0][1] + rs[0][2]) / static_cast<float>(D);
+  }
+  float ss = 0.0f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const float d = v[j] - mu;
+    ss = fmaf(d, d, ss);
+  }
+  ss = wave_sum64(ss);
+  if (lane == 0) rs[1][wv] = ss;
+  __syncthreads();
+  ss = rs[1][0] + rs[1][1] + rs[1][2];
+  const float inv = 1.0f / sqrtf(ss / static_cast<float>(D) + kEps);
+  float x[8];
+  rqm::rv8h cur[1];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const float y = (v[j] - mu) * inv * gg[j];
+    x[j] = valid ? f16r(fmaf(y, s1[j], y) + s2[j]) : 0.0f;
+    cur[0][j] = static_cast<_Float16>(x[j]);
+  }
+  if (valid && h) store8_f16(h + row * D + k, x);
+  rqm::rv8h a1, a2;
+  rqm::hadamard_frags(lane, a1, a2);
+  rqm::rq_row<1, 3, false>(cur, a1, a2, row, valid, lane, wv, o.logb, o.s_t, o.s_over_sqrtb, o.xq, o.xs, nullptr,
+                           nullptr, red, o.tiled, o.sdelta);
 }
 
 // RMS norm, modulation, fp16 rounding and rotate-quantize of one 1024-channel
@@ -1316,6 +1383,15 @@ int norm_rq(oq_dit* h, const float* r, const void* g, const uint16_t* sc, const 
     else
       hipLaunchKernelGGL(norm_rq1024_kernel<false>, dim3(static_cast<unsigned>(M)), dim3(256), 0, st, r, gg, sc, sh,
                          out, M, o);
+    return launch_status();
+  }
+  if (D == 1536 && o.logb == 9) {
+    // Three 512-channel blocks: one row per three-wave workgroup.
+    const dim3 grid(static_cast<unsigned>(M)), block(192);
+    if (ln && sc) hipLaunchKernelGGL((norm_rq1536_kernel<true, true>), grid, block, 0, st, r, gg, sc, sh, out, M, o);
+    else if (ln) hipLaunchKernelGGL((norm_rq1536_kernel<true, false>), grid, block, 0, st, r, gg, sc, sh, out, M, o);
+    else if (sc) hipLaunchKernelGGL((norm_rq1536_kernel<false, true>), grid, block, 0, st, r, gg, sc, sh, out, M, o);
+    else hipLaunchKernelGGL((norm_rq1536_kernel<false, false>), grid, block, 0, st, r, gg, sc, sh, out, M, o);
     return launch_status();
   }
   const bool ok = with_chunks(p.chunks, [&](auto C) {
