@@ -520,7 +520,7 @@ struct AttnArgs {
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 
-// One (sample b, head h, split of KS keys, KS a multiple of 64) on the fp16
+// One (sample b, head h, split of KS keys, KS a multiple of 32) on the fp16
 // matrix cores (v_mfma_f32_16x16x32_f16), ceil(S / 16) waves.  Wave w owns
 // query rows 16w .. 16w+15 (head_dim a multiple of 16; the q.k contraction is
 // padded with zeros to a multiple of 32).  Both products are taken transposed,
@@ -552,7 +552,7 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 // split and dims past head_dim are staged as zeros.
 template <int WAVES, int HD, int KS>
 __global__ __launch_bounds__(64 * WAVES) void attn_partial_kernel(AttnArgs a) {
-  static_assert(KS % 64 == 0, "keys per split");
+  static_assert(KS % 32 == 0, "keys per split");
   constexpr int NT = 64 * WAVES;
   constexpr int PAD = KS + 8;            // padded row (halves): 16-byte reads of 16 rows hit distinct banks
   constexpr int HDL = HD > 0 ? HD : kMaxHeadDim;
@@ -1466,14 +1466,21 @@ int attention_rq(oq_dit* h, const uint16_t* q, int64_t q_ld, const uint16_t* k_p
   if (a.direct) a.out = at<uint16_t>(h, h->lay.o);
   const unsigned waves = static_cast<unsigned>((c.tokens + 15) / 16);
   const dim3 grid(c.batch * c.n_heads, a.nsplit);
-  auto launch = [&](auto W) {
-    constexpr int WV = decltype(W)::value;
+  // At most 32 keys in all (the GR00T self-attention over its 16 action
+  // tokens): a 32-key instance, half the staging and products of 64.
+  const bool short_keys = P + own <= 32;
+  auto launch_ks = [&](auto W, auto KSc) {
+    constexpr int WV = decltype(W)::value, KS = decltype(KSc)::value;
     switch (c.head_dim) {
-      case 48: hipLaunchKernelGGL((attn_partial_kernel<WV, 48, kAttnSplit>), grid, dim3(64 * WV), 0, st, a); break;
-      case 64: hipLaunchKernelGGL((attn_partial_kernel<WV, 64, kAttnSplit>), grid, dim3(64 * WV), 0, st, a); break;
-      case 128: hipLaunchKernelGGL((attn_partial_kernel<WV, 128, kAttnSplit>), grid, dim3(64 * WV), 0, st, a); break;
-      default: hipLaunchKernelGGL((attn_partial_kernel<WV, 0, kAttnSplit>), grid, dim3(64 * WV), 0, st, a); break;
+      case 48: hipLaunchKernelGGL((attn_partial_kernel<WV, 48, KS>), grid, dim3(64 * WV), 0, st, a); break;
+      case 64: hipLaunchKernelGGL((attn_partial_kernel<WV, 64, KS>), grid, dim3(64 * WV), 0, st, a); break;
+      case 128: hipLaunchKernelGGL((attn_partial_kernel<WV, 128, KS>), grid, dim3(64 * WV), 0, st, a); break;
+      default: hipLaunchKernelGGL((attn_partial_kernel<WV, 0, KS>), grid, dim3(64 * WV), 0, st, a); break;
     }
+  };
+  auto launch = [&](auto W) {
+    if (short_keys) launch_ks(W, std::integral_constant<int, 32>{});
+    else launch_ks(W, std::integral_constant<int, kAttnSplit>{});
   };
   switch (waves) {
     case 1: launch(std::integral_constant<int, 1>{}); break;
