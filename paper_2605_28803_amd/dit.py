@@ -98,7 +98,9 @@ class DiT:
                                        self.s_table.ctypes.data_as(C.POINTER(C.c_float)))
         nbytes = C.c_size_t(0)
         _check(self.lib.oq_dit_workspace_bytes(C.byref(self.cfg_c), C.byref(nbytes)), "oq_dit_workspace_bytes")
-        self.workspace = torch.empty((nbytes.value,), dtype=torch.uint8, device=dev)
+        # Zero-filled once, so that the parity views of buffers a path does not
+        # write (gr00t's gate|up, the residual before any step) read zeros.
+        self.workspace = torch.zeros((nbytes.value,), dtype=torch.uint8, device=dev)
         handle = C.c_void_p()
         _check(self.lib.oq_dit_create(C.byref(self.cfg_c), C.byref(self.w_c), C.byref(handle)), "oq_dit_create")
         self.handle = handle
