@@ -223,15 +223,16 @@ __device__ __forceinline__ void lane_stage4_swap(float (&x)[4]) {
   }
 }
 
-// Rotation over the whole 1024-channel row (Hadamard block = K) and the int4
+// Rotation over the whole 256 NW-channel row (Hadamard block = K) and the int4
 // codes (per-token, or with the static steps o.sdelta) of a row held as 4
-// channels per thread (channel 4 t + j) by a 256-thread workgroup: channel
-// bits 0-1 in registers, bits 2-7 across the lanes, bits 8-9 across the four
-// waves through LDS (xch: 1024 floats; red: 4 floats, both unused by the
-// caller meanwhile).  Every thread calls it.
-__device__ __forceinline__ void rq1024_row(float (&x)[4], int64_t row, bool valid, const RQOut& o, float* xch,
-                                           float* red) {
-  constexpr int D = 1024;
+// channels per thread (channel 4 t + j) by a workgroup of NW waves: channel
+// bits 0-1 in registers, bits 2-7 across the lanes, the top log2(NW) bits
+// across the waves in one LDS exchange (xch: 256 NW floats; red: NW floats,
+// both unused by the caller meanwhile).  Every thread calls it.
+template <int NW>
+__device__ __forceinline__ void rq_row4(float (&x)[4], int64_t row, bool valid, const RQOut& o, float* xch,
+                                        float* red) {
+  constexpr int D = 256 * NW;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int k0 = 4 * t;
   // Channel bits 0-1.
@@ -249,13 +250,13 @@ __device__ __forceinline__ void rq1024_row(float (&x)[4], int64_t row, bool vali
   lane_stage4<8>(x, lane);
   lane_stage4_swap<16>(x);
   lane_stage4_swap<32>(x);
-  // Channel bits 8-9: the four waves.
+  // Channel bits 8 and up: the NW waves.
   *reinterpret_cast<float4*>(&xch[k0]) = make_float4(x[0], x[1], x[2], x[3]);
   __syncthreads();
   {
     float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < NW; ++u) {
       const float sg = (__popc(w & u) & 1) ? -1.0f : 1.0f;
       const float4 q = *reinterpret_cast<const float4*>(&xch[(u * 64 + lane) * 4]);
       acc[0] = fmaf(sg, q.x, acc[0]);
@@ -288,7 +289,9 @@ __device__ __forceinline__ void rq1024_row(float (&x)[4], int64_t row, bool vali
   for (int m = 32; m >= 1; m >>= 1) amax = fmaxf(amax, __shfl_xor(amax, m, 64));
   if (lane == 0) red[w] = amax;
   __syncthreads();
-  amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  amax = red[0];
+#pragma unroll
+  for (int u = 1; u < NW; ++u) amax = fmaxf(amax, red[u]);
   const float a_z = amax * o.s_over_sqrtb;
   const float delta = a_z / 7.0f;
   const float gm = delta > 0.0f ? o.s_over_sqrtb / delta : 0.0f;
@@ -298,6 +301,11 @@ __device__ __forceinline__ void rq1024_row(float (&x)[4], int64_t row, bool vali
   for (int j = 0; j < 4; ++j) c[j] = __float_as_uint(fmaf(x[j], gm, rqd::kRoundMagic)) & 0xFu;
   // Byte i: channel 2i in the low nibble, 2i + 1 in the high nibble.
   *reinterpret_cast<uint16_t*>(dst) = static_cast<uint16_t>(c[0] | (c[1] << 4) | (c[2] << 8) | (c[3] << 12));
+}
+
+__device__ __forceinline__ void rq1024_row(float (&x)[4], int64_t row, bool valid, const RQOut& o, float* xch,
+                                           float* red) {
+  rq_row4<4>(x, row, valid, o, xch, red);
 }
 
 // h = fp16(norm(r) g (1 + sc) + sh) for 1536-channel rows (the GR00T hidden
@@ -453,6 +461,39 @@ __global__ __launch_bounds__(256) void inproj_norm_rq1024_kernel(const float* __
   }
   if (valid) *reinterpret_cast<float4*>(r + row * D + 4 * t) = make_float4(v[0], v[1], v[2], v[3]);
   norm1024_row<SC>(v, g, sc, sh, h, row, valid, o, xch, red);
+}
+
+// gelu_rq_kernel for 4096-channel rows with few rows (the Pi-0.5 action
+// tokens, Hadamard block = the row): one row per 1024-thread workgroup, 4
+// consecutive channels per thread, the same activation arithmetic, then
+// rq_row4 over 16 waves.
+template <bool GATED>
+__global__ __launch_bounds__(1024) void gelu_rq4096_kernel(const uint16_t* __restrict__ gu,
+                                                           uint16_t* __restrict__ act, int64_t M, RQOut o) {
+  constexpr int F = 4096;
+  __shared__ __attribute__((aligned(16))) float xch[F];
+  __shared__ float red[16];
+  const int t = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  const bool valid = row < M;
+  const int k0 = 4 * t;
+  const int64_t ld = GATED ? 2 * F : F;
+  const uint16_t* gr = gu + (valid ? row : 0) * ld;
+  const uint2 gq = *reinterpret_cast<const uint2*>(gr + k0);
+  uint2 uq = make_uint2(0x3C003C00u, 0x3C003C00u);  // fp16 1.0 pairs
+  if (GATED) uq = *reinterpret_cast<const uint2*>(gr + F + k0);
+  const uint32_t gw[2] = {gq.x, gq.y}, uw[2] = {uq.x, uq.y};
+  float x[4];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    x[2 * q] = valid ? f16r(gelu_tanh(h2f(gw[q] & 0xFFFFu)) * h2f(uw[q] & 0xFFFFu)) : 0.0f;
+    x[2 * q + 1] = valid ? f16r(gelu_tanh(h2f(gw[q] >> 16)) * h2f(uw[q] >> 16)) : 0.0f;
+  }
+  if (valid && act)
+    *reinterpret_cast<uint2*>(act + row * F + k0) =
+        make_uint2(static_cast<uint32_t>(f2h(x[0])) | (static_cast<uint32_t>(f2h(x[1])) << 16),
+                   static_cast<uint32_t>(f2h(x[2])) | (static_cast<uint32_t>(f2h(x[3])) << 16));
+  rq_row4<16>(x, row, valid, o, xch, red);
 }
 
 // GATED: a = fp16(gelu_tanh(gate) up) from gu = [gate | up] (fp16 [M][2F]);
@@ -1418,8 +1459,15 @@ int gelu_rq(oq_dit* h, const uint16_t* in, uint16_t* act, float s, hipStream_t s
   const int64_t F = h->cfg.mlp;
   RQPlan p;
   const RQOut o = rq_out(h, F, s, &p, sdelta);
-  const FusedLaunch fl = fused_launch(M, F, p);
   const bool gated = !is_gr00t(h->cfg);
+  if (F == 4096 && o.logb == 12 && M <= 256) {
+    if (gated)
+      hipLaunchKernelGGL(gelu_rq4096_kernel<true>, dim3(static_cast<unsigned>(M)), dim3(1024), 0, st, in, act, M, o);
+    else
+      hipLaunchKernelGGL(gelu_rq4096_kernel<false>, dim3(static_cast<unsigned>(M)), dim3(1024), 0, st, in, act, M, o);
+    return launch_status();
+  }
+  const FusedLaunch fl = fused_launch(M, F, p);
   const bool ok = with_chunks(p.chunks, [&](auto C) {
     if (gated)
       hipLaunchKernelGGL((gelu_rq_kernel<decltype(C)::value, true>), fl.grid, fl.block, fl.lds, st, in, act, M,
