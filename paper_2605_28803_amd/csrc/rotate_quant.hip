@@ -127,7 +127,7 @@ int rq_mfma_launch(const void* X, int64_t M, int64_t K, int64_t ldx, int had_blo
   int ng = 0, w = 0;
   rq_mfma_shape(K, &ng, &w);
   // Few rows (the action tokens): two waves per 4096-channel row halve the
-  // serial work of a wave; the grid is far below one wave per SIMD anyway.
+  // serial work of a wave (at most 512 rows: at most one wave per SIMD).
   if (K == 4096 && M <= 512) { ng = 4; w = 2; }
   const int logb = ilog2(had_block);
   const float s_over_sqrtb = static_cast<float>(static_cast<double>(s_t) / std::sqrt(static_cast<double>(had_block)));

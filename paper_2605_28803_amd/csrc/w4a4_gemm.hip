@@ -686,7 +686,7 @@ int launch_small_mb(const GemmArgs& a, hipStream_t stream) {
 // within 16 waves per CU (the 50-row DiT linears: q|k|v, o and down, 1.5 to
 // 5 thousand waves; not the 8192-column gate|up, whose 32-column workgroups of
 // 8 waves would make 8 thousand).
-int small_row_blocks_of_16(const GemmArgs& a) {
+bool small_row_blocks_of_16(const GemmArgs& a) {
   const bool wide = a.N > 4096, shallow = a.K <= 1024;
   const int64_t bn = wide ? 32 : 16, waves = wide ? 8 : (shallow ? 4 : 16);
   const int64_t total = (a.N + bn - 1) / bn * ((a.M + 15) / 16) * waves;
