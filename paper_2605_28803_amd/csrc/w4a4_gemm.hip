@@ -136,8 +136,15 @@ void gemm_big_kernel(GemmArgs a) {
   constexpr int NTG = 64 * WM * WN;         // threads per group
   constexpr int NT = NTG * KG;              // threads
   constexpr int BM = 32 * TM * WM, BN = 32 * TN * WN;
-  constexpr int PA = 2 * BM / NTG, PB = 2 * BN / NTG;  // rows each thread loads per stage
-  static_assert(PA >= 1 && PB >= 1 && 2 * BM % NTG == 0 && 2 * BN % NTG == 0, "load split");
+  // Rows each thread loads per stage (two 32-byte pieces per row).  SPLIT:
+  // fewer row pieces than threads (the 8-wave 128 x 128 tile), so the first
+  // 2 BM threads load one piece of A each and the rest one piece of B.
+  constexpr bool SPLIT = 2 * BM < NTG;
+  constexpr int PA = SPLIT ? 0 : 2 * BM / NTG, PB = SPLIT ? 0 : 2 * BN / NTG;
+  constexpr int PAa = PA > 0 ? PA : 1, PBa = PB > 0 ? PB : 1;  // array extents
+  static_assert(SPLIT ? (2 * (BM + BN) == NTG && !A8 && KG == 1)
+                      : (PA >= 1 && PB >= 1 && 2 * BM % NTG == 0 && 2 * BN % NTG == 0),
+                "load split");
   // Per group two LDS buffers per operand; after the K loop the same memory
   // holds the other groups' accumulators and the 2-byte output tile of the
   // staged epilogue.
@@ -170,14 +177,19 @@ void gemm_big_kernel(GemmArgs a) {
   // and a stage past the end, read clamped addresses; their MFMAs are skipped.
   const int lr = tg >> 1, lh = tg & 1;
   const int njl = (nk + KG - 1) / KG;  // local stages (the same count in every group)
-  const uint8_t* gA[PA];
-  const uint8_t* gB[PB];
+  const uint8_t* gA[PAa];
+  const uint8_t* gB[PBa];
 #pragma unroll
   for (int r = 0; r < PA; ++r) gA[r] = a.A + min<int64_t>(m0 + lr + r * (NTG / 2), a.M - 1) * Ka + lh * 32 * AW;
 #pragma unroll
   for (int r = 0; r < PB; ++r) gB[r] = a.B + min<int64_t>(n0 + lr + r * (NTG / 2), a.N - 1) * Kb + lh * 32;
+  // SPLIT: this thread's operand, its row there and its source row.
+  const bool s_isA = tg < 2 * BM;
+  const int s_row = (s_isA ? tg : tg - 2 * BM) >> 1;
+  const uint8_t* gS = s_isA ? a.A + min<int64_t>(m0 + s_row, a.M - 1) * Ka + lh * 32
+                            : a.B + min<int64_t>(n0 + s_row, a.N - 1) * Kb + lh * 32;
   // NS register stages, indexed only by constants (they stay in VGPRs).
-  uint4 ra[NS][2 * AW * PA], rb[NS][2 * PB];
+  uint4 ra[NS][2 * AW * PAa], rb[NS][2 * PBa], rs[NS][2];
 #define OQ_GLOAD(KS, S)                                                                \
   {                                                                                    \
     const int h_ = min(2 * (KG * (KS) + grp) + lh, nk64 - 1);                           \
@@ -188,6 +200,10 @@ void gemm_big_kernel(GemmArgs a) {
     _Pragma("unroll") for (int r_ = 0; r_ < PB; ++r_) {                          \
       rb[S][2 * r_] = *reinterpret_cast<const uint4*>(gB[r_] + off_);            \
       rb[S][2 * r_ + 1] = *reinterpret_cast<const uint4*>(gB[r_] + off_ + 16);   \
+    }                                                                            \
+    if constexpr (SPLIT) {                                                       \
+      rs[S][0] = *reinterpret_cast<const uint4*>(gS + off_);                     \
+      rs[S][1] = *reinterpret_cast<const uint4*>(gS + off_ + 16);                \
     }                                                                            \
   }
 // Widen 16 packed bytes to 32 int8 (16 * code) and store them: the same
@@ -214,6 +230,12 @@ void gemm_big_kernel(GemmArgs a) {
     _Pragma("unroll") for (int r_ = 0; r_ < PB; ++r_) {                                            \
       OQ_ST32(&sB[(BUF)][(lr + r_ * (NTG / 2)) * BIG8_STRIDE + lh * 64], rb[S][2 * r_])            \
       OQ_ST32(&sB[(BUF)][(lr + r_ * (NTG / 2)) * BIG8_STRIDE + lh * 64 + 32], rb[S][2 * r_ + 1])   \
+    }                                                                                              \
+    if constexpr (SPLIT) {                                                                         \
+      uint8_t* d_ = s_isA ? &sA[(BUF)][s_row * BIG8_STRIDE + lh * 64]                              \
+                          : &sB[(BUF)][s_row * BIG8_STRIDE + lh * 64];                             \
+      OQ_ST32(d_, rs[S][0])                                                                        \
+      OQ_ST32(d_ + 32, rs[S][1])                                                                   \
     }                                                                                              \
   }
 
@@ -741,7 +763,7 @@ int launch_big_a(const GemmArgs& a, Epilogue epi, int64_t tiles, hipStream_t str
 
 template <int WM, int WN, int TM, int TN, int NS, int KG = 1>
 int launch_big(const GemmArgs& a, Epilogue epi, int64_t tiles, hipStream_t stream) {
-  if constexpr (WM * WN * TM * TN <= 16) {
+  if constexpr (WM * WN * TM * TN <= 16 && 2 * 32 * TM * WM >= 64 * WM * WN) {
     if (a.a_i8) return launch_big_a<WM, WN, TM, TN, true, NS, KG>(a, epi, tiles, stream);
   }
   return launch_big_a<WM, WN, TM, TN, false, NS, KG>(a, epi, tiles, stream);
@@ -779,6 +801,7 @@ int gemm_launch(const GemmArgs& a, Epilogue epi, hipStream_t stream) {
   const bool kgroups = !a.a_i8;
   if (mid_tiles >= 256) {
     if (kgroups && mid_tiles <= 256) return launch_big<2, 2, 2, 2, 3, 2>(a, epi, mid_tiles, stream);
+    if (!a.a_i8) return launch_big<2, 4, 2, 1, 3>(a, epi, mid_tiles, stream);
     return launch_big<2, 2, 2, 2, 3>(a, epi, mid_tiles, stream);
   }
   // Fewer 128 x 128 tiles than CUs (prefill-sized M with N ~ 2048): 64 x 64
