@@ -142,7 +142,7 @@ void gemm_big_kernel(GemmArgs a) {
   constexpr bool SPLIT = 2 * BM < NTG;
   constexpr int PA = SPLIT ? 0 : 2 * BM / NTG, PB = SPLIT ? 0 : 2 * BN / NTG;
   constexpr int PAa = PA > 0 ? PA : 1, PBa = PB > 0 ? PB : 1;  // array extents
-  static_assert(SPLIT ? (2 * (BM + BN) == NTG && !A8 && KG == 1)
+  static_assert(SPLIT ? (2 * (BM + BN) == NTG && !A8)
                       : (PA >= 1 && PB >= 1 && 2 * BM % NTG == 0 && 2 * BN % NTG == 0),
                 "load split");
   // Per group two LDS buffers per operand; after the K loop the same memory
@@ -810,8 +810,8 @@ int gemm_launch(const GemmArgs& a, Epilogue epi, hipStream_t stream) {
   // groups: 7-11% faster at M = 816 - 1024, N = 1536 - 2048).
   const int64_t small_tiles = ((a.M + 63) / 64) * ((a.N + 63) / 64);
   if (kgroups && small_tiles <= 512) {
-    if (a.K >= 6144) return launch_big<1, 2, 2, 1, 4, 2>(a, epi, small_tiles, stream);
-    return launch_big<1, 2, 2, 1, 3, 2>(a, epi, small_tiles, stream);
+    if (a.K >= 6144) return launch_big<2, 2, 1, 1, 4, 2>(a, epi, small_tiles, stream);
+    return launch_big<2, 2, 1, 1, 3, 2>(a, epi, small_tiles, stream);
   }
   if (a.K >= 6144) return launch_big<1, 2, 2, 1, 12>(a, epi, small_tiles, stream);
   return launch_big<1, 2, 2, 1, 3>(a, epi, small_tiles, stream);
