@@ -800,7 +800,7 @@ int gemm_launch(const GemmArgs& a, Epilogue epi, hipStream_t stream) {
   // 1536 - 8192; slower once a second round of workgroups is needed.)
   const bool kgroups = !a.a_i8;
   if (mid_tiles >= 256) {
-    if (kgroups && mid_tiles <= 256) return launch_big<2, 2, 2, 2, 3, 2>(a, epi, mid_tiles, stream);
+    if (kgroups && mid_tiles <= 256) return launch_big<2, 4, 2, 1, 3, 2>(a, epi, mid_tiles, stream);
     if (!a.a_i8) return launch_big<2, 4, 2, 1, 3>(a, epi, mid_tiles, stream);
     return launch_big<2, 2, 2, 2, 3>(a, epi, mid_tiles, stream);
   }
