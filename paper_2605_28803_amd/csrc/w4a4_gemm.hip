@@ -813,8 +813,12 @@ int gemm_launch(const GemmArgs& a, Epilogue epi, hipStream_t stream) {
     if (a.K >= 6144) return launch_big<2, 2, 1, 1, 4, 2>(a, epi, small_tiles, stream);
     return launch_big<2, 2, 1, 1, 3, 2>(a, epi, small_tiles, stream);
   }
-  if (a.K >= 6144) return launch_big<1, 2, 2, 1, 12>(a, epi, small_tiles, stream);
-  return launch_big<1, 2, 2, 1, 3>(a, epi, small_tiles, stream);
+  if (a.a_i8) {
+    if (a.K >= 6144) return launch_big<1, 2, 2, 1, 12>(a, epi, small_tiles, stream);
+    return launch_big<1, 2, 2, 1, 3>(a, epi, small_tiles, stream);
+  }
+  if (a.K >= 6144) return launch_big<2, 2, 1, 1, 12>(a, epi, small_tiles, stream);
+  return launch_big<2, 2, 1, 1, 3>(a, epi, small_tiles, stream);
 }
 
 }  // namespace oq
