@@ -604,7 +604,12 @@ int oq_dit_workspace_bytes(const oq_dit_config* cfg, size_t* bytes);
 int oq_dit_create(const oq_dit_config* cfg, const oq_dit_weights* w, oq_dit** out);
 
 /* Attach caller-owned device workspace (256-byte aligned, at least
- * oq_dit_workspace_bytes).  Errors: OQ_ERR_NULL, OQ_ERR_WORKSPACE, OQ_ERR_ALIGN. */
+ * oq_dit_workspace_bytes).  With more than 64 action rows (batch * tokens)
+ * the workspace ends in the split-K scratch of the deep block linears: 16 MB
+ * of int32 partial tiles and 512 arrival tickets, which this call zeroes
+ * synchronously (hipMemset; every later linear leaves them zero).  Calls of
+ * one handle must not overlap in time (they share the workspace).
+ * Errors: OQ_ERR_NULL, OQ_ERR_WORKSPACE, OQ_ERR_ALIGN, OQ_ERR_HIP. */
 int oq_dit_set_workspace(oq_dit* h, void* workspace, size_t bytes);
 
 /* gr00t: compute every cross-attention block's conditioning k|v from cond

@@ -90,6 +90,13 @@ struct GemmArgs {
   int64_t M, N, K, ldc;
   bool a_tiled;          // A is in the 16-row tiled layout (K % 128 == 0)
   bool a_i8;             // A holds 8-bit codes, one byte each, [M][K] (W4A8)
+  // Split-K scratch of the caller (null: no split): int32 partial tiles and
+  // one arrival ticket per tile (zero between launches: the last arrival of
+  // a tile resets its ticket).  Launches that share them must not overlap.
+  int32_t* part = nullptr;
+  int32_t* tickets = nullptr;
+  int64_t part_words = 0, n_tickets = 0;
+  int splitk = 1;        // set by the launcher
 };
 
 int gemm_validate(const uint8_t* Xq, int64_t M, const uint8_t* Wq, int64_t N, int64_t K,

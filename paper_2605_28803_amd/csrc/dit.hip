@@ -1242,7 +1242,8 @@ bool is_gr00t(const oq_dit_config& c) { return c.arch == OQ_DIT_GR00T; }
 int n_cross(const oq_dit_config& c) { return is_gr00t(c) ? (c.n_blocks + 1) / 2 : 0; }
 
 struct Layout {
-  size_t r, h1, qkv, o, h2, gu, act, xq, xs, part_o, part_ml, ckv, ckvh, total;
+  size_t r, h1, qkv, o, h2, gu, act, xq, xs, part_o, part_ml, ckv, ckvh, skp, skt, total;
+  int64_t sk_words, sk_tickets;  // split-K scratch of the row-layout linears (0 with tiled codes)
 };
 
 Layout layout_for(const oq_dit_config& c) {
@@ -1272,6 +1273,13 @@ Layout layout_for(const oq_dit_config& c) {
   // and every cross-attention block's values head-major.
   L.ckv = off; off += align256(static_cast<size_t>(n_cross(c) > 0 ? 1 : 0) * MC * 2 * D * 2);
   L.ckvh = off; off += align256(static_cast<size_t>(n_cross(c)) * MC * 2 * D * 2);
+  // Split-K scratch of the deep block linears with row-layout codes (M > 64):
+  // two int32 partial 64 x 64 tiles for each of up to 512 tiles, and the
+  // tiles' arrival tickets (zeroed by oq_dit_set_workspace).
+  L.sk_tickets = M > 64 ? 512 : 0;
+  L.sk_words = L.sk_tickets * 2 * 64 * 64;
+  L.skp = off; off += align256(static_cast<size_t>(L.sk_words) * 4);
+  L.skt = off; off += align256(static_cast<size_t>(L.sk_tickets) * 4);
   L.total = off;
   return L;
 }
@@ -1484,6 +1492,12 @@ int gemm(oq_dit* h, const oq_qweight& wt, int64_t K, int64_t N, Epilogue epi, vo
   const int64_t M = static_cast<int64_t>(h->cfg.batch) * h->cfg.tokens;
   GemmArgs a{at<uint8_t>(h, h->lay.xq), wt.wq, at<float>(h, h->lay.xs), wt.w_scale, nullptr, out, gate, M, N, K, ldc,
              h->tiled};
+  if (h->lay.sk_tickets > 0) {
+    a.part = at<int32_t>(h, h->lay.skp);
+    a.tickets = at<int32_t>(h, h->lay.skt);
+    a.part_words = h->lay.sk_words;
+    a.n_tickets = h->lay.sk_tickets;
+  }
   return gemm_launch(a, epi, st);
 }
 
@@ -1934,6 +1948,10 @@ extern "C" int oq_dit_set_workspace(oq_dit* h, void* workspace, size_t bytes) {
   }
   h->ws = static_cast<uint8_t*>(workspace);
   h->ws_bytes = bytes;
+  // The split-K tickets start at zero (each launch leaves them so).
+  if (h->lay.sk_tickets > 0 &&
+      hipMemset(h->ws + h->lay.skt, 0, static_cast<size_t>(h->lay.sk_tickets) * 4) != hipSuccess)
+    return OQ_ERR_HIP;
   return OQ_OK;
 }
 

@@ -161,15 +161,23 @@ void gemm_big_kernel(GemmArgs a) {
       reinterpret_cast<uint8_t (*)[BN * BIG8_STRIDE]>(smem + grp * GBYTES + 2 * BM * BIG8_STRIDE);
   const int tiles_m = static_cast<int>((a.M + BM - 1) / BM);
   const int tiles_n = static_cast<int>((a.N + BN - 1) / BN);
+  // Split K (a.splitk > 1): workgroup id = ks * tiles + tile; split ks takes
+  // stages [ks * sps, (ks + 1) * sps) of K.
+  const int ntile = tiles_m * tiles_n;
+  const int tile_id = static_cast<int>(blockIdx.x) % ntile, ks = static_cast<int>(blockIdx.x) / ntile;
   int tm, tn;
-  big_tile(blockIdx.x, tiles_m, tiles_n, &tm, &tn);
+  big_tile(tile_id, tiles_m, tiles_n, &tm, &tn);
   const int64_t m0 = static_cast<int64_t>(tm) * BM;
   const int64_t n0 = static_cast<int64_t>(tn) * BN;
   const int64_t Kb = a.K / 2;
   constexpr int AW = A8 ? 2 : 1;  // A bytes per packed B byte
   const int64_t Ka = Kb * AW;
-  const int nk = static_cast<int>((a.K + BIG_KSTAGE - 1) / BIG_KSTAGE);  // stages (the last may be half)
-  const int nk64 = static_cast<int>(a.K / 64);                            // 64-code halves in total
+  const int nk_all = static_cast<int>((a.K + BIG_KSTAGE - 1) / BIG_KSTAGE);  // stages (the last may be half)
+  const int sps = (nk_all + a.splitk - 1) / a.splitk;                         // stages per split
+  const int s0 = ks * sps;                                                     // this split's first stage
+  const int nk = min(nk_all - s0, sps);                                        // ... and its stage count
+  const int h0 = 2 * s0;                                                       // its first 64-code half
+  const int nk64 = min(static_cast<int>(a.K / 64), 2 * (s0 + sps)) - h0;       // ... and its half count
 
   // Global -> LDS: a stage is BM (A) and BN (B) rows x 64 packed bytes; a
   // thread loads 32 packed bytes (two 16-byte pieces) of rows tg/2 + r NTG/2.
@@ -192,7 +200,7 @@ void gemm_big_kernel(GemmArgs a) {
   uint4 ra[NS][2 * AW * PAa], rb[NS][2 * PBa], rs[NS][2];
 #define OQ_GLOAD(KS, S)                                                                \
   {                                                                                    \
-    const int h_ = min(2 * (KG * (KS) + grp) + lh, nk64 - 1);                           \
+    const int h_ = h0 + min(2 * (KG * (KS) + grp) + lh, nk64 - 1);                      \
     const int64_t off_ = static_cast<int64_t>(h_) * 32 - lh * 32;                      \
     _Pragma("unroll") for (int r_ = 0; r_ < PA; ++r_)                                  \
     _Pragma("unroll") for (int c_ = 0; c_ < 2 * AW; ++c_)                              \
@@ -350,6 +358,51 @@ void gemm_big_kernel(GemmArgs a) {
 #undef OQ_ST32
 #undef OQ_LSTORE
 #undef OQ_COMPUTE
+  if (a.splitk > 1) {
+    // Every split publishes its exact partial (group 0's accumulators,
+    // lane-major) and takes a ticket; the last arrival adds the others' and
+    // runs the epilogue, the rest leave.  No workgroup waits for another.
+    // The partials move through device-scope atomic stores and loads (they
+    // bypass the XCD-local caches) and the ticket is taken after every store
+    // of the workgroup is acknowledged, so no cache-wide write-back or
+    // invalidation is needed (those would evict the other workgroups' A / B
+    // lines from the L2 mid-loop).
+    constexpr int WORDS = WM * WN * TM * TN * 16 * 64;
+    __shared__ int s_last;
+    int32_t* mine = a.part + (static_cast<int64_t>(tile_id) * a.splitk + ks) * WORDS;
+    if (grp == 0) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            __hip_atomic_store(&mine[((wave * TM + i) * TN + j) * 1024 + e * 64 + lane], acc[i][j][e],
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // the stores are acknowledged
+    __syncthreads();
+    if (tid == 0)
+      s_last = __hip_atomic_fetch_add(a.tickets + tile_id, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+               a.splitk - 1;
+    __syncthreads();
+    if (!s_last) return;
+    if (grp == 0) {
+      for (int k2 = 0; k2 < a.splitk; ++k2) {
+        if (k2 == ks) continue;
+        const int32_t* other = a.part + (static_cast<int64_t>(tile_id) * a.splitk + k2) * WORDS;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+              acc[i][j][e] += __hip_atomic_load(&other[((wave * TM + i) * TN + j) * 1024 + e * 64 + lane],
+                                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+    if (tid == 0) __hip_atomic_store(a.tickets + tile_id, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
 
   // Epilogue (32 x 32 layout: element e of lane l is row 8*(e/4) + 4*(l/32) + e%4, column l%32).
   // Each lane's rows come in runs of four consecutive rows: their token scales
@@ -741,7 +794,7 @@ int gemm_validate(const uint8_t* Xq, int64_t M, const uint8_t* Wq, int64_t N, in
 
 template <int WM, int WN, int TM, int TN, bool A8, int NS, int KG>
 int launch_big_a(const GemmArgs& a, Epilogue epi, int64_t tiles, hipStream_t stream) {
-  const dim3 g(static_cast<unsigned>(tiles)), b(64 * WM * WN * KG);
+  const dim3 g(static_cast<unsigned>(tiles * a.splitk)), b(64 * WM * WN * KG);
   switch (epi) {
     case EPI_I32: hipLaunchKernelGGL((gemm_big_kernel<EPI_I32, WM, WN, TM, TN, A8, NS, KG>), g, b, 0, stream, a); break;
     case EPI_F16: hipLaunchKernelGGL((gemm_big_kernel<EPI_F16, WM, WN, TM, TN, A8, NS, KG>), g, b, 0, stream, a); break;
@@ -811,6 +864,17 @@ int gemm_launch(const GemmArgs& a, Epilogue epi, hipStream_t stream) {
   // (K >= 6144) keeps more register stages in flight (twelve without K
   // groups: 7-11% faster at M = 816 - 1024, N = 1536 - 2048).
   const int64_t small_tiles = ((a.M + 63) / 64) * ((a.N + 63) / 64);
+  // Deep K with the caller's split-K scratch: two K halves as separate
+  // one-group workgroups (36 KB of LDS, four per CU), so that 257 - 512 tiles
+  // make 514 - 1024 equal workgroups resident at once, where two-group
+  // workgroups (two per CU) leave some CUs with one tile and others with two.
+  constexpr int64_t kWords64 = 64 * 64;  // int32 partial of a 64 x 64 tile
+  if (kgroups && small_tiles > 256 && small_tiles <= 512 && a.K >= 6144 && a.part && a.tickets &&
+      a.part_words >= 2 * small_tiles * kWords64 && a.n_tickets >= small_tiles) {
+    GemmArgs s2 = a;
+    s2.splitk = 2;
+    return launch_big<2, 2, 1, 1, 4>(s2, epi, small_tiles, stream);
+  }
   if (kgroups && small_tiles <= 512) {
     if (a.K >= 6144) return launch_big<2, 2, 1, 1, 4, 2>(a, epi, small_tiles, stream);
     return launch_big<2, 2, 1, 1, 3, 2>(a, epi, small_tiles, stream);
