@@ -1,7 +1,9 @@
 """Build the HIP library liboq.so in-tree for gfx950 with hipcc.
 
 Every source under csrc/ is compiled (in parallel) to an object under _build/
-and linked into paper_2605_28803_amd/liboq.so.  Always recompiles.
+and linked into paper_2605_28803_amd/liboq.so.  Always recompiles.  Before
+linking, the gfx950 code of every object is disassembled and checked for MFMAs
+that could run under an empty EXEC mask (isa_check).
 """
 from __future__ import annotations
 
@@ -50,6 +52,15 @@ def build(verbose: bool = False) -> str:
     jobs = min(len(srcs), max(1, min(8, os.cpu_count() or 1)))
     with cf.ThreadPoolExecutor(jobs) as ex:
         objs = list(ex.map(_compile, srcs))
+    # Matrix-core instructions ignore EXEC: refuse code in which an MFMA can
+    # run under a narrowed EXEC mask with no branch around it.
+    if ROOT not in sys.path:
+        sys.path.insert(0, ROOT)  # run as a script
+    from paper_2605_28803_amd import isa_check
+    bad = isa_check.check_objects(objs)
+    if bad:
+        raise RuntimeError("MFMA under a possibly-empty EXEC mask (no s_cbranch_execz around it):\n" +
+                           "\n".join(f"  {o}: {f}: {i}" for o, f, i in bad[:20]))
     tmp = LIB + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + objs + ["-lpthread"]
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -261,30 +261,38 @@ void gemm_big_kernel(GemmArgs a) {
   const uint8_t* pB = &sB[0][(wn * 32 * TN + frow) * BIG8_STRIDE + fofs];
   constexpr int ABUF = BM * BIG8_STRIDE, BBUF = BN * BIG8_STRIDE;
 // The int8 fragments of sub-step sub + 1 are read from LDS while sub-step
-// sub is multiplied (two register sets).
+// sub is multiplied (two register sets).  All four sub-steps of every stage
+// are issued without a branch: a sub-step past the stage's codes (the second
+// half of a final half stage, a stage past the end of K) multiplies a zero A
+// fragment and adds exactly 0.  (A branch on the per-lane stage condition may
+// be compiled as an EXEC mask alone, and an MFMA still accumulates with EXEC
+// = 0.)  The fragment reads stay inside the stage's LDS rows.
 #define OQ_COMPUTE(BUF, NSUB)                                                                               \
   {                                                                                                         \
     const int boa_ = (BUF) * ABUF, bob_ = (BUF) * BBUF;                                                      \
-    v4i fa_[2][TM], fb_[2][TN];                                                                                  \
+    const int nsub_ = (NSUB);                                                                               \
+    v4i fa_[2][TM], fb_[2][TN];                                                                             \
     _Pragma("unroll") for (int i = 0; i < TM; ++i)                                                           \
       fa_[0][i] = *reinterpret_cast<const v4i*>(pA + boa_ + i * 32 * BIG8_STRIDE);                          \
     _Pragma("unroll") for (int j = 0; j < TN; ++j)                                                           \
       fb_[0][j] = *reinterpret_cast<const v4i*>(pB + bob_ + j * 32 * BIG8_STRIDE);                          \
     _Pragma("unroll") for (int sub = 0; sub < 4; ++sub) {                                                   \
-      if (sub < (NSUB)) {                                                                                   \
-        const int cur_ = sub & 1;                                                                           \
-        if (sub + 1 < (NSUB)) {                                                                             \
-          _Pragma("unroll") for (int i = 0; i < TM; ++i)                                                     \
-            fa_[cur_ ^ 1][i] = *reinterpret_cast<const v4i*>(pA + boa_ + i * 32 * BIG8_STRIDE + (sub + 1) * 32); \
-          _Pragma("unroll") for (int j = 0; j < TN; ++j)                                                     \
-            fb_[cur_ ^ 1][j] = *reinterpret_cast<const v4i*>(pB + bob_ + j * 32 * BIG8_STRIDE + (sub + 1) * 32); \
-        }                                                                                                   \
-        __builtin_amdgcn_sched_barrier(0);                                                                  \
+      const int cur_ = sub & 1;                                                                             \
+      if (sub + 1 < 4) {                                                                                    \
         _Pragma("unroll") for (int i = 0; i < TM; ++i)                                                       \
+          fa_[cur_ ^ 1][i] = *reinterpret_cast<const v4i*>(pA + boa_ + i * 32 * BIG8_STRIDE + (sub + 1) * 32); \
         _Pragma("unroll") for (int j = 0; j < TN; ++j)                                                       \
-          acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa_[cur_][i], fb_[cur_][j], acc[i][j], 0, 0, 0); \
-        __builtin_amdgcn_sched_barrier(0);                                                                  \
+          fb_[cur_ ^ 1][j] = *reinterpret_cast<const v4i*>(pB + bob_ + j * 32 * BIG8_STRIDE + (sub + 1) * 32); \
       }                                                                                                     \
+      const bool on_ = sub < nsub_;                                                                         \
+      __builtin_amdgcn_sched_barrier(0);                                                                    \
+      _Pragma("unroll") for (int i = 0; i < TM; ++i) {                                                       \
+        v4i a_;                                                                                             \
+        _Pragma("unroll") for (int c_ = 0; c_ < 4; ++c_) a_[c_] = on_ ? fa_[cur_][i][c_] : 0;              \
+        _Pragma("unroll") for (int j = 0; j < TN; ++j)                                                       \
+          acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a_, fb_[cur_][j], acc[i][j], 0, 0, 0);          \
+      }                                                                                                     \
+      __builtin_amdgcn_sched_barrier(0);                                                                    \
     }                                                                                                       \
   }
   // Sub-steps of 32 codes in local stage ks: 4, 2 for a final half stage, 0
@@ -576,7 +584,7 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_small_kernel(GemmArgs a) {
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // scalar: the unit range bounds MFMA loops
   const int64_t n0 = static_cast<int64_t>(blockIdx.x) * BNs;
   const int64_t m0 = static_cast<int64_t>(blockIdx.y) * ROWS;
   const int64_t Kb = a.K / 2;

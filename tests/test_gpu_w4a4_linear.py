@@ -31,7 +31,11 @@ def _codes(rng, R, K):
                                    # the second group's only stage a half stage, no stage at all, an
                                    # odd stage count, deep K, and 256 128 x 128 tiles (ragged N)
                                    (1000, 1000, 192), (130, 200, 64), (500, 700, 320), (520, 1000, 6208),
-                                   (250, 16376, 320), (256, 16384, 1536)])
+                                   (250, 16376, 320), (256, 16384, 1536),
+                                   # two local stages, the second a half stage (group 0 at K = 320,
+                                   # group 1 at K = 448; one group at K = 192 with 520 tiles): its
+                                   # skipped sub-steps must add nothing
+                                   (500, 700, 448), (500, 4160, 192)])
 def test_i32_accumulators_bit_exact(M, N, K):
     print(f"gemm i32 M={M} N={N} K={K}", flush=True)
     rng = np.random.default_rng(M + N + K)
@@ -43,7 +47,8 @@ def test_i32_accumulators_bit_exact(M, N, K):
 
 
 @pytest.mark.parametrize("M,N,K", [(4096, 4096, 256), (4100, 4160, 192), (8192, 2048, 128), (2048, 8320, 64),
-                                   (4096, 4096, 320), (2100, 4160, 192), (8192, 4096, 448), (1100, 8200, 128)])
+                                   (4096, 4096, 320), (2100, 4160, 192), (8192, 4096, 448), (1100, 8200, 128),
+                                   (2100, 2100, 192)])
 def test_i32_bit_exact_large_tiles(M, N, K):
     """Shapes that take the 256 x 256 and the 128 x 128 tile paths, with ragged edges (the 64 x 64 tile
     is taken by the M > 64 shapes of test_i32_accumulators_bit_exact)."""
