@@ -31,6 +31,9 @@ CASES = [
     (301, 16384, 16384, 2.0), (1000, 4096, 4096, 1.0), (999, 1024, 256, 1.0),
     # more rows than one round of resident workgroups
     (6000, 4096, 4096, 1.0), (6001, 4096, 1024, 1.3), (1100, 8192, 8192, 1.0), (1030, 16384, 16384, 0.9),
+    # four-wave rows over several rounds of resident workgroups (b = 4096 at
+    # K = 16384: no wave transpose)
+    (4000, 8192, 8192, 1.0), (2049, 16384, 16384, 0.7), (2500, 16384, 4096, 1.0),
     # three waves per row, one Hadamard block (or several) each: K = 1536 / 6144
     (1024, 1536, 512, 1.0), (1025, 6144, 2048, 1.7), (130, 6144, 64, 1.0), (3, 1536, 32, 2.0),
     # K = 4096 with at most 512 rows: two waves per row (odd M, the last
