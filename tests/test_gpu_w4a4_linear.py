@@ -48,7 +48,9 @@ def test_i32_accumulators_bit_exact(M, N, K):
 
 @pytest.mark.parametrize("M,N,K", [(4096, 4096, 256), (4100, 4160, 192), (8192, 2048, 128), (2048, 8320, 64),
                                    (4096, 4096, 320), (2100, 4160, 192), (8192, 4096, 448), (1100, 8200, 128),
-                                   (2100, 2100, 192)])
+                                   (2100, 2100, 192),
+                                   # 384 / 430 tiles of 128 x 128: ragged edges, a final half stage
+                                   (1000, 6100, 1536), (1200, 5500, 448)])
 def test_i32_bit_exact_large_tiles(M, N, K):
     """Shapes that take the 256 x 256 and the 128 x 128 tile paths, with ragged edges (the 64 x 64 tile
     is taken by the M > 64 shapes of test_i32_accumulators_bit_exact)."""
