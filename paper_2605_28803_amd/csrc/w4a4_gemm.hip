@@ -182,7 +182,8 @@ void gemm_big_kernel(GemmArgs a) {
   // Global -> LDS: a stage is BM (A) and BN (B) rows x 64 packed bytes; a
   // thread loads 32 packed bytes (two 16-byte pieces) of rows tg/2 + r NTG/2.
   // Local stage j of group grp is stage KG j + grp of K.  A half stage past K,
-  // and a stage past the end, read clamped addresses; their MFMAs are skipped.
+  // and a stage past the end, read clamped addresses; their sub-steps past the
+  // codes multiply zero A fragments (OQ_COMPUTE).
   const int lr = tg >> 1, lh = tg & 1;
   const int njl = (nk + KG - 1) / KG;  // local stages (the same count in every group)
   const uint8_t* gA[PAa];
@@ -295,8 +296,8 @@ void gemm_big_kernel(GemmArgs a) {
       __builtin_amdgcn_sched_barrier(0);                                                                    \
     }                                                                                                       \
   }
-  // Sub-steps of 32 codes in local stage ks: 4, 2 for a final half stage, 0
-  // past the end of K.
+  // Sub-steps of 32 codes that hold codes in local stage ks: 4, 2 for a final
+  // half stage, 0 past the end of K (the rest multiply zero A fragments).
 #define OQ_NSUB(KS) ((2 * (KG * (KS) + grp) + 2 <= nk64) ? 4 : (2 * (KG * (KS) + grp) < nk64 ? 2 : 0))
 
   // Global loads run NS - 1 stages ahead of the LDS stage being multiplied:
