@@ -41,6 +41,6 @@ def test_unmasked_code_and_function_boundary():
 
 def test_built_library_is_clean():
     objs = sorted(glob.glob(os.path.join(os.path.dirname(os.path.dirname(__file__)), "_build", "*.o")))
-    if not objs or not os.path.exists(os.path.join(isa_check.LLVM_BIN, "llvm-objdump")):
-        pytest.skip("no built objects or no llvm-objdump")
+    if not objs or not isa_check.tools_present():
+        pytest.skip("no built objects or no llvm-objcopy / llvm-objdump")
     assert isa_check.check_objects(objs) == []
