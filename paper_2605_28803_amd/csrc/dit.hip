@@ -227,8 +227,8 @@ __device__ __forceinline__ void lane_stage4_swap(float (&x)[4]) {
 // codes (per-token, or with the static steps o.sdelta) of a row held as 4
 // channels per thread (channel 4 t + j) by a workgroup of NW waves: channel
 // bits 0-1 in registers, bits 2-7 across the lanes, the top log2(NW) bits
-// across the waves in one LDS exchange (xch: 256 NW floats; red: NW floats,
-// both unused by the caller meanwhile).  Every thread calls it.
+// across the waves through LDS (xch: 256 NW floats, 512 NW when NW = 16; red:
+// NW floats, both unused by the caller meanwhile).  Every thread calls it.
 template <int NW>
 __device__ __forceinline__ void rq_row4(float (&x)[4], int64_t row, bool valid, const RQOut& o, float* xch,
                                         float* red) {
@@ -250,10 +250,40 @@ __device__ __forceinline__ void rq_row4(float (&x)[4], int64_t row, bool valid, 
   lane_stage4<8>(x, lane);
   lane_stage4_swap<16>(x);
   lane_stage4_swap<32>(x);
-  // Channel bits 8 and up: the NW waves.
-  *reinterpret_cast<float4*>(&xch[k0]) = make_float4(x[0], x[1], x[2], x[3]);
-  __syncthreads();
-  {
+  // Channel bits 8 and up: the NW waves.  With 16 waves, two radix-4 rounds
+  // (wave bits 0-1, then 2-3; H_16 = H_4 x H_4) through two LDS buffers: each
+  // thread reads 8 instead of 16 float4, half the LDS traffic of one round.
+  if constexpr (NW == 16) {
+    float* xch2 = xch + D;
+    *reinterpret_cast<float4*>(&xch[k0]) = make_float4(x[0], x[1], x[2], x[3]);
+    __syncthreads();
+    float z[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float sg = (__popc(w & u) & 1) ? -1.0f : 1.0f;
+      const float4 q = *reinterpret_cast<const float4*>(&xch[(((w & ~3) + u) * 64 + lane) * 4]);
+      z[0] = fmaf(sg, q.x, z[0]);
+      z[1] = fmaf(sg, q.y, z[1]);
+      z[2] = fmaf(sg, q.z, z[2]);
+      z[3] = fmaf(sg, q.w, z[3]);
+    }
+    *reinterpret_cast<float4*>(&xch2[k0]) = make_float4(z[0], z[1], z[2], z[3]);
+    __syncthreads();
+    float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float sg = (__popc((w >> 2) & u) & 1) ? -1.0f : 1.0f;
+      const float4 q = *reinterpret_cast<const float4*>(&xch2[((4 * u + (w & 3)) * 64 + lane) * 4]);
+      acc[0] = fmaf(sg, q.x, acc[0]);
+      acc[1] = fmaf(sg, q.y, acc[1]);
+      acc[2] = fmaf(sg, q.z, acc[2]);
+      acc[3] = fmaf(sg, q.w, acc[3]);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) x[j] = acc[j];
+  } else {
+    *reinterpret_cast<float4*>(&xch[k0]) = make_float4(x[0], x[1], x[2], x[3]);
+    __syncthreads();
     float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int u = 0; u < NW; ++u) {
@@ -471,7 +501,7 @@ template <bool GATED>
 __global__ __launch_bounds__(1024) void gelu_rq4096_kernel(const uint16_t* __restrict__ gu,
                                                            uint16_t* __restrict__ act, int64_t M, RQOut o) {
   constexpr int F = 4096;
-  __shared__ __attribute__((aligned(16))) float xch[F];
+  __shared__ __attribute__((aligned(16))) float xch[2 * F];  // the two rounds of the 16-wave exchange
   __shared__ float red[16];
   const int t = threadIdx.x;
   const int64_t row = blockIdx.x;
