@@ -621,6 +621,16 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 // reads whole rows) into LDS as [key][dim]; V as pairs of keys (2j, 2j + 1)
 // by 8 dims, written to V^T [dim][key] as 4-byte key pairs.  Keys past the
 // split and dims past head_dim are staged as zeros.
+// Position of key j of a split in a V^T row.  Within each 32-key step the
+// keys are stored in the order the O^T = V^T P^T operand of a lane takes them
+// (keys 4 g .. 4 g + 3, then 16 + 4 g .. 16 + 4 g + 3, for g = 0 .. 3), so a
+// lane's 8 keys are one 16-byte LDS read; keys j, j + 1 with j even stay
+// adjacent.
+__device__ __forceinline__ int vt_pos(int j) {
+  const int jj = j & 31;
+  return (j & ~31) + 8 * ((jj & 15) >> 2) + 4 * (jj >> 4) + (jj & 3);
+}
+
 template <int WAVES, int HD, int KS>
 __global__ __launch_bounds__(64 * WAVES) void attn_partial_kernel(AttnArgs a) {
   static_assert(KS % 32 == 0, "keys per split");
@@ -735,8 +745,8 @@ __global__ __launch_bounds__(64 * WAVES) void attn_partial_kernel(AttnArgs a) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         // dims c8 + 2q (low halves) and c8 + 2q + 1 (high halves) of keys j, j + 1
-        *reinterpret_cast<uint32_t*>(&sVt[c8 + 2 * q][j]) = (w0[q] & 0xFFFFu) | (w1[q] << 16);
-        *reinterpret_cast<uint32_t*>(&sVt[c8 + 2 * q + 1][j]) = (w0[q] >> 16) | (w1[q] & 0xFFFF0000u);
+        *reinterpret_cast<uint32_t*>(&sVt[c8 + 2 * q][vt_pos(j)]) = (w0[q] & 0xFFFFu) | (w1[q] << 16);
+        *reinterpret_cast<uint32_t*>(&sVt[c8 + 2 * q + 1][vt_pos(j)]) = (w0[q] >> 16) | (w1[q] & 0xFFFF0000u);
       }
     }
   }
@@ -802,9 +812,7 @@ __global__ __launch_bounds__(64 * WAVES) void attn_partial_kernel(AttnArgs a) {
       v4f o = v4f{0, 0, 0, 0};
 #pragma unroll
       for (int st = 0; st < KS / 32; ++st) {
-        const uint16_t* vr = &sVt[nb * 16 + (lane & 15)][st * 32 + 4 * g];
-        const uint2 lo = *reinterpret_cast<const uint2*>(vr), hi = *reinterpret_cast<const uint2*>(vr + 16);
-        const v8h va = __builtin_bit_cast(v8h, make_uint4(lo.x, lo.y, hi.x, hi.y));
+        const v8h va = *reinterpret_cast<const v8h*>(&sVt[nb * 16 + (lane & 15)][st * 32 + 8 * g]);
         o = __builtin_amdgcn_mfma_f32_16x16x32_f16(va, pb[st], o, 0, 0, 0);
       }
       if (qst) {
@@ -926,8 +934,8 @@ __global__ __launch_bounds__(64 * WAVES) void attn_cross_kernel(const uint16_t* 
                                 vjok ? vraw[i].w : 0u};
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-          sVt[d8 + 2 * t][vj] = static_cast<uint16_t>(wv[t] & 0xFFFFu);
-          sVt[d8 + 2 * t + 1][vj] = static_cast<uint16_t>(wv[t] >> 16);
+          sVt[d8 + 2 * t][vt_pos(vj)] = static_cast<uint16_t>(wv[t] & 0xFFFFu);
+          sVt[d8 + 2 * t + 1][vt_pos(vj)] = static_cast<uint16_t>(wv[t] >> 16);
         }
       }
     }
@@ -978,9 +986,7 @@ __global__ __launch_bounds__(64 * WAVES) void attn_cross_kernel(const uint16_t* 
       o[nb] *= alpha;
 #pragma unroll
       for (int st = 0; st < KS / 32; ++st) {
-        const uint16_t* vr = &sVt[nb * 16 + (lane & 15)][st * 32 + 4 * g];
-        const uint2 lo = *reinterpret_cast<const uint2*>(vr), hi = *reinterpret_cast<const uint2*>(vr + 16);
-        const v8h va = __builtin_bit_cast(v8h, make_uint4(lo.x, lo.y, hi.x, hi.y));
+        const v8h va = *reinterpret_cast<const v8h*>(&sVt[nb * 16 + (lane & 15)][st * 32 + 8 * g]);
         o[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(va, pb[st], o[nb], 0, 0, 0);
       }
     }
