@@ -193,9 +193,7 @@ __global__ __launch_bounds__(256) void norm_rq_kernel(const float* __restrict__ 
 // ---------------------------------------------------------------------------
 
 __device__ __forceinline__ float wave_sum64(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
-  return v;
+  return rqd::wave_sum_xor(v);
 }
 
 template <int H>
@@ -315,8 +313,7 @@ __device__ __forceinline__ void rq_row4(float (&x)[4], int64_t row, bool valid, 
   }
   // Row maximum of the unnormalized transform, scales, codes (as rq_core).
   float amax = fmaxf(fmaxf(fabsf(x[0]), fabsf(x[1])), fmaxf(fabsf(x[2]), fabsf(x[3])));
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) amax = fmaxf(amax, __shfl_xor(amax, m, 64));
+  amax = rqd::wave_max(amax);
   if (lane == 0) red[w] = amax;
   __syncthreads();
   amax = red[0];
@@ -781,8 +778,8 @@ __global__ __launch_bounds__(64 * WAVES) void attn_partial_kernel(AttnArgs a) {
       sc[nb][e] = v;
       m_ = fmaxf(m_, v);
     }
-  m_ = fmaxf(m_, rqd::lane_xor<16>(m_));
-  m_ = fmaxf(m_, __shfl_xor(m_, 32, 64));
+  m_ = fmaxf(m_, rqd::lane_xor_far<16>(m_));
+  m_ = fmaxf(m_, rqd::lane_xor_far<32>(m_));
   float l_ = 0.0f;
   v8h pb[KS / 32];  // P^T fragments, one per 32-key step
 #pragma unroll
@@ -793,8 +790,8 @@ __global__ __launch_bounds__(64 * WAVES) void attn_partial_kernel(AttnArgs a) {
       l_ += p;
       pb[st][j] = static_cast<_Float16>(p);
     }
-  l_ += rqd::lane_xor<16>(l_);
-  l_ += __shfl_xor(l_, 32, 64);
+  l_ += rqd::lane_xor_far<16>(l_);
+  l_ += rqd::lane_xor_far<32>(l_);
 
   // O^T = V^T P^T, 16 dims x 16 queries per block.  With a single split
   // (a.direct) the row is complete: o / l, rounded to fp16, goes straight to
@@ -962,8 +959,8 @@ __global__ __launch_bounds__(64 * WAVES) void attn_cross_kernel(const uint16_t* 
         sc[nb][e] = v;
         mx = fmaxf(mx, v);
       }
-    mx = fmaxf(mx, rqd::lane_xor<16>(mx));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    mx = fmaxf(mx, rqd::lane_xor_far<16>(mx));
+    mx = fmaxf(mx, rqd::lane_xor_far<32>(mx));
     const float mn = fmaxf(m, mx);
     const float alpha = __expf(m - mn);  // 0 on the first split (m = -inf)
     float sum = 0.0f;
@@ -976,8 +973,8 @@ __global__ __launch_bounds__(64 * WAVES) void attn_cross_kernel(const uint16_t* 
         sum += pv;
         pb[st][j] = static_cast<_Float16>(pv);
       }
-    sum += rqd::lane_xor<16>(sum);
-    sum += __shfl_xor(sum, 32, 64);
+    sum += rqd::lane_xor_far<16>(sum);
+    sum += rqd::lane_xor_far<32>(sum);
     l = l * alpha + sum;
     m = mn;
     __syncthreads();  // V^T staged
@@ -1117,8 +1114,7 @@ __global__ __launch_bounds__(256) void combine_rq1024_kernel(AttnArgs a, int64_t
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
-  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
-  return v;
+  return rqd::wave_sum_xor(v);
 }
 
 // x[m][:] += dt * (fp16(norm(r[m]) g_f) W_out^T + b_out), norm = RMS norm or
@@ -1226,9 +1222,9 @@ __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ r,
 #pragma unroll
     for (int rr = 0; rr < R; ++rr) {
       float v = acc[rr];
-      v += __shfl_xor(v, 1, 64);
-      v += __shfl_xor(v, 2, 64);
-      v += __shfl_xor(v, 4, 64);
+      v += rqd::lane_xor<1>(v);
+      v += rqd::lane_xor<2>(v);
+      v += rqd::lane_xor<4>(v);
       const int64_t m = m0 + rr;
       if (aok && sl == 0 && m < M) x[m * A + a_idx] += dt * (v + h2f(b_out[a_idx]));
     }

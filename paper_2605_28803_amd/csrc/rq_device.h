@@ -88,6 +88,42 @@ __device__ __forceinline__ void dword_swap(uint32_t& a, uint32_t& b) {
   b = __float_as_uint(y);
 }
 
+// Value of lane (lane ^ H), H = 16 or 32, through the permlane swaps (VALU;
+// no LDS-pipe round trip as with ds_bpermute / ds_swizzle).
+template <int H>
+__device__ __forceinline__ float lane_xor_far(float v) {
+  static_assert(H == 16 || H == 32, "lane_xor_far: H = 16 or 32");
+  float x = v, y = v;
+  permlane_swap<H>(x, y);
+  return (threadIdx.x & H) ? x : y;
+}
+
+// Sum over the 64 lanes of a wave, every lane receiving it: lane ^ 32, 16,
+// 8, 4, 2, 1 in that order (the partners and order of a __shfl_xor loop from
+// 32 down, so the same fp32 sum bit for bit).
+__device__ __forceinline__ float wave_sum_xor(float v) {
+  v += lane_xor_far<32>(v);
+  v += lane_xor_far<16>(v);
+  v += lane_xor<8>(v);
+  v += lane_xor<4>(v);
+  v += lane_xor<2>(v);
+  v += lane_xor<1>(v);
+  return v;
+}
+
+// Maximum over the 64 lanes of a wave, every lane receiving it (order-free):
+// quad permutations, the row half-mirror and mirror (8- and 16-lane groups),
+// then the permlane swaps, all on the VALU.
+__device__ __forceinline__ float wave_max(float v) {
+  v = fmaxf(v, lane_xor<1>(v));
+  v = fmaxf(v, lane_xor<2>(v));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x141, 0xF, 0xF, false)));  // half-mirror
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x140, 0xF, 0xF, false)));  // mirror
+  v = fmaxf(v, lane_xor_far<16>(v));
+  v = fmaxf(v, lane_xor_far<32>(v));
+  return v;
+}
+
 template <int H, int C>
 __device__ __forceinline__ void lane_stage_swap(float (&v)[C][8]) {
 #pragma unroll
@@ -141,8 +177,8 @@ __device__ __forceinline__ float row_reduce(float x, const RowMap& m, float* red
   if (lane_bits > 1) x = op(x, lane_xor<2>(x));
   if (lane_bits > 2) x = op(x, lane_xor<4>(x));
   if (lane_bits > 3) x = op(x, lane_xor<8>(x));
-  if (lane_bits > 4) x = op(x, lane_xor<16>(x));
-  if (lane_bits > 5) x = op(x, __shfl_xor(x, 32, 64));
+  if (lane_bits > 4) x = op(x, lane_xor_far<16>(x));
+  if (lane_bits > 5) x = op(x, lane_xor_far<32>(x));
   if (m.logT > 6) {
     const int w = threadIdx.x >> 6;
     __syncthreads();

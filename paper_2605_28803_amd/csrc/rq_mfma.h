@@ -243,8 +243,8 @@ __device__ __forceinline__ void rq_row(const rv8h (&cur)[NG], const rv8h& a1, co
   amax = fmaxf(amax, rqd::lane_xor<2>(amax));
   amax = fmaxf(amax, rqd::lane_xor<4>(amax));
   amax = fmaxf(amax, rqd::lane_xor<8>(amax));
-  amax = fmaxf(amax, rqd::lane_xor<16>(amax));
-  amax = fmaxf(amax, __shfl_xor(amax, 32, 64));
+  amax = fmaxf(amax, rqd::lane_xor_far<16>(amax));
+  amax = fmaxf(amax, rqd::lane_xor_far<32>(amax));
   if constexpr (W > 1) {
     if (lane == 0) red[wv] = amax;
     __syncthreads();
