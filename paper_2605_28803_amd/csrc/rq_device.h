@@ -98,14 +98,30 @@ __device__ __forceinline__ float lane_xor_far(float v) {
   return (threadIdx.x & H) ? x : y;
 }
 
+// Value of lane (lane ^ H), H = 4 or 8, as two DPP row moves (H = 4: row
+// half-mirror, lane ^ 7 within 8, then the quad reversal, ^ 3; H = 8: row
+// mirror, ^ 15 within 16, then the half-mirror): shorter latency than a
+// ds_swizzle in a dependent chain of one value, while stages over many values
+// keep the swizzle (the LDS pipe works beside the VALU there).
+template <int H>
+__device__ __forceinline__ float lane_xor_dpp(float v) {
+  static_assert(H == 4 || H == 8, "lane_xor_dpp: H = 4 or 8");
+  const int x = __float_as_int(v);
+  if constexpr (H == 4)
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__builtin_amdgcn_mov_dpp(x, 0x141, 0xF, 0xF, false), 0x1B, 0xF,
+                                                   0xF, false));
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__builtin_amdgcn_mov_dpp(x, 0x140, 0xF, 0xF, false), 0x141, 0xF,
+                                                 0xF, false));
+}
+
 // Sum over the 64 lanes of a wave, every lane receiving it: lane ^ 32, 16,
 // 8, 4, 2, 1 in that order (the partners and order of a __shfl_xor loop from
-// 32 down, so the same fp32 sum bit for bit).
+// 32 down, so the same fp32 sum bit for bit), all on the VALU.
 __device__ __forceinline__ float wave_sum_xor(float v) {
   v += lane_xor_far<32>(v);
   v += lane_xor_far<16>(v);
-  v += lane_xor<8>(v);
-  v += lane_xor<4>(v);
+  v += lane_xor_dpp<8>(v);
+  v += lane_xor_dpp<4>(v);
   v += lane_xor<2>(v);
   v += lane_xor<1>(v);
   return v;
