@@ -113,6 +113,69 @@ __global__ __launch_bounds__(256) void inproj_kernel(const float* __restrict__ x
     r[static_cast<int64_t>(m) * D + n] = inproj_dot(xsh, w_in + static_cast<int64_t>(n) * A, A, vec) + h2f(b_in[n]);
 }
 
+// In-projection with the weight row preloaded, for AP = A action channels in
+// {8, 16, 24, 32} and 16-byte aligned rows: a W_in row is AP / 8 16-byte
+// pieces, all issued before the first sum (the loop of inproj_dot waits for
+// each piece before loading the next).  The sums are inproj_dot's: a
+// ascending from 0, the bias added last.
+constexpr int kInprojA = 32;
+
+__host__ __device__ __forceinline__ int inproj_preload_a(int A, const void* w_in) {
+  return A <= kInprojA && A % 8 == 0 && (reinterpret_cast<uintptr_t>(w_in) & 15) == 0 ? A : 0;
+}
+
+template <int AP>
+__device__ __forceinline__ void inproj_load_row(const uint16_t* __restrict__ wr, uint4 (&q)[AP / 8]) {
+#pragma unroll
+  for (int i = 0; i < AP / 8; ++i) q[i] = *reinterpret_cast<const uint4*>(wr + 8 * i);
+}
+
+template <int AP>
+__device__ __forceinline__ float inproj_dot_pre(const float* xa, const uint4 (&q)[AP / 8]) {
+  float acc = 0.0f;
+#pragma unroll
+  for (int i = 0; i < AP / 8; ++i) {
+    const uint32_t qw[4] = {q[i].x, q[i].y, q[i].z, q[i].w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      acc = fmaf(xa[8 * i + 2 * j], h2f(qw[j] & 0xFFFFu), acc);
+      acc = fmaf(xa[8 * i + 2 * j + 1], h2f(qw[j] >> 16), acc);
+    }
+  }
+  return acc;
+}
+
+// r = x W_in^T + b_in with preloaded rows: workgroup (i, j) computes channel
+// n = 256 j + t of rows R i .. R i + R - 1 (R * AP <= 256), thread t loading
+// its W_in row and bias once for the R rows before the action rows are
+// staged in LDS (inproj_kernel reads the whole W_in once per row).
+template <int R, int AP>
+__global__ __launch_bounds__(256) void inproj_rows_kernel(const float* __restrict__ x,
+                                                          const uint16_t* __restrict__ w_in,
+                                                          const uint16_t* __restrict__ b_in, float* __restrict__ r,
+                                                          int64_t M, int D) {
+  static_assert(R * AP <= 256, "one action value per thread");
+  __shared__ float xsh[R][AP];
+  const int t = threadIdx.x;
+  const int n = blockIdx.y * 256 + t;
+  const int nn = n < D ? n : 0;
+  const int64_t m0 = static_cast<int64_t>(blockIdx.x) * R;
+  uint4 q[AP / 8];
+  inproj_load_row<AP>(w_in + static_cast<int64_t>(nn) * AP, q);
+  const float bb = h2f(b_in[nn]);
+  if (t < R * AP) {
+    const int i = t / AP, a = t % AP;
+    const int64_t m = m0 + i < M ? m0 + i : 0;
+    xsh[i][a] = x[m * AP + a];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    const float v = inproj_dot_pre<AP>(xsh[i], q) + bb;
+    if (m0 + i < M && n < D) r[(m0 + i) * D + n] = v;
+  }
+}
+
 // h = fp16(norm(r) g (1 + sc) + sh), then rotate + quantize h.  norm is the
 // RMS norm (LN = false) or the layer norm (LN = true); SC = false means no
 // scale vector (sc is not read, taken as zero); sh is always read.  Every
@@ -1751,6 +1814,31 @@ int run_block(oq_dit* h, int l, int t, float* r, hipStream_t st, int until = 4, 
 
 int final_stage(oq_dit* h, const float* r, float* x, hipStream_t st);
 
+// r = x W_in^T + b_in for the M action rows: inproj_rows_kernel (8 rows per
+// workgroup) when the weight rows can be preloaded, else inproj_kernel (one
+// row per workgroup); the same sums either way.
+int inproj_launch(const oq_dit* h, const float* x, float* r, hipStream_t st) {
+  const oq_dit_config& c = h->cfg;
+  const int64_t M = static_cast<int64_t>(c.batch) * c.tokens;
+  const auto* w_in = static_cast<const uint16_t*>(h->w.w_in);
+  const auto* b_in = static_cast<const uint16_t*>(h->w.b_in);
+  constexpr int R = 8;  // R * A <= 256 for A <= kInprojA
+  const dim3 grid(static_cast<unsigned>((M + R - 1) / R), static_cast<unsigned>((c.hidden + 255) / 256));
+  const int ap = inproj_preload_a(c.action_dim, w_in);
+  if (ap > 0) {
+    switch (ap) {
+      case 8: hipLaunchKernelGGL((inproj_rows_kernel<R, 8>), grid, dim3(256), 0, st, x, w_in, b_in, r, M, c.hidden); break;
+      case 16: hipLaunchKernelGGL((inproj_rows_kernel<R, 16>), grid, dim3(256), 0, st, x, w_in, b_in, r, M, c.hidden); break;
+      case 24: hipLaunchKernelGGL((inproj_rows_kernel<R, 24>), grid, dim3(256), 0, st, x, w_in, b_in, r, M, c.hidden); break;
+      default: hipLaunchKernelGGL((inproj_rows_kernel<R, 32>), grid, dim3(256), 0, st, x, w_in, b_in, r, M, c.hidden); break;
+    }
+  } else {
+    hipLaunchKernelGGL(inproj_kernel, dim3(static_cast<unsigned>(M)), dim3(256), c.action_dim * sizeof(float), st, x,
+                       w_in, b_in, r, c.action_dim, c.hidden);
+  }
+  return launch_status();
+}
+
 // Pi-0.5 with 1024-channel rows on the 1024-wide producer path (at most 256
 // rows, Hadamard block = the row): the step's in-projection and block 0's
 // first norm producer as one kernel (the same arithmetic as inproj_kernel
@@ -1780,12 +1868,7 @@ int run_step(oq_dit* h, float* x, int t, hipStream_t st) {
   bool fused = false;
   int e = inproj_norm1(h, x, r, t, st, &fused);
   if (e != OQ_OK) return e;
-  if (!fused) {
-    hipLaunchKernelGGL(inproj_kernel, dim3(static_cast<unsigned>(M)), dim3(256), c.action_dim * sizeof(float), st, x,
-                       static_cast<const uint16_t*>(h->w.w_in), static_cast<const uint16_t*>(h->w.b_in), r,
-                       c.action_dim, c.hidden);
-    if ((e = launch_status()) != OQ_OK) return e;
-  }
+  if (!fused && (e = inproj_launch(h, x, r, st)) != OQ_OK) return e;
   for (int l = 0; l < c.n_blocks; ++l) {
     e = fused && l == 0 ? run_block_pi(h, 0, t, r, st, 4, false, true) : run_block(h, l, t, r, st, 4, false);
     if (e != OQ_OK) return e;
@@ -2061,12 +2144,7 @@ extern "C" int oq_dit_set_static_steps(oq_dit* h, const float* delta, const oq_q
 extern "C" int oq_dit_in_projection(oq_dit* h, const float* x, float* resid, void* stream) {
   if (!h || !x || !resid) return OQ_ERR_NULL;
   if (!oq::aligned(x, 4) || !oq::aligned(resid, 4)) return OQ_ERR_ALIGN;
-  const oq_dit_config& c = h->cfg;
-  const int64_t M = static_cast<int64_t>(c.batch) * c.tokens;
-  hipLaunchKernelGGL(oq::inproj_kernel, dim3(static_cast<unsigned>(M)), dim3(256), c.action_dim * sizeof(float),
-                     static_cast<hipStream_t>(stream), x, static_cast<const uint16_t*>(h->w.w_in),
-                     static_cast<const uint16_t*>(h->w.b_in), resid, c.action_dim, c.hidden);
-  return oq::launch_status();
+  return oq::inproj_launch(h, x, resid, static_cast<hipStream_t>(stream));
 }
 
 extern "C" int oq_dit_final_stage(oq_dit* h, const float* resid, float* x, void* stream) {

@@ -117,3 +117,28 @@ def assert_block(cfg, inp, model, l, t, r_in, tag="", static_delta=None):
     for k, v in errs.items():
         assert v <= parity.REL_L2_OUT, (l, t, k, v)
     return r_out
+
+
+def assert_in_projection(inp, model, tag=""):
+    """The library's action in-projection (oq_dit_in_projection) against the
+    oracle's r = x W_in^T + b_in, a float64 product of the same fp16 weights and
+    fp32 actions.  Each library output is an fp32 fma chain over the A action
+    channels and then the bias addition, A + 1 roundings, so the standard bound
+    for a recursive sum holds: |r - r_exact| <= gamma_{A+1} (sum_a |x_a w_a| +
+    |b|) with gamma_n = n u / (1 - n u), u = 2^-24."""
+    x = np.ascontiguousarray(inp["x0"], dtype=np.float32)
+    M, D = model.M, model.cfg_c.hidden
+    r = torch.empty((M, D), dtype=torch.float32, device=DEV)
+    model.in_projection(torch.from_numpy(x).to(DEV), r)
+    torch.cuda.synchronize()
+    got = r.cpu().numpy().astype(np.float64)
+    x64 = x.astype(np.float64)
+    want = odit.in_projection(inp["w"], x64)
+    A = x.shape[-1]
+    mag = (np.abs(x64.reshape(M, A)) @ np.abs(np.asarray(inp["w"]["w_in"], np.float64)).T
+           + np.abs(np.asarray(inp["w"]["b_in"], np.float64))[None, :])
+    n, u = A + 1, 2.0 ** -24
+    err = np.abs(got - want)
+    bound = n * u / (1 - n * u) * mag
+    print(f"{tag}in-projection M={M} D={D} A={A}: max |err| / bound {float(np.max(err / bound)):.3f}", flush=True)
+    assert np.all(err <= bound)

@@ -46,6 +46,7 @@ def _setup(n_blocks, batch=None, cfg=configs.DIT_PI, zero_blocks=False):
 
 def test_blocks_teacher_forced_pi():
     cfg, inp, model = _setup(n_blocks=3)
+    dit_parity.assert_in_projection(inp, model, "pi ")
     r0 = odit.in_projection(inp["w"], inp["x0"])
     for t in (0, 7):
         rr = r0

@@ -60,6 +60,7 @@ def _check_cond(inp, model):
 def test_blocks_teacher_forced_gr00t():
     inp, model = _setup(n_blocks=2, batch=4)
     _check_cond(inp, model)
+    dit_parity.assert_in_projection(inp, model, "gr00t ")
     r0 = odit.in_projection(inp["w"], inp["x0"])
     for t in (0, 3):
         rr = r0
@@ -73,6 +74,7 @@ def test_full_size_sampled_blocks_gr00t():
     self-attention block (1) and the last block are checked site by site."""
     inp = dit_inputs.make_dit_inputs(CFG)
     model = oq.DiT(CFG, inp, device="cuda:0")
+    dit_parity.assert_in_projection(inp, model, "gr00t full size ")
     t = 2
     r = torch.from_numpy(odit.in_projection(inp["w"], inp["x0"]).astype(np.float32)).to(DEV)
     for l in range(CFG.n_blocks):

@@ -51,6 +51,11 @@ def test_blocks_teacher_forced(shape):
     print(f"{name}: blocks within the per-site bounds", flush=True)
 
 
+def test_in_projection(shape):
+    name, cfg, inp, model = shape
+    dit_parity.assert_in_projection(inp, model, f"{name} ")
+
+
 def test_final_stage(shape):
     name, cfg, inp, model = shape
     x0 = inp["x0"].astype(np.float32)
