@@ -7,7 +7,11 @@ The Pi-0.5 architecture (Section 5's setting, every block linear W4A4) with
   * a wider model (hidden 2048, 16 heads of 128, 48 action channels, 20
     tokens, 100 prefix keys): the generic producers on 2048-channel rows, the
     merge of two key splits, the final stage's streamed weights (more than
-    32 action channels), the in-projection on its own.
+    32 action channels), the in-projection on its own;
+  * one block with 24 and with 12 action channels: the in-projection's
+    preloaded 24-channel rows kernel (oq_dit_in_projection) beside the step's
+    fused in-projection, and the per-channel sums of both when the action
+    width is not a multiple of 8.
 For each: teacher-forced block parity against the oracle at the bounds of
 the configured shapes, the final stage against its definition, and the timed
 step (graph replay) bit-equal to the step rebuilt from its parts."""
@@ -29,6 +33,8 @@ SHAPES = {
     "pi_batch6": dataclasses.replace(configs.DIT_PI, name="pi_batch6", n_blocks=2, batch=6, steps=3),
     "pi_wide": dataclasses.replace(configs.DIT_PI, name="pi_wide", n_blocks=2, hidden=2048, n_heads=16,
                                    head_dim=128, tokens=20, prefix=100, steps=3, action_dim=48),
+    "pi_a24": dataclasses.replace(configs.DIT_PI, name="pi_a24", n_blocks=1, prefix=64, steps=3, action_dim=24),
+    "pi_a12": dataclasses.replace(configs.DIT_PI, name="pi_a12", n_blocks=1, prefix=64, steps=3, action_dim=12),
 }
 
 
