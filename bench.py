@@ -30,7 +30,7 @@ Also reported (same JSON line):
              the 16384^3 prefill shape, single-threaded and on every core.
 
 --sweep writes the rotate-quantize / GEMM roofline sweep (M x K = N grid) as
-JSON lines to gpurun_out/sweep.jsonl instead; --roofline-only runs just the
+JSON lines to stdout (and to the file --sweep-out names) instead; --roofline-only runs just the
 roofline kernel measurement (the command the committed rocprofv3 summaries of
 that kernel were taken with); --copy-calibration runs a plain copy of known
 size (the counter calibration reference); --gr00t-only times just the
@@ -1067,17 +1067,25 @@ def run_dit(args):
 
 def run_sweep(args):
     """The rotate-quantize / GEMM roofline sweep alone (sweep_records), as JSON
-    lines on stdout and in gpurun_out/sweep.jsonl."""
-    os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
-    path = os.path.join(ROOT, "gpurun_out", "sweep.jsonl")
+    lines on stdout and, when args.sweep_out names a file, in that file."""
     Ms = [int(m) for m in args.sweep_m.split(",")] if args.sweep_m else None
     Ks = [int(k) for k in args.sweep_k.split(",")] if args.sweep_k else None
-    with open(path, "w") as f:
-        def sink(rec):
+    f = None
+    if args.sweep_out:
+        path = os.path.abspath(args.sweep_out)
+        os.makedirs(os.path.dirname(path), exist_ok=True)
+        f = open(path, "w")
+
+    def sink(rec):
+        if f is not None:
             f.write(json.dumps(rec) + "\n")
             f.flush()
-            print(json.dumps(rec), flush=True)
+        print(json.dumps(rec), flush=True)
+    try:
         sweep_records(Ms, Ks, reps=20, sink=sink)
+    finally:
+        if f is not None:
+            f.close()
 
 
 def main():
@@ -1086,6 +1094,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--sweep", action="store_true")
+    ap.add_argument("--sweep-out", default="", help="file that also receives the --sweep JSON lines")
     ap.add_argument("--sweep-m", default="")
     ap.add_argument("--sweep-k", default="")
     ap.add_argument("--no-cpu-baseline", action="store_true")
