@@ -1883,8 +1883,9 @@ int final_stage(oq_dit* h, const float* r, float* x, hipStream_t st) {
   const int64_t M = static_cast<int64_t>(c.batch) * c.tokens;
   const float dt = (is_gr00t(c) ? 1.0f : -1.0f) / static_cast<float>(c.steps);
   // Few rows (the Pi-0.5 action tokens): one row per workgroup, so the rows
-  // spread over as many CUs; else four (the weight slices are read once per
-  // workgroup).
+  // spread over as many CUs; else two (the weight slices are read once per
+  // workgroup; two rows gave 1024 GR00T rows 512 workgroups and a shorter
+  // per-thread product chain than four, for twice the weight reads).
   auto launch = [&](auto LNc, auto Rc) {
     constexpr bool LN = decltype(LNc)::value;
     constexpr int R = decltype(Rc)::value;
@@ -1896,7 +1897,7 @@ int final_stage(oq_dit* h, const float* r, float* x, hipStream_t st) {
   const bool few = M <= 256;
   if (is_gr00t(c)) {
     if (few) launch(std::true_type{}, std::integral_constant<int, 1>{});
-    else launch(std::true_type{}, std::integral_constant<int, 4>{});
+    else launch(std::true_type{}, std::integral_constant<int, 2>{});
   } else {
     if (few) launch(std::false_type{}, std::integral_constant<int, 1>{});
     else launch(std::false_type{}, std::integral_constant<int, 4>{});
